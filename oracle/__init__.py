@@ -1,0 +1,206 @@
+"""CPU oracle for the E2LLM population-fitness path (arXiv 2606.03770).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the smoke check and by
+the bench's CPU-baseline leg, never by the product package.  It wraps the
+plain C implementation in oracle.c (built with gcc into liboracle.so) and
+shares nothing with the HIP library.
+
+Functions mirror the paper's pieces:
+  quantise   -> integer cost tables (Sec. 3.2 definitions of ell and tau)
+  dp_pipe    -> Algorithm 1 / Eq. 1-2 on one device chain
+  solve      -> dp_pipe for every (individual, cluster) of a population
+  fitness    -> Eq. 3-5 with the QoS floor (Sec. 3.3, Sec. 3.5, Algorithm 2)
+  ga_step    -> one generation: elites, tournament, crossover, mutation
+  rng        -> counter-based SplitMix64 hash used by ga_step
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+INF = (1 << 64) - 1
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def build() -> str:
+    """Compile liboracle.so from oracle.c (always recompiles)."""
+    tmp = LIB + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
+                           "-o", tmp, SRC])
+    os.replace(tmp, LIB)
+    return LIB
+
+
+def _load() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        build()
+    lib = ctypes.CDLL(LIB)
+    P = ctypes.c_void_p
+    i32, u32, u64 = ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64
+    lib.oracle_quantise.argtypes = [i32, i32, P, P, P, P, P, P, P, P, P]
+    lib.oracle_quantise.restype = i32
+    lib.oracle_dp_pipe.argtypes = [i32, i32, P, P, P, P, P, u64, P, P, P, P, P]
+    lib.oracle_dp_pipe.restype = i32
+    lib.oracle_solve.argtypes = [i32, i32, P, P, P, P, P, u64, i32, i32, P, P, P, P, P, P, P]
+    lib.oracle_solve.restype = i32
+    lib.oracle_fitness.argtypes = [i32, i32, P, P, P, u64, u64, u64, P, P, P, P]
+    lib.oracle_fitness.restype = i32
+    lib.oracle_ga_step.argtypes = [i32, i32, i32, P, P, P, P, u64, u32, u32, u32, u32, u32, P, P]
+    lib.oracle_ga_step.restype = i32
+    lib.oracle_rng.argtypes = [u64, u64, u64, u64, u64]
+    lib.oracle_rng.restype = u64
+    lib.oracle_splitmix_out.argtypes = [u64]
+    lib.oracle_splitmix_out.restype = u64
+    _lib = lib
+    return lib
+
+
+def _p(a: np.ndarray) -> int:
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data
+
+
+def _u64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.uint64))
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def quantise(n_dev, n_layer, speed_flops, bw_Bps, congestion_ppm, layer_flops, act_bytes,
+             head_flops, **_ignored):
+    """Return (t [2][M][N], h [2][M], tau [2][M][M]) as uint64 arrays."""
+    lib = _load()
+    M, N = int(n_dev), int(n_layer)
+    speed = _u64(speed_flops)
+    bw = _u64(bw_Bps)
+    cong = np.ascontiguousarray(np.asarray(congestion_ppm, dtype=np.uint32))
+    lf = _u64(layer_flops).reshape(2, N)
+    act = _u64(act_bytes)
+    hf = _u64(head_flops)
+    t = np.zeros((2, M, N), dtype=np.uint64)
+    h = np.zeros((2, M), dtype=np.uint64)
+    tau = np.zeros((2, M, M), dtype=np.uint64)
+    rc = lib.oracle_quantise(M, N, _p(speed), _p(bw), _p(cong), _p(lf), _p(act), _p(hf),
+                             _p(t), _p(h), _p(tau))
+    if rc != 0:
+        raise OracleError(f"oracle_quantise failed: {rc}")
+    return t, h, tau
+
+
+def dp_pipe(tk, hk, tau_link, memk, W, HB):
+    """Algorithm 1 on one chain.  Returns (T, Lambda, mu_star, sizes, evaluated)."""
+    lib = _load()
+    tk = _u64(tk)
+    m, N = tk.shape
+    hk, tl, mk, Wv = _u64(hk), _u64(tau_link), _u64(memk), _u64(W)
+    assert hk.shape == (m,) and tl.shape == (m,) and mk.shape == (m,) and Wv.shape == (N,)
+    T = ctypes.c_uint64()
+    L = ctypes.c_uint64()
+    mu = ctypes.c_int()
+    ev = ctypes.c_uint64()
+    sizes = np.zeros(max(m, 1), dtype=np.int32)
+    rc = lib.oracle_dp_pipe(m, N, _p(tk), _p(hk), _p(tl), _p(mk), _p(Wv), int(HB),
+                            ctypes.byref(T), ctypes.byref(L), ctypes.byref(mu), _p(sizes),
+                            ctypes.byref(ev))
+    if rc != 0:
+        raise OracleError(f"oracle_dp_pipe failed: {rc}")
+    return T.value, L.value, mu.value, sizes[:m].copy(), ev.value
+
+
+def solve(tables, mem_bytes, layer_bytes, head_bytes, labels, roles, k_max):
+    """All (individual, cluster) problems.  tables = quantise(...) output.
+
+    Returns dict with T, Lambda [P][k_max] u64, master [P][k_max] i16,
+    layers [P][M] u8 and evaluated (candidate count).
+    """
+    lib = _load()
+    t, h, tau = tables
+    M, N = t.shape[1], t.shape[2]
+    labels = np.ascontiguousarray(labels, dtype=np.uint8)
+    roles = np.ascontiguousarray(roles, dtype=np.uint8)
+    P = labels.shape[0]
+    if labels.shape != (P, M) or roles.shape != (P, int(k_max)):
+        raise OracleError("labels must be [P][M] and roles [P][k_max]")
+    T = np.zeros((P, k_max), dtype=np.uint64)
+    L = np.zeros((P, k_max), dtype=np.uint64)
+    master = np.zeros((P, k_max), dtype=np.int16)
+    layers = np.zeros((P, M), dtype=np.uint8)
+    ev = ctypes.c_uint64()
+    rc = lib.oracle_solve(M, N, _p(t), _p(h), _p(tau), _p(_u64(mem_bytes)),
+                          _p(_u64(layer_bytes)), int(head_bytes), P, int(k_max),
+                          _p(labels), _p(roles), _p(T), _p(L), _p(master), _p(layers),
+                          ctypes.byref(ev))
+    if rc != 0:
+        raise OracleError(f"oracle_solve failed: {rc}")
+    return dict(T=T, Lambda=L, master=master, layers=layers, evaluated=ev.value)
+
+
+def fitness(T, Lambda, roles, t_arrival_ns, nd_tokens, min_tps_milli):
+    """Eq. 3-5 per individual.  Returns dict w, phase, s_p, s_d (u64 [P])."""
+    lib = _load()
+    T, L = _u64(T), _u64(Lambda)
+    roles = np.ascontiguousarray(roles, dtype=np.uint8)
+    P, k_max = T.shape
+    if L.shape != T.shape or roles.shape != T.shape:
+        raise OracleError("T, Lambda and roles must share the shape [P][k_max]")
+    out = {k: np.zeros(P, dtype=np.uint64) for k in ("w", "phase", "s_p", "s_d")}
+    rc = lib.oracle_fitness(P, k_max, _p(T), _p(L), _p(roles), int(t_arrival_ns),
+                            int(nd_tokens), int(min_tps_milli), _p(out["w"]), _p(out["phase"]),
+                            _p(out["s_p"]), _p(out["s_d"]))
+    if rc != 0:
+        raise OracleError(f"oracle_fitness failed: {rc}")
+    return out
+
+
+def eval_population(wl, labels=None, roles=None):
+    """Quantise, solve and score a workload's population (or the given one)."""
+    tables = quantise(**wl.problem_arrays())
+    labels = wl.labels if labels is None else labels
+    roles = wl.roles if roles is None else roles
+    sol = solve(tables, wl.mem_bytes, wl.layer_bytes, wl.head_bytes, labels, roles, wl.k_max)
+    fit = fitness(sol["T"], sol["Lambda"], roles, **wl.fitness_params())
+    sol.update(fit)
+    return sol
+
+
+def ga_step(labels, roles, w, phase, k_max, seed, generation, tournament_k,
+            crossover_thresh_u32, mutation_thresh_u32, n_elite):
+    lib = _load()
+    labels = np.ascontiguousarray(labels, dtype=np.uint8)
+    roles = np.ascontiguousarray(roles, dtype=np.uint8)
+    P, M = labels.shape
+    if roles.shape != (P, int(k_max)):
+        raise OracleError(f"roles shape {roles.shape} != {(P, int(k_max))}")
+    w, phase = _u64(w), _u64(phase)
+    if w.shape != (P,) or phase.shape != (P,):
+        raise OracleError("w and phase must have shape [P]")
+    lo = np.zeros_like(labels)
+    ro = np.zeros_like(roles)
+    rc = lib.oracle_ga_step(M, P, int(k_max), _p(labels), _p(roles), _p(w),
+                            _p(phase), int(seed), int(generation), int(tournament_k),
+                            int(crossover_thresh_u32), int(mutation_thresh_u32), int(n_elite),
+                            _p(lo), _p(ro))
+    if rc != 0:
+        raise OracleError(f"oracle_ga_step failed: {rc}")
+    return lo, ro
+
+
+def rng(seed, g, s, stream, gene) -> int:
+    return int(_load().oracle_rng(seed, g, s, stream, gene))
+
+
+def splitmix_out(z) -> int:
+    return int(_load().oracle_splitmix_out(z))

@@ -1,0 +1,470 @@
+/*
+ * CPU oracle for the E2LLM population-fitness path (arXiv 2606.03770).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the tests, the smoke check and the bench's CPU
+ * baseline leg do.  It shares no code, header, table or helper with the HIP
+ * library: it quantises its own inputs, runs its own dynamic program and its
+ * own fitness and GA arithmetic.
+ *
+ * Style: plain, single-threaded, no SIMD, no blocking, no pruning beyond what
+ * the paper's algorithm states.  Unsigned 64-bit integers throughout,
+ * unsigned __int128 only where a product can exceed 64 bits.  INF is
+ * 2^64 - 1.
+ *
+ * Paper anchors:
+ *   quantisation     "profiled compute time" of a block and tau = A / B
+ *                    (Sec. 3.2, definitions after Eq. 2); congestion scaling
+ *                    of the bandwidth is part of the workload definition.
+ *   dp_pipe          Algorithm 1 with Eq. 1 (k >= 2) and Eq. 2 (k = 1),
+ *                    master enumeration, memory-infeasible candidates = INF,
+ *                    argmin over the master, backtrack (Sec. 3.2).
+ *   Lambda           end-to-end forward time, sum of stage times plus link
+ *                    times (Sec. 3.2, the per-request TPOT paragraph).
+ *   fitness          Eq. 3, Eq. 4, Eq. 5 with rates summed over replicas
+ *                    (Sec. 3.3) and the QoS floor 1/Lambda >= Min_TPS
+ *                    (Algorithm 2, Sec. 3.5).
+ *   ga_step          elite preservation (Algorithm 2; App. A) with the
+ *                    tournament / uniform-crossover / per-gene-mutation
+ *                    operators of the 16384-genome workload.
+ *
+ * Readings where the paper is silent or its listing is inconsistent:
+ *   R1  every device of a chain gets >= 1 contiguous block: DP(-1, k) = INF.
+ *   R2  block indices are 0-based; DP(i, k) covers blocks 0..i.
+ *   R3  TB(i, k) stores the start j of the last stage; the backtrack walks
+ *       k = m..2 and the first device takes the remaining i + 1 blocks.
+ *   R4  ties over j go to the smallest j (strict < in an ascending scan).
+ *   R5  ties over the master go to the smallest chain position.
+ *   R6  tau sits inside the max (compute and transfer overlap).
+ *   R7  head time / bytes are charged to the master's stage.
+ *   R8  memory: stage weight bytes (+ head bytes on the master) <= cap.
+ *   R9  chain order is ascending device id within a cluster label.
+ *   R10 ceil when quantising times, floor for the effective bandwidth.
+ *   R11 fixed-point fitness with SCALE = 2^50 (see oracle_eval).
+ *   R12 GA key (w, phase, index), smaller is better.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef unsigned __int128 u128;
+
+#define INF UINT64_MAX
+#define LIMIT48 ((uint64_t)1 << 48)
+#define SCALE ((uint64_t)1 << 50)
+
+enum { ORC_OK = 0, ORC_EINVAL = -1, ORC_EOVERFLOW = -2, ORC_ENOMEM = -3 };
+
+static uint64_t max2(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+/* ceil(a * 1e9 / b) for b > 0, or INF when the result does not fit 64 bits */
+static uint64_t ceil_ns(uint64_t a, uint64_t b)
+{
+    u128 num = (u128)a * 1000000000u;
+    u128 q = (num + b - 1) / b;
+    if (q >> 64) return INF;
+    return (uint64_t)q;
+}
+
+/*
+ * a0: integer cost tables.
+ *   t[r][d][n] = ceil(layer_flops[r][n] * 1e9 / speed[d])   ns
+ *   h[r][d]    = ceil(head_flops[r]     * 1e9 / speed[d])   ns
+ *   Beff[d][e] = floor(bw[d][e] * cong[d][e] / 1e6)         B/s
+ *   tau[r][d][e] = ceil(act[r] * 1e9 / Beff[d][e]), INF if Beff = 0; 0 on the diagonal
+ * Any finite time >= 2^48 is an overflow error.
+ */
+int oracle_quantise(int M, int N, const uint64_t *speed, const uint64_t *bw,
+                    const uint32_t *cong, const uint64_t *layer_flops /*[2][N]*/,
+                    const uint64_t *act /*[2]*/, const uint64_t *head_flops /*[2]*/,
+                    uint64_t *t /*[2][M][N]*/, uint64_t *h /*[2][M]*/,
+                    uint64_t *tau /*[2][M][M]*/)
+{
+    if (M < 1 || M > 256 || N < 1 || N > 255) return ORC_EINVAL;
+    for (int d = 0; d < M; d++)
+        if (speed[d] == 0) return ORC_EINVAL;
+    for (int i = 0; i < M * M; i++)
+        if (cong[i] > 1000000u) return ORC_EINVAL;
+    for (int r = 0; r < 2; r++) {
+        for (int d = 0; d < M; d++) {
+            for (int n = 0; n < N; n++) {
+                uint64_t v = ceil_ns(layer_flops[r * N + n], speed[d]);
+                if (v >= LIMIT48) return ORC_EOVERFLOW;
+                t[((size_t)r * M + d) * N + n] = v;
+            }
+            uint64_t hv = ceil_ns(head_flops[r], speed[d]);
+            if (hv >= LIMIT48) return ORC_EOVERFLOW;
+            h[r * M + d] = hv;
+        }
+        for (int d = 0; d < M; d++) {
+            for (int e = 0; e < M; e++) {
+                uint64_t v;
+                if (d == e) {
+                    v = 0;
+                } else {
+                    uint64_t beff = (uint64_t)(((u128)bw[d * M + e] * cong[d * M + e]) / 1000000u);
+                    if (beff == 0) {
+                        v = INF;
+                    } else {
+                        v = ceil_ns(act[r], beff);
+                        if (v >= LIMIT48) return ORC_EOVERFLOW;
+                    }
+                }
+                tau[((size_t)r * M + d) * M + e] = v;
+            }
+        }
+    }
+    return ORC_OK;
+}
+
+/*
+ * One DP table for a fixed master position mu (1-based), Eq. 1 and Eq. 2.
+ * D and TB are [N][m+1] (column 0 unused).  pt is [m][N+1] prefix sums of the
+ * chain devices' block times, pw is [N+1] prefix sums of block bytes, so
+ * that the sum over blocks j..i is pt[i+1] - pt[j].  Returns the number of
+ * candidates that reached the max/compare step.
+ */
+static uint64_t dp_table(int m, int N, int mu, const uint64_t *pt, const uint64_t *pw,
+                         const uint64_t *hk, const uint64_t *tau_link, const uint64_t *memk,
+                         uint64_t HB, uint64_t *D, int *TB)
+{
+    const int W = m + 1;
+    uint64_t evaluated = 0;
+    for (int i = 0; i < N; i++) {
+        for (int k = 1; k <= m; k++) {
+            const uint64_t *ptk = pt + (size_t)(k - 1) * (N + 1);
+            const uint64_t head_t = (k == mu) ? hk[k - 1] : 0;
+            const uint64_t head_b = (k == mu) ? HB : 0;
+            D[i * W + k] = INF;
+            TB[i * W + k] = -1;
+            if (k == 1) {
+                /* Eq. 2: the first device holds blocks 0..i */
+                uint64_t bytes = pw[i + 1] - pw[0] + head_b;
+                if (bytes <= memk[0])
+                    D[i * W + 1] = ptk[i + 1] - ptk[0] + head_t;
+                continue;
+            }
+            /* Eq. 1: device k holds blocks j..i, devices 1..k-1 hold 0..j-1 */
+            for (int j = 0; j <= i; j++) {
+                uint64_t prev = (j == 0) ? INF : D[(j - 1) * W + (k - 1)];
+                if (prev == INF) continue;
+                uint64_t bytes = pw[i + 1] - pw[j] + head_b;
+                if (bytes > memk[k - 1]) continue;
+                uint64_t cost = ptk[i + 1] - ptk[j] + head_t;
+                uint64_t v = max2(max2(prev, cost), tau_link[k - 1]);
+                evaluated++;
+                if (v < D[i * W + k]) {
+                    D[i * W + k] = v;
+                    TB[i * W + k] = j;
+                }
+            }
+        }
+    }
+    return evaluated;
+}
+
+/*
+ * DP_Pipe for one chain of m devices (Algorithm 1).
+ *   tk[m][N]   block times of the chain's devices, chain order
+ *   hk[m]      head + output-layer time of each chain device if it is master
+ *   tau_link[m] tau_link[k] = transfer time between chain positions k-1 and k
+ *              (k >= 1); tau_link[0] is unused
+ *   memk[m]    memory caps; W[N] block bytes; HB head bytes
+ * Outputs: *T (INF if infeasible), *Lambda, *mu_star (1-based, 0 if
+ * infeasible), sizes[m] (0 if infeasible), *evaluated (candidate count).
+ */
+int oracle_dp_pipe(int m, int N, const uint64_t *tk, const uint64_t *hk,
+                   const uint64_t *tau_link, const uint64_t *memk, const uint64_t *W,
+                   uint64_t HB, uint64_t *T, uint64_t *Lambda, int *mu_star, int *sizes,
+                   uint64_t *evaluated)
+{
+    *T = INF;
+    *Lambda = INF;
+    *mu_star = 0;
+    *evaluated = 0;
+    for (int k = 0; k < m; k++) sizes[k] = 0;
+    if (m < 1 || N < 1) return ORC_EINVAL;
+    if (m > N) return ORC_OK; /* R1: some device would hold no block */
+
+    uint64_t *pt = malloc(sizeof(uint64_t) * (size_t)m * (N + 1));
+    uint64_t *pw = malloc(sizeof(uint64_t) * (size_t)(N + 1));
+    uint64_t *D = malloc(sizeof(uint64_t) * (size_t)N * (m + 1));
+    int *TB = malloc(sizeof(int) * (size_t)N * (m + 1));
+    int *TBbest = malloc(sizeof(int) * (size_t)N * (m + 1));
+    if (!pt || !pw || !D || !TB || !TBbest) {
+        free(pt); free(pw); free(D); free(TB); free(TBbest);
+        return ORC_ENOMEM;
+    }
+    for (int k = 0; k < m; k++) {
+        pt[(size_t)k * (N + 1)] = 0;
+        for (int n = 0; n < N; n++)
+            pt[(size_t)k * (N + 1) + n + 1] = pt[(size_t)k * (N + 1) + n] + tk[(size_t)k * N + n];
+    }
+    pw[0] = 0;
+    for (int n = 0; n < N; n++) pw[n + 1] = pw[n] + W[n];
+
+    /* outer loop over the master position; keep the smallest mu on ties (R5) */
+    uint64_t best = INF;
+    int best_mu = 0;
+    for (int mu = 1; mu <= m; mu++) {
+        *evaluated += dp_table(m, N, mu, pt, pw, hk, tau_link, memk, HB, D, TB);
+        uint64_t Tmu = D[(N - 1) * (m + 1) + m];
+        if (Tmu < best) {
+            best = Tmu;
+            best_mu = mu;
+            memcpy(TBbest, TB, sizeof(int) * (size_t)N * (m + 1));
+        }
+    }
+    if (best != INF) {
+        /* backtrack (R3) */
+        int i = N - 1;
+        for (int k = m; k >= 2; k--) {
+            int j = TBbest[i * (m + 1) + k];
+            sizes[k - 1] = i - j + 1;
+            i = j - 1;
+        }
+        sizes[0] = i + 1;
+        /* Lambda: sum of stage times plus the chain's link times */
+        uint64_t lam = 0;
+        int start = 0;
+        for (int k = 1; k <= m; k++) {
+            int end = start + sizes[k - 1];
+            lam += pt[(size_t)(k - 1) * (N + 1) + end] - pt[(size_t)(k - 1) * (N + 1) + start];
+            if (k == best_mu) lam += hk[k - 1];
+            if (k >= 2) lam += tau_link[k - 1];
+            start = end;
+        }
+        *T = best;
+        *Lambda = lam;
+        *mu_star = best_mu;
+    }
+    free(pt); free(pw); free(D); free(TB); free(TBbest);
+    return ORC_OK;
+}
+
+/*
+ * Per-(individual, cluster) solve over a population.
+ *   labels[P][M]  cluster id of each device; ids >= k_max mean "unassigned"
+ *   roles[P][k_max] 0 = prefill, nonzero = decode
+ * Outputs T, Lambda [P][k_max] (INF for an empty or infeasible cluster),
+ * master [P][k_max] (device id, -1 if empty or infeasible), layers [P][M]
+ * (blocks on each device, 0 for unassigned devices and infeasible clusters).
+ * The chain of cluster q is its devices in ascending id (R9).
+ */
+int oracle_solve(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
+                 const uint64_t *mem, const uint64_t *W, uint64_t HB,
+                 int P, int k_max, const uint8_t *labels, const uint8_t *roles,
+                 uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers,
+                 uint64_t *evaluated_total)
+{
+    if (M < 1 || M > 256 || N < 1 || N > 255 || P < 0 || k_max < 1 || k_max > 255)
+        return ORC_EINVAL;
+    int chain[256];
+    int sizes[256];
+    uint64_t *tk = malloc(sizeof(uint64_t) * (size_t)M * N);
+    uint64_t hk[256], tl[256], mk[256];
+    if (!tk) return ORC_ENOMEM;
+    uint64_t total = 0;
+    for (int p = 0; p < P; p++) {
+        for (int d = 0; d < M; d++) layers[(size_t)p * M + d] = 0;
+        for (int q = 0; q < k_max; q++) {
+            size_t o = (size_t)p * k_max + q;
+            T[o] = INF;
+            Lambda[o] = INF;
+            master[o] = -1;
+            int m = 0;
+            for (int d = 0; d < M; d++)
+                if (labels[(size_t)p * M + d] == q) chain[m++] = d;
+            if (m == 0) continue;
+            int r = roles[o] != 0;
+            for (int k = 0; k < m; k++) {
+                memcpy(tk + (size_t)k * N, t + ((size_t)r * M + chain[k]) * N, sizeof(uint64_t) * N);
+                hk[k] = h[r * M + chain[k]];
+                mk[k] = mem[chain[k]];
+                tl[k] = (k == 0) ? 0 : tau[((size_t)r * M + chain[k - 1]) * M + chain[k]];
+            }
+            uint64_t Tv, Lv, ev;
+            int mu;
+            int rc = oracle_dp_pipe(m, N, tk, hk, tl, mk, W, HB, &Tv, &Lv, &mu, sizes, &ev);
+            if (rc) { free(tk); return rc; }
+            total += ev;
+            if (Tv == INF) continue;
+            T[o] = Tv;
+            Lambda[o] = Lv;
+            master[o] = (int16_t)chain[mu - 1];
+            for (int k = 0; k < m; k++) layers[(size_t)p * M + chain[k]] = (uint8_t)sizes[k];
+        }
+    }
+    free(tk);
+    if (evaluated_total) *evaluated_total = total;
+    return ORC_OK;
+}
+
+/*
+ * Fitness of one individual from its clusters' (T, Lambda, role), Eq. 3-5.
+ * Rates: a prefill replica serves NP tokens per T, so NP / PS = 1 / sum(1/T);
+ * a decode replica with one KV slot emits one token per T, so
+ * ND / DS = ND / sum(1/T).  In fixed point with SCALE = 2^50:
+ *   rho_c = floor(SCALE / max(T_c, 1))
+ *   S_P   = ceil(SCALE / sum_P rho),  S_D = ND * ceil(SCALE / sum_D rho)
+ *   phase = max(S_P, S_D)                               (Eq. 3)
+ *   excess = phase - T_a if phase > T_a else 0           (Eq. 4)
+ *   w = S_P + excess if excess > 0 else 0                (Eq. 5)
+ * Decode clusters whose Lambda exceeds floor(1e12 / min_tps_milli) ns fail
+ * the QoS floor and are dropped (min_tps_milli = 0 disables the floor).
+ * An individual with no usable prefill or no usable decode cluster gets
+ * w = phase = INF.
+ */
+static void fitness_one(int k_max, const uint64_t *T, const uint64_t *Lambda,
+                        const uint8_t *roles, uint64_t t_arrival, uint64_t nd,
+                        uint64_t min_tps_milli, uint64_t *w, uint64_t *phase,
+                        uint64_t *s_p, uint64_t *s_d)
+{
+    uint64_t sum_p = 0, sum_d = 0;
+    for (int q = 0; q < k_max; q++) {
+        if (T[q] == INF) continue;
+        int decode = roles[q] != 0;
+        if (decode && min_tps_milli > 0 && Lambda[q] > 1000000000000ull / min_tps_milli)
+            continue;
+        uint64_t rho = SCALE / (T[q] > 0 ? T[q] : 1);
+        if (decode) sum_d += rho;
+        else sum_p += rho;
+    }
+    uint64_t SP = sum_p ? (SCALE + sum_p - 1) / sum_p : INF;
+    uint64_t SD = sum_d ? nd * ((SCALE + sum_d - 1) / sum_d) : INF;
+    *s_p = SP;
+    *s_d = SD;
+    if (SP == INF || SD == INF) {
+        *w = INF;
+        *phase = INF;
+        return;
+    }
+    uint64_t ph = max2(SP, SD);
+    uint64_t excess = ph > t_arrival ? ph - t_arrival : 0;
+    *phase = ph;
+    *w = excess > 0 ? SP + excess : 0;
+}
+
+int oracle_fitness(int P, int k_max, const uint64_t *T, const uint64_t *Lambda,
+                   const uint8_t *roles, uint64_t t_arrival, uint64_t nd, uint64_t min_tps_milli,
+                   uint64_t *w, uint64_t *phase, uint64_t *s_p, uint64_t *s_d)
+{
+    if (P < 0 || k_max < 1 || k_max > 255 || nd > 8192) return ORC_EINVAL;
+    for (int p = 0; p < P; p++)
+        fitness_one(k_max, T + (size_t)p * k_max, Lambda + (size_t)p * k_max,
+                    roles + (size_t)p * k_max, t_arrival, nd, min_tps_milli,
+                    w + p, phase + p, s_p + p, s_d + p);
+    return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Counter-based random numbers: the SplitMix64 output function (Steele,   */
+/* Lea and Flood, "Fast splittable pseudorandom number generators",        */
+/* OOPSLA 2014) used as a keyed hash over (seed, generation, slot, stream, */
+/* gene): h <- seed; for c in (g, s, stream, gene): h <- mix(h ^ c).       */
+/* mix(z) = splitmix64 finaliser of (z + golden gamma).                     */
+/* ---------------------------------------------------------------------- */
+static uint64_t splitmix_out(uint64_t z)
+{
+    z += 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+uint64_t oracle_rng(uint64_t seed, uint64_t g, uint64_t s, uint64_t stream, uint64_t gene)
+{
+    uint64_t x = seed;
+    x = splitmix_out(x ^ g);
+    x = splitmix_out(x ^ s);
+    x = splitmix_out(x ^ stream);
+    x = splitmix_out(x ^ gene);
+    return x;
+}
+
+uint64_t oracle_splitmix_out(uint64_t z) { return splitmix_out(z); }
+
+/* GA random streams */
+#define ST_SEL_A 0u    /* + t, t < tournament_k: draws of the first parent  */
+#define ST_SEL_B 64u   /* + t: draws of the second parent                   */
+#define ST_XO_LABEL 128u
+#define ST_XO_ROLE 129u
+#define ST_MUT_LABEL 130u
+#define ST_MUT_ROLE 131u
+
+/* key order (w, phase, index): is individual a better (smaller) than b? */
+static int key_less(const uint64_t *w, const uint64_t *ph, int a, int b)
+{
+    if (w[a] != w[b]) return w[a] < w[b];
+    if (ph[a] != ph[b]) return ph[a] < ph[b];
+    return a < b;
+}
+
+static int tournament(uint64_t seed, uint64_t g, int s, unsigned base, int k, int P,
+                      const uint64_t *w, const uint64_t *ph)
+{
+    int best = -1;
+    for (int t = 0; t < k; t++) {
+        uint64_t u = oracle_rng(seed, g, (uint64_t)s, base + (unsigned)t, 0);
+        int idx = (int)(((u >> 32) * (uint64_t)P) >> 32);
+        if (best < 0 || key_less(w, ph, idx, best)) best = idx;
+    }
+    return best;
+}
+
+/*
+ * One generation of the GA (Algorithm 2: elites; crossover; mutation).
+ * Slots 0..n_elite-1 receive the n_elite best individuals in key order,
+ * copied unchanged.  Every other slot s breeds a child:
+ *   parents a, b: best of tournament_k uniform draws each (with replacement),
+ *     index = floor(hi32(u) * P / 2^32)
+ *   crossover, per label gene d: b[d] if lo32(u) < crossover_thresh else a[d];
+ *     per role gene q likewise (roles are written as 0/1)
+ *   mutation, per label gene: if hi32(u) < mutation_thresh the label is
+ *     redrawn as floor(lo32(u) * k_max / 2^32); per role gene: the bit flips
+ */
+int oracle_ga_step(int M, int P, int k_max, const uint8_t *labels_in, const uint8_t *roles_in,
+                   const uint64_t *w, const uint64_t *phase, uint64_t seed, uint32_t generation,
+                   uint32_t tournament_k, uint32_t xo_thresh, uint32_t mut_thresh,
+                   uint32_t n_elite, uint8_t *labels_out, uint8_t *roles_out)
+{
+    if (M < 1 || M > 256 || P < 1 || k_max < 1 || k_max > 255 || tournament_k < 1 ||
+        tournament_k > 64 || (int)n_elite > P || n_elite > 256)
+        return ORC_EINVAL;
+    const uint64_t g = generation;
+    /* elites: repeated selection of the next-best key (keys are distinct) */
+    int last = -1;
+    for (uint32_t e = 0; e < n_elite; e++) {
+        int pick = -1;
+        for (int p = 0; p < P; p++) {
+            if (last >= 0 && !key_less(w, phase, last, p)) continue; /* only keys after last */
+            if (pick < 0 || key_less(w, phase, p, pick)) pick = p;
+        }
+        memcpy(labels_out + (size_t)e * M, labels_in + (size_t)pick * M, (size_t)M);
+        memcpy(roles_out + (size_t)e * k_max, roles_in + (size_t)pick * k_max, (size_t)k_max);
+        last = pick;
+    }
+    for (int s = (int)n_elite; s < P; s++) {
+        int a = tournament(seed, g, s, ST_SEL_A, (int)tournament_k, P, w, phase);
+        int b = tournament(seed, g, s, ST_SEL_B, (int)tournament_k, P, w, phase);
+        for (int d = 0; d < M; d++) {
+            uint64_t u = oracle_rng(seed, g, (uint64_t)s, ST_XO_LABEL, (uint64_t)d);
+            uint8_t v = ((uint32_t)u < xo_thresh) ? labels_in[(size_t)b * M + d]
+                                                  : labels_in[(size_t)a * M + d];
+            uint64_t z = oracle_rng(seed, g, (uint64_t)s, ST_MUT_LABEL, (uint64_t)d);
+            if ((uint32_t)(z >> 32) < mut_thresh)
+                v = (uint8_t)((((uint64_t)(uint32_t)z) * (uint64_t)k_max) >> 32);
+            labels_out[(size_t)s * M + d] = v;
+        }
+        for (int q = 0; q < k_max; q++) {
+            uint64_t u = oracle_rng(seed, g, (uint64_t)s, ST_XO_ROLE, (uint64_t)q);
+            uint8_t v = ((uint32_t)u < xo_thresh) ? roles_in[(size_t)b * k_max + q]
+                                                  : roles_in[(size_t)a * k_max + q];
+            v = v != 0;
+            uint64_t z = oracle_rng(seed, g, (uint64_t)s, ST_MUT_ROLE, (uint64_t)q);
+            if ((uint32_t)(z >> 32) < mut_thresh) v ^= 1u;
+            roles_out[(size_t)s * k_max + q] = v;
+        }
+    }
+    return ORC_OK;
+}
