@@ -1,0 +1,222 @@
+/*
+ * e2.h - C ABI of the MI355X population-fitness library (libe2.so).
+ *
+ * The library evaluates whole populations of the deployment search of
+ * E2LLM (arXiv 2606.03770): for every (individual, cluster) pair it runs
+ * the paper's bottleneck-minimising layer partition (Algorithm 1, Eq. 1-2,
+ * Sec. 3.2), reduces the clusters of each individual to the queueing
+ * fitness of Eq. 3-5 (Sec. 3.3) under the QoS floor of Sec. 3.5, and
+ * breeds the next generation (Algorithm 2, Sec. 3.4).  All arithmetic is
+ * unsigned integer: times in nanoseconds, sizes in bytes.
+ *
+ * Conventions shared by every entry point:
+ *   - Return value: 0 (E2_OK) or a negative E2_E* code; e2_strerror names it.
+ *     Host-side argument checks run before anything is enqueued, so an
+ *     error return means nothing was launched.
+ *   - Device pointers ("device" below) are HIP device allocations owned by
+ *     the caller (for example torch CUDA tensors).  They must stay valid
+ *     until the work enqueued on `stream` has completed.  The library keeps
+ *     no pointer after a call returns.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.
+ *     Every compute call is asynchronous on that stream and never
+ *     synchronises the device.  Calls that need temporary device memory
+ *     take it stream-ordered from HIP's default memory pool
+ *     (hipMallocAsync / hipFreeAsync on the same stream).
+ *   - INF = UINT64_MAX marks "no feasible value" in every u64 output.
+ *   - A context is immutable after creation: one context may serve several
+ *     streams and host threads at once.  It lives on the device that was
+ *     current when it was created; calls must be made with that device
+ *     current.
+ */
+#ifndef E2_H
+#define E2_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define E2_OK 0
+#define E2_EINVAL (-1)    /* null pointer, size out of range, bad parameter   */
+#define E2_EOVERFLOW (-2) /* a quantised time would reach 2^48 ns             */
+#define E2_ENOMEM (-3)    /* a device or host allocation failed               */
+#define E2_EHIP (-4)      /* a HIP runtime call or kernel launch failed       */
+
+#define E2_INF UINT64_MAX
+#define E2_MAX_DEV 256    /* M: devices in the pool                          */
+#define E2_MAX_LAYER 255  /* N: transformer blocks of the model              */
+#define E2_MAX_CLUSTERS 255 /* k_max: cluster ids per genome                 */
+
+/*
+ * Problem instance: the inputs of Algorithm 1 and Algorithm 2 (Sec. 3.2,
+ * Sec. 3.4).  All pointers are HOST pointers, read only during
+ * e2_ctx_create / e2_quantise.
+ *
+ *   n_dev, n_layer   M in [1, 256] devices, N in [1, 255] blocks
+ *   speed_flops[M]   device compute speed in FLOP/s, > 0
+ *   mem_bytes[M]     memory available for weights on each device
+ *   bw_Bps[M*M]      link bandwidth d -> e in B/s, row-major; diagonal unused
+ *   congestion_ppm[M*M] bandwidth multiplier in parts per million, <= 1e6
+ *   layer_flops[2*N] FLOPs of each block, row 0 for prefill (the whole
+ *                    prompt), row 1 for decode (one token)
+ *   layer_bytes[N]   weight bytes of each block, < 2^48
+ *   act_bytes[2]     activation bytes one microbatch moves across a link
+ *                    (prefill, decode)
+ *   head_flops[2]    FLOPs of the LM head plus output layer, charged to the
+ *                    master device of a replica (Sec. 3.1, Sec. 3.2)
+ *   head_bytes       their weight bytes, counted on the master, < 2^48
+ */
+typedef struct e2_problem {
+    int32_t n_dev;
+    int32_t n_layer;
+    const uint64_t *speed_flops;
+    const uint64_t *mem_bytes;
+    const uint64_t *bw_Bps;
+    const uint32_t *congestion_ppm;
+    const uint64_t *layer_flops;
+    const uint64_t *layer_bytes;
+    uint64_t act_bytes[2];
+    uint64_t head_flops[2];
+    uint64_t head_bytes;
+} e2_problem;
+
+/*
+ * Fitness parameters (Eq. 3-5, Sec. 3.3; QoS floor, Sec. 3.5).
+ *   t_arrival_ns   request inter-arrival time T_a
+ *   nd_tokens      generated tokens per request ND, in [0, 8192]
+ *   min_tps_milli  per-request decode floor Min_TPS in tokens/s * 1000;
+ *                  0 disables the floor
+ */
+typedef struct e2_fitness_params {
+    uint64_t t_arrival_ns;
+    uint64_t nd_tokens;
+    uint64_t min_tps_milli;
+} e2_fitness_params;
+
+/*
+ * GA parameters (Algorithm 2).
+ *   seed, generation      key of the counter-based generator
+ *   tournament_k          draws per tournament, in [1, 64]
+ *   crossover_thresh_u32  a gene comes from the second parent when a
+ *                         uniform u32 draw is below it (2^31 = p 0.5)
+ *   mutation_thresh_u32   a gene mutates when a uniform u32 draw is below
+ *                         it (2^24 = rate 1/256)
+ *   n_elite               best individuals copied unchanged, in [0, 256],
+ *                         at most P
+ */
+typedef struct e2_ga_params {
+    uint64_t seed;
+    uint32_t generation;
+    uint32_t tournament_k;
+    uint32_t crossover_thresh_u32;
+    uint32_t mutation_thresh_u32;
+    uint32_t n_elite;
+} e2_ga_params;
+
+typedef struct e2_ctx e2_ctx;
+
+/*
+ * Validate and quantise a problem, upload the tables to the current device.
+ * Quantisation (the profiled block time and tau = A / B of Sec. 3.2, after
+ * Eq. 2), with exact 128-bit intermediates:
+ *   t[r][d][n]  = ceil(layer_flops[r][n] * 1e9 / speed[d])       ns
+ *   h[r][d]     = ceil(head_flops[r] * 1e9 / speed[d])           ns
+ *   Beff[d][e]  = floor(bw[d][e] * congestion[d][e] / 1e6)       B/s
+ *   tau[r][d][e]= ceil(act_bytes[r] * 1e9 / Beff[d][e]) ns, INF when Beff = 0
+ * Returns E2_EINVAL for a bad size or pointer, a zero speed or congestion
+ * above 1e6; E2_EOVERFLOW when a finite time reaches 2^48 ns or a byte
+ * size reaches 2^48; E2_ENOMEM / E2_EHIP on allocation or copy failure.
+ * On success *out owns device memory until e2_ctx_destroy.
+ */
+int e2_ctx_create(const e2_problem *prob, e2_ctx **out);
+
+/* Free a context (E2_EINVAL for NULL).  Work using it must have completed. */
+int e2_ctx_destroy(e2_ctx *ctx);
+
+/*
+ * Host-only quantisation, same formulas and errors as e2_ctx_create, for
+ * inspection: fills HOST arrays t[2][M][N], h[2][M], tau[2][M][M]
+ * (diagonal 0).  Makes no HIP call.
+ */
+int e2_quantise(const e2_problem *prob, uint64_t *t, uint64_t *h, uint64_t *tau);
+
+/*
+ * Partition every (individual, cluster) problem of a population
+ * (Algorithm 1 per replica, Sec. 3.2).
+ *
+ *   P            individuals, >= 0 (P = 0 is a no-op)
+ *   k_max        cluster ids per genome, in [1, 255]
+ *   labels[P][M] device: cluster id of each device; ids >= k_max leave the
+ *                device unassigned
+ *   roles[P][k_max] device: 0 = prefill replica, nonzero = decode replica
+ *   T[P][k_max]  device out: best bottleneck of the cluster (Eq. 1-2 with
+ *                the master enumerated), INF when the cluster is empty,
+ *                has more devices than blocks, or cannot fit in memory
+ *   Lambda[P][k_max] device out: end-to-end forward time of that best
+ *                plan, sum of stage times and link times (Sec. 3.2); INF
+ *                where T is INF
+ *   master[P][k_max] device out: master device id, -1 where T is INF
+ *   layers[P][M] device out: blocks placed on each device; 0 for unassigned
+ *                devices and devices of infeasible clusters
+ *
+ * A cluster's device chain is its devices in ascending id order.  Each
+ * device holds >= 1 contiguous block; stage k holds blocks j..i with
+ * weight bytes (+ head bytes on the master) <= mem_bytes; the bottleneck
+ * is the max over stage times (+ head time on the master) and link times
+ * of consecutive chain devices; ties go to the smallest master position
+ * and, within the recurrence, to the smallest split point j.
+ */
+int e2_solve_partitions(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                        const uint8_t *labels, const uint8_t *roles,
+                        uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers);
+
+/*
+ * Fitness of every individual (Eq. 3-5, Sec. 3.3) from its clusters'
+ * partitions.  Same labels/roles layout as e2_solve_partitions.
+ *   w[P], phase[P] device out: waiting time (Eq. 5) and bottleneck phase
+ *                  (Eq. 3) in ns; both INF for an individual without a
+ *                  usable prefill or a usable decode cluster
+ *   s_p[P], s_d[P] device out, may be NULL: NP/PS and ND/DS in ns, INF when
+ *                  the role has no usable cluster
+ * Fixed point with SCALE = 2^50: rho_c = floor(SCALE / max(T_c, 1));
+ * S_P = ceil(SCALE / sum_prefill rho); S_D = ND * ceil(SCALE / sum_decode rho);
+ * phase = max(S_P, S_D); w = S_P + (phase - T_a) if phase > T_a else 0.
+ * A decode cluster is usable only if Lambda <= floor(1e12 / min_tps_milli).
+ */
+int e2_eval_population(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                       const uint8_t *labels, const uint8_t *roles,
+                       const e2_fitness_params *fp,
+                       uint64_t *w, uint64_t *phase, uint64_t *s_p, uint64_t *s_d);
+
+/*
+ * One GA generation (Algorithm 2: elites, crossover, mutation; Sec. 3.4).
+ *   labels_in[P][M], roles_in[P][k_max], w_in[P], phase_in[P]  device in
+ *   labels_out[P][M], roles_out[P][k_max]  device out; must not overlap
+ *                                          the inputs
+ * Individuals are ranked by the key (w, phase, index), smaller is better.
+ * Slots 0..n_elite-1 receive the n_elite best in key order, unchanged.
+ * Every other slot s breeds one child with the generator
+ *   rng(seed, g, s, stream, gene): x = seed; then x = mix(x ^ c) for c in
+ *   (g, s, stream, gene), mix = the SplitMix64 output function (Steele,
+ *   Lea and Flood, OOPSLA 2014) of x + 0x9E3779B97F4A7C15;
+ * parent a = best of tournament_k draws on streams 0.., parent b on
+ * streams 64..; draw index = floor(hi32 * P / 2^32);
+ * label gene d: from b if lo32(rng(.., 128, d)) < crossover_thresh, else
+ * a; then redrawn as floor(lo32 * k_max / 2^32) if hi32(rng(.., 130, d))
+ * < mutation_thresh; role gene q: likewise on streams 129 and 131, roles
+ * written as 0/1 and flipped on mutation.
+ */
+int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+               const uint8_t *labels_in, const uint8_t *roles_in,
+               const uint64_t *w_in, const uint64_t *phase_in, const e2_ga_params *gp,
+               uint8_t *labels_out, uint8_t *roles_out);
+
+/* Static string for an E2_* code ("unknown error" otherwise). */
+const char *e2_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* E2_H */

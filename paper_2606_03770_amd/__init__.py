@@ -1,0 +1,262 @@
+"""Python binding of libe2.so, the MI355X population-fitness library.
+
+Argument marshalling only: every step of the path runs in the HIP kernels
+behind the C ABI of include/e2.h.  torch supplies device memory (CUDA
+tensors on ROCm) and streams.  The wrappers keep the C names:
+
+    e2_quantise(problem)                              host tables (t, h, tau)
+    e2_ctx_create(problem) -> Context                 quantise + upload
+    e2_solve_partitions(ctx, labels, roles)           Algorithm 1 per cluster
+    e2_eval_population(ctx, labels, roles, fitness)   Eq. 3-5 per individual
+    e2_ga_step(ctx, labels, roles, w, phase, ga)      one GA generation
+
+`problem` is a dict with the fields of e2_problem (numpy arrays), as
+returned by workload.Workload.problem_arrays().  64-bit unsigned outputs
+come back as torch.int64 tensors holding the same bits; u64() views them as
+numpy uint64.
+
+If libe2.so has not been built, importing works but every call raises
+E2Error: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libe2.so")
+
+E2_OK, E2_EINVAL, E2_EOVERFLOW, E2_ENOMEM, E2_EHIP = 0, -1, -2, -3, -4
+INF = (1 << 64) - 1
+
+EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitions",
+            "e2_eval_population", "e2_ga_step", "e2_strerror")
+
+
+class E2Error(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        msg = lib().e2_strerror(code).decode() if _lib is not None else str(code)
+        super().__init__(f"{where}: {msg} ({code})")
+
+
+class e2_problem(ctypes.Structure):
+    _fields_ = [("n_dev", ctypes.c_int32), ("n_layer", ctypes.c_int32),
+                ("speed_flops", ctypes.c_void_p), ("mem_bytes", ctypes.c_void_p),
+                ("bw_Bps", ctypes.c_void_p), ("congestion_ppm", ctypes.c_void_p),
+                ("layer_flops", ctypes.c_void_p), ("layer_bytes", ctypes.c_void_p),
+                ("act_bytes", ctypes.c_uint64 * 2), ("head_flops", ctypes.c_uint64 * 2),
+                ("head_bytes", ctypes.c_uint64)]
+
+
+class e2_fitness_params(ctypes.Structure):
+    _fields_ = [("t_arrival_ns", ctypes.c_uint64), ("nd_tokens", ctypes.c_uint64),
+                ("min_tps_milli", ctypes.c_uint64)]
+
+
+class e2_ga_params(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("generation", ctypes.c_uint32),
+                ("tournament_k", ctypes.c_uint32), ("crossover_thresh_u32", ctypes.c_uint32),
+                ("mutation_thresh_u32", ctypes.c_uint32), ("n_elite", ctypes.c_uint32)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libe2.so; raises E2Error(-4) style RuntimeError if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run paper_2606_03770_amd.csrc.build")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32 = ctypes.c_void_p, ctypes.c_int32
+    L.e2_strerror.argtypes = [ctypes.c_int]
+    L.e2_strerror.restype = ctypes.c_char_p
+    L.e2_quantise.argtypes = [ctypes.POINTER(e2_problem), vp, vp, vp]
+    L.e2_quantise.restype = ctypes.c_int
+    L.e2_ctx_create.argtypes = [ctypes.POINTER(e2_problem), ctypes.POINTER(vp)]
+    L.e2_ctx_create.restype = ctypes.c_int
+    L.e2_ctx_destroy.argtypes = [vp]
+    L.e2_ctx_destroy.restype = ctypes.c_int
+    L.e2_solve_partitions.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, vp, vp]
+    L.e2_solve_partitions.restype = ctypes.c_int
+    L.e2_eval_population.argtypes = [vp, vp, i32, i32, vp, vp, ctypes.POINTER(e2_fitness_params),
+                                     vp, vp, vp, vp]
+    L.e2_eval_population.restype = ctypes.c_int
+    L.e2_ga_step.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, ctypes.POINTER(e2_ga_params),
+                             vp, vp]
+    L.e2_ga_step.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(rc: int, where: str):
+    if rc != E2_OK:
+        raise E2Error(rc, where)
+
+
+def _np(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=dtype))
+
+
+def _make_problem(problem: dict):
+    """Build an e2_problem; returns (struct, keepalive arrays)."""
+    M, N = int(problem["n_dev"]), int(problem["n_layer"])
+    keep = dict(
+        speed=_np(problem["speed_flops"], np.uint64), mem=_np(problem["mem_bytes"], np.uint64),
+        bw=_np(problem["bw_Bps"], np.uint64), cong=_np(problem["congestion_ppm"], np.uint32),
+        lf=_np(problem["layer_flops"], np.uint64).reshape(-1),
+        lb=_np(problem["layer_bytes"], np.uint64))
+    act = _np(problem["act_bytes"], np.uint64)
+    hf = _np(problem["head_flops"], np.uint64)
+    s = e2_problem(M, N, keep["speed"].ctypes.data, keep["mem"].ctypes.data,
+                   keep["bw"].ctypes.data, keep["cong"].ctypes.data, keep["lf"].ctypes.data,
+                   keep["lb"].ctypes.data, (ctypes.c_uint64 * 2)(int(act[0]), int(act[1])),
+                   (ctypes.c_uint64 * 2)(int(hf[0]), int(hf[1])), int(problem["head_bytes"]))
+    return s, keep
+
+
+def e2_quantise(problem: dict):
+    """Host-only quantisation: returns numpy (t [2][M][N], h [2][M], tau [2][M][M])."""
+    s, keep = _make_problem(problem)
+    M, N = s.n_dev, s.n_layer
+    if not (1 <= M <= 256 and 1 <= N <= 255):
+        _check(E2_EINVAL, "e2_quantise")
+    t = np.zeros((2, M, N), np.uint64)
+    h = np.zeros((2, M), np.uint64)
+    tau = np.zeros((2, M, M), np.uint64)
+    _check(lib().e2_quantise(ctypes.byref(s), t.ctypes.data, h.ctypes.data, tau.ctypes.data),
+           "e2_quantise")
+    return t, h, tau
+
+
+class Context:
+    """Owns one e2_ctx (device tables of one problem instance)."""
+
+    def __init__(self, handle: int, n_dev: int, n_layer: int):
+        self.handle = handle
+        self.n_dev = n_dev
+        self.n_layer = n_layer
+
+    def close(self):
+        if self.handle:
+            _check(lib().e2_ctx_destroy(self.handle), "e2_ctx_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def e2_ctx_create(problem: dict) -> Context:
+    s, keep = _make_problem(problem)
+    h = ctypes.c_void_p()
+    _check(lib().e2_ctx_create(ctypes.byref(s), ctypes.byref(h)), "e2_ctx_create")
+    return Context(h.value, s.n_dev, s.n_layer)
+
+
+def e2_ctx_destroy(ctx: Context):
+    ctx.close()
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, dtype, shape, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA tensor")
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name}: want {dtype} {tuple(shape)} contiguous, got "
+                         f"{t.dtype} {tuple(t.shape)}")
+    return t
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def e2_solve_partitions(ctx: Context, labels, roles, stream=None, out: Optional[dict] = None):
+    """Returns dict T, Lambda (int64 bits of u64) [P][k_max], master int16 [P][k_max],
+    layers uint8 [P][M]."""
+    torch = _torch()
+    P, M = labels.shape
+    k_max = roles.shape[1]
+    _dev(labels, torch.uint8, (P, ctx.n_dev), "labels")
+    _dev(roles, torch.uint8, (P, k_max), "roles")
+    dev = labels.device
+    if out is None:
+        out = dict(T=torch.empty((P, k_max), dtype=torch.int64, device=dev),
+                   Lambda=torch.empty((P, k_max), dtype=torch.int64, device=dev),
+                   master=torch.empty((P, k_max), dtype=torch.int16, device=dev),
+                   layers=torch.empty((P, M), dtype=torch.uint8, device=dev))
+    _check(lib().e2_solve_partitions(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
+                                     _ptr(roles), _ptr(out["T"]), _ptr(out["Lambda"]),
+                                     _ptr(out["master"]), _ptr(out["layers"])),
+           "e2_solve_partitions")
+    return out
+
+
+def e2_eval_population(ctx: Context, labels, roles, fitness: dict, stream=None,
+                       with_rates: bool = True, out: Optional[dict] = None):
+    """Returns dict w, phase (and s_p, s_d) as int64 bits of u64, shape [P]."""
+    torch = _torch()
+    P = labels.shape[0]
+    k_max = roles.shape[1]
+    _dev(labels, torch.uint8, (P, ctx.n_dev), "labels")
+    _dev(roles, torch.uint8, (P, k_max), "roles")
+    dev = labels.device
+    if out is None:
+        names = ("w", "phase", "s_p", "s_d") if with_rates else ("w", "phase")
+        out = {k: torch.empty(P, dtype=torch.int64, device=dev) for k in names}
+    fp = e2_fitness_params(int(fitness["t_arrival_ns"]), int(fitness["nd_tokens"]),
+                           int(fitness["min_tps_milli"]))
+    _check(lib().e2_eval_population(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
+                                    _ptr(roles), ctypes.byref(fp), _ptr(out["w"]),
+                                    _ptr(out["phase"]), _ptr(out.get("s_p")),
+                                    _ptr(out.get("s_d"))),
+           "e2_eval_population")
+    return out
+
+
+def e2_ga_step(ctx: Context, labels_in, roles_in, w, phase, ga: dict, stream=None,
+               out: Optional[tuple] = None):
+    """Returns (labels_out uint8 [P][M], roles_out uint8 [P][k_max])."""
+    torch = _torch()
+    P = labels_in.shape[0]
+    k_max = roles_in.shape[1]
+    _dev(labels_in, torch.uint8, (P, ctx.n_dev), "labels_in")
+    _dev(roles_in, torch.uint8, (P, k_max), "roles_in")
+    _dev(w, torch.int64, (P,), "w")
+    _dev(phase, torch.int64, (P,), "phase")
+    if out is None:
+        out = (torch.empty_like(labels_in), torch.empty_like(roles_in))
+    gp = e2_ga_params(int(ga["seed"]), int(ga["generation"]), int(ga["tournament_k"]),
+                      int(ga["crossover_thresh_u32"]), int(ga["mutation_thresh_u32"]),
+                      int(ga["n_elite"]))
+    _check(lib().e2_ga_step(ctx.handle, _stream(stream), P, k_max, _ptr(labels_in),
+                            _ptr(roles_in), _ptr(w), _ptr(phase), ctypes.byref(gp),
+                            _ptr(out[0]), _ptr(out[1])),
+           "e2_ga_step")
+    return out
+
+
+def u64(t) -> np.ndarray:
+    """View an int64 tensor holding u64 bits as a numpy uint64 array (host copy)."""
+    return t.detach().cpu().numpy().view(np.uint64)

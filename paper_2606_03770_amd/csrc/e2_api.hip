@@ -1,0 +1,359 @@
+// Host side of libe2.so: argument checks, integer quantisation, derived
+// tables, device uploads and the stream-ordered launches behind the C ABI
+// declared in include/e2.h.
+
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "../../include/e2.h"
+#include "e2_internal.h"
+
+namespace {
+
+typedef unsigned __int128 u128;
+constexpr uint64_t kLimit48 = 1ull << 48;
+
+// ceil(a * 1e9 / b) for b > 0 in exact 128-bit arithmetic; saturates to
+// UINT64_MAX (which the callers treat as an overflow).
+uint64_t ceil_ns(uint64_t a, uint64_t b)
+{
+    const u128 num = (u128)a * 1000000000u;
+    const u128 q = num / b + (num % b != 0);
+    return (q >> 64) ? UINT64_MAX : (uint64_t)q;
+}
+
+int check_problem(const e2_problem *pr)
+{
+    if (!pr) return E2_EINVAL;
+    const int M = pr->n_dev, N = pr->n_layer;
+    if (M < 1 || M > E2_MAX_DEV || N < 1 || N > E2_MAX_LAYER) return E2_EINVAL;
+    if (!pr->speed_flops || !pr->mem_bytes || !pr->bw_Bps || !pr->congestion_ppm ||
+        !pr->layer_flops || !pr->layer_bytes)
+        return E2_EINVAL;
+    for (int d = 0; d < M; ++d)
+        if (pr->speed_flops[d] == 0) return E2_EINVAL;
+    for (int i = 0; i < M * M; ++i)
+        if (pr->congestion_ppm[i] > 1000000u) return E2_EINVAL;
+    for (int n = 0; n < N; ++n)
+        if (pr->layer_bytes[n] >= kLimit48) return E2_EOVERFLOW;
+    if (pr->head_bytes >= kLimit48) return E2_EOVERFLOW;
+    return E2_OK;
+}
+
+// Fill t[2][M][N], h[2][M], tau[2][M][M] (host arrays).
+int quantise(const e2_problem *pr, uint64_t *t, uint64_t *h, uint64_t *tau)
+{
+    const int M = pr->n_dev, N = pr->n_layer;
+    for (int r = 0; r < 2; ++r) {
+        for (int d = 0; d < M; ++d) {
+            const uint64_t S = pr->speed_flops[d];
+            for (int n = 0; n < N; ++n) {
+                const uint64_t v = ceil_ns(pr->layer_flops[(size_t)r * N + n], S);
+                if (v >= kLimit48) return E2_EOVERFLOW;
+                t[((size_t)r * M + d) * N + n] = v;
+            }
+            const uint64_t hv = ceil_ns(pr->head_flops[r], S);
+            if (hv >= kLimit48) return E2_EOVERFLOW;
+            h[(size_t)r * M + d] = hv;
+        }
+        for (int d = 0; d < M; ++d) {
+            for (int e = 0; e < M; ++e) {
+                uint64_t v = 0;
+                if (d != e) {
+                    const size_t ix = (size_t)d * M + e;
+                    const uint64_t beff =
+                        (uint64_t)(((u128)pr->bw_Bps[ix] * pr->congestion_ppm[ix]) / 1000000u);
+                    if (beff == 0) {
+                        v = E2_INF64;
+                    } else {
+                        v = ceil_ns(pr->act_bytes[r], beff);
+                        if (v >= kLimit48) return E2_EOVERFLOW;
+                    }
+                }
+                tau[((size_t)r * M + d) * M + e] = v;
+            }
+        }
+    }
+    return E2_OK;
+}
+
+hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+int check_device(const e2_ctx *ctx)
+{
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return E2_EHIP;
+    return cur == ctx->device ? E2_OK : E2_EINVAL;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Stream-ordered scratch for one call.
+struct Scratch {
+    void *base = nullptr;
+    hipStream_t stream = nullptr;
+    ~Scratch()
+    {
+        if (base) (void)hipFreeAsync(base, stream);
+    }
+};
+
+int alloc_scratch(Scratch &sc, hipStream_t s, size_t bytes)
+{
+    sc.stream = s;
+    if (hipMallocAsync(&sc.base, bytes, s) != hipSuccess) {
+        sc.base = nullptr;
+        (void)hipGetLastError();
+        return E2_ENOMEM;
+    }
+    return E2_OK;
+}
+
+// Lay out counters, the problem list and the split-point fallback after
+// `extra` leading bytes.
+size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_bytes)
+{
+    const size_t problems = (size_t)P * k_max;
+    *slots = e2_dp_slots((int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX));
+    const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
+    // the fallback is needed only when some chain's table exceeds the LDS copy
+    const bool need_tb = (size_t)mcap * ctx->N > 4096;
+    *tb_bytes = need_tb ? (size_t)(*slots) * ctx->N * ctx->N : 0;
+    return align256(16) + align256(problems * 4) + align256(*tb_bytes);
+}
+
+void carve_work(void *base, const e2_ctx *ctx, int P, int k_max, int slots, size_t tb_bytes,
+                E2Work *wk)
+{
+    char *p = static_cast<char *>(base);
+    wk->counters = reinterpret_cast<uint32_t *>(p);
+    p += align256(16);
+    wk->list = reinterpret_cast<uint32_t *>(p);
+    p += align256((size_t)P * k_max * 4);
+    wk->tb_global = tb_bytes ? reinterpret_cast<uint8_t *>(p) : nullptr;
+    wk->n_slots = slots;
+    (void)ctx;
+}
+
+int check_pop(int P, int k_max)
+{
+    if (P < 0 || P >= (1 << 24) || k_max < 1 || k_max > E2_MAX_CLUSTERS) return E2_EINVAL;
+    return E2_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *e2_strerror(int code)
+{
+    switch (code) {
+    case E2_OK: return "ok";
+    case E2_EINVAL: return "invalid argument";
+    case E2_EOVERFLOW: return "quantised value reaches 2^48";
+    case E2_ENOMEM: return "out of memory";
+    case E2_EHIP: return "HIP runtime error";
+    default: return "unknown error";
+    }
+}
+
+int e2_quantise(const e2_problem *prob, uint64_t *t, uint64_t *h, uint64_t *tau)
+{
+    const int rc = check_problem(prob);
+    if (rc) return rc;
+    if (!t || !h || !tau) return E2_EINVAL;
+    return quantise(prob, t, h, tau);
+}
+
+int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
+{
+    if (!out) return E2_EINVAL;
+    *out = nullptr;
+    int rc = check_problem(prob);
+    if (rc) return rc;
+    const int M = prob->n_dev, N = prob->n_layer;
+    std::vector<uint64_t> t((size_t)2 * M * N), h((size_t)2 * M), tau((size_t)2 * M * M);
+    rc = quantise(prob, t.data(), h.data(), tau.data());
+    if (rc) return rc;
+
+    // prefix sums of block times per role and device
+    std::vector<uint64_t> pref((size_t)2 * M * (N + 1));
+    for (int r = 0; r < 2; ++r)
+        for (int d = 0; d < M; ++d) {
+            uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
+            row[0] = 0;
+            for (int n = 0; n < N; ++n) row[n + 1] = row[n] + t[((size_t)r * M + d) * N + n];
+        }
+    // memory windows: smallest start j such that bytes(j..i) (+ head) <= mem
+    std::vector<uint64_t> wpref(N + 1, 0);
+    for (int n = 0; n < N; ++n) wpref[n + 1] = wpref[n] + prob->layer_bytes[n];
+    std::vector<uint8_t> win((size_t)2 * M * N), cap0(M), capH(M);
+    for (int f = 0; f < 2; ++f)
+        for (int d = 0; d < M; ++d) {
+            const uint64_t extra = f ? prob->head_bytes : 0;
+            const uint64_t mem = prob->mem_bytes[d];
+            int j = 0, best = 0;
+            for (int i = 0; i < N; ++i) {
+                // advance j until blocks j..i (+ extra) fit or j passes i
+                while (j <= i && wpref[i + 1] - wpref[j] + extra > mem) ++j;
+                uint8_t v = E2_NO_START;
+                if (j <= i) {
+                    v = (uint8_t)j;
+                    if (i - j + 1 > best) best = i - j + 1;
+                }
+                win[((size_t)f * M + d) * N + i] = v;
+            }
+            (f ? capH : cap0)[d] = (uint8_t)best;
+        }
+
+    const size_t b_pref = align256(pref.size() * 8), b_head = align256(h.size() * 8),
+                 b_tau = align256(tau.size() * 8), b_win = align256(win.size()),
+                 b_cap = align256((size_t)M);
+    const size_t total = b_pref + b_head + b_tau + b_win + 2 * b_cap;
+    e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
+    if (!ctx) return E2_ENOMEM;
+    if (hipGetDevice(&ctx->device) != hipSuccess) {
+        free(ctx);
+        return E2_EHIP;
+    }
+    if (hipMalloc(&ctx->blob, total) != hipSuccess) {
+        (void)hipGetLastError();
+        free(ctx);
+        return E2_ENOMEM;
+    }
+    char *p = static_cast<char *>(ctx->blob);
+    char *d_pref = p;
+    char *d_head = d_pref + b_pref;
+    char *d_tau = d_head + b_head;
+    char *d_win = d_tau + b_tau;
+    char *d_cap0 = d_win + b_win;
+    char *d_capH = d_cap0 + b_cap;
+    hipError_t e = hipSuccess;
+    if (e == hipSuccess) e = hipMemcpy(d_pref, pref.data(), pref.size() * 8, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_head, h.data(), h.size() * 8, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_tau, tau.data(), tau.size() * 8, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_win, win.data(), win.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_cap0, cap0.data(), (size_t)M, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_capH, capH.data(), (size_t)M, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(ctx->blob);
+        free(ctx);
+        return E2_EHIP;
+    }
+    ctx->M = M;
+    ctx->N = N;
+    ctx->head_bytes = prob->head_bytes;
+    ctx->tables.pref = reinterpret_cast<const uint64_t *>(d_pref);
+    ctx->tables.head = reinterpret_cast<const uint64_t *>(d_head);
+    ctx->tables.tau = reinterpret_cast<const uint64_t *>(d_tau);
+    ctx->tables.win = reinterpret_cast<const uint8_t *>(d_win);
+    ctx->tables.cap0 = reinterpret_cast<const uint8_t *>(d_cap0);
+    ctx->tables.capH = reinterpret_cast<const uint8_t *>(d_capH);
+    ctx->tables.M = M;
+    ctx->tables.N = N;
+    *out = ctx;
+    return E2_OK;
+}
+
+int e2_ctx_destroy(e2_ctx *ctx)
+{
+    if (!ctx) return E2_EINVAL;
+    const hipError_t e = hipFree(ctx->blob);
+    free(ctx);
+    return e == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+int e2_solve_partitions(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                        const uint8_t *labels, const uint8_t *roles, uint64_t *T,
+                        uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    if (!ctx) return E2_EINVAL;
+    int rc = check_pop(P, k_max);
+    if (rc) return rc;
+    if (P == 0) return E2_OK;
+    if (!labels || !roles || !T || !Lambda || !master || !layers) return E2_EINVAL;
+    if ((rc = check_device(ctx))) return rc;
+    hipStream_t s = as_stream(stream);
+    int slots;
+    size_t tbb;
+    const size_t bytes = work_bytes(ctx, P, k_max, &slots, &tbb);
+    Scratch sc;
+    if ((rc = alloc_scratch(sc, s, bytes))) return rc;
+    E2Work wk;
+    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk);
+    const hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, labels, roles, wk, T,
+                                              Lambda, master, layers);
+    return e == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+int e2_eval_population(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                       const uint8_t *labels, const uint8_t *roles, const e2_fitness_params *fp,
+                       uint64_t *w, uint64_t *phase, uint64_t *s_p, uint64_t *s_d)
+{
+    if (!ctx || !fp) return E2_EINVAL;
+    int rc = check_pop(P, k_max);
+    if (rc) return rc;
+    if (fp->nd_tokens > 8192) return E2_EINVAL;
+    if (P == 0) return E2_OK;
+    if (!labels || !roles || !w || !phase) return E2_EINVAL;
+    if ((rc = check_device(ctx))) return rc;
+    hipStream_t s = as_stream(stream);
+    int slots;
+    size_t tbb;
+    const size_t wb = work_bytes(ctx, P, k_max, &slots, &tbb);
+    const size_t tl = align256((size_t)P * k_max * 8);
+    Scratch sc;
+    if ((rc = alloc_scratch(sc, s, wb + 2 * tl))) return rc;
+    E2Work wk;
+    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk);
+    uint64_t *Ts = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
+    uint64_t *Ls = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb + tl);
+    hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, labels, roles, wk, Ts, Ls,
+                                        nullptr, nullptr);
+    if (e != hipSuccess) return E2_EHIP;
+    const uint64_t lam_max =
+        fp->min_tps_milli ? 1000000000000ull / fp->min_tps_milli : E2_INF64;
+    e = e2_launch_fitness(s, P, k_max, Ts, Ls, roles, fp->t_arrival_ns, fp->nd_tokens, lam_max,
+                          w, phase, s_p, s_d);
+    return e == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_t *labels_in,
+               const uint8_t *roles_in, const uint64_t *w_in, const uint64_t *phase_in,
+               const e2_ga_params *gp, uint8_t *labels_out, uint8_t *roles_out)
+{
+    if (!ctx || !gp) return E2_EINVAL;
+    int rc = check_pop(P, k_max);
+    if (rc) return rc;
+    if (P == 0) return E2_OK;
+    if (!labels_in || !roles_in || !w_in || !phase_in || !labels_out || !roles_out)
+        return E2_EINVAL;
+    if (gp->tournament_k < 1 || gp->tournament_k > 64 || gp->n_elite > 256 ||
+        gp->n_elite > (uint32_t)P)
+        return E2_EINVAL;
+    const size_t M = (size_t)ctx->M;
+    // outputs must not overlap the inputs
+    auto overlap = [](const void *a, size_t na, const void *b, size_t nb) {
+        const char *x = static_cast<const char *>(a), *y = static_cast<const char *>(b);
+        return x < y + nb && y < x + na;
+    };
+    const size_t nl = (size_t)P * M, nr = (size_t)P * k_max;
+    if (overlap(labels_out, nl, labels_in, nl) || overlap(labels_out, nl, roles_in, nr) ||
+        overlap(roles_out, nr, labels_in, nl) || overlap(roles_out, nr, roles_in, nr) ||
+        overlap(labels_out, nl, roles_out, nr))
+        return E2_EINVAL;
+    if ((rc = check_device(ctx))) return rc;
+    hipStream_t s = as_stream(stream);
+    Scratch sc;
+    if ((rc = alloc_scratch(sc, s, align256(256 * 4)))) return rc;
+    const hipError_t e = e2_launch_ga(s, ctx->M, P, k_max, labels_in, roles_in, w_in, phase_in,
+                                      gp->seed, gp->generation, gp->tournament_k,
+                                      gp->crossover_thresh_u32, gp->mutation_thresh_u32,
+                                      gp->n_elite, static_cast<uint32_t *>(sc.base), labels_out,
+                                      roles_out);
+    return e == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+}  // extern "C"

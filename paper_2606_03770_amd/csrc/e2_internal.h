@@ -1,0 +1,58 @@
+// Internal declarations shared by the host API (e2_api.hip) and the kernels
+// (e2_kernels.hip) of libe2.so.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define E2_INF64 0xFFFFFFFFFFFFFFFFull
+#define E2_NO_START 0xFFu  // window table: no stage ending at i fits
+
+// Read-only device tables built once per context.
+struct E2Tables {
+    const uint64_t *pref;  // [2][M][N+1] prefix sums of block times per role and device
+    const uint64_t *head;  // [2][M] head + output-layer time per role and device
+    const uint64_t *tau;   // [2][M][M] link time per role, INF for a dead link
+    const uint8_t *win;    // [2][M][N] smallest stage start j so that blocks j..i fit
+                           //   ([0]: no head bytes, [1]: with head bytes), E2_NO_START if none
+    const uint8_t *cap0;   // [M] most blocks one stage can hold without the head
+    const uint8_t *capH;   // [M] most blocks one stage can hold with the head
+    int M;
+    int N;
+};
+
+struct e2_ctx {
+    int device;
+    int M, N;
+    uint64_t head_bytes;
+    void *blob;  // one device allocation holding every table
+    E2Tables tables;
+};
+
+// Scratch layout of one solve/eval call (device memory, stream-ordered).
+struct E2Work {
+    uint32_t *counters;  // [0] problems listed, [1] next problem to take
+    uint32_t *list;      // [P * k_max] (p << 8) | q of problems needing the DP
+    uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
+    int n_slots;         // waves of the DP kernel
+};
+
+// Number of DP waves launched for `problems` upper-bound problems.
+int e2_dp_slots(int problems);
+
+// Enqueue cluster extraction + DP.  Outputs may be the caller's (solve) or
+// scratch (eval; master/layers null).
+hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_max,
+                                const uint8_t *labels, const uint8_t *roles, const E2Work &wk,
+                                uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers);
+
+hipError_t e2_launch_fitness(hipStream_t s, int P, int k_max, const uint64_t *T,
+                             const uint64_t *Lambda, const uint8_t *roles, uint64_t t_arrival,
+                             uint64_t nd, uint64_t lambda_max, uint64_t *w, uint64_t *phase,
+                             uint64_t *s_p, uint64_t *s_d);
+
+hipError_t e2_launch_ga(hipStream_t s, int M, int P, int k_max, const uint8_t *labels_in,
+                        const uint8_t *roles_in, const uint64_t *w, const uint64_t *phase,
+                        uint64_t seed, uint32_t generation, uint32_t tournament_k,
+                        uint32_t xo_thresh, uint32_t mut_thresh, uint32_t n_elite,
+                        uint32_t *elite_scratch, uint8_t *labels_out, uint8_t *roles_out);

@@ -1,0 +1,204 @@
+"""GPU parity: every output of the HIP path equals the CPU oracle bit for bit.
+
+All integer work, so the bar is exact equality on T, Lambda, master, layers
+(Algorithm 1 per cluster), w, phase, S_P, S_D (Eq. 3-5) and the bred
+genomes (GA step).  Inputs are seeded synthetic workloads; the named ones are
+run at their full population in the same launch configuration the bench
+uses, and checked on sampled individuals where the oracle would take long.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2606_03770_amd as e2
+from paper_2606_03770_amd import workload
+
+pytestmark = pytest.mark.gpu
+INF = (1 << 64) - 1
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    e2.lib()
+    return torch, torch.device("cuda:0")
+
+
+def _gpu_all(torch_dev, wl, labels=None, roles=None, ctx=None):
+    torch, dev = torch_dev
+    labels = wl.labels if labels is None else labels
+    roles = wl.roles if roles is None else roles
+    ctx = ctx or e2.e2_ctx_create(wl.problem_arrays())
+    L = torch.from_numpy(np.ascontiguousarray(labels)).to(dev)
+    R = torch.from_numpy(np.ascontiguousarray(roles)).to(dev)
+    sol = e2.e2_solve_partitions(ctx, L, R)
+    fit = e2.e2_eval_population(ctx, L, R, wl.fitness_params())
+    torch.cuda.synchronize()
+    out = dict(T=e2.u64(sol["T"]), Lambda=e2.u64(sol["Lambda"]),
+               master=sol["master"].cpu().numpy(), layers=sol["layers"].cpu().numpy())
+    for k in ("w", "phase", "s_p", "s_d"):
+        out[k] = e2.u64(fit[k])
+    return out
+
+
+def _oracle_all(wl, labels=None, roles=None):
+    return oracle.eval_population(wl, labels, roles)
+
+
+def _assert_equal(got, want, rows=None, tag=""):
+    for k in ("T", "Lambda", "master", "layers", "w", "phase", "s_p", "s_d"):
+        g = got[k] if rows is None else got[k][rows]
+        w = want[k]
+        bad = np.argwhere(np.asarray(g != w).reshape(len(w), -1).any(axis=1)).ravel()
+        assert bad.size == 0, f"{tag} {k}: {bad.size} rows differ, first {bad[:5]}"
+
+
+def _small_cases():
+    cases = []
+    rng = np.random.default_rng(2026)
+    for seed in range(24):
+        M = int(rng.integers(1, 48))
+        N = int(rng.integers(1, 70))
+        P = int(rng.integers(1, 24))
+        k_max = int(rng.integers(1, 9))
+        kw = dict(mem_hi_layers=float(rng.uniform(3, 60)), zero_bw_frac=0.1,
+                  head=bool(seed % 3), layer_var=bool(seed % 2))
+        cases.append((seed, M, N, P, k_max, kw))
+    return cases
+
+
+@pytest.mark.parametrize("case", _small_cases(), ids=lambda c: f"s{c[0]}-M{c[1]}-N{c[2]}")
+def test_random_small_parity(torch_dev, case):
+    seed, M, N, P, k_max, kw = case
+    print(f"case seed={seed} M={M} N={N} P={P} k_max={k_max}", flush=True)
+    wl = workload.random_small(seed, M=M, N=N, P=P, k_max=k_max, **kw)
+    labels = wl.labels.copy()
+    rng = np.random.default_rng(seed)
+    labels[rng.uniform(size=labels.shape) < 0.05] = 250  # some devices unassigned
+    _assert_equal(_gpu_all(torch_dev, wl, labels), _oracle_all(wl, labels), tag=f"seed {seed}")
+
+
+def test_uniform_layers_many_ties(torch_dev):
+    """Identical blocks and devices: every master and many split points tie."""
+    wl = workload.random_small(5, M=30, N=40, P=12, k_max=3, layer_var=False,
+                               mem_hi_layers=80, cong_full=True)
+    wl.speed_flops[:] = wl.speed_flops[0]
+    _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag="ties")
+
+
+def test_large_chain_uses_global_split_table(torch_dev):
+    """m * N above the LDS copy of the split-point table (70 x 100)."""
+    wl = workload.random_small(8, M=70, N=100, P=2, k_max=1, mem_lo_layers=3,
+                               mem_hi_layers=30)
+    _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag="global tb")
+
+
+def test_maximum_sizes(torch_dev):
+    """M = 256 devices, N = 255 blocks, k_max = 255 (mostly single-device
+    clusters) and k_max = 4 (chains of ~64 devices)."""
+    for k_max, P in ((255, 3), (4, 2)):
+        print(f"max sizes k_max={k_max}", flush=True)
+        wl = workload.random_small(9 + k_max, M=256, N=255, P=P, k_max=k_max,
+                                   mem_lo_layers=2, mem_hi_layers=25)
+        _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag=f"max k={k_max}")
+
+
+def test_degenerate_shapes(torch_dev):
+    for (M, N, k_max) in ((1, 1, 1), (1, 7, 1), (5, 1, 5), (5, 1, 1), (3, 2, 1)):
+        wl = workload.random_small(M * 100 + N, M=M, N=N, P=4, k_max=k_max, mem_hi_layers=20)
+        _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag=f"M{M} N{N}")
+
+
+def test_empty_population_is_a_no_op(torch_dev):
+    torch, dev = torch_dev
+    wl = workload.random_small(1, M=4, N=4, P=1, k_max=2)
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    L = torch.zeros((0, 4), dtype=torch.uint8, device=dev)
+    R = torch.zeros((0, 2), dtype=torch.uint8, device=dev)
+    out = e2.e2_solve_partitions(ctx, L, R)
+    fit = e2.e2_eval_population(ctx, L, R, wl.fitness_params())
+    torch.cuda.synchronize()
+    assert out["T"].numel() == 0 and fit["w"].numel() == 0
+
+
+@pytest.mark.parametrize("name,rows", [
+    ("c1_tiny_12dev_32L", None), ("c2_32dev_48L", None), ("c3_64dev_80L", None),
+    ("c4_128dev_80L", 384), ("c5_256dev_126L_ga", 48)])
+def test_named_workloads(torch_dev, name, rows):
+    """Full population on the GPU; the oracle checks all rows or a sample."""
+    print(f"workload {name}", flush=True)
+    wl = workload.make(name)
+    got = _gpu_all(torch_dev, wl)
+    if rows is None:
+        _assert_equal(got, _oracle_all(wl), tag=name)
+        return
+    rng = np.random.default_rng(99)
+    pick = np.sort(np.r_[np.arange(8), rng.choice(np.arange(8, wl.population), rows - 8,
+                                                   replace=False)])
+    sub = wl.subset(pick)
+    _assert_equal(got, _oracle_all(sub), rows=pick, tag=name)
+    # the feasible fraction must be meaningful for this workload
+    assert (got["T"] != INF).any() and (got["w"] != INF).any()
+
+
+def test_population_order_does_not_matter(torch_dev):
+    wl = workload.make("c2_32dev_48L")
+    a = _gpu_all(torch_dev, wl)
+    perm = np.random.default_rng(3).permutation(wl.population)
+    b = _gpu_all(torch_dev, wl, wl.labels[perm], wl.roles[perm])
+    for k in a:
+        assert (a[k][perm] == b[k]).all(), k
+
+
+def _gpu_ga(torch_dev, wl, labels, roles, w, phase, gen):
+    torch, dev = torch_dev
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    L = torch.from_numpy(np.ascontiguousarray(labels)).to(dev)
+    R = torch.from_numpy(np.ascontiguousarray(roles)).to(dev)
+    W = torch.from_numpy(np.asarray(w, np.uint64).view(np.int64)).to(dev)
+    PH = torch.from_numpy(np.asarray(phase, np.uint64).view(np.int64)).to(dev)
+    lo, ro = e2.e2_ga_step(ctx, L, R, W, PH, wl.ga_params(gen))
+    torch.cuda.synchronize()
+    return lo.cpu().numpy(), ro.cpu().numpy()
+
+
+@pytest.mark.parametrize("n_elite,tk", [(1, 4), (0, 1), (7, 9), (256, 4)])
+def test_ga_step_parity_random(torch_dev, n_elite, tk):
+    rng = np.random.default_rng(n_elite * 31 + tk)
+    P, M, k_max = 300, 37, 11
+    wl = workload.random_small(4, M=M, N=8, P=P, k_max=k_max)
+    wl.n_elite, wl.tournament_k = n_elite, tk
+    wl.mutation_thresh_u32 = 1 << 28
+    w = rng.integers(0, 50, size=P).astype(np.uint64)  # many ties in w
+    w[rng.uniform(size=P) < 0.2] = np.uint64(INF)
+    ph = rng.integers(0, 5, size=P).astype(np.uint64)
+    got = _gpu_ga(torch_dev, wl, wl.labels, wl.roles, w, ph, 17)
+    want = oracle.ga_step(wl.labels, wl.roles, w, ph, k_max, **wl.ga_params(17))
+    assert (got[0] == want[0]).all() and (got[1] == want[1]).all()
+
+
+def test_ga_loop_on_the_16384_genome_workload(torch_dev):
+    """Three generations of eval + GA on the GPU; each generation's GA output
+    equals the oracle's GA fed the GPU's population and fitness, and sampled
+    individuals' fitness equals the oracle's."""
+    torch, dev = torch_dev
+    wl = workload.make("c5_256dev_126L_ga")
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    rng = np.random.default_rng(5)
+    for g in range(3):
+        print(f"generation {g}", flush=True)
+        fit = e2.e2_eval_population(ctx, L, R, wl.fitness_params())
+        lo, ro = e2.e2_ga_step(ctx, L, R, fit["w"], fit["phase"], wl.ga_params(g))
+        torch.cuda.synchronize()
+        labels, roles = L.cpu().numpy(), R.cpu().numpy()
+        w, ph = e2.u64(fit["w"]), e2.u64(fit["phase"])
+        pick = np.sort(rng.choice(wl.population, 12, replace=False))
+        sub = wl.subset(pick)
+        want = oracle.eval_population(sub, labels[pick], roles[pick])
+        assert (w[pick] == want["w"]).all() and (ph[pick] == want["phase"]).all()
+        el, er = oracle.ga_step(labels, roles, w, ph, wl.k_max, **wl.ga_params(g))
+        assert (lo.cpu().numpy() == el).all() and (ro.cpu().numpy() == er).all()
+        L, R = lo, ro
