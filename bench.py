@@ -139,7 +139,13 @@ def main():
     ap.add_argument("--workload", default="c5_256dev_126L_ga", choices=workload.NAMES)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU-oracle sample (0 disables)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES bytes 5 times "
+                         "(reference for the HBM byte counters) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported in this build "
               f"(the evaluation shards by genome range; see the design notes)", file=sys.stderr)
@@ -242,6 +248,18 @@ def main():
     if args.cpu_seconds > 0:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def copy_calibration(nbytes):
+    """A plain copy of a known size: FETCH_SIZE / WRITE_SIZE per dispatch of
+    this kernel, against nbytes, give the scale of the byte counters."""
+    import torch
+    src = torch.ones(nbytes // 8, dtype=torch.int64, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": (nbytes // 8) * 8, "launches": 5}), flush=True)
 
 
 def cpu_baseline(wl, seconds):
