@@ -118,8 +118,9 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
     const size_t problems = (size_t)P * k_max;
     *slots = e2_dp_slots((int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX));
     const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
-    // the fallback is needed only when some chain's table exceeds the LDS copy
-    const bool need_tb = (size_t)mcap * ctx->N > 4096;
+    // the fallback is needed only when some chain's split points exceed the
+    // LDS pool of the reference path
+    const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_pool_cells(ctx->N) * 8;
     *tb_bytes = need_tb ? (size_t)(*slots) * ctx->N * ctx->N : 0;
     return align256(16) + align256(problems * 4) + align256(*tb_bytes);
 }
@@ -189,7 +190,7 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     // memory windows: smallest start j such that bytes(j..i) (+ head) <= mem
     std::vector<uint64_t> wpref(N + 1, 0);
     for (int n = 0; n < N; ++n) wpref[n + 1] = wpref[n] + prob->layer_bytes[n];
-    std::vector<uint8_t> win((size_t)2 * M * N), cap0(M), capH(M);
+    std::vector<uint8_t> win((size_t)2 * M * N), wend((size_t)M * N), cap0(M), capH(M);
     for (int f = 0; f < 2; ++f)
         for (int d = 0; d < M; ++d) {
             const uint64_t extra = f ? prob->head_bytes : 0;
@@ -207,11 +208,20 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
             }
             (f ? capH : cap0)[d] = (uint8_t)best;
         }
+    // window ends (no head): largest i such that blocks j..i fit, scanning j downwards
+    for (int d = 0; d < M; ++d) {
+        const uint64_t mem = prob->mem_bytes[d];
+        int i = N - 1;
+        for (int j = N - 1; j >= 0; --j) {
+            while (i >= j && wpref[i + 1] - wpref[j] > mem) --i;
+            wend[(size_t)d * N + j] = (i >= j) ? (uint8_t)i : E2_NO_START;
+        }
+    }
 
     const size_t b_pref = align256(pref.size() * 8), b_head = align256(h.size() * 8),
                  b_tau = align256(tau.size() * 8), b_win = align256(win.size()),
-                 b_cap = align256((size_t)M);
-    const size_t total = b_pref + b_head + b_tau + b_win + 2 * b_cap;
+                 b_wend = align256(wend.size()), b_cap = align256((size_t)M);
+    const size_t total = b_pref + b_head + b_tau + b_win + b_wend + 2 * b_cap;
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
     if (!ctx) return E2_ENOMEM;
     if (hipGetDevice(&ctx->device) != hipSuccess) {
@@ -228,13 +238,15 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     char *d_head = d_pref + b_pref;
     char *d_tau = d_head + b_head;
     char *d_win = d_tau + b_tau;
-    char *d_cap0 = d_win + b_win;
+    char *d_wend = d_win + b_win;
+    char *d_cap0 = d_wend + b_wend;
     char *d_capH = d_cap0 + b_cap;
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMemcpy(d_pref, pref.data(), pref.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_head, h.data(), h.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_tau, tau.data(), tau.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_win, win.data(), win.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_wend, wend.data(), wend.size(), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_cap0, cap0.data(), (size_t)M, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_capH, capH.data(), (size_t)M, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
@@ -249,6 +261,7 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     ctx->tables.head = reinterpret_cast<const uint64_t *>(d_head);
     ctx->tables.tau = reinterpret_cast<const uint64_t *>(d_tau);
     ctx->tables.win = reinterpret_cast<const uint8_t *>(d_win);
+    ctx->tables.wend = reinterpret_cast<const uint8_t *>(d_wend);
     ctx->tables.cap0 = reinterpret_cast<const uint8_t *>(d_cap0);
     ctx->tables.capH = reinterpret_cast<const uint8_t *>(d_capH);
     ctx->tables.M = M;

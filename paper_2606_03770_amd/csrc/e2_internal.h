@@ -15,6 +15,8 @@ struct E2Tables {
     const uint64_t *tau;   // [2][M][M] link time per role, INF for a dead link
     const uint8_t *win;    // [2][M][N] smallest stage start j so that blocks j..i fit
                            //   ([0]: no head bytes, [1]: with head bytes), E2_NO_START if none
+    const uint8_t *wend;   // [M][N] largest stage end i so that blocks j..i fit without the
+                           //   head, E2_NO_START if block j alone does not fit
     const uint8_t *cap0;   // [M] most blocks one stage can hold without the head
     const uint8_t *capH;   // [M] most blocks one stage can hold with the head
     int M;
@@ -39,6 +41,9 @@ struct E2Work {
 
 // Number of DP waves launched for `problems` upper-bound problems.
 int e2_dp_slots(int problems);
+// Forward-row pool of one DP wave (u64 cells) and its dynamic LDS bytes.
+int e2_dp_pool_cells(int N);
+size_t e2_dp_lds_bytes(int N);
 
 // Enqueue cluster extraction + DP.  Outputs may be the caller's (solve) or
 // scratch (eval; master/layers null).
