@@ -15,9 +15,9 @@ Printed on one JSON line:
   fitness_evals_per_s   genomes scored per second
   roofline     the DP launch (extraction + DP + fitness kernels of one
                e2_eval_population call, timed with events on its stream)
-               against the int32 VALU peak: 8 int32 VALU ops per j-candidate
-               the kernel evaluates (64-bit subtract 2, 64-bit max 3,
-               64-bit min 3)
+               against the int32 VALU peak: 8 int32 VALU ops per useful
+               j-candidate of the DP kernel (64-bit subtract 2, 64-bit max 3,
+               64-bit min 3), counted on the host from the same inputs
   cpu_baseline the CPU oracle on a bounded sample of the same generation-0
                population, single-threaded
 """
@@ -52,17 +52,22 @@ def log(msg):
 # ---------------------------------------------------------------------------
 # Work accounting (host side, from the same integer inputs).
 # ---------------------------------------------------------------------------
+POOL_CELLS = 1024  # forward-row pool of one DP wave (k_dp)
+
+
 def window_tables(wl):
-    """win[f][d][i]: smallest start j with blocks j..i (+ head if f) within
-    device d's memory, 255 if none; cap[f][d]: longest stage that fits."""
+    """Per device: window starts win[f][d][i] (smallest j with blocks j..i,
+    plus the head if f, within memory; 255 if none), reversed-block window
+    starts winR[d][x], and the longest stage cap[f][d]."""
     M, N = wl.n_dev, wl.n_layer
     wp = np.concatenate([[0], np.cumsum(wl.layer_bytes.astype(object))])
     win = np.full((2, M, N), 255, dtype=np.int64)
+    winR = np.full((M, N), 255, dtype=np.int64)
     cap = np.zeros((2, M), dtype=np.int64)
-    for f in range(2):
-        extra = int(wl.head_bytes) if f else 0
-        for d in range(M):
-            mem = int(wl.mem_bytes[d])
+    for d in range(M):
+        mem = int(wl.mem_bytes[d])
+        for f in range(2):
+            extra = int(wl.head_bytes) if f else 0
             j = 0
             for i in range(N):
                 while j <= i and wp[i + 1] - wp[j] + extra > mem:
@@ -70,63 +75,141 @@ def window_tables(wl):
                 if j <= i:
                     win[f, d, i] = j
                     cap[f, d] = max(cap[f, d], i - j + 1)
-    return win, cap
+        y = 0
+        for x in range(N):
+            while y <= x and wp[N - y] - wp[N - 1 - x] > mem:
+                y += 1
+            if y <= x:
+                winR[d, x] = y
+    return win, winR, cap
 
 
-def row_candidates(win, N):
-    """rc[f][d][k]: j-candidates of DP row k (k >= 2) on device d."""
-    i = np.arange(N)
-    rc = np.zeros(win.shape[:2] + (N + 1,), dtype=np.int64)
-    for k in range(2, N + 1):
-        lo = np.maximum(win, k - 1)
-        c = np.where((win == 255) | (i < k - 1), 0, np.maximum(0, i - lo + 1))
-        rc[:, :, k] = c.sum(axis=2)
-    return rc
+def count_tables(win, winR, N):
+    """Prefix sums over cells of the window lengths i - max(w(i), kmin) + 1
+    (0 where no stage fits), for every device and every kmin:
+    C[f][d][kmin][i] (forward, f = head), CR[d][kmin][x] (reversed)."""
+    def build(w):
+        k = np.arange(N)[:, None]                  # kmin
+        i = np.arange(N)[None, :]                  # cell
+        lo = np.maximum(w[..., None, :], k)        # [..., kmin, cell]
+        c = np.where(w[..., None, :] == 255, 0, np.maximum(0, i - lo + 1))
+        out = np.zeros(c.shape[:-1] + (N + 1,), dtype=np.int64)
+        np.cumsum(c, axis=-1, out=out[..., 1:])
+        return out
+    return build(win), build(winR)
 
 
-def generation_work(wl, labels, T, master, win_cap_rc):
-    """(Algorithm 1 cells over feasible problems, j-candidates the DP kernel
-    evaluates) for one population, vectorised over (genome, device)."""
-    win, cap, rc = win_cap_rc
+def generation_work(wl, labels, T, master, tabs):
+    """(Algorithm 1 cells over feasible problems, useful j-candidates the DP
+    kernel evaluates) for one population.  The candidate count follows k_dp
+    row by row: forward rows, reversed rows, one combine per master, the
+    chosen master's rows and last cell (or, for chains whose bands exceed
+    the pool, one full table per master plus the chosen master's again)."""
+    win, winR, cap, C, CR = tabs
     N, K = wl.n_layer, wl.k_max
     P, M = labels.shape
-    lab = labels.astype(np.int64)
-    assigned = lab < K
-    pp = np.repeat(np.arange(P), M).reshape(P, M)
-    dd = np.tile(np.arange(M), (P, 1))
-    key = (pp * 256 + np.where(assigned, lab, 255)).ravel()
-    m = np.bincount(key, minlength=P * 256).reshape(P, 256)[:, :K]
     feasible = T != INF
-    cells = int((m * (m * N - m * (m - 1) // 2))[feasible].sum())
-    # chain position (1-based) of every device: rank by id within (genome, label)
-    order = np.lexsort((dd.ravel(), key))
-    sk = key[order]
-    first = np.r_[0, np.nonzero(np.diff(sk))[0] + 1]
-    start = np.repeat(first, np.diff(np.r_[first, len(sk)]))
-    rank = np.empty(P * M, dtype=np.int64)
-    rank[order] = np.arange(P * M) - start + 1
-    rank = rank.reshape(P, M)
-    c0 = cap[0][dd]
-    csum = np.bincount(key, weights=c0.ravel(), minlength=P * 256).reshape(P, 256)[:, :K]
-    cmin = np.full(P * 256, 1 << 30, dtype=np.int64)
-    np.minimum.at(cmin, key, c0.ravel())
-    cmin = cmin.reshape(P, 256)[:, :K]
-    hmax = np.zeros(P * 256, dtype=np.int64)
-    np.maximum.at(hmax, key, cap[1][dd].ravel())
-    hmax = hmax.reshape(P, 256)[:, :K]
-    listed = (m >= 1) & (m <= N) & (csum >= N) & (cmin >= 1) & (hmax >= 1)
-    k = np.minimum(rank, N)
-    r0 = np.where(rank >= 2, rc[0][dd, k], 0)
-    r1 = np.where(rank >= 2, rc[1][dd, k], 0)
-    mq = np.where(assigned, m[pp, np.minimum(lab, K - 1)], 0)
-    per_dev = (mq - 1) * r0 + r1  # every master position
-    # one more pass for the chosen master of feasible clusters
-    safe_lab = np.minimum(lab, K - 1)
-    mdev = master[pp, safe_lab].astype(np.int64)
-    mrank = np.where(mdev >= 0, rank[pp, np.maximum(mdev, 0)], 0)
-    per_dev += np.where(feasible[pp, safe_lab], np.where(rank == mrank, r1, r0), 0)
-    use = assigned & listed[pp, safe_lab]
-    cand = int(per_dev[use].sum())
+    cells = 0
+    cand = 0
+
+    def rows(f, d, kmin, lo, hi):
+        """useful candidates of rows with cells lo..hi (arrays, broadcast)"""
+        ok = hi >= lo
+        lo_c = np.clip(lo, 0, N)
+        hi_c = np.clip(hi + 1, 0, N)
+        v = C[f, d, np.clip(kmin, 0, N - 1), hi_c] - C[f, d, np.clip(kmin, 0, N - 1), lo_c]
+        return np.where(ok, v, 0)
+
+    def rrows(d, kmin, lo, hi):
+        ok = hi >= lo
+        v = CR[d, np.clip(kmin, 0, N - 1), np.clip(hi + 1, 0, N)] - \
+            CR[d, np.clip(kmin, 0, N - 1), np.clip(lo, 0, N)]
+        return np.where(ok, v, 0)
+
+    # group problems by chain length
+    probs = {}
+    for p in range(P):
+        row = labels[p]
+        for q in np.unique(row):
+            if q >= K:
+                continue
+            chain = np.nonzero(row == q)[0]
+            probs.setdefault(len(chain), []).append((p, q, chain))
+    for m, lst in probs.items():
+        n = len(lst)
+        pq = np.array([(a, b) for a, b, _ in lst])
+        ch = np.stack([c for _, _, c in lst])                      # [n, m]
+        feas = feasible[pq[:, 0], pq[:, 1]]
+        cells += int(feas.sum()) * m * (m * N - m * (m - 1) // 2)
+        c0, cH = cap[0][ch], cap[1][ch]
+        listed = (m <= N) & (c0.sum(1) >= N) & (c0.min(1) >= 1) & (cH.max(1) >= 1)
+        if not listed.any():
+            continue
+        ch, c0, cH, feas, pq = ch[listed], c0[listed], cH[listed], feas[listed], pq[listed]
+        n = len(ch)
+        mu = np.zeros(n, dtype=np.int64)
+        mdev = master[pq[:, 0], pq[:, 1]].astype(np.int64)
+        for a in range(n):
+            if feas[a]:
+                mu[a] = int(np.nonzero(ch[a] == mdev[a])[0][0]) + 1
+        k = np.arange(1, m + 1)                                     # [m]
+        pre = np.concatenate([np.zeros((n, 1), np.int64), np.cumsum(c0, 1)], 1)
+        tot = pre[:, m:m + 1]
+        flo = np.maximum(k - 1, N - 1 - (tot - pre[:, 1:]))
+        fhi = np.minimum(N - 1 - (m - k), pre[:, 1:] - 1)
+        sizes = np.where(fhi >= flo, fhi - flo + 1, 0)
+        pool = sizes[:, :m - 1].sum(1)
+        fast = pool <= POOL_CELLS
+        # --- fast path
+        if fast.any():
+            chf, c0f, cHf = ch[fast], c0[fast], cH[fast]
+            lof, hif, muf = flo[fast], fhi[fast], mu[fast]
+            pref = pre[fast]
+            kk = np.broadcast_to(k, lof.shape)
+            jm0 = np.maximum(kk - 1, lof - c0f + 1)
+            jmH = np.maximum(kk - 1, lof - cHf + 1)
+            # forward rows 2..m-1 and combines 2..m
+            fwd = rows(0, chf, jm0, lof, hif)
+            comb = np.where(cHf > 0, rows(1, chf, jmH, lof, hif), 0)
+            tot_f = fwd[:, 1:m - 1].sum(1) + comb[:, 1:].sum(1)
+            # reversed rows t = 2..m-1: device k = m+1-t
+            for t in range(2, m):
+                kd = m + 1 - t
+                tt = pref[:, m]
+                gl = np.maximum(kd - 1, N - (tt - pref[:, kd - 1]))
+                gh = np.minimum(pref[:, kd - 1], N - (m - kd + 1))
+                xlo, xhi = N - 1 - gh, N - 1 - gl
+                d = chf[:, kd - 1]
+                jm = np.maximum(t - 1, xlo - c0f[:, kd - 1] + 1)
+                tot_f += np.where(gh >= gl, rrows(d, jm, xlo, xhi), 0)
+            # chosen master's rows mu*..m-1 and the last cell
+            ff = muf > 0
+            for kk1 in range(2, m):
+                isn = (kk1 == muf)
+                sel = ff & (kk1 >= muf)
+                f_arr = isn.astype(np.int64)
+                jm = np.where(isn, jmH[:, kk1 - 1], jm0[:, kk1 - 1])
+                v0 = rows(0, chf[:, kk1 - 1], jm, lof[:, kk1 - 1], hif[:, kk1 - 1])
+                v1 = rows(1, chf[:, kk1 - 1], jm, lof[:, kk1 - 1], hif[:, kk1 - 1])
+                tot_f += np.where(sel, np.where(f_arr == 1, v1, v0), 0)
+            if m >= 2:
+                isn = (muf == m)
+                capl = np.where(isn, cHf[:, m - 1], c0f[:, m - 1])
+                jm = np.maximum(m - 1, N - capl)
+                v0 = rows(0, chf[:, m - 1], jm, np.full(len(chf), N - 1), np.full(len(chf), N - 1))
+                v1 = rows(1, chf[:, m - 1], jm, np.full(len(chf), N - 1), np.full(len(chf), N - 1))
+                tot_f += np.where(ff, np.where(isn, v1, v0), 0)
+            cand += int(tot_f.sum())
+        # --- reference path
+        if (~fast).any():
+            chs, mus = ch[~fast], mu[~fast]
+            lo = np.broadcast_to(k - 1, chs.shape)
+            hi = np.full(chs.shape, N - 1)
+            r0 = rows(0, chs, lo, lo, hi)
+            r1 = rows(1, chs, lo, lo, hi)
+            per = ((m - 1) * r0 + r1)[:, 1:].sum(1)
+            extra = np.where(np.arange(1, m + 1)[None, :] == mus[:, None], r1, r0)[:, 1:].sum(1)
+            cand += int((per + np.where(mus > 0, extra, 0)).sum())
     return cells, cand
 
 
@@ -203,8 +286,8 @@ def main():
         f"{np.mean(eval_ms):.3f} ms avg")
 
     # replay the same generations to count the work (outside the timed region)
-    wcr = window_tables(wl)
-    wcr = (wcr[0], wcr[1], row_candidates(wcr[0], wl.n_layer))
+    win, winR, cap = window_tables(wl)
+    wcr = (win, winR, cap) + count_tables(win, winR, wl.n_layer)
     Lr, Rr = L0.clone(), R0.clone()
     cells = cand = 0
     for g in range(args.steps):

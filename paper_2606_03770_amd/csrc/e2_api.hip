@@ -190,7 +190,7 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     // memory windows: smallest start j such that bytes(j..i) (+ head) <= mem
     std::vector<uint64_t> wpref(N + 1, 0);
     for (int n = 0; n < N; ++n) wpref[n + 1] = wpref[n] + prob->layer_bytes[n];
-    std::vector<uint8_t> win((size_t)2 * M * N), wend((size_t)M * N), cap0(M), capH(M);
+    std::vector<uint8_t> win((size_t)2 * M * N), cap0(M), capH(M);
     for (int f = 0; f < 2; ++f)
         for (int d = 0; d < M; ++d) {
             const uint64_t extra = f ? prob->head_bytes : 0;
@@ -208,20 +208,30 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
             }
             (f ? capH : cap0)[d] = (uint8_t)best;
         }
-    // window ends (no head): largest i such that blocks j..i fit, scanning j downwards
+    // reversed blocks (block N-1 first): prefix sums and window starts, used
+    // by the backward rows of the DP, which run as forward rows on them
+    std::vector<uint64_t> prefR((size_t)2 * M * (N + 1));
+    for (int r = 0; r < 2; ++r)
+        for (int d = 0; d < M; ++d) {
+            const uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
+            uint64_t *rev = &prefR[((size_t)r * M + d) * (N + 1)];
+            for (int x = 0; x <= N; ++x) rev[x] = row[N] - row[N - x];
+        }
+    std::vector<uint8_t> winR((size_t)M * N);
     for (int d = 0; d < M; ++d) {
         const uint64_t mem = prob->mem_bytes[d];
-        int i = N - 1;
-        for (int j = N - 1; j >= 0; --j) {
-            while (i >= j && wpref[i + 1] - wpref[j] > mem) --i;
-            wend[(size_t)d * N + j] = (i >= j) ? (uint8_t)i : E2_NO_START;
+        // reversed blocks y..x are original blocks N-1-x..N-1-y
+        int y = 0;
+        for (int x = 0; x < N; ++x) {
+            while (y <= x && wpref[N - y] - wpref[N - 1 - x] > mem) ++y;
+            winR[(size_t)d * N + x] = (y <= x) ? (uint8_t)y : E2_NO_START;
         }
     }
 
     const size_t b_pref = align256(pref.size() * 8), b_head = align256(h.size() * 8),
                  b_tau = align256(tau.size() * 8), b_win = align256(win.size()),
-                 b_wend = align256(wend.size()), b_cap = align256((size_t)M);
-    const size_t total = b_pref + b_head + b_tau + b_win + b_wend + 2 * b_cap;
+                 b_winR = align256(winR.size()), b_cap = align256((size_t)M);
+    const size_t total = 2 * b_pref + b_head + b_tau + b_win + b_winR + 2 * b_cap;
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
     if (!ctx) return E2_ENOMEM;
     if (hipGetDevice(&ctx->device) != hipSuccess) {
@@ -238,15 +248,18 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     char *d_head = d_pref + b_pref;
     char *d_tau = d_head + b_head;
     char *d_win = d_tau + b_tau;
-    char *d_wend = d_win + b_win;
-    char *d_cap0 = d_wend + b_wend;
+    char *d_winR = d_win + b_win;
+    char *d_prefR = d_winR + b_winR;
+    char *d_cap0 = d_prefR + b_pref;
     char *d_capH = d_cap0 + b_cap;
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMemcpy(d_pref, pref.data(), pref.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_head, h.data(), h.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_tau, tau.data(), tau.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_win, win.data(), win.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_wend, wend.data(), wend.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_winR, winR.data(), winR.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(d_prefR, prefR.data(), prefR.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_cap0, cap0.data(), (size_t)M, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_capH, capH.data(), (size_t)M, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
@@ -261,7 +274,8 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     ctx->tables.head = reinterpret_cast<const uint64_t *>(d_head);
     ctx->tables.tau = reinterpret_cast<const uint64_t *>(d_tau);
     ctx->tables.win = reinterpret_cast<const uint8_t *>(d_win);
-    ctx->tables.wend = reinterpret_cast<const uint8_t *>(d_wend);
+    ctx->tables.winR = reinterpret_cast<const uint8_t *>(d_winR);
+    ctx->tables.prefR = reinterpret_cast<const uint64_t *>(d_prefR);
     ctx->tables.cap0 = reinterpret_cast<const uint8_t *>(d_cap0);
     ctx->tables.capH = reinterpret_cast<const uint8_t *>(d_capH);
     ctx->tables.M = M;

@@ -15,8 +15,10 @@ struct E2Tables {
     const uint64_t *tau;   // [2][M][M] link time per role, INF for a dead link
     const uint8_t *win;    // [2][M][N] smallest stage start j so that blocks j..i fit
                            //   ([0]: no head bytes, [1]: with head bytes), E2_NO_START if none
-    const uint8_t *wend;   // [M][N] largest stage end i so that blocks j..i fit without the
-                           //   head, E2_NO_START if block j alone does not fit
+    const uint64_t *prefR; // [2][M][N+1] prefix sums over reversed blocks: prefR[x] =
+                           //   pref[N] - pref[N-x] (block N-1 first)
+    const uint8_t *winR;   // [M][N] reversed-block window starts without the head:
+                           //   smallest y so that reversed blocks y..x fit, E2_NO_START if none
     const uint8_t *cap0;   // [M] most blocks one stage can hold without the head
     const uint8_t *capH;   // [M] most blocks one stage can hold with the head
     int M;

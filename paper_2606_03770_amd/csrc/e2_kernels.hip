@@ -111,21 +111,42 @@ __global__ __launch_bounds__(256) void k_extract(E2Tables tb, int P, int k_max,
 }
 
 // ---------------------------------------------------------------------------
-// Shared-memory layout of one DP wave.  Rows hold N+1 entries.
+// One forward DP row.  Stage device c holds blocks j..i after `kmin` devices
+// that hold blocks 0..j-1:
+//   out(i) = min_{j in [max(win(i), kmin), i]} max(prev(j-1), tau, cost(j, i) + head)
+// as packed scores (value << 8 | j).  The backward rows of the decomposition
+// are the same rows over reversed blocks (block N-1 first), so every row of
+// every table goes through this code.
+//
+// Candidates are scanned with a wave-uniform trip count: lane i visits
+// j = i, i-1, ... and, once past its own window, re-reads its window's first
+// split point (a repeated candidate leaves a minimum unchanged).  Split
+// points keep (prefix term, shifted prefix sum) as one 16-byte LDS pair.
 // ---------------------------------------------------------------------------
-struct DpSmem {
-    uint64_t *Pp;    // packed prefix term of the current row, by split point j
-    uint64_t *S2;    // packed prefix sums of the current row's device
-    uint64_t *Ga;    // backward row (ping)
-    uint64_t *Gb;    // backward row (pong)
-    uint64_t *pool;  // band-packed forward rows, pool_cells entries
-    uint8_t *tbp;    // split points, same packing as pool
-    int pool_cells;
+struct PS {
+    uint64_t a;  // max(prev(j-1), tau) << 8 | j, INF when unusable
+    uint64_t s;  // (P[j] << 8) - j
+};
+
+struct Row {
+    const uint64_t *pr;    // prefix sums P[0..N] of the stage device
+    const uint8_t *wr;     // smallest stage start per stage end, E2_NO_START if none
+    uint64_t hadd;         // head time when this device is the master, else 0
+    uint64_t tau;          // link from the previous device
+    int lo, hi;            // cells of this row
+    int kmin;              // devices before this one
+    int cap;               // longest stage that fits the device
+    const uint64_t *prev;  // previous row, band-packed over [plo, phi]; null: first device
+    int plo, phi;
 };
 
 __device__ __forceinline__ const uint64_t *pref_row(const E2Tables &tb, int r, int c)
 {
     return tb.pref + ((size_t)r * tb.M + c) * (tb.N + 1);
+}
+__device__ __forceinline__ const uint64_t *prefR_row(const E2Tables &tb, int r, int c)
+{
+    return tb.prefR + ((size_t)r * tb.M + c) * (tb.N + 1);
 }
 __device__ __forceinline__ const uint8_t *win_row(const E2Tables &tb, int f, int c)
 {
@@ -140,227 +161,191 @@ __device__ __forceinline__ uint64_t pack_prev(uint64_t prev, uint64_t tau, int j
     return (prev == E2_INF64 || tau == E2_INF64) ? E2_INF64
                                                   : ((umax64(prev, tau) << 8) | (uint64_t)j);
 }
-
-// Minimum packed score of cell i: min over j in [jlo, i] of max(Pp[j], cost(j, i)).
-__device__ __forceinline__ uint64_t cell_min(const uint64_t *Pp, const uint64_t *S2, uint64_t si1,
-                                             int jlo, int i)
+__device__ __forceinline__ int wave_max_i32(int v)
 {
+    for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, kWave));
+    return v;
+}
+__device__ __forceinline__ int wave_min_i32(int v)
+{
+    for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off, kWave));
+    return v;
+}
+__device__ __forceinline__ uint64_t cand(const PS &e, uint64_t si1)
+{
+    return umax64(e.a, si1 - e.s);
+}
+
+// Fill the split-point pairs j in [jmin, hi] of a row.
+__device__ __forceinline__ void row_build(const Row &rw, PS *ps, int jmin, int lane)
+{
+    for (int j = jmin + lane; j <= rw.hi; j += kWave) {
+        const int pj = j - 1;
+        const uint64_t pv = (pj >= rw.plo && pj <= rw.phi) ? rw.prev[pj - rw.plo] : E2_INF64;
+        ps[j].a = pack_prev(pv, rw.tau, j);
+        ps[j].s = (rw.pr[j] << 8) - (uint64_t)j;
+    }
+}
+
+// Packed minimum of the lane's cell i over j in [jlo, i]; len = i - jlo + 1
+// (0 for a lane without a cell).  All lanes of the wave call it together.
+__device__ __forceinline__ uint64_t row_scan(const PS *ps, int i, int jlo, int len, int jmin,
+                                             uint64_t si1)
+{
+    const int L = wave_max_i32(len);
+    int Lmin = wave_min_i32(len > 0 ? len : 0x7FFF);
+    if (Lmin > L) Lmin = L;
+    if (len == 0) {  // idle lane: any in-range split point
+        i = jmin + (Lmin > 0 ? Lmin - 1 : 0);
+        jlo = jmin;
+    }
     uint64_t best = E2_INF64;
-    for (int j = jlo; j <= i; ++j) best = umin64(best, umax64(Pp[j], si1 - S2[j]));
+    int w = 0;
+    for (; w + 4 <= Lmin; w += 4) {
+        const PS *q = ps + (i - w - 3);
+        best = umin64(best, cand(q[3], si1));
+        best = umin64(best, cand(q[2], si1));
+        best = umin64(best, cand(q[1], si1));
+        best = umin64(best, cand(q[0], si1));
+    }
+    for (; w < L; ++w) {
+        int j = i - w;
+        if (j < jlo) j = jlo;
+        best = umin64(best, cand(ps[j], si1));
+    }
     return best;
 }
 
-// ---------------------------------------------------------------------------
-// Exact reference path: one full table per master position (Algorithm 1 as
-// stated), used when a chain's band-packed rows do not fit the LDS pool.
-// D, Pp, S2 are LDS rows; tbp (LDS or global) receives split points of rows
-// 2..m.  Returns DP_mu(N-1, m).
-// ---------------------------------------------------------------------------
-__device__ uint64_t dp_table(const E2Tables &tb, int r, const uint8_t *chain, int m, int mu,
-                             uint8_t *tbp, uint64_t *D, uint64_t *Pp, uint64_t *S2, int lane)
+// Store mode: values (and split points if out_tb) of cells lo..hi, packed
+// as out[i - lo].  Combine mode (G != null): returns the wave minimum over
+// cells of max(value(i), B(i)), B(i) = max(tau_next, G(N-2-i)) from the
+// band-packed reversed row G over [glo, ghi] (bnext_last: B = 0 at i = N-1).
+__device__ uint64_t row_pass(const Row &rw, PS *ps, int lane, int N, uint64_t *out,
+                             uint8_t *out_tb, const uint64_t *G, int glo, int ghi,
+                             uint64_t tau_next, bool combine, bool b_last_only)
 {
-    const int N = tb.N;
-    {
-        const int c = chain[0];
-        const int f = (mu == 1);
-        const uint64_t *pr = pref_row(tb, r, c);
-        const uint8_t *wr = win_row(tb, f, c);
-        const uint64_t hadd = f ? tb.head[r * tb.M + c] : 0;
-        for (int i = lane; i < N; i += kWave) D[i] = (wr[i] == 0) ? pr[i + 1] + hadd : E2_INF64;
+    uint64_t lane_best = E2_INF64;
+    if (rw.prev == nullptr) {  // first device: Eq. 2, no split point
+        for (int i = rw.lo + lane; i <= rw.hi; i += kWave) {
+            const uint64_t v = (rw.wr[i] == 0) ? rw.pr[i + 1] + rw.hadd : E2_INF64;
+            if (!combine) {
+                out[i - rw.lo] = v;
+                continue;
+            }
+            uint64_t b;
+            if (b_last_only) b = (i == N - 1) ? 0 : E2_INF64;
+            else {
+                const int x = N - 2 - i;
+                const uint64_t g = (x >= glo && x <= ghi) ? G[x - glo] : E2_INF64;
+                b = (g == E2_INF64 || tau_next == E2_INF64) ? E2_INF64 : umax64(g, tau_next);
+            }
+            if (v != E2_INF64 && b != E2_INF64) lane_best = umin64(lane_best, umax64(v, b));
+        }
+        __syncthreads();
+        return combine ? wave_min_u64(lane_best) : 0;
+    }
+    int jmin = rw.lo - rw.cap + 1;
+    if (jmin < rw.kmin) jmin = rw.kmin;
+    row_build(rw, ps, jmin, lane);
+    __syncthreads();
+    for (int base = rw.lo; base <= rw.hi; base += kWave) {
+        const int i = base + lane;
+        int len = 0, jlo = jmin;
+        uint64_t si1 = 0;
+        if (i <= rw.hi) {
+            const int w = rw.wr[i];
+            if (w != (int)E2_NO_START) {
+                jlo = w > jmin ? w : jmin;
+                len = i - jlo + 1;
+                si1 = (rw.pr[i + 1] + rw.hadd) << 8;
+            }
+        }
+        const uint64_t best = row_scan(ps, i, jlo, len, jmin, si1);
+        if (i > rw.hi) continue;
+        const uint64_t v = (len == 0 || best == E2_INF64) ? E2_INF64 : (best >> 8);
+        if (!combine) {
+            out[i - rw.lo] = v;
+            if (out_tb) out_tb[i - rw.lo] = (uint8_t)(best & 0xFF);
+            continue;
+        }
+        uint64_t b;
+        if (b_last_only) b = (i == N - 1) ? 0 : E2_INF64;
+        else {
+            const int x = N - 2 - i;
+            const uint64_t g = (x >= glo && x <= ghi) ? G[x - glo] : E2_INF64;
+            b = (g == E2_INF64 || tau_next == E2_INF64) ? E2_INF64 : umax64(g, tau_next);
+        }
+        if (v != E2_INF64 && b != E2_INF64) lane_best = umin64(lane_best, umax64(v, b));
     }
     __syncthreads();
-    for (int k = 2; k <= m; ++k) {
-        const int c = chain[k - 1];
-        const int f = (mu == k);
-        const uint64_t tau = link_tau(tb, r, chain[k - 2], c);
-        const uint64_t *pr = pref_row(tb, r, c);
-        const uint8_t *wr = win_row(tb, f, c);
-        const uint64_t hadd = f ? tb.head[r * tb.M + c] : 0;
-        for (int j = lane; j < N; j += kWave) {
-            Pp[j] = pack_prev(j == 0 ? E2_INF64 : D[j - 1], tau, j);
-            S2[j] = (pr[j] << 8) - (uint64_t)j;
-        }
-        __syncthreads();
-        for (int i = lane; i < N; i += kWave) {
-            uint64_t best = E2_INF64;
-            int lo = wr[i];
-            if (lo != (int)E2_NO_START && i >= k - 1)
-                best = cell_min(Pp, S2, (pr[i + 1] + hadd) << 8, lo < k - 1 ? k - 1 : lo, i);
-            D[i] = (best == E2_INF64) ? E2_INF64 : (best >> 8);
-            if (tbp) tbp[(size_t)(k - 2) * N + i] = (uint8_t)(best & 0xFF);
-        }
-        __syncthreads();
-    }
-    return D[N - 1];
+    return combine ? wave_min_u64(lane_best) : 0;
 }
 
 // ---------------------------------------------------------------------------
-// Band-pruned forward/backward path.
+// Band-pruned decomposition of the master enumeration.
 //
 // With cap0[k] the longest stage device k holds without the head and
-// pre[k] = cap0[1] + ... + cap0[k], a cell (i, k) of any table can lie on a
-// complete memory-feasible partition only if
-//     max(k-1, N-1-(pre[m]-pre[k])) <= i <= min(N-1-(m-k), pre[k]-1)
-// (its devices cover blocks 0..i, the remaining devices cover the rest).
+// pre[k] = cap0[1] + ... + cap0[k], a cell (i, k) can lie on a complete
+// memory-feasible partition only if
+//     max(k-1, N-1-(pre[m]-pre[k])) <= i <= min(N-1-(m-k), pre[k]-1).
 // Every memory-feasible candidate of an in-band cell reads an in-band cell
 // of the previous row or an infinite one, so computing only in-band cells
 // (others INF) leaves every in-band value and split point exact.
 //
 //   F_k  forward rows without master, k = 1..m-1 (pool, with split points)
-//   G_k  backward rows without master: blocks j..N-1 on devices k..m,
-//        k = m..2, each device >= 1 block, links k..m included
-//   T_mu = min_i max( min_j max(A(j), cost_mu(j, i) + head), B(i) )
-//        A(j) = max(F_{mu-1}(j-1), tau(mu-1, mu))   (mu = 1: j = 0 only)
-//        B(i) = max(tau(mu, mu+1), G_{mu+1}(i+1))   (mu = m: i = N-1 only)
+//   G_k  backward rows without master: blocks j..N-1 on devices k..m with
+//        links k..m, computed as forward rows over reversed blocks
+//   T_mu = min_i max( min_j max(F_{mu-1}(j-1), tau(mu-1, mu), cost_mu(j, i)
+//                    + head_mu), tau(mu, mu+1), G_{mu+1}(i+1) )
+//        (mu = 1: the stage starts at block 0; mu = m: it ends at N-1)
 //   which is the optimum of the table of Algorithm 1 for master mu.  The
 //   smallest mu attaining min T_mu is the master; rows mu*..m of its table
 //   (rows below mu* are F) give the split points for the back tracing.
-// Returns false (nothing written) if the bands do not fit the pool.
+// Returns false (nothing decided) if the forward bands do not fit the pool.
 // ---------------------------------------------------------------------------
 struct Bands {
     uint8_t flo[256], fhi[256];  // forward band per row 1..m
-    uint8_t glo[256], ghi[256];  // backward band per row 2..m
+    uint8_t glo[256], ghi[256];  // reversed band per reversed row t = 1..m-1
     uint16_t off[257];           // pool offset per forward row 1..m-1
     uint16_t pre[257];           // prefix sums of cap0 over the chain
     uint8_t cH[256];             // capH per chain position (1-based)
+    uint8_t last_tb;
 };
 
-// Forward row k of the table for master mu (mu = 0: no master), cells in
-// [lo, hi], from the previous row (pool row k-1 with band plo..phi) into
-// pool row k (values + split points).  Row 1 uses Eq. 2 directly.
-__device__ void fwd_row(const E2Tables &tb, const DpSmem &sm, const Bands &bd, int r,
-                        const uint8_t *chain, int k, int mu, int lane, uint64_t *out,
-                        uint8_t *out_tb)
+struct DpSmem {
+    PS *ps;          // split-point pairs, N entries
+    uint64_t *Ga;    // reversed row (ping), band-packed
+    uint64_t *Gb;    // reversed row (pong)
+    uint64_t *pool;  // band-packed forward rows
+    uint8_t *tbp;    // their split points
+    int pool_cells;
+};
+
+__device__ Row fwd_rowdesc(const E2Tables &tb, const Bands &bd, const DpSmem &sm, int r,
+                           const uint8_t *chain, int k, int mu)
 {
     const int c = chain[k - 1];
     const int f = (mu == k);
-    const int lo = bd.flo[k], hi = bd.fhi[k];
-    const uint64_t *pr = pref_row(tb, r, c);
-    const uint8_t *wr = win_row(tb, f, c);
-    const uint64_t hadd = f ? tb.head[r * tb.M + c] : 0;
+    Row rw;
+    rw.pr = pref_row(tb, r, c);
+    rw.wr = win_row(tb, f, c);
+    rw.hadd = f ? tb.head[r * tb.M + c] : 0;
+    rw.lo = bd.flo[k];
+    rw.hi = bd.fhi[k];
+    rw.kmin = k - 1;
+    rw.cap = f ? bd.cH[k] : (int)(bd.pre[k] - bd.pre[k - 1]);
     if (k == 1) {
-        for (int i = lo + lane; i <= hi; i += kWave)
-            out[i - lo] = (wr[i] == 0) ? pr[i + 1] + hadd : E2_INF64;
-        __syncthreads();
-        return;
+        rw.tau = 0;
+        rw.prev = nullptr;
+        rw.plo = 1;
+        rw.phi = 0;
+    } else {
+        rw.tau = link_tau(tb, r, chain[k - 2], c);
+        rw.prev = sm.pool + bd.off[k - 1];
+        rw.plo = bd.flo[k - 1];
+        rw.phi = bd.fhi[k - 1];
     }
-    const int cap = f ? bd.cH[k] : (int)(bd.pre[k] - bd.pre[k - 1]);
-    int jmin = lo - cap + 1;
-    if (jmin < k - 1) jmin = k - 1;
-    const uint64_t tau = link_tau(tb, r, chain[k - 2], c);
-    const int plo = bd.flo[k - 1], phi = bd.fhi[k - 1];
-    const uint64_t *prev = sm.pool + bd.off[k - 1];
-    for (int j = jmin + lane; j <= hi; j += kWave) {
-        const int pj = j - 1;
-        sm.Pp[j] = pack_prev((pj >= plo && pj <= phi) ? prev[pj - plo] : E2_INF64, tau, j);
-        sm.S2[j] = (pr[j] << 8) - (uint64_t)j;
-    }
-    __syncthreads();
-    for (int i = lo + lane; i <= hi; i += kWave) {
-        uint64_t best = E2_INF64;
-        const int w = wr[i];
-        if (w != (int)E2_NO_START)
-            best = cell_min(sm.Pp, sm.S2, (pr[i + 1] + hadd) << 8, w < jmin ? jmin : w, i);
-        out[i - lo] = (best == E2_INF64) ? E2_INF64 : (best >> 8);
-        out_tb[i - lo] = (uint8_t)(best & 0xFF);
-    }
-    __syncthreads();
-}
-
-// Backward row k (k = m..2) into Gout (full length, INF outside the band).
-__device__ void bwd_row(const E2Tables &tb, const DpSmem &sm, const Bands &bd, int r,
-                        const uint8_t *chain, int k, int m, int lane, const uint64_t *Gin,
-                        uint64_t *Gout)
-{
-    const int N = tb.N;
-    const int c = chain[k - 1];
-    const int lo = bd.glo[k], hi = bd.ghi[k];
-    const uint64_t *pr = pref_row(tb, r, c);
-    if (k == m) {
-        const int w = win_row(tb, 0, c)[N - 1];
-        for (int j = lane; j < N; j += kWave)
-            Gout[j] = (j >= lo && j <= hi && w != (int)E2_NO_START && j >= w)
-                          ? pr[N] - pr[j] : E2_INF64;
-        __syncthreads();
-        return;
-    }
-    const uint8_t *we = tb.wend + (size_t)c * N;
-    const int imax = N - 1 - (m - k);
-    const int cap = bd.pre[k] - bd.pre[k - 1];
-    int ihi = hi + cap - 1;
-    if (ihi > imax) ihi = imax;
-    const uint64_t tau = link_tau(tb, r, c, chain[k]);
-    // Pp <- Q(i) = max(G_{k+1}(i+1), tau(k, k+1)); S2 <- plain prefix sums
-    for (int i = lo + lane; i <= ihi; i += kWave) {
-        const uint64_t g = Gin[i + 1];
-        sm.Pp[i] = (g == E2_INF64 || tau == E2_INF64) ? E2_INF64 : umax64(g, tau);
-    }
-    for (int i = lo + lane; i <= ihi + 1; i += kWave) sm.S2[i] = pr[i];
-    __syncthreads();
-    for (int j = lane; j < N; j += kWave) {
-        uint64_t best = E2_INF64;
-        if (j >= lo && j <= hi) {
-            const int e = we[j];
-            if (e != (int)E2_NO_START) {
-                const int iend = e < imax ? e : imax;
-                const uint64_t pj = sm.S2[j];
-                for (int i = j; i <= iend; ++i)
-                    best = umin64(best, umax64(sm.Pp[i], sm.S2[i + 1] - pj));
-            }
-        }
-        Gout[j] = best;
-    }
-    __syncthreads();
-}
-
-// T_mu from F_{mu-1} (pool), the head on device mu, and G_{mu+1} (Gnext).
-__device__ uint64_t combine(const E2Tables &tb, const DpSmem &sm, const Bands &bd, int r,
-                            const uint8_t *chain, int mu, int m, int lane, const uint64_t *Gnext)
-{
-    const int N = tb.N;
-    const int c = chain[mu - 1];
-    const int lo = bd.flo[mu], hi = bd.fhi[mu];
-    const int cap = bd.cH[mu];
-    uint64_t lane_best = E2_INF64;
-    if (cap > 0 && lo <= hi) {
-        const uint64_t *pr = pref_row(tb, r, c);
-        const uint8_t *wr = win_row(tb, 1, c);
-        const uint64_t hadd = tb.head[r * tb.M + c];
-        int jmin = lo - cap + 1;
-        if (jmin < mu - 1) jmin = mu - 1;
-        if (mu == 1) {
-            for (int j = jmin + lane; j <= hi; j += kWave) {
-                sm.Pp[j] = (j == 0) ? 0ull : E2_INF64;
-                sm.S2[j] = (pr[j] << 8) - (uint64_t)j;
-            }
-        } else {
-            const uint64_t tau = link_tau(tb, r, chain[mu - 2], c);
-            const int plo = bd.flo[mu - 1], phi = bd.fhi[mu - 1];
-            const uint64_t *prev = sm.pool + bd.off[mu - 1];
-            for (int j = jmin + lane; j <= hi; j += kWave) {
-                const int pj = j - 1;
-                sm.Pp[j] = pack_prev((pj >= plo && pj <= phi) ? prev[pj - plo] : E2_INF64, tau, j);
-                sm.S2[j] = (pr[j] << 8) - (uint64_t)j;
-            }
-        }
-        __syncthreads();
-        const uint64_t tnext = (mu < m) ? link_tau(tb, r, c, chain[mu]) : 0;
-        for (int i = lo + lane; i <= hi; i += kWave) {
-            uint64_t b;
-            if (mu == m) b = (i == N - 1) ? 0 : E2_INF64;
-            else {
-                const uint64_t g = (i + 1 < N) ? Gnext[i + 1] : E2_INF64;
-                b = (g == E2_INF64 || tnext == E2_INF64) ? E2_INF64 : umax64(g, tnext);
-            }
-            const int w = wr[i];
-            if (b == E2_INF64 || w == (int)E2_NO_START) continue;
-            const uint64_t best =
-                cell_min(sm.Pp, sm.S2, (pr[i + 1] + hadd) << 8, w < jmin ? jmin : w, i);
-            if (best != E2_INF64) lane_best = umin64(lane_best, umax64(best >> 8, b));
-        }
-    }
-    __syncthreads();
-    return wave_min_u64(lane_best);
+    return rw;
 }
 
 __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r,
@@ -368,7 +353,6 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
                           uint8_t *start)
 {
     const int N = tb.N;
-    // capacities and bands (one lane; m steps)
     if (lane == 0) {
         bd.pre[0] = 0;
         for (int k = 1; k <= m; ++k) {
@@ -387,69 +371,99 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
             bd.fhi[k] = (uint8_t)hi;
             bd.off[k] = (uint16_t)off;
             if (k < m) off += hi - lo + 1;
-            if (k >= 2) {
-                int gl = N - (tot - bd.pre[k - 1]);
-                if (gl < k - 1) gl = k - 1;
-                int gh = bd.pre[k - 1];
-                if (gh > N - (m - k + 1)) gh = N - (m - k + 1);
-                if (gh < gl) { gl = 1; gh = 0; }
-                bd.glo[k] = (uint8_t)gl;
-                bd.ghi[k] = (uint8_t)gh;
-            }
         }
         bd.off[m] = (uint16_t)(off > 65535 ? 65535 : off);
+        // reversed row t covers devices m..m+1-t (original k = m+1-t): blocks
+        // j..N-1 with max(k-1, N-(tot-pre[k-1])) <= j <= min(N-(m-k+1), pre[k-1]),
+        // i.e. reversed cells x = N-1-j
+        for (int t = 1; t < m; ++t) {
+            const int k = m + 1 - t;
+            int gl = N - (tot - bd.pre[k - 1]);
+            if (gl < k - 1) gl = k - 1;
+            int gh = bd.pre[k - 1];
+            if (gh > N - (m - k + 1)) gh = N - (m - k + 1);
+            if (gh < gl) { bd.glo[t] = 1; bd.ghi[t] = 0; }
+            else { bd.glo[t] = (uint8_t)(N - 1 - gh); bd.ghi[t] = (uint8_t)(N - 1 - gl); }
+        }
     }
     __syncthreads();
     if ((int)bd.off[m] > sm.pool_cells) return false;
 
     // forward rows F_1..F_{m-1}
-    for (int k = 1; k < m; ++k)
-        fwd_row(tb, sm, bd, r, chain, k, 0, lane, sm.pool + bd.off[k], sm.tbp + bd.off[k]);
-
-    // combines, interleaved with the backward rows
-    uint64_t best = combine(tb, sm, bd, r, chain, m, m, lane, nullptr);
+    for (int k = 1; k < m; ++k) {
+        const Row rw = fwd_rowdesc(tb, bd, sm, r, chain, k, 0);
+        row_pass(rw, sm.ps, lane, N, sm.pool + bd.off[k], sm.tbp + bd.off[k], nullptr, 1, 0, 0,
+                 false, false);
+    }
+    // master mu = m: its stage ends at block N-1
+    uint64_t best;
+    {
+        Row rw = fwd_rowdesc(tb, bd, sm, r, chain, m, m);
+        best = (rw.cap > 0) ? row_pass(rw, sm.ps, lane, N, nullptr, nullptr, nullptr, 1, 0, 0,
+                                       true, true)
+                            : E2_INF64;
+    }
     int best_mu = best == E2_INF64 ? 0 : m;
-    uint64_t *Gcur = sm.Ga, *Gnew = sm.Gb;
-    for (int k = m; k >= 2; --k) {
-        bwd_row(tb, sm, bd, r, chain, k, m, lane, Gcur, Gnew);
-        uint64_t *t = Gcur;
-        Gcur = Gnew;
-        Gnew = t;
-        const uint64_t v = combine(tb, sm, bd, r, chain, k - 1, m, lane, Gcur);
-        if (v <= best && v != E2_INF64) {  // descending mu: ties go to the smaller mu
-            best = v;
-            best_mu = k - 1;
+    // reversed rows t = 1..m-1 (original backward row k = m+1-t), each
+    // followed by the combine of master mu = m - t
+    uint64_t *Gprev = sm.Gb, *Gcur = sm.Ga;
+    for (int t = 1; t < m; ++t) {
+        const int k = m + 1 - t;  // device of this backward row
+        const int c = chain[k - 1];
+        Row g;
+        g.pr = prefR_row(tb, r, c);
+        g.wr = tb.winR + (size_t)c * N;
+        g.hadd = 0;
+        g.lo = bd.glo[t];
+        g.hi = bd.ghi[t];
+        g.kmin = t - 1;
+        g.cap = bd.pre[k] - bd.pre[k - 1];
+        if (t == 1) {
+            g.tau = 0;
+            g.prev = nullptr;
+            g.plo = 1;
+            g.phi = 0;
+        } else {
+            g.tau = link_tau(tb, r, c, chain[k]);
+            g.prev = Gprev;
+            g.plo = bd.glo[t - 1];
+            g.phi = bd.ghi[t - 1];
         }
+        row_pass(g, sm.ps, lane, N, Gcur, nullptr, nullptr, 1, 0, 0, false, false);
+        const int mu = m - t;
+        Row rw = fwd_rowdesc(tb, bd, sm, r, chain, mu, mu);
+        if (rw.cap > 0) {
+            const uint64_t v = row_pass(rw, sm.ps, lane, N, nullptr, nullptr, Gcur, bd.glo[t],
+                                        bd.ghi[t], link_tau(tb, r, chain[mu - 1], chain[mu]),
+                                        true, false);
+            if (v != E2_INF64 && v <= best) {  // descending mu: ties go to the smaller mu
+                best = v;
+                best_mu = mu;
+            }
+        }
+        uint64_t *tmp = Gprev;
+        Gprev = Gcur;
+        Gcur = tmp;
     }
     *T_out = best;
     *mu_out = best_mu;
     if (best == E2_INF64) return true;
 
     // rows mu*..m-1 of the chosen master's table overwrite F in the pool
-    for (int k = best_mu; k < m; ++k)
-        fwd_row(tb, sm, bd, r, chain, k, best_mu, lane, sm.pool + bd.off[k], sm.tbp + bd.off[k]);
-    // split point of the last stage: cell N-1 of row m
+    for (int k = best_mu; k < m; ++k) {
+        const Row rw = fwd_rowdesc(tb, bd, sm, r, chain, k, best_mu);
+        row_pass(rw, sm.ps, lane, N, sm.pool + bd.off[k], sm.tbp + bd.off[k], nullptr, 1, 0, 0,
+                 false, false);
+    }
     if (m >= 2) {
-        const int c = chain[m - 1];
-        const int f = (best_mu == m);
-        const uint64_t *pr = pref_row(tb, r, c);
-        const int w = win_row(tb, f, c)[N - 1];
-        const uint64_t tau = link_tau(tb, r, chain[m - 2], c);
-        const int plo = bd.flo[m - 1], phi = bd.fhi[m - 1];
-        const uint64_t *prev = sm.pool + bd.off[m - 1];
-        const uint64_t si1 = (pr[N] + (f ? tb.head[r * tb.M + c] : 0)) << 8;
-        // lanes over j, then the smallest j with the minimum packed score
-        uint64_t lb = E2_INF64;
-        for (int j = (w > m - 1 ? w : m - 1) + lane; j <= N - 1; j += kWave) {
-            const int pj = j - 1;
-            const uint64_t pp = pack_prev((pj >= plo && pj <= phi) ? prev[pj - plo] : E2_INF64,
-                                          tau, j);
-            lb = umin64(lb, umax64(pp, si1 - ((pr[j] << 8) - (uint64_t)j)));
-        }
-        const uint64_t key = wave_min_u64(lb);
+        // cell N-1 of row m: split point of the last stage
+        Row rw = fwd_rowdesc(tb, bd, sm, r, chain, m, best_mu);
+        rw.lo = rw.hi = N - 1;
+        uint64_t dummy;
+        row_pass(rw, sm.ps, lane, N, &dummy, &bd.last_tb, nullptr, 1, 0, 0, false, false);
         if (lane == 0) {
             int i = N - 1;
-            int j = (int)(key & 0xFF);
+            int j = bd.last_tb;
             if (j > i) j = i;
             start[m - 1] = (uint8_t)j;
             i = j - 1;
@@ -468,11 +482,56 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
     __syncthreads();
     return true;
 }
+
+// Reference path (chains whose bands exceed the pool): Algorithm 1's table
+// for one master position, full rows k-1..N-1, ping-ponging Ga/Gb; split
+// points of rows 2..m go to tbp (row k at (k-2)*N) when tbp is not null.
+__device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
+                             int m, int mu, uint8_t *tbp, int lane)
+{
+    const int N = tb.N;
+    uint64_t *cur = sm.Ga, *prv = sm.Gb;
+    uint64_t last = E2_INF64;
+    for (int k = 1; k <= m; ++k) {
+        const int c = chain[k - 1];
+        const int f = (mu == k);
+        Row rw;
+        rw.pr = pref_row(tb, r, c);
+        rw.wr = win_row(tb, f, c);
+        rw.hadd = f ? tb.head[r * tb.M + c] : 0;
+        rw.lo = k - 1;
+        rw.hi = N - 1;
+        rw.kmin = k - 1;
+        rw.cap = N;
+        if (k == 1) {
+            rw.tau = 0;
+            rw.prev = nullptr;
+            rw.plo = 1;
+            rw.phi = 0;
+        } else {
+            rw.tau = link_tau(tb, r, chain[k - 2], c);
+            rw.prev = prv;
+            rw.plo = k - 2;
+            rw.phi = N - 1;
+        }
+        row_pass(rw, sm.ps, lane, N, cur, (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1)
+                                                           : nullptr,
+                 nullptr, 1, 0, 0, false, false);
+        uint64_t *tmp = prv;
+        prv = cur;
+        cur = tmp;
+    }
+    last = prv[(N - 1) - (m - 1)];
+    __syncthreads();
+    return last;
+}
+
 // ---------------------------------------------------------------------------
 // Persistent DP kernel: one wave per workgroup; waves take listed problems
 // in list order through an atomic counter and exit when the list is
-// exhausted.  Dynamic LDS: four rows of N+1 u64, then the forward-row pool
-// (pool_cells u64) and its split-point bytes.
+// exhausted.  Dynamic LDS: split-point pairs (N x 16 B), two reversed rows
+// (2 x (N+1) x 8 B), then the forward-row pool (pool_cells x 8 B) and its
+// split-point bytes.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cells,
                                            const uint8_t *__restrict__ labels,
@@ -488,13 +547,11 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
     __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
-    const int R = N + 1;
     DpSmem sm;
-    sm.Pp = dyn;
-    sm.S2 = dyn + R;
-    sm.Ga = dyn + 2 * R;
-    sm.Gb = dyn + 3 * R;
-    sm.pool = dyn + 4 * R;
+    sm.ps = reinterpret_cast<PS *>(dyn);
+    sm.Ga = dyn + 2 * N;
+    sm.Gb = sm.Ga + (N + 1);
+    sm.pool = sm.Gb + (N + 1);
     sm.tbp = reinterpret_cast<uint8_t *>(sm.pool + pool_cells);
     sm.pool_cells = pool_cells;
     const uint32_t n_jobs = counters[0];
@@ -525,10 +582,10 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
         uint64_t best = E2_INF64;
         int best_mu = 0;
         if (!dp_banded(tb, sm, bd, r, chain, m, lane, &best, &best_mu, start)) {
-            // exact reference path: a full table per master, then the chosen
+            // reference path: a full table per master, then the chosen
             // master's table again with split points
             for (int mu = 1; mu <= m; ++mu) {
-                const uint64_t v = dp_table(tb, r, chain, m, mu, nullptr, sm.Ga, sm.Pp, sm.S2, lane);
+                const uint64_t v = dp_table(tb, sm, r, chain, m, mu, nullptr, lane);
                 if (v < best) {
                     best = v;
                     best_mu = mu;
@@ -538,7 +595,7 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
                 uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)pool_cells * 8)
                                    ? reinterpret_cast<uint8_t *>(sm.pool)
                                    : tb_global + (size_t)blockIdx.x * N * N;
-                dp_table(tb, r, chain, m, best_mu, tbp, sm.Ga, sm.Pp, sm.S2, lane);
+                dp_table(tb, sm, r, chain, m, best_mu, tbp, lane);
                 __threadfence_block();
                 __syncthreads();
                 if (lane == 0) {
@@ -744,7 +801,7 @@ int e2_dp_pool_cells(int N)
 
 size_t e2_dp_lds_bytes(int N)
 {
-    return (size_t)4 * (N + 1) * 8 + (size_t)e2_dp_pool_cells(N) * 9;
+    return (size_t)2 * N * 8 + (size_t)2 * (N + 1) * 8 + (size_t)e2_dp_pool_cells(N) * 9;
 }
 
 int e2_dp_slots(int problems)
