@@ -33,16 +33,62 @@ constexpr int kWave = 64;
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 __device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
+// Wave-wide reductions: DPP permutations within each 16-lane row (quad
+// swaps, half mirror, mirror), then the four row results read into scalars.
+// The results are wave-uniform.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v)
 {
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
-    return v;
+    return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v)
+{
+    const int lo = dpp_i32<CTRL>((int)(uint32_t)v);
+    const int hi = dpp_i32<CTRL>((int)(uint32_t)(v >> 32));
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
 }
 
+__device__ __forceinline__ int wave_max_i32(int v)
+{
+    v = max(v, dpp_i32<0xb1>(v));
+    v = max(v, dpp_i32<0x4e>(v));
+    v = max(v, dpp_i32<0x141>(v));
+    v = max(v, dpp_i32<0x140>(v));
+    return max(max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
+               max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
+}
+__device__ __forceinline__ int wave_min_i32(int v)
+{
+    v = min(v, dpp_i32<0xb1>(v));
+    v = min(v, dpp_i32<0x4e>(v));
+    v = min(v, dpp_i32<0x141>(v));
+    v = min(v, dpp_i32<0x140>(v));
+    return min(min(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
+               min(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
+}
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
 {
-    for (int off = 32; off >= 1; off >>= 1) v = umin64(v, __shfl_xor(v, off, kWave));
-    return v;
+    v = umin64(v, dpp_u64<0xb1>(v));
+    v = umin64(v, dpp_u64<0x4e>(v));
+    v = umin64(v, dpp_u64<0x141>(v));
+    v = umin64(v, dpp_u64<0x140>(v));
+    return umin64(umin64(readlane_u64(v, 0), readlane_u64(v, 16)),
+                  umin64(readlane_u64(v, 32), readlane_u64(v, 48)));
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
+{
+    v += dpp_u64<0xb1>(v);
+    v += dpp_u64<0x4e>(v);
+    v += dpp_u64<0x141>(v);
+    v += dpp_u64<0x140>(v);
+    return readlane_u64(v, 0) + readlane_u64(v, 16) + readlane_u64(v, 32) + readlane_u64(v, 48);
 }
 
 __global__ void k_init(uint32_t *counters)
@@ -161,16 +207,6 @@ __device__ __forceinline__ uint64_t pack_prev(uint64_t prev, uint64_t tau, int j
     return (prev == E2_INF64 || tau == E2_INF64) ? E2_INF64
                                                   : ((umax64(prev, tau) << 8) | (uint64_t)j);
 }
-__device__ __forceinline__ int wave_max_i32(int v)
-{
-    for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, kWave));
-    return v;
-}
-__device__ __forceinline__ int wave_min_i32(int v)
-{
-    for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off, kWave));
-    return v;
-}
 __device__ __forceinline__ uint64_t cand(const PS &e, uint64_t si1)
 {
     return umax64(e.a, si1 - e.s);
@@ -246,19 +282,29 @@ __device__ uint64_t row_pass(const Row &rw, PS *ps, int lane, int N, uint64_t *o
     }
     int jmin = rw.lo - rw.cap + 1;
     if (jmin < rw.kmin) jmin = rw.kmin;
+    // the first cell pass's global loads go out before the split points are built
+    int w_next = E2_NO_START;
+    uint64_t p_next = 0;
+    if (rw.lo + lane <= rw.hi) {
+        w_next = rw.wr[rw.lo + lane];
+        p_next = rw.pr[rw.lo + lane + 1];
+    }
     row_build(rw, ps, jmin, lane);
     __syncthreads();
     for (int base = rw.lo; base <= rw.hi; base += kWave) {
         const int i = base + lane;
+        const int w = w_next;
+        const uint64_t p1 = p_next;
+        if (i + kWave <= rw.hi) {
+            w_next = rw.wr[i + kWave];
+            p_next = rw.pr[i + kWave + 1];
+        }
         int len = 0, jlo = jmin;
         uint64_t si1 = 0;
-        if (i <= rw.hi) {
-            const int w = rw.wr[i];
-            if (w != (int)E2_NO_START) {
-                jlo = w > jmin ? w : jmin;
-                len = i - jlo + 1;
-                si1 = (rw.pr[i + 1] + rw.hadd) << 8;
-            }
+        if (i <= rw.hi && w != (int)E2_NO_START) {
+            jlo = w > jmin ? w : jmin;
+            len = i - jlo + 1;
+            si1 = (p1 + rw.hadd) << 8;
         }
         const uint64_t best = row_scan(ps, i, jlo, len, jmin, si1);
         if (i > rw.hi) continue;
