@@ -52,7 +52,7 @@ def log(msg):
 # ---------------------------------------------------------------------------
 # Work accounting (host side, from the same integer inputs).
 # ---------------------------------------------------------------------------
-POOL_CELLS = 1024  # forward-row pool of one DP wave (k_dp)
+POOL_CELLS = 2048  # forward-row pool of one DP wave (k_dp)
 
 
 def window_tables(wl):

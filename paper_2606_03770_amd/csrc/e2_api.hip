@@ -120,9 +120,10 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
     const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
     // the fallback is needed only when some chain's split points exceed the
     // LDS pool of the reference path
-    const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_pool_cells(ctx->N) * 8;
+    const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_pool_cells(ctx->N);
     *tb_bytes = need_tb ? (size_t)(*slots) * ctx->N * ctx->N : 0;
-    return align256(16) + align256(problems * 4) + align256(*tb_bytes);
+    return align256(16) + align256(problems * 4) +
+           align256((size_t)(*slots) * e2_dp_row_words(ctx->N) * 8) + align256(*tb_bytes);
 }
 
 void carve_work(void *base, const e2_ctx *ctx, int P, int k_max, int slots, size_t tb_bytes,
@@ -133,6 +134,8 @@ void carve_work(void *base, const e2_ctx *ctx, int P, int k_max, int slots, size
     p += align256(16);
     wk->list = reinterpret_cast<uint32_t *>(p);
     p += align256((size_t)P * k_max * 4);
+    wk->rows = reinterpret_cast<uint64_t *>(p);
+    p += align256((size_t)slots * e2_dp_row_words(ctx->N) * 8);
     wk->tb_global = tb_bytes ? reinterpret_cast<uint8_t *>(p) : nullptr;
     wk->n_slots = slots;
     (void)ctx;
@@ -228,10 +231,28 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
         }
     }
 
+    // lower bounds of window lengths over cells i >= x (0 = no fitting cell)
+    std::vector<uint8_t> minwin((size_t)2 * M * N), minwinR((size_t)M * N);
+    auto suffix_min = [N](const uint8_t *w, uint8_t *out) {
+        int best = 0;  // 0 encodes "none yet"
+        for (int x = N - 1; x >= 0; --x) {
+            if (w[x] != E2_NO_START) {
+                const int len = x - w[x] + 1;
+                best = (best == 0 || len < best) ? len : best;
+            }
+            out[x] = (uint8_t)best;
+        }
+    };
+    for (int f = 0; f < 2; ++f)
+        for (int d = 0; d < M; ++d)
+            suffix_min(&win[((size_t)f * M + d) * N], &minwin[((size_t)f * M + d) * N]);
+    for (int d = 0; d < M; ++d) suffix_min(&winR[(size_t)d * N], &minwinR[(size_t)d * N]);
+
     const size_t b_pref = align256(pref.size() * 8), b_head = align256(h.size() * 8),
                  b_tau = align256(tau.size() * 8), b_win = align256(win.size()),
                  b_winR = align256(winR.size()), b_cap = align256((size_t)M);
-    const size_t total = 2 * b_pref + b_head + b_tau + b_win + b_winR + 2 * b_cap;
+    const size_t b_mw = align256(minwin.size()), b_mwR = align256(minwinR.size());
+    const size_t total = 2 * b_pref + b_head + b_tau + b_win + b_winR + b_mw + b_mwR + 2 * b_cap;
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
     if (!ctx) return E2_ENOMEM;
     if (hipGetDevice(&ctx->device) != hipSuccess) {
@@ -250,7 +271,9 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     char *d_win = d_tau + b_tau;
     char *d_winR = d_win + b_win;
     char *d_prefR = d_winR + b_winR;
-    char *d_cap0 = d_prefR + b_pref;
+    char *d_mw = d_prefR + b_pref;
+    char *d_mwR = d_mw + b_mw;
+    char *d_cap0 = d_mwR + b_mwR;
     char *d_capH = d_cap0 + b_cap;
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMemcpy(d_pref, pref.data(), pref.size() * 8, hipMemcpyHostToDevice);
@@ -258,6 +281,9 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     if (e == hipSuccess) e = hipMemcpy(d_tau, tau.data(), tau.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_win, win.data(), win.size(), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_winR, winR.data(), winR.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_mw, minwin.data(), minwin.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(d_mwR, minwinR.data(), minwinR.size(), hipMemcpyHostToDevice);
     if (e == hipSuccess)
         e = hipMemcpy(d_prefR, prefR.data(), prefR.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_cap0, cap0.data(), (size_t)M, hipMemcpyHostToDevice);
@@ -275,6 +301,8 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     ctx->tables.tau = reinterpret_cast<const uint64_t *>(d_tau);
     ctx->tables.win = reinterpret_cast<const uint8_t *>(d_win);
     ctx->tables.winR = reinterpret_cast<const uint8_t *>(d_winR);
+    ctx->tables.minwin = reinterpret_cast<const uint8_t *>(d_mw);
+    ctx->tables.minwinR = reinterpret_cast<const uint8_t *>(d_mwR);
     ctx->tables.prefR = reinterpret_cast<const uint64_t *>(d_prefR);
     ctx->tables.cap0 = reinterpret_cast<const uint8_t *>(d_cap0);
     ctx->tables.capH = reinterpret_cast<const uint8_t *>(d_capH);

@@ -19,6 +19,9 @@ struct E2Tables {
                            //   pref[N] - pref[N-x] (block N-1 first)
     const uint8_t *winR;   // [M][N] reversed-block window starts without the head:
                            //   smallest y so that reversed blocks y..x fit, E2_NO_START if none
+    const uint8_t *minwin; // [2][M][N] lower bound of window lengths i - win(i) + 1 over
+                           //   cells i >= x (0 if unknown); same for reversed blocks in
+    const uint8_t *minwinR;//   [M][N]
     const uint8_t *cap0;   // [M] most blocks one stage can hold without the head
     const uint8_t *capH;   // [M] most blocks one stage can hold with the head
     int M;
@@ -37,14 +40,17 @@ struct e2_ctx {
 struct E2Work {
     uint32_t *counters;  // [0] problems listed, [1] next problem to take
     uint32_t *list;      // [P * k_max] (p << 8) | q of problems needing the DP
+    uint64_t *rows;      // [n_slots][pool + 2 (N+1)] per-wave DP rows
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
     int n_slots;         // waves of the DP kernel
 };
 
 // Number of DP waves launched for `problems` upper-bound problems.
 int e2_dp_slots(int problems);
-// Forward-row pool of one DP wave (u64 cells) and its dynamic LDS bytes.
+// Forward-row pool of one DP wave (u64 cells), its global row storage
+// (u64 per wave) and its dynamic LDS bytes.
 int e2_dp_pool_cells(int N);
+size_t e2_dp_row_words(int N);
 size_t e2_dp_lds_bytes(int N);
 
 // Enqueue cluster extraction + DP.  Outputs may be the caller's (solve) or

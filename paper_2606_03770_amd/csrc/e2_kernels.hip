@@ -55,24 +55,6 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane)
     return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ int wave_max_i32(int v)
-{
-    v = max(v, dpp_i32<0xb1>(v));
-    v = max(v, dpp_i32<0x4e>(v));
-    v = max(v, dpp_i32<0x141>(v));
-    v = max(v, dpp_i32<0x140>(v));
-    return max(max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
-               max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
-}
-__device__ __forceinline__ int wave_min_i32(int v)
-{
-    v = min(v, dpp_i32<0xb1>(v));
-    v = min(v, dpp_i32<0x4e>(v));
-    v = min(v, dpp_i32<0x141>(v));
-    v = min(v, dpp_i32<0x140>(v));
-    return min(min(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
-               min(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
-}
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
 {
     v = umin64(v, dpp_u64<0xb1>(v));
@@ -164,10 +146,15 @@ __global__ __launch_bounds__(256) void k_extract(E2Tables tb, int P, int k_max,
 // are the same rows over reversed blocks (block N-1 first), so every row of
 // every table goes through this code.
 //
-// Candidates are scanned with a wave-uniform trip count: lane i visits
-// j = i, i-1, ... and, once past its own window, re-reads its window's first
-// split point (a repeated candidate leaves a minimum unchanged).  Split
-// points keep (prefix term, shifted prefix sum) as one 16-byte LDS pair.
+// Lane mapping: S lanes per cell (S = 4 for at most 16 cells, 2 for at most
+// 32, else 1); lane o of a cell visits j = i - o - S t for t = 0, 1, ...
+// With L = min(cap, hi - jmin + 1) an upper bound and Lm a lower bound of
+// the cells' window lengths, the first floor(Lm / S) steps stay inside
+// every window and run unclamped (four at a time); the remaining steps
+// clamp j to the lane's window start (a repeated candidate leaves a minimum
+// unchanged).  The S partial minima meet through DPP quad permutations.
+// Split points keep (prefix term, shifted prefix sum) as one 16-byte LDS
+// pair.
 // ---------------------------------------------------------------------------
 struct PS {
     uint64_t a;  // max(prev(j-1), tau) << 8 | j, INF when unusable
@@ -182,6 +169,7 @@ struct Row {
     int lo, hi;            // cells of this row
     int kmin;              // devices before this one
     int cap;               // longest stage that fits the device
+    int lmin;              // lower bound of window lengths over cells >= lo (0: none)
     const uint64_t *prev;  // previous row, band-packed over [plo, phi]; null: first device
     int plo, phi;
 };
@@ -212,119 +200,143 @@ __device__ __forceinline__ uint64_t cand(const PS &e, uint64_t si1)
     return umax64(e.a, si1 - e.s);
 }
 
-// Fill the split-point pairs j in [jmin, hi] of a row.
-__device__ __forceinline__ void row_build(const Row &rw, PS *ps, int jmin, int lane)
+// B(i) of a combine: max(tau_next, G(N-2-i)) from the band-packed reversed
+// row G over [glo, ghi]; with last_only, B = 0 at i = N-1 and INF elsewhere.
+__device__ __forceinline__ uint64_t combine_b(int i, int N, const uint64_t *G, int glo, int ghi,
+                                              uint64_t tau_next, bool last_only)
 {
-    for (int j = jmin + lane; j <= rw.hi; j += kWave) {
-        const int pj = j - 1;
-        const uint64_t pv = (pj >= rw.plo && pj <= rw.phi) ? rw.prev[pj - rw.plo] : E2_INF64;
-        ps[j].a = pack_prev(pv, rw.tau, j);
-        ps[j].s = (rw.pr[j] << 8) - (uint64_t)j;
-    }
+    if (last_only) return (i == N - 1) ? 0 : E2_INF64;
+    const int x = N - 2 - i;
+    const uint64_t g = (x >= glo && x <= ghi) ? G[x - glo] : E2_INF64;
+    return (g == E2_INF64 || tau_next == E2_INF64) ? E2_INF64 : umax64(g, tau_next);
 }
 
-// Packed minimum of the lane's cell i over j in [jlo, i]; len = i - jlo + 1
-// (0 for a lane without a cell).  All lanes of the wave call it together.
-__device__ __forceinline__ uint64_t row_scan(const PS *ps, int i, int jlo, int len, int jmin,
-                                             uint64_t si1)
+template <int S>
+__device__ __forceinline__ uint64_t scan_cell(const PS *ps, int i, int jlo, int o, uint64_t si1,
+                                              int t_safe, int t_all)
 {
-    const int L = wave_max_i32(len);
-    int Lmin = wave_min_i32(len > 0 ? len : 0x7FFF);
-    if (Lmin > L) Lmin = L;
-    if (len == 0) {  // idle lane: any in-range split point
-        i = jmin + (Lmin > 0 ? Lmin - 1 : 0);
-        jlo = jmin;
-    }
     uint64_t best = E2_INF64;
-    int w = 0;
-    for (; w + 4 <= Lmin; w += 4) {
-        const PS *q = ps + (i - w - 3);
-        best = umin64(best, cand(q[3], si1));
-        best = umin64(best, cand(q[2], si1));
-        best = umin64(best, cand(q[1], si1));
+    int t = 0;
+    const PS *top = ps + (i - o);  // j at step t is top - S t
+    for (; t + 4 <= t_safe; t += 4) {
+        const PS *q = top - S * (t + 3);
+        best = umin64(best, cand(q[3 * S], si1));
+        best = umin64(best, cand(q[2 * S], si1));
+        best = umin64(best, cand(q[S], si1));
         best = umin64(best, cand(q[0], si1));
     }
-    for (; w < L; ++w) {
-        int j = i - w;
+    for (; t < t_all; ++t) {
+        int j = i - o - S * t;
         if (j < jlo) j = jlo;
         best = umin64(best, cand(ps[j], si1));
     }
+    if (S >= 2) best = umin64(best, dpp_u64<0xb1>(best));
+    if (S >= 4) best = umin64(best, dpp_u64<0x4e>(best));
     return best;
 }
 
-// Store mode: values (and split points if out_tb) of cells lo..hi, packed
-// as out[i - lo].  Combine mode (G != null): returns the wave minimum over
-// cells of max(value(i), B(i)), B(i) = max(tau_next, G(N-2-i)) from the
-// band-packed reversed row G over [glo, ghi] (bnext_last: B = 0 at i = N-1).
+// Store mode: values (and split points if out_tb) of cells lo..hi, written
+// as out[i - lo].  Combine mode: returns the wave minimum over cells of
+// max(value(i), B(i)).
+template <int S>
+__device__ uint64_t row_pass_s(const Row &rw, PS *ps, int lane, int N, uint64_t *out,
+                               uint8_t *out_tb, const uint64_t *G, int glo, int ghi,
+                               uint64_t tau_next, bool combine, bool last_only)
+{
+    constexpr int CPP = kWave / S;  // cells per pass
+    const int o = lane % S;
+    const int cl = lane / S;
+    int jmin = rw.lo - rw.cap + 1;
+    if (jmin < rw.kmin) jmin = rw.kmin;
+    // first pass's cell loads go out before the split points are built
+    int w_nx = E2_NO_START;
+    uint64_t p_nx = 0, b_nx = 0;
+    {
+        const int i = rw.lo + cl;
+        if (i <= rw.hi) {
+            w_nx = rw.wr[i];
+            p_nx = rw.pr[i + 1];
+            if (combine) b_nx = combine_b(i, N, G, glo, ghi, tau_next, last_only);
+        }
+    }
+    for (int j = jmin + lane; j <= rw.hi; j += kWave) {
+        const int pj = j - 1;
+        const uint64_t pv = (pj >= rw.plo && pj <= rw.phi) ? rw.prev[pj - rw.plo] : E2_INF64;
+        const uint64_t pj8 = rw.pr[j] << 8;
+        ps[j].a = pack_prev(pv, rw.tau, j);
+        ps[j].s = pj8 - (uint64_t)j;
+    }
+    __syncthreads();
+    int L = rw.hi - jmin + 1;
+    if (L > rw.cap) L = rw.cap;
+    int Lm = rw.lo - jmin + 1;
+    if (rw.lmin < Lm) Lm = rw.lmin;
+    if (Lm < 0) Lm = 0;
+    const int t_all = (L + S - 1) / S;
+    const int t_safe = Lm / S;
+    uint64_t lane_best = E2_INF64;
+    for (int base = rw.lo; base <= rw.hi; base += CPP) {
+        const int i = base + cl;
+        const int w = w_nx;
+        const uint64_t p1 = p_nx, b = b_nx;
+        if (base + CPP <= rw.hi && i + CPP <= rw.hi) {
+            w_nx = rw.wr[i + CPP];
+            p_nx = rw.pr[i + CPP + 1];
+            if (combine) b_nx = combine_b(i + CPP, N, G, glo, ghi, tau_next, last_only);
+        }
+        const bool act = i <= rw.hi && w != (int)E2_NO_START;
+        int ie = jmin + (Lm > 0 ? Lm - 1 : 0), jlo = jmin;  // idle lanes: in-range reads
+        uint64_t si1 = 0;
+        if (act) {
+            ie = i;
+            jlo = w > jmin ? w : jmin;
+            si1 = (p1 + rw.hadd) << 8;
+        }
+        const uint64_t best = scan_cell<S>(ps, ie, jlo, o, si1, t_safe, t_all);
+        if (o != 0 || i > rw.hi) continue;
+        const uint64_t v = (!act || best == E2_INF64) ? E2_INF64 : (best >> 8);
+        if (!combine) {
+            out[i - rw.lo] = v;
+            if (out_tb) out_tb[i - rw.lo] = (uint8_t)(best & 0xFF);
+        } else if (v != E2_INF64 && b != E2_INF64) {
+            lane_best = umin64(lane_best, umax64(v, b));
+        }
+    }
+    __syncthreads();
+    return combine ? wave_min_u64(lane_best) : 0;
+}
+
 __device__ uint64_t row_pass(const Row &rw, PS *ps, int lane, int N, uint64_t *out,
                              uint8_t *out_tb, const uint64_t *G, int glo, int ghi,
-                             uint64_t tau_next, bool combine, bool b_last_only)
+                             uint64_t tau_next, bool combine, bool last_only)
 {
-    uint64_t lane_best = E2_INF64;
     if (rw.prev == nullptr) {  // first device: Eq. 2, no split point
+        uint64_t lane_best = E2_INF64;
         for (int i = rw.lo + lane; i <= rw.hi; i += kWave) {
             const uint64_t v = (rw.wr[i] == 0) ? rw.pr[i + 1] + rw.hadd : E2_INF64;
             if (!combine) {
                 out[i - rw.lo] = v;
                 continue;
             }
-            uint64_t b;
-            if (b_last_only) b = (i == N - 1) ? 0 : E2_INF64;
-            else {
-                const int x = N - 2 - i;
-                const uint64_t g = (x >= glo && x <= ghi) ? G[x - glo] : E2_INF64;
-                b = (g == E2_INF64 || tau_next == E2_INF64) ? E2_INF64 : umax64(g, tau_next);
-            }
+            const uint64_t b = combine_b(i, N, G, glo, ghi, tau_next, last_only);
             if (v != E2_INF64 && b != E2_INF64) lane_best = umin64(lane_best, umax64(v, b));
         }
         __syncthreads();
         return combine ? wave_min_u64(lane_best) : 0;
     }
-    int jmin = rw.lo - rw.cap + 1;
-    if (jmin < rw.kmin) jmin = rw.kmin;
-    // the first cell pass's global loads go out before the split points are built
-    int w_next = E2_NO_START;
-    uint64_t p_next = 0;
-    if (rw.lo + lane <= rw.hi) {
-        w_next = rw.wr[rw.lo + lane];
-        p_next = rw.pr[rw.lo + lane + 1];
+    const int n = rw.hi - rw.lo + 1;
+    if (n <= 0) {
+        __syncthreads();
+        return E2_INF64;
     }
-    row_build(rw, ps, jmin, lane);
-    __syncthreads();
-    for (int base = rw.lo; base <= rw.hi; base += kWave) {
-        const int i = base + lane;
-        const int w = w_next;
-        const uint64_t p1 = p_next;
-        if (i + kWave <= rw.hi) {
-            w_next = rw.wr[i + kWave];
-            p_next = rw.pr[i + kWave + 1];
-        }
-        int len = 0, jlo = jmin;
-        uint64_t si1 = 0;
-        if (i <= rw.hi && w != (int)E2_NO_START) {
-            jlo = w > jmin ? w : jmin;
-            len = i - jlo + 1;
-            si1 = (p1 + rw.hadd) << 8;
-        }
-        const uint64_t best = row_scan(ps, i, jlo, len, jmin, si1);
-        if (i > rw.hi) continue;
-        const uint64_t v = (len == 0 || best == E2_INF64) ? E2_INF64 : (best >> 8);
-        if (!combine) {
-            out[i - rw.lo] = v;
-            if (out_tb) out_tb[i - rw.lo] = (uint8_t)(best & 0xFF);
-            continue;
-        }
-        uint64_t b;
-        if (b_last_only) b = (i == N - 1) ? 0 : E2_INF64;
-        else {
-            const int x = N - 2 - i;
-            const uint64_t g = (x >= glo && x <= ghi) ? G[x - glo] : E2_INF64;
-            b = (g == E2_INF64 || tau_next == E2_INF64) ? E2_INF64 : umax64(g, tau_next);
-        }
-        if (v != E2_INF64 && b != E2_INF64) lane_best = umin64(lane_best, umax64(v, b));
-    }
-    __syncthreads();
-    return combine ? wave_min_u64(lane_best) : 0;
+    if (n <= 16)
+        return row_pass_s<4>(rw, ps, lane, N, out, out_tb, G, glo, ghi, tau_next, combine,
+                             last_only);
+    if (n <= 32)
+        return row_pass_s<2>(rw, ps, lane, N, out, out_tb, G, glo, ghi, tau_next, combine,
+                             last_only);
+    return row_pass_s<1>(rw, ps, lane, N, out, out_tb, G, glo, ghi, tau_next, combine,
+                         last_only);
 }
 
 // ---------------------------------------------------------------------------
@@ -359,11 +371,11 @@ struct Bands {
 };
 
 struct DpSmem {
-    PS *ps;          // split-point pairs, N entries
-    uint64_t *Ga;    // reversed row (ping), band-packed
+    PS *ps;          // split-point pairs, N entries (LDS)
+    uint64_t *Ga;    // reversed row (ping), band-packed (global, per wave)
     uint64_t *Gb;    // reversed row (pong)
-    uint64_t *pool;  // band-packed forward rows
-    uint8_t *tbp;    // their split points
+    uint64_t *pool;  // band-packed forward rows (global, per wave)
+    uint8_t *tbp;    // their split points (LDS)
     int pool_cells;
 };
 
@@ -380,6 +392,7 @@ __device__ Row fwd_rowdesc(const E2Tables &tb, const Bands &bd, const DpSmem &sm
     rw.hi = bd.fhi[k];
     rw.kmin = k - 1;
     rw.cap = f ? bd.cH[k] : (int)(bd.pre[k] - bd.pre[k - 1]);
+    rw.lmin = (rw.lo <= rw.hi) ? tb.minwin[((size_t)f * tb.M + c) * tb.N + rw.lo] : 0;
     if (k == 1) {
         rw.tau = 0;
         rw.prev = nullptr;
@@ -464,6 +477,7 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
         g.hi = bd.ghi[t];
         g.kmin = t - 1;
         g.cap = bd.pre[k] - bd.pre[k - 1];
+        g.lmin = (g.lo <= g.hi) ? tb.minwinR[(size_t)c * N + g.lo] : 0;
         if (t == 1) {
             g.tau = 0;
             g.prev = nullptr;
@@ -505,8 +519,9 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
         // cell N-1 of row m: split point of the last stage
         Row rw = fwd_rowdesc(tb, bd, sm, r, chain, m, best_mu);
         rw.lo = rw.hi = N - 1;
-        uint64_t dummy;
-        row_pass(rw, sm.ps, lane, N, &dummy, &bd.last_tb, nullptr, 1, 0, 0, false, false);
+        rw.lmin = tb.minwin[((size_t)(best_mu == m) * tb.M + chain[m - 1]) * N + (N - 1)];
+        uint64_t *dummy = sm.Gb;  // the reversed rows are no longer needed
+        row_pass(rw, sm.ps, lane, N, dummy, &bd.last_tb, nullptr, 1, 0, 0, false, false);
         if (lane == 0) {
             int i = N - 1;
             int j = bd.last_tb;
@@ -537,7 +552,6 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
 {
     const int N = tb.N;
     uint64_t *cur = sm.Ga, *prv = sm.Gb;
-    uint64_t last = E2_INF64;
     for (int k = 1; k <= m; ++k) {
         const int c = chain[k - 1];
         const int f = (mu == k);
@@ -549,6 +563,7 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
         rw.hi = N - 1;
         rw.kmin = k - 1;
         rw.cap = N;
+        rw.lmin = tb.minwin[((size_t)f * tb.M + c) * N + rw.lo];
         if (k == 1) {
             rw.tau = 0;
             rw.prev = nullptr;
@@ -567,24 +582,22 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
         prv = cur;
         cur = tmp;
     }
-    last = prv[(N - 1) - (m - 1)];
-    __syncthreads();
-    return last;
+    return prv[(N - 1) - (m - 1)];
 }
 
 // ---------------------------------------------------------------------------
 // Persistent DP kernel: one wave per workgroup; waves take listed problems
 // in list order through an atomic counter and exit when the list is
-// exhausted.  Dynamic LDS: split-point pairs (N x 16 B), two reversed rows
-// (2 x (N+1) x 8 B), then the forward-row pool (pool_cells x 8 B) and its
-// split-point bytes.
+// exhausted.  LDS: split-point pairs (N x 16 B) and the split-point bytes
+// of the forward-row pool; the row values live in a per-wave global region
+// (pool_cells + 2 (N+1) u64).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cells,
                                            const uint8_t *__restrict__ labels,
                                            const uint8_t *__restrict__ roles,
                                            uint32_t *counters, const uint32_t *__restrict__ list,
-                                           uint8_t *tb_global, uint64_t *T, uint64_t *Lambda,
-                                           int16_t *master, uint8_t *layers)
+                                           uint64_t *rows, uint8_t *tb_global, uint64_t *T,
+                                           uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
     extern __shared__ uint64_t dyn[];
     __shared__ Bands bd;
@@ -595,10 +608,11 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
     const int M = tb.M, N = tb.N;
     DpSmem sm;
     sm.ps = reinterpret_cast<PS *>(dyn);
-    sm.Ga = dyn + 2 * N;
+    sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N);
+    uint64_t *my_rows = rows + (size_t)blockIdx.x * ((size_t)pool_cells + 2 * (N + 1));
+    sm.pool = my_rows;
+    sm.Ga = my_rows + pool_cells;
     sm.Gb = sm.Ga + (N + 1);
-    sm.pool = sm.Gb + (N + 1);
-    sm.tbp = reinterpret_cast<uint8_t *>(sm.pool + pool_cells);
     sm.pool_cells = pool_cells;
     const uint32_t n_jobs = counters[0];
 
@@ -638,8 +652,8 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
                 }
             }
             if (best != E2_INF64) {
-                uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)pool_cells * 8)
-                                   ? reinterpret_cast<uint8_t *>(sm.pool)
+                uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)pool_cells)
+                                   ? sm.tbp
                                    : tb_global + (size_t)blockIdx.x * N * N;
                 dp_table(tb, sm, r, chain, m, best_mu, tbp, lane);
                 __threadfence_block();
@@ -842,17 +856,19 @@ __global__ __launch_bounds__(64) void k_breed(int M, int P, int k_max,
 int e2_dp_pool_cells(int N)
 {
     (void)N;
-    return 1024;
+    return 2048;
 }
+
+size_t e2_dp_row_words(int N) { return (size_t)e2_dp_pool_cells(N) + 2 * (size_t)(N + 1); }
 
 size_t e2_dp_lds_bytes(int N)
 {
-    return (size_t)2 * N * 8 + (size_t)2 * (N + 1) * 8 + (size_t)e2_dp_pool_cells(N) * 9;
+    return (size_t)16 * N + (size_t)e2_dp_pool_cells(N);
 }
 
 int e2_dp_slots(int problems)
 {
-    const int cap = 256 * 16;  // 16 one-wave workgroups per CU on a 256-CU part
+    const int cap = 256 * 20;  // 20 one-wave workgroups per CU on a 256-CU part
     return problems < cap ? (problems > 0 ? problems : 1) : cap;
 }
 
@@ -865,8 +881,8 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
                                 layers);
     const int pool = e2_dp_pool_cells(t.N);
     k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, labels, roles, wk.counters,
-                                                      wk.list, wk.tb_global, T, Lambda, master,
-                                                      layers);
+                                                      wk.list, wk.rows, wk.tb_global, T, Lambda,
+                                                      master, layers);
     return hipGetLastError();
 }
 
