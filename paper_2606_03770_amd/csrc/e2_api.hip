@@ -122,7 +122,7 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
     // LDS pool of the reference path
     const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_pool_cells(ctx->N);
     *tb_bytes = need_tb ? (size_t)(*slots) * ctx->N * ctx->N : 0;
-    return align256(16) + align256(problems * 4) +
+    return align256(32) + align256(problems * 4 * 4) +
            align256((size_t)(*slots) * e2_dp_row_words(ctx->N) * 8) + align256(*tb_bytes);
 }
 
@@ -131,9 +131,9 @@ void carve_work(void *base, const e2_ctx *ctx, int P, int k_max, int slots, size
 {
     char *p = static_cast<char *>(base);
     wk->counters = reinterpret_cast<uint32_t *>(p);
-    p += align256(16);
-    wk->list = reinterpret_cast<uint32_t *>(p);
-    p += align256((size_t)P * k_max * 4);
+    p += align256(32);
+    wk->list = reinterpret_cast<uint32_t *>(p);  // four chain-length segments of P * k_max
+    p += align256((size_t)P * k_max * 4 * 4);
     wk->rows = reinterpret_cast<uint64_t *>(p);
     p += align256((size_t)slots * e2_dp_row_words(ctx->N) * 8);
     wk->tb_global = tb_bytes ? reinterpret_cast<uint8_t *>(p) : nullptr;

@@ -38,8 +38,8 @@ struct e2_ctx {
 
 // Scratch layout of one solve/eval call (device memory, stream-ordered).
 struct E2Work {
-    uint32_t *counters;  // [0] problems listed, [1] next problem to take
-    uint32_t *list;      // [P * k_max] (p << 8) | q of problems needing the DP
+    uint32_t *counters;  // [0..3] problems listed per chain-length class, [4] next job
+    uint32_t *list;      // [4][P * k_max] (p << 8) | q of problems needing the DP
     uint64_t *rows;      // [n_slots][pool + 2 (N+1)] per-wave DP rows
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
     int n_slots;         // waves of the DP kernel

@@ -1,15 +1,16 @@
 // HIP kernels (gfx950, wave64) of the population-fitness path.
 //
 //   k_init        zero the per-call counters (a fill kernel, no memset node)
-//   k_extract     one workgroup per individual: cluster sizes, a necessary
+//   k_extract     one wave per individual: cluster sizes, a necessary
 //                 memory/size pre-check, the list of clusters that need the
-//                 DP; writes INF results for the others
+//                 DP (bucketed by chain length); INF results for the others
 //   k_dp          persistent waves: each takes the next listed cluster,
 //                 rebuilds its device chain from the genome, runs the
 //                 bottleneck DP of Algorithm 1 / Eq. 1-2 for every master
 //                 position, picks the best master, backtracks and writes
 //                 T, Lambda, master and per-device block counts
-//   k_fitness     Eq. 3-5 per individual with the QoS floor
+//   k_fitness     Eq. 3-5 per individual with the QoS floor (one wave per
+//                 individual, lanes over clusters)
 //   k_elites      one workgroup: the n_elite best keys (w, phase, index)
 //   k_breed       one wave per output slot: elite copy or tournament +
 //                 uniform crossover + per-gene mutation
@@ -75,67 +76,143 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
 
 __global__ void k_init(uint32_t *counters)
 {
-    if (threadIdx.x < 4) counters[threadIdx.x] = 0;
+    if (threadIdx.x < 8) counters[threadIdx.x] = 0;
 }
 
 // ---------------------------------------------------------------------------
-// Extraction and pre-check: one 256-thread workgroup per individual.
+// Extraction and pre-check: one wave per genome, kEG genomes per workgroup.
 // A cluster goes to the DP list unless it is empty or provably infeasible:
 //   more devices than blocks (every device must hold a block), a device that
 //   cannot hold a single block, total single-stage capacity below N, or no
 //   device able to hold a block plus the head (no possible master).
+// Listed problems are bucketed by chain length into kClasses segments of the
+// list (longest chains first), so the DP kernel schedules large problems
+// early; each workgroup reserves its range of each segment with one atomic.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_extract(E2Tables tb, int P, int k_max,
-                                                 const uint8_t *__restrict__ labels,
-                                                 uint32_t *counters, uint32_t *list,
-                                                 uint64_t *T, uint64_t *Lambda, int16_t *master,
-                                                 uint8_t *layers)
+constexpr int kEG = 8;       // genomes per extraction workgroup
+constexpr int kClasses = 4;  // chain-length classes: m >= 16, 12..15, 8..11, < 8
+
+__device__ __forceinline__ int size_class(int m)
 {
-    __shared__ uint32_t cnt[256], csum[256], cmin[256], hasH[256];
-    __shared__ uint8_t listed[256];
-    __shared__ uint32_t nlist, base;
-    const int p = blockIdx.x;
-    const int t = threadIdx.x;
+    return m >= 16 ? 0 : (m >= 12 ? 1 : (m >= 8 ? 2 : 3));
+}
+
+__global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_max,
+                                                      const uint8_t *__restrict__ labels,
+                                                      uint32_t *counters, uint32_t *list,
+                                                      size_t seg_cap, uint64_t *T,
+                                                      uint64_t *Lambda, int16_t *master,
+                                                      uint8_t *layers)
+{
+    // per genome: (count << 16) + sum of cap0, min cap0, head-capable bitmask,
+    // listed bitmask
+    __shared__ uint32_t packed[kEG][256];
+    __shared__ uint32_t mincap[kEG][256];
+    __shared__ uint32_t hmask[kEG][8];
+    __shared__ uint32_t lmask[kEG][8];
+    __shared__ uint32_t ncls[kEG][kClasses];
+    __shared__ uint32_t base[kEG][kClasses];
+    const int g = threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    const int p = blockIdx.x * kEG + g;
     const int M = tb.M, N = tb.N;
-    cnt[t] = 0;
-    csum[t] = 0;
-    cmin[t] = 0xFFFFFFFFu;
-    hasH[t] = 0;
-    if (t == 0) nlist = 0;
+    for (int q = lane; q < 256; q += 64) {
+        packed[g][q] = 0;
+        mincap[g][q] = 0xFFFFFFFFu;
+    }
+    if (lane < 8) {
+        hmask[g][lane] = 0;
+        lmask[g][lane] = 0;
+    }
     __syncthreads();
-    int lab = 256;
-    if (t < M) {
-        lab = labels[(size_t)p * M + t];
-        if (lab < k_max) {
-            atomicAdd(&cnt[lab], 1u);
-            atomicAdd(&csum[lab], (uint32_t)tb.cap0[t]);
-            atomicMin(&cmin[lab], (uint32_t)tb.cap0[t]);
-            if (tb.capH[t]) atomicOr(&hasH[lab], 1u);
+    int labs[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int d = lane + 64 * u;
+        labs[u] = 256;
+        if (p < P && d < M) {
+            const int lab = labels[(size_t)p * M + d];
+            labs[u] = lab;
+            if (lab < k_max) {
+                const uint32_t c0 = tb.cap0[d];
+                atomicAdd(&packed[g][lab], (1u << 16) | c0);
+                atomicMin(&mincap[g][lab], c0);
+                if (tb.capH[d]) atomicOr(&hmask[g][lab >> 5], 1u << (lab & 31));
+            }
         }
     }
     __syncthreads();
-    bool feas = false;
-    uint32_t slot = 0;
-    if (t < k_max) {
-        const uint32_t m = cnt[t];
-        feas = m >= 1 && m <= (uint32_t)N && csum[t] >= (uint32_t)N && cmin[t] >= 1 && hasH[t];
-        if (feas) slot = atomicAdd(&nlist, 1u);
-        listed[t] = feas;
-    }
+    // decide per cluster; count listed problems per class
+    uint32_t my_cls[4] = {0, 0, 0, 0};
+    for (int c = 0; c < kClasses; ++c) ncls[g][c] = 0;  // every lane writes the same zero
     __syncthreads();
-    if (t == 0 && nlist) base = atomicAdd(&counters[0], nlist);
-    __syncthreads();
-    if (t < k_max) {
-        const size_t o = (size_t)p * k_max + t;
-        if (feas) {
-            list[base + slot] = ((uint32_t)p << 8) | (uint32_t)t;
-        } else {
-            T[o] = E2_INF64;
-            Lambda[o] = E2_INF64;
-            if (master) master[o] = -1;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int q = lane + 64 * u;
+        bool feas = false;
+        int cls = 0;
+        if (p < P && q < k_max) {
+            const uint32_t pk = packed[g][q];
+            const uint32_t m = pk >> 16, csum = pk & 0xFFFF;
+            feas = m >= 1 && m <= (uint32_t)N && csum >= (uint32_t)N && mincap[g][q] >= 1 &&
+                   ((hmask[g][q >> 5] >> (q & 31)) & 1u);
+            cls = size_class((int)m);
+            if (!feas) {
+                const size_t o = (size_t)p * k_max + q;
+                T[o] = E2_INF64;
+                Lambda[o] = E2_INF64;
+                if (master) master[o] = -1;
+            }
+        }
+        my_cls[u] = feas ? (uint32_t)(cls + 1) : 0;
+        const uint64_t fm = __ballot(feas);
+        if (lane == 0 && fm) {
+            // q = 64u + bit: listed bitmask words 2u and 2u + 1
+            lmask[g][2 * u] = (uint32_t)fm;
+            lmask[g][2 * u + 1] = (uint32_t)(fm >> 32);
+        }
+        for (int c = 0; c < kClasses; ++c) {
+            const uint64_t bm = __ballot(feas && cls == c);
+            if (lane == 0) ncls[g][c] += (uint32_t)__popcll(bm);
         }
     }
-    if (layers && t < M && (lab >= k_max || !listed[lab])) layers[(size_t)p * M + t] = 0;
+    __syncthreads();
+    // one atomic per class per workgroup; genome g's share follows genomes < g
+    if (threadIdx.x < kClasses) {
+        const int c = threadIdx.x;
+        uint32_t tot = 0;
+        for (int h = 0; h < kEG; ++h) tot += ncls[h][c];
+        uint32_t b0 = tot ? atomicAdd(&counters[c], tot) : 0;
+        for (int h = 0; h < kEG; ++h) {
+            base[h][c] = b0;
+            b0 += ncls[h][c];
+        }
+    }
+    __syncthreads();
+    uint32_t run[kClasses] = {0, 0, 0, 0};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int q = lane + 64 * u;
+        const uint32_t mc = my_cls[u];
+        for (int c = 0; c < kClasses; ++c) {
+            const uint64_t bm = __ballot(mc == (uint32_t)(c + 1));
+            if (mc == (uint32_t)(c + 1)) {
+                const uint32_t pos =
+                    base[g][c] + run[c] + (uint32_t)__popcll(bm & ((1ull << lane) - 1));
+                list[(size_t)c * seg_cap + pos] = ((uint32_t)p << 8) | (uint32_t)q;
+            }
+            run[c] += (uint32_t)__popcll(bm);
+        }
+    }
+    if (layers && p < P) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int d = lane + 64 * u;
+            const int lab = labs[u];
+            if (d < M && (lab >= k_max || !((lmask[g][lab >> 5] >> (lab & 31)) & 1u)))
+                layers[(size_t)p * M + d] = 0;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -596,7 +673,8 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
                                            const uint8_t *__restrict__ labels,
                                            const uint8_t *__restrict__ roles,
                                            uint32_t *counters, const uint32_t *__restrict__ list,
-                                           uint64_t *rows, uint8_t *tb_global, uint64_t *T,
+                                           size_t seg_cap, uint64_t *rows, uint8_t *tb_global,
+                                           uint64_t *T,
                                            uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
     extern __shared__ uint64_t dyn[];
@@ -614,15 +692,22 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
     sm.Ga = my_rows + pool_cells;
     sm.Gb = sm.Ga + (N + 1);
     sm.pool_cells = pool_cells;
-    const uint32_t n_jobs = counters[0];
+    static_assert(kClasses == 4, "job mapping below assumes four classes");
+    const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
+    const uint32_t n_jobs = n0 + n1 + n2 + n3;
 
     for (;;) {
-        if (lane == 0) job = atomicAdd(&counters[1], 1u);
+        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
         __syncthreads();
-        const uint32_t idx = job;
+        uint32_t idx = job;
         __syncthreads();
         if (idx >= n_jobs) break;
-        const uint32_t code = list[idx];
+        // classes in order, longest chains first
+        int cls = 0;
+        if (idx >= n0) { idx -= n0; cls = 1;
+            if (idx >= n1) { idx -= n1; cls = 2;
+                if (idx >= n2) { idx -= n2; cls = 3; } } }
+        const uint32_t code = list[(size_t)cls * seg_cap + idx];
         const int p = (int)(code >> 8);
         const int q = (int)(code & 0xFF);
 
@@ -711,15 +796,19 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
 // ---------------------------------------------------------------------------
 constexpr uint64_t kScale = 1ull << 50;
 
-__global__ void k_fitness(int P, int k_max, const uint64_t *__restrict__ T,
-                          const uint64_t *__restrict__ Lambda, const uint8_t *__restrict__ roles,
-                          uint64_t t_arrival, uint64_t nd, uint64_t lambda_max, uint64_t *w,
-                          uint64_t *phase, uint64_t *s_p, uint64_t *s_d)
+__global__ __launch_bounds__(256) void k_fitness(int P, int k_max, const uint64_t *__restrict__ T,
+                                                 const uint64_t *__restrict__ Lambda,
+                                                 const uint8_t *__restrict__ roles,
+                                                 uint64_t t_arrival, uint64_t nd,
+                                                 uint64_t lambda_max, uint64_t *w, uint64_t *phase,
+                                                 uint64_t *s_p, uint64_t *s_d)
 {
-    const int p = blockIdx.x * blockDim.x + threadIdx.x;
+    // one wave per genome, lanes over clusters
+    const int p = blockIdx.x * 4 + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
     if (p >= P) return;
     uint64_t sp = 0, sd = 0;
-    for (int q = 0; q < k_max; ++q) {
+    for (int q = lane; q < k_max; q += kWave) {
         const size_t o = (size_t)p * k_max + q;
         const uint64_t t = T[o];
         if (t == E2_INF64) continue;
@@ -729,6 +818,9 @@ __global__ void k_fitness(int P, int k_max, const uint64_t *__restrict__ T,
         if (dec) sd += rho;
         else sp += rho;
     }
+    sp = wave_sum_u64(sp);
+    sd = wave_sum_u64(sd);
+    if (lane != 0) return;
     const uint64_t SP = sp ? (kScale + sp - 1) / sp : E2_INF64;
     const uint64_t SD = sd ? nd * ((kScale + sd - 1) / sd) : E2_INF64;
     if (s_p) s_p[p] = SP;
@@ -876,13 +968,14 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
                                 const uint8_t *labels, const uint8_t *roles, const E2Work &wk,
                                 uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
+    const size_t seg = (size_t)P * k_max;
     k_init<<<1, 64, 0, s>>>(wk.counters);
-    k_extract<<<P, 256, 0, s>>>(t, P, k_max, labels, wk.counters, wk.list, T, Lambda, master,
-                                layers);
+    k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, labels, wk.counters, wk.list,
+                                                       seg, T, Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
     k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, labels, roles, wk.counters,
-                                                      wk.list, wk.rows, wk.tb_global, T, Lambda,
-                                                      master, layers);
+                                                      wk.list, seg, wk.rows, wk.tb_global, T,
+                                                      Lambda, master, layers);
     return hipGetLastError();
 }
 
@@ -891,7 +984,7 @@ hipError_t e2_launch_fitness(hipStream_t s, int P, int k_max, const uint64_t *T,
                              uint64_t nd, uint64_t lambda_max, uint64_t *w, uint64_t *phase,
                              uint64_t *s_p, uint64_t *s_d)
 {
-    k_fitness<<<(P + 255) / 256, 256, 0, s>>>(P, k_max, T, Lambda, roles, t_arrival, nd,
+    k_fitness<<<(P + 3) / 4, 256, 0, s>>>(P, k_max, T, Lambda, roles, t_arrival, nd,
                                               lambda_max, w, phase, s_p, s_d);
     return hipGetLastError();
 }
