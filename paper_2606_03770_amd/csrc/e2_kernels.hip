@@ -232,12 +232,19 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
 // unchanged).  The S partial minima meet through DPP quad permutations.
 // Split points keep (prefix term, shifted prefix sum) as one 16-byte LDS
 // pair.
+//
+// INF needs no branches: finite values are below 2^56 - 256, so a packed
+// key built from an INF prefix term or link is >= kInfKey and loses every
+// comparison with a finite key.
 // ---------------------------------------------------------------------------
+constexpr uint64_t kInfKey = 0xFFFFFFFFFFFFFF00ull;
+
 struct PS {
-    uint64_t a;  // max(prev(j-1), tau) << 8 | j, INF when unusable
+    uint64_t a;  // max(prev(j-1), tau) << 8 | j
     uint64_t s;  // (P[j] << 8) - j
 };
 
+// Wave-uniform description of a row (scalar registers).
 struct Row {
     const uint64_t *pr;    // prefix sums P[0..N] of the stage device
     const uint8_t *wr;     // smallest stage start per stage end, E2_NO_START if none
@@ -250,6 +257,29 @@ struct Row {
     const uint64_t *prev;  // previous row, band-packed over [plo, phi]; null: first device
     int plo, phi;
 };
+
+// Where a row's results go: stored values (+ split points), or, for a
+// combine, a running per-lane minimum of (max(value(i), B(i)) << 8 | mu) with
+// B(i) = max(tau_next, G(N-2-i)) from the band-packed reversed row G over
+// [glo, ghi] (last_only: B = 0 at i = N-1, INF elsewhere).
+struct RowOut {
+    uint64_t *vals;
+    uint8_t *tbs;
+    bool combine;
+    bool last_only;
+    const uint64_t *G;
+    int glo, ghi;
+    uint64_t tau_next;
+    int mu;
+};
+
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ uint64_t uni64(uint64_t x)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
 
 __device__ __forceinline__ const uint64_t *pref_row(const E2Tables &tb, int r, int c)
 {
@@ -265,27 +295,29 @@ __device__ __forceinline__ const uint8_t *win_row(const E2Tables &tb, int f, int
 }
 __device__ __forceinline__ uint64_t link_tau(const E2Tables &tb, int r, int a, int b)
 {
-    return tb.tau[((size_t)r * tb.M + a) * tb.M + b];
+    return uni64(tb.tau[((size_t)r * tb.M + a) * tb.M + b]);
 }
 __device__ __forceinline__ uint64_t pack_prev(uint64_t prev, uint64_t tau, int j)
 {
-    return (prev == E2_INF64 || tau == E2_INF64) ? E2_INF64
-                                                  : ((umax64(prev, tau) << 8) | (uint64_t)j);
+    return (umax64(prev, tau) << 8) | (uint64_t)j;
+}
+__device__ __forceinline__ uint64_t unpack_val(uint64_t key)
+{
+    return key >= kInfKey ? E2_INF64 : (key >> 8);
 }
 __device__ __forceinline__ uint64_t cand(const PS &e, uint64_t si1)
 {
     return umax64(e.a, si1 - e.s);
 }
-
-// B(i) of a combine: max(tau_next, G(N-2-i)) from the band-packed reversed
-// row G over [glo, ghi]; with last_only, B = 0 at i = N-1 and INF elsewhere.
-__device__ __forceinline__ uint64_t combine_b(int i, int N, const uint64_t *G, int glo, int ghi,
-                                              uint64_t tau_next, bool last_only)
+__device__ __forceinline__ uint64_t combine_b(int i, int N, const RowOut &ro)
 {
-    if (last_only) return (i == N - 1) ? 0 : E2_INF64;
+    if (ro.last_only) return (i == N - 1) ? 0 : E2_INF64;
     const int x = N - 2 - i;
-    const uint64_t g = (x >= glo && x <= ghi) ? G[x - glo] : E2_INF64;
-    return (g == E2_INF64 || tau_next == E2_INF64) ? E2_INF64 : umax64(g, tau_next);
+    return (x >= ro.glo && x <= ro.ghi) ? umax64(ro.G[x - ro.glo], ro.tau_next) : E2_INF64;
+}
+__device__ __forceinline__ uint64_t combine_key(uint64_t v, uint64_t b, int mu)
+{
+    return (umax64(v, b) << 8) | (uint64_t)mu;
 }
 
 template <int S>
@@ -312,19 +344,13 @@ __device__ __forceinline__ uint64_t scan_cell(const PS *ps, int i, int jlo, int 
     return best;
 }
 
-// Store mode: values (and split points if out_tb) of cells lo..hi, written
-// as out[i - lo].  Combine mode: returns the wave minimum over cells of
-// max(value(i), B(i)).
 template <int S>
-__device__ uint64_t row_pass_s(const Row &rw, PS *ps, int lane, int N, uint64_t *out,
-                               uint8_t *out_tb, const uint64_t *G, int glo, int ghi,
-                               uint64_t tau_next, bool combine, bool last_only)
+__device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane, int N)
 {
     constexpr int CPP = kWave / S;  // cells per pass
     const int o = lane % S;
     const int cl = lane / S;
-    int jmin = rw.lo - rw.cap + 1;
-    if (jmin < rw.kmin) jmin = rw.kmin;
+    const int jmin = max(rw.kmin, rw.lo - rw.cap + 1);
     // first pass's cell loads go out before the split points are built
     int w_nx = E2_NO_START;
     uint64_t p_nx = 0, b_nx = 0;
@@ -333,7 +359,7 @@ __device__ uint64_t row_pass_s(const Row &rw, PS *ps, int lane, int N, uint64_t 
         if (i <= rw.hi) {
             w_nx = rw.wr[i];
             p_nx = rw.pr[i + 1];
-            if (combine) b_nx = combine_b(i, N, G, glo, ghi, tau_next, last_only);
+            if (ro.combine) b_nx = combine_b(i, N, ro);
         }
     }
     for (int j = jmin + lane; j <= rw.hi; j += kWave) {
@@ -344,76 +370,76 @@ __device__ uint64_t row_pass_s(const Row &rw, PS *ps, int lane, int N, uint64_t 
         ps[j].s = pj8 - (uint64_t)j;
     }
     __syncthreads();
-    int L = rw.hi - jmin + 1;
-    if (L > rw.cap) L = rw.cap;
-    int Lm = rw.lo - jmin + 1;
-    if (rw.lmin < Lm) Lm = rw.lmin;
-    if (Lm < 0) Lm = 0;
+    const int L = min(rw.cap, rw.hi - jmin + 1);
+    const int Lm = max(0, min(rw.lmin, rw.lo - jmin + 1));
     const int t_all = (L + S - 1) / S;
     const int t_safe = Lm / S;
-    uint64_t lane_best = E2_INF64;
+    const int i_idle = jmin + (Lm > 0 ? Lm - 1 : 0);  // idle lanes: in-range reads
+    uint64_t acc = E2_INF64;
     for (int base = rw.lo; base <= rw.hi; base += CPP) {
         const int i = base + cl;
         const int w = w_nx;
         const uint64_t p1 = p_nx, b = b_nx;
-        if (base + CPP <= rw.hi && i + CPP <= rw.hi) {
+        if (i + CPP <= rw.hi) {
             w_nx = rw.wr[i + CPP];
             p_nx = rw.pr[i + CPP + 1];
-            if (combine) b_nx = combine_b(i + CPP, N, G, glo, ghi, tau_next, last_only);
+            if (ro.combine) b_nx = combine_b(i + CPP, N, ro);
         }
         const bool act = i <= rw.hi && w != (int)E2_NO_START;
-        int ie = jmin + (Lm > 0 ? Lm - 1 : 0), jlo = jmin;  // idle lanes: in-range reads
-        uint64_t si1 = 0;
-        if (act) {
-            ie = i;
-            jlo = w > jmin ? w : jmin;
-            si1 = (p1 + rw.hadd) << 8;
-        }
+        const int ie = act ? i : i_idle;
+        const int jlo = act ? max(w, jmin) : jmin;
+        const uint64_t si1 = (p1 + rw.hadd) << 8;
         const uint64_t best = scan_cell<S>(ps, ie, jlo, o, si1, t_safe, t_all);
         if (o != 0 || i > rw.hi) continue;
-        const uint64_t v = (!act || best == E2_INF64) ? E2_INF64 : (best >> 8);
-        if (!combine) {
-            out[i - rw.lo] = v;
-            if (out_tb) out_tb[i - rw.lo] = (uint8_t)(best & 0xFF);
-        } else if (v != E2_INF64 && b != E2_INF64) {
-            lane_best = umin64(lane_best, umax64(v, b));
+        const uint64_t v = act ? unpack_val(best) : E2_INF64;
+        if (!ro.combine) {
+            ro.vals[i - rw.lo] = v;
+            if (ro.tbs) ro.tbs[i - rw.lo] = (uint8_t)(best & 0xFF);
+        } else {
+            acc = umin64(acc, combine_key(v, b, ro.mu));
         }
     }
     __syncthreads();
-    return combine ? wave_min_u64(lane_best) : 0;
+    return acc;
 }
 
-__device__ uint64_t row_pass(const Row &rw, PS *ps, int lane, int N, uint64_t *out,
-                             uint8_t *out_tb, const uint64_t *G, int glo, int ghi,
-                             uint64_t tau_next, bool combine, bool last_only)
+// Store mode returns INF; combine mode returns the lane's running minimum of
+// (max(value, B) << 8 | mu) (the caller reduces over the wave once).
+__device__ uint64_t row_pass(const Row &rw, const RowOut &ro, PS *ps, int lane, int N)
 {
     if (rw.prev == nullptr) {  // first device: Eq. 2, no split point
-        uint64_t lane_best = E2_INF64;
+        uint64_t acc = E2_INF64;
         for (int i = rw.lo + lane; i <= rw.hi; i += kWave) {
             const uint64_t v = (rw.wr[i] == 0) ? rw.pr[i + 1] + rw.hadd : E2_INF64;
-            if (!combine) {
-                out[i - rw.lo] = v;
-                continue;
-            }
-            const uint64_t b = combine_b(i, N, G, glo, ghi, tau_next, last_only);
-            if (v != E2_INF64 && b != E2_INF64) lane_best = umin64(lane_best, umax64(v, b));
+            if (!ro.combine) ro.vals[i - rw.lo] = v;
+            else acc = umin64(acc, combine_key(v, combine_b(i, N, ro), ro.mu));
         }
         __syncthreads();
-        return combine ? wave_min_u64(lane_best) : 0;
+        return acc;
     }
     const int n = rw.hi - rw.lo + 1;
     if (n <= 0) {
         __syncthreads();
         return E2_INF64;
     }
-    if (n <= 16)
-        return row_pass_s<4>(rw, ps, lane, N, out, out_tb, G, glo, ghi, tau_next, combine,
-                             last_only);
-    if (n <= 32)
-        return row_pass_s<2>(rw, ps, lane, N, out, out_tb, G, glo, ghi, tau_next, combine,
-                             last_only);
-    return row_pass_s<1>(rw, ps, lane, N, out, out_tb, G, glo, ghi, tau_next, combine,
-                         last_only);
+    if (n <= 16) return row_pass_s<4>(rw, ro, ps, lane, N);
+    if (n <= 32) return row_pass_s<2>(rw, ro, ps, lane, N);
+    return row_pass_s<1>(rw, ro, ps, lane, N);
+}
+
+__device__ __forceinline__ RowOut store_to(uint64_t *vals, uint8_t *tbs)
+{
+    RowOut ro;
+    ro.vals = vals;
+    ro.tbs = tbs;
+    ro.combine = false;
+    ro.last_only = false;
+    ro.G = nullptr;
+    ro.glo = 1;
+    ro.ghi = 0;
+    ro.tau_next = 0;
+    ro.mu = 0;
+    return ro;
 }
 
 // ---------------------------------------------------------------------------
@@ -434,8 +460,9 @@ __device__ uint64_t row_pass(const Row &rw, PS *ps, int lane, int N, uint64_t *o
 //                    + head_mu), tau(mu, mu+1), G_{mu+1}(i+1) )
 //        (mu = 1: the stage starts at block 0; mu = m: it ends at N-1)
 //   which is the optimum of the table of Algorithm 1 for master mu.  The
-//   smallest mu attaining min T_mu is the master; rows mu*..m of its table
-//   (rows below mu* are F) give the split points for the back tracing.
+//   minimum of (T_mu << 8 | mu) gives the best T and the smallest master
+//   attaining it; rows mu*..m of its table (rows below mu* are F) give the
+//   split points for the back tracing.
 // Returns false (nothing decided) if the forward bands do not fit the pool.
 // ---------------------------------------------------------------------------
 struct Bands {
@@ -459,27 +486,27 @@ struct DpSmem {
 __device__ Row fwd_rowdesc(const E2Tables &tb, const Bands &bd, const DpSmem &sm, int r,
                            const uint8_t *chain, int k, int mu)
 {
-    const int c = chain[k - 1];
+    const int c = uni(chain[k - 1]);
     const int f = (mu == k);
     Row rw;
     rw.pr = pref_row(tb, r, c);
     rw.wr = win_row(tb, f, c);
-    rw.hadd = f ? tb.head[r * tb.M + c] : 0;
-    rw.lo = bd.flo[k];
-    rw.hi = bd.fhi[k];
+    rw.hadd = f ? uni64(tb.head[r * tb.M + c]) : 0;
+    rw.lo = uni(bd.flo[k]);
+    rw.hi = uni(bd.fhi[k]);
     rw.kmin = k - 1;
-    rw.cap = f ? bd.cH[k] : (int)(bd.pre[k] - bd.pre[k - 1]);
-    rw.lmin = (rw.lo <= rw.hi) ? tb.minwin[((size_t)f * tb.M + c) * tb.N + rw.lo] : 0;
+    rw.cap = f ? uni(bd.cH[k]) : uni(bd.pre[k] - bd.pre[k - 1]);
+    rw.lmin = (rw.lo <= rw.hi) ? uni(tb.minwin[((size_t)f * tb.M + c) * tb.N + rw.lo]) : 0;
     if (k == 1) {
         rw.tau = 0;
         rw.prev = nullptr;
         rw.plo = 1;
         rw.phi = 0;
     } else {
-        rw.tau = link_tau(tb, r, chain[k - 2], c);
-        rw.prev = sm.pool + bd.off[k - 1];
-        rw.plo = bd.flo[k - 1];
-        rw.phi = bd.fhi[k - 1];
+        rw.tau = link_tau(tb, r, uni(chain[k - 2]), c);
+        rw.prev = sm.pool + uni(bd.off[k - 1]);
+        rw.plo = uni(bd.flo[k - 1]);
+        rw.phi = uni(bd.fhi[k - 1]);
     }
     return rw;
 }
@@ -523,82 +550,87 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
         }
     }
     __syncthreads();
-    if ((int)bd.off[m] > sm.pool_cells) return false;
+    if (uni(bd.off[m]) > sm.pool_cells) return false;
 
     // forward rows F_1..F_{m-1}
     for (int k = 1; k < m; ++k) {
-        const Row rw = fwd_rowdesc(tb, bd, sm, r, chain, k, 0);
-        row_pass(rw, sm.ps, lane, N, sm.pool + bd.off[k], sm.tbp + bd.off[k], nullptr, 1, 0, 0,
-                 false, false);
+        const int off = uni(bd.off[k]);
+        row_pass(fwd_rowdesc(tb, bd, sm, r, chain, k, 0), store_to(sm.pool + off, sm.tbp + off),
+                 sm.ps, lane, N);
     }
-    // master mu = m: its stage ends at block N-1
-    uint64_t best;
+    // combines: master mu = m (stage ends at block N-1), then, after each
+    // reversed row t = 1..m-1 (original backward row k = m+1-t), master m - t
+    uint64_t acc = E2_INF64;
     {
-        Row rw = fwd_rowdesc(tb, bd, sm, r, chain, m, m);
-        best = (rw.cap > 0) ? row_pass(rw, sm.ps, lane, N, nullptr, nullptr, nullptr, 1, 0, 0,
-                                       true, true)
-                            : E2_INF64;
+        const Row rw = fwd_rowdesc(tb, bd, sm, r, chain, m, m);
+        if (rw.cap > 0) {
+            RowOut ro = store_to(nullptr, nullptr);
+            ro.combine = true;
+            ro.last_only = true;
+            ro.mu = m;
+            acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
+        }
     }
-    int best_mu = best == E2_INF64 ? 0 : m;
-    // reversed rows t = 1..m-1 (original backward row k = m+1-t), each
-    // followed by the combine of master mu = m - t
     uint64_t *Gprev = sm.Gb, *Gcur = sm.Ga;
     for (int t = 1; t < m; ++t) {
         const int k = m + 1 - t;  // device of this backward row
-        const int c = chain[k - 1];
+        const int c = uni(chain[k - 1]);
         Row g;
         g.pr = prefR_row(tb, r, c);
         g.wr = tb.winR + (size_t)c * N;
         g.hadd = 0;
-        g.lo = bd.glo[t];
-        g.hi = bd.ghi[t];
+        g.lo = uni(bd.glo[t]);
+        g.hi = uni(bd.ghi[t]);
         g.kmin = t - 1;
-        g.cap = bd.pre[k] - bd.pre[k - 1];
-        g.lmin = (g.lo <= g.hi) ? tb.minwinR[(size_t)c * N + g.lo] : 0;
+        g.cap = uni(bd.pre[k] - bd.pre[k - 1]);
+        g.lmin = (g.lo <= g.hi) ? uni(tb.minwinR[(size_t)c * N + g.lo]) : 0;
         if (t == 1) {
             g.tau = 0;
             g.prev = nullptr;
             g.plo = 1;
             g.phi = 0;
         } else {
-            g.tau = link_tau(tb, r, c, chain[k]);
+            g.tau = link_tau(tb, r, c, uni(chain[k]));
             g.prev = Gprev;
-            g.plo = bd.glo[t - 1];
-            g.phi = bd.ghi[t - 1];
+            g.plo = uni(bd.glo[t - 1]);
+            g.phi = uni(bd.ghi[t - 1]);
         }
-        row_pass(g, sm.ps, lane, N, Gcur, nullptr, nullptr, 1, 0, 0, false, false);
+        row_pass(g, store_to(Gcur, nullptr), sm.ps, lane, N);
         const int mu = m - t;
-        Row rw = fwd_rowdesc(tb, bd, sm, r, chain, mu, mu);
+        const Row rw = fwd_rowdesc(tb, bd, sm, r, chain, mu, mu);
         if (rw.cap > 0) {
-            const uint64_t v = row_pass(rw, sm.ps, lane, N, nullptr, nullptr, Gcur, bd.glo[t],
-                                        bd.ghi[t], link_tau(tb, r, chain[mu - 1], chain[mu]),
-                                        true, false);
-            if (v != E2_INF64 && v <= best) {  // descending mu: ties go to the smaller mu
-                best = v;
-                best_mu = mu;
-            }
+            RowOut ro = store_to(nullptr, nullptr);
+            ro.combine = true;
+            ro.G = Gcur;
+            ro.glo = g.lo;
+            ro.ghi = g.hi;
+            ro.tau_next = link_tau(tb, r, uni(chain[mu - 1]), uni(chain[mu]));
+            ro.mu = mu;
+            acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
         }
         uint64_t *tmp = Gprev;
         Gprev = Gcur;
         Gcur = tmp;
     }
+    const uint64_t key = wave_min_u64(acc);
+    const uint64_t best = unpack_val(key);
+    const int best_mu = best == E2_INF64 ? 0 : (int)(key & 0xFF);
     *T_out = best;
     *mu_out = best_mu;
     if (best == E2_INF64) return true;
 
     // rows mu*..m-1 of the chosen master's table overwrite F in the pool
     for (int k = best_mu; k < m; ++k) {
-        const Row rw = fwd_rowdesc(tb, bd, sm, r, chain, k, best_mu);
-        row_pass(rw, sm.ps, lane, N, sm.pool + bd.off[k], sm.tbp + bd.off[k], nullptr, 1, 0, 0,
-                 false, false);
+        const int off = uni(bd.off[k]);
+        row_pass(fwd_rowdesc(tb, bd, sm, r, chain, k, best_mu),
+                 store_to(sm.pool + off, sm.tbp + off), sm.ps, lane, N);
     }
     if (m >= 2) {
         // cell N-1 of row m: split point of the last stage
         Row rw = fwd_rowdesc(tb, bd, sm, r, chain, m, best_mu);
         rw.lo = rw.hi = N - 1;
-        rw.lmin = tb.minwin[((size_t)(best_mu == m) * tb.M + chain[m - 1]) * N + (N - 1)];
-        uint64_t *dummy = sm.Gb;  // the reversed rows are no longer needed
-        row_pass(rw, sm.ps, lane, N, dummy, &bd.last_tb, nullptr, 1, 0, 0, false, false);
+        rw.lmin = uni(tb.minwin[((size_t)(best_mu == m) * tb.M + uni(chain[m - 1])) * N + (N - 1)]);
+        row_pass(rw, store_to(sm.Gb, &bd.last_tb), sm.ps, lane, N);  // Gb is free by now
         if (lane == 0) {
             int i = N - 1;
             int j = bd.last_tb;
@@ -630,31 +662,30 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
     const int N = tb.N;
     uint64_t *cur = sm.Ga, *prv = sm.Gb;
     for (int k = 1; k <= m; ++k) {
-        const int c = chain[k - 1];
+        const int c = uni(chain[k - 1]);
         const int f = (mu == k);
         Row rw;
         rw.pr = pref_row(tb, r, c);
         rw.wr = win_row(tb, f, c);
-        rw.hadd = f ? tb.head[r * tb.M + c] : 0;
+        rw.hadd = f ? uni64(tb.head[r * tb.M + c]) : 0;
         rw.lo = k - 1;
         rw.hi = N - 1;
         rw.kmin = k - 1;
         rw.cap = N;
-        rw.lmin = tb.minwin[((size_t)f * tb.M + c) * N + rw.lo];
+        rw.lmin = uni(tb.minwin[((size_t)f * tb.M + c) * N + rw.lo]);
         if (k == 1) {
             rw.tau = 0;
             rw.prev = nullptr;
             rw.plo = 1;
             rw.phi = 0;
         } else {
-            rw.tau = link_tau(tb, r, chain[k - 2], c);
+            rw.tau = link_tau(tb, r, uni(chain[k - 2]), c);
             rw.prev = prv;
             rw.plo = k - 2;
             rw.phi = N - 1;
         }
-        row_pass(rw, sm.ps, lane, N, cur, (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1)
-                                                           : nullptr,
-                 nullptr, 1, 0, 0, false, false);
+        row_pass(rw, store_to(cur, (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1) : nullptr),
+                 sm.ps, lane, N);
         uint64_t *tmp = prv;
         prv = cur;
         cur = tmp;
