@@ -295,7 +295,12 @@ __device__ __forceinline__ const uint8_t *win_row(const E2Tables &tb, int f, int
 }
 __device__ __forceinline__ uint64_t link_tau(const E2Tables &tb, int r, int a, int b)
 {
-    return uni64(tb.tau[((size_t)r * tb.M + a) * tb.M + b]);
+    return tb.tau[((size_t)r * tb.M + a) * tb.M + b];
+}
+// same, for wave-uniform device ids (the result goes to scalar registers)
+__device__ __forceinline__ uint64_t link_tau_u(const E2Tables &tb, int r, int a, int b)
+{
+    return uni64(link_tau(tb, r, a, b));
 }
 __device__ __forceinline__ uint64_t pack_prev(uint64_t prev, uint64_t tau, int j)
 {
@@ -503,7 +508,7 @@ __device__ Row fwd_rowdesc(const E2Tables &tb, const Bands &bd, const DpSmem &sm
         rw.plo = 1;
         rw.phi = 0;
     } else {
-        rw.tau = link_tau(tb, r, uni(chain[k - 2]), c);
+        rw.tau = link_tau_u(tb, r, uni(chain[k - 2]), c);
         rw.prev = sm.pool + uni(bd.off[k - 1]);
         rw.plo = uni(bd.flo[k - 1]);
         rw.phi = uni(bd.fhi[k - 1]);
@@ -590,7 +595,7 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
             g.plo = 1;
             g.phi = 0;
         } else {
-            g.tau = link_tau(tb, r, c, uni(chain[k]));
+            g.tau = link_tau_u(tb, r, c, uni(chain[k]));
             g.prev = Gprev;
             g.plo = uni(bd.glo[t - 1]);
             g.phi = uni(bd.ghi[t - 1]);
@@ -604,7 +609,7 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
             ro.G = Gcur;
             ro.glo = g.lo;
             ro.ghi = g.hi;
-            ro.tau_next = link_tau(tb, r, uni(chain[mu - 1]), uni(chain[mu]));
+            ro.tau_next = link_tau_u(tb, r, uni(chain[mu - 1]), uni(chain[mu]));
             ro.mu = mu;
             acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
         }
@@ -679,7 +684,7 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
             rw.plo = 1;
             rw.phi = 0;
         } else {
-            rw.tau = link_tau(tb, r, uni(chain[k - 2]), c);
+            rw.tau = link_tau_u(tb, r, uni(chain[k - 2]), c);
             rw.prev = prv;
             rw.plo = k - 2;
             rw.phi = N - 1;
