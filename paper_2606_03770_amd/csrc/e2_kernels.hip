@@ -263,8 +263,9 @@ struct Row {
 // B(i) = max(tau_next, G(N-2-i)) from the band-packed reversed row G over
 // [glo, ghi] (last_only: B = 0 at i = N-1, INF elsewhere).
 struct RowOut {
-    uint64_t *vals;
-    uint8_t *tbs;
+    uint64_t *vals;     // band-packed values (LDS), may be null in combine mode
+    uint64_t *vals_g;   // second copy of the values (global), or null
+    uint8_t *tbs;       // split points, or null
     bool combine;
     bool last_only;
     const uint64_t *G;
@@ -399,6 +400,7 @@ __device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane
         const uint64_t v = act ? unpack_val(best) : E2_INF64;
         if (!ro.combine) {
             ro.vals[i - rw.lo] = v;
+            if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
             if (ro.tbs) ro.tbs[i - rw.lo] = (uint8_t)(best & 0xFF);
         } else {
             acc = umin64(acc, combine_key(v, b, ro.mu));
@@ -416,8 +418,12 @@ __device__ uint64_t row_pass(const Row &rw, const RowOut &ro, PS *ps, int lane, 
         uint64_t acc = E2_INF64;
         for (int i = rw.lo + lane; i <= rw.hi; i += kWave) {
             const uint64_t v = (rw.wr[i] == 0) ? rw.pr[i + 1] + rw.hadd : E2_INF64;
-            if (!ro.combine) ro.vals[i - rw.lo] = v;
-            else acc = umin64(acc, combine_key(v, combine_b(i, N, ro), ro.mu));
+            if (!ro.combine) {
+                ro.vals[i - rw.lo] = v;
+                if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
+            } else {
+                acc = umin64(acc, combine_key(v, combine_b(i, N, ro), ro.mu));
+            }
         }
         __syncthreads();
         return acc;
@@ -432,10 +438,11 @@ __device__ uint64_t row_pass(const Row &rw, const RowOut &ro, PS *ps, int lane, 
     return row_pass_s<1>(rw, ro, ps, lane, N);
 }
 
-__device__ __forceinline__ RowOut store_to(uint64_t *vals, uint8_t *tbs)
+__device__ __forceinline__ RowOut store_to(uint64_t *vals, uint64_t *vals_g, uint8_t *tbs)
 {
     RowOut ro;
     ro.vals = vals;
+    ro.vals_g = vals_g;
     ro.tbs = tbs;
     ro.combine = false;
     ro.last_only = false;
@@ -458,7 +465,8 @@ __device__ __forceinline__ RowOut store_to(uint64_t *vals, uint8_t *tbs)
 // of the previous row or an infinite one, so computing only in-band cells
 // (others INF) leaves every in-band value and split point exact.
 //
-//   F_k  forward rows without master, k = 1..m-1 (pool, with split points)
+//   F_k  forward rows without master, k = 1..m-1 (values kept for the
+//        combines, split points in LDS)
 //   G_k  backward rows without master: blocks j..N-1 on devices k..m with
 //        links k..m, computed as forward rows over reversed blocks
 //   T_mu = min_i max( min_j max(F_{mu-1}(j-1), tau(mu-1, mu), cost_mu(j, i)
@@ -468,154 +476,188 @@ __device__ __forceinline__ RowOut store_to(uint64_t *vals, uint8_t *tbs)
 //   minimum of (T_mu << 8 | mu) gives the best T and the smallest master
 //   attaining it; rows mu*..m of its table (rows below mu* are F) give the
 //   split points for the back tracing.
-// Returns false (nothing decided) if the forward bands do not fit the pool.
+//
+// The per-position data of a chain (device, capacities, links, head time,
+// bands, pool offsets, window-length bounds) is loaded once, one position
+// per lane (m <= 64), and each row reads its scalars with readlane.  The
+// previous row of every sweep sits in an LDS ping-pong pair; forward rows
+// are also written to a per-wave global pool for the combines.
 // ---------------------------------------------------------------------------
-struct Bands {
-    uint8_t flo[256], fhi[256];  // forward band per row 1..m
-    uint8_t glo[256], ghi[256];  // reversed band per reversed row t = 1..m-1
-    uint16_t off[257];           // pool offset per forward row 1..m-1
-    uint16_t pre[257];           // prefix sums of cap0 over the chain
-    uint8_t cH[256];             // capH per chain position (1-based)
-    uint8_t last_tb;
+constexpr int kMaxBandedChain = kWave;
+
+struct ChainRegs {          // lane k-1 holds chain position k (1-based)
+    int dev, cap0, capH;
+    uint64_t tau;           // link from position k-1 (k >= 2)
+    uint64_t head;          // head time of the device
+    int flo, fhi, off;      // forward band and pool offset of row k
+    int lmin0, lmin1;       // window-length bounds of row k (no head / head)
+    int devR, capR;         // reversed row t = k: device of position m+1-k, its cap0
+    int glo, ghi;           // reversed band of reversed row t = k
+    int lminR;              // window-length bound of reversed row t = k
+    uint64_t tauR;          // link of reversed row t = k: position m+1-k -> m+2-k
 };
+
+__device__ __forceinline__ int lane_i(int v, int k) { return __builtin_amdgcn_readlane(v, k); }
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int k) { return readlane_u64(v, k); }
+
+__device__ __forceinline__ int scan_incl_i32(int x, int lane)
+{
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int y = __shfl_up(x, d, kWave);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
 
 struct DpSmem {
     PS *ps;          // split-point pairs, N entries (LDS)
-    uint64_t *Ga;    // reversed row (ping), band-packed (global, per wave)
-    uint64_t *Gb;    // reversed row (pong)
-    uint64_t *pool;  // band-packed forward rows (global, per wave)
-    uint8_t *tbp;    // their split points (LDS)
+    uint64_t *Rw0;   // LDS row ping-pong, N+1 entries each
+    uint64_t *Rw1;
+    uint8_t *tbp;    // split points of the forward rows, band-packed (LDS)
+    uint64_t *pool;  // band-packed forward row values (global, per wave)
+    uint64_t *Ga;    // full rows of the reference path (global, per wave)
+    uint64_t *Gb;
     int pool_cells;
 };
 
-__device__ Row fwd_rowdesc(const E2Tables &tb, const Bands &bd, const DpSmem &sm, int r,
-                           const uint8_t *chain, int k, int mu)
+// Row k (1-based) of the table for master mu (mu = 0: no master) as a
+// forward row; prev / plo / phi are filled in by the caller.
+__device__ __forceinline__ Row fwd_row_of(const E2Tables &tb, const ChainRegs &cr, int r, int k,
+                                          int mu)
 {
-    const int c = uni(chain[k - 1]);
     const int f = (mu == k);
+    const int c = lane_i(cr.dev, k - 1);
     Row rw;
     rw.pr = pref_row(tb, r, c);
     rw.wr = win_row(tb, f, c);
-    rw.hadd = f ? uni64(tb.head[r * tb.M + c]) : 0;
-    rw.lo = uni(bd.flo[k]);
-    rw.hi = uni(bd.fhi[k]);
+    rw.hadd = f ? lane_u64(cr.head, k - 1) : 0;
+    rw.tau = (k >= 2) ? lane_u64(cr.tau, k - 1) : 0;
+    rw.lo = lane_i(cr.flo, k - 1);
+    rw.hi = lane_i(cr.fhi, k - 1);
     rw.kmin = k - 1;
-    rw.cap = f ? uni(bd.cH[k]) : uni(bd.pre[k] - bd.pre[k - 1]);
-    rw.lmin = (rw.lo <= rw.hi) ? uni(tb.minwin[((size_t)f * tb.M + c) * tb.N + rw.lo]) : 0;
-    if (k == 1) {
-        rw.tau = 0;
-        rw.prev = nullptr;
-        rw.plo = 1;
-        rw.phi = 0;
-    } else {
-        rw.tau = link_tau_u(tb, r, uni(chain[k - 2]), c);
-        rw.prev = sm.pool + uni(bd.off[k - 1]);
-        rw.plo = uni(bd.flo[k - 1]);
-        rw.phi = uni(bd.fhi[k - 1]);
-    }
+    rw.cap = f ? lane_i(cr.capH, k - 1) : lane_i(cr.cap0, k - 1);
+    rw.lmin = f ? lane_i(cr.lmin1, k - 1) : lane_i(cr.lmin0, k - 1);
+    rw.prev = nullptr;
+    rw.plo = 1;
+    rw.phi = 0;
     return rw;
 }
 
-__device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r,
-                          const uint8_t *chain, int m, int lane, uint64_t *T_out, int *mu_out,
-                          uint8_t *start)
+__device__ __forceinline__ void set_prev(Row &rw, const uint64_t *prev, int plo, int phi)
 {
-    const int N = tb.N;
-    if (lane == 0) {
-        bd.pre[0] = 0;
-        for (int k = 1; k <= m; ++k) {
-            bd.pre[k] = bd.pre[k - 1] + tb.cap0[chain[k - 1]];
-            bd.cH[k] = tb.capH[chain[k - 1]];
-        }
-        const int tot = bd.pre[m];
-        int off = 0;
-        for (int k = 1; k <= m; ++k) {
-            int lo = N - 1 - (tot - bd.pre[k]);
-            if (lo < k - 1) lo = k - 1;
-            int hi = bd.pre[k] - 1;
-            if (hi > N - 1 - (m - k)) hi = N - 1 - (m - k);
-            if (hi < lo) { lo = 1; hi = 0; }
-            bd.flo[k] = (uint8_t)lo;
-            bd.fhi[k] = (uint8_t)hi;
-            bd.off[k] = (uint16_t)off;
-            if (k < m) off += hi - lo + 1;
-        }
-        bd.off[m] = (uint16_t)(off > 65535 ? 65535 : off);
-        // reversed row t covers devices m..m+1-t (original k = m+1-t): blocks
-        // j..N-1 with max(k-1, N-(tot-pre[k-1])) <= j <= min(N-(m-k+1), pre[k-1]),
-        // i.e. reversed cells x = N-1-j
-        for (int t = 1; t < m; ++t) {
-            const int k = m + 1 - t;
-            int gl = N - (tot - bd.pre[k - 1]);
-            if (gl < k - 1) gl = k - 1;
-            int gh = bd.pre[k - 1];
-            if (gh > N - (m - k + 1)) gh = N - (m - k + 1);
-            if (gh < gl) { bd.glo[t] = 1; bd.ghi[t] = 0; }
-            else { bd.glo[t] = (uint8_t)(N - 1 - gh); bd.ghi[t] = (uint8_t)(N - 1 - gl); }
-        }
-    }
-    __syncthreads();
-    if (uni(bd.off[m]) > sm.pool_cells) return false;
+    rw.prev = prev;
+    rw.plo = plo;
+    rw.phi = phi;
+}
 
-    // forward rows F_1..F_{m-1}
-    for (int k = 1; k < m; ++k) {
-        const int off = uni(bd.off[k]);
-        row_pass(fwd_rowdesc(tb, bd, sm, r, chain, k, 0), store_to(sm.pool + off, sm.tbp + off),
-                 sm.ps, lane, N);
+__device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
+                          int m, int lane, uint64_t *T_out, int *mu_out, uint8_t *start,
+                          uint8_t *last_tb)
+{
+    const int N = tb.N, M = tb.M;
+    if (m > kMaxBandedChain) return false;
+    // ---- per-position table, one position per lane
+    ChainRegs cr;
+    const bool valid = lane < m;
+    const int k1 = lane + 1;
+    cr.dev = valid ? chain[lane] : 0;
+    cr.cap0 = valid ? tb.cap0[cr.dev] : 0;
+    cr.capH = valid ? tb.capH[cr.dev] : 0;
+    cr.head = valid ? tb.head[r * M + cr.dev] : 0;
+    cr.tau = (valid && lane >= 1) ? link_tau(tb, r, chain[lane - 1], cr.dev) : 0;
+    const int pre = scan_incl_i32(cr.cap0, lane);
+    const int tot = lane_i(pre, m - 1);
+    int lo = max(k1 - 1, N - 1 - (tot - pre));
+    int hi = min(N - 1 - (m - k1), pre - 1);
+    if (hi < lo) { lo = 1; hi = 0; }
+    cr.flo = lo;
+    cr.fhi = hi;
+    const int size = (valid && k1 < m) ? hi - lo + 1 : 0;
+    const int size_incl = scan_incl_i32(size, lane);
+    cr.off = size_incl - size;
+    const int pool_need = lane_i(size_incl, kWave - 1);
+    cr.lmin0 = (valid && lo <= hi) ? tb.minwin[(size_t)cr.dev * N + lo] : 0;
+    cr.lmin1 = (valid && lo <= hi) ? tb.minwin[((size_t)M + cr.dev) * N + lo] : 0;
+    // reversed row t = k1 covers original position kk = m+1-t: blocks j..N-1
+    // with max(kk-1, N-(tot-pre[kk-1])) <= j <= min(N-(m-kk+1), pre[kk-1]),
+    // i.e. reversed cells x = N-1-j
+    const int kk = m + 1 - k1;
+    const int src = max(0, min(kWave - 1, kk - 1));
+    cr.devR = __shfl(cr.dev, src, kWave);
+    cr.capR = __shfl(cr.cap0, src, kWave);
+    const int pre_km1 = (kk >= 2) ? __shfl(pre, max(0, kk - 2), kWave) : 0;
+    cr.tauR = __shfl(cr.tau, max(0, min(kWave - 1, kk)), kWave);  // link kk -> kk+1
+    {
+        const bool vr = k1 < m;
+        int gl = max(kk - 1, N - (tot - pre_km1));
+        int gh = min(pre_km1, N - (m - kk + 1));
+        if (!vr || gh < gl) { cr.glo = 1; cr.ghi = 0; }
+        else { cr.glo = N - 1 - gh; cr.ghi = N - 1 - gl; }
+        cr.lminR = (vr && cr.glo <= cr.ghi) ? tb.minwinR[(size_t)cr.devR * N + cr.glo] : 0;
     }
-    // combines: master mu = m (stage ends at block N-1), then, after each
-    // reversed row t = 1..m-1 (original backward row k = m+1-t), master m - t
+    if (pool_need > sm.pool_cells) return false;
+
+    uint64_t *Rw[2] = {sm.Rw0, sm.Rw1};
+    // ---- forward rows F_1..F_{m-1}: LDS ping-pong + global pool + split points
+    for (int k = 1; k < m; ++k) {
+        Row rw = fwd_row_of(tb, cr, r, k, 0);
+        if (k >= 2) set_prev(rw, Rw[(k - 1) & 1], lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
+        const int off = lane_i(cr.off, k - 1);
+        row_pass(rw, store_to(Rw[k & 1], sm.pool + off, sm.tbp + off), sm.ps, lane, N);
+    }
+    // the combines read the forward rows back from the pool
+    __builtin_amdgcn_s_waitcnt(0);
+    __threadfence_block();
+
+    // ---- combines: master m (its stage ends at N-1), then, after each
+    // reversed row t = 1..m-1 (backward row m+1-t), master m - t
     uint64_t acc = E2_INF64;
     {
-        const Row rw = fwd_rowdesc(tb, bd, sm, r, chain, m, m);
+        Row rw = fwd_row_of(tb, cr, r, m, m);
         if (rw.cap > 0) {
-            RowOut ro = store_to(nullptr, nullptr);
+            if (m >= 2)
+                set_prev(rw, sm.pool + lane_i(cr.off, m - 2), lane_i(cr.flo, m - 2),
+                         lane_i(cr.fhi, m - 2));
+            RowOut ro = store_to(nullptr, nullptr, nullptr);
             ro.combine = true;
             ro.last_only = true;
             ro.mu = m;
             acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
         }
     }
-    uint64_t *Gprev = sm.Gb, *Gcur = sm.Ga;
     for (int t = 1; t < m; ++t) {
-        const int k = m + 1 - t;  // device of this backward row
-        const int c = uni(chain[k - 1]);
+        const int c = lane_i(cr.devR, t - 1);
         Row g;
         g.pr = prefR_row(tb, r, c);
         g.wr = tb.winR + (size_t)c * N;
         g.hadd = 0;
-        g.lo = uni(bd.glo[t]);
-        g.hi = uni(bd.ghi[t]);
+        g.tau = (t >= 2) ? lane_u64(cr.tauR, t - 1) : 0;
+        g.lo = lane_i(cr.glo, t - 1);
+        g.hi = lane_i(cr.ghi, t - 1);
         g.kmin = t - 1;
-        g.cap = uni(bd.pre[k] - bd.pre[k - 1]);
-        g.lmin = (g.lo <= g.hi) ? uni(tb.minwinR[(size_t)c * N + g.lo]) : 0;
-        if (t == 1) {
-            g.tau = 0;
-            g.prev = nullptr;
-            g.plo = 1;
-            g.phi = 0;
-        } else {
-            g.tau = link_tau_u(tb, r, c, uni(chain[k]));
-            g.prev = Gprev;
-            g.plo = uni(bd.glo[t - 1]);
-            g.phi = uni(bd.ghi[t - 1]);
-        }
-        row_pass(g, store_to(Gcur, nullptr), sm.ps, lane, N);
+        g.cap = lane_i(cr.capR, t - 1);
+        g.lmin = lane_i(cr.lminR, t - 1);
+        g.prev = nullptr;
+        g.plo = 1;
+        g.phi = 0;
+        if (t >= 2) set_prev(g, Rw[(t - 1) & 1], lane_i(cr.glo, t - 2), lane_i(cr.ghi, t - 2));
+        uint64_t *Gt = Rw[t & 1];
+        row_pass(g, store_to(Gt, nullptr, nullptr), sm.ps, lane, N);
         const int mu = m - t;
-        const Row rw = fwd_rowdesc(tb, bd, sm, r, chain, mu, mu);
+        Row rw = fwd_row_of(tb, cr, r, mu, mu);
         if (rw.cap > 0) {
-            RowOut ro = store_to(nullptr, nullptr);
+            if (mu >= 2)
+                set_prev(rw, sm.pool + lane_i(cr.off, mu - 2), lane_i(cr.flo, mu - 2),
+                         lane_i(cr.fhi, mu - 2));
+            RowOut ro = store_to(nullptr, nullptr, nullptr);
             ro.combine = true;
-            ro.G = Gcur;
+            ro.G = Gt;
             ro.glo = g.lo;
             ro.ghi = g.hi;
-            ro.tau_next = link_tau_u(tb, r, uni(chain[mu - 1]), uni(chain[mu]));
+            ro.tau_next = lane_u64(cr.tau, mu);  // link mu -> mu+1
             ro.mu = mu;
             acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
         }
-        uint64_t *tmp = Gprev;
-        Gprev = Gcur;
-        Gcur = tmp;
     }
     const uint64_t key = wave_min_u64(acc);
     const uint64_t best = unpack_val(key);
@@ -624,29 +666,39 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, Bands &bd, int r
     *mu_out = best_mu;
     if (best == E2_INF64) return true;
 
-    // rows mu*..m-1 of the chosen master's table overwrite F in the pool
+    // ---- rows mu*..m-1 of the chosen master's table (split points overwrite
+    // those of F), then cell N-1 of row m
     for (int k = best_mu; k < m; ++k) {
-        const int off = uni(bd.off[k]);
-        row_pass(fwd_rowdesc(tb, bd, sm, r, chain, k, best_mu),
-                 store_to(sm.pool + off, sm.tbp + off), sm.ps, lane, N);
+        Row rw = fwd_row_of(tb, cr, r, k, best_mu);
+        if (k >= 2) {
+            const uint64_t *prev = (k == best_mu) ? sm.pool + lane_i(cr.off, k - 2)
+                                                  : Rw[(k - 1) & 1];
+            set_prev(rw, prev, lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
+        }
+        const int off = lane_i(cr.off, k - 1);
+        row_pass(rw, store_to(Rw[k & 1], nullptr, sm.tbp + off), sm.ps, lane, N);
     }
     if (m >= 2) {
-        // cell N-1 of row m: split point of the last stage
-        Row rw = fwd_rowdesc(tb, bd, sm, r, chain, m, best_mu);
+        Row rw = fwd_row_of(tb, cr, r, m, best_mu);
+        const uint64_t *prev = (best_mu == m) ? sm.pool + lane_i(cr.off, m - 2)
+                                              : Rw[(m - 1) & 1];
+        set_prev(rw, prev, lane_i(cr.flo, m - 2), lane_i(cr.fhi, m - 2));
         rw.lo = rw.hi = N - 1;
-        rw.lmin = uni(tb.minwin[((size_t)(best_mu == m) * tb.M + uni(chain[m - 1])) * N + (N - 1)]);
-        row_pass(rw, store_to(sm.Gb, &bd.last_tb), sm.ps, lane, N);  // Gb is free by now
+        rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + lane_i(cr.dev, m - 1)) * N + (N - 1)];
+        rw.lmin = uni(rw.lmin);
+        row_pass(rw, store_to(Rw[m & 1], nullptr, last_tb), sm.ps, lane, N);
         if (lane == 0) {
             int i = N - 1;
-            int j = bd.last_tb;
+            int j = *last_tb;
             if (j > i) j = i;
             start[m - 1] = (uint8_t)j;
             i = j - 1;
             for (int k = m - 1; k >= 2; --k) {
+                const int blo = lane_i(cr.flo, k - 1), bhi = lane_i(cr.fhi, k - 1);
                 // path cells lie in their band; the clamp only keeps a
                 // corrupted table from indexing outside its row
-                const int ii = i < bd.flo[k] ? bd.flo[k] : (i > bd.fhi[k] ? bd.fhi[k] : i);
-                j = sm.tbp[bd.off[k] + (ii - bd.flo[k])];
+                const int ii = i < blo ? blo : (i > bhi ? bhi : i);
+                j = sm.tbp[lane_i(cr.off, k - 1) + (ii - blo)];
                 if (j > i) j = i;
                 start[k - 1] = (uint8_t)j;
                 i = j - 1;
@@ -689,7 +741,9 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
             rw.plo = k - 2;
             rw.phi = N - 1;
         }
-        row_pass(rw, store_to(cur, (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1) : nullptr),
+        row_pass(rw,
+                 store_to(cur, nullptr, (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1)
+                                                        : nullptr),
                  sm.ps, lane, N);
         uint64_t *tmp = prv;
         prv = cur;
@@ -714,15 +768,17 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
                                            uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
     extern __shared__ uint64_t dyn[];
-    __shared__ Bands bd;
     __shared__ uint8_t chain[256];
     __shared__ uint8_t start[256];
+    __shared__ uint8_t last_tb;
     __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
     DpSmem sm;
     sm.ps = reinterpret_cast<PS *>(dyn);
-    sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N);
+    sm.Rw0 = dyn + 2 * N;
+    sm.Rw1 = sm.Rw0 + (N + 1);
+    sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
     uint64_t *my_rows = rows + (size_t)blockIdx.x * ((size_t)pool_cells + 2 * (N + 1));
     sm.pool = my_rows;
     sm.Ga = my_rows + pool_cells;
@@ -762,7 +818,7 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
 
         uint64_t best = E2_INF64;
         int best_mu = 0;
-        if (!dp_banded(tb, sm, bd, r, chain, m, lane, &best, &best_mu, start)) {
+        if (!dp_banded(tb, sm, r, chain, m, lane, &best, &best_mu, start, &last_tb)) {
             // reference path: a full table per master, then the chosen
             // master's table again with split points
             for (int mu = 1; mu <= m; ++mu) {
@@ -991,7 +1047,7 @@ size_t e2_dp_row_words(int N) { return (size_t)e2_dp_pool_cells(N) + 2 * (size_t
 
 size_t e2_dp_lds_bytes(int N)
 {
-    return (size_t)16 * N + (size_t)e2_dp_pool_cells(N);
+    return (size_t)16 * N + (size_t)16 * (N + 1) + (size_t)e2_dp_pool_cells(N);
 }
 
 int e2_dp_slots(int problems)
