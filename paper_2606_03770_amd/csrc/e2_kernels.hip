@@ -643,22 +643,27 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
     }
     if (pool_need > sm.pool_cells) return false;
 
-    // LDS row ping-pong: row k of a sweep goes to rw_buf(k)
-    auto rw_buf = [&](int k) { return (k & 1) ? sm.Rw1 : sm.Rw0; };
+    uint64_t *Rw[2] = {sm.Rw0, sm.Rw1};
     // ---- forward rows F_1..F_{m-1}: LDS ping-pong + global pool + split points
     auto f_row = [&](int k) {
         Row rw = fwd_row_of(tb, cr, r, k, 0);
-        if (k >= 2) set_prev(rw, rw_buf(k - 1), lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
+        if (k >= 2) set_prev(rw, Rw[(k - 1) & 1], lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
         return rw;
     };
     if (m >= 2) {
-        Pre pcur = row_prefetch(f_row(1), false, lane);
+        Row cur = f_row(1);
+        Pre pcur = row_prefetch(cur, false, lane);
         for (int k = 1; k < m; ++k) {
-            // the next row's loads go out before this row is computed
-            const Pre pnxt = (k + 1 < m) ? row_prefetch(f_row(k + 1), false, lane) : pcur;
+            Row nxt = cur;
+            Pre pnxt = pcur;
+            if (k + 1 < m) {
+                nxt = f_row(k + 1);
+                pnxt = row_prefetch(nxt, false, lane);
+            }
             const int off = lane_i(cr.off, k - 1);
-            row_pass(f_row(k), store_to(rw_buf(k), sm.pool + off, sm.tbp + off), pcur, false,
-                     sm.ps, lane, N);
+            row_pass(cur, store_to(Rw[k & 1], sm.pool + off, sm.tbp + off), pcur, false, sm.ps,
+                     lane, N);
+            cur = nxt;
             pcur = pnxt;
         }
     }
@@ -694,8 +699,8 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
             x.rw.plo = 1;
             x.rw.phi = 0;
             if (t >= 2)
-                set_prev(x.rw, rw_buf(t - 1), lane_i(cr.glo, t - 2), lane_i(cr.ghi, t - 2));
-            x.ro = store_to(rw_buf(t), nullptr, nullptr);
+                set_prev(x.rw, Rw[(t - 1) & 1], lane_i(cr.glo, t - 2), lane_i(cr.ghi, t - 2));
+            x.ro = store_to(Rw[t & 1], nullptr, nullptr);
             x.pglob = false;
             x.skip = false;
         } else {
@@ -711,7 +716,7 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
             if (t == 0) {
                 x.ro.last_only = true;
             } else {
-                x.ro.G = rw_buf(t);
+                x.ro.G = Rw[t & 1];
                 x.ro.glo = lane_i(cr.glo, t - 1);
                 x.ro.ghi = lane_i(cr.ghi, t - 1);
                 x.ro.tau_next = lane_u64(cr.tau, mu);  // link mu -> mu+1
@@ -724,19 +729,21 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
     uint64_t acc = E2_INF64;
     {
         const int nsteps = 2 * m - 1;
-        auto b_pre = [&](int st) {
-            const Step x = b_step(st);
-            return x.skip ? Pre{0, E2_INF64, 0, (int)E2_NO_START}
-                          : row_prefetch(x.rw, x.pglob, lane);
-        };
-        Pre pcur = b_pre(0);
+        Step cur = b_step(0);
+        Pre pcur = cur.skip ? Pre{0, E2_INF64, 0, (int)E2_NO_START}
+                            : row_prefetch(cur.rw, cur.pglob, lane);
         for (int st = 0; st < nsteps; ++st) {
-            const Pre pnxt = (st + 1 < nsteps) ? b_pre(st + 1) : pcur;
-            const Step cur = b_step(st);
+            Step nxt = cur;
+            Pre pnxt = pcur;
+            if (st + 1 < nsteps) {
+                nxt = b_step(st + 1);
+                if (!nxt.skip) pnxt = row_prefetch(nxt.rw, nxt.pglob, lane);
+            }
             if (!cur.skip) {
                 const uint64_t v = row_pass(cur.rw, cur.ro, pcur, cur.pglob, sm.ps, lane, N);
                 if (cur.ro.combine) acc = umin64(acc, v);
             }
+            cur = nxt;
             pcur = pnxt;
         }
     }
@@ -753,7 +760,7 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
         Row rw = fwd_row_of(tb, cr, r, k, best_mu);
         if (k >= 2) {
             const uint64_t *prev = (k == best_mu) ? sm.pool + lane_i(cr.off, k - 2)
-                                                  : rw_buf(k - 1);
+                                                  : Rw[(k - 1) & 1];
             set_prev(rw, prev, lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
         }
         if (k == m) {
@@ -764,18 +771,24 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
         return rw;
     };
     if (m >= 2) {
-        Pre pcur = row_prefetch(p_row(best_mu), best_mu >= 2, lane);
+        Row cur = p_row(best_mu);
+        Pre pcur = row_prefetch(cur, best_mu >= 2, lane);
         for (int k = best_mu; k <= m; ++k) {
-            const Pre pnxt = (k + 1 <= m) ? row_prefetch(p_row(k + 1), false, lane) : pcur;
-            const bool pg = (k == best_mu) && k >= 2;
+            Row nxt = cur;
+            Pre pnxt = pcur;
+            if (k + 1 <= m) {
+                nxt = p_row(k + 1);
+                pnxt = row_prefetch(nxt, k + 1 == best_mu, lane);
+            }
             if (k < m) {
                 const int off = lane_i(cr.off, k - 1);
-                row_pass(p_row(k), store_to(rw_buf(k), nullptr, sm.tbp + off), pcur, pg, sm.ps,
-                         lane, N);
+                row_pass(cur, store_to(Rw[k & 1], nullptr, sm.tbp + off), pcur, k == best_mu && k >= 2,
+                         sm.ps, lane, N);
             } else {
-                row_pass(p_row(k), store_to(rw_buf(m), nullptr, last_tb), pcur, pg, sm.ps, lane,
-                         N);
+                row_pass(cur, store_to(Rw[m & 1], nullptr, last_tb), pcur, best_mu == m, sm.ps,
+                         lane, N);
             }
+            cur = nxt;
             pcur = pnxt;
         }
         if (lane == 0) {
