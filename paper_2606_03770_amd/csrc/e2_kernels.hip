@@ -350,63 +350,28 @@ __device__ __forceinline__ uint64_t scan_cell(const PS *ps, int i, int jlo, int 
     return best;
 }
 
-// First-pass global loads of a row, issued ahead of time (one row of
-// lookahead in every sweep).  pv is used only when the previous row lives in
-// global memory (written long before); an LDS previous row is read in place.
-struct Pre {
-    uint64_t pj;  // pr[jmin + lane]
-    uint64_t pv;  // prev(jmin + lane - 1) or INF
-    uint64_t pi;  // pr[i0 + 1] with i0 = lo + lane / S (first device: lo + lane)
-    int w;        // wr[i0]
-};
-
-__device__ __forceinline__ int row_S(int n) { return n <= 16 ? 4 : (n <= 32 ? 2 : 1); }
-
-__device__ __forceinline__ Pre row_prefetch(const Row &rw, bool prev_global, int lane)
-{
-    Pre pf;
-    pf.pj = 0;
-    pf.pv = E2_INF64;
-    pf.pi = 0;
-    pf.w = E2_NO_START;
-    const int n = rw.hi - rw.lo + 1;
-    if (n <= 0) return pf;
-    int i = rw.lo + lane;
-    if (rw.prev != nullptr) {
-        const int jmin = max(rw.kmin, rw.lo - rw.cap + 1);
-        const int j = jmin + lane;
-        if (j <= rw.hi) {
-            pf.pj = rw.pr[j];
-            const int pj = j - 1;
-            if (prev_global && pj >= rw.plo && pj <= rw.phi) pf.pv = rw.prev[pj - rw.plo];
-        }
-        i = rw.lo + lane / row_S(n);
-    }
-    if (i <= rw.hi) {
-        pf.w = rw.wr[i];
-        pf.pi = rw.pr[i + 1];
-    }
-    return pf;
-}
-
 template <int S>
-__device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, const Pre &pf, bool prev_global,
-                               PS *ps, int lane, int N)
+__device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane, int N)
 {
     constexpr int CPP = kWave / S;  // cells per pass
     const int o = lane % S;
     const int cl = lane / S;
     const int jmin = max(rw.kmin, rw.lo - rw.cap + 1);
-    int w_nx = pf.w;
-    uint64_t p_nx = pf.pi, b_nx = 0;
-    if (ro.combine && rw.lo + cl <= rw.hi) b_nx = combine_b(rw.lo + cl, N, ro);
+    // first pass's cell loads go out before the split points are built
+    int w_nx = E2_NO_START;
+    uint64_t p_nx = 0, b_nx = 0;
+    {
+        const int i = rw.lo + cl;
+        if (i <= rw.hi) {
+            w_nx = rw.wr[i];
+            p_nx = rw.pr[i + 1];
+            if (ro.combine) b_nx = combine_b(i, N, ro);
+        }
+    }
     for (int j = jmin + lane; j <= rw.hi; j += kWave) {
-        const bool first = j == jmin + lane;
         const int pj = j - 1;
-        uint64_t pv;
-        if (first && prev_global) pv = pf.pv;
-        else pv = (pj >= rw.plo && pj <= rw.phi) ? rw.prev[pj - rw.plo] : E2_INF64;
-        const uint64_t pj8 = (first ? pf.pj : rw.pr[j]) << 8;
+        const uint64_t pv = (pj >= rw.plo && pj <= rw.phi) ? rw.prev[pj - rw.plo] : E2_INF64;
+        const uint64_t pj8 = rw.pr[j] << 8;
         ps[j].a = pack_prev(pv, rw.tau, j);
         ps[j].s = pj8 - (uint64_t)j;
     }
@@ -447,16 +412,12 @@ __device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, const Pre &pf, b
 
 // Store mode returns INF; combine mode returns the lane's running minimum of
 // (max(value, B) << 8 | mu) (the caller reduces over the wave once).
-__device__ uint64_t row_pass(const Row &rw, const RowOut &ro, const Pre &pf, bool prev_global,
-                             PS *ps, int lane, int N)
+__device__ uint64_t row_pass(const Row &rw, const RowOut &ro, PS *ps, int lane, int N)
 {
     if (rw.prev == nullptr) {  // first device: Eq. 2, no split point
         uint64_t acc = E2_INF64;
         for (int i = rw.lo + lane; i <= rw.hi; i += kWave) {
-            const bool first = i == rw.lo + lane;
-            const int w = first ? pf.w : rw.wr[i];
-            const uint64_t p1 = first ? pf.pi : rw.pr[i + 1];
-            const uint64_t v = (w == 0) ? p1 + rw.hadd : E2_INF64;
+            const uint64_t v = (rw.wr[i] == 0) ? rw.pr[i + 1] + rw.hadd : E2_INF64;
             if (!ro.combine) {
                 ro.vals[i - rw.lo] = v;
                 if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
@@ -472,16 +433,9 @@ __device__ uint64_t row_pass(const Row &rw, const RowOut &ro, const Pre &pf, boo
         __syncthreads();
         return E2_INF64;
     }
-    if (n <= 16) return row_pass_s<4>(rw, ro, pf, prev_global, ps, lane, N);
-    if (n <= 32) return row_pass_s<2>(rw, ro, pf, prev_global, ps, lane, N);
-    return row_pass_s<1>(rw, ro, pf, prev_global, ps, lane, N);
-}
-
-// Without lookahead (reference path).
-__device__ __forceinline__ uint64_t row_pass(const Row &rw, const RowOut &ro, PS *ps, int lane,
-                                             int N)
-{
-    return row_pass(rw, ro, row_prefetch(rw, true, lane), true, ps, lane, N);
+    if (n <= 16) return row_pass_s<4>(rw, ro, ps, lane, N);
+    if (n <= 32) return row_pass_s<2>(rw, ro, ps, lane, N);
+    return row_pass_s<1>(rw, ro, ps, lane, N);
 }
 
 __device__ __forceinline__ RowOut store_to(uint64_t *vals, uint64_t *vals_g, uint8_t *tbs)
@@ -645,106 +599,64 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
 
     uint64_t *Rw[2] = {sm.Rw0, sm.Rw1};
     // ---- forward rows F_1..F_{m-1}: LDS ping-pong + global pool + split points
-    auto f_row = [&](int k) {
+    for (int k = 1; k < m; ++k) {
         Row rw = fwd_row_of(tb, cr, r, k, 0);
         if (k >= 2) set_prev(rw, Rw[(k - 1) & 1], lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
-        return rw;
-    };
-    if (m >= 2) {
-        Row cur = f_row(1);
-        Pre pcur = row_prefetch(cur, false, lane);
-        for (int k = 1; k < m; ++k) {
-            Row nxt = cur;
-            Pre pnxt = pcur;
-            if (k + 1 < m) {
-                nxt = f_row(k + 1);
-                pnxt = row_prefetch(nxt, false, lane);
-            }
-            const int off = lane_i(cr.off, k - 1);
-            row_pass(cur, store_to(Rw[k & 1], sm.pool + off, sm.tbp + off), pcur, false, sm.ps,
-                     lane, N);
-            cur = nxt;
-            pcur = pnxt;
-        }
+        const int off = lane_i(cr.off, k - 1);
+        row_pass(rw, store_to(Rw[k & 1], sm.pool + off, sm.tbp + off), sm.ps, lane, N);
     }
     // the combines read the forward rows back from the pool
     __builtin_amdgcn_s_waitcnt(0);
     __threadfence_block();
 
-    // ---- combines and reversed rows, in the order C_m, G_1, C_{m-1}, G_2, ...,
-    // G_{m-1}, C_1: step 0 is the combine of master m (its stage ends at
-    // N-1), odd step 2t-1 the reversed row t (backward row m+1-t), even step
-    // 2t the combine of master m - t, which reads reversed row t.
-    struct Step {
-        Row rw;
-        RowOut ro;
-        bool pglob;  // previous row in the global pool
-        bool skip;   // combine of a device that cannot be master
-    };
-    auto b_step = [&](int st) {
-        Step x;
-        if (st & 1) {
-            const int t = (st + 1) / 2;
-            const int c = lane_i(cr.devR, t - 1);
-            x.rw.pr = prefR_row(tb, r, c);
-            x.rw.wr = tb.winR + (size_t)c * N;
-            x.rw.hadd = 0;
-            x.rw.tau = (t >= 2) ? lane_u64(cr.tauR, t - 1) : 0;
-            x.rw.lo = lane_i(cr.glo, t - 1);
-            x.rw.hi = lane_i(cr.ghi, t - 1);
-            x.rw.kmin = t - 1;
-            x.rw.cap = lane_i(cr.capR, t - 1);
-            x.rw.lmin = lane_i(cr.lminR, t - 1);
-            x.rw.prev = nullptr;
-            x.rw.plo = 1;
-            x.rw.phi = 0;
-            if (t >= 2)
-                set_prev(x.rw, Rw[(t - 1) & 1], lane_i(cr.glo, t - 2), lane_i(cr.ghi, t - 2));
-            x.ro = store_to(Rw[t & 1], nullptr, nullptr);
-            x.pglob = false;
-            x.skip = false;
-        } else {
-            const int t = st / 2;
-            const int mu = m - t;
-            x.rw = fwd_row_of(tb, cr, r, mu, mu);
-            if (mu >= 2)
-                set_prev(x.rw, sm.pool + lane_i(cr.off, mu - 2), lane_i(cr.flo, mu - 2),
-                         lane_i(cr.fhi, mu - 2));
-            x.ro = store_to(nullptr, nullptr, nullptr);
-            x.ro.combine = true;
-            x.ro.mu = mu;
-            if (t == 0) {
-                x.ro.last_only = true;
-            } else {
-                x.ro.G = Rw[t & 1];
-                x.ro.glo = lane_i(cr.glo, t - 1);
-                x.ro.ghi = lane_i(cr.ghi, t - 1);
-                x.ro.tau_next = lane_u64(cr.tau, mu);  // link mu -> mu+1
-            }
-            x.pglob = mu >= 2;
-            x.skip = x.rw.cap <= 0;
-        }
-        return x;
-    };
+    // ---- combines: master m (its stage ends at N-1), then, after each
+    // reversed row t = 1..m-1 (backward row m+1-t), master m - t
     uint64_t acc = E2_INF64;
     {
-        const int nsteps = 2 * m - 1;
-        Step cur = b_step(0);
-        Pre pcur = cur.skip ? Pre{0, E2_INF64, 0, (int)E2_NO_START}
-                            : row_prefetch(cur.rw, cur.pglob, lane);
-        for (int st = 0; st < nsteps; ++st) {
-            Step nxt = cur;
-            Pre pnxt = pcur;
-            if (st + 1 < nsteps) {
-                nxt = b_step(st + 1);
-                if (!nxt.skip) pnxt = row_prefetch(nxt.rw, nxt.pglob, lane);
-            }
-            if (!cur.skip) {
-                const uint64_t v = row_pass(cur.rw, cur.ro, pcur, cur.pglob, sm.ps, lane, N);
-                if (cur.ro.combine) acc = umin64(acc, v);
-            }
-            cur = nxt;
-            pcur = pnxt;
+        Row rw = fwd_row_of(tb, cr, r, m, m);
+        if (rw.cap > 0) {
+            if (m >= 2)
+                set_prev(rw, sm.pool + lane_i(cr.off, m - 2), lane_i(cr.flo, m - 2),
+                         lane_i(cr.fhi, m - 2));
+            RowOut ro = store_to(nullptr, nullptr, nullptr);
+            ro.combine = true;
+            ro.last_only = true;
+            ro.mu = m;
+            acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
+        }
+    }
+    for (int t = 1; t < m; ++t) {
+        const int c = lane_i(cr.devR, t - 1);
+        Row g;
+        g.pr = prefR_row(tb, r, c);
+        g.wr = tb.winR + (size_t)c * N;
+        g.hadd = 0;
+        g.tau = (t >= 2) ? lane_u64(cr.tauR, t - 1) : 0;
+        g.lo = lane_i(cr.glo, t - 1);
+        g.hi = lane_i(cr.ghi, t - 1);
+        g.kmin = t - 1;
+        g.cap = lane_i(cr.capR, t - 1);
+        g.lmin = lane_i(cr.lminR, t - 1);
+        g.prev = nullptr;
+        g.plo = 1;
+        g.phi = 0;
+        if (t >= 2) set_prev(g, Rw[(t - 1) & 1], lane_i(cr.glo, t - 2), lane_i(cr.ghi, t - 2));
+        uint64_t *Gt = Rw[t & 1];
+        row_pass(g, store_to(Gt, nullptr, nullptr), sm.ps, lane, N);
+        const int mu = m - t;
+        Row rw = fwd_row_of(tb, cr, r, mu, mu);
+        if (rw.cap > 0) {
+            if (mu >= 2)
+                set_prev(rw, sm.pool + lane_i(cr.off, mu - 2), lane_i(cr.flo, mu - 2),
+                         lane_i(cr.fhi, mu - 2));
+            RowOut ro = store_to(nullptr, nullptr, nullptr);
+            ro.combine = true;
+            ro.G = Gt;
+            ro.glo = g.lo;
+            ro.ghi = g.hi;
+            ro.tau_next = lane_u64(cr.tau, mu);  // link mu -> mu+1
+            ro.mu = mu;
+            acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
         }
     }
     const uint64_t key = wave_min_u64(acc);
@@ -756,41 +668,25 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
 
     // ---- rows mu*..m-1 of the chosen master's table (split points overwrite
     // those of F), then cell N-1 of row m
-    auto p_row = [&](int k) {
+    for (int k = best_mu; k < m; ++k) {
         Row rw = fwd_row_of(tb, cr, r, k, best_mu);
         if (k >= 2) {
             const uint64_t *prev = (k == best_mu) ? sm.pool + lane_i(cr.off, k - 2)
                                                   : Rw[(k - 1) & 1];
             set_prev(rw, prev, lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
         }
-        if (k == m) {
-            rw.lo = rw.hi = N - 1;
-            rw.lmin = uni(tb.minwin[((size_t)(best_mu == m) * M + lane_i(cr.dev, m - 1)) * N +
-                                    (N - 1)]);
-        }
-        return rw;
-    };
+        const int off = lane_i(cr.off, k - 1);
+        row_pass(rw, store_to(Rw[k & 1], nullptr, sm.tbp + off), sm.ps, lane, N);
+    }
     if (m >= 2) {
-        Row cur = p_row(best_mu);
-        Pre pcur = row_prefetch(cur, best_mu >= 2, lane);
-        for (int k = best_mu; k <= m; ++k) {
-            Row nxt = cur;
-            Pre pnxt = pcur;
-            if (k + 1 <= m) {
-                nxt = p_row(k + 1);
-                pnxt = row_prefetch(nxt, k + 1 == best_mu, lane);
-            }
-            if (k < m) {
-                const int off = lane_i(cr.off, k - 1);
-                row_pass(cur, store_to(Rw[k & 1], nullptr, sm.tbp + off), pcur, k == best_mu && k >= 2,
-                         sm.ps, lane, N);
-            } else {
-                row_pass(cur, store_to(Rw[m & 1], nullptr, last_tb), pcur, best_mu == m, sm.ps,
-                         lane, N);
-            }
-            cur = nxt;
-            pcur = pnxt;
-        }
+        Row rw = fwd_row_of(tb, cr, r, m, best_mu);
+        const uint64_t *prev = (best_mu == m) ? sm.pool + lane_i(cr.off, m - 2)
+                                              : Rw[(m - 1) & 1];
+        set_prev(rw, prev, lane_i(cr.flo, m - 2), lane_i(cr.fhi, m - 2));
+        rw.lo = rw.hi = N - 1;
+        rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + lane_i(cr.dev, m - 1)) * N + (N - 1)];
+        rw.lmin = uni(rw.lmin);
+        row_pass(rw, store_to(Rw[m & 1], nullptr, last_tb), sm.ps, lane, N);
         if (lane == 0) {
             int i = N - 1;
             int j = *last_tb;
