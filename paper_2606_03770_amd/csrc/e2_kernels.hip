@@ -759,7 +759,7 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
 // of the forward-row pool; the row values live in a per-wave global region
 // (pool_cells + 2 (N+1) u64).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(6))) void k_dp(E2Tables tb, int k_max, int pool_cells,
+__global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cells,
                                            const uint8_t *__restrict__ labels,
                                            const uint8_t *__restrict__ roles,
                                            uint32_t *counters, const uint32_t *__restrict__ list,
@@ -1052,7 +1052,7 @@ size_t e2_dp_lds_bytes(int N)
 
 int e2_dp_slots(int problems)
 {
-    const int cap = 256 * 24;  // 24 one-wave workgroups per CU on a 256-CU part
+    const int cap = 256 * 20;  // 20 one-wave workgroups per CU on a 256-CU part
     return problems < cap ? (problems > 0 ? problems : 1) : cap;
 }
 
