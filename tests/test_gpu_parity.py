@@ -79,6 +79,28 @@ def test_random_small_parity(torch_dev, case):
     _assert_equal(_gpu_all(torch_dev, wl, labels), _oracle_all(wl, labels), tag=f"seed {seed}")
 
 
+def test_random_sweep_parity(torch_dev):
+    """120 more seeded instances across regimes: identical blocks (many ties),
+    no head (every master ties), tight and loose memory, dead links, long
+    chains (one cluster), many clusters."""
+    rng = np.random.default_rng(77)
+    for it in range(120):
+        M = int(rng.integers(1, 80))
+        N = int(rng.integers(1, 130))
+        P = int(rng.integers(1, 6))
+        k_max = int(rng.choice([1, 2, 3, 5, 9, 17]))
+        kw = dict(mem_lo_layers=float(rng.uniform(0.5, 3)),
+                  mem_hi_layers=float(rng.uniform(3, 80)),
+                  zero_bw_frac=float(rng.choice([0.0, 0.05, 0.3])),
+                  head=bool(rng.integers(0, 2)), layer_var=bool(rng.integers(0, 2)),
+                  cong_full=bool(rng.integers(0, 2)))
+        wl = workload.random_small(1000 + it, M=M, N=N, P=P, k_max=k_max, **kw)
+        if not kw["layer_var"] and rng.uniform() < 0.5:
+            wl.speed_flops[:] = wl.speed_flops[0]
+        print(f"sweep {it}: M={M} N={N} P={P} k_max={k_max} {kw}", flush=True)
+        _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag=f"sweep {it}")
+
+
 def test_uniform_layers_many_ties(torch_dev):
     """Identical blocks and devices: every master and many split points tie."""
     wl = workload.random_small(5, M=30, N=40, P=12, k_max=3, layer_var=False,
