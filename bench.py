@@ -13,11 +13,13 @@ Printed on one JSON line:
                summed over every feasible (genome, cluster) problem of each
                timed generation, divided by the timed wall time
   fitness_evals_per_s   genomes scored per second
-  roofline     the DP launch (extraction + DP + fitness kernels of one
-               e2_eval_population call, timed with events on its stream)
-               against the int32 VALU peak: 8 int32 VALU ops per useful
-               j-candidate of the DP kernel (64-bit subtract 2, 64-bit max 3,
-               64-bit min 3), counted on the host from the same inputs
+  roofline     the DP kernel k_dp (timed with HIP events the library records
+               around it on the call's stream) against the int32 VALU peak:
+               8 int32 VALU ops per useful j-candidate of the DP kernel
+               (64-bit subtract 2, 64-bit max 3, 64-bit min 3), counted on
+               the host from the same inputs; traffic = HBM bytes per launch
+               from the committed rocprofv3 counters when they were taken on
+               the current kernel sources
   cpu_baseline the CPU oracle on a bounded sample of the same generation-0
                population, single-threaded
 """
@@ -52,7 +54,8 @@ def log(msg):
 # ---------------------------------------------------------------------------
 # Work accounting (host side, from the same integer inputs).
 # ---------------------------------------------------------------------------
-POOL_CELLS = 2048  # forward-row pool of one DP wave (k_dp)
+POOL_CELLS = 2048  # forward-row pool of a whole-wave DP problem (k_dp)
+
 
 
 def window_tables(wl):
@@ -159,7 +162,9 @@ def generation_work(wl, labels, T, master, tabs):
         fhi = np.minimum(N - 1 - (m - k), pre[:, 1:] - 1)
         sizes = np.where(fhi >= flo, fhi - flo + 1, 0)
         pool = sizes[:, :m - 1].sum(1)
-        fast = pool <= POOL_CELLS
+        # chains of up to 64 devices whose forward bands fit the pool take the
+        # banded path, the others one full table per master
+        fast = (m <= 64) & (pool <= POOL_CELLS)
         # --- fast path
         if fast.any():
             chf, c0f, cHf = ch[fast], c0[fast], cH[fast]
@@ -276,14 +281,19 @@ def main():
     reset()
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(args.steps)]
+    # the library records HIP events around its DP kernel on the call's stream
+    e2.e2_ctx_dp_timing(ctx, args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     run(args.steps, events)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    n_dp, dp_ms = e2.e2_ctx_dp_elapsed(ctx)
+    e2.e2_ctx_dp_timing(ctx, 0)
+    assert n_dp == args.steps, (n_dp, args.steps)
     eval_ms = [a.elapsed_time(b) for a, b in events]
     log(f"timed {args.steps} steps: {elapsed * 1e3:.2f} ms; eval launches "
-        f"{np.mean(eval_ms):.3f} ms avg")
+        f"{np.mean(eval_ms):.3f} ms avg; DP kernel {dp_ms / n_dp:.3f} ms avg")
 
     # replay the same generations to count the work (outside the timed region)
     win, winR, cap = window_tables(wl)
@@ -301,8 +311,9 @@ def main():
         cand += c2
         Lr, Rr = lo, ro
     value = cells / elapsed
-    dp_time = sum(eval_ms) / 1e3
+    dp_time = dp_ms / 1e3
     achieved = cand * OPS_PER_CANDIDATE / dp_time
+    traffic = profiled_traffic(wl.name)
     result = {
         "metric": METRIC,
         "value": value,
@@ -322,15 +333,44 @@ def main():
         "fitness_evals_per_s": P * args.steps / elapsed,
         "dp_cells_per_step": cells / args.steps,
         "j_candidates_per_step": cand / args.steps,
-        "roofline": {"bound": "alu", "kernel": "k_dp (e2_eval_population launch)",
+        "roofline": {"bound": "alu", "kernel": "k_dp",
                      "achieved": achieved / 1e12, "peak": INT_VALU_PEAK / 1e12,
                      "unit": "TOP/s (int32 VALU)", "frac": achieved / INT_VALU_PEAK,
-                     "traffic": None,
-                     "avg_launch_ms": dp_time * 1e3 / args.steps},
+                     "traffic": traffic,
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                                     "copy-calibrated)",
+                     "avg_launch_ms": dp_time * 1e3 / args.steps,
+                     "eval_launch_ms": float(np.mean(eval_ms))},
     }
     if args.cpu_seconds > 0:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+LIB_SOURCES = ("e2_api.hip", "e2_internal.h", "e2_kernels.hip")
+
+
+def source_hash() -> str:
+    """Hash of the library sources that decide what the DP kernel does."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in LIB_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_03770_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic(workload_name):
+    """HBM bytes per DP launch from the committed rocprofv3 counter summary
+    of this workload, or None when none exists or the kernel sources have
+    changed since it was taken."""
+    import glob
+    for f in sorted(glob.glob(os.path.join(ROOT, "profiles", "k_dp_*.json"))):
+        with open(f) as fh:
+            meta = json.load(fh)
+        if meta.get("workload") == workload_name and meta.get("sources_sha256_16") == source_hash():
+            return meta.get("k_dp_hbm_bytes_per_launch")
+    return None
 
 
 def copy_calibration(nbytes):

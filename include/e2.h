@@ -23,8 +23,9 @@
  *     take it stream-ordered from HIP's default memory pool
  *     (hipMallocAsync / hipFreeAsync on the same stream).
  *   - INF = UINT64_MAX marks "no feasible value" in every u64 output.
- *   - A context is immutable after creation: one context may serve several
- *     streams and host threads at once.  It lives on the device that was
+ *   - A context is immutable after creation (apart from the profiling
+ *     records of e2_ctx_dp_timing): one context may serve several streams
+ *     and host threads at once.  It lives on the device that was
  *     current when it was created; calls must be made with that device
  *     current.
  */
@@ -211,6 +212,23 @@ int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
                const uint8_t *labels_in, const uint8_t *roles_in,
                const uint64_t *w_in, const uint64_t *phase_in, const e2_ga_params *gp,
                uint8_t *labels_out, uint8_t *roles_out);
+
+/*
+ * Profiling of the DP kernel (the dominant cost of e2_solve_partitions and
+ * e2_eval_population), for benchmarks and profilers.
+ *
+ * e2_ctx_dp_timing(ctx, n): for the next n solve/eval calls on ctx, record
+ * a HIP event on the call's stream just before and just after its DP
+ * kernel (n in [0, 4096]; 0 turns the recording off).  Discards earlier
+ * records.  Allocates n event pairs; E2_ENOMEM / E2_EHIP if that fails.
+ * e2_ctx_dp_elapsed(ctx, &launches, &ms): waits for the recorded events
+ * and returns how many DP launches were recorded and their summed
+ * duration in milliseconds.
+ * While recording is on, ctx must not be used by several host threads at
+ * once (the calls take the next event pair from the context).
+ */
+int e2_ctx_dp_timing(e2_ctx *ctx, int32_t max_launches);
+int e2_ctx_dp_elapsed(e2_ctx *ctx, int32_t *launches, double *total_ms);
 
 /* Static string for an E2_* code ("unknown error" otherwise). */
 const char *e2_strerror(int code);

@@ -33,7 +33,8 @@ E2_OK, E2_EINVAL, E2_EOVERFLOW, E2_ENOMEM, E2_EHIP = 0, -1, -2, -3, -4
 INF = (1 << 64) - 1
 
 EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitions",
-            "e2_eval_population", "e2_ga_step", "e2_strerror")
+            "e2_eval_population", "e2_ga_step", "e2_ctx_dp_timing", "e2_ctx_dp_elapsed",
+            "e2_strerror")
 
 
 class E2Error(RuntimeError):
@@ -91,6 +92,10 @@ def lib() -> ctypes.CDLL:
     L.e2_ga_step.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, ctypes.POINTER(e2_ga_params),
                              vp, vp]
     L.e2_ga_step.restype = ctypes.c_int
+    L.e2_ctx_dp_timing.argtypes = [vp, i32]
+    L.e2_ctx_dp_timing.restype = ctypes.c_int
+    L.e2_ctx_dp_elapsed.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
+    L.e2_ctx_dp_elapsed.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -164,6 +169,21 @@ def e2_ctx_create(problem: dict) -> Context:
 
 def e2_ctx_destroy(ctx: Context):
     ctx.close()
+
+
+def e2_ctx_dp_timing(ctx: Context, max_launches: int):
+    """Record HIP events around the DP kernel of the next `max_launches`
+    solve/eval calls on ctx (0 stops recording)."""
+    _check(lib().e2_ctx_dp_timing(ctx.handle, int(max_launches)), "e2_ctx_dp_timing")
+
+
+def e2_ctx_dp_elapsed(ctx: Context):
+    """(recorded DP launches, their summed duration in ms); waits for them."""
+    n = ctypes.c_int32()
+    ms = ctypes.c_double()
+    _check(lib().e2_ctx_dp_elapsed(ctx.handle, ctypes.byref(n), ctypes.byref(ms)),
+           "e2_ctx_dp_elapsed")
+    return n.value, ms.value
 
 
 def _torch():

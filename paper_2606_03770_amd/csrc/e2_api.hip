@@ -111,8 +111,7 @@ int alloc_scratch(Scratch &sc, hipStream_t s, size_t bytes)
     return E2_OK;
 }
 
-// Lay out counters, the problem list and the split-point fallback after
-// `extra` leading bytes.
+// Lay out counters, the problem list and the split-point fallback.
 size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_bytes)
 {
     const size_t problems = (size_t)P * k_max;
@@ -126,7 +125,7 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
            align256((size_t)(*slots) * e2_dp_row_words(ctx->N) * 8) + align256(*tb_bytes);
 }
 
-void carve_work(void *base, const e2_ctx *ctx, int P, int k_max, int slots, size_t tb_bytes,
+void carve_work(void *base, e2_ctx *ctx, int P, int k_max, int slots, size_t tb_bytes,
                 E2Work *wk)
 {
     char *p = static_cast<char *>(base);
@@ -138,7 +137,21 @@ void carve_work(void *base, const e2_ctx *ctx, int P, int k_max, int slots, size
     p += align256((size_t)slots * e2_dp_row_words(ctx->N) * 8);
     wk->tb_global = tb_bytes ? reinterpret_cast<uint8_t *>(p) : nullptr;
     wk->n_slots = slots;
-    (void)ctx;
+    wk->ev_begin = wk->ev_end = nullptr;
+    if (ctx->dp_events && ctx->dp_events_used < ctx->dp_event_pairs) {
+        wk->ev_begin = ctx->dp_events[2 * ctx->dp_events_used];
+        wk->ev_end = ctx->dp_events[2 * ctx->dp_events_used + 1];
+        ++ctx->dp_events_used;
+    }
+}
+
+void free_dp_events(e2_ctx *ctx)
+{
+    if (!ctx->dp_events) return;
+    for (int i = 0; i < 2 * ctx->dp_event_pairs; ++i) (void)hipEventDestroy(ctx->dp_events[i]);
+    free(ctx->dp_events);
+    ctx->dp_events = nullptr;
+    ctx->dp_event_pairs = ctx->dp_events_used = 0;
 }
 
 int check_pop(int P, int k_max)
@@ -315,9 +328,53 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
 int e2_ctx_destroy(e2_ctx *ctx)
 {
     if (!ctx) return E2_EINVAL;
+    free_dp_events(ctx);
     const hipError_t e = hipFree(ctx->blob);
     free(ctx);
     return e == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+int e2_ctx_dp_timing(e2_ctx *ctx, int32_t max_launches)
+{
+    if (!ctx || max_launches < 0 || max_launches > 4096) return E2_EINVAL;
+    int rc = check_device(ctx);
+    if (rc) return rc;
+    free_dp_events(ctx);
+    if (max_launches == 0) return E2_OK;
+    ctx->dp_events = static_cast<hipEvent_t *>(calloc(2 * (size_t)max_launches, sizeof(hipEvent_t)));
+    if (!ctx->dp_events) return E2_ENOMEM;
+    for (int i = 0; i < 2 * max_launches; ++i)
+        if (hipEventCreate(&ctx->dp_events[i]) != hipSuccess) {
+            (void)hipGetLastError();
+            for (int k = 0; k < i; ++k) (void)hipEventDestroy(ctx->dp_events[k]);
+            free(ctx->dp_events);
+            ctx->dp_events = nullptr;
+            return E2_EHIP;
+        }
+    ctx->dp_event_pairs = max_launches;
+    ctx->dp_events_used = 0;
+    return E2_OK;
+}
+
+int e2_ctx_dp_elapsed(e2_ctx *ctx, int32_t *launches, double *total_ms)
+{
+    if (!ctx || !launches || !total_ms) return E2_EINVAL;
+    int rc = check_device(ctx);
+    if (rc) return rc;
+    double sum = 0;
+    for (int i = 0; i < ctx->dp_events_used; ++i) {
+        float ms = 0;
+        if (hipEventSynchronize(ctx->dp_events[2 * i + 1]) != hipSuccess ||
+            hipEventElapsedTime(&ms, ctx->dp_events[2 * i], ctx->dp_events[2 * i + 1]) !=
+                hipSuccess) {
+            (void)hipGetLastError();
+            return E2_EHIP;
+        }
+        sum += ms;
+    }
+    *launches = ctx->dp_events_used;
+    *total_ms = sum;
+    return E2_OK;
 }
 
 int e2_solve_partitions(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,

@@ -34,6 +34,10 @@ struct e2_ctx {
     uint64_t head_bytes;
     void *blob;  // one device allocation holding every table
     E2Tables tables;
+    // DP launch timing (profiling): event pairs and how many are recorded
+    hipEvent_t *dp_events;
+    int dp_event_pairs;
+    int dp_events_used;
 };
 
 // Scratch layout of one solve/eval call (device memory, stream-ordered).
@@ -43,6 +47,8 @@ struct E2Work {
     uint64_t *rows;      // [n_slots][pool + 2 (N+1)] per-wave DP rows
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
     int n_slots;         // waves of the DP kernel
+    hipEvent_t ev_begin; // recorded just before / after the DP kernel, or null
+    hipEvent_t ev_end;
 };
 
 // Number of DP waves launched for `problems` upper-bound problems.

@@ -1065,9 +1065,11 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
     k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, labels, wk.counters, wk.list,
                                                        seg, T, Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
+    if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
     k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, labels, roles, wk.counters,
                                                       wk.list, seg, wk.rows, wk.tb_global, T,
                                                       Lambda, master, layers);
+    if (wk.ev_end) (void)hipEventRecord(wk.ev_end, s);
     return hipGetLastError();
 }
 

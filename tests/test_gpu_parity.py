@@ -224,3 +224,21 @@ def test_ga_loop_on_the_16384_genome_workload(torch_dev):
         el, er = oracle.ga_step(labels, roles, w, ph, wl.k_max, **wl.ga_params(g))
         assert (lo.cpu().numpy() == el).all() and (ro.cpu().numpy() == er).all()
         L, R = lo, ro
+
+
+def test_dp_timing_records_each_launch(torch_dev):
+    """The profiling hook records one event pair per solve/eval call, up to
+    the requested number, and leaves results unchanged."""
+    torch, dev = torch_dev
+    wl = workload.make("c2_32dev_48L")
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    want = _gpu_all(torch_dev, wl, ctx=ctx)
+    e2.e2_ctx_dp_timing(ctx, 2)
+    got = _gpu_all(torch_dev, wl, ctx=ctx)          # solve + eval: two launches
+    extra = _gpu_all(torch_dev, wl, ctx=ctx)        # beyond the limit: not recorded
+    n, ms = e2.e2_ctx_dp_elapsed(ctx)
+    assert n == 2 and ms > 0
+    e2.e2_ctx_dp_timing(ctx, 0)
+    assert e2.e2_ctx_dp_elapsed(ctx) == (0, 0.0)
+    for k in want:
+        assert (got[k] == want[k]).all() and (extra[k] == want[k]).all(), k
