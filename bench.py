@@ -15,9 +15,10 @@ Printed on one JSON line:
   fitness_evals_per_s   genomes scored per second
   roofline     the DP kernel k_dp (timed with HIP events the library records
                around it on the call's stream) against the int32 VALU peak:
-               8 int32 VALU ops per useful j-candidate of the DP kernel
-               (64-bit subtract 2, 64-bit max 3, 64-bit min 3), counted on
-               the host from the same inputs; traffic = HBM bytes per launch
+               int32 VALU ops per useful j-candidate of the DP kernel, 8 with
+               u64 keys (64-bit subtract 2, max 3, min 3) and 3 with u32 keys
+               (subtract, max, min), candidates counted on the host from the
+               same inputs; traffic = HBM bytes per launch
                from the committed rocprofv3 counters when they were taken on
                the current kernel sources
   cpu_baseline the CPU oracle on a bounded sample of the same generation-0
@@ -55,6 +56,8 @@ def log(msg):
 # Work accounting (host side, from the same integer inputs).
 # ---------------------------------------------------------------------------
 POOL_CELLS = 2048  # forward-row pool of a whole-wave DP problem (k_dp)
+U32_MAX_VALUE = 0xFFFFFE  # largest finite value of the u32-key path
+OPS_PER_CANDIDATE_U32 = 3  # 32-bit subtract, max, min
 
 
 
@@ -102,18 +105,44 @@ def count_tables(win, winR, N):
     return build(win), build(winR)
 
 
-def generation_work(wl, labels, T, master, tabs):
+def value_bounds(wl, win):
+    """vmax[r][d]: the largest cost of a memory-fitting stage of device d in
+    role r (plus the head time for stages holding the head bytes), and the
+    quantised link times tau[r][d][e] (INF for dead links)."""
+    t, h, tau = e2.e2_quantise(wl.problem_arrays())
+    M, N = wl.n_dev, wl.n_layer
+    vmax = np.zeros((2, M), dtype=object)
+    for r in range(2):
+        P = np.concatenate([np.zeros((M, 1), np.uint64), np.cumsum(t[r], axis=1, dtype=np.uint64)],
+                           1)
+        for d in range(M):
+            best = 0
+            for f in range(2):
+                ok = win[f, d] != 255
+                if ok.any():
+                    i = np.nonzero(ok)[0]
+                    c = P[d, i + 1] - P[d, win[f, d, i]]
+                    best = max(best, int(c.max()) + (int(h[r, d]) if f else 0))
+            vmax[r, d] = best
+    return vmax, tau
+
+
+def generation_work(wl, labels, roles, T, master, tabs):
     """(Algorithm 1 cells over feasible problems, useful j-candidates the DP
-    kernel evaluates) for one population.  The candidate count follows k_dp
-    row by row: forward rows, reversed rows, one combine per master, the
-    chosen master's rows and last cell (or, for chains whose bands exceed
-    the pool, one full table per master plus the chosen master's again)."""
-    win, winR, cap, C, CR = tabs
+    kernel evaluates with u64 keys, those it evaluates with u32 keys) for one
+    population.  The candidate count follows k_dp row by row: forward rows,
+    reversed rows, one combine per master, the chosen master's rows and last
+    cell (or, for chains whose bands exceed the pool, one full table per
+    master plus the chosen master's again).  A banded problem takes u32 keys
+    when every finite value it can produce (largest fitting stage cost of its
+    devices, largest finite link time) is at most U32_MAX_VALUE."""
+    win, winR, cap, C, CR, vmax, tau = tabs
     N, K = wl.n_layer, wl.k_max
     P, M = labels.shape
     feasible = T != INF
     cells = 0
     cand = 0
+    cand32 = 0
 
     def rows(f, d, kmin, lo, hi):
         """useful candidates of rows with cells lo..hi (arrays, broadcast)"""
@@ -150,6 +179,12 @@ def generation_work(wl, labels, T, master, tabs):
             continue
         ch, c0, cH, feas, pq = ch[listed], c0[listed], cH[listed], feas[listed], pq[listed]
         n = len(ch)
+        rr = (roles[pq[:, 0], pq[:, 1]] != 0).astype(np.int64)
+        bnd = np.array([max([vmax[rr[a], d] for d in ch[a]] +
+                            [int(tau[rr[a], ch[a][k - 1], ch[a][k]]) for k in range(1, m)
+                             if int(tau[rr[a], ch[a][k - 1], ch[a][k]]) != INF])
+                        for a in range(n)], dtype=object)
+        narrow = np.array([b <= U32_MAX_VALUE for b in bnd], dtype=bool)
         mu = np.zeros(n, dtype=np.int64)
         mdev = master[pq[:, 0], pq[:, 1]].astype(np.int64)
         for a in range(n):
@@ -204,7 +239,9 @@ def generation_work(wl, labels, T, master, tabs):
                 v0 = rows(0, chf[:, m - 1], jm, np.full(len(chf), N - 1), np.full(len(chf), N - 1))
                 v1 = rows(1, chf[:, m - 1], jm, np.full(len(chf), N - 1), np.full(len(chf), N - 1))
                 tot_f += np.where(ff, np.where(isn, v1, v0), 0)
-            cand += int(tot_f.sum())
+            nf = narrow[fast]
+            cand += int(tot_f[~nf].sum())
+            cand32 += int(tot_f[nf].sum())
         # --- reference path
         if (~fast).any():
             chs, mus = ch[~fast], mu[~fast]
@@ -215,7 +252,7 @@ def generation_work(wl, labels, T, master, tabs):
             per = ((m - 1) * r0 + r1)[:, 1:].sum(1)
             extra = np.where(np.arange(1, m + 1)[None, :] == mus[:, None], r1, r0)[:, 1:].sum(1)
             cand += int((per + np.where(mus > 0, extra, 0)).sum())
-    return cells, cand
+    return cells, cand, cand32
 
 
 # ---------------------------------------------------------------------------
@@ -297,22 +334,23 @@ def main():
 
     # replay the same generations to count the work (outside the timed region)
     win, winR, cap = window_tables(wl)
-    wcr = (win, winR, cap) + count_tables(win, winR, wl.n_layer)
+    wcr = (win, winR, cap) + count_tables(win, winR, wl.n_layer) + value_bounds(wl, win)
     Lr, Rr = L0.clone(), R0.clone()
-    cells = cand = 0
+    cells = cand = cand32 = 0
     for g in range(args.steps):
         sol = e2.e2_solve_partitions(ctx, Lr, Rr)
         f2 = e2.e2_eval_population(ctx, Lr, Rr, fp, with_rates=False)
         lo, ro = e2.e2_ga_step(ctx, Lr, Rr, f2["w"], f2["phase"], wl.ga_params(g))
         torch.cuda.synchronize()
-        c1, c2 = generation_work(wl, Lr.cpu().numpy(), e2.u64(sol["T"]),
-                                 sol["master"].cpu().numpy(), wcr)
+        c1, c2, c3 = generation_work(wl, Lr.cpu().numpy(), Rr.cpu().numpy(), e2.u64(sol["T"]),
+                                     sol["master"].cpu().numpy(), wcr)
         cells += c1
         cand += c2
+        cand32 += c3
         Lr, Rr = lo, ro
     value = cells / elapsed
     dp_time = dp_ms / 1e3
-    achieved = cand * OPS_PER_CANDIDATE / dp_time
+    achieved = (cand * OPS_PER_CANDIDATE + cand32 * OPS_PER_CANDIDATE_U32) / dp_time
     traffic = profiled_traffic(wl.name)
     result = {
         "metric": METRIC,
@@ -332,7 +370,8 @@ def main():
                    "step": "one GA generation: e2_eval_population + e2_ga_step"},
         "fitness_evals_per_s": P * args.steps / elapsed,
         "dp_cells_per_step": cells / args.steps,
-        "j_candidates_per_step": cand / args.steps,
+        "j_candidates_per_step": (cand + cand32) / args.steps,
+        "j_candidates_u32_keys_per_step": cand32 / args.steps,
         "roofline": {"bound": "alu", "kernel": "k_dp",
                      "achieved": achieved / 1e12, "peak": INT_VALU_PEAK / 1e12,
                      "unit": "TOP/s (int32 VALU)", "frac": achieved / INT_VALU_PEAK,

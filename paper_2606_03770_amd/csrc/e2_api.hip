@@ -115,7 +115,7 @@ int alloc_scratch(Scratch &sc, hipStream_t s, size_t bytes)
 size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_bytes)
 {
     const size_t problems = (size_t)P * k_max;
-    *slots = e2_dp_slots((int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX));
+    *slots = e2_dp_slots(ctx->N, (int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX));
     const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
     // the fallback is needed only when some chain's split points exceed the
     // LDS pool of the reference path
@@ -261,11 +261,32 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
             suffix_min(&win[((size_t)f * M + d) * N], &minwin[((size_t)f * M + d) * N]);
     for (int d = 0; d < M; ++d) suffix_min(&winR[(size_t)d * N], &minwinR[(size_t)d * N]);
 
+    // largest cost of a memory-fitting stage per role and device (with the
+    // head time for stages that carry the head bytes): every finite value a
+    // DP over a chain produces is at most the largest of these over its
+    // devices and its largest finite link time
+    std::vector<uint64_t> vmax((size_t)2 * M, 0);
+    for (int r = 0; r < 2; ++r)
+        for (int d = 0; d < M; ++d) {
+            const uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
+            uint64_t best = 0;
+            for (int f = 0; f < 2; ++f)
+                for (int i = 0; i < N; ++i) {
+                    const uint8_t j = win[((size_t)f * M + d) * N + i];
+                    if (j == E2_NO_START) continue;
+                    const uint64_t c = row[i + 1] - row[j] + (f ? h[(size_t)r * M + d] : 0);
+                    if (c > best) best = c;
+                }
+            vmax[(size_t)r * M + d] = best;
+        }
+
     const size_t b_pref = align256(pref.size() * 8), b_head = align256(h.size() * 8),
                  b_tau = align256(tau.size() * 8), b_win = align256(win.size()),
                  b_winR = align256(winR.size()), b_cap = align256((size_t)M);
     const size_t b_mw = align256(minwin.size()), b_mwR = align256(minwinR.size());
-    const size_t total = 2 * b_pref + b_head + b_tau + b_win + b_winR + b_mw + b_mwR + 2 * b_cap;
+    const size_t b_vmax = align256(vmax.size() * 8);
+    const size_t total =
+        2 * b_pref + b_head + b_tau + b_win + b_winR + b_mw + b_mwR + 2 * b_cap + b_vmax;
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
     if (!ctx) return E2_ENOMEM;
     if (hipGetDevice(&ctx->device) != hipSuccess) {
@@ -288,6 +309,7 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     char *d_mwR = d_mw + b_mw;
     char *d_cap0 = d_mwR + b_mwR;
     char *d_capH = d_cap0 + b_cap;
+    char *d_vmax = d_capH + b_cap;
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMemcpy(d_pref, pref.data(), pref.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_head, h.data(), h.size() * 8, hipMemcpyHostToDevice);
@@ -301,6 +323,8 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
         e = hipMemcpy(d_prefR, prefR.data(), prefR.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_cap0, cap0.data(), (size_t)M, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_capH, capH.data(), (size_t)M, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(d_vmax, vmax.data(), vmax.size() * 8, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(ctx->blob);
         free(ctx);
@@ -319,6 +343,7 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     ctx->tables.prefR = reinterpret_cast<const uint64_t *>(d_prefR);
     ctx->tables.cap0 = reinterpret_cast<const uint8_t *>(d_cap0);
     ctx->tables.capH = reinterpret_cast<const uint8_t *>(d_capH);
+    ctx->tables.vmax = reinterpret_cast<const uint64_t *>(d_vmax);
     ctx->tables.M = M;
     ctx->tables.N = N;
     *out = ctx;

@@ -24,6 +24,8 @@ struct E2Tables {
     const uint8_t *minwinR;//   [M][N]
     const uint8_t *cap0;   // [M] most blocks one stage can hold without the head
     const uint8_t *capH;   // [M] most blocks one stage can hold with the head
+    const uint64_t *vmax;  // [2][M] largest cost of a fitting stage (+ head time when it
+                           //   holds the head bytes) per role and device
     int M;
     int N;
 };
@@ -51,8 +53,8 @@ struct E2Work {
     hipEvent_t ev_end;
 };
 
-// Number of DP waves launched for `problems` upper-bound problems.
-int e2_dp_slots(int problems);
+// Number of DP waves launched for at most `problems` problems of N blocks.
+int e2_dp_slots(int N, int problems);
 // Forward-row pool of one DP wave (u64 cells), its global row storage
 // (u64 per wave) and its dynamic LDS bytes.
 int e2_dp_pool_cells(int N);

@@ -223,6 +223,15 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
 // are the same rows over reversed blocks (block N-1 first), so every row of
 // every table goes through this code.
 //
+// Key width K.  Every finite value of a problem is at most the largest cost
+// of a memory-fitting stage of its devices (with the head time where the
+// stage carries the head) or its largest finite link time.  When that bound
+// is below 2^24 - 1 the packed keys fit in 32 bits: rows, split-point pairs
+// and pools hold u32 and a candidate costs one subtract, one max and one
+// min; otherwise keys are u64 (values < 2^56).  Stage costs come from u64
+// prefix sums; the 32-bit path keeps the low 32 bits of (P << 8), whose
+// differences are exact because every visited stage cost is below 2^24.
+//
 // Lane mapping: S lanes per cell (S = 4 for at most 16 cells, 2 for at most
 // 32, else 1); lane o of a cell visits j = i - o - S t for t = 0, 1, ...
 // With L = min(cap, hi - jmin + 1) an upper bound and Lm a lower bound of
@@ -230,31 +239,72 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
 // every window and run unclamped (four at a time); the remaining steps
 // clamp j to the lane's window start (a repeated candidate leaves a minimum
 // unchanged).  The S partial minima meet through DPP quad permutations.
-// Split points keep (prefix term, shifted prefix sum) as one 16-byte LDS
-// pair.
+// Split points keep (prefix term, shifted prefix sum) as one LDS pair.
 //
-// INF needs no branches: finite values are below 2^56 - 256, so a packed
-// key built from an INF prefix term or link is >= kInfKey and loses every
-// comparison with a finite key.
+// INF needs no branches: finite values are below the key's INF threshold
+// divided by 256, so a packed key built from an INF prefix term or link is
+// >= the threshold and loses every comparison with a finite key.
 // ---------------------------------------------------------------------------
-constexpr uint64_t kInfKey = 0xFFFFFFFFFFFFFF00ull;
+template <typename K> struct KeyT;
+template <> struct KeyT<uint64_t> {
+    static constexpr uint64_t inf = E2_INF64;
+    static constexpr uint64_t inf_key = 0xFFFFFFFFFFFFFF00ull;
+};
+template <> struct KeyT<uint32_t> {
+    static constexpr uint32_t inf = 0xFFFFFFFFu;
+    static constexpr uint32_t inf_key = 0xFFFFFF00u;
+};
+constexpr uint64_t kU32MaxValue = 0xFFFFFEull;  // largest finite value of the 32-bit path
 
+template <typename K> __device__ __forceinline__ K kmax(K a, K b) { return a > b ? a : b; }
+template <typename K> __device__ __forceinline__ K kmin(K a, K b) { return a < b ? a : b; }
+template <int CTRL, typename K> __device__ __forceinline__ K dppk(K v)
+{
+    if constexpr (sizeof(K) == 8) return dpp_u64<CTRL>(v);
+    else return (K)(uint32_t)dpp_i32<CTRL>((int)v);
+}
+template <typename K> __device__ __forceinline__ K readlane_k(K v, int lane)
+{
+    if constexpr (sizeof(K) == 8) return readlane_u64(v, lane);
+    else return (K)(uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+template <typename K> __device__ __forceinline__ K wave_min_k(K v)
+{
+    v = kmin(v, dppk<0xb1>(v));
+    v = kmin(v, dppk<0x4e>(v));
+    v = kmin(v, dppk<0x141>(v));
+    v = kmin(v, dppk<0x140>(v));
+    return kmin(kmin(readlane_k(v, 0), readlane_k(v, 16)),
+                kmin(readlane_k(v, 32), readlane_k(v, 48)));
+}
+// a u64 time (INF allowed) as a key-width value
+template <typename K> __device__ __forceinline__ K to_k(uint64_t v)
+{
+    return v == E2_INF64 ? KeyT<K>::inf : (K)v;
+}
+template <typename K> __device__ __forceinline__ uint64_t to_u64(K v)
+{
+    return v == KeyT<K>::inf ? E2_INF64 : (uint64_t)v;
+}
+
+template <typename K>
 struct PS {
-    uint64_t a;  // max(prev(j-1), tau) << 8 | j
-    uint64_t s;  // (P[j] << 8) - j
+    K a;  // max(prev(j-1), tau) << 8 | j
+    K s;  // (P[j] << 8) - j
 };
 
 // Wave-uniform description of a row (scalar registers).
+template <typename K>
 struct Row {
     const uint64_t *pr;    // prefix sums P[0..N] of the stage device
     const uint8_t *wr;     // smallest stage start per stage end, E2_NO_START if none
     uint64_t hadd;         // head time when this device is the master, else 0
-    uint64_t tau;          // link from the previous device
+    K tau;                 // link from the previous device
     int lo, hi;            // cells of this row
     int kmin;              // devices before this one
     int cap;               // longest stage that fits the device
     int lmin;              // lower bound of window lengths over cells >= lo (0: none)
-    const uint64_t *prev;  // previous row, band-packed over [plo, phi]; null: first device
+    const K *prev;         // previous row, band-packed over [plo, phi]; null: first device
     int plo, phi;
 };
 
@@ -262,15 +312,16 @@ struct Row {
 // combine, a running per-lane minimum of (max(value(i), B(i)) << 8 | mu) with
 // B(i) = max(tau_next, G(N-2-i)) from the band-packed reversed row G over
 // [glo, ghi] (last_only: B = 0 at i = N-1, INF elsewhere).
+template <typename K>
 struct RowOut {
-    uint64_t *vals;     // band-packed values (LDS), may be null in combine mode
-    uint64_t *vals_g;   // second copy of the values (global), or null
+    K *vals;            // band-packed values (LDS), may be null in combine mode
+    K *vals_g;          // second copy of the values (global), or null
     uint8_t *tbs;       // split points, or null
     bool combine;
     bool last_only;
-    const uint64_t *G;
+    const K *G;
     int glo, ghi;
-    uint64_t tau_next;
+    K tau_next;
     int mu;
 };
 
@@ -303,55 +354,55 @@ __device__ __forceinline__ uint64_t link_tau_u(const E2Tables &tb, int r, int a,
 {
     return uni64(link_tau(tb, r, a, b));
 }
-__device__ __forceinline__ uint64_t pack_prev(uint64_t prev, uint64_t tau, int j)
+template <typename K> __device__ __forceinline__ K pack_prev(K prev, K tau, int j)
 {
-    return (umax64(prev, tau) << 8) | (uint64_t)j;
+    return (kmax(prev, tau) << 8) | (K)j;
 }
-__device__ __forceinline__ uint64_t unpack_val(uint64_t key)
+template <typename K> __device__ __forceinline__ K unpack_val(K key)
 {
-    return key >= kInfKey ? E2_INF64 : (key >> 8);
+    return key >= KeyT<K>::inf_key ? KeyT<K>::inf : (key >> 8);
 }
-__device__ __forceinline__ uint64_t cand(const PS &e, uint64_t si1)
+template <typename K> __device__ __forceinline__ K cand(const PS<K> &e, K si1)
 {
-    return umax64(e.a, si1 - e.s);
+    return kmax(e.a, (K)(si1 - e.s));
 }
-__device__ __forceinline__ uint64_t combine_b(int i, int N, const RowOut &ro)
+template <typename K> __device__ __forceinline__ K combine_b(int i, int N, const RowOut<K> &ro)
 {
-    if (ro.last_only) return (i == N - 1) ? 0 : E2_INF64;
+    if (ro.last_only) return (i == N - 1) ? (K)0 : KeyT<K>::inf;
     const int x = N - 2 - i;
-    return (x >= ro.glo && x <= ro.ghi) ? umax64(ro.G[x - ro.glo], ro.tau_next) : E2_INF64;
+    return (x >= ro.glo && x <= ro.ghi) ? kmax(ro.G[x - ro.glo], ro.tau_next) : KeyT<K>::inf;
 }
-__device__ __forceinline__ uint64_t combine_key(uint64_t v, uint64_t b, int mu)
+template <typename K> __device__ __forceinline__ K combine_key(K v, K b, int mu)
 {
-    return (umax64(v, b) << 8) | (uint64_t)mu;
+    return (kmax(v, b) << 8) | (K)mu;
 }
 
-template <int S>
-__device__ __forceinline__ uint64_t scan_cell(const PS *ps, int i, int jlo, int o, uint64_t si1,
-                                              int t_safe, int t_all)
+template <int S, typename K>
+__device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K si1, int t_safe,
+                                       int t_all)
 {
-    uint64_t best = E2_INF64;
+    K best = KeyT<K>::inf;
     int t = 0;
-    const PS *top = ps + (i - o);  // j at step t is top - S t
+    const PS<K> *top = ps + (i - o);  // j at step t is top - S t
     for (; t + 4 <= t_safe; t += 4) {
-        const PS *q = top - S * (t + 3);
-        best = umin64(best, cand(q[3 * S], si1));
-        best = umin64(best, cand(q[2 * S], si1));
-        best = umin64(best, cand(q[S], si1));
-        best = umin64(best, cand(q[0], si1));
+        const PS<K> *q = top - S * (t + 3);
+        best = kmin(best, cand(q[3 * S], si1));
+        best = kmin(best, cand(q[2 * S], si1));
+        best = kmin(best, cand(q[S], si1));
+        best = kmin(best, cand(q[0], si1));
     }
     for (; t < t_all; ++t) {
         int j = i - o - S * t;
         if (j < jlo) j = jlo;
-        best = umin64(best, cand(ps[j], si1));
+        best = kmin(best, cand(ps[j], si1));
     }
-    if (S >= 2) best = umin64(best, dpp_u64<0xb1>(best));
-    if (S >= 4) best = umin64(best, dpp_u64<0x4e>(best));
+    if (S >= 2) best = kmin(best, dppk<0xb1>(best));
+    if (S >= 4) best = kmin(best, dppk<0x4e>(best));
     return best;
 }
 
-template <int S>
-__device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane, int N)
+template <int S, typename K>
+__device__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int lane, int N)
 {
     constexpr int CPP = kWave / S;  // cells per pass
     const int o = lane % S;
@@ -359,7 +410,8 @@ __device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane
     const int jmin = max(rw.kmin, rw.lo - rw.cap + 1);
     // first pass's cell loads go out before the split points are built
     int w_nx = E2_NO_START;
-    uint64_t p_nx = 0, b_nx = 0;
+    uint64_t p_nx = 0;
+    K b_nx = 0;
     {
         const int i = rw.lo + cl;
         if (i <= rw.hi) {
@@ -370,10 +422,10 @@ __device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane
     }
     for (int j = jmin + lane; j <= rw.hi; j += kWave) {
         const int pj = j - 1;
-        const uint64_t pv = (pj >= rw.plo && pj <= rw.phi) ? rw.prev[pj - rw.plo] : E2_INF64;
+        const K pv = (pj >= rw.plo && pj <= rw.phi) ? rw.prev[pj - rw.plo] : KeyT<K>::inf;
         const uint64_t pj8 = rw.pr[j] << 8;
         ps[j].a = pack_prev(pv, rw.tau, j);
-        ps[j].s = pj8 - (uint64_t)j;
+        ps[j].s = (K)(pj8 - (uint64_t)j);
     }
     __syncthreads();
     const int L = min(rw.cap, rw.hi - jmin + 1);
@@ -381,11 +433,12 @@ __device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane
     const int t_all = (L + S - 1) / S;
     const int t_safe = Lm / S;
     const int i_idle = jmin + (Lm > 0 ? Lm - 1 : 0);  // idle lanes: in-range reads
-    uint64_t acc = E2_INF64;
+    K acc = KeyT<K>::inf;
     for (int base = rw.lo; base <= rw.hi; base += CPP) {
         const int i = base + cl;
         const int w = w_nx;
-        const uint64_t p1 = p_nx, b = b_nx;
+        const uint64_t p1 = p_nx;
+        const K b = b_nx;
         if (i + CPP <= rw.hi) {
             w_nx = rw.wr[i + CPP];
             p_nx = rw.pr[i + CPP + 1];
@@ -394,16 +447,16 @@ __device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane
         const bool act = i <= rw.hi && w != (int)E2_NO_START;
         const int ie = act ? i : i_idle;
         const int jlo = act ? max(w, jmin) : jmin;
-        const uint64_t si1 = (p1 + rw.hadd) << 8;
-        const uint64_t best = scan_cell<S>(ps, ie, jlo, o, si1, t_safe, t_all);
+        const K si1 = (K)((p1 + rw.hadd) << 8);
+        const K best = scan_cell<S>(ps, ie, jlo, o, si1, t_safe, t_all);
         if (o != 0 || i > rw.hi) continue;
-        const uint64_t v = act ? unpack_val(best) : E2_INF64;
+        const K v = act ? unpack_val(best) : KeyT<K>::inf;
         if (!ro.combine) {
             ro.vals[i - rw.lo] = v;
             if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
             if (ro.tbs) ro.tbs[i - rw.lo] = (uint8_t)(best & 0xFF);
         } else {
-            acc = umin64(acc, combine_key(v, b, ro.mu));
+            acc = kmin(acc, combine_key(v, b, ro.mu));
         }
     }
     __syncthreads();
@@ -412,17 +465,18 @@ __device__ uint64_t row_pass_s(const Row &rw, const RowOut &ro, PS *ps, int lane
 
 // Store mode returns INF; combine mode returns the lane's running minimum of
 // (max(value, B) << 8 | mu) (the caller reduces over the wave once).
-__device__ uint64_t row_pass(const Row &rw, const RowOut &ro, PS *ps, int lane, int N)
+template <typename K>
+__device__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int lane, int N)
 {
     if (rw.prev == nullptr) {  // first device: Eq. 2, no split point
-        uint64_t acc = E2_INF64;
+        K acc = KeyT<K>::inf;
         for (int i = rw.lo + lane; i <= rw.hi; i += kWave) {
-            const uint64_t v = (rw.wr[i] == 0) ? rw.pr[i + 1] + rw.hadd : E2_INF64;
+            const K v = (rw.wr[i] == 0) ? (K)(rw.pr[i + 1] + rw.hadd) : KeyT<K>::inf;
             if (!ro.combine) {
                 ro.vals[i - rw.lo] = v;
                 if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
             } else {
-                acc = umin64(acc, combine_key(v, combine_b(i, N, ro), ro.mu));
+                acc = kmin(acc, combine_key(v, combine_b(i, N, ro), ro.mu));
             }
         }
         __syncthreads();
@@ -431,16 +485,17 @@ __device__ uint64_t row_pass(const Row &rw, const RowOut &ro, PS *ps, int lane, 
     const int n = rw.hi - rw.lo + 1;
     if (n <= 0) {
         __syncthreads();
-        return E2_INF64;
+        return KeyT<K>::inf;
     }
     if (n <= 16) return row_pass_s<4>(rw, ro, ps, lane, N);
     if (n <= 32) return row_pass_s<2>(rw, ro, ps, lane, N);
     return row_pass_s<1>(rw, ro, ps, lane, N);
 }
 
-__device__ __forceinline__ RowOut store_to(uint64_t *vals, uint64_t *vals_g, uint8_t *tbs)
+template <typename K>
+__device__ __forceinline__ RowOut<K> store_to(K *vals, K *vals_g, uint8_t *tbs)
 {
-    RowOut ro;
+    RowOut<K> ro;
     ro.vals = vals;
     ro.vals_g = vals_g;
     ro.tbs = tbs;
@@ -485,19 +540,37 @@ __device__ __forceinline__ RowOut store_to(uint64_t *vals, uint64_t *vals_g, uin
 // ---------------------------------------------------------------------------
 constexpr int kMaxBandedChain = kWave;
 
-struct ChainRegs {          // lane k-1 holds chain position k (1-based)
-    int dev, cap0, capH;
-    uint64_t tau;           // link from position k-1 (k >= 2)
-    uint64_t head;          // head time of the device
-    int flo, fhi, off;      // forward band and pool offset of row k
-    int lmin0, lmin1;       // window-length bounds of row k (no head / head)
-    int devR, capR;         // reversed row t = k: device of position m+1-k, its cap0
-    int glo, ghi;           // reversed band of reversed row t = k
-    int lminR;              // window-length bound of reversed row t = k
-    uint64_t tauR;          // link of reversed row t = k: position m+1-k -> m+2-k
+// Per-position table of a chain: lane k-1 holds chain position k (1-based)
+// as four packed words (fields < 256 except the pool offset) and three u64
+// times; a row reads its words with one readlane each and unpacks them in
+// scalar registers.
+struct ChainRegs {
+    uint32_t wa;    // dev | cap0 << 8 | capH << 16 | lmin0 << 24      (forward row k)
+    uint32_t wb;    // flo | fhi << 8 | lmin1 << 16                    (forward row k)
+    uint32_t wc;    // pool offset of row k | lminR << 16 | capR << 24 (reversed row t = k)
+    uint32_t wd;    // devR | glo << 8 | ghi << 16                     (reversed row t = k)
+    uint64_t tau;   // link from position k-1 (k >= 2)
+    uint64_t head;  // head time of the device
+    uint64_t tauR;  // link of reversed row t = k: position m+1-k -> m+2-k
 };
+// cap0 / capH are the longest stages without / with the head, [flo, fhi]
+// the forward band, lmin0 / lmin1 its window-length bounds; reversed row
+// t = k runs on device devR (position m+1-k) with cap0 capR over the band
+// [glo, ghi] with window-length bound lminR.
+__device__ __forceinline__ int f8(uint32_t w, int sh) { return (int)((w >> sh) & 0xFFu); }
 
 __device__ __forceinline__ int lane_i(int v, int k) { return __builtin_amdgcn_readlane(v, k); }
+__device__ __forceinline__ uint32_t lane_w(uint32_t v, int k)
+{
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, k);
+}
+// band of forward row k and its pool offset
+__device__ __forceinline__ int band_lo(const ChainRegs &cr, int k) { return f8(lane_w(cr.wb, k - 1), 0); }
+__device__ __forceinline__ int band_hi(const ChainRegs &cr, int k) { return f8(lane_w(cr.wb, k - 1), 8); }
+__device__ __forceinline__ int pool_off(const ChainRegs &cr, int k)
+{
+    return (int)(lane_w(cr.wc, k - 1) & 0xFFFFu);
+}
 __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int k) { return readlane_u64(v, k); }
 
 __device__ __forceinline__ int scan_incl_i32(int x, int lane)
@@ -510,7 +583,7 @@ __device__ __forceinline__ int scan_incl_i32(int x, int lane)
 }
 
 struct DpSmem {
-    PS *ps;          // split-point pairs, N entries (LDS)
+    void *ps;        // split-point pairs, N entries (LDS)
     uint64_t *Rw0;   // LDS row ping-pong, N+1 entries each
     uint64_t *Rw1;
     uint8_t *tbp;    // split points of the forward rows, band-packed (LDS)
@@ -522,88 +595,114 @@ struct DpSmem {
 
 // Row k (1-based) of the table for master mu (mu = 0: no master) as a
 // forward row; prev / plo / phi are filled in by the caller.
-__device__ __forceinline__ Row fwd_row_of(const E2Tables &tb, const ChainRegs &cr, int r, int k,
-                                          int mu)
+template <typename K>
+__device__ __forceinline__ Row<K> fwd_row_of(const E2Tables &tb, const ChainRegs &cr, int r, int k,
+                                             int mu)
 {
     const int f = (mu == k);
-    const int c = lane_i(cr.dev, k - 1);
-    Row rw;
+    const uint32_t wa = lane_w(cr.wa, k - 1), wb = lane_w(cr.wb, k - 1);
+    const int c = f8(wa, 0);
+    Row<K> rw;
     rw.pr = pref_row(tb, r, c);
     rw.wr = win_row(tb, f, c);
     rw.hadd = f ? lane_u64(cr.head, k - 1) : 0;
-    rw.tau = (k >= 2) ? lane_u64(cr.tau, k - 1) : 0;
-    rw.lo = lane_i(cr.flo, k - 1);
-    rw.hi = lane_i(cr.fhi, k - 1);
+    rw.tau = (k >= 2) ? to_k<K>(lane_u64(cr.tau, k - 1)) : (K)0;
+    rw.lo = f8(wb, 0);
+    rw.hi = f8(wb, 8);
     rw.kmin = k - 1;
-    rw.cap = f ? lane_i(cr.capH, k - 1) : lane_i(cr.cap0, k - 1);
-    rw.lmin = f ? lane_i(cr.lmin1, k - 1) : lane_i(cr.lmin0, k - 1);
+    rw.cap = f ? f8(wa, 16) : f8(wa, 8);
+    rw.lmin = f ? f8(wb, 16) : f8(wa, 24);
     rw.prev = nullptr;
     rw.plo = 1;
     rw.phi = 0;
     return rw;
 }
 
-__device__ __forceinline__ void set_prev(Row &rw, const uint64_t *prev, int plo, int phi)
+template <typename K>
+__device__ __forceinline__ void set_prev(Row<K> &rw, const K *prev, int plo, int phi)
 {
     rw.prev = prev;
     rw.plo = plo;
     rw.phi = phi;
 }
 
-__device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
-                          int m, int lane, uint64_t *T_out, int *mu_out, uint8_t *start,
-                          uint8_t *last_tb)
+// Per-position table of a chain and the largest finite value its DP can
+// produce; false when the banded path cannot take the chain.
+__device__ bool chain_regs(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
+                           int m, int lane, ChainRegs &cr, uint64_t *bound)
 {
     const int N = tb.N, M = tb.M;
     if (m > kMaxBandedChain) return false;
-    // ---- per-position table, one position per lane
-    ChainRegs cr;
     const bool valid = lane < m;
     const int k1 = lane + 1;
-    cr.dev = valid ? chain[lane] : 0;
-    cr.cap0 = valid ? tb.cap0[cr.dev] : 0;
-    cr.capH = valid ? tb.capH[cr.dev] : 0;
-    cr.head = valid ? tb.head[r * M + cr.dev] : 0;
-    cr.tau = (valid && lane >= 1) ? link_tau(tb, r, chain[lane - 1], cr.dev) : 0;
-    const int pre = scan_incl_i32(cr.cap0, lane);
+    const int dev = valid ? chain[lane] : 0;
+    const int cap0 = valid ? tb.cap0[dev] : 0;
+    const int capH = valid ? tb.capH[dev] : 0;
+    cr.head = valid ? tb.head[r * M + dev] : 0;
+    cr.tau = (valid && lane >= 1) ? link_tau(tb, r, chain[lane - 1], dev) : 0;
+    uint64_t vb = valid ? tb.vmax[r * M + dev] : 0;
+    if (cr.tau != E2_INF64) vb = umax64(vb, cr.tau);
+    vb = umax64(vb, dpp_u64<0xb1>(vb));
+    vb = umax64(vb, dpp_u64<0x4e>(vb));
+    vb = umax64(vb, dpp_u64<0x141>(vb));
+    vb = umax64(vb, dpp_u64<0x140>(vb));
+    *bound = umax64(umax64(readlane_u64(vb, 0), readlane_u64(vb, 16)),
+                    umax64(readlane_u64(vb, 32), readlane_u64(vb, 48)));
+    const int pre = scan_incl_i32(cap0, lane);
     const int tot = lane_i(pre, m - 1);
     int lo = max(k1 - 1, N - 1 - (tot - pre));
     int hi = min(N - 1 - (m - k1), pre - 1);
     if (hi < lo) { lo = 1; hi = 0; }
-    cr.flo = lo;
-    cr.fhi = hi;
     const int size = (valid && k1 < m) ? hi - lo + 1 : 0;
     const int size_incl = scan_incl_i32(size, lane);
-    cr.off = size_incl - size;
+    const int off = size_incl - size;
     const int pool_need = lane_i(size_incl, kWave - 1);
-    cr.lmin0 = (valid && lo <= hi) ? tb.minwin[(size_t)cr.dev * N + lo] : 0;
-    cr.lmin1 = (valid && lo <= hi) ? tb.minwin[((size_t)M + cr.dev) * N + lo] : 0;
+    const int lmin0 = (valid && lo <= hi) ? tb.minwin[(size_t)dev * N + lo] : 0;
+    const int lmin1 = (valid && lo <= hi) ? tb.minwin[((size_t)M + dev) * N + lo] : 0;
     // reversed row t = k1 covers original position kk = m+1-t: blocks j..N-1
     // with max(kk-1, N-(tot-pre[kk-1])) <= j <= min(N-(m-kk+1), pre[kk-1]),
     // i.e. reversed cells x = N-1-j
     const int kk = m + 1 - k1;
     const int src = max(0, min(kWave - 1, kk - 1));
-    cr.devR = __shfl(cr.dev, src, kWave);
-    cr.capR = __shfl(cr.cap0, src, kWave);
+    const int devR = __shfl(dev, src, kWave);
+    const int capR = __shfl(cap0, src, kWave);
     const int pre_km1 = (kk >= 2) ? __shfl(pre, max(0, kk - 2), kWave) : 0;
     cr.tauR = __shfl(cr.tau, max(0, min(kWave - 1, kk)), kWave);  // link kk -> kk+1
+    int glo = 1, ghi = 0, lminR = 0;
     {
         const bool vr = k1 < m;
-        int gl = max(kk - 1, N - (tot - pre_km1));
-        int gh = min(pre_km1, N - (m - kk + 1));
-        if (!vr || gh < gl) { cr.glo = 1; cr.ghi = 0; }
-        else { cr.glo = N - 1 - gh; cr.ghi = N - 1 - gl; }
-        cr.lminR = (vr && cr.glo <= cr.ghi) ? tb.minwinR[(size_t)cr.devR * N + cr.glo] : 0;
+        const int gl = max(kk - 1, N - (tot - pre_km1));
+        const int gh = min(pre_km1, N - (m - kk + 1));
+        if (vr && gh >= gl) {
+            glo = N - 1 - gh;
+            ghi = N - 1 - gl;
+            lminR = tb.minwinR[(size_t)devR * N + glo];
+        }
     }
-    if (pool_need > sm.pool_cells) return false;
+    cr.wa = (uint32_t)dev | (uint32_t)cap0 << 8 | (uint32_t)capH << 16 | (uint32_t)lmin0 << 24;
+    cr.wb = (uint32_t)lo | (uint32_t)hi << 8 | (uint32_t)lmin1 << 16;
+    cr.wc = ((uint32_t)off & 0xFFFFu) | (uint32_t)lminR << 16 | (uint32_t)capR << 24;
+    cr.wd = (uint32_t)devR | (uint32_t)glo << 8 | (uint32_t)ghi << 16;
+    return pool_need <= sm.pool_cells;
+}
 
-    uint64_t *Rw[2] = {sm.Rw0, sm.Rw1};
+// The banded DP of one chain with keys of width K.  Returns the optimum as
+// a u64 (INF if none) and its master position in *mu_out (0 if none); the
+// stage starts go to start[].
+template <typename K>
+__device__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs &cr, int r, int m,
+                          int lane, uint64_t *T_out, int *mu_out, uint8_t *start, uint8_t *last_tb)
+{
+    const int N = tb.N, M = tb.M;
+    PS<K> *ps = static_cast<PS<K> *>(sm.ps);
+    K *pool = reinterpret_cast<K *>(sm.pool);
+    K *Rw[2] = {reinterpret_cast<K *>(sm.Rw0), reinterpret_cast<K *>(sm.Rw1)};
     // ---- forward rows F_1..F_{m-1}: LDS ping-pong + global pool + split points
     for (int k = 1; k < m; ++k) {
-        Row rw = fwd_row_of(tb, cr, r, k, 0);
-        if (k >= 2) set_prev(rw, Rw[(k - 1) & 1], lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
-        const int off = lane_i(cr.off, k - 1);
-        row_pass(rw, store_to(Rw[k & 1], sm.pool + off, sm.tbp + off), sm.ps, lane, N);
+        Row<K> rw = fwd_row_of<K>(tb, cr, r, k, 0);
+        if (k >= 2) set_prev(rw, (const K *)Rw[(k - 1) & 1], band_lo(cr, k - 1), band_hi(cr, k - 1));
+        const int off = pool_off(cr, k);
+        row_pass(rw, store_to<K>(Rw[k & 1], pool + off, sm.tbp + off), ps, lane, N);
     }
     // the combines read the forward rows back from the pool
     __builtin_amdgcn_s_waitcnt(0);
@@ -611,82 +710,85 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
 
     // ---- combines: master m (its stage ends at N-1), then, after each
     // reversed row t = 1..m-1 (backward row m+1-t), master m - t
-    uint64_t acc = E2_INF64;
+    K acc = KeyT<K>::inf;
     {
-        Row rw = fwd_row_of(tb, cr, r, m, m);
+        Row<K> rw = fwd_row_of<K>(tb, cr, r, m, m);
         if (rw.cap > 0) {
             if (m >= 2)
-                set_prev(rw, sm.pool + lane_i(cr.off, m - 2), lane_i(cr.flo, m - 2),
-                         lane_i(cr.fhi, m - 2));
-            RowOut ro = store_to(nullptr, nullptr, nullptr);
+                set_prev(rw, (const K *)(pool + pool_off(cr, m - 1)), band_lo(cr, m - 1),
+                         band_hi(cr, m - 1));
+            RowOut<K> ro = store_to<K>(nullptr, nullptr, nullptr);
             ro.combine = true;
             ro.last_only = true;
             ro.mu = m;
-            acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
+            acc = kmin(acc, row_pass(rw, ro, ps, lane, N));
         }
     }
     for (int t = 1; t < m; ++t) {
-        const int c = lane_i(cr.devR, t - 1);
-        Row g;
+        const uint32_t wc = lane_w(cr.wc, t - 1), wd = lane_w(cr.wd, t - 1);
+        const int c = f8(wd, 0);
+        Row<K> g;
         g.pr = prefR_row(tb, r, c);
         g.wr = tb.winR + (size_t)c * N;
         g.hadd = 0;
-        g.tau = (t >= 2) ? lane_u64(cr.tauR, t - 1) : 0;
-        g.lo = lane_i(cr.glo, t - 1);
-        g.hi = lane_i(cr.ghi, t - 1);
+        g.tau = (t >= 2) ? to_k<K>(lane_u64(cr.tauR, t - 1)) : (K)0;
+        g.lo = f8(wd, 8);
+        g.hi = f8(wd, 16);
         g.kmin = t - 1;
-        g.cap = lane_i(cr.capR, t - 1);
-        g.lmin = lane_i(cr.lminR, t - 1);
+        g.cap = f8(wc, 24);
+        g.lmin = f8(wc, 16);
         g.prev = nullptr;
         g.plo = 1;
         g.phi = 0;
-        if (t >= 2) set_prev(g, Rw[(t - 1) & 1], lane_i(cr.glo, t - 2), lane_i(cr.ghi, t - 2));
-        uint64_t *Gt = Rw[t & 1];
-        row_pass(g, store_to(Gt, nullptr, nullptr), sm.ps, lane, N);
+        if (t >= 2)
+            set_prev(g, (const K *)Rw[(t - 1) & 1], f8(lane_w(cr.wd, t - 2), 8),
+                     f8(lane_w(cr.wd, t - 2), 16));
+        K *Gt = Rw[t & 1];
+        row_pass(g, store_to<K>(Gt, nullptr, nullptr), ps, lane, N);
         const int mu = m - t;
-        Row rw = fwd_row_of(tb, cr, r, mu, mu);
+        Row<K> rw = fwd_row_of<K>(tb, cr, r, mu, mu);
         if (rw.cap > 0) {
             if (mu >= 2)
-                set_prev(rw, sm.pool + lane_i(cr.off, mu - 2), lane_i(cr.flo, mu - 2),
-                         lane_i(cr.fhi, mu - 2));
-            RowOut ro = store_to(nullptr, nullptr, nullptr);
+                set_prev(rw, (const K *)(pool + pool_off(cr, mu - 1)), band_lo(cr, mu - 1),
+                         band_hi(cr, mu - 1));
+            RowOut<K> ro = store_to<K>(nullptr, nullptr, nullptr);
             ro.combine = true;
             ro.G = Gt;
             ro.glo = g.lo;
             ro.ghi = g.hi;
-            ro.tau_next = lane_u64(cr.tau, mu);  // link mu -> mu+1
+            ro.tau_next = to_k<K>(lane_u64(cr.tau, mu));  // link mu -> mu+1
             ro.mu = mu;
-            acc = umin64(acc, row_pass(rw, ro, sm.ps, lane, N));
+            acc = kmin(acc, row_pass(rw, ro, ps, lane, N));
         }
     }
-    const uint64_t key = wave_min_u64(acc);
-    const uint64_t best = unpack_val(key);
-    const int best_mu = best == E2_INF64 ? 0 : (int)(key & 0xFF);
-    *T_out = best;
+    const K key = wave_min_k(acc);
+    const K bestk = unpack_val(key);
+    const int best_mu = bestk == KeyT<K>::inf ? 0 : (int)(key & 0xFF);
+    *T_out = to_u64(bestk);
     *mu_out = best_mu;
-    if (best == E2_INF64) return true;
+    if (bestk == KeyT<K>::inf) return;
 
     // ---- rows mu*..m-1 of the chosen master's table (split points overwrite
     // those of F), then cell N-1 of row m
     for (int k = best_mu; k < m; ++k) {
-        Row rw = fwd_row_of(tb, cr, r, k, best_mu);
+        Row<K> rw = fwd_row_of<K>(tb, cr, r, k, best_mu);
         if (k >= 2) {
-            const uint64_t *prev = (k == best_mu) ? sm.pool + lane_i(cr.off, k - 2)
-                                                  : Rw[(k - 1) & 1];
-            set_prev(rw, prev, lane_i(cr.flo, k - 2), lane_i(cr.fhi, k - 2));
+            const K *prev = (k == best_mu) ? (const K *)(pool + pool_off(cr, k - 1))
+                                           : (const K *)Rw[(k - 1) & 1];
+            set_prev(rw, prev, band_lo(cr, k - 1), band_hi(cr, k - 1));
         }
-        const int off = lane_i(cr.off, k - 1);
-        row_pass(rw, store_to(Rw[k & 1], nullptr, sm.tbp + off), sm.ps, lane, N);
+        const int off = pool_off(cr, k);
+        row_pass(rw, store_to<K>(Rw[k & 1], nullptr, sm.tbp + off), ps, lane, N);
     }
     if (m >= 2) {
-        Row rw = fwd_row_of(tb, cr, r, m, best_mu);
-        const uint64_t *prev = (best_mu == m) ? sm.pool + lane_i(cr.off, m - 2)
-                                              : Rw[(m - 1) & 1];
-        set_prev(rw, prev, lane_i(cr.flo, m - 2), lane_i(cr.fhi, m - 2));
+        Row<K> rw = fwd_row_of<K>(tb, cr, r, m, best_mu);
+        const K *prev = (best_mu == m) ? (const K *)(pool + pool_off(cr, m - 1))
+                                       : (const K *)Rw[(m - 1) & 1];
+        set_prev(rw, prev, band_lo(cr, m - 1), band_hi(cr, m - 1));
         rw.lo = rw.hi = N - 1;
-        rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + lane_i(cr.dev, m - 1)) * N + (N - 1)];
+        rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + f8(lane_w(cr.wa, m - 1), 0)) * N + (N - 1)];
         rw.lmin = uni(rw.lmin);
-        row_pass(rw, store_to(Rw[m & 1], nullptr, last_tb), sm.ps, lane, N);
+        row_pass(rw, store_to<K>(Rw[m & 1], nullptr, last_tb), ps, lane, N);
         if (lane == 0) {
             int i = N - 1;
             int j = *last_tb;
@@ -694,11 +796,11 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
             start[m - 1] = (uint8_t)j;
             i = j - 1;
             for (int k = m - 1; k >= 2; --k) {
-                const int blo = lane_i(cr.flo, k - 1), bhi = lane_i(cr.fhi, k - 1);
+                const int blo = band_lo(cr, k), bhi = band_hi(cr, k);
                 // path cells lie in their band; the clamp only keeps a
                 // corrupted table from indexing outside its row
                 const int ii = i < blo ? blo : (i > bhi ? bhi : i);
-                j = sm.tbp[lane_i(cr.off, k - 1) + (ii - blo)];
+                j = sm.tbp[pool_off(cr, k) + (ii - blo)];
                 if (j > i) j = i;
                 start[k - 1] = (uint8_t)j;
                 i = j - 1;
@@ -707,7 +809,6 @@ __device__ bool dp_banded(const E2Tables &tb, const DpSmem &sm, int r, const uin
     }
     if (lane == 0) start[0] = 0;
     __syncthreads();
-    return true;
 }
 
 // Reference path (chains whose bands exceed the pool): Algorithm 1's table
@@ -717,11 +818,12 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
                              int m, int mu, uint8_t *tbp, int lane)
 {
     const int N = tb.N;
+    PS<uint64_t> *ps = static_cast<PS<uint64_t> *>(sm.ps);
     uint64_t *cur = sm.Ga, *prv = sm.Gb;
     for (int k = 1; k <= m; ++k) {
         const int c = uni(chain[k - 1]);
         const int f = (mu == k);
-        Row rw;
+        Row<uint64_t> rw;
         rw.pr = pref_row(tb, r, c);
         rw.wr = win_row(tb, f, c);
         rw.hadd = f ? uni64(tb.head[r * tb.M + c]) : 0;
@@ -742,9 +844,9 @@ __device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const 
             rw.phi = N - 1;
         }
         row_pass(rw,
-                 store_to(cur, nullptr, (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1)
-                                                        : nullptr),
-                 sm.ps, lane, N);
+                 store_to<uint64_t>(cur, nullptr,
+                                    (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1) : nullptr),
+                 ps, lane, N);
         uint64_t *tmp = prv;
         prv = cur;
         cur = tmp;
@@ -775,7 +877,7 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
     DpSmem sm;
-    sm.ps = reinterpret_cast<PS *>(dyn);
+    sm.ps = dyn;
     sm.Rw0 = dyn + 2 * N;
     sm.Rw1 = sm.Rw0 + (N + 1);
     sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
@@ -818,7 +920,14 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
 
         uint64_t best = E2_INF64;
         int best_mu = 0;
-        if (!dp_banded(tb, sm, r, chain, m, lane, &best, &best_mu, start, &last_tb)) {
+        ChainRegs cr;
+        uint64_t bound = E2_INF64;
+        const bool banded = chain_regs(tb, sm, r, chain, m, lane, cr, &bound);
+        if (banded && bound <= kU32MaxValue)
+            dp_banded<uint32_t>(tb, sm, cr, r, m, lane, &best, &best_mu, start, &last_tb);
+        else if (banded)
+            dp_banded<uint64_t>(tb, sm, cr, r, m, lane, &best, &best_mu, start, &last_tb);
+        else {
             // reference path: a full table per master, then the chosen
             // master's table again with split points
             for (int mu = 1; mu <= m; ++mu) {
@@ -1050,9 +1159,35 @@ size_t e2_dp_lds_bytes(int N)
     return (size_t)16 * N + (size_t)16 * (N + 1) + (size_t)e2_dp_pool_cells(N);
 }
 
-int e2_dp_slots(int problems)
+int e2_dp_slots(int N, int problems)
 {
-    const int cap = 256 * 20;  // 20 one-wave workgroups per CU on a 256-CU part
+    // resident one-wave workgroups per CU for this LDS size (the occupancy
+    // the compiled kernel reaches), times the CUs of the device
+    static int per_cu[256];
+    static int n_cu;
+    if (N < 1 || N > 255) return 1;
+    if (n_cu == 0) {
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                hipSuccess ||
+            cus < 1) {
+            (void)hipGetLastError();
+            cus = 256;
+        }
+        n_cu = cus;
+    }
+    if (per_cu[N] == 0) {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_dp, 64, e2_dp_lds_bytes(N)) !=
+                hipSuccess ||
+            nb < 1) {
+            (void)hipGetLastError();
+            nb = 20;
+        }
+        per_cu[N] = nb > 32 ? 32 : nb;
+    }
+    const int cap = n_cu * per_cu[N];
     return problems < cap ? (problems > 0 ? problems : 1) : cap;
 }
 
