@@ -1,0 +1,149 @@
+"""The bench's work accounting (host logic, no GPU).
+
+bench.generation_work counts, with vectorised prefix tables, the useful
+j-candidates the DP kernel evaluates, split by key width; the roofline's
+`achieved` is built from it.  Here the same counts come from a direct walk
+over every row, cell and window of the banded decomposition, and the key
+width from a direct scan of every stage that fits memory.
+"""
+import numpy as np
+import pytest
+
+import bench
+import oracle
+import paper_2606_03770_amd as e2
+from paper_2606_03770_amd import workload
+
+INF = bench.INF
+
+
+def _windows(wl):
+    """Smallest fitting start per stage end, by brute force over starts."""
+    M, N = wl.n_dev, wl.n_layer
+    b = [int(x) for x in wl.layer_bytes]
+    win = np.full((2, M, N), 255, dtype=np.int64)
+    winR = np.full((M, N), 255, dtype=np.int64)
+    for d in range(M):
+        mem = int(wl.mem_bytes[d])
+        for f in range(2):
+            extra = int(wl.head_bytes) if f else 0
+            for i in range(N):
+                for j in range(i + 1):
+                    if sum(b[j:i + 1]) + extra <= mem:
+                        win[f, d, i] = j
+                        break
+        for x in range(N):          # reversed blocks y..x = blocks N-1-x..N-1-y
+            for y in range(x + 1):
+                if sum(b[N - 1 - x:N - y]) <= mem:
+                    winR[d, x] = y
+                    break
+    return win, winR
+
+
+def _direct(wl, labels, roles, T, master):
+    N, K = wl.n_layer, wl.k_max
+    win, winR = _windows(wl)
+    t, h, tau = e2.e2_quantise(wl.problem_arrays())
+    cap = np.zeros((2, wl.n_dev), dtype=np.int64)
+    for f in range(2):
+        for d in range(wl.n_dev):
+            ok = win[f, d] != 255
+            cap[f, d] = max((i - win[f, d, i] + 1 for i in range(N) if ok[i]), default=0)
+
+    def stage_max(r, d):
+        best = 0
+        for f in range(2):
+            for i in range(N):
+                j = int(win[f, d, i])
+                if j != 255:
+                    best = max(best, int(t[r, d, j:i + 1].sum()) + (int(h[r, d]) if f else 0))
+        return best
+
+    def cnt(w, kmin, lo, hi):
+        return sum(max(0, i - max(int(w[i]), kmin) + 1) for i in range(lo, hi + 1) if w[i] != 255)
+
+    c64 = c32 = 0
+    for p in range(labels.shape[0]):
+        for q in range(K):
+            ch = np.nonzero(labels[p] == q)[0]
+            m = len(ch)
+            if m == 0:
+                continue
+            c0, cH = cap[0][ch], cap[1][ch]
+            if not (m <= N and c0.sum() >= N and c0.min() >= 1 and cH.max() >= 1):
+                continue
+            r = int(roles[p, q] != 0)
+            pre = np.r_[0, np.cumsum(c0)]
+            tot = pre[m]
+            flo = {k: max(k - 1, N - 1 - (tot - pre[k])) for k in range(1, m + 1)}
+            fhi = {k: min(N - 1 - (m - k), pre[k] - 1) for k in range(1, m + 1)}
+            pool = sum(max(0, fhi[k] - flo[k] + 1) for k in range(1, m))
+            mu = int(np.nonzero(ch == master[p, q])[0][0]) + 1 if T[p, q] != INF else 0
+            c = 0
+            banded = m <= 64 and pool <= bench.POOL_CELLS
+            if banded:
+                for k in range(2, m):                            # forward rows
+                    c += cnt(win[0][ch[k - 1]], max(k - 1, flo[k] - c0[k - 1] + 1), flo[k], fhi[k])
+                for mm in range(2, m + 1):                       # combines
+                    if cH[mm - 1] > 0:
+                        c += cnt(win[1][ch[mm - 1]], max(mm - 1, flo[mm] - cH[mm - 1] + 1),
+                                 flo[mm], fhi[mm])
+                for tt in range(2, m):                           # reversed rows
+                    kd = m + 1 - tt
+                    gl = max(kd - 1, N - (tot - pre[kd - 1]))
+                    gh = min(pre[kd - 1], N - (m - kd + 1))
+                    if gh >= gl:
+                        c += cnt(winR[ch[kd - 1]], max(tt - 1, N - 1 - gh - c0[kd - 1] + 1),
+                                 N - 1 - gh, N - 1 - gl)
+                if mu:                                           # chosen master's rows
+                    for k in range(max(mu, 2), m):
+                        f = int(k == mu)
+                        cp = cH[k - 1] if f else c0[k - 1]
+                        c += cnt(win[f][ch[k - 1]], max(k - 1, flo[k] - cp + 1), flo[k], fhi[k])
+                    if m >= 2:
+                        f = int(mu == m)
+                        cp = cH[m - 1] if f else c0[m - 1]
+                        c += cnt(win[f][ch[m - 1]], max(m - 1, N - cp), N - 1, N - 1)
+            else:                                                # one table per master
+                for mm in list(range(1, m + 1)) + ([mu] if mu else []):
+                    for k in range(2, m + 1):
+                        c += cnt(win[int(k == mm)][ch[k - 1]], k - 1, k - 1, N - 1)
+            links = [int(tau[r, ch[k - 1], ch[k]]) for k in range(1, m)]
+            bound = max([stage_max(r, d) for d in ch] + [x for x in links if x != INF])
+            if banded and bound <= bench.U32_MAX_VALUE:
+                c32 += c
+            else:
+                c64 += c
+    return c64, c32
+
+
+@pytest.mark.parametrize("name,P", [("c1_tiny_12dev_32L", 16), ("c2_32dev_48L", 24),
+                                    ("c5_256dev_126L_ga", 6)])
+def test_candidate_counts_match_a_direct_walk(orc, name, P):
+    wl = workload.make(name, population=P)
+    sol = oracle.eval_population(wl)
+    win, winR, cap = bench.window_tables(wl)
+    tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
+    cells, c64, c32 = bench.generation_work(wl, wl.labels, wl.roles, sol["T"], sol["master"], tabs)
+    assert (c64, c32) == _direct(wl, wl.labels, wl.roles, sol["T"], sol["master"])
+    assert c64 + c32 > 0
+    if name.startswith("c5"):
+        assert c32 > 0 and c64 > 0   # both key widths occur
+
+
+def test_reference_path_counts():
+    """Chains with more than 64 devices take one full table per master."""
+    wl = workload.random_small(3, M=70, N=80, P=1, k_max=1, mem_lo_layers=3, mem_hi_layers=30)
+    sol = oracle.eval_population(wl)
+    win, winR, cap = bench.window_tables(wl)
+    tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
+    _, c64, c32 = bench.generation_work(wl, wl.labels, wl.roles, sol["T"], sol["master"], tabs)
+    assert (c64, c32) == _direct(wl, wl.labels, wl.roles, sol["T"], sol["master"])
+    assert c64 > 0 and c32 == 0   # the reference path has u64 keys only
+
+
+def test_window_tables_match_brute_force():
+    wl = workload.random_small(11, M=9, N=21, P=1, k_max=2, mem_lo_layers=1, mem_hi_layers=12)
+    win, winR, _ = bench.window_tables(wl)
+    w2, wR2 = _windows(wl)
+    assert (win == w2).all() and (winR == wR2).all()
