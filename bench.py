@@ -15,10 +15,11 @@ Printed on one JSON line:
   fitness_evals_per_s   genomes scored per second
   roofline     the DP kernel k_dp (timed with HIP events the library records
                around it on the call's stream) against the int32 VALU peak:
-               int32 VALU ops per useful j-candidate of the DP kernel, 8 with
-               u64 keys (64-bit subtract 2, max 3, min 3) and 3 with u32 keys
-               (subtract, max, min), candidates counted on the host from the
-               same inputs; traffic = HBM bytes per launch
+               VALU ops per useful j-candidate of the DP kernel, 3 with u32 or
+               fp64 keys (subtract, max, min; fp64 vector ops issue at the
+               int32 rate on MI355X) and 8 with the u64 keys of the reference
+               path (64-bit subtract 2, max 3, min 3), candidates counted on
+               the host from the same inputs; traffic = HBM bytes per launch
                from the committed rocprofv3 counters when they were taken on
                the current kernel sources
   cpu_baseline the CPU oracle on a bounded sample of the same generation-0
@@ -57,7 +58,8 @@ def log(msg):
 # ---------------------------------------------------------------------------
 POOL_CELLS = 2048  # forward-row pool of a whole-wave DP problem (k_dp)
 U32_MAX_VALUE = 0xFFFFFE  # largest finite value of the u32-key path
-OPS_PER_CANDIDATE_U32 = 3  # 32-bit subtract, max, min
+F64_LIMIT = 1 << 45       # prefix sums, head and link times of an fp64-key problem stay below
+OPS_PER_CANDIDATE_NARROW = 3  # u32 or fp64 keys: subtract, max, min
 
 
 
@@ -107,10 +109,13 @@ def count_tables(win, winR, N):
 
 def value_bounds(wl, win):
     """vmax[r][d]: the largest cost of a memory-fitting stage of device d in
-    role r (plus the head time for stages holding the head bytes), and the
-    quantised link times tau[r][d][e] (INF for dead links)."""
+    role r (plus the head time for stages holding the head bytes); vtot[r][d]:
+    the time of all blocks plus the head; and the quantised link times
+    tau[r][d][e] (INF for dead links)."""
     t, h, tau = e2.e2_quantise(wl.problem_arrays())
     M, N = wl.n_dev, wl.n_layer
+    vtot = np.array([[int(t[r, d].sum(dtype=np.uint64)) + int(h[r, d]) for d in range(M)]
+                     for r in range(2)], dtype=object)
     vmax = np.zeros((2, M), dtype=object)
     for r in range(2):
         P = np.concatenate([np.zeros((M, 1), np.uint64), np.cumsum(t[r], axis=1, dtype=np.uint64)],
@@ -124,19 +129,22 @@ def value_bounds(wl, win):
                     c = P[d, i + 1] - P[d, win[f, d, i]]
                     best = max(best, int(c.max()) + (int(h[r, d]) if f else 0))
             vmax[r, d] = best
-    return vmax, tau
+    return vmax, vtot, tau
 
 
 def generation_work(wl, labels, roles, T, master, tabs):
     """(Algorithm 1 cells over feasible problems, useful j-candidates the DP
-    kernel evaluates with u64 keys, those it evaluates with u32 keys) for one
-    population.  The candidate count follows k_dp row by row: forward rows,
-    reversed rows, one combine per master, the chosen master's rows and last
-    cell (or, for chains whose bands exceed the pool, one full table per
-    master plus the chosen master's again).  A banded problem takes u32 keys
-    when every finite value it can produce (largest fitting stage cost of its
-    devices, largest finite link time) is at most U32_MAX_VALUE."""
-    win, winR, cap, C, CR, vmax, tau = tabs
+    kernel evaluates with u64 keys, those it evaluates with u32 or fp64 keys)
+    for one population.  The candidate count follows k_dp row by row:
+    forward rows, reversed rows, one combine per master, the chosen master's
+    rows and last cell (banded path), or one full table per master plus the
+    chosen master's again (reference path, u64 keys).  A problem takes the
+    banded path when its chain has at most 64 devices, its forward bands fit
+    the pool and either every finite value it can produce (largest fitting
+    stage cost of its devices, largest finite link time) is at most
+    U32_MAX_VALUE (u32 keys) or its devices' total times and its link times
+    are below F64_LIMIT (fp64 keys)."""
+    win, winR, cap, C, CR, vmax, vtot, tau = tabs
     N, K = wl.n_layer, wl.k_max
     P, M = labels.shape
     feasible = T != INF
@@ -180,11 +188,12 @@ def generation_work(wl, labels, roles, T, master, tabs):
         ch, c0, cH, feas, pq = ch[listed], c0[listed], cH[listed], feas[listed], pq[listed]
         n = len(ch)
         rr = (roles[pq[:, 0], pq[:, 1]] != 0).astype(np.int64)
-        bnd = np.array([max([vmax[rr[a], d] for d in ch[a]] +
-                            [int(tau[rr[a], ch[a][k - 1], ch[a][k]]) for k in range(1, m)
-                             if int(tau[rr[a], ch[a][k - 1], ch[a][k]]) != INF])
-                        for a in range(n)], dtype=object)
-        narrow = np.array([b <= U32_MAX_VALUE for b in bnd], dtype=bool)
+        links = [[int(tau[rr[a], ch[a][k - 1], ch[a][k]]) for k in range(1, m)] for a in range(n)]
+        links = [[x for x in lk if x != INF] for lk in links]
+        b32 = [max([vmax[rr[a], d] for d in ch[a]] + links[a]) for a in range(n)]
+        b64 = [max([vtot[rr[a], d] for d in ch[a]] + links[a]) for a in range(n)]
+        narrow = np.array([b <= U32_MAX_VALUE or bt < F64_LIMIT for b, bt in zip(b32, b64)],
+                          dtype=bool)
         mu = np.zeros(n, dtype=np.int64)
         mdev = master[pq[:, 0], pq[:, 1]].astype(np.int64)
         for a in range(n):
@@ -199,7 +208,7 @@ def generation_work(wl, labels, roles, T, master, tabs):
         pool = sizes[:, :m - 1].sum(1)
         # chains of up to 64 devices whose forward bands fit the pool take the
         # banded path, the others one full table per master
-        fast = (m <= 64) & (pool <= POOL_CELLS)
+        fast = (m <= 64) & (pool <= POOL_CELLS) & narrow
         # --- fast path
         if fast.any():
             chf, c0f, cHf = ch[fast], c0[fast], cH[fast]
@@ -239,9 +248,7 @@ def generation_work(wl, labels, roles, T, master, tabs):
                 v0 = rows(0, chf[:, m - 1], jm, np.full(len(chf), N - 1), np.full(len(chf), N - 1))
                 v1 = rows(1, chf[:, m - 1], jm, np.full(len(chf), N - 1), np.full(len(chf), N - 1))
                 tot_f += np.where(ff, np.where(isn, v1, v0), 0)
-            nf = narrow[fast]
-            cand += int(tot_f[~nf].sum())
-            cand32 += int(tot_f[nf].sum())
+            cand32 += int(tot_f.sum())
         # --- reference path
         if (~fast).any():
             chs, mus = ch[~fast], mu[~fast]
@@ -350,7 +357,7 @@ def main():
         Lr, Rr = lo, ro
     value = cells / elapsed
     dp_time = dp_ms / 1e3
-    achieved = (cand * OPS_PER_CANDIDATE + cand32 * OPS_PER_CANDIDATE_U32) / dp_time
+    achieved = (cand * OPS_PER_CANDIDATE + cand32 * OPS_PER_CANDIDATE_NARROW) / dp_time
     traffic = profiled_traffic(wl.name)
     result = {
         "metric": METRIC,
@@ -371,7 +378,7 @@ def main():
         "fitness_evals_per_s": P * args.steps / elapsed,
         "dp_cells_per_step": cells / args.steps,
         "j_candidates_per_step": (cand + cand32) / args.steps,
-        "j_candidates_u32_keys_per_step": cand32 / args.steps,
+        "j_candidates_u32_or_f64_keys_per_step": cand32 / args.steps,
         "roofline": {"bound": "alu", "kernel": "k_dp",
                      "achieved": achieved / 1e12, "peak": INT_VALU_PEAK / 1e12,
                      "unit": "TOP/s (int32 VALU)", "frac": achieved / INT_VALU_PEAK,

@@ -279,6 +279,14 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
                 }
             vmax[(size_t)r * M + d] = best;
         }
+    // largest prefix sum (+ head time) per role and device: every shifted
+    // prefix sum of a chain stays below 2^53 when these and its link times
+    // are below 2^45
+    std::vector<uint64_t> vtot((size_t)2 * M, 0);
+    for (int r = 0; r < 2; ++r)
+        for (int d = 0; d < M; ++d)
+            vtot[(size_t)r * M + d] =
+                pref[((size_t)r * M + d) * (N + 1) + N] + h[(size_t)r * M + d];
 
     const size_t b_pref = align256(pref.size() * 8), b_head = align256(h.size() * 8),
                  b_tau = align256(tau.size() * 8), b_win = align256(win.size()),
@@ -286,7 +294,7 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     const size_t b_mw = align256(minwin.size()), b_mwR = align256(minwinR.size());
     const size_t b_vmax = align256(vmax.size() * 8);
     const size_t total =
-        2 * b_pref + b_head + b_tau + b_win + b_winR + b_mw + b_mwR + 2 * b_cap + b_vmax;
+        2 * b_pref + b_head + b_tau + b_win + b_winR + b_mw + b_mwR + 2 * b_cap + 2 * b_vmax;
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
     if (!ctx) return E2_ENOMEM;
     if (hipGetDevice(&ctx->device) != hipSuccess) {
@@ -310,6 +318,7 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     char *d_cap0 = d_mwR + b_mwR;
     char *d_capH = d_cap0 + b_cap;
     char *d_vmax = d_capH + b_cap;
+    char *d_vtot = d_vmax + b_vmax;
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMemcpy(d_pref, pref.data(), pref.size() * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d_head, h.data(), h.size() * 8, hipMemcpyHostToDevice);
@@ -325,6 +334,8 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     if (e == hipSuccess) e = hipMemcpy(d_capH, capH.data(), (size_t)M, hipMemcpyHostToDevice);
     if (e == hipSuccess)
         e = hipMemcpy(d_vmax, vmax.data(), vmax.size() * 8, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(d_vtot, vtot.data(), vtot.size() * 8, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(ctx->blob);
         free(ctx);
@@ -344,6 +355,7 @@ int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
     ctx->tables.cap0 = reinterpret_cast<const uint8_t *>(d_cap0);
     ctx->tables.capH = reinterpret_cast<const uint8_t *>(d_capH);
     ctx->tables.vmax = reinterpret_cast<const uint64_t *>(d_vmax);
+    ctx->tables.vtot = reinterpret_cast<const uint64_t *>(d_vtot);
     ctx->tables.M = M;
     ctx->tables.N = N;
     *out = ctx;

@@ -26,6 +26,7 @@ struct E2Tables {
     const uint8_t *capH;   // [M] most blocks one stage can hold with the head
     const uint64_t *vmax;  // [2][M] largest cost of a fitting stage (+ head time when it
                            //   holds the head bytes) per role and device
+    const uint64_t *vtot;  // [2][M] total time of all blocks + head time per role and device
     int M;
     int N;
 };

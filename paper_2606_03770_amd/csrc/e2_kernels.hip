@@ -65,6 +65,15 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
     return umin64(umin64(readlane_u64(v, 0), readlane_u64(v, 16)),
                   umin64(readlane_u64(v, 32), readlane_u64(v, 48)));
 }
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
+{
+    v = umax64(v, dpp_u64<0xb1>(v));
+    v = umax64(v, dpp_u64<0x4e>(v));
+    v = umax64(v, dpp_u64<0x141>(v));
+    v = umax64(v, dpp_u64<0x140>(v));
+    return umax64(umax64(readlane_u64(v, 0), readlane_u64(v, 16)),
+                  umax64(readlane_u64(v, 32), readlane_u64(v, 48)));
+}
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
 {
     v += dpp_u64<0xb1>(v);
@@ -254,18 +263,51 @@ template <> struct KeyT<uint32_t> {
     static constexpr uint32_t inf = 0xFFFFFFFFu;
     static constexpr uint32_t inf_key = 0xFFFFFF00u;
 };
-constexpr uint64_t kU32MaxValue = 0xFFFFFEull;  // largest finite value of the 32-bit path
+// fp64 keys: value * 256 + j is an integer below 2^53, so sums, differences,
+// max and min are exact; INF is +infinity
+template <> struct KeyT<double> {
+    static constexpr double inf = __builtin_huge_val();
+    static constexpr double inf_key = __builtin_huge_val();
+};
+constexpr uint64_t kU32MaxValue = 0xFFFFFEull;         // largest finite value of the 32-bit path
+constexpr uint64_t kF64Limit = 1ull << 45;             // every value of the fp64 path is below
 
-template <typename K> __device__ __forceinline__ K kmax(K a, K b) { return a > b ? a : b; }
-template <typename K> __device__ __forceinline__ K kmin(K a, K b) { return a < b ? a : b; }
+// fp64 keys are never NaN, so the hardware max/min are used directly (the
+// compiler's IEEE-mode fmax/fmin would first quiet every loaded operand)
+__device__ __forceinline__ double vmax_f64(double a, double b)
+{
+    double r;
+    asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ double vmin_f64(double a, double b)
+{
+    double r;
+    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+template <typename K> __device__ __forceinline__ K kmax(K a, K b)
+{
+    if constexpr (__is_same(K, double)) return vmax_f64(a, b);
+    else return a > b ? a : b;
+}
+template <typename K> __device__ __forceinline__ K kmin(K a, K b)
+{
+    if constexpr (__is_same(K, double)) return vmin_f64(a, b);
+    else return a < b ? a : b;
+}
 template <int CTRL, typename K> __device__ __forceinline__ K dppk(K v)
 {
-    if constexpr (sizeof(K) == 8) return dpp_u64<CTRL>(v);
+    if constexpr (__is_same(K, double))
+        return __builtin_bit_cast(double, dpp_u64<CTRL>(__builtin_bit_cast(uint64_t, v)));
+    else if constexpr (sizeof(K) == 8) return dpp_u64<CTRL>(v);
     else return (K)(uint32_t)dpp_i32<CTRL>((int)v);
 }
 template <typename K> __device__ __forceinline__ K readlane_k(K v, int lane)
 {
-    if constexpr (sizeof(K) == 8) return readlane_u64(v, lane);
+    if constexpr (__is_same(K, double))
+        return __builtin_bit_cast(double, readlane_u64(__builtin_bit_cast(uint64_t, v), lane));
+    else if constexpr (sizeof(K) == 8) return readlane_u64(v, lane);
     else return (K)(uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 template <typename K> __device__ __forceinline__ K wave_min_k(K v)
@@ -333,17 +375,19 @@ __device__ __forceinline__ uint64_t uni64(uint64_t x)
     return ((uint64_t)hi << 32) | lo;
 }
 
+// Row starts of the per-device tables (element offsets fit in 32 bits:
+// at most 2 x 256 x 256 entries).
 __device__ __forceinline__ const uint64_t *pref_row(const E2Tables &tb, int r, int c)
 {
-    return tb.pref + ((size_t)r * tb.M + c) * (tb.N + 1);
+    return tb.pref + (uint32_t)((r * tb.M + c) * (tb.N + 1));
 }
 __device__ __forceinline__ const uint64_t *prefR_row(const E2Tables &tb, int r, int c)
 {
-    return tb.prefR + ((size_t)r * tb.M + c) * (tb.N + 1);
+    return tb.prefR + (uint32_t)((r * tb.M + c) * (tb.N + 1));
 }
 __device__ __forceinline__ const uint8_t *win_row(const E2Tables &tb, int f, int c)
 {
-    return tb.win + ((size_t)f * tb.M + c) * tb.N;
+    return tb.win + (uint32_t)((f * tb.M + c) * tb.N);
 }
 __device__ __forceinline__ uint64_t link_tau(const E2Tables &tb, int r, int a, int b)
 {
@@ -356,11 +400,27 @@ __device__ __forceinline__ uint64_t link_tau_u(const E2Tables &tb, int r, int a,
 }
 template <typename K> __device__ __forceinline__ K pack_prev(K prev, K tau, int j)
 {
-    return (kmax(prev, tau) << 8) | (K)j;
+    if constexpr (__is_same(K, double)) return __builtin_fma(kmax(prev, tau), 256.0, (double)j);
+    else return (kmax(prev, tau) << 8) | (K)j;
 }
 template <typename K> __device__ __forceinline__ K unpack_val(K key)
 {
-    return key >= KeyT<K>::inf_key ? KeyT<K>::inf : (key >> 8);
+    if constexpr (__is_same(K, double))
+        return key >= KeyT<K>::inf_key ? KeyT<K>::inf : __builtin_floor(key * (1.0 / 256.0));
+    else return key >= KeyT<K>::inf_key ? KeyT<K>::inf : (key >> 8);
+}
+// low 8 bits of a finite key (the split point or master position it carries)
+template <typename K> __device__ __forceinline__ int key_low8(K key)
+{
+    if constexpr (__is_same(K, double))
+        return (int)(key - __builtin_floor(key * (1.0 / 256.0)) * 256.0);
+    else return (int)(key & 0xFF);
+}
+// (v << 8) | x for a finite or infinite value v and x < 256
+template <typename K> __device__ __forceinline__ K pack_low8(K v, int x)
+{
+    if constexpr (__is_same(K, double)) return __builtin_fma(v, 256.0, (double)x);
+    else return (v << 8) | (K)x;
 }
 template <typename K> __device__ __forceinline__ K cand(const PS<K> &e, K si1)
 {
@@ -374,7 +434,7 @@ template <typename K> __device__ __forceinline__ K combine_b(int i, int N, const
 }
 template <typename K> __device__ __forceinline__ K combine_key(K v, K b, int mu)
 {
-    return (kmax(v, b) << 8) | (K)mu;
+    return pack_low8(kmax(v, b), mu);
 }
 
 template <int S, typename K>
@@ -402,7 +462,7 @@ __device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K
 }
 
 template <int S, typename K>
-__device__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int lane, int N)
+__device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int lane, int N)
 {
     constexpr int CPP = kWave / S;  // cells per pass
     const int o = lane % S;
@@ -420,12 +480,25 @@ __device__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int la
             if (ro.combine) b_nx = combine_b(i, N, ro);
         }
     }
+    // both loads of an entry go out before either is waited for: the
+    // previous-row value comes from a clamped index and is replaced by INF
+    // outside the previous band
+    const int pspan = rw.phi - rw.plo;  // < 0: empty previous band (slot 0 is read, unused)
     for (int j = jmin + lane; j <= rw.hi; j += kWave) {
-        const int pj = j - 1;
-        const K pv = (pj >= rw.plo && pj <= rw.phi) ? rw.prev[pj - rw.plo] : KeyT<K>::inf;
-        const uint64_t pj8 = rw.pr[j] << 8;
+        const int px = j - 1 - rw.plo;
+        const int pxc = max(0, min(px, pspan));
+        const uint64_t prj = rw.pr[j];
+        const K pvr = rw.prev[pxc];
+        K pv;
+        if constexpr (__is_same(K, double))
+            pv = (px < 0 || px > pspan) ? KeyT<K>::inf : pvr;
+        else  // all ones (INF) outside the previous band, without a branch
+            pv = pvr | ((K)0 - (K)(px < 0 || px > pspan));
         ps[j].a = pack_prev(pv, rw.tau, j);
-        ps[j].s = (K)(pj8 - (uint64_t)j);
+        if constexpr (__is_same(K, double))  // may be negative when blocks take 0 ns
+            ps[j].s = __builtin_fma((double)prj, 256.0, -(double)j);
+        else  // modular: only differences are used
+            ps[j].s = (K)((prj << 8) - (uint64_t)j);
     }
     __syncthreads();
     const int L = min(rw.cap, rw.hi - jmin + 1);
@@ -454,7 +527,7 @@ __device__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int la
         if (!ro.combine) {
             ro.vals[i - rw.lo] = v;
             if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
-            if (ro.tbs) ro.tbs[i - rw.lo] = (uint8_t)(best & 0xFF);
+            if (ro.tbs) ro.tbs[i - rw.lo] = (uint8_t)key_low8(best);
         } else {
             acc = kmin(acc, combine_key(v, b, ro.mu));
         }
@@ -466,7 +539,7 @@ __device__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int la
 // Store mode returns INF; combine mode returns the lane's running minimum of
 // (max(value, B) << 8 | mu) (the caller reduces over the wave once).
 template <typename K>
-__device__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int lane, int N)
+__device__ __forceinline__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int lane, int N)
 {
     if (rw.prev == nullptr) {  // first device: Eq. 2, no split point
         K acc = KeyT<K>::inf;
@@ -628,8 +701,9 @@ __device__ __forceinline__ void set_prev(Row<K> &rw, const K *prev, int plo, int
 
 // Per-position table of a chain and the largest finite value its DP can
 // produce; false when the banded path cannot take the chain.
-__device__ bool chain_regs(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
-                           int m, int lane, ChainRegs &cr, uint64_t *bound)
+__device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm, int r,
+                                           const uint8_t *chain, int m, int lane, ChainRegs &cr,
+                                           uint64_t *bound, uint64_t *bound_tot)
 {
     const int N = tb.N, M = tb.M;
     if (m > kMaxBandedChain) return false;
@@ -640,14 +714,9 @@ __device__ bool chain_regs(const E2Tables &tb, const DpSmem &sm, int r, const ui
     const int capH = valid ? tb.capH[dev] : 0;
     cr.head = valid ? tb.head[r * M + dev] : 0;
     cr.tau = (valid && lane >= 1) ? link_tau(tb, r, chain[lane - 1], dev) : 0;
-    uint64_t vb = valid ? tb.vmax[r * M + dev] : 0;
-    if (cr.tau != E2_INF64) vb = umax64(vb, cr.tau);
-    vb = umax64(vb, dpp_u64<0xb1>(vb));
-    vb = umax64(vb, dpp_u64<0x4e>(vb));
-    vb = umax64(vb, dpp_u64<0x141>(vb));
-    vb = umax64(vb, dpp_u64<0x140>(vb));
-    *bound = umax64(umax64(readlane_u64(vb, 0), readlane_u64(vb, 16)),
-                    umax64(readlane_u64(vb, 32), readlane_u64(vb, 48)));
+    const uint64_t tf = cr.tau != E2_INF64 ? cr.tau : 0;
+    *bound = wave_max_u64(umax64(valid ? tb.vmax[r * M + dev] : 0, tf));
+    *bound_tot = wave_max_u64(umax64(valid ? tb.vtot[r * M + dev] : 0, tf));
     const int pre = scan_incl_i32(cap0, lane);
     const int tot = lane_i(pre, m - 1);
     int lo = max(k1 - 1, N - 1 - (tot - pre));
@@ -690,7 +759,7 @@ __device__ bool chain_regs(const E2Tables &tb, const DpSmem &sm, int r, const ui
 // a u64 (INF if none) and its master position in *mu_out (0 if none); the
 // stage starts go to start[].
 template <typename K>
-__device__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs &cr, int r, int m,
+__device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs &cr, int r, int m,
                           int lane, uint64_t *T_out, int *mu_out, uint8_t *start, uint8_t *last_tb)
 {
     const int N = tb.N, M = tb.M;
@@ -729,7 +798,7 @@ __device__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs 
         const int c = f8(wd, 0);
         Row<K> g;
         g.pr = prefR_row(tb, r, c);
-        g.wr = tb.winR + (size_t)c * N;
+        g.wr = tb.winR + (uint32_t)(c * N);
         g.hadd = 0;
         g.tau = (t >= 2) ? to_k<K>(lane_u64(cr.tauR, t - 1)) : (K)0;
         g.lo = f8(wd, 8);
@@ -763,7 +832,7 @@ __device__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs 
     }
     const K key = wave_min_k(acc);
     const K bestk = unpack_val(key);
-    const int best_mu = bestk == KeyT<K>::inf ? 0 : (int)(key & 0xFF);
+    const int best_mu = bestk == KeyT<K>::inf ? 0 : key_low8(key);
     *T_out = to_u64(bestk);
     *mu_out = best_mu;
     if (bestk == KeyT<K>::inf) return;
@@ -814,7 +883,7 @@ __device__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs 
 // Reference path (chains whose bands exceed the pool): Algorithm 1's table
 // for one master position, full rows k-1..N-1, ping-ponging Ga/Gb; split
 // points of rows 2..m go to tbp (row k at (k-2)*N) when tbp is not null.
-__device__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
+__device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
                              int m, int mu, uint8_t *tbp, int lane)
 {
     const int N = tb.N;
@@ -921,12 +990,12 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
         uint64_t best = E2_INF64;
         int best_mu = 0;
         ChainRegs cr;
-        uint64_t bound = E2_INF64;
-        const bool banded = chain_regs(tb, sm, r, chain, m, lane, cr, &bound);
+        uint64_t bound = E2_INF64, bound_tot = E2_INF64;
+        const bool banded = chain_regs(tb, sm, r, chain, m, lane, cr, &bound, &bound_tot);
         if (banded && bound <= kU32MaxValue)
             dp_banded<uint32_t>(tb, sm, cr, r, m, lane, &best, &best_mu, start, &last_tb);
-        else if (banded)
-            dp_banded<uint64_t>(tb, sm, cr, r, m, lane, &best, &best_mu, start, &last_tb);
+        else if (banded && bound_tot < kF64Limit)
+            dp_banded<double>(tb, sm, cr, r, m, lane, &best, &best_mu, start, &last_tb);
         else {
             // reference path: a full table per master, then the chosen
             // master's table again with split points

@@ -101,6 +101,38 @@ def test_random_sweep_parity(torch_dev):
         _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag=f"sweep {it}")
 
 
+def _scaled(seed, M, N, P, k_max, block_ns, head_ns, zero_blocks=0, **kw):
+    """random_small with every device at 1e9 FLOP/s, so that a block takes
+    exactly its FLOPs in ns: block times drawn from [block_ns / 2, block_ns],
+    the head `head_ns`, `zero_blocks` blocks of 0 ns."""
+    wl = workload.random_small(seed, M=M, N=N, P=P, k_max=k_max, **kw)
+    rng = np.random.default_rng(seed + 1)
+    wl.speed_flops[:] = 10**9
+    lf = rng.integers(block_ns // 2, block_ns + 1, size=(2, N)).astype(np.uint64)
+    if zero_blocks:
+        lf[:, rng.choice(N, zero_blocks, replace=False)] = 0
+    wl.layer_flops = lf
+    wl.head_flops = np.array([head_ns, head_ns], dtype=np.uint64)
+    return wl
+
+
+@pytest.mark.parametrize("block_ns,head_ns,zeros", [
+    (1 << 14, 1 << 12, 0),              # u32 keys, far from the limit
+    (0xFFFFFE // 12, 0, 3),             # u32 keys near 2^24, blocks of 0 ns
+    (0xFFFFFE // 6, 0xFFFFFE // 7, 0),  # around the u32 / fp64 switch
+    ((1 << 45) // 30, 1 << 20, 2),      # fp64 keys near 2^53, blocks of 0 ns
+    ((1 << 45) // 12, 1 << 40, 0),      # beyond the fp64 limit: u64 reference path
+])
+def test_key_width_boundaries(torch_dev, block_ns, head_ns, zeros):
+    """Values around the limits of the u32 and fp64 key paths (each problem
+    takes the narrowest exact width), including blocks that take 0 ns."""
+    for seed in range(3):
+        wl = _scaled(300 + seed, M=20, N=24, P=6, k_max=3, block_ns=block_ns, head_ns=head_ns,
+                     zero_blocks=zeros, mem_lo_layers=2, mem_hi_layers=14, cong_full=True)
+        print(f"block_ns={block_ns} head_ns={head_ns} seed={seed}", flush=True)
+        _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag=f"{block_ns}/{seed}")
+
+
 def test_uniform_layers_many_ties(torch_dev):
     """Identical blocks and devices: every master and many split points tie."""
     wl = workload.random_small(5, M=30, N=40, P=12, k_max=3, layer_var=False,
