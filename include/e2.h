@@ -214,6 +214,92 @@ int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
                uint8_t *labels_out, uint8_t *roles_out);
 
 /*
+ * Two-chromosome genomes (App. A, gene definition): per individual an
+ * ordering chromosome and a grouping chromosome, plus a role per replica.
+ *   order[P][M]   device: a permutation of 0..M-1 (an id >= M makes its
+ *                 replica infeasible; a device missing from the ordering
+ *                 gets 0 layers; a repeated id gives unspecified layers for
+ *                 that device)
+ *   sizes[P][k_max] device, u16: replica r holds the devices at ordering
+ *                 positions sizes[0] + ... + sizes[r-1] onwards, sizes[r] of
+ *                 them, clipped to M; 0 = no replica
+ *   roles[P][k_max] device: 0 = prefill replica, nonzero = decode replica
+ * A replica's device chain is its run of the ordering, in ordering order
+ * (the paper's node ordering, Sec. 3.2).  The paper's example
+ * [(0,1,2,3,4,5), (3,1,2)] has replicas {0,1,2}, {3}, {4,5}.
+ *
+ * e2_solve_partitions_ordered / e2_eval_population_ordered: as
+ * e2_solve_partitions / e2_eval_population with replicas in place of
+ * clusters (outputs per replica index r < k_max; same layouts, errors and
+ * fitness).
+ */
+int e2_solve_partitions_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                                const uint8_t *order, const uint16_t *sizes,
+                                const uint8_t *roles, uint64_t *T, uint64_t *Lambda,
+                                int16_t *master, uint8_t *layers);
+int e2_eval_population_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                               const uint8_t *order, const uint16_t *sizes, const uint8_t *roles,
+                               const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
+                               uint64_t *s_p, uint64_t *s_d);
+
+/*
+ * Parameters of the two-chromosome GA (App. A).
+ *   seed, generation, tournament_k, n_elite   as in e2_ga_params
+ *   mutation_thresh_u32  a child mutates when a uniform u32 draw is below
+ *                        it (about 0.3 * 2^32 in the paper)
+ *   max_replica          largest replica size drawn when a grouping
+ *                        regrows, in [1, 256]
+ */
+typedef struct e2_ga2_params {
+    uint64_t seed;
+    uint32_t generation;
+    uint32_t tournament_k;
+    uint32_t mutation_thresh_u32;
+    uint32_t n_elite;
+    uint32_t max_replica;
+} e2_ga2_params;
+
+/*
+ * One generation of the two-chromosome GA (Algorithm 2, App. A).  Inputs
+ * and outputs as above (order, sizes, roles), w_in / phase_in as in
+ * e2_ga_step; outputs must not overlap the inputs or each other.
+ * Slots 0..n_elite-1 receive the n_elite best individuals (key (w, phase,
+ * index)) unchanged.  Every other slot s, with draws rng(seed, generation,
+ * s, stream, gene) of the generator of e2_ga_step:
+ *   parents a, b      tournaments on streams 0.. and 64.. (as e2_ga_step)
+ *   ordering          c = 1 + floor(lo32(rng(.., 140, 0)) * (M-1) / 2^32);
+ *                     the child takes a's first c devices, then b's later
+ *                     positions; a device of b's part already present
+ *                     leaves a hole, and the holes are filled left to right
+ *                     with b's first-c devices missing from the child, in
+ *                     b's order (M = 1: a copy of a)
+ *   grouping, roles   those of b if lo32(rng(.., 141, 0)) < 2^31, else of a
+ *                     (roles written as 0/1)
+ *   mutation          u = rng(.., 142, 0) fires when hi32(u) <
+ *                     mutation_thresh; lo32(u) then picks, below 0.20,
+ *                     0.70, 0.85 of 2^32 and above:
+ *                     swap ordering positions floor(hi32(v) M / 2^32) and
+ *                       floor(lo32(v) M / 2^32), v = rng(.., 143, 0);
+ *                     regrow the grouping from replica floor(hi32(rng(..,
+ *                       144, 0)) R / 2^32), R = replicas holding devices;
+ *                     regrow the whole grouping;
+ *                     a new ordering (Fisher-Yates from the identity, step
+ *                       t = M-1..1 swapping t with floor(hi32(rng(.., 146,
+ *                       t)) (t+1) / 2^32)) and a regrown grouping.
+ *   regrowth          replicas before the start keep size and role; each
+ *                     later replica r gets size 1 + floor(hi32(u) *
+ *                     max_replica / 2^32), capped by the devices left (slot
+ *                     k_max-1 takes all that are left), and role
+ *                     lo32(u) >= 2^31, u = rng(.., 145, r); unused slots 0.
+ * E2_EINVAL for tournament_k outside [1, 64], n_elite > min(256, P),
+ * max_replica outside [1, 256] or overlapping buffers.
+ */
+int e2_ga_step_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                       const uint8_t *order_in, const uint16_t *sizes_in, const uint8_t *roles_in,
+                       const uint64_t *w_in, const uint64_t *phase_in, const e2_ga2_params *gp,
+                       uint8_t *order_out, uint16_t *sizes_out, uint8_t *roles_out);
+
+/*
  * Profiling of the DP kernel (the dominant cost of e2_solve_partitions and
  * e2_eval_population), for benchmarks and profilers.
  *

@@ -12,6 +12,9 @@ Functions mirror the paper's pieces:
   fitness    -> Eq. 3-5 with the QoS floor (Sec. 3.3, Sec. 3.5, Algorithm 2)
   ga_step    -> one generation: elites, tournament, crossover, mutation
   rng        -> counter-based SplitMix64 hash used by ga_step
+Two-chromosome genomes (App. A: an ordering chromosome and replica sizes):
+  replica_range, solve_ordered, eval_population_ordered,
+  order_crossover, regrow, ga_step_ordered
 """
 from __future__ import annotations
 
@@ -58,6 +61,19 @@ def _load() -> ctypes.CDLL:
     lib.oracle_fitness.restype = i32
     lib.oracle_ga_step.argtypes = [i32, i32, i32, P, P, P, P, u64, u32, u32, u32, u32, u32, P, P]
     lib.oracle_ga_step.restype = i32
+    lib.oracle_solve_ordered.argtypes = [i32, i32, P, P, P, P, P, u64, i32, i32, P, P, P, P, P,
+                                         P, P]
+    lib.oracle_solve_ordered.restype = i32
+    lib.oracle_ga_step_ordered.argtypes = [i32, i32, i32, P, P, P, P, P, u64, u32, u32, u32, u32,
+                                           u32, P, P, P]
+    lib.oracle_ga_step_ordered.restype = i32
+    lib.oracle_order_crossover.argtypes = [i32, P, P, i32, P]
+    lib.oracle_order_crossover.restype = None
+    lib.oracle_regrow.argtypes = [i32, i32, u64, u64, i32, i32, i32, P, P]
+    lib.oracle_regrow.restype = None
+    lib.oracle_replica_range.argtypes = [i32, i32, P, i32, ctypes.POINTER(i32),
+                                         ctypes.POINTER(i32)]
+    lib.oracle_replica_range.restype = i32
     lib.oracle_rng.argtypes = [u64, u64, u64, u64, u64]
     lib.oracle_rng.restype = u64
     lib.oracle_splitmix_out.argtypes = [u64]
@@ -204,3 +220,89 @@ def rng(seed, g, s, stream, gene) -> int:
 
 def splitmix_out(z) -> int:
     return int(_load().oracle_splitmix_out(z))
+
+
+# --- two-chromosome genomes (App. A) -------------------------------------
+
+def replica_range(sizes, r, M):
+    """[lo, hi) of replica r on the ordering chromosome (clipped to M)."""
+    sizes = np.ascontiguousarray(sizes, dtype=np.uint16)
+    lo, hi = ctypes.c_int(), ctypes.c_int()
+    rc = _load().oracle_replica_range(int(M), sizes.shape[0], _p(sizes), int(r), ctypes.byref(lo),
+                                      ctypes.byref(hi))
+    if rc != 0:
+        raise OracleError(f"oracle_replica_range failed: {rc}")
+    return lo.value, hi.value
+
+
+def solve_ordered(tables, mem_bytes, layer_bytes, head_bytes, order, sizes, roles):
+    """All (individual, replica) problems of two-chromosome genomes:
+    order u8 [P][M], sizes u16 [P][k_max], roles u8 [P][k_max]."""
+    lib = _load()
+    t, h, tau = tables
+    M, N = t.shape[1], t.shape[2]
+    order = np.ascontiguousarray(order, dtype=np.uint8)
+    sizes = np.ascontiguousarray(sizes, dtype=np.uint16)
+    roles = np.ascontiguousarray(roles, dtype=np.uint8)
+    P, k_max = sizes.shape
+    if order.shape != (P, M) or roles.shape != (P, k_max):
+        raise OracleError("order must be [P][M], sizes and roles [P][k_max]")
+    T = np.zeros((P, k_max), dtype=np.uint64)
+    L = np.zeros((P, k_max), dtype=np.uint64)
+    master = np.zeros((P, k_max), dtype=np.int16)
+    layers = np.zeros((P, M), dtype=np.uint8)
+    rc = lib.oracle_solve_ordered(M, N, _p(t), _p(h), _p(tau), _p(_u64(mem_bytes)),
+                                  _p(_u64(layer_bytes)), int(head_bytes), P, k_max, _p(order),
+                                  _p(sizes), _p(roles), _p(T), _p(L), _p(master), _p(layers))
+    if rc != 0:
+        raise OracleError(f"oracle_solve_ordered failed: {rc}")
+    return dict(T=T, Lambda=L, master=master, layers=layers)
+
+
+def eval_population_ordered(wl, order, sizes, roles):
+    """Quantise, solve and score a population of two-chromosome genomes."""
+    tables = quantise(**wl.problem_arrays())
+    sol = solve_ordered(tables, wl.mem_bytes, wl.layer_bytes, wl.head_bytes, order, sizes, roles)
+    sol.update(fitness(sol["T"], sol["Lambda"], roles, **wl.fitness_params()))
+    return sol
+
+
+def order_crossover(a, b, c):
+    """The child ordering of parents a, b cut at c, repaired (App. A)."""
+    a = np.ascontiguousarray(a, dtype=np.uint8)
+    b = np.ascontiguousarray(b, dtype=np.uint8)
+    child = np.zeros_like(a)
+    _load().oracle_order_crossover(a.shape[0], _p(a), _p(b), int(c), _p(child))
+    return child
+
+
+def regrow(sizes, roles, M, seed, g, s, pos, max_replica):
+    """Regrow a grouping from replica pos (in place on copies, returned)."""
+    sizes = np.array(sizes, dtype=np.uint16)
+    roles = np.array(roles, dtype=np.uint8)
+    _load().oracle_regrow(int(M), sizes.shape[0], int(seed), int(g), int(s), int(pos),
+                          int(max_replica), _p(sizes), _p(roles))
+    return sizes, roles
+
+
+def ga_step_ordered(order, sizes, roles, w, phase, seed, generation, tournament_k,
+                    mutation_thresh_u32, n_elite, max_replica):
+    lib = _load()
+    order = np.ascontiguousarray(order, dtype=np.uint8)
+    sizes = np.ascontiguousarray(sizes, dtype=np.uint16)
+    roles = np.ascontiguousarray(roles, dtype=np.uint8)
+    P, M = order.shape
+    k_max = sizes.shape[1]
+    if sizes.shape != (P, k_max) or roles.shape != (P, k_max):
+        raise OracleError("sizes and roles must be [P][k_max]")
+    w, phase = _u64(w), _u64(phase)
+    if w.shape != (P,) or phase.shape != (P,):
+        raise OracleError("w and phase must have shape [P]")
+    oo, so, ro = np.zeros_like(order), np.zeros_like(sizes), np.zeros_like(roles)
+    rc = lib.oracle_ga_step_ordered(M, P, k_max, _p(order), _p(sizes), _p(roles), _p(w), _p(phase),
+                                    int(seed), int(generation), int(tournament_k),
+                                    int(mutation_thresh_u32), int(n_elite), int(max_replica),
+                                    _p(oo), _p(so), _p(ro))
+    if rc != 0:
+        raise OracleError(f"oracle_ga_step_ordered failed: {rc}")
+    return oo, so, ro

@@ -468,3 +468,265 @@ int oracle_ga_step(int M, int P, int k_max, const uint8_t *labels_in, const uint
     }
     return ORC_OK;
 }
+
+/* ====================================================================== */
+/* Two-chromosome genomes (App. A): an ordering chromosome order[M] (a     */
+/* permutation of the devices) and a grouping chromosome sizes[k_max]      */
+/* (replica sizes).  Replica r holds the devices at ordering positions     */
+/* off_r .. off_r + sizes[r] - 1, off_r = sizes[0] + ... + sizes[r-1],     */
+/* clipped to M; its chain order is the ordering (Sec. 3.2 "node          */
+/* ordering"; App. A gene example).  roles[k_max] belongs to the replicas. */
+/* ====================================================================== */
+
+/* replica r's ordering range [*lo, *hi), clipped to M */
+static void replica_range(int M, int k_max, const uint16_t *sizes, int r, int *lo, int *hi)
+{
+    long off = 0;
+    for (int q = 0; q < r && q < k_max; q++) off += sizes[q];
+    long end = off + sizes[r];
+    *lo = (int)(off < M ? off : M);
+    *hi = (int)(end < M ? end : M);
+}
+
+int oracle_replica_range(int M, int k_max, const uint16_t *sizes, int r, int *lo, int *hi)
+{
+    if (M < 1 || M > 256 || k_max < 1 || k_max > 255 || r < 0 || r >= k_max) return ORC_EINVAL;
+    replica_range(M, k_max, sizes, r, lo, hi);
+    return ORC_OK;
+}
+
+/*
+ * Per-(individual, replica) solve for two-chromosome genomes: as
+ * oracle_solve, with replica r's chain = order[off_r .. off_r + m_r - 1].
+ * Devices outside every replica get 0 layers; a replica holding an id
+ * >= M (not a device) is infeasible.
+ */
+int oracle_solve_ordered(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
+                         const uint64_t *mem, const uint64_t *W, uint64_t HB, int P, int k_max,
+                         const uint8_t *order, const uint16_t *sizes, const uint8_t *roles,
+                         uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    if (M < 1 || M > 256 || N < 1 || N > 255 || P < 0 || k_max < 1 || k_max > 255)
+        return ORC_EINVAL;
+    int chain[256];
+    int szs[256];
+    uint64_t *tk = malloc(sizeof(uint64_t) * (size_t)M * N);
+    uint64_t hk[256], tl[256], mk[256];
+    if (!tk) return ORC_ENOMEM;
+    for (int p = 0; p < P; p++) {
+        for (int d = 0; d < M; d++) layers[(size_t)p * M + d] = 0;
+        for (int q = 0; q < k_max; q++) {
+            size_t o = (size_t)p * k_max + q;
+            T[o] = INF;
+            Lambda[o] = INF;
+            master[o] = -1;
+            int lo, hi;
+            replica_range(M, k_max, sizes + (size_t)p * k_max, q, &lo, &hi);
+            int m = hi - lo;
+            if (m <= 0) continue;
+            int valid = 1;
+            for (int k = 0; k < m; k++) {
+                chain[k] = order[(size_t)p * M + lo + k];
+                if (chain[k] >= M) valid = 0;
+            }
+            if (!valid) continue;
+            int r = roles[o] != 0;
+            for (int k = 0; k < m; k++) {
+                memcpy(tk + (size_t)k * N, t + ((size_t)r * M + chain[k]) * N, sizeof(uint64_t) * N);
+                hk[k] = h[r * M + chain[k]];
+                mk[k] = mem[chain[k]];
+                tl[k] = (k == 0) ? 0 : tau[((size_t)r * M + chain[k - 1]) * M + chain[k]];
+            }
+            uint64_t Tv, Lv, ev;
+            int mu;
+            int rc = oracle_dp_pipe(m, N, tk, hk, tl, mk, W, HB, &Tv, &Lv, &mu, szs, &ev);
+            if (rc) { free(tk); return rc; }
+            if (Tv == INF) continue;
+            T[o] = Tv;
+            Lambda[o] = Lv;
+            master[o] = (int16_t)chain[mu - 1];
+            for (int k = 0; k < m; k++) layers[(size_t)p * M + chain[k]] = (uint8_t)szs[k];
+        }
+    }
+    free(tk);
+    return ORC_OK;
+}
+
+/* Two-chromosome GA streams */
+#define ST_O_CUT 140u    /* crossover point of the ordering                 */
+#define ST_O_GROUP 141u  /* which parent gives the grouping (and roles)     */
+#define ST_O_MUT 142u    /* whether the child mutates, and which mutation   */
+#define ST_O_SWAP 143u   /* the two ordering positions of a swap            */
+#define ST_O_REGEN 144u  /* the replica from which the grouping regrows     */
+#define ST_O_SIZE 145u   /* + nothing; gene = replica: its size and role    */
+#define ST_O_PERM 146u   /* gene = step of the Fisher-Yates shuffle         */
+
+/* mutation kinds, as fractions of 2^32 of a uniform u32 (App. A) */
+#define MUT_SWAP_BELOW 858993459u    /* 0.20: exchange two ordering positions      */
+#define MUT_REGROW_BELOW 3006477107u /* 0.70: regrow the grouping from a replica   */
+#define MUT_ALLGROUP_BELOW 3650722201u /* 0.85: regrow the whole grouping; else both */
+
+/*
+ * Ordering crossover with repair (App. A): the child takes a[0..c) and
+ * then b[c..M); a node of b's part that already occurs in a[0..c) leaves a
+ * hole, and the holes are filled left to right with the nodes of b[0..c)
+ * that are not in a[0..c), in b's order.  Every node then occurs once.
+ */
+void oracle_order_crossover(int M, const uint8_t *a, const uint8_t *b, int c, uint8_t *child)
+{
+    unsigned char used[256] = {0};
+    for (int t = 0; t < c; t++) {
+        child[t] = a[t];
+        used[a[t]] = 1;
+    }
+    int fill[256], nf = 0;
+    for (int t = 0; t < c; t++)
+        if (!used[b[t]]) fill[nf++] = b[t];
+    int k = 0;
+    for (int t = c; t < M; t++) child[t] = used[b[t]] ? (uint8_t)fill[k++] : b[t];
+}
+
+/*
+ * Regrow the grouping from replica pos: replicas 0..pos-1 keep their sizes
+ * and roles; the remaining devices are cut into replicas of
+ * 1 + floor(hi32(u) * max_replica / 2^32) devices (the last replica slot,
+ * k_max - 1, takes whatever remains), each with role lo32(u) >= 2^31, u =
+ * rng(seed, g, slot, ST_O_SIZE, replica); unused slots get size 0, role 0.
+ */
+static void regrow(int M, int k_max, uint64_t seed, uint64_t g, int s, int pos, int max_replica,
+                   uint16_t *sizes, uint8_t *roles)
+{
+    long kept = 0;
+    for (int r = 0; r < pos; r++) kept += sizes[r];
+    long remaining = M - kept;
+    if (remaining < 0) remaining = 0;
+    int r = pos;
+    while (remaining > 0 && r < k_max) {
+        uint64_t u = oracle_rng(seed, g, (uint64_t)s, ST_O_SIZE, (uint64_t)r);
+        long sz = 1 + (long)((((u >> 32)) * (uint64_t)max_replica) >> 32);
+        if (r == k_max - 1 || sz > remaining) sz = remaining;
+        sizes[r] = (uint16_t)sz;
+        roles[r] = (uint32_t)u >= 0x80000000u;
+        remaining -= sz;
+        r++;
+    }
+    for (; r < k_max; r++) {
+        sizes[r] = 0;
+        roles[r] = 0;
+    }
+}
+
+void oracle_regrow(int M, int k_max, uint64_t seed, uint64_t g, int s, int pos, int max_replica,
+                   uint16_t *sizes, uint8_t *roles)
+{
+    regrow(M, k_max, seed, g, s, pos, max_replica, sizes, roles);
+}
+
+/* number of leading replicas that hold at least one device */
+static int replica_count(int M, int k_max, const uint16_t *sizes)
+{
+    int n = 0;
+    long off = 0;
+    for (int r = 0; r < k_max; r++) {
+        if (sizes[r] == 0 || off >= M) break;
+        off += sizes[r];
+        n++;
+    }
+    return n;
+}
+
+/*
+ * One generation of the two-chromosome GA (Algorithm 2, App. A).
+ * Slots 0..n_elite-1 receive the n_elite best individuals in key order,
+ * unchanged.  Every other slot s:
+ *   parents a, b: tournaments as in oracle_ga_step (streams 0.., 64..)
+ *   ordering: crossover with repair at c = 1 + floor(lo32(u) * (M-1) / 2^32),
+ *     u = rng(.., ST_O_CUT, 0) (the child copies a when M = 1)
+ *   grouping and roles: from b if lo32(rng(.., ST_O_GROUP, 0)) < 2^31, else a
+ *   mutation, u = rng(.., ST_O_MUT, 0): fires when hi32(u) < mutation_thresh;
+ *     lo32(u) < 0.20 * 2^32: swap ordering positions floor(hi32(v) * M / 2^32)
+ *       and floor(lo32(v) * M / 2^32), v = rng(.., ST_O_SWAP, 0);
+ *     < 0.70: regrow the grouping from replica floor(hi32(rng(.., ST_O_REGEN,
+ *       0)) * R / 2^32), R = replicas holding devices (0 if none);
+ *     < 0.85: regrow the whole grouping;
+ *     else: a new ordering (Fisher-Yates from the identity: for t = M-1..1
+ *       swap t with floor(hi32(rng(.., ST_O_PERM, t)) * (t+1) / 2^32)) and a
+ *       regrown grouping.
+ *   roles are written as 0/1.
+ */
+int oracle_ga_step_ordered(int M, int P, int k_max, const uint8_t *order_in,
+                           const uint16_t *sizes_in, const uint8_t *roles_in, const uint64_t *w,
+                           const uint64_t *phase, uint64_t seed, uint32_t generation,
+                           uint32_t tournament_k, uint32_t mut_thresh, uint32_t n_elite,
+                           uint32_t max_replica, uint8_t *order_out, uint16_t *sizes_out,
+                           uint8_t *roles_out)
+{
+    if (M < 1 || M > 256 || P < 1 || k_max < 1 || k_max > 255 || tournament_k < 1 ||
+        tournament_k > 64 || (int)n_elite > P || n_elite > 256 || max_replica < 1 ||
+        max_replica > 256)
+        return ORC_EINVAL;
+    const uint64_t g = generation;
+    int last = -1;
+    for (uint32_t e = 0; e < n_elite; e++) {
+        int pick = -1;
+        for (int p = 0; p < P; p++) {
+            if (last >= 0 && !key_less(w, phase, last, p)) continue;
+            if (pick < 0 || key_less(w, phase, p, pick)) pick = p;
+        }
+        memcpy(order_out + (size_t)e * M, order_in + (size_t)pick * M, (size_t)M);
+        memcpy(sizes_out + (size_t)e * k_max, sizes_in + (size_t)pick * k_max,
+               sizeof(uint16_t) * (size_t)k_max);
+        memcpy(roles_out + (size_t)e * k_max, roles_in + (size_t)pick * k_max, (size_t)k_max);
+        last = pick;
+    }
+    for (int s = (int)n_elite; s < P; s++) {
+        int a = tournament(seed, g, s, ST_SEL_A, (int)tournament_k, P, w, phase);
+        int b = tournament(seed, g, s, ST_SEL_B, (int)tournament_k, P, w, phase);
+        uint8_t *ord = order_out + (size_t)s * M;
+        uint16_t *sz = sizes_out + (size_t)s * k_max;
+        uint8_t *ro = roles_out + (size_t)s * k_max;
+        if (M >= 2) {
+            uint64_t u = oracle_rng(seed, g, (uint64_t)s, ST_O_CUT, 0);
+            int c = 1 + (int)((((uint64_t)(uint32_t)u) * (uint64_t)(M - 1)) >> 32);
+            oracle_order_crossover(M, order_in + (size_t)a * M, order_in + (size_t)b * M, c, ord);
+        } else {
+            ord[0] = order_in[(size_t)a * M];
+        }
+        uint64_t ug = oracle_rng(seed, g, (uint64_t)s, ST_O_GROUP, 0);
+        int src = ((uint32_t)ug < 0x80000000u) ? b : a;
+        for (int r = 0; r < k_max; r++) {
+            sz[r] = sizes_in[(size_t)src * k_max + r];
+            ro[r] = roles_in[(size_t)src * k_max + r] != 0;
+        }
+        uint64_t um = oracle_rng(seed, g, (uint64_t)s, ST_O_MUT, 0);
+        if ((uint32_t)(um >> 32) < mut_thresh) {
+            uint32_t kind = (uint32_t)um;
+            if (kind < MUT_SWAP_BELOW) {
+                uint64_t v = oracle_rng(seed, g, (uint64_t)s, ST_O_SWAP, 0);
+                int i = (int)(((v >> 32) * (uint64_t)M) >> 32);
+                int j = (int)((((uint64_t)(uint32_t)v) * (uint64_t)M) >> 32);
+                uint8_t x = ord[i];
+                ord[i] = ord[j];
+                ord[j] = x;
+            } else if (kind < MUT_REGROW_BELOW) {
+                int R = replica_count(M, k_max, sz);
+                uint64_t v = oracle_rng(seed, g, (uint64_t)s, ST_O_REGEN, 0);
+                int pos = (int)(((v >> 32) * (uint64_t)R) >> 32);
+                regrow(M, k_max, seed, g, s, pos, (int)max_replica, sz, ro);
+            } else {
+                if (kind >= MUT_ALLGROUP_BELOW) {
+                    for (int t = 0; t < M; t++) ord[t] = (uint8_t)t;
+                    for (int t = M - 1; t >= 1; t--) {
+                        uint64_t v = oracle_rng(seed, g, (uint64_t)s, ST_O_PERM, (uint64_t)t);
+                        int j = (int)(((v >> 32) * (uint64_t)(t + 1)) >> 32);
+                        uint8_t x = ord[t];
+                        ord[t] = ord[j];
+                        ord[j] = x;
+                    }
+                }
+                regrow(M, k_max, seed, g, s, 0, (int)max_replica, sz, ro);
+            }
+        }
+    }
+    return ORC_OK;
+}

@@ -9,6 +9,9 @@ tensors on ROCm) and streams.  The wrappers keep the C names:
     e2_solve_partitions(ctx, labels, roles)           Algorithm 1 per cluster
     e2_eval_population(ctx, labels, roles, fitness)   Eq. 3-5 per individual
     e2_ga_step(ctx, labels, roles, w, phase, ga)      one GA generation
+    e2_solve_partitions_ordered(ctx, order, sizes, roles)          the same on
+    e2_eval_population_ordered(ctx, order, sizes, roles, fitness)  two-chromosome
+    e2_ga_step_ordered(ctx, order, sizes, roles, w, phase, ga)     genomes (App. A)
 
 `problem` is a dict with the fields of e2_problem (numpy arrays), as
 returned by workload.Workload.problem_arrays().  64-bit unsigned outputs
@@ -33,8 +36,9 @@ E2_OK, E2_EINVAL, E2_EOVERFLOW, E2_ENOMEM, E2_EHIP = 0, -1, -2, -3, -4
 INF = (1 << 64) - 1
 
 EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitions",
-            "e2_eval_population", "e2_ga_step", "e2_ctx_dp_timing", "e2_ctx_dp_elapsed",
-            "e2_strerror")
+            "e2_eval_population", "e2_ga_step", "e2_solve_partitions_ordered",
+            "e2_eval_population_ordered", "e2_ga_step_ordered", "e2_ctx_dp_timing",
+            "e2_ctx_dp_elapsed", "e2_strerror")
 
 
 class E2Error(RuntimeError):
@@ -62,6 +66,12 @@ class e2_ga_params(ctypes.Structure):
     _fields_ = [("seed", ctypes.c_uint64), ("generation", ctypes.c_uint32),
                 ("tournament_k", ctypes.c_uint32), ("crossover_thresh_u32", ctypes.c_uint32),
                 ("mutation_thresh_u32", ctypes.c_uint32), ("n_elite", ctypes.c_uint32)]
+
+
+class e2_ga2_params(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("generation", ctypes.c_uint32),
+                ("tournament_k", ctypes.c_uint32), ("mutation_thresh_u32", ctypes.c_uint32),
+                ("n_elite", ctypes.c_uint32), ("max_replica", ctypes.c_uint32)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -92,6 +102,14 @@ def lib() -> ctypes.CDLL:
     L.e2_ga_step.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, ctypes.POINTER(e2_ga_params),
                              vp, vp]
     L.e2_ga_step.restype = ctypes.c_int
+    L.e2_solve_partitions_ordered.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+    L.e2_solve_partitions_ordered.restype = ctypes.c_int
+    L.e2_eval_population_ordered.argtypes = [vp, vp, i32, i32, vp, vp, vp,
+                                             ctypes.POINTER(e2_fitness_params), vp, vp, vp, vp]
+    L.e2_eval_population_ordered.restype = ctypes.c_int
+    L.e2_ga_step_ordered.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, vp,
+                                     ctypes.POINTER(e2_ga2_params), vp, vp, vp]
+    L.e2_ga_step_ordered.restype = ctypes.c_int
     L.e2_ctx_dp_timing.argtypes = [vp, i32]
     L.e2_ctx_dp_timing.restype = ctypes.c_int
     L.e2_ctx_dp_elapsed.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
@@ -274,6 +292,74 @@ def e2_ga_step(ctx: Context, labels_in, roles_in, w, phase, ga: dict, stream=Non
                             _ptr(roles_in), _ptr(w), _ptr(phase), ctypes.byref(gp),
                             _ptr(out[0]), _ptr(out[1])),
            "e2_ga_step")
+    return out
+
+
+def _ordered_args(ctx, order, sizes, roles):
+    torch = _torch()
+    P, k_max = sizes.shape
+    _dev(order, torch.uint8, (P, ctx.n_dev), "order")
+    _dev(sizes, torch.uint16, (P, k_max), "sizes")
+    _dev(roles, torch.uint8, (P, k_max), "roles")
+    return P, k_max
+
+
+def e2_solve_partitions_ordered(ctx: Context, order, sizes, roles, stream=None,
+                                out: Optional[dict] = None):
+    """As e2_solve_partitions, for genomes order uint8 [P][M], sizes uint16
+    [P][k_max], roles uint8 [P][k_max]; outputs per replica."""
+    torch = _torch()
+    P, k_max = _ordered_args(ctx, order, sizes, roles)
+    dev = order.device
+    if out is None:
+        out = dict(T=torch.empty((P, k_max), dtype=torch.int64, device=dev),
+                   Lambda=torch.empty((P, k_max), dtype=torch.int64, device=dev),
+                   master=torch.empty((P, k_max), dtype=torch.int16, device=dev),
+                   layers=torch.empty((P, ctx.n_dev), dtype=torch.uint8, device=dev))
+    _check(lib().e2_solve_partitions_ordered(ctx.handle, _stream(stream), P, k_max, _ptr(order),
+                                             _ptr(sizes), _ptr(roles), _ptr(out["T"]),
+                                             _ptr(out["Lambda"]), _ptr(out["master"]),
+                                             _ptr(out["layers"])),
+           "e2_solve_partitions_ordered")
+    return out
+
+
+def e2_eval_population_ordered(ctx: Context, order, sizes, roles, fitness: dict, stream=None,
+                               with_rates: bool = True, out: Optional[dict] = None):
+    """As e2_eval_population, for two-chromosome genomes."""
+    torch = _torch()
+    P, k_max = _ordered_args(ctx, order, sizes, roles)
+    if out is None:
+        names = ("w", "phase", "s_p", "s_d") if with_rates else ("w", "phase")
+        out = {k: torch.empty(P, dtype=torch.int64, device=order.device) for k in names}
+    fp = e2_fitness_params(int(fitness["t_arrival_ns"]), int(fitness["nd_tokens"]),
+                           int(fitness["min_tps_milli"]))
+    _check(lib().e2_eval_population_ordered(ctx.handle, _stream(stream), P, k_max, _ptr(order),
+                                            _ptr(sizes), _ptr(roles), ctypes.byref(fp),
+                                            _ptr(out["w"]), _ptr(out["phase"]),
+                                            _ptr(out.get("s_p")), _ptr(out.get("s_d"))),
+           "e2_eval_population_ordered")
+    return out
+
+
+def e2_ga_step_ordered(ctx: Context, order_in, sizes_in, roles_in, w, phase, ga: dict,
+                       stream=None, out: Optional[tuple] = None):
+    """Returns (order_out uint8 [P][M], sizes_out uint16 [P][k_max],
+    roles_out uint8 [P][k_max])."""
+    torch = _torch()
+    P, k_max = _ordered_args(ctx, order_in, sizes_in, roles_in)
+    _dev(w, torch.int64, (P,), "w")
+    _dev(phase, torch.int64, (P,), "phase")
+    if out is None:
+        out = (torch.empty_like(order_in), torch.empty_like(sizes_in), torch.empty_like(roles_in))
+    gp = e2_ga2_params(int(ga["seed"]), int(ga["generation"]), int(ga["tournament_k"]),
+                       int(ga["mutation_thresh_u32"]), int(ga["n_elite"]),
+                       int(ga["max_replica"]))
+    _check(lib().e2_ga_step_ordered(ctx.handle, _stream(stream), P, k_max, _ptr(order_in),
+                                    _ptr(sizes_in), _ptr(roles_in), _ptr(w), _ptr(phase),
+                                    ctypes.byref(gp), _ptr(out[0]), _ptr(out[1]),
+                                    _ptr(out[2])),
+           "e2_ga_step_ordered")
     return out
 
 

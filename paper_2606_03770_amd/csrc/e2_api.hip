@@ -414,15 +414,19 @@ int e2_ctx_dp_elapsed(e2_ctx *ctx, int32_t *launches, double *total_ms)
     return E2_OK;
 }
 
-int e2_solve_partitions(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
-                        const uint8_t *labels, const uint8_t *roles, uint64_t *T,
-                        uint64_t *Lambda, int16_t *master, uint8_t *layers)
+}  // extern "C"
+
+namespace {
+
+int solve_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genomes &gen,
+               const uint8_t *roles, uint64_t *T, uint64_t *Lambda, int16_t *master,
+               uint8_t *layers)
 {
     if (!ctx) return E2_EINVAL;
     int rc = check_pop(P, k_max);
     if (rc) return rc;
     if (P == 0) return E2_OK;
-    if (!labels || !roles || !T || !Lambda || !master || !layers) return E2_EINVAL;
+    if (!roles || !T || !Lambda || !master || !layers) return E2_EINVAL;
     if ((rc = check_device(ctx))) return rc;
     hipStream_t s = as_stream(stream);
     int slots;
@@ -432,21 +436,21 @@ int e2_solve_partitions(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
     if ((rc = alloc_scratch(sc, s, bytes))) return rc;
     E2Work wk;
     carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk);
-    const hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, labels, roles, wk, T,
+    const hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, roles, wk, T,
                                               Lambda, master, layers);
     return e == hipSuccess ? E2_OK : E2_EHIP;
 }
 
-int e2_eval_population(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
-                       const uint8_t *labels, const uint8_t *roles, const e2_fitness_params *fp,
-                       uint64_t *w, uint64_t *phase, uint64_t *s_p, uint64_t *s_d)
+int eval_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genomes &gen,
+              const uint8_t *roles, const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
+              uint64_t *s_p, uint64_t *s_d)
 {
     if (!ctx || !fp) return E2_EINVAL;
     int rc = check_pop(P, k_max);
     if (rc) return rc;
     if (fp->nd_tokens > 8192) return E2_EINVAL;
     if (P == 0) return E2_OK;
-    if (!labels || !roles || !w || !phase) return E2_EINVAL;
+    if (!roles || !w || !phase) return E2_EINVAL;
     if ((rc = check_device(ctx))) return rc;
     hipStream_t s = as_stream(stream);
     int slots;
@@ -459,13 +463,97 @@ int e2_eval_population(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
     carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk);
     uint64_t *Ts = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
     uint64_t *Ls = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb + tl);
-    hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, labels, roles, wk, Ts, Ls,
+    hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, roles, wk, Ts, Ls,
                                         nullptr, nullptr);
     if (e != hipSuccess) return E2_EHIP;
     const uint64_t lam_max =
         fp->min_tps_milli ? 1000000000000ull / fp->min_tps_milli : E2_INF64;
     e = e2_launch_fitness(s, P, k_max, Ts, Ls, roles, fp->t_arrival_ns, fp->nd_tokens, lam_max,
                           w, phase, s_p, s_d);
+    return e == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb)
+{
+    const char *x = static_cast<const char *>(a), *y = static_cast<const char *>(b);
+    return x < y + nb && y < x + na;
+}
+
+}  // namespace
+
+extern "C" {
+
+int e2_solve_partitions(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                        const uint8_t *labels, const uint8_t *roles, uint64_t *T,
+                        uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    if (P > 0 && !labels) return E2_EINVAL;
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    return solve_impl(ctx, stream, P, k_max, gen, roles, T, Lambda, master, layers);
+}
+
+int e2_eval_population(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                       const uint8_t *labels, const uint8_t *roles, const e2_fitness_params *fp,
+                       uint64_t *w, uint64_t *phase, uint64_t *s_p, uint64_t *s_d)
+{
+    if (P > 0 && !labels) return E2_EINVAL;
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    return eval_impl(ctx, stream, P, k_max, gen, roles, fp, w, phase, s_p, s_d);
+}
+
+int e2_solve_partitions_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                                const uint8_t *order, const uint16_t *sizes,
+                                const uint8_t *roles, uint64_t *T, uint64_t *Lambda,
+                                int16_t *master, uint8_t *layers)
+{
+    if (P > 0 && (!order || !sizes)) return E2_EINVAL;
+    const E2Genomes gen = {nullptr, order, sizes};
+    return solve_impl(ctx, stream, P, k_max, gen, roles, T, Lambda, master, layers);
+}
+
+int e2_eval_population_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                               const uint8_t *order, const uint16_t *sizes, const uint8_t *roles,
+                               const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
+                               uint64_t *s_p, uint64_t *s_d)
+{
+    if (P > 0 && (!order || !sizes)) return E2_EINVAL;
+    const E2Genomes gen = {nullptr, order, sizes};
+    return eval_impl(ctx, stream, P, k_max, gen, roles, fp, w, phase, s_p, s_d);
+}
+
+int e2_ga_step_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                       const uint8_t *order_in, const uint16_t *sizes_in, const uint8_t *roles_in,
+                       const uint64_t *w_in, const uint64_t *phase_in, const e2_ga2_params *gp,
+                       uint8_t *order_out, uint16_t *sizes_out, uint8_t *roles_out)
+{
+    if (!ctx || !gp) return E2_EINVAL;
+    int rc = check_pop(P, k_max);
+    if (rc) return rc;
+    if (P == 0) return E2_OK;
+    if (!order_in || !sizes_in || !roles_in || !w_in || !phase_in || !order_out || !sizes_out ||
+        !roles_out)
+        return E2_EINVAL;
+    if (gp->tournament_k < 1 || gp->tournament_k > 64 || gp->n_elite > 256 ||
+        gp->n_elite > (uint32_t)P || gp->max_replica < 1 || gp->max_replica > 256)
+        return E2_EINVAL;
+    const size_t no = (size_t)P * ctx->M, ns = (size_t)P * k_max * 2, nr = (size_t)P * k_max;
+    const void *ins[3] = {order_in, sizes_in, roles_in};
+    const size_t nin[3] = {no, ns, nr};
+    void *outs[3] = {order_out, sizes_out, roles_out};
+    for (int i = 0; i < 3; ++i) {
+        for (int j = 0; j < 3; ++j)
+            if (overlap(outs[i], nin[i], ins[j], nin[j])) return E2_EINVAL;
+        for (int j = i + 1; j < 3; ++j)
+            if (overlap(outs[i], nin[i], outs[j], nin[j])) return E2_EINVAL;
+    }
+    if ((rc = check_device(ctx))) return rc;
+    hipStream_t s = as_stream(stream);
+    Scratch sc;
+    if ((rc = alloc_scratch(sc, s, align256(256 * 4)))) return rc;
+    const hipError_t e = e2_launch_ga_ordered(
+        s, ctx->M, P, k_max, order_in, sizes_in, roles_in, w_in, phase_in, gp->seed,
+        gp->generation, gp->tournament_k, gp->mutation_thresh_u32, gp->n_elite, gp->max_replica,
+        static_cast<uint32_t *>(sc.base), order_out, sizes_out, roles_out);
     return e == hipSuccess ? E2_OK : E2_EHIP;
 }
 
@@ -484,10 +572,6 @@ int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_
         return E2_EINVAL;
     const size_t M = (size_t)ctx->M;
     // outputs must not overlap the inputs
-    auto overlap = [](const void *a, size_t na, const void *b, size_t nb) {
-        const char *x = static_cast<const char *>(a), *y = static_cast<const char *>(b);
-        return x < y + nb && y < x + na;
-    };
     const size_t nl = (size_t)P * M, nr = (size_t)P * k_max;
     if (overlap(labels_out, nl, labels_in, nl) || overlap(labels_out, nl, roles_in, nr) ||
         overlap(roles_out, nr, labels_in, nl) || overlap(roles_out, nr, roles_in, nr) ||

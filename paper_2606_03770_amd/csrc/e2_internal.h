@@ -62,10 +62,19 @@ int e2_dp_pool_cells(int N);
 size_t e2_dp_row_words(int N);
 size_t e2_dp_lds_bytes(int N);
 
+// The genomes of a population: labels [P][M] (cluster id per device), or,
+// when labels is null, two-chromosome genomes: an ordering order [P][M] and
+// replica sizes [P][k_max].
+struct E2Genomes {
+    const uint8_t *labels;
+    const uint8_t *order;
+    const uint16_t *sizes;
+};
+
 // Enqueue cluster extraction + DP.  Outputs may be the caller's (solve) or
 // scratch (eval; master/layers null).
 hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_max,
-                                const uint8_t *labels, const uint8_t *roles, const E2Work &wk,
+                                const E2Genomes &gen, const uint8_t *roles, const E2Work &wk,
                                 uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers);
 
 hipError_t e2_launch_fitness(hipStream_t s, int P, int k_max, const uint64_t *T,
@@ -78,3 +87,10 @@ hipError_t e2_launch_ga(hipStream_t s, int M, int P, int k_max, const uint8_t *l
                         uint64_t seed, uint32_t generation, uint32_t tournament_k,
                         uint32_t xo_thresh, uint32_t mut_thresh, uint32_t n_elite,
                         uint32_t *elite_scratch, uint8_t *labels_out, uint8_t *roles_out);
+
+hipError_t e2_launch_ga_ordered(hipStream_t s, int M, int P, int k_max, const uint8_t *order_in,
+                                const uint16_t *sizes_in, const uint8_t *roles_in,
+                                const uint64_t *w, const uint64_t *phase, uint64_t seed,
+                                uint32_t generation, uint32_t tournament_k, uint32_t mut_thresh,
+                                uint32_t n_elite, uint32_t max_replica, uint32_t *elite_scratch,
+                                uint8_t *order_out, uint16_t *sizes_out, uint8_t *roles_out);

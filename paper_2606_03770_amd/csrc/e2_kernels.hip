@@ -14,6 +14,9 @@
 //   k_elites      one workgroup: the n_elite best keys (w, phase, index)
 //   k_breed       one wave per output slot: elite copy or tournament +
 //                 uniform crossover + per-gene mutation
+//   k_breed_ordered  the same for two-chromosome genomes (App. A):
+//                 ordering crossover with repair, one parent's grouping,
+//                 four kinds of mutation
 //
 // DP encoding.  A candidate of row k (device c holds blocks j..i, devices
 // 1..k-1 hold 0..j-1) is scored max(DP(j-1, k-1), tau(k-1, k), cost(j, i)).
@@ -106,12 +109,27 @@ __device__ __forceinline__ int size_class(int m)
     return m >= 16 ? 0 : (m >= 12 ? 1 : (m >= 8 ? 2 : 3));
 }
 
+// Replica of ordering position t of a two-chromosome genome: the largest r
+// with offs[r] <= t (offs[r] = clipped start of replica r; empty replicas
+// share their start with the next one), or 256 when t lies beyond every
+// replica.
+__device__ __forceinline__ int replica_at(const uint32_t *offs, int k_max, int t)
+{
+    if ((uint32_t)t >= offs[k_max]) return 256;
+    int lo = 0, hi = k_max - 1;  // offs[lo] <= t < offs[hi + 1]
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (offs[mid] <= (uint32_t)t) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
 __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_max,
-                                                      const uint8_t *__restrict__ labels,
-                                                      uint32_t *counters, uint32_t *list,
-                                                      size_t seg_cap, uint64_t *T,
-                                                      uint64_t *Lambda, int16_t *master,
-                                                      uint8_t *layers)
+                                                      E2Genomes gen, uint32_t *counters,
+                                                      uint32_t *list, size_t seg_cap,
+                                                      uint64_t *T, uint64_t *Lambda,
+                                                      int16_t *master, uint8_t *layers)
 {
     // per genome: (count << 16) + sum of cap0, min cap0, head-capable bitmask,
     // listed bitmask
@@ -121,10 +139,28 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
     __shared__ uint32_t lmask[kEG][8];
     __shared__ uint32_t ncls[kEG][kClasses];
     __shared__ uint32_t base[kEG][kClasses];
+    __shared__ uint32_t offs[kEG][256];  // replica starts of two-chromosome genomes
+    __shared__ uint32_t bad[kEG][8];     // replicas holding a device id >= M
     const int g = threadIdx.x / 64;
     const int lane = threadIdx.x % 64;
     const int p = blockIdx.x * kEG + g;
     const int M = tb.M, N = tb.N;
+    const bool ordered = gen.labels == nullptr;
+    if (ordered && p < P) {
+        // offs[r] = min(M, sizes[0] + ... + sizes[r-1]), r = 0..k_max
+        uint32_t carry = 0;
+        for (int r0 = 0; r0 <= k_max; r0 += kWave) {
+            const int r = r0 + lane;
+            const uint32_t v = (r >= 1 && r <= k_max) ? gen.sizes[(size_t)p * k_max + r - 1] : 0;
+            uint32_t x = v;
+            for (int d = 1; d < kWave; d <<= 1) {
+                const uint32_t y = __shfl_up(x, d, kWave);
+                if (lane >= d) x += y;
+            }
+            if (r <= k_max) offs[g][r] = min(carry + x, (uint32_t)M);
+            carry += __shfl(x, kWave - 1, kWave);
+        }
+    }
     for (int q = lane; q < 256; q += 64) {
         packed[g][q] = 0;
         mincap[g][q] = 0xFFFFFFFFu;
@@ -132,15 +168,29 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
     if (lane < 8) {
         hmask[g][lane] = 0;
         lmask[g][lane] = 0;
+        bad[g][lane] = 0;
     }
     __syncthreads();
+    // labels: slot u of a lane is device x, in cluster labs[u]; ordered
+    // genomes: ordering position x, holding device d, in replica labs[u]
     int labs[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-        const int d = lane + 64 * u;
+        const int x = lane + 64 * u;
         labs[u] = 256;
-        if (p < P && d < M) {
-            const int lab = labels[(size_t)p * M + d];
+        if (p < P && x < M) {
+            int lab, d = x;
+            if (ordered) {
+                d = gen.order[(size_t)p * M + x];
+                lab = replica_at(offs[g], k_max, x);
+                if (d >= M) {  // not a device: its replica cannot be solved
+                    if (lab < k_max) atomicOr(&bad[g][lab >> 5], 1u << (lab & 31));
+                    lab = 256;
+                    d = 0;
+                }
+            } else {
+                lab = gen.labels[(size_t)p * M + x];
+            }
             labs[u] = lab;
             if (lab < k_max) {
                 const uint32_t c0 = tb.cap0[d];
@@ -164,7 +214,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             const uint32_t pk = packed[g][q];
             const uint32_t m = pk >> 16, csum = pk & 0xFFFF;
             feas = m >= 1 && m <= (uint32_t)N && csum >= (uint32_t)N && mincap[g][q] >= 1 &&
-                   ((hmask[g][q >> 5] >> (q & 31)) & 1u);
+                   ((hmask[g][q >> 5] >> (q & 31)) & 1u) && !((bad[g][q >> 5] >> (q & 31)) & 1u);
             cls = size_class((int)m);
             if (!feas) {
                 const size_t o = (size_t)p * k_max + q;
@@ -213,13 +263,17 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             run[c] += (uint32_t)__popcll(bm);
         }
     }
+    // layers of devices the DP kernel will not write: those outside every
+    // listed cluster; for ordered genomes every device (the DP kernel, which
+    // runs after this one, writes the listed replicas' devices, and a device
+    // missing from the ordering keeps 0)
     if (layers && p < P) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int d = lane + 64 * u;
+            const int x = lane + 64 * u;
             const int lab = labs[u];
-            if (d < M && (lab >= k_max || !((lmask[g][lab >> 5] >> (lab & 31)) & 1u)))
-                layers[(size_t)p * M + d] = 0;
+            if (x < M && (ordered || lab >= k_max || !((lmask[g][lab >> 5] >> (lab & 31)) & 1u)))
+                layers[(size_t)p * M + x] = 0;
         }
     }
 }
@@ -931,8 +985,7 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
 // (pool_cells + 2 (N+1) u64).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cells,
-                                           const uint8_t *__restrict__ labels,
-                                           const uint8_t *__restrict__ roles,
+                                           E2Genomes gen, const uint8_t *__restrict__ roles,
                                            uint32_t *counters, const uint32_t *__restrict__ list,
                                            size_t seg_cap, uint64_t *rows, uint8_t *tb_global,
                                            uint64_t *T,
@@ -974,14 +1027,25 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
         const int p = (int)(code >> 8);
         const int q = (int)(code & 0xFF);
 
-        // chain = devices with label q in ascending id (wave ballot compaction)
         int m = 0;
-        for (int base = 0; base < M; base += kWave) {
-            const int d = base + lane;
-            const bool in = d < M && labels[(size_t)p * M + d] == q;
-            const uint64_t mask = __ballot(in);
-            if (in) chain[m + __popcll(mask & ((1ull << lane) - 1))] = (uint8_t)d;
-            m += __popcll(mask);
+        if (gen.labels) {
+            // chain = devices with label q in ascending id (wave ballot compaction)
+            for (int base = 0; base < M; base += kWave) {
+                const int d = base + lane;
+                const bool in = d < M && gen.labels[(size_t)p * M + d] == q;
+                const uint64_t mask = __ballot(in);
+                if (in) chain[m + __popcll(mask & ((1ull << lane) - 1))] = (uint8_t)d;
+                m += __popcll(mask);
+            }
+        } else {
+            // chain = replica q's run of the ordering chromosome, in order
+            uint64_t part = 0;
+            for (int r = lane; r < q; r += kWave) part += gen.sizes[(size_t)p * k_max + r];
+            const uint64_t off = wave_sum_u64(part);
+            const int lo = (int)(off < (uint64_t)M ? off : (uint64_t)M);
+            const uint64_t end = off + gen.sizes[(size_t)p * k_max + q];
+            m = (int)(end < (uint64_t)M ? end : (uint64_t)M) - lo;
+            for (int k = lane; k < m; k += kWave) chain[k] = gen.order[(size_t)p * M + lo + k];
         }
         __syncthreads();
         const int r = roles[(size_t)p * k_max + q] != 0;
@@ -1213,6 +1277,184 @@ __global__ __launch_bounds__(64) void k_breed(int M, int P, int k_max,
     }
 }
 
+// ---------------------------------------------------------------------------
+// Two-chromosome GA (App. A): an ordering chromosome (a permutation of the
+// devices) and replica sizes, with a role per replica.  One wave per output
+// slot: elite copy, or tournaments (as above), ordering crossover with
+// repair, the grouping and roles of one parent, and with about 30%
+// probability one of four mutations.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kStOCut = 140, kStOGroup = 141, kStOMut = 142, kStOSwap = 143,
+                   kStORegen = 144, kStOSize = 145, kStOPerm = 146;
+// mutation kinds as fractions of 2^32: swap 0.20, regrow from a replica
+// 0.50, regrow the whole grouping 0.15, new ordering and grouping 0.15
+constexpr uint32_t kMutSwapBelow = 858993459u, kMutRegrowBelow = 3006477107u,
+                   kMutAllGroupBelow = 3650722201u;
+
+__device__ __forceinline__ uint64_t rng_at(uint64_t hs, uint32_t stream, uint64_t gene)
+{
+    return sm64(sm64(hs ^ (uint64_t)stream) ^ gene);
+}
+
+__global__ __launch_bounds__(64) void k_breed_ordered(
+    int M, int P, int k_max, const uint8_t *__restrict__ order_in,
+    const uint16_t *__restrict__ sizes_in, const uint8_t *__restrict__ roles_in,
+    const uint64_t *__restrict__ w, const uint64_t *__restrict__ ph, uint64_t seed, uint32_t g,
+    uint32_t tk, uint32_t mut, uint32_t n_elite, uint32_t max_replica,
+    const uint32_t *__restrict__ elite, uint8_t *order_out, uint16_t *sizes_out,
+    uint8_t *roles_out)
+{
+    __shared__ uint8_t child[256];
+    __shared__ uint8_t fill[256];
+    __shared__ uint32_t used[8];
+    __shared__ uint16_t szs[256];
+    __shared__ uint8_t rls[256];
+    const int s = blockIdx.x;
+    const int lane = threadIdx.x;
+    if ((uint32_t)s < n_elite) {
+        const uint32_t src = elite[s];
+        for (int t = lane; t < M; t += kWave)
+            order_out[(size_t)s * M + t] = order_in[(size_t)src * M + t];
+        for (int r = lane; r < k_max; r += kWave) {
+            sizes_out[(size_t)s * k_max + r] = sizes_in[(size_t)src * k_max + r];
+            roles_out[(size_t)s * k_max + r] = roles_in[(size_t)src * k_max + r];
+        }
+        return;
+    }
+    const uint64_t hs = sm64(sm64(seed ^ (uint64_t)g) ^ (uint64_t)s);  // (seed, g, s) prefix
+    uint32_t win = 0;
+    if (lane < 2) {
+        const uint32_t st0 = lane == 0 ? kStSelA : kStSelB;
+        uint32_t best = 0xFFFFFFFFu;
+        for (uint32_t t = 0; t < tk; ++t) {
+            const uint64_t u = sm64(sm64(hs ^ (uint64_t)(st0 + t)) ^ 0ull);
+            const uint32_t idx = (uint32_t)(((u >> 32) * (uint64_t)P) >> 32);
+            if (best == 0xFFFFFFFFu || key_less(w, ph, idx, best)) best = idx;
+        }
+        win = best;
+    }
+    const uint32_t a = __shfl(win, 0, kWave);
+    const uint32_t b = __shfl(win, 1, kWave);
+    const uint8_t *A = order_in + (size_t)a * M;
+    const uint8_t *B = order_in + (size_t)b * M;
+    const uint64_t lt = (1ull << lane) - 1;
+
+    // ordering crossover at c: a's prefix, then b's positions; b's nodes
+    // already in the prefix become holes, filled with b's prefix nodes that
+    // are missing, in b's order (M = 1: the child copies a)
+    if (lane < 8) used[lane] = 0;
+    __syncthreads();
+    int c = M;
+    if (M >= 2) {
+        const uint64_t u = rng_at(hs, kStOCut, 0);
+        c = 1 + (int)((((uint64_t)(uint32_t)u) * (uint64_t)(M - 1)) >> 32);
+    }
+    for (int t = lane; t < c; t += kWave) {
+        const uint32_t x = A[t];
+        child[t] = (uint8_t)x;
+        atomicOr(&used[x >> 5], 1u << (x & 31));
+    }
+    __syncthreads();
+    uint32_t nfill = 0;
+    for (int base = 0; base < c; base += kWave) {
+        const int t = base + lane;
+        bool f = false;
+        uint32_t x = 0;
+        if (t < c) {
+            x = B[t];
+            f = !((used[x >> 5] >> (x & 31)) & 1u);
+        }
+        const uint64_t mask = __ballot(f);
+        if (f) fill[nfill + __popcll(mask & lt)] = (uint8_t)x;
+        nfill += __popcll(mask);
+    }
+    __syncthreads();
+    uint32_t nh = 0;
+    for (int base = c; base < M; base += kWave) {
+        const int t = base + lane;
+        bool h = false;
+        uint32_t x = 0;
+        if (t < M) {
+            x = B[t];
+            h = (used[x >> 5] >> (x & 31)) & 1u;
+        }
+        const uint64_t mask = __ballot(h);
+        if (t < M) {
+            const uint32_t k = nh + __popcll(mask & lt);
+            child[t] = h ? fill[k < nfill ? k : 0] : (uint8_t)x;
+        }
+        nh += __popcll(mask);
+    }
+    // grouping and roles of one parent
+    const uint64_t ug = rng_at(hs, kStOGroup, 0);
+    const uint32_t src = ((uint32_t)ug < 0x80000000u) ? b : a;
+    for (int r = lane; r < k_max; r += kWave) {
+        szs[r] = sizes_in[(size_t)src * k_max + r];
+        rls[r] = roles_in[(size_t)src * k_max + r] != 0;
+    }
+    __syncthreads();
+    const uint64_t um = rng_at(hs, kStOMut, 0);
+    if ((uint32_t)(um >> 32) < mut && lane == 0) {
+        const uint32_t kind = (uint32_t)um;
+        if (kind < kMutSwapBelow) {
+            const uint64_t v = rng_at(hs, kStOSwap, 0);
+            const int i = (int)(((v >> 32) * (uint64_t)M) >> 32);
+            const int j = (int)((((uint64_t)(uint32_t)v) * (uint64_t)M) >> 32);
+            const uint8_t x = child[i];
+            child[i] = child[j];
+            child[j] = x;
+        } else {
+            int pos = 0;
+            if (kind < kMutRegrowBelow) {
+                // replicas that hold devices, then a uniform one among them
+                int R = 0;
+                long off = 0;
+                for (int r = 0; r < k_max; ++r) {
+                    if (szs[r] == 0 || off >= M) break;
+                    off += szs[r];
+                    ++R;
+                }
+                const uint64_t v = rng_at(hs, kStORegen, 0);
+                pos = (int)(((v >> 32) * (uint64_t)R) >> 32);
+            } else if (kind >= kMutAllGroupBelow) {
+                // a new ordering: Fisher-Yates from the identity
+                for (int t = 0; t < M; ++t) child[t] = (uint8_t)t;
+                for (int t = M - 1; t >= 1; --t) {
+                    const uint64_t v = rng_at(hs, kStOPerm, (uint64_t)t);
+                    const int j = (int)(((v >> 32) * (uint64_t)(t + 1)) >> 32);
+                    const uint8_t x = child[t];
+                    child[t] = child[j];
+                    child[j] = x;
+                }
+            }
+            // regrow the grouping from replica pos
+            long remaining = M;
+            for (int r = 0; r < pos; ++r) remaining -= szs[r];
+            if (remaining < 0) remaining = 0;
+            int r = pos;
+            while (remaining > 0 && r < k_max) {
+                const uint64_t u = rng_at(hs, kStOSize, (uint64_t)r);
+                long sz = 1 + (long)(((u >> 32) * (uint64_t)max_replica) >> 32);
+                if (r == k_max - 1 || sz > remaining) sz = remaining;
+                szs[r] = (uint16_t)sz;
+                rls[r] = (uint32_t)u >= 0x80000000u;
+                remaining -= sz;
+                ++r;
+            }
+            for (; r < k_max; ++r) {
+                szs[r] = 0;
+                rls[r] = 0;
+            }
+        }
+    }
+    __syncthreads();
+    for (int t = lane; t < M; t += kWave) order_out[(size_t)s * M + t] = child[t];
+    for (int r = lane; r < k_max; r += kWave) {
+        sizes_out[(size_t)s * k_max + r] = szs[r];
+        roles_out[(size_t)s * k_max + r] = rls[r];
+    }
+}
+
 }  // namespace
 
 int e2_dp_pool_cells(int N)
@@ -1261,16 +1503,16 @@ int e2_dp_slots(int N, int problems)
 }
 
 hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_max,
-                                const uint8_t *labels, const uint8_t *roles, const E2Work &wk,
+                                const E2Genomes &gen, const uint8_t *roles, const E2Work &wk,
                                 uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
     const size_t seg = (size_t)P * k_max;
     k_init<<<1, 64, 0, s>>>(wk.counters);
-    k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, labels, wk.counters, wk.list,
+    k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, wk.counters, wk.list,
                                                        seg, T, Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
-    k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, labels, roles, wk.counters,
+    k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles, wk.counters,
                                                       wk.list, seg, wk.rows, wk.tb_global, T,
                                                       Lambda, master, layers);
     if (wk.ev_end) (void)hipEventRecord(wk.ev_end, s);
@@ -1297,5 +1539,19 @@ hipError_t e2_launch_ga(hipStream_t s, int M, int P, int k_max, const uint8_t *l
     k_breed<<<P, 64, 0, s>>>(M, P, k_max, labels_in, roles_in, w, phase, seed, generation,
                              tournament_k, xo_thresh, mut_thresh, n_elite, elite_scratch,
                              labels_out, roles_out);
+    return hipGetLastError();
+}
+
+hipError_t e2_launch_ga_ordered(hipStream_t s, int M, int P, int k_max, const uint8_t *order_in,
+                                const uint16_t *sizes_in, const uint8_t *roles_in,
+                                const uint64_t *w, const uint64_t *phase, uint64_t seed,
+                                uint32_t generation, uint32_t tournament_k, uint32_t mut_thresh,
+                                uint32_t n_elite, uint32_t max_replica, uint32_t *elite_scratch,
+                                uint8_t *order_out, uint16_t *sizes_out, uint8_t *roles_out)
+{
+    if (n_elite > 0) k_elites<<<1, 1024, 0, s>>>(P, n_elite, w, phase, elite_scratch);
+    k_breed_ordered<<<P, 64, 0, s>>>(M, P, k_max, order_in, sizes_in, roles_in, w, phase, seed,
+                                     generation, tournament_k, mut_thresh, n_elite, max_replica,
+                                     elite_scratch, order_out, sizes_out, roles_out);
     return hipGetLastError();
 }

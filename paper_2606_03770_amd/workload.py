@@ -236,3 +236,57 @@ def random_small(seed: int, M: int, N: int, P: int, k_max: int, *,
         t_arrival_ns=int(rng.integers(0, 10**9)), nd_tokens=int(rng.integers(0, 2048)),
         min_tps_milli=int(rng.choice([0, 7000, 100000])),
         ga_seed=seed, generations=0)
+
+
+@dataclasses.dataclass
+class OrderedPopulation:
+    """A population of two-chromosome genomes (the paper's App. A gene): an
+    ordering chromosome order[P][M] (a permutation of the devices), a
+    grouping chromosome sizes[P][k_max] (replica sizes in ordering order,
+    summing to M, zeros after the last replica) and a role per replica."""
+    order: np.ndarray   # u8 [P][M]
+    sizes: np.ndarray   # u16 [P][k_max]
+    roles: np.ndarray   # u8 [P][k_max]
+    max_replica: int    # largest replica size the GA draws when it regrows a grouping
+    mutation_thresh_u32: int = int(0.3 * 2**32)  # App. A: about 30% of genes mutate
+
+    def ga_params(self, wl: Workload, generation: int = 0) -> dict:
+        return dict(seed=wl.ga_seed, generation=generation, tournament_k=wl.tournament_k,
+                    mutation_thresh_u32=self.mutation_thresh_u32, n_elite=wl.n_elite,
+                    max_replica=self.max_replica)
+
+    def subset(self, rows) -> "OrderedPopulation":
+        return dataclasses.replace(self, order=np.ascontiguousarray(self.order[rows]),
+                                   sizes=np.ascontiguousarray(self.sizes[rows]),
+                                   roles=np.ascontiguousarray(self.roles[rows]))
+
+
+def ordered_population(wl: Workload, seed: Optional[int] = None,
+                       population: Optional[int] = None) -> OrderedPopulation:
+    """Two-chromosome genomes for a named workload's problem instance.
+
+    Per genome: a uniform random ordering; K replicas with K drawn from the
+    workload's K range; replica sizes from K - 1 distinct uniform cut points
+    of the ordering; roles prefill with the workload's P(prefill).  The GA
+    regrows groupings with replica sizes up to twice M / (mean K).
+    """
+    spec = SPECS[wl.name] if wl.name in SPECS else None
+    klo, khi = spec["K"] if spec else (1, wl.k_max)
+    p_prefill = spec["p_prefill"] if spec else 0.5
+    if seed is None:
+        seed = 1000 + wl.ga_seed
+    rng = np.random.Generator(np.random.PCG64(seed))
+    M = wl.n_dev
+    P = wl.labels.shape[0] if population is None else int(population)
+    khi = min(khi, M)
+    klo = min(klo, khi)
+    order = np.stack([rng.permutation(M) for _ in range(P)]).astype(np.uint8)
+    sizes = np.zeros((P, wl.k_max), dtype=np.uint16)
+    K = rng.integers(klo, khi + 1, size=P)
+    for p in range(P):
+        cuts = np.sort(rng.choice(np.arange(1, M), size=int(K[p]) - 1, replace=False)) \
+            if K[p] > 1 else np.array([], dtype=np.int64)
+        sizes[p, :K[p]] = np.diff(np.concatenate([[0], cuts, [M]]))
+    roles = (rng.uniform(size=(P, wl.k_max)) >= p_prefill).astype(np.uint8)
+    max_replica = max(1, min(256, int(round(2 * M / ((klo + khi) / 2)))))
+    return OrderedPopulation(order=order, sizes=sizes, roles=roles, max_replica=max_replica)
