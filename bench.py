@@ -24,6 +24,10 @@ Printed on one JSON line:
                the current kernel sources
   cpu_baseline the CPU oracle on a bounded sample of the same generation-0
                population, single-threaded
+  two_chromosome  the same measurements for the paper's two-chromosome
+               genomes (an ordering of the devices cut into replicas, App. A):
+               e2_eval_population_ordered + e2_ga_step_ordered per generation
+               on the same problem instance and population size
 """
 from __future__ import annotations
 
@@ -56,7 +60,17 @@ def log(msg):
 # ---------------------------------------------------------------------------
 # Work accounting (host side, from the same integer inputs).
 # ---------------------------------------------------------------------------
-POOL_CELLS = 2048  # forward-row pool of a whole-wave DP problem (k_dp)
+MAX_BANDED_CHAIN = 64  # longest chain the banded DP path takes (one device per lane)
+LDS_TB_CELLS = 2048    # split-point bytes a DP wave keeps in LDS
+
+
+def pool_cells(N):
+    """Cells of a DP wave's forward-row pool: the largest band total
+    (m - 1)(N - m + 1) of a chain the banded path takes."""
+    best = max([(m - 1) * (N - m + 1) for m in range(2, min(MAX_BANDED_CHAIN, N) + 1)], default=0)
+    return max(best, LDS_TB_CELLS)
+
+
 U32_MAX_VALUE = 0xFFFFFE  # largest finite value of the u32-key path
 F64_LIMIT = 1 << 45       # prefix sums, head and link times of an fp64-key problem stay below
 OPS_PER_CANDIDATE_NARROW = 3  # u32 or fp64 keys: subtract, max, min
@@ -132,10 +146,38 @@ def value_bounds(wl, win):
     return vmax, vtot, tau
 
 
-def generation_work(wl, labels, roles, T, master, tabs):
+def label_problems(labels, k_max):
+    """(genome, cluster, chain) of every non-empty cluster of labelled
+    genomes; a chain lists the cluster's devices in ascending id."""
+    out = []
+    for p in range(labels.shape[0]):
+        row = labels[p]
+        for q in np.unique(row):
+            if q < k_max:
+                out.append((p, int(q), np.nonzero(row == q)[0]))
+    return out
+
+
+def ordered_problems(order, sizes):
+    """(genome, replica, chain) of every non-empty replica of two-chromosome
+    genomes; a chain is the replica's run of the ordering.  Replicas holding
+    an id >= M are left out (the library rejects them before the DP)."""
+    P, M = order.shape
+    ends = np.minimum(np.cumsum(sizes.astype(np.int64), axis=1), M)
+    starts = np.concatenate([np.zeros((P, 1), np.int64), ends[:, :-1]], axis=1)
+    out = []
+    for p in range(P):
+        for q in np.nonzero(ends[p] > starts[p])[0]:
+            chain = order[p, starts[p, q]:ends[p, q]].astype(np.int64)
+            if chain.max() < M:
+                out.append((p, int(q), chain))
+    return out
+
+
+def generation_work(wl, problems, roles, T, master, tabs):
     """(Algorithm 1 cells over feasible problems, useful j-candidates the DP
     kernel evaluates with u64 keys, those it evaluates with u32 or fp64 keys)
-    for one population.  The candidate count follows k_dp row by row:
+    for one population, given as its (genome, cluster, chain) problems.  The candidate count follows k_dp row by row:
     forward rows, reversed rows, one combine per master, the chosen master's
     rows and last cell (banded path), or one full table per master plus the
     chosen master's again (reference path, u64 keys).  A problem takes the
@@ -145,8 +187,7 @@ def generation_work(wl, labels, roles, T, master, tabs):
     U32_MAX_VALUE (u32 keys) or its devices' total times and its link times
     are below F64_LIMIT (fp64 keys)."""
     win, winR, cap, C, CR, vmax, vtot, tau = tabs
-    N, K = wl.n_layer, wl.k_max
-    P, M = labels.shape
+    N = wl.n_layer
     feasible = T != INF
     cells = 0
     cand = 0
@@ -168,13 +209,8 @@ def generation_work(wl, labels, roles, T, master, tabs):
 
     # group problems by chain length
     probs = {}
-    for p in range(P):
-        row = labels[p]
-        for q in np.unique(row):
-            if q >= K:
-                continue
-            chain = np.nonzero(row == q)[0]
-            probs.setdefault(len(chain), []).append((p, q, chain))
+    for p, q, chain in problems:
+        probs.setdefault(len(chain), []).append((p, q, chain))
     for m, lst in probs.items():
         n = len(lst)
         pq = np.array([(a, b) for a, b, _ in lst])
@@ -208,7 +244,7 @@ def generation_work(wl, labels, roles, T, master, tabs):
         pool = sizes[:, :m - 1].sum(1)
         # chains of up to 64 devices whose forward bands fit the pool take the
         # banded path, the others one full table per master
-        fast = (m <= 64) & (pool <= POOL_CELLS) & narrow
+        fast = (m <= MAX_BANDED_CHAIN) & (pool <= pool_cells(N)) & narrow
         # --- fast path
         if fast.any():
             chf, c0f, cHf = ch[fast], c0[fast], cH[fast]
@@ -269,6 +305,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5_256dev_126L_ga", choices=workload.NAMES)
+    ap.add_argument("--ordered-steps", type=int, default=5,
+                    help="timed generations of the two-chromosome GA (0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU-oracle sample (0 disables)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -294,79 +332,42 @@ def main():
     P, M, K = wl.population, wl.n_dev, wl.k_max
     ctx = e2.e2_ctx_create(wl.problem_arrays())
     stream = torch.cuda.current_stream()
-    L0 = torch.from_numpy(wl.labels).to(dev)
-    R0 = torch.from_numpy(wl.roles).to(dev)
-    Lb = [torch.empty_like(L0), torch.empty_like(L0)]
-    Rb = [torch.empty_like(R0), torch.empty_like(R0)]
-    fit = {k: torch.empty(P, dtype=torch.int64, device=dev) for k in ("w", "phase")}
     fp = wl.fitness_params()
-
-    def reset():
-        Lb[0].copy_(L0)
-        Rb[0].copy_(R0)
-        torch.cuda.synchronize()
-
-    def run(n_steps, events=None):
-        cur = 0
-        for g in range(n_steps):
-            if events is not None:
-                events[g][0].record(stream)
-            e2.e2_eval_population(ctx, Lb[cur], Rb[cur], fp, with_rates=False, out=fit)
-            if events is not None:
-                events[g][1].record(stream)
-            e2.e2_ga_step(ctx, Lb[cur], Rb[cur], fit["w"], fit["phase"], wl.ga_params(g),
-                          out=(Lb[1 - cur], Rb[1 - cur]))
-            cur = 1 - cur
-
-    log(f"workload {wl.name}: P={P} M={M} N={wl.n_layer} k_max={K}; warmup {args.warmup}")
-    reset()
-    run(args.warmup)
-    torch.cuda.synchronize()
-    reset()
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
-    # the library records HIP events around its DP kernel on the call's stream
-    e2.e2_ctx_dp_timing(ctx, args.steps)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    run(args.steps, events)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    n_dp, dp_ms = e2.e2_ctx_dp_elapsed(ctx)
-    e2.e2_ctx_dp_timing(ctx, 0)
-    assert n_dp == args.steps, (n_dp, args.steps)
-    eval_ms = [a.elapsed_time(b) for a, b in events]
-    log(f"timed {args.steps} steps: {elapsed * 1e3:.2f} ms; eval launches "
-        f"{np.mean(eval_ms):.3f} ms avg; DP kernel {dp_ms / n_dp:.3f} ms avg")
-
-    # replay the same generations to count the work (outside the timed region)
     win, winR, cap = window_tables(wl)
     wcr = (win, winR, cap) + count_tables(win, winR, wl.n_layer) + value_bounds(wl, win)
-    Lr, Rr = L0.clone(), R0.clone()
-    cells = cand = cand32 = 0
-    for g in range(args.steps):
-        sol = e2.e2_solve_partitions(ctx, Lr, Rr)
-        f2 = e2.e2_eval_population(ctx, Lr, Rr, fp, with_rates=False)
-        lo, ro = e2.e2_ga_step(ctx, Lr, Rr, f2["w"], f2["phase"], wl.ga_params(g))
+
+    # --- labelled genomes (the headline): cluster labels per device
+    L0 = torch.from_numpy(wl.labels).to(dev)
+    R0 = torch.from_numpy(wl.roles).to(dev)
+    bufs = [(torch.empty_like(L0), torch.empty_like(R0)) for _ in range(2)]
+    fit = {k: torch.empty(P, dtype=torch.int64, device=dev) for k in ("w", "phase")}
+
+    def step(g, cur):
+        L, R = bufs[cur]
+        e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=fit)
+        e2.e2_ga_step(ctx, L, R, fit["w"], fit["phase"], wl.ga_params(g), out=bufs[1 - cur])
+
+    def count(g, pop):
+        L, R = pop
+        sol = e2.e2_solve_partitions(ctx, L, R)
+        f2 = e2.e2_eval_population(ctx, L, R, fp, with_rates=False)
+        nxt = e2.e2_ga_step(ctx, L, R, f2["w"], f2["phase"], wl.ga_params(g))
         torch.cuda.synchronize()
-        c1, c2, c3 = generation_work(wl, Lr.cpu().numpy(), Rr.cpu().numpy(), e2.u64(sol["T"]),
-                                     sol["master"].cpu().numpy(), wcr)
-        cells += c1
-        cand += c2
-        cand32 += c3
-        Lr, Rr = lo, ro
-    value = cells / elapsed
-    dp_time = dp_ms / 1e3
-    achieved = (cand * OPS_PER_CANDIDATE + cand32 * OPS_PER_CANDIDATE_NARROW) / dp_time
-    traffic = profiled_traffic(wl.name)
+        labels = L.cpu().numpy()
+        work = generation_work(wl, label_problems(labels, K), R.cpu().numpy(),
+                               e2.u64(sol["T"]), sol["master"].cpu().numpy(), wcr)
+        return work, nxt
+
+    log(f"workload {wl.name}: P={P} M={M} N={wl.n_layer} k_max={K}; warmup {args.warmup}")
+    t = measure(torch, ctx, stream, bufs, (L0, R0), step, count, args.warmup, args.steps)
     result = {
         "metric": METRIC,
-        "value": value,
+        "value": t["cells"] / t["elapsed"],
         "unit": "DP cells/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": elapsed * 1e3 / args.steps,
+        "ms_per_step": t["elapsed"] * 1e3 / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -375,22 +376,115 @@ def main():
         "config": {"workload": wl.name, "devices": M, "layers": wl.n_layer,
                    "population": P, "clusters_per_genome": "32-48" if K == 48 else str(K),
                    "step": "one GA generation: e2_eval_population + e2_ga_step"},
-        "fitness_evals_per_s": P * args.steps / elapsed,
-        "dp_cells_per_step": cells / args.steps,
-        "j_candidates_per_step": (cand + cand32) / args.steps,
-        "j_candidates_u32_or_f64_keys_per_step": cand32 / args.steps,
-        "roofline": {"bound": "alu", "kernel": "k_dp",
-                     "achieved": achieved / 1e12, "peak": INT_VALU_PEAK / 1e12,
-                     "unit": "TOP/s (int32 VALU)", "frac": achieved / INT_VALU_PEAK,
-                     "traffic": traffic,
-                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
-                                     "copy-calibrated)",
-                     "avg_launch_ms": dp_time * 1e3 / args.steps,
-                     "eval_launch_ms": float(np.mean(eval_ms))},
+        "fitness_evals_per_s": P * args.steps / t["elapsed"],
+        "dp_cells_per_step": t["cells"] / args.steps,
+        "j_candidates_per_step": (t["cand"] + t["cand32"]) / args.steps,
+        "j_candidates_u32_or_f64_keys_per_step": t["cand32"] / args.steps,
+        "roofline": roofline(t, args.steps, profiled_traffic(wl.name)),
     }
+
+    # --- two-chromosome genomes (ordering + replica sizes, App. A) on the
+    # same problem instance and population size
+    if args.ordered_steps > 0:
+        op = workload.ordered_population(wl)
+        O0, S0, Q0 = (torch.from_numpy(a).to(dev) for a in (op.order, op.sizes, op.roles))
+        obufs = [tuple(torch.empty_like(x) for x in (O0, S0, Q0)) for _ in range(2)]
+
+        def ostep(g, cur):
+            O, S, Q = obufs[cur]
+            e2.e2_eval_population_ordered(ctx, O, S, Q, fp, with_rates=False, out=fit)
+            e2.e2_ga_step_ordered(ctx, O, S, Q, fit["w"], fit["phase"], op.ga_params(wl, g),
+                                  out=obufs[1 - cur])
+
+        def ocount(g, pop):
+            O, S, Q = pop
+            sol = e2.e2_solve_partitions_ordered(ctx, O, S, Q)
+            f2 = e2.e2_eval_population_ordered(ctx, O, S, Q, fp, with_rates=False)
+            nxt = e2.e2_ga_step_ordered(ctx, O, S, Q, f2["w"], f2["phase"], op.ga_params(wl, g))
+            torch.cuda.synchronize()
+            probs = ordered_problems(O.cpu().numpy(), S.cpu().numpy())
+            work = generation_work(wl, probs, Q.cpu().numpy(), e2.u64(sol["T"]),
+                                   sol["master"].cpu().numpy(), wcr)
+            return work, nxt
+
+        log(f"two-chromosome genomes: P={P}, max replica {op.max_replica}")
+        n = args.ordered_steps
+        t2 = measure(torch, ctx, stream, obufs, (O0, S0, Q0), ostep, ocount, args.warmup, n)
+        result["two_chromosome"] = {
+            "step": "one GA generation: e2_eval_population_ordered + e2_ga_step_ordered",
+            "steps": n,
+            "ms_per_step": t2["elapsed"] * 1e3 / n,
+            "dp_cells_per_s": t2["cells"] / t2["elapsed"],
+            "fitness_evals_per_s": P * n / t2["elapsed"],
+            "dp_cells_per_step": t2["cells"] / n,
+            "j_candidates_per_step": (t2["cand"] + t2["cand32"]) / n,
+            "roofline": roofline(t2, n, None),
+        }
     if args.cpu_seconds > 0:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def measure(torch, ctx, stream, bufs, init, step, count, warmup, steps):
+    """Time `steps` generations (after `warmup` untimed ones) from the
+    initial population `init`, ping-ponging between the two buffer sets;
+    then replay the same generations outside the timed region and count
+    their work.  The library records HIP events around its DP kernel on the
+    call's stream, one pair per evaluation."""
+    def reset():
+        for dst, src in zip(bufs[0], init):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    def run(n, events=None):
+        cur = 0
+        for g in range(n):
+            if events is not None:
+                events[g][0].record(stream)
+            step(g, cur)
+            if events is not None:
+                events[g][1].record(stream)
+            cur = 1 - cur
+
+    reset()
+    run(warmup)
+    torch.cuda.synchronize()
+    reset()
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+    e2.e2_ctx_dp_timing(ctx, steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(steps, events)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    n_dp, dp_ms = e2.e2_ctx_dp_elapsed(ctx)
+    e2.e2_ctx_dp_timing(ctx, 0)
+    assert n_dp == steps, (n_dp, steps)
+    step_ms = [a.elapsed_time(b) for a, b in events]
+    log(f"timed {steps} steps: {elapsed * 1e3:.2f} ms; generation {np.mean(step_ms):.3f} ms "
+        f"avg on the stream; DP kernel {dp_ms / n_dp:.3f} ms avg")
+    cells = cand = cand32 = 0
+    pop = tuple(x.clone() for x in init)
+    for g in range(steps):
+        (c1, c2, c3), pop = count(g, pop)
+        cells += c1
+        cand += c2
+        cand32 += c3
+    return dict(elapsed=elapsed, dp_s=dp_ms / 1e3, step_ms=float(np.mean(step_ms)), cells=cells,
+                cand=cand, cand32=cand32)
+
+
+def roofline(t, steps, traffic):
+    achieved = (t["cand"] * OPS_PER_CANDIDATE + t["cand32"] * OPS_PER_CANDIDATE_NARROW) / t["dp_s"]
+    return {"bound": "alu", "kernel": "k_dp",
+            "achieved": achieved / 1e12, "peak": INT_VALU_PEAK / 1e12,
+            "unit": "TOP/s (int32 VALU)", "frac": achieved / INT_VALU_PEAK,
+            "traffic": traffic,
+            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                            "copy-calibrated)",
+            "avg_launch_ms": t["dp_s"] * 1e3 / steps,
+            "generation_ms_on_stream": t["step_ms"]}
 
 
 LIB_SOURCES = ("e2_api.hip", "e2_internal.h", "e2_kernels.hip")

@@ -117,9 +117,9 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
     const size_t problems = (size_t)P * k_max;
     *slots = e2_dp_slots(ctx->N, (int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX));
     const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
-    // the fallback is needed only when some chain's split points exceed the
-    // LDS pool of the reference path
-    const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_pool_cells(ctx->N);
+    // the global split-point table is needed only when some chain's split
+    // points (m - 1 rows of at most N cells) can exceed their LDS copy
+    const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_lds_tb_cells(ctx->N);
     *tb_bytes = need_tb ? (size_t)(*slots) * ctx->N * ctx->N : 0;
     return align256(32) + align256(problems * 4 * 4) +
            align256((size_t)(*slots) * e2_dp_row_words(ctx->N) * 8) + align256(*tb_bytes);

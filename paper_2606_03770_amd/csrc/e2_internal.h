@@ -59,6 +59,7 @@ int e2_dp_slots(int N, int problems);
 // Forward-row pool of one DP wave (u64 cells), its global row storage
 // (u64 per wave) and its dynamic LDS bytes.
 int e2_dp_pool_cells(int N);
+int e2_dp_lds_tb_cells(int N);
 size_t e2_dp_row_words(int N);
 size_t e2_dp_lds_bytes(int N);
 

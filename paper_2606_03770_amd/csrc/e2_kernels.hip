@@ -35,7 +35,6 @@ namespace {
 constexpr int kWave = 64;
 
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
-__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 
 // Wave-wide reductions: DPP permutations within each 16-lane row (quad
 // swaps, half mirror, mirror), then the four row results read into scalars.
@@ -59,15 +58,6 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane)
     return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
-{
-    v = umin64(v, dpp_u64<0xb1>(v));
-    v = umin64(v, dpp_u64<0x4e>(v));
-    v = umin64(v, dpp_u64<0x141>(v));
-    v = umin64(v, dpp_u64<0x140>(v));
-    return umin64(umin64(readlane_u64(v, 0), readlane_u64(v, 16)),
-                  umin64(readlane_u64(v, 32), readlane_u64(v, 48)));
-}
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
 {
     v = umax64(v, dpp_u64<0xb1>(v));
@@ -666,6 +656,10 @@ __device__ __forceinline__ RowOut<K> store_to(K *vals, K *vals_g, uint8_t *tbs)
 // are also written to a per-wave global pool for the combines.
 // ---------------------------------------------------------------------------
 constexpr int kMaxBandedChain = kWave;
+// split-point bytes kept in LDS per wave; larger tables (the bands of long
+// chains with roomy devices, or the reference path's full rows) go to the
+// wave's region of the global split-point table
+constexpr int kLdsTbCells = 2048;
 
 // Per-position table of a chain: lane k-1 holds chain position k (1-based)
 // as four packed words (fields < 256 except the pool offset) and three u64
@@ -757,7 +751,7 @@ __device__ __forceinline__ void set_prev(Row<K> &rw, const K *prev, int plo, int
 // produce; false when the banded path cannot take the chain.
 __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm, int r,
                                            const uint8_t *chain, int m, int lane, ChainRegs &cr,
-                                           uint64_t *bound, uint64_t *bound_tot)
+                                           uint64_t *bound, uint64_t *bound_tot, int *pool_cells)
 {
     const int N = tb.N, M = tb.M;
     if (m > kMaxBandedChain) return false;
@@ -806,6 +800,7 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
     cr.wb = (uint32_t)lo | (uint32_t)hi << 8 | (uint32_t)lmin1 << 16;
     cr.wc = ((uint32_t)off & 0xFFFFu) | (uint32_t)lminR << 16 | (uint32_t)capR << 24;
     cr.wd = (uint32_t)devR | (uint32_t)glo << 8 | (uint32_t)ghi << 16;
+    *pool_cells = pool_need;
     return pool_need <= sm.pool_cells;
 }
 
@@ -912,6 +907,10 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + f8(lane_w(cr.wa, m - 1), 0)) * N + (N - 1)];
         rw.lmin = uni(rw.lmin);
         row_pass(rw, store_to<K>(Rw[m & 1], nullptr, last_tb), ps, lane, N);
+        // the split points may sit in global memory (long bands): complete
+        // every lane's stores before lane 0 walks them
+        __builtin_amdgcn_s_waitcnt(0);
+        __threadfence_block();
         if (lane == 0) {
             int i = N - 1;
             int j = *last_tb;
@@ -984,7 +983,7 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
 // of the forward-row pool; the row values live in a per-wave global region
 // (pool_cells + 2 (N+1) u64).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cells,
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_dp(E2Tables tb, int k_max, int pool_cells,
                                            E2Genomes gen, const uint8_t *__restrict__ roles,
                                            uint32_t *counters, const uint32_t *__restrict__ list,
                                            size_t seg_cap, uint64_t *rows, uint8_t *tb_global,
@@ -1055,11 +1054,18 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
         int best_mu = 0;
         ChainRegs cr;
         uint64_t bound = E2_INF64, bound_tot = E2_INF64;
-        const bool banded = chain_regs(tb, sm, r, chain, m, lane, cr, &bound, &bound_tot);
+        int pool_need = 0;
+        bool banded = chain_regs(tb, sm, r, chain, m, lane, cr, &bound, &bound_tot, &pool_need);
+        // split points of bands beyond the LDS copy go to the global table
+        DpSmem smb = sm;
+        if (pool_need > kLdsTbCells) {
+            smb.tbp = tb_global ? tb_global + (size_t)blockIdx.x * N * N : nullptr;
+            banded = banded && tb_global != nullptr;
+        }
         if (banded && bound <= kU32MaxValue)
-            dp_banded<uint32_t>(tb, sm, cr, r, m, lane, &best, &best_mu, start, &last_tb);
+            dp_banded<uint32_t>(tb, smb, cr, r, m, lane, &best, &best_mu, start, &last_tb);
         else if (banded && bound_tot < kF64Limit)
-            dp_banded<double>(tb, sm, cr, r, m, lane, &best, &best_mu, start, &last_tb);
+            dp_banded<double>(tb, smb, cr, r, m, lane, &best, &best_mu, start, &last_tb);
         else {
             // reference path: a full table per master, then the chosen
             // master's table again with split points
@@ -1071,7 +1077,7 @@ __global__ __launch_bounds__(64) void k_dp(E2Tables tb, int k_max, int pool_cell
                 }
             }
             if (best != E2_INF64) {
-                uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)pool_cells)
+                uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)kLdsTbCells)
                                    ? sm.tbp
                                    : tb_global + (size_t)blockIdx.x * N * N;
                 dp_table(tb, sm, r, chain, m, best_mu, tbp, lane);
@@ -1459,15 +1465,25 @@ __global__ __launch_bounds__(64) void k_breed_ordered(
 
 int e2_dp_pool_cells(int N)
 {
+    // the forward bands of a chain of m devices hold at most
+    // (m-1)(N-m+1) cells (band k lies in [k-1, N-1-(m-k)]); the pool takes
+    // the largest such count over the chains the banded path accepts
+    int best = 0;
+    for (int m = 2; m <= kMaxBandedChain && m <= N; ++m) best = max(best, (m - 1) * (N - m + 1));
+    return max(best, kLdsTbCells);
+}
+
+int e2_dp_lds_tb_cells(int N)
+{
     (void)N;
-    return 2048;
+    return kLdsTbCells;
 }
 
 size_t e2_dp_row_words(int N) { return (size_t)e2_dp_pool_cells(N) + 2 * (size_t)(N + 1); }
 
 size_t e2_dp_lds_bytes(int N)
 {
-    return (size_t)16 * N + (size_t)16 * (N + 1) + (size_t)e2_dp_pool_cells(N);
+    return (size_t)16 * N + (size_t)16 * (N + 1) + (size_t)kLdsTbCells;
 }
 
 int e2_dp_slots(int N, int problems)

@@ -265,10 +265,13 @@ def ordered_population(wl: Workload, seed: Optional[int] = None,
                        population: Optional[int] = None) -> OrderedPopulation:
     """Two-chromosome genomes for a named workload's problem instance.
 
-    Per genome: a uniform random ordering; K replicas with K drawn from the
-    workload's K range; replica sizes from K - 1 distinct uniform cut points
-    of the ordering; roles prefill with the workload's P(prefill).  The GA
-    regrows groupings with replica sizes up to twice M / (mean K).
+    Each genome is generated the way the GA regenerates both chromosomes: a
+    uniform random ordering, then replicas of 1 + floor(U * max_replica)
+    devices (U uniform in [0, 1)) along it until the devices run out, the
+    last of the k_max slots taking whatever remains; roles prefill with the
+    workload's P(prefill).  max_replica, also the GA's regrowth bound, is
+    twice M over the mean of the workload's K range, so a genome holds about
+    that many replicas.
     """
     spec = SPECS[wl.name] if wl.name in SPECS else None
     klo, khi = spec["K"] if spec else (1, wl.k_max)
@@ -280,13 +283,18 @@ def ordered_population(wl: Workload, seed: Optional[int] = None,
     P = wl.labels.shape[0] if population is None else int(population)
     khi = min(khi, M)
     klo = min(klo, khi)
-    order = np.stack([rng.permutation(M) for _ in range(P)]).astype(np.uint8)
-    sizes = np.zeros((P, wl.k_max), dtype=np.uint16)
-    K = rng.integers(klo, khi + 1, size=P)
-    for p in range(P):
-        cuts = np.sort(rng.choice(np.arange(1, M), size=int(K[p]) - 1, replace=False)) \
-            if K[p] > 1 else np.array([], dtype=np.int64)
-        sizes[p, :K[p]] = np.diff(np.concatenate([[0], cuts, [M]]))
-    roles = (rng.uniform(size=(P, wl.k_max)) >= p_prefill).astype(np.uint8)
     max_replica = max(1, min(256, int(round(2 * M / ((klo + khi) / 2)))))
+    K = wl.k_max
+    order = np.stack([rng.permutation(M) for _ in range(P)]).astype(np.uint8)
+    draws = 1 + (rng.uniform(size=(P, K)) * max_replica).astype(np.int64)
+    sizes = np.zeros((P, K), dtype=np.uint16)
+    for p in range(P):
+        left = M
+        for r in range(K):
+            if left == 0:
+                break
+            s = left if r == K - 1 else min(int(draws[p, r]), left)
+            sizes[p, r] = s
+            left -= s
+    roles = ((rng.uniform(size=(P, K)) >= p_prefill) & (sizes > 0)).astype(np.uint8)
     return OrderedPopulation(order=order, sizes=sizes, roles=roles, max_replica=max_replica)

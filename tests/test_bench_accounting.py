@@ -40,8 +40,8 @@ def _windows(wl):
     return win, winR
 
 
-def _direct(wl, labels, roles, T, master):
-    N, K = wl.n_layer, wl.k_max
+def _direct(wl, problems, roles, T, master):
+    N = wl.n_layer
     win, winR = _windows(wl)
     t, h, tau = e2.e2_quantise(wl.problem_arrays())
     cap = np.zeros((2, wl.n_dev), dtype=np.int64)
@@ -63,66 +63,64 @@ def _direct(wl, labels, roles, T, master):
         return sum(max(0, i - max(int(w[i]), kmin) + 1) for i in range(lo, hi + 1) if w[i] != 255)
 
     c64 = c32 = 0
-    for p in range(labels.shape[0]):
-        for q in range(K):
-            ch = np.nonzero(labels[p] == q)[0]
-            m = len(ch)
-            if m == 0:
-                continue
-            c0, cH = cap[0][ch], cap[1][ch]
-            if not (m <= N and c0.sum() >= N and c0.min() >= 1 and cH.max() >= 1):
-                continue
-            r = int(roles[p, q] != 0)
-            pre = np.r_[0, np.cumsum(c0)]
-            tot = pre[m]
-            flo = {k: max(k - 1, N - 1 - (tot - pre[k])) for k in range(1, m + 1)}
-            fhi = {k: min(N - 1 - (m - k), pre[k] - 1) for k in range(1, m + 1)}
-            pool = sum(max(0, fhi[k] - flo[k] + 1) for k in range(1, m))
-            mu = int(np.nonzero(ch == master[p, q])[0][0]) + 1 if T[p, q] != INF else 0
+    for p, q, ch in problems:
+        m = len(ch)
+        c0, cH = cap[0][ch], cap[1][ch]
+        if not (m <= N and c0.sum() >= N and c0.min() >= 1 and cH.max() >= 1):
+            continue
+        r = int(roles[p, q] != 0)
+        pre = np.r_[0, np.cumsum(c0)]
+        tot = pre[m]
+        flo = {k: max(k - 1, N - 1 - (tot - pre[k])) for k in range(1, m + 1)}
+        fhi = {k: min(N - 1 - (m - k), pre[k] - 1) for k in range(1, m + 1)}
+        pool = sum(max(0, fhi[k] - flo[k] + 1) for k in range(1, m))
+        mu = int(np.nonzero(ch == master[p, q])[0][0]) + 1 if T[p, q] != INF else 0
+        c = 0
+        # every band total is at most (m - 1)(N - m + 1)
+        assert pool <= (m - 1) * (N - m + 1)
+        banded = m <= 64 and pool <= bench.pool_cells(N)
+        if banded:
+            for k in range(2, m):                            # forward rows
+                c += cnt(win[0][ch[k - 1]], max(k - 1, flo[k] - c0[k - 1] + 1), flo[k], fhi[k])
+            for mm in range(2, m + 1):                       # combines
+                if cH[mm - 1] > 0:
+                    c += cnt(win[1][ch[mm - 1]], max(mm - 1, flo[mm] - cH[mm - 1] + 1),
+                             flo[mm], fhi[mm])
+            for tt in range(2, m):                           # reversed rows
+                kd = m + 1 - tt
+                gl = max(kd - 1, N - (tot - pre[kd - 1]))
+                gh = min(pre[kd - 1], N - (m - kd + 1))
+                if gh >= gl:
+                    c += cnt(winR[ch[kd - 1]], max(tt - 1, N - 1 - gh - c0[kd - 1] + 1),
+                             N - 1 - gh, N - 1 - gl)
+            if mu:                                           # chosen master's rows
+                for k in range(max(mu, 2), m):
+                    f = int(k == mu)
+                    cp = cH[k - 1] if f else c0[k - 1]
+                    c += cnt(win[f][ch[k - 1]], max(k - 1, flo[k] - cp + 1), flo[k], fhi[k])
+                if m >= 2:
+                    f = int(mu == m)
+                    cp = cH[m - 1] if f else c0[m - 1]
+                    c += cnt(win[f][ch[m - 1]], max(m - 1, N - cp), N - 1, N - 1)
+        else:                                                # one table per master
+            for mm in list(range(1, m + 1)) + ([mu] if mu else []):
+                for k in range(2, m + 1):
+                    c += cnt(win[int(k == mm)][ch[k - 1]], k - 1, k - 1, N - 1)
+        links = [int(tau[r, ch[k - 1], ch[k]]) for k in range(1, m)]
+        links = [x for x in links if x != INF]
+        bound = max([stage_max(r, d) for d in ch] + links)
+        bound_tot = max([int(t[r, d].sum(dtype=np.uint64)) + int(h[r, d]) for d in ch] + links)
+        narrow = bound <= bench.U32_MAX_VALUE or bound_tot < bench.F64_LIMIT
+        if banded and not narrow:      # the reference path: recount as full tables
             c = 0
-            banded = m <= 64 and pool <= bench.POOL_CELLS
-            if banded:
-                for k in range(2, m):                            # forward rows
-                    c += cnt(win[0][ch[k - 1]], max(k - 1, flo[k] - c0[k - 1] + 1), flo[k], fhi[k])
-                for mm in range(2, m + 1):                       # combines
-                    if cH[mm - 1] > 0:
-                        c += cnt(win[1][ch[mm - 1]], max(mm - 1, flo[mm] - cH[mm - 1] + 1),
-                                 flo[mm], fhi[mm])
-                for tt in range(2, m):                           # reversed rows
-                    kd = m + 1 - tt
-                    gl = max(kd - 1, N - (tot - pre[kd - 1]))
-                    gh = min(pre[kd - 1], N - (m - kd + 1))
-                    if gh >= gl:
-                        c += cnt(winR[ch[kd - 1]], max(tt - 1, N - 1 - gh - c0[kd - 1] + 1),
-                                 N - 1 - gh, N - 1 - gl)
-                if mu:                                           # chosen master's rows
-                    for k in range(max(mu, 2), m):
-                        f = int(k == mu)
-                        cp = cH[k - 1] if f else c0[k - 1]
-                        c += cnt(win[f][ch[k - 1]], max(k - 1, flo[k] - cp + 1), flo[k], fhi[k])
-                    if m >= 2:
-                        f = int(mu == m)
-                        cp = cH[m - 1] if f else c0[m - 1]
-                        c += cnt(win[f][ch[m - 1]], max(m - 1, N - cp), N - 1, N - 1)
-            else:                                                # one table per master
-                for mm in list(range(1, m + 1)) + ([mu] if mu else []):
-                    for k in range(2, m + 1):
-                        c += cnt(win[int(k == mm)][ch[k - 1]], k - 1, k - 1, N - 1)
-            links = [int(tau[r, ch[k - 1], ch[k]]) for k in range(1, m)]
-            links = [x for x in links if x != INF]
-            bound = max([stage_max(r, d) for d in ch] + links)
-            bound_tot = max([int(t[r, d].sum(dtype=np.uint64)) + int(h[r, d]) for d in ch] + links)
-            narrow = bound <= bench.U32_MAX_VALUE or bound_tot < bench.F64_LIMIT
-            if banded and not narrow:      # the reference path: recount as full tables
-                c = 0
-                for mm in list(range(1, m + 1)) + ([mu] if mu else []):
-                    for k in range(2, m + 1):
-                        c += cnt(win[int(k == mm)][ch[k - 1]], k - 1, k - 1, N - 1)
-                banded = False
-            if banded:
-                c32 += c
-            else:
-                c64 += c
+            for mm in list(range(1, m + 1)) + ([mu] if mu else []):
+                for k in range(2, m + 1):
+                    c += cnt(win[int(k == mm)][ch[k - 1]], k - 1, k - 1, N - 1)
+            banded = False
+        if banded:
+            c32 += c
+        else:
+            c64 += c
     return c64, c32
 
 
@@ -133,8 +131,9 @@ def test_candidate_counts_match_a_direct_walk(orc, name, P):
     sol = oracle.eval_population(wl)
     win, winR, cap = bench.window_tables(wl)
     tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
-    cells, c64, c32 = bench.generation_work(wl, wl.labels, wl.roles, sol["T"], sol["master"], tabs)
-    assert (c64, c32) == _direct(wl, wl.labels, wl.roles, sol["T"], sol["master"])
+    probs = bench.label_problems(wl.labels, wl.k_max)
+    cells, c64, c32 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs)
+    assert (c64, c32) == _direct(wl, probs, wl.roles, sol["T"], sol["master"])
     assert c64 + c32 > 0
     assert c32 > 0                   # u32 / fp64 keys
 
@@ -145,9 +144,33 @@ def test_reference_path_counts():
     sol = oracle.eval_population(wl)
     win, winR, cap = bench.window_tables(wl)
     tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
-    _, c64, c32 = bench.generation_work(wl, wl.labels, wl.roles, sol["T"], sol["master"], tabs)
-    assert (c64, c32) == _direct(wl, wl.labels, wl.roles, sol["T"], sol["master"])
+    probs = bench.label_problems(wl.labels, wl.k_max)
+    _, c64, c32 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs)
+    assert (c64, c32) == _direct(wl, probs, wl.roles, sol["T"], sol["master"])
     assert c64 > 0 and c32 == 0   # the reference path has u64 keys only
+
+
+@pytest.mark.parametrize("name,P", [("c2_32dev_48L", 24), ("c5_256dev_126L_ga", 6)])
+def test_candidate_counts_of_ordered_genomes(orc, name, P):
+    """Two-chromosome genomes: the problems are the replicas' ordering runs
+    (checked against the oracle's replica ranges) and the counts match the
+    direct walk over those chains."""
+    wl = workload.make(name, population=P)
+    op = workload.ordered_population(wl)
+    probs = bench.ordered_problems(op.order, op.sizes)
+    want = []
+    for p in range(P):
+        for q in range(wl.k_max):
+            lo, hi = orc.replica_range(op.sizes[p], q, wl.n_dev)
+            if hi > lo:
+                want.append((p, q, list(op.order[p, lo:hi])))
+    assert [(p, q, list(c)) for p, q, c in probs] == want
+    sol = oracle.eval_population_ordered(wl, op.order, op.sizes, op.roles)
+    win, winR, cap = bench.window_tables(wl)
+    tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
+    cells, c64, c32 = bench.generation_work(wl, probs, op.roles, sol["T"], sol["master"], tabs)
+    assert (c64, c32) == _direct(wl, probs, op.roles, sol["T"], sol["master"])
+    assert c64 + c32 > 0 and cells > 0
 
 
 def test_window_tables_match_brute_force():

@@ -141,6 +141,21 @@ def test_uniform_layers_many_ties(torch_dev):
     _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag="ties")
 
 
+@pytest.mark.parametrize("M,N,P,head", [(40, 200, 3, True), (64, 255, 2, True),
+                                         (30, 126, 4, False), (48, 100, 2, True)])
+def test_long_bands_keep_split_points_in_global_memory(torch_dev, M, N, P, head):
+    """One chain of up to 64 roomy devices: its forward bands total up to
+    (m - 1)(N - m + 1) cells, beyond the LDS copy of the split points, and
+    the banded path keeps them in the wave's global table."""
+    import bench
+    wl = workload.random_small(70 + M + N, M=M, N=N, P=P, k_max=1, mem_lo_layers=40,
+                               mem_hi_layers=150, head=head)
+    _, _, cap = bench.window_tables(wl)
+    assert (M - 1) * (N - M + 1) > bench.LDS_TB_CELLS and cap[0].min() >= 1
+    print(f"long bands M={M} N={N}", flush=True)
+    _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag=f"long bands M{M} N{N}")
+
+
 def test_large_chain_uses_global_split_table(torch_dev):
     """m * N above the LDS copy of the split-point table (70 x 100)."""
     wl = workload.random_small(8, M=70, N=100, P=2, k_max=1, mem_lo_layers=3,
