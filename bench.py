@@ -305,8 +305,11 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5_256dev_126L_ga", choices=workload.NAMES)
+    ap.add_argument("--genomes", default="both", choices=("both", "labels", "two_chromosome"),
+                    help="which genome kind(s) to time; the first is the headline")
     ap.add_argument("--ordered-steps", type=int, default=5,
-                    help="timed generations of the two-chromosome GA (0 disables)")
+                    help="timed generations of the two-chromosome GA after the headline "
+                         "(with --genomes both; 0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU-oracle sample (0 disables)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -336,67 +339,46 @@ def main():
     win, winR, cap = window_tables(wl)
     wcr = (win, winR, cap) + count_tables(win, winR, wl.n_layer) + value_bounds(wl, win)
 
-    # --- labelled genomes (the headline): cluster labels per device
-    L0 = torch.from_numpy(wl.labels).to(dev)
-    R0 = torch.from_numpy(wl.roles).to(dev)
-    bufs = [(torch.empty_like(L0), torch.empty_like(R0)) for _ in range(2)]
     fit = {k: torch.empty(P, dtype=torch.int64, device=dev) for k in ("w", "phase")}
-
-    def step(g, cur):
-        L, R = bufs[cur]
-        e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=fit)
-        e2.e2_ga_step(ctx, L, R, fit["w"], fit["phase"], wl.ga_params(g), out=bufs[1 - cur])
-
-    def count(g, pop):
-        L, R = pop
-        sol = e2.e2_solve_partitions(ctx, L, R)
-        f2 = e2.e2_eval_population(ctx, L, R, fp, with_rates=False)
-        nxt = e2.e2_ga_step(ctx, L, R, f2["w"], f2["phase"], wl.ga_params(g))
-        torch.cuda.synchronize()
-        labels = L.cpu().numpy()
-        work = generation_work(wl, label_problems(labels, K), R.cpu().numpy(),
-                               e2.u64(sol["T"]), sol["master"].cpu().numpy(), wcr)
-        return work, nxt
-
     log(f"workload {wl.name}: P={P} M={M} N={wl.n_layer} k_max={K}; warmup {args.warmup}")
-    t = measure(torch, ctx, stream, bufs, (L0, R0), step, count, args.warmup, args.steps)
-    result = {
-        "metric": METRIC,
-        "value": t["cells"] / t["elapsed"],
-        "unit": "DP cells/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": t["elapsed"] * 1e3 / args.steps,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "u64",
-        "data": "synthetic",
-        "config": {"workload": wl.name, "devices": M, "layers": wl.n_layer,
-                   "population": P, "clusters_per_genome": "32-48" if K == 48 else str(K),
-                   "step": "one GA generation: e2_eval_population + e2_ga_step"},
-        "fitness_evals_per_s": P * args.steps / t["elapsed"],
-        "dp_cells_per_step": t["cells"] / args.steps,
-        "j_candidates_per_step": (t["cand"] + t["cand32"]) / args.steps,
-        "j_candidates_u32_or_f64_keys_per_step": t["cand32"] / args.steps,
-        "roofline": roofline(t, args.steps, profiled_traffic(wl.name)),
-    }
 
-    # --- two-chromosome genomes (ordering + replica sizes, App. A) on the
-    # same problem instance and population size
-    if args.ordered_steps > 0:
+    def labelled(n):
+        """Genomes as cluster labels per device (the 16384-genome workload's GA)."""
+        L0 = torch.from_numpy(wl.labels).to(dev)
+        R0 = torch.from_numpy(wl.roles).to(dev)
+        bufs = [(torch.empty_like(L0), torch.empty_like(R0)) for _ in range(2)]
+
+        def step(g, cur):
+            L, R = bufs[cur]
+            e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=fit)
+            e2.e2_ga_step(ctx, L, R, fit["w"], fit["phase"], wl.ga_params(g), out=bufs[1 - cur])
+
+        def count(g, pop):
+            L, R = pop
+            sol = e2.e2_solve_partitions(ctx, L, R)
+            f2 = e2.e2_eval_population(ctx, L, R, fp, with_rates=False)
+            nxt = e2.e2_ga_step(ctx, L, R, f2["w"], f2["phase"], wl.ga_params(g))
+            torch.cuda.synchronize()
+            work = generation_work(wl, label_problems(L.cpu().numpy(), K), R.cpu().numpy(),
+                                   e2.u64(sol["T"]), sol["master"].cpu().numpy(), wcr)
+            return work, nxt
+
+        return measure(torch, ctx, stream, bufs, (L0, R0), step, count, args.warmup, n)
+
+    def two_chromosome(n):
+        """Genomes as an ordering of the devices cut into replicas (App. A)."""
         op = workload.ordered_population(wl)
-        O0, S0, Q0 = (torch.from_numpy(a).to(dev) for a in (op.order, op.sizes, op.roles))
-        obufs = [tuple(torch.empty_like(x) for x in (O0, S0, Q0)) for _ in range(2)]
+        log(f"two-chromosome genomes: P={P}, max replica {op.max_replica}")
+        O0, S0, Q0 = (torch.from_numpy(x).to(dev) for x in (op.order, op.sizes, op.roles))
+        bufs = [tuple(torch.empty_like(x) for x in (O0, S0, Q0)) for _ in range(2)]
 
-        def ostep(g, cur):
-            O, S, Q = obufs[cur]
+        def step(g, cur):
+            O, S, Q = bufs[cur]
             e2.e2_eval_population_ordered(ctx, O, S, Q, fp, with_rates=False, out=fit)
             e2.e2_ga_step_ordered(ctx, O, S, Q, fit["w"], fit["phase"], op.ga_params(wl, g),
-                                  out=obufs[1 - cur])
+                                  out=bufs[1 - cur])
 
-        def ocount(g, pop):
+        def count(g, pop):
             O, S, Q = pop
             sol = e2.e2_solve_partitions_ordered(ctx, O, S, Q)
             f2 = e2.e2_eval_population_ordered(ctx, O, S, Q, fp, with_rates=False)
@@ -407,20 +389,49 @@ def main():
                                    sol["master"].cpu().numpy(), wcr)
             return work, nxt
 
-        log(f"two-chromosome genomes: P={P}, max replica {op.max_replica}")
-        n = args.ordered_steps
-        t2 = measure(torch, ctx, stream, obufs, (O0, S0, Q0), ostep, ocount, args.warmup, n)
-        result["two_chromosome"] = {
-            "step": "one GA generation: e2_eval_population_ordered + e2_ga_step_ordered",
-            "steps": n,
-            "ms_per_step": t2["elapsed"] * 1e3 / n,
-            "dp_cells_per_s": t2["cells"] / t2["elapsed"],
-            "fitness_evals_per_s": P * n / t2["elapsed"],
-            "dp_cells_per_step": t2["cells"] / n,
-            "j_candidates_per_step": (t2["cand"] + t2["cand32"]) / n,
-            "roofline": roofline(t2, n, None),
+        return measure(torch, ctx, stream, bufs, (O0, S0, Q0), step, count, args.warmup, n)
+
+    def summary(t, n, genomes):
+        return {
+            "ms_per_step": t["elapsed"] * 1e3 / n,
+            "fitness_evals_per_s": P * n / t["elapsed"],
+            "dp_cells_per_step": t["cells"] / n,
+            "j_candidates_per_step": (t["cand"] + t["cand32"]) / n,
+            "j_candidates_u32_or_f64_keys_per_step": t["cand32"] / n,
+            "roofline": roofline(t, n, profiled_traffic(wl.name, genomes)),
         }
-    if args.cpu_seconds > 0:
+
+    steps = {"labels": "one GA generation: e2_eval_population + e2_ga_step",
+             "two_chromosome": "one GA generation: e2_eval_population_ordered + "
+                               "e2_ga_step_ordered"}
+    head = "two_chromosome" if args.genomes == "two_chromosome" else "labels"
+    t = (two_chromosome if head == "two_chromosome" else labelled)(args.steps)
+    result = {
+        "metric": METRIC,
+        "value": t["cells"] / t["elapsed"],
+        "unit": "DP cells/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "devices": M, "layers": wl.n_layer,
+                   "population": P, "clusters_per_genome": "32-48" if K == 48 else str(K),
+                   "genomes": head, "step": steps[head]},
+    }
+    result.update(summary(t, args.steps, head))
+    # the paper's two-chromosome genomes on the same problem instance and
+    # population size
+    if args.genomes == "both" and args.ordered_steps > 0:
+        n = args.ordered_steps
+        t2 = two_chromosome(n)
+        result["two_chromosome"] = dict(step=steps["two_chromosome"], steps=n,
+                                        dp_cells_per_s=t2["cells"] / t2["elapsed"],
+                                        **summary(t2, n, "two_chromosome"))
+    if args.cpu_seconds > 0 and head == "labels":
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
@@ -500,15 +511,16 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def profiled_traffic(workload_name):
+def profiled_traffic(workload_name, genomes="labels"):
     """HBM bytes per DP launch from the committed rocprofv3 counter summary
-    of this workload, or None when none exists or the kernel sources have
-    changed since it was taken."""
+    of this workload and genome kind, or None when none exists or the kernel
+    sources have changed since it was taken."""
     import glob
     for f in sorted(glob.glob(os.path.join(ROOT, "profiles", "k_dp_*.json"))):
         with open(f) as fh:
             meta = json.load(fh)
-        if meta.get("workload") == workload_name and meta.get("sources_sha256_16") == source_hash():
+        if (meta.get("workload") == workload_name and meta.get("genomes", "labels") == genomes
+                and meta.get("sources_sha256_16") == source_hash()):
             return meta.get("k_dp_hbm_bytes_per_launch")
     return None
 
