@@ -74,6 +74,11 @@ def _load() -> ctypes.CDLL:
     lib.oracle_replica_range.argtypes = [i32, i32, P, i32, ctypes.POINTER(i32),
                                          ctypes.POINTER(i32)]
     lib.oracle_replica_range.restype = i32
+    lib.oracle_quantise_slots.argtypes = [i32, i32, P, P, P, P, P, P, i32, u32, P, P, P]
+    lib.oracle_quantise_slots.restype = i32
+    lib.oracle_search_roles.argtypes = [i32, i32, P, P, P, P, P, u64, u64, i32, i32, i32, P,
+                                        u64, u64, u64, P, P, P, P, P, P]
+    lib.oracle_search_roles.restype = i32
     lib.oracle_rng.argtypes = [u64, u64, u64, u64, u64]
     lib.oracle_rng.restype = u64
     lib.oracle_splitmix_out.argtypes = [u64]
@@ -306,3 +311,57 @@ def ga_step_ordered(order, sizes, roles, w, phase, seed, generation, tournament_
     if rc != 0:
         raise OracleError(f"oracle_ga_step_ordered failed: {rc}")
     return oo, so, ro
+
+
+def quantise_slots(problem, b_max, beta_ppm):
+    """Cost tables for role indices r = 0 (prefill) and r = b = 1..b_max
+    (decode with b requests in flight): (t [R][M][N], h [R][M], tau [R][M][M])."""
+    lib = _load()
+    M, N = int(problem["n_dev"]), int(problem["n_layer"])
+    R = int(b_max) + 1
+    speed = _u64(problem["speed_flops"])
+    bw = _u64(problem["bw_Bps"])
+    cong = np.ascontiguousarray(np.asarray(problem["congestion_ppm"], dtype=np.uint32))
+    lf = _u64(problem["layer_flops"]).reshape(2, N)
+    act = _u64(problem["act_bytes"])
+    hf = _u64(problem["head_flops"])
+    t = np.zeros((max(R, 2), M, N), dtype=np.uint64)
+    h = np.zeros((max(R, 2), M), dtype=np.uint64)
+    tau = np.zeros((max(R, 2), M, M), dtype=np.uint64)
+    rc = lib.oracle_quantise_slots(M, N, _p(speed), _p(bw), _p(cong), _p(lf), _p(act), _p(hf),
+                                   int(b_max), int(beta_ppm), _p(t), _p(h), _p(tau))
+    if rc != 0:
+        raise OracleError(f"oracle_quantise_slots failed: {rc}")
+    return t[:R], h[:R], tau[:R]
+
+
+def search_roles(wl, slot_model, labels=None):
+    """Algorithm 2's inner loop for a population of label genomes: the DP for
+    prefill and for every decode slot count, the highest feasible slot count
+    under the QoS floor, and the best role assignment by brute force.
+    slot_model: dict(b_max, beta_ppm, kv_bytes_per_block_slot).  Returns dict
+    T_all, Lambda_all [P][k_max][b_max + 1], roles, slots [P][k_max], w, phase [P]."""
+    lib = _load()
+    labels = np.ascontiguousarray(wl.labels if labels is None else labels, dtype=np.uint8)
+    P, M = labels.shape
+    K = int(wl.k_max)
+    b_max = int(slot_model["b_max"])
+    R = b_max + 1
+    t, h, tau = quantise_slots(wl.problem_arrays(), b_max, slot_model["beta_ppm"])
+    t, h, tau = (np.ascontiguousarray(x) for x in (t, h, tau))
+    T = np.zeros((P, K, R), dtype=np.uint64)
+    L = np.zeros((P, K, R), dtype=np.uint64)
+    roles = np.zeros((P, K), dtype=np.uint8)
+    slots = np.zeros((P, K), dtype=np.uint8)
+    w = np.zeros(P, dtype=np.uint64)
+    ph = np.zeros(P, dtype=np.uint64)
+    fp = wl.fitness_params()
+    rc = lib.oracle_search_roles(M, wl.n_layer, _p(t), _p(h), _p(tau), _p(_u64(wl.mem_bytes)),
+                                 _p(_u64(wl.layer_bytes)), int(wl.head_bytes),
+                                 int(slot_model["kv_bytes_per_block_slot"]), b_max, P, K,
+                                 _p(labels), int(fp["t_arrival_ns"]), int(fp["nd_tokens"]),
+                                 int(fp["min_tps_milli"]), _p(T), _p(L), _p(roles), _p(slots),
+                                 _p(w), _p(ph))
+    if rc != 0:
+        raise OracleError(f"oracle_search_roles failed: {rc}")
+    return dict(T_all=T, Lambda_all=L, roles=roles, slots=slots, w=w, phase=ph)

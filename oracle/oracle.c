@@ -315,6 +315,26 @@ int oracle_solve(int M, int N, const uint64_t *t, const uint64_t *h, const uint6
  * An individual with no usable prefill or no usable decode cluster gets
  * w = phase = INF.
  */
+/* Eq. 3-5 from the summed fixed-point rates of the prefill and decode
+ * replicas (0 = none usable) */
+static void rates_fitness(uint64_t sum_p, uint64_t sum_d, uint64_t t_arrival, uint64_t nd,
+                          uint64_t *w, uint64_t *phase, uint64_t *s_p, uint64_t *s_d)
+{
+    uint64_t SP = sum_p ? (SCALE + sum_p - 1) / sum_p : INF;
+    uint64_t SD = sum_d ? nd * ((SCALE + sum_d - 1) / sum_d) : INF;
+    *s_p = SP;
+    *s_d = SD;
+    if (SP == INF || SD == INF) {
+        *w = INF;
+        *phase = INF;
+        return;
+    }
+    uint64_t ph = max2(SP, SD);
+    uint64_t excess = ph > t_arrival ? ph - t_arrival : 0;
+    *phase = ph;
+    *w = excess > 0 ? SP + excess : 0;
+}
+
 static void fitness_one(int k_max, const uint64_t *T, const uint64_t *Lambda,
                         const uint8_t *roles, uint64_t t_arrival, uint64_t nd,
                         uint64_t min_tps_milli, uint64_t *w, uint64_t *phase,
@@ -330,19 +350,7 @@ static void fitness_one(int k_max, const uint64_t *T, const uint64_t *Lambda,
         if (decode) sum_d += rho;
         else sum_p += rho;
     }
-    uint64_t SP = sum_p ? (SCALE + sum_p - 1) / sum_p : INF;
-    uint64_t SD = sum_d ? nd * ((SCALE + sum_d - 1) / sum_d) : INF;
-    *s_p = SP;
-    *s_d = SD;
-    if (SP == INF || SD == INF) {
-        *w = INF;
-        *phase = INF;
-        return;
-    }
-    uint64_t ph = max2(SP, SD);
-    uint64_t excess = ph > t_arrival ? ph - t_arrival : 0;
-    *phase = ph;
-    *w = excess > 0 ? SP + excess : 0;
+    rates_fitness(sum_p, sum_d, t_arrival, nd, w, phase, s_p, s_d);
 }
 
 int oracle_fitness(int P, int k_max, const uint64_t *T, const uint64_t *Lambda,
@@ -728,5 +736,185 @@ int oracle_ga_step_ordered(int M, int P, int k_max, const uint8_t *order_in,
             }
         }
     }
+    return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Decode slots and role search (Algorithm 2's inner loop, Sec. 3.4).      */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * Cost tables for role indices r = 0..b_max: r = 0 is prefill, r = b is a
+ * decode replica holding b requests in flight (b KV-cache slots).  The
+ * paper profiles the decode block time per b without giving a model; this
+ * build's synthetic one (parity unpinned by the paper):
+ *   t[0], h[0], tau[0]   prefill tables, as oracle_quantise
+ *   t[1], h[1], tau[1]   decode with one request, as oracle_quantise
+ *   t[b][d][n] = t[1][d][n] + (b-1) * ceil(t[1][d][n] * beta_ppm / 1e6)
+ *   h[b][d]    = h[1][d]    + (b-1) * ceil(h[1][d] * beta_ppm / 1e6)
+ *   tau[b][d][e] = ceil(b * act[1] * 1e9 / Beff[d][e]) (INF if Beff = 0)
+ * i.e. each further request costs beta of a lone request's block and head
+ * time (decode is memory-bound), and a link carries b activations.
+ */
+int oracle_quantise_slots(int M, int N, const uint64_t *speed, const uint64_t *bw,
+                          const uint32_t *cong, const uint64_t *layer_flops,
+                          const uint64_t *act, const uint64_t *head_flops, int b_max,
+                          uint32_t beta_ppm, uint64_t *t /*[R][M][N]*/, uint64_t *h /*[R][M]*/,
+                          uint64_t *tau /*[R][M][M]*/)
+{
+    if (b_max < 1 || b_max > 15 || beta_ppm > 1000000u) return ORC_EINVAL;
+    int rc = oracle_quantise(M, N, speed, bw, cong, layer_flops, act, head_flops, t, h, tau);
+    if (rc) return rc;
+    for (int b = 2; b <= b_max; b++) {
+        for (int d = 0; d < M; d++) {
+            for (int n = 0; n < N; n++) {
+                uint64_t one = t[((size_t)1 * M + d) * N + n];
+                uint64_t extra = (uint64_t)(((u128)one * beta_ppm + 999999u) / 1000000u);
+                uint64_t v = one + (uint64_t)(b - 1) * extra;
+                if (v >= LIMIT48) return ORC_EOVERFLOW;
+                t[((size_t)b * M + d) * N + n] = v;
+            }
+            uint64_t one = h[M + d];
+            uint64_t extra = (uint64_t)(((u128)one * beta_ppm + 999999u) / 1000000u);
+            uint64_t hv = one + (uint64_t)(b - 1) * extra;
+            if (hv >= LIMIT48) return ORC_EOVERFLOW;
+            h[(size_t)b * M + d] = hv;
+        }
+        for (int d = 0; d < M; d++) {
+            for (int e = 0; e < M; e++) {
+                uint64_t v;
+                if (d == e) {
+                    v = 0;
+                } else {
+                    uint64_t beff = (uint64_t)(((u128)bw[d * M + e] * cong[d * M + e]) / 1000000u);
+                    if (beff == 0) {
+                        v = INF;
+                    } else {
+                        u128 num = (u128)act[1] * (uint64_t)b * 1000000000u;
+                        u128 qv = (num + beff - 1) / beff;
+                        if (qv >= LIMIT48) return ORC_EOVERFLOW;
+                        v = (uint64_t)qv;
+                    }
+                }
+                tau[((size_t)b * M + d) * M + e] = v;
+            }
+        }
+    }
+    return ORC_OK;
+}
+
+/*
+ * The paper's inner loop for one population of label genomes (Algorithm 2;
+ * Sec. 3.4, role assignment paragraph).  For every non-empty cluster q of
+ * genome p (chain in ascending id):
+ *   - DP_Pipe with the prefill tables (r = 0) and with the decode tables of
+ *     each b = 1..b_max (r = b), block bytes W[n] + kv * slots(r), slots(0)
+ *     = 1 (the request being prefilled), slots(b) = b;
+ *     T_all, L_all [P][k_max][b_max + 1] receive T and Lambda (INF if empty
+ *     or infeasible);
+ *   - prefill rate rho_P = floor(SCALE / max(T_0, 1)), 0 if infeasible;
+ *   - b* = the highest b whose DP is feasible and passes the QoS floor
+ *     Lambda_b <= floor(1e12 / min_tps_milli) (no floor if 0); decode rate
+ *     rho_D = floor(b* SCALE / max(T_b*, 1)), 0 if no b qualifies (b
+ *     requests share the pipeline, which emits b tokens per T).
+ * Then every assignment of a role to each non-empty cluster is scored by
+ * Eq. 3-5 on the summed rates (rates_fitness), and the smallest (w, phase)
+ * wins; ties go to the assignment whose decode set, as a bitmask over q, is
+ * smallest.  roles_out[p][q] = 1 for decode, 0 for prefill and for empty
+ * clusters; slots_out[p][q] = b* of a decode cluster (0 if none qualified),
+ * 0 otherwise.  At most 16 clusters per genome (2^16 assignments).
+ */
+int oracle_search_roles(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
+                        const uint64_t *mem, const uint64_t *W, uint64_t HB, uint64_t kv,
+                        int b_max, int P, int k_max, const uint8_t *labels, uint64_t t_arrival,
+                        uint64_t nd, uint64_t min_tps_milli, uint64_t *T_all, uint64_t *L_all,
+                        uint8_t *roles_out, uint8_t *slots_out, uint64_t *w, uint64_t *phase)
+{
+    if (M < 1 || M > 256 || N < 1 || N > 255 || P < 0 || k_max < 1 || k_max > 16 ||
+        b_max < 1 || b_max > 15 || nd > 8192)
+        return ORC_EINVAL;
+    const int R = b_max + 1;
+    int chain[256], sizes[256];
+    uint64_t hk[256], tl[256], mk[256];
+    uint64_t *tk = malloc(sizeof(uint64_t) * (size_t)M * N);
+    uint64_t *Wr = malloc(sizeof(uint64_t) * (size_t)N);
+    if (!tk || !Wr) { free(tk); free(Wr); return ORC_ENOMEM; }
+    const uint64_t lam_max = min_tps_milli ? 1000000000000ull / min_tps_milli : INF;
+    for (int p = 0; p < P; p++) {
+        uint64_t rho_p[16], rho_d[16];
+        int bstar[16], used[16], n_used = 0;
+        for (int q = 0; q < k_max; q++) {
+            int m = 0;
+            for (int d = 0; d < M; d++)
+                if (labels[(size_t)p * M + d] == q) chain[m++] = d;
+            uint64_t *To = T_all + ((size_t)p * k_max + q) * R;
+            uint64_t *Lo = L_all + ((size_t)p * k_max + q) * R;
+            for (int r = 0; r < R; r++) To[r] = Lo[r] = INF;
+            rho_p[q] = rho_d[q] = 0;
+            bstar[q] = 0;
+            if (m == 0) continue;
+            used[n_used++] = q;
+            for (int r = 0; r < R; r++) {
+                uint64_t slots = r == 0 ? 1 : (uint64_t)r;
+                for (int n = 0; n < N; n++) Wr[n] = W[n] + kv * slots;
+                for (int k = 0; k < m; k++) {
+                    memcpy(tk + (size_t)k * N, t + ((size_t)r * M + chain[k]) * N,
+                           sizeof(uint64_t) * N);
+                    hk[k] = h[(size_t)r * M + chain[k]];
+                    mk[k] = mem[chain[k]];
+                    tl[k] = (k == 0) ? 0 : tau[((size_t)r * M + chain[k - 1]) * M + chain[k]];
+                }
+                uint64_t Tv, Lv, ev;
+                int mu;
+                int rc = oracle_dp_pipe(m, N, tk, hk, tl, mk, Wr, HB, &Tv, &Lv, &mu, sizes, &ev);
+                if (rc) { free(tk); free(Wr); return rc; }
+                To[r] = Tv;
+                Lo[r] = Tv == INF ? INF : Lv;
+            }
+            if (To[0] != INF) rho_p[q] = SCALE / (To[0] > 0 ? To[0] : 1);
+            for (int b = b_max; b >= 1; b--) {
+                if (To[b] != INF && Lo[b] <= lam_max) {
+                    bstar[q] = b;
+                    rho_d[q] = ((uint64_t)b * SCALE) / (To[b] > 0 ? To[b] : 1);
+                    break;
+                }
+            }
+        }
+        /* every role assignment of the used clusters, in increasing order of
+         * the decode set's bitmask over q */
+        uint64_t best_w = INF, best_ph = INF;
+        unsigned best_mask = 0;
+        int have = 0;
+        for (unsigned x = 0; x < (1u << n_used); x++) {
+            unsigned mask = 0;
+            uint64_t sum_p = 0, sum_d = 0;
+            for (int i = 0; i < n_used; i++) {
+                int q = used[i];
+                if ((x >> i) & 1u) {
+                    mask |= 1u << q;
+                    sum_d += rho_d[q];
+                } else {
+                    sum_p += rho_p[q];
+                }
+            }
+            uint64_t wv, pv, sp, sd;
+            rates_fitness(sum_p, sum_d, t_arrival, nd, &wv, &pv, &sp, &sd);
+            if (!have || wv < best_w || (wv == best_w && pv < best_ph)) {
+                best_w = wv;
+                best_ph = pv;
+                best_mask = mask;
+                have = 1;
+            }
+        }
+        for (int q = 0; q < k_max; q++) {
+            int dec = (best_mask >> q) & 1u;
+            roles_out[(size_t)p * k_max + q] = (uint8_t)dec;
+            slots_out[(size_t)p * k_max + q] = (uint8_t)(dec ? bstar[q] : 0);
+        }
+        w[p] = best_w;
+        phase[p] = best_ph;
+    }
+    free(tk);
+    free(Wr);
     return ORC_OK;
 }

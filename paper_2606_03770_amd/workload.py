@@ -298,3 +298,20 @@ def ordered_population(wl: Workload, seed: Optional[int] = None,
             left -= s
     roles = ((rng.uniform(size=(P, K)) >= p_prefill) & (sizes > 0)).astype(np.uint8)
     return OrderedPopulation(order=order, sizes=sizes, roles=roles, max_replica=max_replica)
+
+
+def slot_model(wl: Workload, b_max: int = 8, beta_ppm: int = 125_000) -> dict:
+    """Decode-slot model of a workload for the role and slot search.
+
+    A request in flight holds the K and V of its NP + ND tokens for each
+    block it passes: 2 * (hidden * 2 bytes) * (NP + ND) bytes per block,
+    with hidden * 2 = the decode activation bytes and NP their ratio to the
+    prefill activation.  Each further request adds beta_ppm / 1e6 of a lone
+    request's decode block and head time.  b_max = 8 follows the paper's
+    example of a device whose memory holds four or, with a second pipeline
+    stage, eight concurrent requests.
+    """
+    act = [int(x) for x in wl.act_bytes]
+    np_tokens = act[0] // max(act[1], 1)
+    kv = 2 * act[1] * (np_tokens + int(wl.nd_tokens))
+    return dict(b_max=int(b_max), beta_ppm=int(beta_ppm), kv_bytes_per_block_slot=kv)
