@@ -48,6 +48,8 @@ extern "C" {
 #define E2_MAX_DEV 256    /* M: devices in the pool                          */
 #define E2_MAX_LAYER 255  /* N: transformer blocks of the model              */
 #define E2_MAX_CLUSTERS 255 /* k_max: cluster ids per genome                 */
+#define E2_MAX_SLOTS 15     /* b_max: decode slot counts of a slot model      */
+#define E2_MAX_SEARCH_CLUSTERS 16 /* k_max of e2_search_roles (2^16 role sets) */
 
 /*
  * Problem instance: the inputs of Algorithm 1 and Algorithm 2 (Sec. 3.2,
@@ -131,6 +133,36 @@ typedef struct e2_ctx e2_ctx;
  * On success *out owns device memory until e2_ctx_destroy.
  */
 int e2_ctx_create(const e2_problem *prob, e2_ctx **out);
+
+/*
+ * Decode-slot model (Algorithm 2's b loop; Sec. 3.4).  A decode replica may
+ * hold b = 1..b_max requests in flight, one KV-cache slot each.  The paper
+ * profiles the decode block time for each b; this library models it:
+ *   beta_ppm                 each further request adds ceil(beta * lone
+ *                            time) to a block's and to the head's decode
+ *                            time (beta = beta_ppm / 1e6, in [0, 1])
+ *   kv_bytes_per_block_slot  KV-cache bytes one request keeps per block
+ * and a link carries b activations: tau_b = ceil(b * act_bytes[1] * 1e9 /
+ * Beff).  A stage's bytes become its blocks' weight bytes plus slots * kv
+ * per block (+ head bytes on the master), slots = 1 for prefill (the
+ * request being prefilled) and b for decode.
+ */
+typedef struct e2_slot_model {
+    int32_t b_max;                    /* 1..E2_MAX_SLOTS */
+    uint32_t beta_ppm;                /* 0..1000000 */
+    uint64_t kv_bytes_per_block_slot; /* KV bytes per block per request */
+} e2_slot_model;
+
+/*
+ * e2_ctx_create with a slot model: tables for role index 0 (prefill) and
+ * b = 1..b_max (decode with b requests), each with its own memory windows
+ * when kv_bytes_per_block_slot > 0.  e2_solve_partitions /
+ * e2_eval_population on such a context use role index 0 or 1 (roles[] = 0
+ * or nonzero), i.e. they count one request's KV bytes.  Errors as
+ * e2_ctx_create, plus E2_EINVAL for a NULL or out-of-range model and
+ * E2_EOVERFLOW when a block's bytes with b_max slots reach 2^48.
+ */
+int e2_ctx_create_slots(const e2_problem *prob, const e2_slot_model *sm, e2_ctx **out);
 
 /* Free a context (E2_EINVAL for NULL).  Work using it must have completed. */
 int e2_ctx_destroy(e2_ctx *ctx);
@@ -298,6 +330,37 @@ int e2_ga_step_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
                        const uint8_t *order_in, const uint16_t *sizes_in, const uint8_t *roles_in,
                        const uint64_t *w_in, const uint64_t *phase_in, const e2_ga2_params *gp,
                        uint8_t *order_out, uint16_t *sizes_out, uint8_t *roles_out);
+
+/*
+ * Role and slot search for label genomes (Algorithm 2's inner loop and its
+ * brute-force role assignment, Sec. 3.4).  For every non-empty cluster of
+ * every genome (chain in ascending device id): Algorithm 1 with the prefill
+ * tables and with the decode tables of each b = 1..b_max of the context
+ * (b_max = 1 for a context without a slot model); then
+ *   rho_P = floor(2^50 / max(T_prefill, 1)), 0 if infeasible;
+ *   b*    = the largest b whose DP is feasible and whose Lambda passes the
+ *           QoS floor of fp (floor(1e12 / min_tps_milli) ns, none if 0);
+ *   rho_D = floor(b* 2^50 / max(T_b*, 1)), 0 if no b qualifies;
+ * and every prefill/decode assignment of the clusters is scored as
+ * e2_eval_population scores summed rates (Eq. 3-5); the smallest (w,
+ * phase) wins, ties going to the assignment whose decode set, as a bitmask
+ * over cluster ids, is smallest.
+ *   labels[P][M]     device: cluster id per device (ids >= k_max unassigned)
+ *   k_max            1..E2_MAX_SEARCH_CLUSTERS
+ *   roles_out[P][k_max]  device: 1 decode, 0 prefill or empty cluster
+ *   slots_out[P][k_max]  device: b* of a decode cluster (0 if none
+ *                    qualified), 0 otherwise
+ *   w, phase [P]     device: the winning fitness (INF if no assignment has
+ *                    both a usable prefill and a usable decode cluster)
+ *   T_all, Lambda_all [P][k_max][b_max+1]  device, optional (both or
+ *                    neither): every DP result, index 0 prefill, b decode
+ *                    with b requests; INF for empty or infeasible
+ * Asynchronous on `stream`.  E2_EINVAL for sizes out of range, nd_tokens >
+ * 8192 or a NULL required pointer.
+ */
+int e2_search_roles(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_t *labels,
+                    const e2_fitness_params *fp, uint8_t *roles_out, uint8_t *slots_out,
+                    uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all);
 
 /*
  * Profiling of the DP kernel (the dominant cost of e2_solve_partitions and

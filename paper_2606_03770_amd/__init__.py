@@ -12,6 +12,8 @@ tensors on ROCm) and streams.  The wrappers keep the C names:
     e2_solve_partitions_ordered(ctx, order, sizes, roles)          the same on
     e2_eval_population_ordered(ctx, order, sizes, roles, fitness)  two-chromosome
     e2_ga_step_ordered(ctx, order, sizes, roles, w, phase, ga)     genomes (App. A)
+    e2_ctx_create_slots(problem, slot_model) -> Context   with decode slot counts
+    e2_search_roles(ctx, labels, fitness)   role + slot search (Algorithm 2 inner loop)
 
 `problem` is a dict with the fields of e2_problem (numpy arrays), as
 returned by workload.Workload.problem_arrays().  64-bit unsigned outputs
@@ -37,8 +39,8 @@ INF = (1 << 64) - 1
 
 EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitions",
             "e2_eval_population", "e2_ga_step", "e2_solve_partitions_ordered",
-            "e2_eval_population_ordered", "e2_ga_step_ordered", "e2_ctx_dp_timing",
-            "e2_ctx_dp_elapsed", "e2_strerror")
+            "e2_eval_population_ordered", "e2_ga_step_ordered", "e2_ctx_create_slots",
+            "e2_search_roles", "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror")
 
 
 class E2Error(RuntimeError):
@@ -72,6 +74,11 @@ class e2_ga2_params(ctypes.Structure):
     _fields_ = [("seed", ctypes.c_uint64), ("generation", ctypes.c_uint32),
                 ("tournament_k", ctypes.c_uint32), ("mutation_thresh_u32", ctypes.c_uint32),
                 ("n_elite", ctypes.c_uint32), ("max_replica", ctypes.c_uint32)]
+
+
+class e2_slot_model(ctypes.Structure):
+    _fields_ = [("b_max", ctypes.c_int32), ("beta_ppm", ctypes.c_uint32),
+                ("kv_bytes_per_block_slot", ctypes.c_uint64)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -110,6 +117,12 @@ def lib() -> ctypes.CDLL:
     L.e2_ga_step_ordered.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, vp,
                                      ctypes.POINTER(e2_ga2_params), vp, vp, vp]
     L.e2_ga_step_ordered.restype = ctypes.c_int
+    L.e2_ctx_create_slots.argtypes = [ctypes.POINTER(e2_problem), ctypes.POINTER(e2_slot_model),
+                                      ctypes.POINTER(vp)]
+    L.e2_ctx_create_slots.restype = ctypes.c_int
+    L.e2_search_roles.argtypes = [vp, vp, i32, i32, vp, ctypes.POINTER(e2_fitness_params), vp, vp,
+                                  vp, vp, vp, vp]
+    L.e2_search_roles.restype = ctypes.c_int
     L.e2_ctx_dp_timing.argtypes = [vp, i32]
     L.e2_ctx_dp_timing.restype = ctypes.c_int
     L.e2_ctx_dp_elapsed.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
@@ -161,10 +174,11 @@ def e2_quantise(problem: dict):
 class Context:
     """Owns one e2_ctx (device tables of one problem instance)."""
 
-    def __init__(self, handle: int, n_dev: int, n_layer: int):
+    def __init__(self, handle: int, n_dev: int, n_layer: int, b_max: int = 1):
         self.handle = handle
         self.n_dev = n_dev
         self.n_layer = n_layer
+        self.b_max = b_max  # decode slot counts (1 without a slot model)
 
     def close(self):
         if self.handle:
@@ -183,6 +197,18 @@ def e2_ctx_create(problem: dict) -> Context:
     h = ctypes.c_void_p()
     _check(lib().e2_ctx_create(ctypes.byref(s), ctypes.byref(h)), "e2_ctx_create")
     return Context(h.value, s.n_dev, s.n_layer)
+
+
+def e2_ctx_create_slots(problem: dict, slot_model: dict) -> Context:
+    """A context with decode slot counts 1..b_max; slot_model has b_max,
+    beta_ppm and kv_bytes_per_block_slot."""
+    s, keep = _make_problem(problem)
+    sm = e2_slot_model(int(slot_model["b_max"]), int(slot_model["beta_ppm"]),
+                       int(slot_model["kv_bytes_per_block_slot"]))
+    h = ctypes.c_void_p()
+    _check(lib().e2_ctx_create_slots(ctypes.byref(s), ctypes.byref(sm), ctypes.byref(h)),
+           "e2_ctx_create_slots")
+    return Context(h.value, s.n_dev, s.n_layer, sm.b_max)
 
 
 def e2_ctx_destroy(ctx: Context):
@@ -360,6 +386,34 @@ def e2_ga_step_ordered(ctx: Context, order_in, sizes_in, roles_in, w, phase, ga:
                                     ctypes.byref(gp), _ptr(out[0]), _ptr(out[1]),
                                     _ptr(out[2])),
            "e2_ga_step_ordered")
+    return out
+
+
+def e2_search_roles(ctx: Context, labels, fitness: dict, k_max: int, stream=None,
+                    with_tables: bool = False, out: Optional[dict] = None):
+    """Role and slot search for label genomes.  Returns dict roles, slots
+    (uint8 [P][k_max]), w, phase (int64 bits of u64 [P]) and, with_tables,
+    T_all, Lambda_all (int64 bits of u64 [P][k_max][b_max + 1])."""
+    torch = _torch()
+    P = labels.shape[0]
+    _dev(labels, torch.uint8, (P, ctx.n_dev), "labels")
+    dev = labels.device
+    R = ctx.b_max + 1
+    if out is None:
+        out = dict(roles=torch.empty((P, k_max), dtype=torch.uint8, device=dev),
+                   slots=torch.empty((P, k_max), dtype=torch.uint8, device=dev),
+                   w=torch.empty(P, dtype=torch.int64, device=dev),
+                   phase=torch.empty(P, dtype=torch.int64, device=dev))
+        if with_tables:
+            out["T_all"] = torch.empty((P, k_max, R), dtype=torch.int64, device=dev)
+            out["Lambda_all"] = torch.empty((P, k_max, R), dtype=torch.int64, device=dev)
+    fp = e2_fitness_params(int(fitness["t_arrival_ns"]), int(fitness["nd_tokens"]),
+                           int(fitness["min_tps_milli"]))
+    _check(lib().e2_search_roles(ctx.handle, _stream(stream), P, int(k_max), _ptr(labels),
+                                 ctypes.byref(fp), _ptr(out["roles"]), _ptr(out["slots"]),
+                                 _ptr(out["w"]), _ptr(out["phase"]), _ptr(out.get("T_all")),
+                                 _ptr(out.get("Lambda_all"))),
+           "e2_search_roles")
     return out
 
 

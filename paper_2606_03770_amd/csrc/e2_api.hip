@@ -112,9 +112,10 @@ int alloc_scratch(Scratch &sc, hipStream_t s, size_t bytes)
 }
 
 // Lay out counters, the problem list and the split-point fallback.
-size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_bytes)
+size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_bytes,
+                  int n_r = 1)
 {
-    const size_t problems = (size_t)P * k_max;
+    const size_t problems = (size_t)P * k_max * n_r;
     *slots = e2_dp_slots(ctx->N, (int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX));
     const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
     // the global split-point table is needed only when some chain's split
@@ -126,13 +127,13 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
 }
 
 void carve_work(void *base, e2_ctx *ctx, int P, int k_max, int slots, size_t tb_bytes,
-                E2Work *wk)
+                E2Work *wk, int n_r = 1)
 {
     char *p = static_cast<char *>(base);
     wk->counters = reinterpret_cast<uint32_t *>(p);
     p += align256(32);
-    wk->list = reinterpret_cast<uint32_t *>(p);  // four chain-length segments of P * k_max
-    p += align256((size_t)P * k_max * 4 * 4);
+    wk->list = reinterpret_cast<uint32_t *>(p);  // four chain-length segments of P * k_max * n_r
+    p += align256((size_t)P * k_max * n_r * 4 * 4);
     wk->rows = reinterpret_cast<uint64_t *>(p);
     p += align256((size_t)slots * e2_dp_row_words(ctx->N) * 8);
     wk->tb_global = tb_bytes ? reinterpret_cast<uint8_t *>(p) : nullptr;
@@ -157,6 +158,233 @@ void free_dp_events(e2_ctx *ctx)
 int check_pop(int P, int k_max)
 {
     if (P < 0 || P >= (1 << 24) || k_max < 1 || k_max > E2_MAX_CLUSTERS) return E2_EINVAL;
+    return E2_OK;
+}
+
+// ceil(num / den) for den > 0; saturates to UINT64_MAX
+uint64_t ceil_div(u128 num, uint64_t den)
+{
+    const u128 q = num / den + (num % den != 0);
+    return (q >> 64) ? UINT64_MAX : (uint64_t)q;
+}
+
+// Decode tables for b = 2..b_max (role index b) from the one-request ones
+// (role index 1): each further request adds ceil(beta * lone time) to a
+// block and to the head, and a link carries b activations.
+int extend_slots(const e2_problem *pr, int b_max, uint32_t beta_ppm, uint64_t *t, uint64_t *h,
+                 uint64_t *tau)
+{
+    const int M = pr->n_dev, N = pr->n_layer;
+    for (int b = 2; b <= b_max; ++b) {
+        for (int d = 0; d < M; ++d) {
+            for (int n = 0; n < N; ++n) {
+                const uint64_t one = t[((size_t)M + d) * N + n];
+                const uint64_t v = one + (uint64_t)(b - 1) * ceil_div((u128)one * beta_ppm, 1000000u);
+                if (v >= kLimit48) return E2_EOVERFLOW;
+                t[((size_t)b * M + d) * N + n] = v;
+            }
+            const uint64_t one = h[(size_t)M + d];
+            const uint64_t hv = one + (uint64_t)(b - 1) * ceil_div((u128)one * beta_ppm, 1000000u);
+            if (hv >= kLimit48) return E2_EOVERFLOW;
+            h[(size_t)b * M + d] = hv;
+        }
+        for (int d = 0; d < M; ++d)
+            for (int e = 0; e < M; ++e) {
+                uint64_t v = 0;
+                if (d != e) {
+                    const size_t ix = (size_t)d * M + e;
+                    const uint64_t beff =
+                        (uint64_t)(((u128)pr->bw_Bps[ix] * pr->congestion_ppm[ix]) / 1000000u);
+                    if (beff == 0) {
+                        v = E2_INF64;
+                    } else {
+                        v = ceil_div((u128)pr->act_bytes[1] * (uint64_t)b * 1000000000u, beff);
+                        if (v >= kLimit48) return E2_EOVERFLOW;
+                    }
+                }
+                tau[((size_t)b * M + d) * M + e] = v;
+            }
+    }
+    return E2_OK;
+}
+
+// Build a context: R = b_max + 1 role indices of time tables and, with KV
+// bytes, one memory class per role index (block bytes W[n] + kv * slots,
+// slots = 1 for prefill and b for decode with b requests).
+int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv, e2_ctx **out)
+{
+    if (!out) return E2_EINVAL;
+    *out = nullptr;
+    int rc = check_problem(prob);
+    if (rc) return rc;
+    const int M = prob->n_dev, N = prob->n_layer;
+    const int R = b_max + 1;
+    const int C = kv ? R : 1;
+    std::vector<uint64_t> t((size_t)R * M * N), h((size_t)R * M), tau((size_t)R * M * M);
+    rc = quantise(prob, t.data(), h.data(), tau.data());
+    if (rc) return rc;
+    if ((rc = extend_slots(prob, b_max, beta_ppm, t.data(), h.data(), tau.data()))) return rc;
+
+    // prefix sums of block times per role and device
+    std::vector<uint64_t> pref((size_t)R * M * (N + 1));
+    for (int r = 0; r < R; ++r)
+        for (int d = 0; d < M; ++d) {
+            uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
+            row[0] = 0;
+            for (int n = 0; n < N; ++n) row[n + 1] = row[n] + t[((size_t)r * M + d) * N + n];
+        }
+    // per memory class: block-byte prefix sums, then windows (smallest start
+    // j such that bytes(j..i) (+ head) <= mem) forward and over reversed blocks
+    std::vector<uint8_t> win((size_t)C * 2 * M * N), cap0((size_t)C * M), capH((size_t)C * M);
+    std::vector<uint8_t> winR((size_t)C * M * N);
+    std::vector<uint64_t> wpref(N + 1, 0);
+    for (int c = 0; c < C; ++c) {
+        const uint64_t extra_kv = kv * (uint64_t)(c == 0 ? 1 : c);
+        for (int n = 0; n < N; ++n) {
+            const uint64_t wb = prob->layer_bytes[n] + extra_kv;
+            if (extra_kv >= kLimit48 || wb >= kLimit48) return E2_EOVERFLOW;
+            wpref[n + 1] = wpref[n] + wb;
+        }
+        for (int f = 0; f < 2; ++f)
+            for (int d = 0; d < M; ++d) {
+                const uint64_t extra = f ? prob->head_bytes : 0;
+                const uint64_t mem = prob->mem_bytes[d];
+                int j = 0, best = 0;
+                for (int i = 0; i < N; ++i) {
+                    // advance j until blocks j..i (+ extra) fit or j passes i
+                    while (j <= i && wpref[i + 1] - wpref[j] + extra > mem) ++j;
+                    uint8_t v = E2_NO_START;
+                    if (j <= i) {
+                        v = (uint8_t)j;
+                        if (i - j + 1 > best) best = i - j + 1;
+                    }
+                    win[(((size_t)c * 2 + f) * M + d) * N + i] = v;
+                }
+                (f ? capH : cap0)[(size_t)c * M + d] = (uint8_t)best;
+            }
+        for (int d = 0; d < M; ++d) {
+            const uint64_t mem = prob->mem_bytes[d];
+            // reversed blocks y..x are original blocks N-1-x..N-1-y
+            int y = 0;
+            for (int x = 0; x < N; ++x) {
+                while (y <= x && wpref[N - y] - wpref[N - 1 - x] > mem) ++y;
+                winR[((size_t)c * M + d) * N + x] = (y <= x) ? (uint8_t)y : E2_NO_START;
+            }
+        }
+    }
+    // reversed blocks (block N-1 first): prefix sums, used by the backward
+    // rows of the DP, which run as forward rows on them
+    std::vector<uint64_t> prefR((size_t)R * M * (N + 1));
+    for (int r = 0; r < R; ++r)
+        for (int d = 0; d < M; ++d) {
+            const uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
+            uint64_t *rev = &prefR[((size_t)r * M + d) * (N + 1)];
+            for (int x = 0; x <= N; ++x) rev[x] = row[N] - row[N - x];
+        }
+
+    // lower bounds of window lengths over cells i >= x (0 = no fitting cell)
+    std::vector<uint8_t> minwin((size_t)C * 2 * M * N), minwinR((size_t)C * M * N);
+    auto suffix_min = [N](const uint8_t *w, uint8_t *o) {
+        int best = 0;  // 0 encodes "none yet"
+        for (int x = N - 1; x >= 0; --x) {
+            if (w[x] != E2_NO_START) {
+                const int len = x - w[x] + 1;
+                best = (best == 0 || len < best) ? len : best;
+            }
+            o[x] = (uint8_t)best;
+        }
+    };
+    for (size_t row = 0; row < (size_t)C * 2 * M; ++row)
+        suffix_min(&win[row * N], &minwin[row * N]);
+    for (size_t row = 0; row < (size_t)C * M; ++row) suffix_min(&winR[row * N], &minwinR[row * N]);
+
+    // largest cost of a memory-fitting stage per role and device (with the
+    // head time for stages that carry the head bytes): every finite value a
+    // DP over a chain produces is at most the largest of these over its
+    // devices and its largest finite link time
+    std::vector<uint64_t> vmax((size_t)R * M, 0);
+    for (int r = 0; r < R; ++r) {
+        const int c = C > 1 ? r : 0;
+        for (int d = 0; d < M; ++d) {
+            const uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
+            uint64_t best = 0;
+            for (int f = 0; f < 2; ++f)
+                for (int i = 0; i < N; ++i) {
+                    const uint8_t j = win[(((size_t)c * 2 + f) * M + d) * N + i];
+                    if (j == E2_NO_START) continue;
+                    const uint64_t v = row[i + 1] - row[j] + (f ? h[(size_t)r * M + d] : 0);
+                    if (v > best) best = v;
+                }
+            vmax[(size_t)r * M + d] = best;
+        }
+    }
+    // largest prefix sum (+ head time) per role and device: every shifted
+    // prefix sum of a chain stays below 2^53 when these and its link times
+    // are below 2^45
+    std::vector<uint64_t> vtot((size_t)R * M, 0);
+    for (int r = 0; r < R; ++r)
+        for (int d = 0; d < M; ++d)
+            vtot[(size_t)r * M + d] =
+                pref[((size_t)r * M + d) * (N + 1) + N] + h[(size_t)r * M + d];
+
+    struct Part {
+        const void *src;
+        size_t bytes;
+        char *dst;
+    };
+    Part parts[] = {{pref.data(), pref.size() * 8, nullptr},   {h.data(), h.size() * 8, nullptr},
+                    {tau.data(), tau.size() * 8, nullptr},     {win.data(), win.size(), nullptr},
+                    {winR.data(), winR.size(), nullptr},       {prefR.data(), prefR.size() * 8, nullptr},
+                    {minwin.data(), minwin.size(), nullptr},   {minwinR.data(), minwinR.size(), nullptr},
+                    {cap0.data(), cap0.size(), nullptr},       {capH.data(), capH.size(), nullptr},
+                    {vmax.data(), vmax.size() * 8, nullptr},   {vtot.data(), vtot.size() * 8, nullptr}};
+    size_t total = 0;
+    for (const Part &pt : parts) total += align256(pt.bytes);
+    e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
+    if (!ctx) return E2_ENOMEM;
+    if (hipGetDevice(&ctx->device) != hipSuccess) {
+        free(ctx);
+        return E2_EHIP;
+    }
+    if (hipMalloc(&ctx->blob, total) != hipSuccess) {
+        (void)hipGetLastError();
+        free(ctx);
+        return E2_ENOMEM;
+    }
+    char *p = static_cast<char *>(ctx->blob);
+    hipError_t e = hipSuccess;
+    for (Part &pt : parts) {
+        pt.dst = p;
+        p += align256(pt.bytes);
+        if (e == hipSuccess) e = hipMemcpy(pt.dst, pt.src, pt.bytes, hipMemcpyHostToDevice);
+    }
+    if (e != hipSuccess) {
+        (void)hipFree(ctx->blob);
+        free(ctx);
+        return E2_EHIP;
+    }
+    ctx->M = M;
+    ctx->N = N;
+    ctx->b_max = b_max;
+    ctx->head_bytes = prob->head_bytes;
+    E2Tables &tb = ctx->tables;
+    tb.pref = reinterpret_cast<const uint64_t *>(parts[0].dst);
+    tb.head = reinterpret_cast<const uint64_t *>(parts[1].dst);
+    tb.tau = reinterpret_cast<const uint64_t *>(parts[2].dst);
+    tb.win = reinterpret_cast<const uint8_t *>(parts[3].dst);
+    tb.winR = reinterpret_cast<const uint8_t *>(parts[4].dst);
+    tb.prefR = reinterpret_cast<const uint64_t *>(parts[5].dst);
+    tb.minwin = reinterpret_cast<const uint8_t *>(parts[6].dst);
+    tb.minwinR = reinterpret_cast<const uint8_t *>(parts[7].dst);
+    tb.cap0 = reinterpret_cast<const uint8_t *>(parts[8].dst);
+    tb.capH = reinterpret_cast<const uint8_t *>(parts[9].dst);
+    tb.vmax = reinterpret_cast<const uint64_t *>(parts[10].dst);
+    tb.vtot = reinterpret_cast<const uint64_t *>(parts[11].dst);
+    tb.M = M;
+    tb.N = N;
+    tb.R = R;
+    tb.n_mem = C;
+    *out = ctx;
     return E2_OK;
 }
 
@@ -186,180 +414,16 @@ int e2_quantise(const e2_problem *prob, uint64_t *t, uint64_t *h, uint64_t *tau)
 
 int e2_ctx_create(const e2_problem *prob, e2_ctx **out)
 {
+    return build_ctx(prob, 1, 0, 0, out);
+}
+
+int e2_ctx_create_slots(const e2_problem *prob, const e2_slot_model *sm, e2_ctx **out)
+{
     if (!out) return E2_EINVAL;
     *out = nullptr;
-    int rc = check_problem(prob);
-    if (rc) return rc;
-    const int M = prob->n_dev, N = prob->n_layer;
-    std::vector<uint64_t> t((size_t)2 * M * N), h((size_t)2 * M), tau((size_t)2 * M * M);
-    rc = quantise(prob, t.data(), h.data(), tau.data());
-    if (rc) return rc;
-
-    // prefix sums of block times per role and device
-    std::vector<uint64_t> pref((size_t)2 * M * (N + 1));
-    for (int r = 0; r < 2; ++r)
-        for (int d = 0; d < M; ++d) {
-            uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
-            row[0] = 0;
-            for (int n = 0; n < N; ++n) row[n + 1] = row[n] + t[((size_t)r * M + d) * N + n];
-        }
-    // memory windows: smallest start j such that bytes(j..i) (+ head) <= mem
-    std::vector<uint64_t> wpref(N + 1, 0);
-    for (int n = 0; n < N; ++n) wpref[n + 1] = wpref[n] + prob->layer_bytes[n];
-    std::vector<uint8_t> win((size_t)2 * M * N), cap0(M), capH(M);
-    for (int f = 0; f < 2; ++f)
-        for (int d = 0; d < M; ++d) {
-            const uint64_t extra = f ? prob->head_bytes : 0;
-            const uint64_t mem = prob->mem_bytes[d];
-            int j = 0, best = 0;
-            for (int i = 0; i < N; ++i) {
-                // advance j until blocks j..i (+ extra) fit or j passes i
-                while (j <= i && wpref[i + 1] - wpref[j] + extra > mem) ++j;
-                uint8_t v = E2_NO_START;
-                if (j <= i) {
-                    v = (uint8_t)j;
-                    if (i - j + 1 > best) best = i - j + 1;
-                }
-                win[((size_t)f * M + d) * N + i] = v;
-            }
-            (f ? capH : cap0)[d] = (uint8_t)best;
-        }
-    // reversed blocks (block N-1 first): prefix sums and window starts, used
-    // by the backward rows of the DP, which run as forward rows on them
-    std::vector<uint64_t> prefR((size_t)2 * M * (N + 1));
-    for (int r = 0; r < 2; ++r)
-        for (int d = 0; d < M; ++d) {
-            const uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
-            uint64_t *rev = &prefR[((size_t)r * M + d) * (N + 1)];
-            for (int x = 0; x <= N; ++x) rev[x] = row[N] - row[N - x];
-        }
-    std::vector<uint8_t> winR((size_t)M * N);
-    for (int d = 0; d < M; ++d) {
-        const uint64_t mem = prob->mem_bytes[d];
-        // reversed blocks y..x are original blocks N-1-x..N-1-y
-        int y = 0;
-        for (int x = 0; x < N; ++x) {
-            while (y <= x && wpref[N - y] - wpref[N - 1 - x] > mem) ++y;
-            winR[(size_t)d * N + x] = (y <= x) ? (uint8_t)y : E2_NO_START;
-        }
-    }
-
-    // lower bounds of window lengths over cells i >= x (0 = no fitting cell)
-    std::vector<uint8_t> minwin((size_t)2 * M * N), minwinR((size_t)M * N);
-    auto suffix_min = [N](const uint8_t *w, uint8_t *out) {
-        int best = 0;  // 0 encodes "none yet"
-        for (int x = N - 1; x >= 0; --x) {
-            if (w[x] != E2_NO_START) {
-                const int len = x - w[x] + 1;
-                best = (best == 0 || len < best) ? len : best;
-            }
-            out[x] = (uint8_t)best;
-        }
-    };
-    for (int f = 0; f < 2; ++f)
-        for (int d = 0; d < M; ++d)
-            suffix_min(&win[((size_t)f * M + d) * N], &minwin[((size_t)f * M + d) * N]);
-    for (int d = 0; d < M; ++d) suffix_min(&winR[(size_t)d * N], &minwinR[(size_t)d * N]);
-
-    // largest cost of a memory-fitting stage per role and device (with the
-    // head time for stages that carry the head bytes): every finite value a
-    // DP over a chain produces is at most the largest of these over its
-    // devices and its largest finite link time
-    std::vector<uint64_t> vmax((size_t)2 * M, 0);
-    for (int r = 0; r < 2; ++r)
-        for (int d = 0; d < M; ++d) {
-            const uint64_t *row = &pref[((size_t)r * M + d) * (N + 1)];
-            uint64_t best = 0;
-            for (int f = 0; f < 2; ++f)
-                for (int i = 0; i < N; ++i) {
-                    const uint8_t j = win[((size_t)f * M + d) * N + i];
-                    if (j == E2_NO_START) continue;
-                    const uint64_t c = row[i + 1] - row[j] + (f ? h[(size_t)r * M + d] : 0);
-                    if (c > best) best = c;
-                }
-            vmax[(size_t)r * M + d] = best;
-        }
-    // largest prefix sum (+ head time) per role and device: every shifted
-    // prefix sum of a chain stays below 2^53 when these and its link times
-    // are below 2^45
-    std::vector<uint64_t> vtot((size_t)2 * M, 0);
-    for (int r = 0; r < 2; ++r)
-        for (int d = 0; d < M; ++d)
-            vtot[(size_t)r * M + d] =
-                pref[((size_t)r * M + d) * (N + 1) + N] + h[(size_t)r * M + d];
-
-    const size_t b_pref = align256(pref.size() * 8), b_head = align256(h.size() * 8),
-                 b_tau = align256(tau.size() * 8), b_win = align256(win.size()),
-                 b_winR = align256(winR.size()), b_cap = align256((size_t)M);
-    const size_t b_mw = align256(minwin.size()), b_mwR = align256(minwinR.size());
-    const size_t b_vmax = align256(vmax.size() * 8);
-    const size_t total =
-        2 * b_pref + b_head + b_tau + b_win + b_winR + b_mw + b_mwR + 2 * b_cap + 2 * b_vmax;
-    e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
-    if (!ctx) return E2_ENOMEM;
-    if (hipGetDevice(&ctx->device) != hipSuccess) {
-        free(ctx);
-        return E2_EHIP;
-    }
-    if (hipMalloc(&ctx->blob, total) != hipSuccess) {
-        (void)hipGetLastError();
-        free(ctx);
-        return E2_ENOMEM;
-    }
-    char *p = static_cast<char *>(ctx->blob);
-    char *d_pref = p;
-    char *d_head = d_pref + b_pref;
-    char *d_tau = d_head + b_head;
-    char *d_win = d_tau + b_tau;
-    char *d_winR = d_win + b_win;
-    char *d_prefR = d_winR + b_winR;
-    char *d_mw = d_prefR + b_pref;
-    char *d_mwR = d_mw + b_mw;
-    char *d_cap0 = d_mwR + b_mwR;
-    char *d_capH = d_cap0 + b_cap;
-    char *d_vmax = d_capH + b_cap;
-    char *d_vtot = d_vmax + b_vmax;
-    hipError_t e = hipSuccess;
-    if (e == hipSuccess) e = hipMemcpy(d_pref, pref.data(), pref.size() * 8, hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_head, h.data(), h.size() * 8, hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_tau, tau.data(), tau.size() * 8, hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_win, win.data(), win.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_winR, winR.data(), winR.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_mw, minwin.data(), minwin.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-        e = hipMemcpy(d_mwR, minwinR.data(), minwinR.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-        e = hipMemcpy(d_prefR, prefR.data(), prefR.size() * 8, hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_cap0, cap0.data(), (size_t)M, hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_capH, capH.data(), (size_t)M, hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-        e = hipMemcpy(d_vmax, vmax.data(), vmax.size() * 8, hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-        e = hipMemcpy(d_vtot, vtot.data(), vtot.size() * 8, hipMemcpyHostToDevice);
-    if (e != hipSuccess) {
-        (void)hipFree(ctx->blob);
-        free(ctx);
-        return E2_EHIP;
-    }
-    ctx->M = M;
-    ctx->N = N;
-    ctx->head_bytes = prob->head_bytes;
-    ctx->tables.pref = reinterpret_cast<const uint64_t *>(d_pref);
-    ctx->tables.head = reinterpret_cast<const uint64_t *>(d_head);
-    ctx->tables.tau = reinterpret_cast<const uint64_t *>(d_tau);
-    ctx->tables.win = reinterpret_cast<const uint8_t *>(d_win);
-    ctx->tables.winR = reinterpret_cast<const uint8_t *>(d_winR);
-    ctx->tables.minwin = reinterpret_cast<const uint8_t *>(d_mw);
-    ctx->tables.minwinR = reinterpret_cast<const uint8_t *>(d_mwR);
-    ctx->tables.prefR = reinterpret_cast<const uint64_t *>(d_prefR);
-    ctx->tables.cap0 = reinterpret_cast<const uint8_t *>(d_cap0);
-    ctx->tables.capH = reinterpret_cast<const uint8_t *>(d_capH);
-    ctx->tables.vmax = reinterpret_cast<const uint64_t *>(d_vmax);
-    ctx->tables.vtot = reinterpret_cast<const uint64_t *>(d_vtot);
-    ctx->tables.M = M;
-    ctx->tables.N = N;
-    *out = ctx;
-    return E2_OK;
+    if (!sm || sm->b_max < 1 || sm->b_max > E2_MAX_SLOTS || sm->beta_ppm > 1000000u)
+        return E2_EINVAL;
+    return build_ctx(prob, sm->b_max, sm->beta_ppm, sm->kv_bytes_per_block_slot, out);
 }
 
 int e2_ctx_destroy(e2_ctx *ctx)
@@ -554,6 +618,42 @@ int e2_ga_step_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
         s, ctx->M, P, k_max, order_in, sizes_in, roles_in, w_in, phase_in, gp->seed,
         gp->generation, gp->tournament_k, gp->mutation_thresh_u32, gp->n_elite, gp->max_replica,
         static_cast<uint32_t *>(sc.base), order_out, sizes_out, roles_out);
+    return e == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+int e2_search_roles(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_t *labels,
+                    const e2_fitness_params *fp, uint8_t *roles_out, uint8_t *slots_out,
+                    uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all)
+{
+    if (!ctx || !fp) return E2_EINVAL;
+    if (P < 0 || P >= (1 << 24) || k_max < 1 || k_max > E2_MAX_SEARCH_CLUSTERS) return E2_EINVAL;
+    if (fp->nd_tokens > 8192) return E2_EINVAL;
+    if ((T_all == nullptr) != (Lambda_all == nullptr)) return E2_EINVAL;
+    if (P == 0) return E2_OK;
+    if (!labels || !roles_out || !slots_out || !w || !phase) return E2_EINVAL;
+    int rc = check_device(ctx);
+    if (rc) return rc;
+    const int R = ctx->b_max + 1;
+    hipStream_t s = as_stream(stream);
+    int slots;
+    size_t tbb;
+    const size_t wb = work_bytes(ctx, P, k_max, &slots, &tbb, R);
+    const size_t tl = T_all ? 0 : align256((size_t)P * k_max * R * 8);
+    Scratch sc;
+    if ((rc = alloc_scratch(sc, s, wb + 2 * tl))) return rc;
+    E2Work wk;
+    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk, R);
+    uint64_t *Ts = T_all ? T_all : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
+    uint64_t *Ls = Lambda_all ? Lambda_all
+                              : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb + tl);
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, nullptr, wk, Ts, Ls,
+                                        nullptr, nullptr);
+    if (e != hipSuccess) return E2_EHIP;
+    const uint64_t lam_max =
+        fp->min_tps_milli ? 1000000000000ull / fp->min_tps_milli : E2_INF64;
+    e = e2_launch_roles(s, P, k_max, R, Ts, Ls, fp->t_arrival_ns, fp->nd_tokens, lam_max,
+                        roles_out, slots_out, w, phase);
     return e == hipSuccess ? E2_OK : E2_EHIP;
 }
 

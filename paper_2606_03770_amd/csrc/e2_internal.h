@@ -8,32 +8,39 @@
 #define E2_INF64 0xFFFFFFFFFFFFFFFFull
 #define E2_NO_START 0xFFu  // window table: no stage ending at i fits
 
-// Read-only device tables built once per context.
+// Read-only device tables built once per context.  Role index r: 0 =
+// prefill, b = 1..R-1 = decode with b requests in flight (R = 2 without a
+// slot model).  Memory tables exist per memory class: one shared class
+// (n_mem = 1, no KV bytes) or one per role index (n_mem = R, block bytes
+// W[n] + kv * slots(r)); the [C] below is that class.
 struct E2Tables {
-    const uint64_t *pref;  // [2][M][N+1] prefix sums of block times per role and device
-    const uint64_t *head;  // [2][M] head + output-layer time per role and device
-    const uint64_t *tau;   // [2][M][M] link time per role, INF for a dead link
-    const uint8_t *win;    // [2][M][N] smallest stage start j so that blocks j..i fit
+    const uint64_t *pref;  // [R][M][N+1] prefix sums of block times per role and device
+    const uint64_t *head;  // [R][M] head + output-layer time per role and device
+    const uint64_t *tau;   // [R][M][M] link time per role, INF for a dead link
+    const uint8_t *win;    // [C][2][M][N] smallest stage start j so that blocks j..i fit
                            //   ([0]: no head bytes, [1]: with head bytes), E2_NO_START if none
-    const uint64_t *prefR; // [2][M][N+1] prefix sums over reversed blocks: prefR[x] =
+    const uint64_t *prefR; // [R][M][N+1] prefix sums over reversed blocks: prefR[x] =
                            //   pref[N] - pref[N-x] (block N-1 first)
-    const uint8_t *winR;   // [M][N] reversed-block window starts without the head:
+    const uint8_t *winR;   // [C][M][N] reversed-block window starts without the head:
                            //   smallest y so that reversed blocks y..x fit, E2_NO_START if none
-    const uint8_t *minwin; // [2][M][N] lower bound of window lengths i - win(i) + 1 over
+    const uint8_t *minwin; // [C][2][M][N] lower bound of window lengths i - win(i) + 1 over
                            //   cells i >= x (0 if unknown); same for reversed blocks in
-    const uint8_t *minwinR;//   [M][N]
-    const uint8_t *cap0;   // [M] most blocks one stage can hold without the head
-    const uint8_t *capH;   // [M] most blocks one stage can hold with the head
-    const uint64_t *vmax;  // [2][M] largest cost of a fitting stage (+ head time when it
+    const uint8_t *minwinR;//   [C][M][N]
+    const uint8_t *cap0;   // [C][M] most blocks one stage can hold without the head
+    const uint8_t *capH;   // [C][M] most blocks one stage can hold with the head
+    const uint64_t *vmax;  // [R][M] largest cost of a fitting stage (+ head time when it
                            //   holds the head bytes) per role and device
-    const uint64_t *vtot;  // [2][M] total time of all blocks + head time per role and device
+    const uint64_t *vtot;  // [R][M] total time of all blocks + head time per role and device
     int M;
     int N;
+    int R;      // role indices
+    int n_mem;  // memory classes: 1 or R
 };
 
 struct e2_ctx {
     int device;
     int M, N;
+    int b_max;  // decode slot counts of the slot model (1 without one)
     uint64_t head_bytes;
     void *blob;  // one device allocation holding every table
     E2Tables tables;
@@ -46,7 +53,8 @@ struct e2_ctx {
 // Scratch layout of one solve/eval call (device memory, stream-ordered).
 struct E2Work {
     uint32_t *counters;  // [0..3] problems listed per chain-length class, [4] next job
-    uint32_t *list;      // [4][P * k_max] (p << 8) | q of problems needing the DP
+    uint32_t *list;      // [4][P * k_max * n_r] problems needing the DP: (p << 8) | q, or
+                         //   with every role index searched (p << 8) | (q << 4) | r
     uint64_t *rows;      // [n_slots][pool + 2 (N+1)] per-wave DP rows
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
     int n_slots;         // waves of the DP kernel
@@ -73,10 +81,18 @@ struct E2Genomes {
 };
 
 // Enqueue cluster extraction + DP.  Outputs may be the caller's (solve) or
-// scratch (eval; master/layers null).
+// scratch (eval; master/layers null).  With roles null, every cluster is
+// solved for every role index (k_max <= 16, R <= 16) and T, Lambda are
+// [P][k_max][R]; master and layers must then be null.
 hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_max,
                                 const E2Genomes &gen, const uint8_t *roles, const E2Work &wk,
                                 uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers);
+
+// Role and slot search per genome from T, Lambda [P][k_max][R].
+hipError_t e2_launch_roles(hipStream_t s, int P, int k_max, int R, const uint64_t *T_all,
+                           const uint64_t *L_all, uint64_t t_arrival, uint64_t nd,
+                           uint64_t lambda_max, uint8_t *roles_out, uint8_t *slots_out,
+                           uint64_t *w, uint64_t *phase);
 
 hipError_t e2_launch_fitness(hipStream_t s, int P, int k_max, const uint64_t *T,
                              const uint64_t *Lambda, const uint8_t *roles, uint64_t t_arrival,

@@ -115,8 +115,30 @@ __device__ __forceinline__ int replica_at(const uint32_t *offs, int k_max, int t
     return lo;
 }
 
+// Memory class of a role index: one shared class, or one per role index.
+__device__ __forceinline__ int mem_class(const E2Tables &tb, int r) { return tb.n_mem > 1 ? r : 0; }
+
+// The tables with the memory windows and capacities of role index r.
+__device__ __forceinline__ E2Tables mem_view(const E2Tables &tb, int r)
+{
+    E2Tables v = tb;
+    const size_t c = (size_t)mem_class(tb, r);
+    const size_t MN = (size_t)tb.M * tb.N;
+    v.win += c * 2 * MN;
+    v.minwin += c * 2 * MN;
+    v.winR += c * MN;
+    v.minwinR += c * MN;
+    v.cap0 += c * tb.M;
+    v.capH += c * tb.M;
+    return v;
+}
+
+// n_r = 0: one problem per cluster, at role index (roles[q] != 0); n_r = R:
+// one problem per cluster and role index (k_max <= 16), outputs
+// [P][k_max][R] and list codes (p << 8) | (q << 4) | r.
 __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_max,
-                                                      E2Genomes gen, uint32_t *counters,
+                                                      E2Genomes gen, const uint8_t *roles,
+                                                      int n_r, uint32_t *counters,
                                                       uint32_t *list, size_t seg_cap,
                                                       uint64_t *T, uint64_t *Lambda,
                                                       int16_t *master, uint8_t *layers)
@@ -151,23 +173,16 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             carry += __shfl(x, kWave - 1, kWave);
         }
     }
-    for (int q = lane; q < 256; q += 64) {
-        packed[g][q] = 0;
-        mincap[g][q] = 0xFFFFFFFFu;
-    }
-    if (lane < 8) {
-        hmask[g][lane] = 0;
-        lmask[g][lane] = 0;
-        bad[g][lane] = 0;
-    }
+    if (lane < 8) bad[g][lane] = 0;
     __syncthreads();
     // labels: slot u of a lane is device x, in cluster labs[u]; ordered
-    // genomes: ordering position x, holding device d, in replica labs[u]
-    int labs[4];
+    // genomes: ordering position x, holding device devs[u], in replica labs[u]
+    int labs[4], devs[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const int x = lane + 64 * u;
         labs[u] = 256;
+        devs[u] = 0;
         if (p < P && x < M) {
             int lab, d = x;
             if (ordered) {
@@ -181,77 +196,102 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             } else {
                 lab = gen.labels[(size_t)p * M + x];
             }
-            labs[u] = lab;
+            labs[u] = lab < k_max ? lab : 256;
+            devs[u] = d;
+        }
+    }
+    const int passes = n_r > 0 ? n_r : 1;
+    for (int ri = 0; ri < passes; ++ri) {
+        for (int q = lane; q < 256; q += 64) {
+            packed[g][q] = 0;
+            mincap[g][q] = 0xFFFFFFFFu;
+        }
+        if (lane < 8) {
+            hmask[g][lane] = 0;
+            lmask[g][lane] = 0;
+        }
+        if (lane < kClasses) ncls[g][lane] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int lab = labs[u];
             if (lab < k_max) {
-                const uint32_t c0 = tb.cap0[d];
+                // role index of this pass, or of the cluster
+                const int r = n_r > 0 ? ri : (tb.n_mem > 1 ? roles[(size_t)p * k_max + lab] != 0 : 0);
+                const int c = mem_class(tb, r);
+                const uint32_t c0 = tb.cap0[(size_t)c * M + devs[u]];
                 atomicAdd(&packed[g][lab], (1u << 16) | c0);
                 atomicMin(&mincap[g][lab], c0);
-                if (tb.capH[d]) atomicOr(&hmask[g][lab >> 5], 1u << (lab & 31));
+                if (tb.capH[(size_t)c * M + devs[u]])
+                    atomicOr(&hmask[g][lab >> 5], 1u << (lab & 31));
             }
         }
-    }
-    __syncthreads();
-    // decide per cluster; count listed problems per class
-    uint32_t my_cls[4] = {0, 0, 0, 0};
-    for (int c = 0; c < kClasses; ++c) ncls[g][c] = 0;  // every lane writes the same zero
-    __syncthreads();
+        __syncthreads();
+        // decide per cluster; count listed problems per class
+        uint32_t my_cls[4] = {0, 0, 0, 0};
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int q = lane + 64 * u;
-        bool feas = false;
-        int cls = 0;
-        if (p < P && q < k_max) {
-            const uint32_t pk = packed[g][q];
-            const uint32_t m = pk >> 16, csum = pk & 0xFFFF;
-            feas = m >= 1 && m <= (uint32_t)N && csum >= (uint32_t)N && mincap[g][q] >= 1 &&
-                   ((hmask[g][q >> 5] >> (q & 31)) & 1u) && !((bad[g][q >> 5] >> (q & 31)) & 1u);
-            cls = size_class((int)m);
-            if (!feas) {
-                const size_t o = (size_t)p * k_max + q;
-                T[o] = E2_INF64;
-                Lambda[o] = E2_INF64;
-                if (master) master[o] = -1;
+        for (int u = 0; u < 4; ++u) {
+            const int q = lane + 64 * u;
+            bool feas = false;
+            int cls = 0;
+            if (p < P && q < k_max) {
+                const uint32_t pk = packed[g][q];
+                const uint32_t m = pk >> 16, csum = pk & 0xFFFF;
+                feas = m >= 1 && m <= (uint32_t)N && csum >= (uint32_t)N && mincap[g][q] >= 1 &&
+                       ((hmask[g][q >> 5] >> (q & 31)) & 1u) &&
+                       !((bad[g][q >> 5] >> (q & 31)) & 1u);
+                cls = size_class((int)m);
+                if (!feas) {
+                    const size_t o = n_r > 0 ? ((size_t)p * k_max + q) * n_r + ri
+                                             : (size_t)p * k_max + q;
+                    T[o] = E2_INF64;
+                    Lambda[o] = E2_INF64;
+                    if (master) master[o] = -1;
+                }
+            }
+            my_cls[u] = feas ? (uint32_t)(cls + 1) : 0;
+            const uint64_t fm = __ballot(feas);
+            if (lane == 0 && fm) {
+                // q = 64u + bit: listed bitmask words 2u and 2u + 1
+                lmask[g][2 * u] = (uint32_t)fm;
+                lmask[g][2 * u + 1] = (uint32_t)(fm >> 32);
+            }
+            for (int c = 0; c < kClasses; ++c) {
+                const uint64_t bm = __ballot(feas && cls == c);
+                if (lane == 0) ncls[g][c] += (uint32_t)__popcll(bm);
             }
         }
-        my_cls[u] = feas ? (uint32_t)(cls + 1) : 0;
-        const uint64_t fm = __ballot(feas);
-        if (lane == 0 && fm) {
-            // q = 64u + bit: listed bitmask words 2u and 2u + 1
-            lmask[g][2 * u] = (uint32_t)fm;
-            lmask[g][2 * u + 1] = (uint32_t)(fm >> 32);
+        __syncthreads();
+        // one atomic per class per workgroup; genome g's share follows genomes < g
+        if (threadIdx.x < kClasses) {
+            const int c = threadIdx.x;
+            uint32_t tot = 0;
+            for (int h = 0; h < kEG; ++h) tot += ncls[h][c];
+            uint32_t b0 = tot ? atomicAdd(&counters[c], tot) : 0;
+            for (int h = 0; h < kEG; ++h) {
+                base[h][c] = b0;
+                b0 += ncls[h][c];
+            }
         }
-        for (int c = 0; c < kClasses; ++c) {
-            const uint64_t bm = __ballot(feas && cls == c);
-            if (lane == 0) ncls[g][c] += (uint32_t)__popcll(bm);
-        }
-    }
-    __syncthreads();
-    // one atomic per class per workgroup; genome g's share follows genomes < g
-    if (threadIdx.x < kClasses) {
-        const int c = threadIdx.x;
-        uint32_t tot = 0;
-        for (int h = 0; h < kEG; ++h) tot += ncls[h][c];
-        uint32_t b0 = tot ? atomicAdd(&counters[c], tot) : 0;
-        for (int h = 0; h < kEG; ++h) {
-            base[h][c] = b0;
-            b0 += ncls[h][c];
-        }
-    }
-    __syncthreads();
-    uint32_t run[kClasses] = {0, 0, 0, 0};
+        __syncthreads();
+        uint32_t run[kClasses] = {0, 0, 0, 0};
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int q = lane + 64 * u;
-        const uint32_t mc = my_cls[u];
-        for (int c = 0; c < kClasses; ++c) {
-            const uint64_t bm = __ballot(mc == (uint32_t)(c + 1));
-            if (mc == (uint32_t)(c + 1)) {
-                const uint32_t pos =
-                    base[g][c] + run[c] + (uint32_t)__popcll(bm & ((1ull << lane) - 1));
-                list[(size_t)c * seg_cap + pos] = ((uint32_t)p << 8) | (uint32_t)q;
+        for (int u = 0; u < 4; ++u) {
+            const int q = lane + 64 * u;
+            const uint32_t mc = my_cls[u];
+            for (int c = 0; c < kClasses; ++c) {
+                const uint64_t bm = __ballot(mc == (uint32_t)(c + 1));
+                if (mc == (uint32_t)(c + 1)) {
+                    const uint32_t pos =
+                        base[g][c] + run[c] + (uint32_t)__popcll(bm & ((1ull << lane) - 1));
+                    list[(size_t)c * seg_cap + pos] =
+                        n_r > 0 ? ((uint32_t)p << 8) | ((uint32_t)q << 4) | (uint32_t)ri
+                                : ((uint32_t)p << 8) | (uint32_t)q;
+                }
+                run[c] += (uint32_t)__popcll(bm);
             }
-            run[c] += (uint32_t)__popcll(bm);
         }
+        __syncthreads();
     }
     // layers of devices the DP kernel will not write: those outside every
     // listed cluster; for ordered genomes every device (the DP kernel, which
@@ -985,7 +1025,7 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_dp(E2Tables tb, int k_max, int pool_cells,
                                            E2Genomes gen, const uint8_t *__restrict__ roles,
-                                           uint32_t *counters, const uint32_t *__restrict__ list,
+                                           int n_r, uint32_t *counters, const uint32_t *__restrict__ list,
                                            size_t seg_cap, uint64_t *rows, uint8_t *tb_global,
                                            uint64_t *T,
                                            uint64_t *Lambda, int16_t *master, uint8_t *layers)
@@ -1024,7 +1064,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
                 if (idx >= n2) { idx -= n2; cls = 3; } } }
         const uint32_t code = list[(size_t)cls * seg_cap + idx];
         const int p = (int)(code >> 8);
-        const int q = (int)(code & 0xFF);
+        const int q = n_r > 0 ? (int)((code >> 4) & 0xF) : (int)(code & 0xFF);
 
         int m = 0;
         if (gen.labels) {
@@ -1047,15 +1087,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
             for (int k = lane; k < m; k += kWave) chain[k] = gen.order[(size_t)p * M + lo + k];
         }
         __syncthreads();
-        const int r = roles[(size_t)p * k_max + q] != 0;
-        const size_t o = (size_t)p * k_max + q;
+        // role index: from the job (every role searched) or the genome's role
+        const int r = n_r > 0 ? (int)(code & 0xF) : roles[(size_t)p * k_max + q] != 0;
+        const size_t o = n_r > 0 ? ((size_t)p * k_max + q) * n_r + r : (size_t)p * k_max + q;
+        const E2Tables tv = mem_view(tb, r);
 
         uint64_t best = E2_INF64;
         int best_mu = 0;
         ChainRegs cr;
         uint64_t bound = E2_INF64, bound_tot = E2_INF64;
         int pool_need = 0;
-        bool banded = chain_regs(tb, sm, r, chain, m, lane, cr, &bound, &bound_tot, &pool_need);
+        bool banded = chain_regs(tv, sm, r, chain, m, lane, cr, &bound, &bound_tot, &pool_need);
         // split points of bands beyond the LDS copy go to the global table
         DpSmem smb = sm;
         if (pool_need > kLdsTbCells) {
@@ -1063,14 +1105,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
             banded = banded && tb_global != nullptr;
         }
         if (banded && bound <= kU32MaxValue)
-            dp_banded<uint32_t>(tb, smb, cr, r, m, lane, &best, &best_mu, start, &last_tb);
+            dp_banded<uint32_t>(tv, smb, cr, r, m, lane, &best, &best_mu, start, &last_tb);
         else if (banded && bound_tot < kF64Limit)
-            dp_banded<double>(tb, smb, cr, r, m, lane, &best, &best_mu, start, &last_tb);
+            dp_banded<double>(tv, smb, cr, r, m, lane, &best, &best_mu, start, &last_tb);
         else {
             // reference path: a full table per master, then the chosen
             // master's table again with split points
             for (int mu = 1; mu <= m; ++mu) {
-                const uint64_t v = dp_table(tb, sm, r, chain, m, mu, nullptr, lane);
+                const uint64_t v = dp_table(tv, sm, r, chain, m, mu, nullptr, lane);
                 if (v < best) {
                     best = v;
                     best_mu = mu;
@@ -1080,7 +1122,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
                 uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)kLdsTbCells)
                                    ? sm.tbp
                                    : tb_global + (size_t)blockIdx.x * N * N;
-                dp_table(tb, sm, r, chain, m, best_mu, tbp, lane);
+                dp_table(tv, sm, r, chain, m, best_mu, tbp, lane);
                 __threadfence_block();
                 __syncthreads();
                 if (lane == 0) {
@@ -1115,10 +1157,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
             int e = (k + 1 < m) ? start[k + 1] : N;
             if (e > N) e = N;
             if (e < s0) e = s0;
-            const uint64_t *pr = pref_row(tb, r, c);
+            const uint64_t *pr = pref_row(tv, r, c);
             part += pr[e] - pr[s0];
-            if (k + 1 == best_mu) part += tb.head[r * M + c];
-            if (k >= 1) part += link_tau(tb, r, chain[k - 1], c);
+            if (k + 1 == best_mu) part += tv.head[r * M + c];
+            if (k >= 1) part += link_tau(tv, r, chain[k - 1], c);
             if (layers) layers[(size_t)p * M + c] = (uint8_t)(e - s0);
         }
         const uint64_t lam = wave_sum_u64(part);
@@ -1135,6 +1177,30 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
 // Fitness (Eq. 3-5): one thread per individual.
 // ---------------------------------------------------------------------------
 constexpr uint64_t kScale = 1ull << 50;
+
+// Eq. 3-5 from the summed fixed-point rates of the prefill and the decode
+// replicas (0 = none usable): S_P = ceil(SCALE / sum_P), S_D = ND *
+// ceil(SCALE / sum_D), phase = max(S_P, S_D), w = S_P + (phase - T_a) when
+// phase > T_a, else 0; INF without a usable replica of either role.
+struct Fit {
+    uint64_t w, phase, sp, sd;
+};
+
+__device__ __forceinline__ Fit fitness_of_rates(uint64_t sum_p, uint64_t sum_d, uint64_t t_arrival,
+                                                uint64_t nd)
+{
+    Fit f;
+    f.sp = sum_p ? (kScale + sum_p - 1) / sum_p : E2_INF64;
+    f.sd = sum_d ? nd * ((kScale + sum_d - 1) / sum_d) : E2_INF64;
+    if (f.sp == E2_INF64 || f.sd == E2_INF64) {
+        f.w = f.phase = E2_INF64;
+        return f;
+    }
+    f.phase = umax64(f.sp, f.sd);
+    const uint64_t excess = f.phase > t_arrival ? f.phase - t_arrival : 0;
+    f.w = excess ? f.sp + excess : 0;
+    return f;
+}
 
 __global__ __launch_bounds__(256) void k_fitness(int P, int k_max, const uint64_t *__restrict__ T,
                                                  const uint64_t *__restrict__ Lambda,
@@ -1161,19 +1227,110 @@ __global__ __launch_bounds__(256) void k_fitness(int P, int k_max, const uint64_
     sp = wave_sum_u64(sp);
     sd = wave_sum_u64(sd);
     if (lane != 0) return;
-    const uint64_t SP = sp ? (kScale + sp - 1) / sp : E2_INF64;
-    const uint64_t SD = sd ? nd * ((kScale + sd - 1) / sd) : E2_INF64;
-    if (s_p) s_p[p] = SP;
-    if (s_d) s_d[p] = SD;
-    if (SP == E2_INF64 || SD == E2_INF64) {
-        w[p] = E2_INF64;
-        phase[p] = E2_INF64;
-        return;
+    const Fit f = fitness_of_rates(sp, sd, t_arrival, nd);
+    if (s_p) s_p[p] = f.sp;
+    if (s_d) s_d[p] = f.sd;
+    w[p] = f.w;
+    phase[p] = f.phase;
+}
+
+// ---------------------------------------------------------------------------
+// Role and slot search (Algorithm 2's inner loop and its brute-force role
+// assignment): one wave per genome.  Lane q < k_max turns cluster q's DP
+// results into a prefill rate and, at the largest slot count b that is
+// feasible and meets the QoS floor, a decode rate b * SCALE / T_b.  A
+// cluster without a decode rate is prefill in every optimum (as decode it
+// adds nothing to the decode sum and takes its prefill rate away; ties go
+// to the smaller decode set), so the wave enumerates the role sets of the F
+// other clusters: lanes stride over the 2^F subsets in increasing order of
+// the decode bitmask, each keeps its smallest (w, phase, mask), and a wave
+// reduction picks the overall smallest.
+// ---------------------------------------------------------------------------
+struct Best {
+    uint64_t w, phase;
+    uint32_t mask;
+};
+
+__device__ __forceinline__ bool best_less(const Best &a, const Best &b)
+{
+    if (a.w != b.w) return a.w < b.w;
+    if (a.phase != b.phase) return a.phase < b.phase;
+    return a.mask < b.mask;
+}
+
+__global__ __launch_bounds__(64) void k_roles(int P, int k_max, int R,
+                                              const uint64_t *__restrict__ T_all,
+                                              const uint64_t *__restrict__ L_all,
+                                              uint64_t t_arrival, uint64_t nd, uint64_t lambda_max,
+                                              uint8_t *roles_out, uint8_t *slots_out, uint64_t *w,
+                                              uint64_t *phase)
+{
+    __shared__ uint64_t rho_p[16], rho_d[16];
+    __shared__ uint32_t bstar[16];
+    const int p = blockIdx.x;
+    const int lane = threadIdx.x;
+    if (lane < k_max) {
+        const uint64_t *Tq = T_all + ((size_t)p * k_max + lane) * R;
+        const uint64_t *Lq = L_all + ((size_t)p * k_max + lane) * R;
+        const uint64_t t0 = Tq[0];
+        rho_p[lane] = t0 != E2_INF64 ? kScale / (t0 > 0 ? t0 : 1) : 0;
+        uint32_t bs = 0;
+        uint64_t rd = 0;
+        for (int b = R - 1; b >= 1; --b) {
+            const uint64_t tb = Tq[b];
+            if (tb != E2_INF64 && Lq[b] <= lambda_max) {
+                bs = (uint32_t)b;
+                rd = ((uint64_t)b * kScale) / (tb > 0 ? tb : 1);
+                break;
+            }
+        }
+        rho_d[lane] = rd;
+        bstar[lane] = bs;
     }
-    const uint64_t ph = umax64(SP, SD);
-    const uint64_t excess = ph > t_arrival ? ph - t_arrival : 0;
-    phase[p] = ph;
-    w[p] = excess ? SP + excess : 0;
+    __syncthreads();
+    // free clusters (a decode rate), in increasing q; the others are prefill
+    uint32_t fmask = 0;
+    uint64_t fixed_p = 0;
+    for (int q = 0; q < k_max; ++q) {
+        if (rho_d[q]) fmask |= 1u << q;
+        else fixed_p += rho_p[q];
+    }
+    const int F = __popc(fmask);
+    Best best = {E2_INF64, E2_INF64, 0xFFFFFFFFu};
+    for (uint32_t x = (uint32_t)lane; x < (1u << F); x += kWave) {
+        // deposit the bits of x onto the free clusters (order preserving)
+        uint32_t mask = 0, rest = fmask;
+        uint64_t sp = fixed_p, sd = 0;
+        for (int i = 0; i < F; ++i) {
+            const int q = __ffs(rest) - 1;
+            rest &= rest - 1;
+            if ((x >> i) & 1u) {
+                mask |= 1u << q;
+                sd += rho_d[q];
+            } else {
+                sp += rho_p[q];
+            }
+        }
+        const Fit f = fitness_of_rates(sp, sd, t_arrival, nd);
+        const Best c = {f.w, f.phase, mask};
+        if (best_less(c, best)) best = c;
+    }
+    for (int off = kWave / 2; off >= 1; off >>= 1) {
+        Best o;
+        o.w = __shfl_xor(best.w, off, kWave);
+        o.phase = __shfl_xor(best.phase, off, kWave);
+        o.mask = __shfl_xor(best.mask, off, kWave);
+        if (best_less(o, best)) best = o;
+    }
+    if (lane < k_max) {
+        const uint32_t dec = (best.mask >> lane) & 1u;
+        roles_out[(size_t)p * k_max + lane] = (uint8_t)dec;
+        slots_out[(size_t)p * k_max + lane] = (uint8_t)(dec ? bstar[lane] : 0);
+    }
+    if (lane == 0) {
+        w[p] = best.w;
+        phase[p] = best.phase;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1522,15 +1679,17 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
                                 const E2Genomes &gen, const uint8_t *roles, const E2Work &wk,
                                 uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
-    const size_t seg = (size_t)P * k_max;
+    // without roles, every role index of every cluster
+    const int n_r = roles ? 0 : t.R;
+    const size_t seg = (size_t)P * k_max * (n_r ? n_r : 1);
     k_init<<<1, 64, 0, s>>>(wk.counters);
-    k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, wk.counters, wk.list,
-                                                       seg, T, Lambda, master, layers);
+    k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, roles, n_r, wk.counters,
+                                                       wk.list, seg, T, Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
-    k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles, wk.counters,
-                                                      wk.list, seg, wk.rows, wk.tb_global, T,
-                                                      Lambda, master, layers);
+    k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles, n_r,
+                                                      wk.counters, wk.list, seg, wk.rows,
+                                                      wk.tb_global, T, Lambda, master, layers);
     if (wk.ev_end) (void)hipEventRecord(wk.ev_end, s);
     return hipGetLastError();
 }
@@ -1542,6 +1701,16 @@ hipError_t e2_launch_fitness(hipStream_t s, int P, int k_max, const uint64_t *T,
 {
     k_fitness<<<(P + 3) / 4, 256, 0, s>>>(P, k_max, T, Lambda, roles, t_arrival, nd,
                                               lambda_max, w, phase, s_p, s_d);
+    return hipGetLastError();
+}
+
+hipError_t e2_launch_roles(hipStream_t s, int P, int k_max, int R, const uint64_t *T_all,
+                           const uint64_t *L_all, uint64_t t_arrival, uint64_t nd,
+                           uint64_t lambda_max, uint8_t *roles_out, uint8_t *slots_out,
+                           uint64_t *w, uint64_t *phase)
+{
+    k_roles<<<P, 64, 0, s>>>(P, k_max, R, T_all, L_all, t_arrival, nd, lambda_max, roles_out,
+                             slots_out, w, phase);
     return hipGetLastError();
 }
 
