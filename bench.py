@@ -24,6 +24,10 @@ Printed on one JSON line:
                the current kernel sources
   cpu_baseline the CPU oracle on a bounded sample of the same generation-0
                population, single-threaded
+  role_search  e2_search_roles on the 1024-genome, 64-device workload (at
+               most 16 clusters per genome) with its decode-slot model: per
+               call, every cluster is solved for prefill and for 1..8 decode
+               requests in flight, then roles are brute-forced per genome
   two_chromosome  the same measurements for the paper's two-chromosome
                genomes (an ordering of the devices cut into replicas, App. A):
                e2_eval_population_ordered + e2_ga_step_ordered per generation
@@ -310,6 +314,9 @@ def main():
     ap.add_argument("--ordered-steps", type=int, default=5,
                     help="timed generations of the two-chromosome GA after the headline "
                          "(with --genomes both; 0 disables)")
+    ap.add_argument("--search-steps", type=int, default=5,
+                    help="timed role and slot searches on the 1024-genome workload "
+                         "(with --genomes both; 0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU-oracle sample (0 disables)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -431,9 +438,60 @@ def main():
         result["two_chromosome"] = dict(step=steps["two_chromosome"], steps=n,
                                         dp_cells_per_s=t2["cells"] / t2["elapsed"],
                                         **summary(t2, n, "two_chromosome"))
+    if args.genomes == "both" and args.search_steps > 0:
+        result["role_search"] = role_search(torch, dev, args.search_steps, args.warmup)
     if args.cpu_seconds > 0 and head == "labels":
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+SEARCH_WORKLOAD = "c3_64dev_80L"
+
+
+def role_search(torch, dev, steps, warmup):
+    """Time e2_search_roles (every cluster for prefill and each decode slot
+    count, the QoS-feasible slot count, brute-force roles) on the 1024-genome
+    workload with its slot model; count the Algorithm 1 cells of the
+    feasible (cluster, role index) problems."""
+    wl = workload.make(SEARCH_WORKLOAD)
+    sm = workload.slot_model(wl)
+    ctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
+    L = torch.from_numpy(wl.labels).to(dev)
+    fp = wl.fitness_params()
+    out = e2.e2_search_roles(ctx, L, fp, wl.k_max, with_tables=True)
+    for _ in range(warmup):
+        e2.e2_search_roles(ctx, L, fp, wl.k_max, out=out)
+    torch.cuda.synchronize()
+    e2.e2_ctx_dp_timing(ctx, steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        e2.e2_search_roles(ctx, L, fp, wl.k_max, out=out)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    n_dp, dp_ms = e2.e2_ctx_dp_elapsed(ctx)
+    e2.e2_ctx_dp_timing(ctx, 0)
+    assert n_dp == steps, (n_dp, steps)
+    T_all = e2.u64(out["T_all"])
+    N = wl.n_layer
+    cells = problems = 0
+    for p, q, chain in label_problems(wl.labels, wl.k_max):
+        m = len(chain)
+        ok = int((T_all[p, q] != INF).sum())
+        problems += ok
+        cells += ok * m * (m * N - m * (m - 1) // 2)
+    slots = out["slots"].cpu().numpy()
+    log(f"role search on {wl.name}: {elapsed * 1e3 / steps:.3f} ms per call, DP kernel "
+        f"{dp_ms / n_dp:.3f} ms")
+    return {"workload": wl.name, "population": wl.population, "devices": wl.n_dev,
+            "layers": N, "clusters_per_genome": "8-12", "slot_model": sm,
+            "call": "e2_search_roles", "steps": steps,
+            "ms_per_call": elapsed * 1e3 / steps,
+            "genomes_per_s": wl.population * steps / elapsed,
+            "feasible_dp_problems_per_call": problems,
+            "dp_cells_per_s": cells * steps / elapsed,
+            "k_dp_avg_ms": dp_ms / n_dp,
+            "decode_replicas_at_b_max": int((slots == sm["b_max"]).sum())}
 
 
 def measure(torch, ctx, stream, bufs, init, step, count, warmup, steps):
