@@ -79,6 +79,14 @@ def _load() -> ctypes.CDLL:
     lib.oracle_search_roles.argtypes = [i32, i32, P, P, P, P, P, u64, u64, i32, i32, i32, P,
                                         u64, u64, u64, P, P, P, P, P, P]
     lib.oracle_search_roles.restype = i32
+    lib.oracle_assign_roles_splitwise.argtypes = [i32, i32, P, P, P, P, P, u64, u64, i32, i32,
+                                                  i32, P, u64, u64, u64, u64, P, P, P, P, P, P]
+    lib.oracle_assign_roles_splitwise.restype = i32
+    lib.oracle_solve_obj.argtypes = [i32, i32, P, P, P, P, P, u64, i32, i32, i32, P, P, P, P, P,
+                                     P, P]
+    lib.oracle_solve_obj.restype = i32
+    lib.oracle_dp_pipe_obj.argtypes = [i32, i32, P, P, P, P, P, u64, i32, P, P, P, P, P]
+    lib.oracle_dp_pipe_obj.restype = i32
     lib.oracle_rng.argtypes = [u64, u64, u64, u64, u64]
     lib.oracle_rng.restype = u64
     lib.oracle_splitmix_out.argtypes = [u64]
@@ -335,12 +343,20 @@ def quantise_slots(problem, b_max, beta_ppm):
     return t[:R], h[:R], tau[:R]
 
 
-def search_roles(wl, slot_model, labels=None):
+def np_tokens(wl):
+    """Prompt tokens NP of a workload: the ratio of its prefill to its decode
+    activation bytes (NP tokens against one)."""
+    act = [int(x) for x in wl.act_bytes]
+    return act[0] // max(act[1], 1)
+
+
+def search_roles(wl, slot_model, labels=None, policy="search"):
     """Algorithm 2's inner loop for a population of label genomes: the DP for
     prefill and for every decode slot count, the highest feasible slot count
     under the QoS floor, and the best role assignment by brute force.
     slot_model: dict(b_max, beta_ppm, kv_bytes_per_block_slot).  Returns dict
-    T_all, Lambda_all [P][k_max][b_max + 1], roles, slots [P][k_max], w, phase [P]."""
+    T_all, Lambda_all [P][k_max][b_max + 1], roles, slots [P][k_max], w, phase [P].
+    policy "splitwise": the adapted-SplitWise rule in place of the brute force."""
     lib = _load()
     labels = np.ascontiguousarray(wl.labels if labels is None else labels, dtype=np.uint8)
     P, M = labels.shape
@@ -356,12 +372,61 @@ def search_roles(wl, slot_model, labels=None):
     w = np.zeros(P, dtype=np.uint64)
     ph = np.zeros(P, dtype=np.uint64)
     fp = wl.fitness_params()
-    rc = lib.oracle_search_roles(M, wl.n_layer, _p(t), _p(h), _p(tau), _p(_u64(wl.mem_bytes)),
-                                 _p(_u64(wl.layer_bytes)), int(wl.head_bytes),
-                                 int(slot_model["kv_bytes_per_block_slot"]), b_max, P, K,
-                                 _p(labels), int(fp["t_arrival_ns"]), int(fp["nd_tokens"]),
-                                 int(fp["min_tps_milli"]), _p(T), _p(L), _p(roles), _p(slots),
-                                 _p(w), _p(ph))
+    common = (M, wl.n_layer, _p(t), _p(h), _p(tau), _p(_u64(wl.mem_bytes)),
+              _p(_u64(wl.layer_bytes)), int(wl.head_bytes),
+              int(slot_model["kv_bytes_per_block_slot"]), b_max, P, K, _p(labels),
+              int(fp["t_arrival_ns"]), int(fp["nd_tokens"]), int(fp["min_tps_milli"]))
+    outs = (_p(T), _p(L), _p(roles), _p(slots), _p(w), _p(ph))
+    if policy == "search":
+        rc = lib.oracle_search_roles(*common, *outs)
+    elif policy == "splitwise":
+        rc = lib.oracle_assign_roles_splitwise(*common, np_tokens(wl), *outs)
+    else:
+        raise OracleError(f"unknown policy {policy}")
     if rc != 0:
-        raise OracleError(f"oracle_search_roles failed: {rc}")
+        raise OracleError(f"oracle role assignment ({policy}) failed: {rc}")
     return dict(T_all=T, Lambda_all=L, roles=roles, slots=slots, w=w, phase=ph)
+
+
+def eval_population_ft(wl, labels=None, roles=None):
+    """The finishing-time ablation: each cluster's master and split points
+    minimise its end-to-end time (stage plus link times) instead of the
+    bottleneck; T is that partition's bottleneck, Lambda its end-to-end
+    time; fitness by Eq. 3-5 as usual."""
+    lib = _load()
+    t, h, tau = quantise(**wl.problem_arrays())
+    labels = np.ascontiguousarray(wl.labels if labels is None else labels, dtype=np.uint8)
+    roles = np.ascontiguousarray(wl.roles if roles is None else roles, dtype=np.uint8)
+    P, M = labels.shape
+    K = int(wl.k_max)
+    T = np.zeros((P, K), dtype=np.uint64)
+    L = np.zeros((P, K), dtype=np.uint64)
+    master = np.zeros((P, K), dtype=np.int16)
+    layers = np.zeros((P, M), dtype=np.uint8)
+    ev = np.zeros(1, dtype=np.uint64)
+    rc = lib.oracle_solve_obj(M, wl.n_layer, _p(t), _p(h), _p(tau), _p(_u64(wl.mem_bytes)),
+                              _p(_u64(wl.layer_bytes)), int(wl.head_bytes), 1, P, K, _p(labels),
+                              _p(roles), _p(T), _p(L), _p(master), _p(layers), _p(ev))
+    if rc != 0:
+        raise OracleError(f"oracle_solve_obj failed: {rc}")
+    sol = dict(T=T, Lambda=L, master=master, layers=layers)
+    sol.update(fitness(T, L, roles, **wl.fitness_params()))
+    return sol
+
+
+def dp_pipe_ft(tk, hk, tau_link, memk, W, HB):
+    """The finishing-time DP on one chain: (T = bottleneck of the chosen
+    partition, Lambda = its end-to-end time, mu_star, sizes)."""
+    lib = _load()
+    tk = _u64(tk)
+    m, N = tk.shape
+    sizes = np.zeros(m, dtype=np.int32)
+    T = np.zeros(1, np.uint64)
+    L = np.zeros(1, np.uint64)
+    mu = np.zeros(1, np.int32)
+    ev = np.zeros(1, np.uint64)
+    rc = lib.oracle_dp_pipe_obj(m, N, _p(tk), _p(_u64(hk)), _p(_u64(tau_link)), _p(_u64(memk)),
+                                _p(_u64(W)), int(HB), 1, _p(T), _p(L), _p(mu), _p(sizes), _p(ev))
+    if rc != 0:
+        raise OracleError(f"oracle_dp_pipe_obj failed: {rc}")
+    return int(T[0]), int(L[0]), int(mu[0]), [int(x) for x in sizes]

@@ -143,6 +143,62 @@ class Chain:
         sizes[0] = i + 1
         return sizes
 
+    def end_to_end(self, sizes, mu: int) -> int:
+        """Sum of stage times and link times (the finishing-time objective);
+        INF if a stage does not fit or a link is dead."""
+        v = 0
+        start = 0
+        for k, s in enumerate(sizes):
+            c = self.stage_cost(k, start, start + s - 1, k + 1 == mu)
+            if c == INF or (k >= 1 and self.tl[k] == INF):
+                return INF
+            v += c + (self.tl[k] if k >= 1 else 0)
+            start += s
+        return v
+
+    def solve_sum(self):
+        """The finishing-time variant by enumeration: the master and stages
+        with the least end-to-end time (smallest master on ties, then the
+        split points the backtrack's smallest-j rule recovers).  Returns
+        (bottleneck of that partition, its end-to-end time, mu, sizes)."""
+        m, N = self.m, self.N
+        if m > N:
+            return INF, INF, 0, [0] * m
+        best, best_mu = INF, 0
+        for mu in range(1, m + 1):
+            s_mu = min((self.end_to_end(c, mu) for c in compositions(N, m)), default=INF)
+            if s_mu < best:
+                best, best_mu = s_mu, mu
+        if best == INF:
+            return INF, INF, 0, [0] * m
+        mu = best_mu
+
+        @lru_cache(maxsize=None)
+        def opt(i: int, k: int) -> int:
+            """Least end-to-end time of blocks 0..i on devices 1..k."""
+            if i + 1 < k:
+                return INF
+            return min((self.end_to_end(c, mu) for c in compositions(i + 1, k)), default=INF)
+
+        sizes = [0] * m
+        i = N - 1
+        for k in range(m, 1, -1):
+            target = opt(i, k)
+            chosen = None
+            for j in range(0, i + 1):
+                prev = opt(j - 1, k - 1) if j >= 1 else INF
+                c = self.stage_cost(k - 1, j, i, k == mu)
+                if prev == INF or c == INF or self.tl[k - 1] == INF:
+                    continue
+                if prev + c + self.tl[k - 1] == target:
+                    chosen = j
+                    break
+            assert chosen is not None
+            sizes[k - 1] = i - chosen + 1
+            i = chosen - 1
+        sizes[0] = i + 1
+        return self.bottleneck(sizes, mu), best, mu, sizes
+
     def solve_idle_relaxed(self) -> int:
         """Optimum when devices may hold zero blocks (they then leave the
         pipeline; links join consecutive participating devices).  The master

@@ -164,6 +164,51 @@ static uint64_t dp_table(int m, int N, int mu, const uint64_t *pt, const uint64_
 }
 
 /*
+ * The finishing-time variant of one master's table (the FT ablation of
+ * Sec. 4.2): Eq. 1 with the bottleneck max replaced by a sum, so that
+ * DP(i, k) is the least end-to-end time of blocks 0..i on devices 1..k
+ * (stage times plus link times); Eq. 2 and the memory test unchanged,
+ * ties to the smallest j as R4.
+ */
+static uint64_t dp_table_sum(int m, int N, int mu, const uint64_t *pt, const uint64_t *pw,
+                             const uint64_t *hk, const uint64_t *tau_link, const uint64_t *memk,
+                             uint64_t HB, uint64_t *D, int *TB)
+{
+    const int W = m + 1;
+    uint64_t evaluated = 0;
+    for (int i = 0; i < N; i++) {
+        for (int k = 1; k <= m; k++) {
+            const uint64_t *ptk = pt + (size_t)(k - 1) * (N + 1);
+            const uint64_t head_t = (k == mu) ? hk[k - 1] : 0;
+            const uint64_t head_b = (k == mu) ? HB : 0;
+            D[i * W + k] = INF;
+            TB[i * W + k] = -1;
+            if (k == 1) {
+                uint64_t bytes = pw[i + 1] - pw[0] + head_b;
+                if (bytes <= memk[0])
+                    D[i * W + 1] = ptk[i + 1] - ptk[0] + head_t;
+                continue;
+            }
+            if (tau_link[k - 1] == INF) continue;
+            for (int j = 0; j <= i; j++) {
+                uint64_t prev = (j == 0) ? INF : D[(j - 1) * W + (k - 1)];
+                if (prev == INF) continue;
+                uint64_t bytes = pw[i + 1] - pw[j] + head_b;
+                if (bytes > memk[k - 1]) continue;
+                uint64_t cost = ptk[i + 1] - ptk[j] + head_t;
+                uint64_t v = prev + cost + tau_link[k - 1];
+                evaluated++;
+                if (v < D[i * W + k]) {
+                    D[i * W + k] = v;
+                    TB[i * W + k] = j;
+                }
+            }
+        }
+    }
+    return evaluated;
+}
+
+/*
  * DP_Pipe for one chain of m devices (Algorithm 1).
  *   tk[m][N]   block times of the chain's devices, chain order
  *   hk[m]      head + output-layer time of each chain device if it is master
@@ -173,10 +218,40 @@ static uint64_t dp_table(int m, int N, int mu, const uint64_t *pt, const uint64_
  * Outputs: *T (INF if infeasible), *Lambda, *mu_star (1-based, 0 if
  * infeasible), sizes[m] (0 if infeasible), *evaluated (candidate count).
  */
+static int dp_pipe_obj(int m, int N, const uint64_t *tk, const uint64_t *hk,
+                       const uint64_t *tau_link, const uint64_t *memk, const uint64_t *W,
+                       uint64_t HB, int objective, uint64_t *T, uint64_t *Lambda, int *mu_star,
+                       int *sizes, uint64_t *evaluated);
+
 int oracle_dp_pipe(int m, int N, const uint64_t *tk, const uint64_t *hk,
                    const uint64_t *tau_link, const uint64_t *memk, const uint64_t *W,
                    uint64_t HB, uint64_t *T, uint64_t *Lambda, int *mu_star, int *sizes,
                    uint64_t *evaluated)
+{
+    return dp_pipe_obj(m, N, tk, hk, tau_link, memk, W, HB, 0, T, Lambda, mu_star, sizes,
+                       evaluated);
+}
+
+/*
+ * objective 0: Algorithm 1 (least bottleneck).  objective 1: the
+ * finishing-time variant (least end-to-end time, dp_table_sum); the master
+ * and split points minimise that sum, *Lambda is the sum and *T the
+ * bottleneck (max over stage times and link times, R6) of the chosen
+ * partition.
+ */
+int oracle_dp_pipe_obj(int m, int N, const uint64_t *tk, const uint64_t *hk,
+                       const uint64_t *tau_link, const uint64_t *memk, const uint64_t *W,
+                       uint64_t HB, int objective, uint64_t *T, uint64_t *Lambda, int *mu_star,
+                       int *sizes, uint64_t *evaluated)
+{
+    return dp_pipe_obj(m, N, tk, hk, tau_link, memk, W, HB, objective, T, Lambda, mu_star, sizes,
+                       evaluated);
+}
+
+static int dp_pipe_obj(int m, int N, const uint64_t *tk, const uint64_t *hk,
+                       const uint64_t *tau_link, const uint64_t *memk, const uint64_t *W,
+                       uint64_t HB, int objective, uint64_t *T, uint64_t *Lambda, int *mu_star,
+                       int *sizes, uint64_t *evaluated)
 {
     *T = INF;
     *Lambda = INF;
@@ -207,7 +282,8 @@ int oracle_dp_pipe(int m, int N, const uint64_t *tk, const uint64_t *hk,
     uint64_t best = INF;
     int best_mu = 0;
     for (int mu = 1; mu <= m; mu++) {
-        *evaluated += dp_table(m, N, mu, pt, pw, hk, tau_link, memk, HB, D, TB);
+        *evaluated += objective ? dp_table_sum(m, N, mu, pt, pw, hk, tau_link, memk, HB, D, TB)
+                                : dp_table(m, N, mu, pt, pw, hk, tau_link, memk, HB, D, TB);
         uint64_t Tmu = D[(N - 1) * (m + 1) + m];
         if (Tmu < best) {
             best = Tmu;
@@ -224,17 +300,23 @@ int oracle_dp_pipe(int m, int N, const uint64_t *tk, const uint64_t *hk,
             i = j - 1;
         }
         sizes[0] = i + 1;
-        /* Lambda: sum of stage times plus the chain's link times */
-        uint64_t lam = 0;
+        /* Lambda: sum of stage times plus the chain's link times; the
+         * bottleneck of the same partition (equal to best for objective 0) */
+        uint64_t lam = 0, bott = 0;
         int start = 0;
         for (int k = 1; k <= m; k++) {
             int end = start + sizes[k - 1];
-            lam += pt[(size_t)(k - 1) * (N + 1) + end] - pt[(size_t)(k - 1) * (N + 1) + start];
-            if (k == best_mu) lam += hk[k - 1];
-            if (k >= 2) lam += tau_link[k - 1];
+            uint64_t st = pt[(size_t)(k - 1) * (N + 1) + end] - pt[(size_t)(k - 1) * (N + 1) + start];
+            if (k == best_mu) st += hk[k - 1];
+            lam += st;
+            bott = max2(bott, st);
+            if (k >= 2) {
+                lam += tau_link[k - 1];
+                bott = max2(bott, tau_link[k - 1]);
+            }
             start = end;
         }
-        *T = best;
+        *T = objective ? bott : best;
         *Lambda = lam;
         *mu_star = best_mu;
     }
@@ -251,11 +333,28 @@ int oracle_dp_pipe(int m, int N, const uint64_t *tk, const uint64_t *hk,
  * (blocks on each device, 0 for unassigned devices and infeasible clusters).
  * The chain of cluster q is its devices in ascending id (R9).
  */
+int oracle_solve_obj(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
+                     const uint64_t *mem, const uint64_t *W, uint64_t HB, int objective,
+                     int P, int k_max, const uint8_t *labels, const uint8_t *roles,
+                     uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers,
+                     uint64_t *evaluated_total);
+
 int oracle_solve(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
                  const uint64_t *mem, const uint64_t *W, uint64_t HB,
                  int P, int k_max, const uint8_t *labels, const uint8_t *roles,
                  uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers,
                  uint64_t *evaluated_total)
+{
+    return oracle_solve_obj(M, N, t, h, tau, mem, W, HB, 0, P, k_max, labels, roles, T, Lambda,
+                            master, layers, evaluated_total);
+}
+
+/* oracle_solve with the DP objective of oracle_dp_pipe_obj */
+int oracle_solve_obj(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
+                     const uint64_t *mem, const uint64_t *W, uint64_t HB, int objective,
+                     int P, int k_max, const uint8_t *labels, const uint8_t *roles,
+                     uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers,
+                     uint64_t *evaluated_total)
 {
     if (M < 1 || M > 256 || N < 1 || N > 255 || P < 0 || k_max < 1 || k_max > 255)
         return ORC_EINVAL;
@@ -285,7 +384,7 @@ int oracle_solve(int M, int N, const uint64_t *t, const uint64_t *h, const uint6
             }
             uint64_t Tv, Lv, ev;
             int mu;
-            int rc = oracle_dp_pipe(m, N, tk, hk, tl, mk, W, HB, &Tv, &Lv, &mu, sizes, &ev);
+            int rc = dp_pipe_obj(m, N, tk, hk, tl, mk, W, HB, objective, &Tv, &Lv, &mu, sizes, &ev);
             if (rc) { free(tk); return rc; }
             total += ev;
             if (Tv == INF) continue;
@@ -824,13 +923,54 @@ int oracle_quantise_slots(int M, int N, const uint64_t *speed, const uint64_t *b
  * clusters; slots_out[p][q] = b* of a decode cluster (0 if none qualified),
  * 0 otherwise.  At most 16 clusters per genome (2^16 assignments).
  */
+static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
+                        const uint64_t *mem, const uint64_t *W, uint64_t HB, uint64_t kv,
+                        int b_max, int P, int k_max, const uint8_t *labels, uint64_t t_arrival,
+                        uint64_t nd, uint64_t min_tps_milli, int policy, uint64_t np_tokens,
+                        uint64_t *T_all, uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
+                        uint64_t *w, uint64_t *phase);
+
 int oracle_search_roles(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
                         const uint64_t *mem, const uint64_t *W, uint64_t HB, uint64_t kv,
                         int b_max, int P, int k_max, const uint8_t *labels, uint64_t t_arrival,
                         uint64_t nd, uint64_t min_tps_milli, uint64_t *T_all, uint64_t *L_all,
                         uint8_t *roles_out, uint8_t *slots_out, uint64_t *w, uint64_t *phase)
 {
-    if (M < 1 || M > 256 || N < 1 || N > 255 || P < 0 || k_max < 1 || k_max > 16 ||
+    if (k_max > 16) return ORC_EINVAL;
+    return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, labels, t_arrival, nd,
+                        min_tps_milli, 0, 0, T_all, L_all, roles_out, slots_out, w, phase);
+}
+
+/*
+ * The adapted-SplitWise role rule (the ablation of Sec. 4.2): the same
+ * per-cluster DPs, prefill rates, kept slot counts and decode rates as
+ * oracle_search_roles, but instead of the brute force the R' non-empty
+ * clusters of a genome split by the token ratio: n_P = R'  NP / (NP + ND)
+ * rounded half up and clamped to [1, R' - 1] (R' itself when R' <= 1; 1/2
+ * of R' when NP + ND = 0), the n_P clusters with the highest prefill rate
+ * (ties to the smaller q) take prefill and the rest decode.  k_max <= 255.
+ */
+int oracle_assign_roles_splitwise(int M, int N, const uint64_t *t, const uint64_t *h,
+                                  const uint64_t *tau, const uint64_t *mem, const uint64_t *W,
+                                  uint64_t HB, uint64_t kv, int b_max, int P, int k_max,
+                                  const uint8_t *labels, uint64_t t_arrival, uint64_t nd,
+                                  uint64_t min_tps_milli, uint64_t np_tokens, uint64_t *T_all,
+                                  uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
+                                  uint64_t *w, uint64_t *phase)
+{
+    return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, labels, t_arrival, nd,
+                        min_tps_milli, 1, np_tokens, T_all, L_all, roles_out, slots_out, w,
+                        phase);
+}
+
+static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
+                        const uint64_t *mem, const uint64_t *W, uint64_t HB, uint64_t kv,
+                        int b_max, int P, int k_max, const uint8_t *labels, uint64_t t_arrival,
+                        uint64_t nd, uint64_t min_tps_milli, int policy, uint64_t np_tokens,
+                        uint64_t *T_all, uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
+                        uint64_t *w, uint64_t *phase)
+{
+    if (M < 1 || M > 256 || N < 1 || N > 255 || P < 0 || k_max < 1 || k_max > 255 ||
         b_max < 1 || b_max > 15 || nd > 8192)
         return ORC_EINVAL;
     const int R = b_max + 1;
@@ -841,8 +981,8 @@ int oracle_search_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
     if (!tk || !Wr) { free(tk); free(Wr); return ORC_ENOMEM; }
     const uint64_t lam_max = min_tps_milli ? 1000000000000ull / min_tps_milli : INF;
     for (int p = 0; p < P; p++) {
-        uint64_t rho_p[16], rho_d[16];
-        int bstar[16], used[16], n_used = 0;
+        uint64_t rho_p[256], rho_d[256];
+        int bstar[256], used[256], n_used = 0;
         for (int q = 0; q < k_max; q++) {
             int m = 0;
             for (int d = 0; d < M; d++)
@@ -879,6 +1019,39 @@ int oracle_search_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
                     break;
                 }
             }
+        }
+        if (policy == 1) {
+            /* prefill count from the token ratio, then the strongest
+             * clusters by prefill rate take prefill */
+            int n_p = n_used;
+            if (n_used >= 2) {
+                uint64_t tot = np_tokens + nd;
+                n_p = tot ? (int)((2 * (uint64_t)n_used * np_tokens + tot) / (2 * tot))
+                          : (n_used + 1) / 2;
+                if (n_p < 1) n_p = 1;
+                if (n_p > n_used - 1) n_p = n_used - 1;
+            }
+            uint8_t dec[256] = {0};
+            for (int i = 0; i < n_used; i++) {
+                int qi = used[i], rank = 0;
+                for (int k = 0; k < n_used; k++) {
+                    int qk = used[k];
+                    if (rho_p[qk] > rho_p[qi] || (rho_p[qk] == rho_p[qi] && qk < qi)) rank++;
+                }
+                dec[qi] = rank >= n_p;
+            }
+            uint64_t sum_p = 0, sum_d = 0, sp, sd;
+            for (int i = 0; i < n_used; i++) {
+                int q = used[i];
+                if (dec[q]) sum_d += rho_d[q];
+                else sum_p += rho_p[q];
+            }
+            rates_fitness(sum_p, sum_d, t_arrival, nd, w + p, phase + p, &sp, &sd);
+            for (int q = 0; q < k_max; q++) {
+                roles_out[(size_t)p * k_max + q] = dec[q];
+                slots_out[(size_t)p * k_max + q] = (uint8_t)(dec[q] ? bstar[q] : 0);
+            }
+            continue;
         }
         /* every role assignment of the used clusters, in increasing order of
          * the decode set's bitmask over q */
