@@ -355,12 +355,44 @@ int e2_ga_step_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
  *   T_all, Lambda_all [P][k_max][b_max+1]  device, optional (both or
  *                    neither): every DP result, index 0 prefill, b decode
  *                    with b requests; INF for empty or infeasible
- * Asynchronous on `stream`.  E2_EINVAL for sizes out of range, nd_tokens >
- * 8192 or a NULL required pointer.
+ * Asynchronous on `stream`.  E2_EINVAL for sizes out of range (P below
+ * 2^20), nd_tokens > 8192 or a NULL required pointer.
  */
 int e2_search_roles(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_t *labels,
                     const e2_fitness_params *fp, uint8_t *roles_out, uint8_t *slots_out,
                     uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all);
+
+/*
+ * The adapted-SplitWise role rule (the ablation of Sec. 4.2), on the same
+ * per-cluster DP results as e2_search_roles: per genome the R' non-empty
+ * clusters split by the token ratio, n_P = R' * np_tokens / (np_tokens +
+ * nd_tokens) rounded half up and clamped to [1, R' - 1] (R' when R' <= 1,
+ * half of R' rounded up when both token counts are 0); the n_P clusters
+ * with the highest prefill rate (ties to the smaller cluster id) prefill,
+ * the rest decode at their kept slot count.  Arguments and outputs as
+ * e2_search_roles, with k_max up to E2_MAX_CLUSTERS and P below 2^20.
+ */
+int e2_assign_roles_splitwise(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                              const uint8_t *labels, const e2_fitness_params *fp,
+                              uint32_t np_tokens, uint8_t *roles_out, uint8_t *slots_out,
+                              uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all);
+
+/*
+ * The finishing-time objective (the FT ablation of Sec. 4.2): as
+ * e2_solve_partitions / e2_eval_population, but each cluster's master and
+ * split points minimise its end-to-end time (stage times plus link times,
+ * Eq. 1 with the max replaced by a sum; memory, Eq. 2 and the tie rules
+ * unchanged).  T is the bottleneck of that partition (max over stage and
+ * link times), Lambda its end-to-end time; fitness by Eq. 3-5 as usual.
+ * One DP table per master (O(m^2 N^2) per cluster).
+ */
+int e2_solve_partitions_ft(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                           const uint8_t *labels, const uint8_t *roles, uint64_t *T,
+                           uint64_t *Lambda, int16_t *master, uint8_t *layers);
+int e2_eval_population_ft(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                          const uint8_t *labels, const uint8_t *roles,
+                          const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
+                          uint64_t *s_p, uint64_t *s_d);
 
 /*
  * Profiling of the DP kernel (the dominant cost of e2_solve_partitions and

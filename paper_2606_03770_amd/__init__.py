@@ -14,6 +14,9 @@ tensors on ROCm) and streams.  The wrappers keep the C names:
     e2_ga_step_ordered(ctx, order, sizes, roles, w, phase, ga)     genomes (App. A)
     e2_ctx_create_slots(problem, slot_model) -> Context   with decode slot counts
     e2_search_roles(ctx, labels, fitness)   role + slot search (Algorithm 2 inner loop)
+    e2_search_roles(..., splitwise_np_tokens=NP)     the ablations of Sec. 4.2:
+    e2_solve_partitions(..., objective="finish_time")  adapted-SplitWise roles,
+    e2_eval_population(..., objective="finish_time")   finishing-time objective
 
 `problem` is a dict with the fields of e2_problem (numpy arrays), as
 returned by workload.Workload.problem_arrays().  64-bit unsigned outputs
@@ -40,7 +43,8 @@ INF = (1 << 64) - 1
 EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitions",
             "e2_eval_population", "e2_ga_step", "e2_solve_partitions_ordered",
             "e2_eval_population_ordered", "e2_ga_step_ordered", "e2_ctx_create_slots",
-            "e2_search_roles", "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror")
+            "e2_search_roles", "e2_assign_roles_splitwise", "e2_solve_partitions_ft",
+            "e2_eval_population_ft", "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror")
 
 
 class E2Error(RuntimeError):
@@ -123,6 +127,15 @@ def lib() -> ctypes.CDLL:
     L.e2_search_roles.argtypes = [vp, vp, i32, i32, vp, ctypes.POINTER(e2_fitness_params), vp, vp,
                                   vp, vp, vp, vp]
     L.e2_search_roles.restype = ctypes.c_int
+    L.e2_assign_roles_splitwise.argtypes = [vp, vp, i32, i32, vp,
+                                            ctypes.POINTER(e2_fitness_params), ctypes.c_uint32,
+                                            vp, vp, vp, vp, vp, vp]
+    L.e2_assign_roles_splitwise.restype = ctypes.c_int
+    L.e2_solve_partitions_ft.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, vp, vp]
+    L.e2_solve_partitions_ft.restype = ctypes.c_int
+    L.e2_eval_population_ft.argtypes = [vp, vp, i32, i32, vp, vp,
+                                        ctypes.POINTER(e2_fitness_params), vp, vp, vp, vp]
+    L.e2_eval_population_ft.restype = ctypes.c_int
     L.e2_ctx_dp_timing.argtypes = [vp, i32]
     L.e2_ctx_dp_timing.restype = ctypes.c_int
     L.e2_ctx_dp_elapsed.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
@@ -256,9 +269,10 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
-def e2_solve_partitions(ctx: Context, labels, roles, stream=None, out: Optional[dict] = None):
+def e2_solve_partitions(ctx: Context, labels, roles, stream=None, out: Optional[dict] = None,
+                        objective: str = "bottleneck"):
     """Returns dict T, Lambda (int64 bits of u64) [P][k_max], master int16 [P][k_max],
-    layers uint8 [P][M]."""
+    layers uint8 [P][M].  objective "finish_time" calls e2_solve_partitions_ft."""
     torch = _torch()
     P, M = labels.shape
     k_max = roles.shape[1]
@@ -270,16 +284,18 @@ def e2_solve_partitions(ctx: Context, labels, roles, stream=None, out: Optional[
                    Lambda=torch.empty((P, k_max), dtype=torch.int64, device=dev),
                    master=torch.empty((P, k_max), dtype=torch.int16, device=dev),
                    layers=torch.empty((P, M), dtype=torch.uint8, device=dev))
-    _check(lib().e2_solve_partitions(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
-                                     _ptr(roles), _ptr(out["T"]), _ptr(out["Lambda"]),
-                                     _ptr(out["master"]), _ptr(out["layers"])),
-           "e2_solve_partitions")
+    name = {"bottleneck": "e2_solve_partitions", "finish_time": "e2_solve_partitions_ft"}[objective]
+    _check(getattr(lib(), name)(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
+                                _ptr(roles), _ptr(out["T"]), _ptr(out["Lambda"]),
+                                _ptr(out["master"]), _ptr(out["layers"])), name)
     return out
 
 
 def e2_eval_population(ctx: Context, labels, roles, fitness: dict, stream=None,
-                       with_rates: bool = True, out: Optional[dict] = None):
-    """Returns dict w, phase (and s_p, s_d) as int64 bits of u64, shape [P]."""
+                       with_rates: bool = True, out: Optional[dict] = None,
+                       objective: str = "bottleneck"):
+    """Returns dict w, phase (and s_p, s_d) as int64 bits of u64, shape [P].
+    objective "finish_time" calls e2_eval_population_ft."""
     torch = _torch()
     P = labels.shape[0]
     k_max = roles.shape[1]
@@ -291,11 +307,11 @@ def e2_eval_population(ctx: Context, labels, roles, fitness: dict, stream=None,
         out = {k: torch.empty(P, dtype=torch.int64, device=dev) for k in names}
     fp = e2_fitness_params(int(fitness["t_arrival_ns"]), int(fitness["nd_tokens"]),
                            int(fitness["min_tps_milli"]))
-    _check(lib().e2_eval_population(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
-                                    _ptr(roles), ctypes.byref(fp), _ptr(out["w"]),
-                                    _ptr(out["phase"]), _ptr(out.get("s_p")),
-                                    _ptr(out.get("s_d"))),
-           "e2_eval_population")
+    name = {"bottleneck": "e2_eval_population", "finish_time": "e2_eval_population_ft"}[objective]
+    _check(getattr(lib(), name)(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
+                                _ptr(roles), ctypes.byref(fp), _ptr(out["w"]),
+                                _ptr(out["phase"]), _ptr(out.get("s_p")),
+                                _ptr(out.get("s_d"))), name)
     return out
 
 
@@ -390,10 +406,13 @@ def e2_ga_step_ordered(ctx: Context, order_in, sizes_in, roles_in, w, phase, ga:
 
 
 def e2_search_roles(ctx: Context, labels, fitness: dict, k_max: int, stream=None,
-                    with_tables: bool = False, out: Optional[dict] = None):
+                    with_tables: bool = False, out: Optional[dict] = None,
+                    splitwise_np_tokens: Optional[int] = None):
     """Role and slot search for label genomes.  Returns dict roles, slots
     (uint8 [P][k_max]), w, phase (int64 bits of u64 [P]) and, with_tables,
-    T_all, Lambda_all (int64 bits of u64 [P][k_max][b_max + 1])."""
+    T_all, Lambda_all (int64 bits of u64 [P][k_max][b_max + 1]).  With
+    splitwise_np_tokens, e2_assign_roles_splitwise in place of the brute
+    force."""
     torch = _torch()
     P = labels.shape[0]
     _dev(labels, torch.uint8, (P, ctx.n_dev), "labels")
@@ -409,11 +428,16 @@ def e2_search_roles(ctx: Context, labels, fitness: dict, k_max: int, stream=None
             out["Lambda_all"] = torch.empty((P, k_max, R), dtype=torch.int64, device=dev)
     fp = e2_fitness_params(int(fitness["t_arrival_ns"]), int(fitness["nd_tokens"]),
                            int(fitness["min_tps_milli"]))
-    _check(lib().e2_search_roles(ctx.handle, _stream(stream), P, int(k_max), _ptr(labels),
-                                 ctypes.byref(fp), _ptr(out["roles"]), _ptr(out["slots"]),
-                                 _ptr(out["w"]), _ptr(out["phase"]), _ptr(out.get("T_all")),
-                                 _ptr(out.get("Lambda_all"))),
-           "e2_search_roles")
+    outs = (_ptr(out["roles"]), _ptr(out["slots"]), _ptr(out["w"]), _ptr(out["phase"]),
+            _ptr(out.get("T_all")), _ptr(out.get("Lambda_all")))
+    if splitwise_np_tokens is None:
+        _check(lib().e2_search_roles(ctx.handle, _stream(stream), P, int(k_max), _ptr(labels),
+                                     ctypes.byref(fp), *outs), "e2_search_roles")
+    else:
+        _check(lib().e2_assign_roles_splitwise(ctx.handle, _stream(stream), P, int(k_max),
+                                               _ptr(labels), ctypes.byref(fp),
+                                               int(splitwise_np_tokens), *outs),
+               "e2_assign_roles_splitwise")
     return out
 
 

@@ -484,7 +484,7 @@ namespace {
 
 int solve_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genomes &gen,
                const uint8_t *roles, uint64_t *T, uint64_t *Lambda, int16_t *master,
-               uint8_t *layers)
+               uint8_t *layers, int objective = 0)
 {
     if (!ctx) return E2_EINVAL;
     int rc = check_pop(P, k_max);
@@ -501,13 +501,13 @@ int solve_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Geno
     E2Work wk;
     carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk);
     const hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, roles, wk, T,
-                                              Lambda, master, layers);
+                                              Lambda, master, layers, objective);
     return e == hipSuccess ? E2_OK : E2_EHIP;
 }
 
 int eval_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genomes &gen,
               const uint8_t *roles, const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
-              uint64_t *s_p, uint64_t *s_d)
+              uint64_t *s_p, uint64_t *s_d, int objective = 0)
 {
     if (!ctx || !fp) return E2_EINVAL;
     int rc = check_pop(P, k_max);
@@ -528,12 +528,51 @@ int eval_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genom
     uint64_t *Ts = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
     uint64_t *Ls = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb + tl);
     hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, roles, wk, Ts, Ls,
-                                        nullptr, nullptr);
+                                        nullptr, nullptr, objective);
     if (e != hipSuccess) return E2_EHIP;
     const uint64_t lam_max =
         fp->min_tps_milli ? 1000000000000ull / fp->min_tps_milli : E2_INF64;
     e = e2_launch_fitness(s, P, k_max, Ts, Ls, roles, fp->t_arrival_ns, fp->nd_tokens, lam_max,
                           w, phase, s_p, s_d);
+    return e == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+// Every cluster for every role index, then the role assignment of policy
+// 0 (brute force) or 1 (adapted SplitWise).
+int roles_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_t *labels,
+               const e2_fitness_params *fp, int policy, uint32_t np_tokens, uint8_t *roles_out,
+               uint8_t *slots_out, uint64_t *w, uint64_t *phase, uint64_t *T_all,
+               uint64_t *Lambda_all)
+{
+    if (!ctx || !fp) return E2_EINVAL;
+    if (P < 0 || P >= (1 << 20) || k_max < 1 || k_max > E2_MAX_CLUSTERS) return E2_EINVAL;
+    if (fp->nd_tokens > 8192) return E2_EINVAL;
+    if ((T_all == nullptr) != (Lambda_all == nullptr)) return E2_EINVAL;
+    if (P == 0) return E2_OK;
+    if (!labels || !roles_out || !slots_out || !w || !phase) return E2_EINVAL;
+    int rc = check_device(ctx);
+    if (rc) return rc;
+    const int R = ctx->b_max + 1;
+    hipStream_t s = as_stream(stream);
+    int slots;
+    size_t tbb;
+    const size_t wb = work_bytes(ctx, P, k_max, &slots, &tbb, R);
+    const size_t tl = T_all ? 0 : align256((size_t)P * k_max * R * 8);
+    Scratch sc;
+    if ((rc = alloc_scratch(sc, s, wb + 2 * tl))) return rc;
+    E2Work wk;
+    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk, R);
+    uint64_t *Ts = T_all ? T_all : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
+    uint64_t *Ls = Lambda_all ? Lambda_all
+                              : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb + tl);
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, nullptr, wk, Ts, Ls,
+                                        nullptr, nullptr);
+    if (e != hipSuccess) return E2_EHIP;
+    const uint64_t lam_max =
+        fp->min_tps_milli ? 1000000000000ull / fp->min_tps_milli : E2_INF64;
+    e = e2_launch_roles(s, P, ctx->M, k_max, R, policy, np_tokens, labels, Ts, Ls,
+                        fp->t_arrival_ns, fp->nd_tokens, lam_max, roles_out, slots_out, w, phase);
     return e == hipSuccess ? E2_OK : E2_EHIP;
 }
 
@@ -625,36 +664,37 @@ int e2_search_roles(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const u
                     const e2_fitness_params *fp, uint8_t *roles_out, uint8_t *slots_out,
                     uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all)
 {
-    if (!ctx || !fp) return E2_EINVAL;
-    if (P < 0 || P >= (1 << 24) || k_max < 1 || k_max > E2_MAX_SEARCH_CLUSTERS) return E2_EINVAL;
-    if (fp->nd_tokens > 8192) return E2_EINVAL;
-    if ((T_all == nullptr) != (Lambda_all == nullptr)) return E2_EINVAL;
-    if (P == 0) return E2_OK;
-    if (!labels || !roles_out || !slots_out || !w || !phase) return E2_EINVAL;
-    int rc = check_device(ctx);
-    if (rc) return rc;
-    const int R = ctx->b_max + 1;
-    hipStream_t s = as_stream(stream);
-    int slots;
-    size_t tbb;
-    const size_t wb = work_bytes(ctx, P, k_max, &slots, &tbb, R);
-    const size_t tl = T_all ? 0 : align256((size_t)P * k_max * R * 8);
-    Scratch sc;
-    if ((rc = alloc_scratch(sc, s, wb + 2 * tl))) return rc;
-    E2Work wk;
-    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk, R);
-    uint64_t *Ts = T_all ? T_all : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
-    uint64_t *Ls = Lambda_all ? Lambda_all
-                              : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb + tl);
+    if (k_max > E2_MAX_SEARCH_CLUSTERS) return E2_EINVAL;
+    return roles_impl(ctx, stream, P, k_max, labels, fp, 0, 0, roles_out, slots_out, w, phase,
+                      T_all, Lambda_all);
+}
+
+int e2_assign_roles_splitwise(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                              const uint8_t *labels, const e2_fitness_params *fp,
+                              uint32_t np_tokens, uint8_t *roles_out, uint8_t *slots_out,
+                              uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all)
+{
+    return roles_impl(ctx, stream, P, k_max, labels, fp, 1, np_tokens, roles_out, slots_out, w,
+                      phase, T_all, Lambda_all);
+}
+
+int e2_solve_partitions_ft(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                           const uint8_t *labels, const uint8_t *roles, uint64_t *T,
+                           uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    if (P > 0 && !labels) return E2_EINVAL;
     const E2Genomes gen = {labels, nullptr, nullptr};
-    hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, nullptr, wk, Ts, Ls,
-                                        nullptr, nullptr);
-    if (e != hipSuccess) return E2_EHIP;
-    const uint64_t lam_max =
-        fp->min_tps_milli ? 1000000000000ull / fp->min_tps_milli : E2_INF64;
-    e = e2_launch_roles(s, P, k_max, R, Ts, Ls, fp->t_arrival_ns, fp->nd_tokens, lam_max,
-                        roles_out, slots_out, w, phase);
-    return e == hipSuccess ? E2_OK : E2_EHIP;
+    return solve_impl(ctx, stream, P, k_max, gen, roles, T, Lambda, master, layers, 1);
+}
+
+int e2_eval_population_ft(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                          const uint8_t *labels, const uint8_t *roles,
+                          const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
+                          uint64_t *s_p, uint64_t *s_d)
+{
+    if (P > 0 && !labels) return E2_EINVAL;
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    return eval_impl(ctx, stream, P, k_max, gen, roles, fp, w, phase, s_p, s_d, 1);
 }
 
 int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_t *labels_in,

@@ -54,7 +54,7 @@ struct e2_ctx {
 struct E2Work {
     uint32_t *counters;  // [0..3] problems listed per chain-length class, [4] next job
     uint32_t *list;      // [4][P * k_max * n_r] problems needing the DP: (p << 8) | q, or
-                         //   with every role index searched (p << 8) | (q << 4) | r
+                         //   with every role index searched (p << 12) | (q << 4) | r
     uint64_t *rows;      // [n_slots][pool + 2 (N+1)] per-wave DP rows
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
     int n_slots;         // waves of the DP kernel
@@ -82,14 +82,21 @@ struct E2Genomes {
 
 // Enqueue cluster extraction + DP.  Outputs may be the caller's (solve) or
 // scratch (eval; master/layers null).  With roles null, every cluster is
-// solved for every role index (k_max <= 16, R <= 16) and T, Lambda are
+// solved for every role index (R <= 16, P < 2^20) and T, Lambda are
 // [P][k_max][R]; master and layers must then be null.
+// objective 1: the finishing-time variant (least end-to-end time per
+// cluster; T reports that partition's bottleneck), label or ordered genomes
+// with roles only.
 hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_max,
                                 const E2Genomes &gen, const uint8_t *roles, const E2Work &wk,
-                                uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers);
+                                uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers,
+                                int objective = 0);
 
-// Role and slot search per genome from T, Lambda [P][k_max][R].
-hipError_t e2_launch_roles(hipStream_t s, int P, int k_max, int R, const uint64_t *T_all,
+// Role assignment per genome from T, Lambda [P][k_max][R]: policy 0 the
+// brute force (k_max <= 16), policy 1 the adapted-SplitWise rule (labels
+// give the non-empty clusters, np_tokens the prompt length).
+hipError_t e2_launch_roles(hipStream_t s, int P, int M, int k_max, int R, int policy,
+                           uint32_t np_tokens, const uint8_t *labels, const uint64_t *T_all,
                            const uint64_t *L_all, uint64_t t_arrival, uint64_t nd,
                            uint64_t lambda_max, uint8_t *roles_out, uint8_t *slots_out,
                            uint64_t *w, uint64_t *phase);

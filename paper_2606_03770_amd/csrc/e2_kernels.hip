@@ -134,8 +134,8 @@ __device__ __forceinline__ E2Tables mem_view(const E2Tables &tb, int r)
 }
 
 // n_r = 0: one problem per cluster, at role index (roles[q] != 0); n_r = R:
-// one problem per cluster and role index (k_max <= 16), outputs
-// [P][k_max][R] and list codes (p << 8) | (q << 4) | r.
+// one problem per cluster and role index (R <= 16, P < 2^20), outputs
+// [P][k_max][R] and list codes (p << 12) | (q << 4) | r.
 __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_max,
                                                       E2Genomes gen, const uint8_t *roles,
                                                       int n_r, uint32_t *counters,
@@ -285,7 +285,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                     const uint32_t pos =
                         base[g][c] + run[c] + (uint32_t)__popcll(bm & ((1ull << lane) - 1));
                     list[(size_t)c * seg_cap + pos] =
-                        n_r > 0 ? ((uint32_t)p << 8) | ((uint32_t)q << 4) | (uint32_t)ri
+                        n_r > 0 ? ((uint32_t)p << 12) | ((uint32_t)q << 4) | (uint32_t)ri
                                 : ((uint32_t)p << 8) | (uint32_t)q;
                 }
                 run[c] += (uint32_t)__popcll(bm);
@@ -1016,6 +1016,33 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
     return prv[(N - 1) - (m - 1)];
 }
 
+// The device chain of cluster q of genome p into chain[] (LDS); returns its
+// length.  Labels: the devices with label q in ascending id (wave ballot
+// compaction); two-chromosome genomes: replica q's run of the ordering.
+__device__ __forceinline__ int build_chain(const E2Genomes &gen, int p, int q, int k_max, int M,
+                                           int lane, uint8_t *chain)
+{
+    int m = 0;
+    if (gen.labels) {
+        for (int base = 0; base < M; base += kWave) {
+            const int d = base + lane;
+            const bool in = d < M && gen.labels[(size_t)p * M + d] == q;
+            const uint64_t mask = __ballot(in);
+            if (in) chain[m + __popcll(mask & ((1ull << lane) - 1))] = (uint8_t)d;
+            m += __popcll(mask);
+        }
+    } else {
+        uint64_t part = 0;
+        for (int r = lane; r < q; r += kWave) part += gen.sizes[(size_t)p * k_max + r];
+        const uint64_t off = wave_sum_u64(part);
+        const int lo = (int)(off < (uint64_t)M ? off : (uint64_t)M);
+        const uint64_t end = off + gen.sizes[(size_t)p * k_max + q];
+        m = (int)(end < (uint64_t)M ? end : (uint64_t)M) - lo;
+        for (int k = lane; k < m; k += kWave) chain[k] = gen.order[(size_t)p * M + lo + k];
+    }
+    return m;
+}
+
 // ---------------------------------------------------------------------------
 // Persistent DP kernel: one wave per workgroup; waves take listed problems
 // in list order through an atomic counter and exit when the list is
@@ -1063,29 +1090,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
             if (idx >= n1) { idx -= n1; cls = 2;
                 if (idx >= n2) { idx -= n2; cls = 3; } } }
         const uint32_t code = list[(size_t)cls * seg_cap + idx];
-        const int p = (int)(code >> 8);
-        const int q = n_r > 0 ? (int)((code >> 4) & 0xF) : (int)(code & 0xFF);
+        const int p = n_r > 0 ? (int)(code >> 12) : (int)(code >> 8);
+        const int q = n_r > 0 ? (int)((code >> 4) & 0xFF) : (int)(code & 0xFF);
 
-        int m = 0;
-        if (gen.labels) {
-            // chain = devices with label q in ascending id (wave ballot compaction)
-            for (int base = 0; base < M; base += kWave) {
-                const int d = base + lane;
-                const bool in = d < M && gen.labels[(size_t)p * M + d] == q;
-                const uint64_t mask = __ballot(in);
-                if (in) chain[m + __popcll(mask & ((1ull << lane) - 1))] = (uint8_t)d;
-                m += __popcll(mask);
-            }
-        } else {
-            // chain = replica q's run of the ordering chromosome, in order
-            uint64_t part = 0;
-            for (int r = lane; r < q; r += kWave) part += gen.sizes[(size_t)p * k_max + r];
-            const uint64_t off = wave_sum_u64(part);
-            const int lo = (int)(off < (uint64_t)M ? off : (uint64_t)M);
-            const uint64_t end = off + gen.sizes[(size_t)p * k_max + q];
-            m = (int)(end < (uint64_t)M ? end : (uint64_t)M) - lo;
-            for (int k = lane; k < m; k += kWave) chain[k] = gen.order[(size_t)p * M + lo + k];
-        }
+        const int m = build_chain(gen, p, q, k_max, M, lane, chain);
         __syncthreads();
         // role index: from the job (every role searched) or the genome's role
         const int r = n_r > 0 ? (int)(code & 0xF) : roles[(size_t)p * k_max + q] != 0;
@@ -1174,6 +1182,174 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
 }
 
 // ---------------------------------------------------------------------------
+// The finishing-time objective (the FT ablation): Eq. 1 with the bottleneck
+// max replaced by a sum, so that a master's table holds the least
+// end-to-end time (stage times plus link times) of blocks 0..i on devices
+// 1..k; Eq. 2 and the memory windows unchanged.  One full table per master:
+// lanes over cells i, each scanning its window of j in ascending order
+// (strict <, so ties keep the smallest j); the two rows ping-pong in the
+// wave's LDS; split points of rows 2..m go to tbp (row k at (k-2) N) when
+// tbp is not null.  Values stay below 2^58 (at most 255 block times and 255
+// link times, each below 2^48); INF terms are skipped.
+// ---------------------------------------------------------------------------
+__device__ uint64_t ft_table(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
+                             int m, int mu, uint8_t *tbp, int lane)
+{
+    const int N = tb.N, M = tb.M;
+    uint64_t *cur = sm.Rw0, *prv = sm.Rw1;
+    for (int k = 1; k <= m; ++k) {
+        const int c = uni(chain[k - 1]);
+        const int f = (mu == k);
+        const uint64_t *pr = pref_row(tb, r, c);
+        const uint8_t *wr = win_row(tb, f, c);
+        const uint64_t hadd = f ? uni64(tb.head[r * M + c]) : 0;
+        const uint64_t tau = k >= 2 ? link_tau_u(tb, r, uni(chain[k - 2]), c) : 0;
+        for (int i = lane; i < N; i += kWave) {
+            uint64_t best = E2_INF64;
+            int bj = 0;
+            const int w = wr[i];
+            if (i >= k - 1 && w != E2_NO_START) {
+                const uint64_t end = pr[i + 1] + hadd;
+                if (k == 1) {
+                    if (w == 0) best = end - pr[0];
+                } else if (tau != E2_INF64) {
+                    for (int j = max(w, k - 1); j <= i; ++j) {
+                        const uint64_t pv = prv[j - 1];
+                        if (pv == E2_INF64) continue;
+                        const uint64_t v = pv + tau + (end - pr[j]);
+                        if (v < best) {
+                            best = v;
+                            bj = j;
+                        }
+                    }
+                }
+            }
+            cur[i] = best;
+            if (tbp && k >= 2) tbp[(size_t)(k - 2) * N + i] = (uint8_t)bj;
+        }
+        __threadfence_block();
+        __syncthreads();
+        uint64_t *tmp = prv;
+        prv = cur;
+        cur = tmp;
+    }
+    return prv[N - 1];
+}
+
+__global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_cells, E2Genomes gen,
+                                              const uint8_t *__restrict__ roles,
+                                              uint32_t *counters,
+                                              const uint32_t *__restrict__ list, size_t seg_cap,
+                                              uint64_t *rows, uint8_t *tb_global, uint64_t *T,
+                                              uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    extern __shared__ uint64_t dyn[];
+    __shared__ uint8_t chain[256];
+    __shared__ uint8_t start[256];
+    __shared__ uint32_t job;
+    const int lane = threadIdx.x;
+    const int M = tb.M, N = tb.N;
+    DpSmem sm;
+    sm.ps = dyn;
+    sm.Rw0 = dyn + 2 * N;
+    sm.Rw1 = sm.Rw0 + (N + 1);
+    sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
+    uint64_t *my_rows = rows + (size_t)blockIdx.x * ((size_t)pool_cells + 2 * (N + 1));
+    sm.pool = my_rows;
+    sm.Ga = my_rows + pool_cells;
+    sm.Gb = sm.Ga + (N + 1);
+    sm.pool_cells = pool_cells;
+    const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
+    const uint32_t n_jobs = n0 + n1 + n2 + n3;
+    for (;;) {
+        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
+        __syncthreads();
+        uint32_t idx = job;
+        __syncthreads();
+        if (idx >= n_jobs) break;
+        int cls = 0;
+        if (idx >= n0) { idx -= n0; cls = 1;
+            if (idx >= n1) { idx -= n1; cls = 2;
+                if (idx >= n2) { idx -= n2; cls = 3; } } }
+        const uint32_t code = list[(size_t)cls * seg_cap + idx];
+        const int p = (int)(code >> 8);
+        const int q = (int)(code & 0xFF);
+        const int m = build_chain(gen, p, q, k_max, M, lane, chain);
+        __syncthreads();
+        const int r = roles[(size_t)p * k_max + q] != 0;
+        const size_t o = (size_t)p * k_max + q;
+        const E2Tables tv = mem_view(tb, r);
+        // least end-to-end time over masters, the smallest master on ties
+        uint64_t best = E2_INF64;
+        int best_mu = 0;
+        for (int mu = 1; mu <= m; ++mu) {
+            const uint64_t v = ft_table(tv, sm, r, chain, m, mu, nullptr, lane);
+            if (v < best) {
+                best = v;
+                best_mu = mu;
+            }
+        }
+        if (best == E2_INF64) {
+            if (lane == 0) {
+                T[o] = E2_INF64;
+                Lambda[o] = E2_INF64;
+                if (master) master[o] = -1;
+            }
+            if (layers)
+                for (int k = lane; k < m; k += kWave) layers[(size_t)p * M + chain[k]] = 0;
+            __syncthreads();
+            continue;
+        }
+        uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)kLdsTbCells)
+                           ? sm.tbp
+                           : tb_global + (size_t)blockIdx.x * N * N;
+        ft_table(tv, sm, r, chain, m, best_mu, tbp, lane);
+        __builtin_amdgcn_s_waitcnt(0);
+        __threadfence_block();
+        __syncthreads();
+        if (lane == 0) {
+            int i = N - 1;
+            for (int k = m; k >= 2; --k) {
+                int j = tbp[(size_t)(k - 2) * N + (i < 0 ? 0 : i)];
+                if (j > i) j = i < 0 ? 0 : i;
+                start[k - 1] = (uint8_t)j;
+                i = j - 1;
+            }
+            start[0] = 0;
+        }
+        __syncthreads();
+        // the partition's end-to-end time and its bottleneck
+        uint64_t part = 0, bott = 0;
+        for (int k = lane; k < m; k += kWave) {
+            const int c = chain[k];
+            const int s0 = start[k] < N ? start[k] : N;
+            int e = (k + 1 < m) ? start[k + 1] : N;
+            if (e > N) e = N;
+            if (e < s0) e = s0;
+            const uint64_t *pr = pref_row(tv, r, c);
+            uint64_t st = pr[e] - pr[s0];
+            if (k + 1 == best_mu) st += tv.head[r * M + c];
+            part += st;
+            bott = umax64(bott, st);
+            if (k >= 1) {
+                const uint64_t tl = link_tau(tv, r, chain[k - 1], c);
+                part += tl;
+                bott = umax64(bott, tl);
+            }
+            if (layers) layers[(size_t)p * M + c] = (uint8_t)(e - s0);
+        }
+        const uint64_t lam = wave_sum_u64(part);
+        const uint64_t bn = wave_max_u64(bott);
+        if (lane == 0) {
+            T[o] = bn;
+            Lambda[o] = lam;
+            if (master) master[o] = (int16_t)chain[best_mu - 1];
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Fitness (Eq. 3-5): one thread per individual.
 // ---------------------------------------------------------------------------
 constexpr uint64_t kScale = 1ull << 50;
@@ -1236,7 +1412,8 @@ __global__ __launch_bounds__(256) void k_fitness(int P, int k_max, const uint64_
 
 // ---------------------------------------------------------------------------
 // Role and slot search (Algorithm 2's inner loop and its brute-force role
-// assignment): one wave per genome.  Lane q < k_max turns cluster q's DP
+// assignment, policy 0; the adapted-SplitWise rule, policy 1, below): one
+// wave per genome.  Lane q < k_max turns cluster q's DP
 // results into a prefill rate and, at the largest slot count b that is
 // feasible and meets the QoS floor, a decode rate b * SCALE / T_b.  A
 // cluster without a decode rate is prefill in every optimum (as decode it
@@ -1258,22 +1435,25 @@ __device__ __forceinline__ bool best_less(const Best &a, const Best &b)
     return a.mask < b.mask;
 }
 
-__global__ __launch_bounds__(64) void k_roles(int P, int k_max, int R,
+__global__ __launch_bounds__(64) void k_roles(int P, int M, int k_max, int R, int policy,
+                                              uint32_t np_tokens, const uint8_t *__restrict__ labels,
                                               const uint64_t *__restrict__ T_all,
                                               const uint64_t *__restrict__ L_all,
                                               uint64_t t_arrival, uint64_t nd, uint64_t lambda_max,
                                               uint8_t *roles_out, uint8_t *slots_out, uint64_t *w,
                                               uint64_t *phase)
 {
-    __shared__ uint64_t rho_p[16], rho_d[16];
-    __shared__ uint32_t bstar[16];
+    __shared__ uint64_t rho_p[256], rho_d[256];
+    __shared__ uint32_t bstar[256];
+    __shared__ uint32_t used[8];
     const int p = blockIdx.x;
     const int lane = threadIdx.x;
-    if (lane < k_max) {
-        const uint64_t *Tq = T_all + ((size_t)p * k_max + lane) * R;
-        const uint64_t *Lq = L_all + ((size_t)p * k_max + lane) * R;
+    if (lane < 8) used[lane] = 0;
+    for (int q = lane; q < k_max; q += kWave) {
+        const uint64_t *Tq = T_all + ((size_t)p * k_max + q) * R;
+        const uint64_t *Lq = L_all + ((size_t)p * k_max + q) * R;
         const uint64_t t0 = Tq[0];
-        rho_p[lane] = t0 != E2_INF64 ? kScale / (t0 > 0 ? t0 : 1) : 0;
+        rho_p[q] = t0 != E2_INF64 ? kScale / (t0 > 0 ? t0 : 1) : 0;
         uint32_t bs = 0;
         uint64_t rd = 0;
         for (int b = R - 1; b >= 1; --b) {
@@ -1284,11 +1464,54 @@ __global__ __launch_bounds__(64) void k_roles(int P, int k_max, int R,
                 break;
             }
         }
-        rho_d[lane] = rd;
-        bstar[lane] = bs;
+        rho_d[q] = rd;
+        bstar[q] = bs;
     }
     __syncthreads();
-    // free clusters (a decode rate), in increasing q; the others are prefill
+    if (policy == 1) {
+        // adapted SplitWise: the token ratio sets the prefill count, the
+        // highest prefill rates (ties to the smaller cluster id) take it
+        for (int d = lane; d < M; d += kWave) {
+            const int lab = labels[(size_t)p * M + d];
+            if (lab < k_max) atomicOr(&used[lab >> 5], 1u << (lab & 31));
+        }
+        __syncthreads();
+        int n_used = 0;
+        for (int i = 0; i < 8; ++i) n_used += __popc(used[i]);
+        int n_p = n_used;
+        if (n_used >= 2) {
+            const uint64_t tot = (uint64_t)np_tokens + nd;
+            n_p = tot ? (int)((2 * (uint64_t)n_used * np_tokens + tot) / (2 * tot))
+                      : (n_used + 1) / 2;
+            n_p = n_p < 1 ? 1 : (n_p > n_used - 1 ? n_used - 1 : n_p);
+        }
+        uint64_t sp = 0, sd = 0;
+        for (int q = lane; q < k_max; q += kWave) {
+            uint32_t dec = 0;
+            if ((used[q >> 5] >> (q & 31)) & 1u) {
+                int rank = 0;
+                for (int k = 0; k < k_max; ++k) {
+                    if (!((used[k >> 5] >> (k & 31)) & 1u)) continue;
+                    rank += rho_p[k] > rho_p[q] || (rho_p[k] == rho_p[q] && k < q);
+                }
+                dec = rank >= n_p;
+                if (dec) sd += rho_d[q];
+                else sp += rho_p[q];
+            }
+            roles_out[(size_t)p * k_max + q] = (uint8_t)dec;
+            slots_out[(size_t)p * k_max + q] = (uint8_t)(dec ? bstar[q] : 0);
+        }
+        sp = wave_sum_u64(sp);
+        sd = wave_sum_u64(sd);
+        if (lane == 0) {
+            const Fit f = fitness_of_rates(sp, sd, t_arrival, nd);
+            w[p] = f.w;
+            phase[p] = f.phase;
+        }
+        return;
+    }
+    // brute force (k_max <= 16): free clusters (a decode rate), in
+    // increasing q; the others are prefill
     uint32_t fmask = 0;
     uint64_t fixed_p = 0;
     for (int q = 0; q < k_max; ++q) {
@@ -1677,7 +1900,8 @@ int e2_dp_slots(int N, int problems)
 
 hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_max,
                                 const E2Genomes &gen, const uint8_t *roles, const E2Work &wk,
-                                uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers)
+                                uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers,
+                                int objective)
 {
     // without roles, every role index of every cluster
     const int n_r = roles ? 0 : t.R;
@@ -1687,9 +1911,15 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
                                                        wk.list, seg, T, Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
-    k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles, n_r,
-                                                      wk.counters, wk.list, seg, wk.rows,
-                                                      wk.tb_global, T, Lambda, master, layers);
+    if (objective == 1)
+        k_dp_ft<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles,
+                                                             wk.counters, wk.list, seg, wk.rows,
+                                                             wk.tb_global, T, Lambda, master,
+                                                             layers);
+    else
+        k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles, n_r,
+                                                          wk.counters, wk.list, seg, wk.rows,
+                                                          wk.tb_global, T, Lambda, master, layers);
     if (wk.ev_end) (void)hipEventRecord(wk.ev_end, s);
     return hipGetLastError();
 }
@@ -1704,13 +1934,14 @@ hipError_t e2_launch_fitness(hipStream_t s, int P, int k_max, const uint64_t *T,
     return hipGetLastError();
 }
 
-hipError_t e2_launch_roles(hipStream_t s, int P, int k_max, int R, const uint64_t *T_all,
+hipError_t e2_launch_roles(hipStream_t s, int P, int M, int k_max, int R, int policy,
+                           uint32_t np_tokens, const uint8_t *labels, const uint64_t *T_all,
                            const uint64_t *L_all, uint64_t t_arrival, uint64_t nd,
                            uint64_t lambda_max, uint8_t *roles_out, uint8_t *slots_out,
                            uint64_t *w, uint64_t *phase)
 {
-    k_roles<<<P, 64, 0, s>>>(P, k_max, R, T_all, L_all, t_arrival, nd, lambda_max, roles_out,
-                             slots_out, w, phase);
+    k_roles<<<P, 64, 0, s>>>(P, M, k_max, R, policy, np_tokens, labels, T_all, L_all, t_arrival,
+                             nd, lambda_max, roles_out, slots_out, w, phase);
     return hipGetLastError();
 }
 

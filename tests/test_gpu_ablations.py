@@ -1,0 +1,148 @@
+"""GPU parity for the two ablations of Sec. 4.2.
+
+The finishing-time objective (e2_solve_partitions_ft, e2_eval_population_ft)
+and the adapted-SplitWise role rule (e2_assign_roles_splitwise) against the
+CPU oracle, bit for bit, on random instances and the named workloads.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2606_03770_amd as e2
+from paper_2606_03770_amd import workload
+
+pytestmark = pytest.mark.gpu
+INF = (1 << 64) - 1
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    e2.lib()
+    return torch, torch.device("cuda:0")
+
+
+def _gpu_ft(torch_dev, wl, labels=None):
+    torch, dev = torch_dev
+    labels = wl.labels if labels is None else labels
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    L = torch.from_numpy(np.ascontiguousarray(labels)).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    sol = e2.e2_solve_partitions(ctx, L, R, objective="finish_time")
+    fit = e2.e2_eval_population(ctx, L, R, wl.fitness_params(), objective="finish_time")
+    torch.cuda.synchronize()
+    out = dict(T=e2.u64(sol["T"]), Lambda=e2.u64(sol["Lambda"]),
+               master=sol["master"].cpu().numpy(), layers=sol["layers"].cpu().numpy())
+    for k in ("w", "phase", "s_p", "s_d"):
+        out[k] = e2.u64(fit[k])
+    return out
+
+
+def _assert_equal(got, want, keys, rows=None, tag=""):
+    for k in keys:
+        g = got[k] if rows is None else got[k][rows]
+        w = want[k]
+        bad = np.argwhere(np.asarray(g != w).reshape(len(w), -1).any(axis=1)).ravel()
+        assert bad.size == 0, f"{tag} {k}: {bad.size} rows differ, first {bad[:5]}"
+
+
+FT_KEYS = ("T", "Lambda", "master", "layers", "w", "phase", "s_p", "s_d")
+
+
+def test_ft_random_parity(torch_dev):
+    rng = np.random.default_rng(4040)
+    for it in range(40):
+        M = int(rng.integers(1, 40))
+        N = int(rng.integers(1, 90))
+        P = int(rng.integers(1, 8))
+        k_max = int(rng.integers(1, 9))
+        kw = dict(mem_lo_layers=float(rng.uniform(0.5, 3)),
+                  mem_hi_layers=float(rng.uniform(3, 60)),
+                  zero_bw_frac=float(rng.choice([0.0, 0.1, 0.3])),
+                  head=bool(rng.integers(0, 2)), layer_var=bool(rng.integers(0, 2)))
+        wl = workload.random_small(7000 + it, M=M, N=N, P=P, k_max=k_max, **kw)
+        labels = wl.labels.copy()
+        labels[rng.uniform(size=labels.shape) < 0.05] = 220
+        print(f"ft {it}: M={M} N={N} P={P} k_max={k_max} {kw}", flush=True)
+        _assert_equal(_gpu_ft(torch_dev, wl, labels), oracle.eval_population_ft(wl, labels),
+                      FT_KEYS, tag=f"ft {it}")
+
+
+def test_ft_long_chain_uses_the_global_split_table(torch_dev):
+    """70 devices x 100 blocks: the chosen master's split points (69 x 100
+    bytes) exceed their LDS copy."""
+    wl = workload.random_small(8, M=70, N=100, P=2, k_max=1, mem_lo_layers=3, mem_hi_layers=30)
+    got = _gpu_ft(torch_dev, wl)
+    _assert_equal(got, oracle.eval_population_ft(wl), FT_KEYS, tag="ft long")
+    assert (got["T"] != INF).any()
+
+
+@pytest.mark.parametrize("name,rows", [("c1_tiny_12dev_32L", None), ("c2_32dev_48L", None),
+                                       ("c3_64dev_80L", None)])
+def test_ft_named_workloads(torch_dev, name, rows):
+    print(f"ft workload {name}", flush=True)
+    wl = workload.make(name)
+    got = _gpu_ft(torch_dev, wl)
+    _assert_equal(got, oracle.eval_population_ft(wl), FT_KEYS, tag=name)
+    # the ablation changes partitions: no cluster is slower end to end than
+    # under Algorithm 1, and some are slower at the bottleneck
+    bn = oracle.eval_population(wl)
+    fin = bn["T"] != INF
+    assert (got["Lambda"][fin] <= bn["Lambda"][fin]).all()
+    assert (got["T"][fin] >= bn["T"][fin]).all() and (got["T"][fin] > bn["T"][fin]).any()
+
+
+def _gpu_splitwise(torch_dev, wl, sm, labels=None):
+    torch, dev = torch_dev
+    labels = wl.labels if labels is None else labels
+    ctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
+    L = torch.from_numpy(np.ascontiguousarray(labels)).to(dev)
+    out = e2.e2_search_roles(ctx, L, wl.fitness_params(), wl.k_max, with_tables=True,
+                             splitwise_np_tokens=oracle.np_tokens(wl))
+    torch.cuda.synchronize()
+    return dict(T_all=e2.u64(out["T_all"]), Lambda_all=e2.u64(out["Lambda_all"]),
+                roles=out["roles"].cpu().numpy(), slots=out["slots"].cpu().numpy(),
+                w=e2.u64(out["w"]), phase=e2.u64(out["phase"]))
+
+
+SW_KEYS = ("T_all", "Lambda_all", "roles", "slots", "w", "phase")
+
+
+def test_splitwise_random_parity(torch_dev):
+    rng = np.random.default_rng(5151)
+    for it in range(30):
+        M = int(rng.integers(1, 40))
+        N = int(rng.integers(1, 70))
+        P = int(rng.integers(1, 8))
+        k_max = int(rng.choice([1, 2, 5, 9, 20, 40]))
+        wl = workload.random_small(8000 + it, M=M, N=N, P=P, k_max=k_max,
+                                   mem_hi_layers=float(rng.uniform(3, 60)))
+        labels = wl.labels.copy()
+        labels[rng.uniform(size=labels.shape) < 0.05] = 250
+        if rng.uniform() < 0.5:
+            wl.min_tps_milli = 0
+        sm = dict(b_max=int(rng.choice([1, 3, 8])), beta_ppm=125_000,
+                  kv_bytes_per_block_slot=int(rng.choice([0, 10**6])))
+        print(f"splitwise {it}: M={M} N={N} P={P} k_max={k_max} {sm}", flush=True)
+        _assert_equal(_gpu_splitwise(torch_dev, wl, sm, labels),
+                      oracle.search_roles(wl, sm, labels, policy="splitwise"), SW_KEYS,
+                      tag=f"sw {it}")
+
+
+@pytest.mark.parametrize("name,rows", [("c2_32dev_48L", None), ("c3_64dev_80L", 192),
+                                       ("c5_256dev_126L_ga", 24)])
+def test_splitwise_named_workloads(torch_dev, name, rows):
+    """Includes the 16384-genome workload (48 clusters per genome, beyond the
+    brute force's reach)."""
+    print(f"splitwise workload {name}", flush=True)
+    wl = workload.make(name)
+    sm = workload.slot_model(wl)
+    got = _gpu_splitwise(torch_dev, wl, sm)
+    if rows is None:
+        _assert_equal(got, oracle.search_roles(wl, sm, policy="splitwise"), SW_KEYS, tag=name)
+        return
+    pick = np.sort(np.random.default_rng(23).choice(wl.population, rows, replace=False))
+    sub = wl.subset(pick)
+    _assert_equal(got, oracle.search_roles(sub, sm, policy="splitwise"), SW_KEYS, rows=pick,
+                  tag=name)
