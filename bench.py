@@ -28,6 +28,10 @@ Printed on one JSON line:
                most 16 clusters per genome) with its decode-slot model: per
                call, every cluster is solved for prefill and for 1..8 decode
                requests in flight, then roles are brute-forced per genome
+  ablations    the two ablations of Sec. 4.2 on the same 1024-genome
+               workload: finishing-time objective vs Algorithm 1, adapted
+               SplitWise roles vs the brute-force search (time per call and
+               how many genomes each side wins)
   two_chromosome  the same measurements for the paper's two-chromosome
                genomes (an ordering of the devices cut into replicas, App. A):
                e2_eval_population_ordered + e2_ga_step_ordered per generation
@@ -440,6 +444,7 @@ def main():
                                         **summary(t2, n, "two_chromosome"))
     if args.genomes == "both" and args.search_steps > 0:
         result["role_search"] = role_search(torch, dev, args.search_steps, args.warmup)
+        result["ablations"] = ablations(torch, dev, args.search_steps, args.warmup)
     if args.cpu_seconds > 0 and head == "labels":
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
@@ -492,6 +497,65 @@ def role_search(torch, dev, steps, warmup):
             "dp_cells_per_s": cells * steps / elapsed,
             "k_dp_avg_ms": dp_ms / n_dp,
             "decode_replicas_at_b_max": int((slots == sm["b_max"]).sum())}
+
+
+def _timed(torch, fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def _key_stats(w_a, ph_a, w_b, ph_b):
+    """Genomes where the first method's (w, phase) is strictly better, equal,
+    or worse than the second's."""
+    a = list(zip(w_a.tolist(), ph_a.tolist()))
+    b = list(zip(w_b.tolist(), ph_b.tolist()))
+    return {"better": sum(x < y for x, y in zip(a, b)), "equal": sum(x == y for x, y in zip(a, b)),
+            "worse": sum(x > y for x, y in zip(a, b))}
+
+
+def ablations(torch, dev, steps, warmup):
+    """The two ablations of Sec. 4.2 on the 1024-genome workload: the
+    finishing-time objective against Algorithm 1's bottleneck (same genomes,
+    roles and fitness), and the adapted-SplitWise role rule against the
+    brute-force role search (same slot model and DP results)."""
+    import oracle
+    wl = workload.make(SEARCH_WORKLOAD)
+    fp = wl.fitness_params()
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    bn = e2.e2_eval_population(ctx, L, R, fp, with_rates=False)
+    ft = e2.e2_eval_population(ctx, L, R, fp, with_rates=False, objective="finish_time")
+    ms_bn = _timed(torch, lambda: e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=bn),
+                   steps, warmup)
+    ms_ft = _timed(torch, lambda: e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=ft,
+                                                       objective="finish_time"), steps, warmup)
+    sm = workload.slot_model(wl)
+    sctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
+    se = e2.e2_search_roles(sctx, L, fp, wl.k_max)
+    sw = e2.e2_search_roles(sctx, L, fp, wl.k_max, splitwise_np_tokens=oracle.np_tokens(wl))
+    ms_sw = _timed(torch, lambda: e2.e2_search_roles(sctx, L, fp, wl.k_max, out=sw,
+                                                    splitwise_np_tokens=oracle.np_tokens(wl)),
+                   steps, warmup)
+    torch.cuda.synchronize()
+    log(f"ablations on {wl.name}: eval {ms_bn:.3f} ms, finishing-time eval {ms_ft:.3f} ms, "
+        f"SplitWise roles {ms_sw:.3f} ms")
+    return {"workload": wl.name, "population": wl.population, "steps": steps,
+            "finish_time": {"call": "e2_eval_population_ft", "ms_per_call": ms_ft,
+                            "bottleneck_ms_per_call": ms_bn,
+                            "bottleneck_vs_finish_time": _key_stats(
+                                e2.u64(bn["w"]), e2.u64(bn["phase"]), e2.u64(ft["w"]),
+                                e2.u64(ft["phase"]))},
+            "splitwise": {"call": "e2_assign_roles_splitwise", "ms_per_call": ms_sw,
+                          "search_vs_splitwise": _key_stats(
+                              e2.u64(se["w"]), e2.u64(se["phase"]), e2.u64(sw["w"]),
+                              e2.u64(sw["phase"]))}}
 
 
 def measure(torch, ctx, stream, bufs, init, step, count, warmup, steps):
