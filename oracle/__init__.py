@@ -87,6 +87,10 @@ def _load() -> ctypes.CDLL:
     lib.oracle_solve_obj.restype = i32
     lib.oracle_dp_pipe_obj.argtypes = [i32, i32, P, P, P, P, P, u64, i32, P, P, P, P, P]
     lib.oracle_dp_pipe_obj.restype = i32
+    lib.oracle_dp_idle.argtypes = [i32, i32, P, P, P, P, P, u64, P, P, P, P]
+    lib.oracle_dp_idle.restype = i32
+    lib.oracle_solve_idle.argtypes = [i32, i32, P, P, P, P, P, u64, i32, i32, P, P, P, P, P, P]
+    lib.oracle_solve_idle.restype = i32
     lib.oracle_rng.argtypes = [u64, u64, u64, u64, u64]
     lib.oracle_rng.restype = u64
     lib.oracle_splitmix_out.argtypes = [u64]
@@ -430,3 +434,42 @@ def dp_pipe_ft(tk, hk, tau_link, memk, W, HB):
     if rc != 0:
         raise OracleError(f"oracle_dp_pipe_obj failed: {rc}")
     return int(T[0]), int(L[0]), int(mu[0]), [int(x) for x in sizes]
+
+
+def dp_idle(tk, hk, tau_full, memk, W, HB):
+    """The idle-device relaxation on one chain: (T, Lambda, mu_star, sizes),
+    sizes 0 for devices that sit out; tau_full[a][b] links chain positions."""
+    lib = _load()
+    tk = _u64(tk)
+    m, N = tk.shape
+    sizes = np.zeros(m, dtype=np.int32)
+    T = np.zeros(1, np.uint64)
+    L = np.zeros(1, np.uint64)
+    mu = np.zeros(1, np.int32)
+    rc = lib.oracle_dp_idle(m, N, _p(tk), _p(_u64(hk)), _p(_u64(tau_full).reshape(m, m)),
+                            _p(_u64(memk)), _p(_u64(W)), int(HB), _p(T), _p(L), _p(mu), _p(sizes))
+    if rc != 0:
+        raise OracleError(f"oracle_dp_idle failed: {rc}")
+    return int(T[0]), int(L[0]), int(mu[0]), [int(x) for x in sizes]
+
+
+def eval_population_idle(wl, labels=None, roles=None):
+    """Quantise, solve under the idle-device relaxation and score."""
+    lib = _load()
+    t, h, tau = quantise(**wl.problem_arrays())
+    labels = np.ascontiguousarray(wl.labels if labels is None else labels, dtype=np.uint8)
+    roles = np.ascontiguousarray(wl.roles if roles is None else roles, dtype=np.uint8)
+    P, M = labels.shape
+    K = int(wl.k_max)
+    T = np.zeros((P, K), dtype=np.uint64)
+    L = np.zeros((P, K), dtype=np.uint64)
+    master = np.zeros((P, K), dtype=np.int16)
+    layers = np.zeros((P, M), dtype=np.uint8)
+    rc = lib.oracle_solve_idle(M, wl.n_layer, _p(t), _p(h), _p(tau), _p(_u64(wl.mem_bytes)),
+                               _p(_u64(wl.layer_bytes)), int(wl.head_bytes), P, K, _p(labels),
+                               _p(roles), _p(T), _p(L), _p(master), _p(layers))
+    if rc != 0:
+        raise OracleError(f"oracle_solve_idle failed: {rc}")
+    sol = dict(T=T, Lambda=L, master=master, layers=layers)
+    sol.update(fitness(T, L, roles, **wl.fitness_params()))
+    return sol

@@ -199,13 +199,16 @@ class Chain:
         sizes[0] = i + 1
         return self.bottleneck(sizes, mu), best, mu, sizes
 
-    def solve_idle_relaxed(self) -> int:
+    def solve_idle_relaxed(self, only_mu=None) -> int:
         """Optimum when devices may hold zero blocks (they then leave the
         pipeline; links join consecutive participating devices).  The master
-        always participates, with its head, even with zero blocks."""
+        always participates, with its head, even with zero blocks.  With
+        only_mu, the optimum for that master position."""
         m, N = self.m, self.N
         best = INF
         for mu in range(1, m + 1):
+            if only_mu is not None and mu != only_mu:
+                continue
             for c in compositions(N, m, min_part=0):
                 used = [k for k in range(m) if c[k] > 0 or k + 1 == mu]
                 v = 0
@@ -228,6 +231,31 @@ class Chain:
                         v = max(v, self.link(a, b))
                 best = min(best, v)
         return best
+
+    def idle_bottleneck(self, sizes, mu: int) -> int:
+        """Bottleneck of a relaxed partition: participants are the devices
+        with blocks and the master (head only when it holds none)."""
+        used = [k for k in range(self.m) if sizes[k] > 0 or k + 1 == mu]
+        start = [0] * self.m
+        s = 0
+        for k in range(self.m):
+            start[k] = s
+            s += sizes[k]
+        v = 0
+        for idx, k in enumerate(used):
+            if sizes[k] > 0:
+                c = self.stage_cost(k, start[k], start[k] + sizes[k] - 1, k + 1 == mu)
+            else:
+                c = self.hk[k] if self.HB <= self.mem[k] else INF
+            if c == INF:
+                return INF
+            v = max(v, c)
+            if idx >= 1:
+                lt = self.link(used[idx - 1], k)
+                if lt == INF:
+                    return INF
+                v = max(v, lt)
+        return v
 
     def link(self, a: int, b: int) -> int:
         """Link time between chain positions a < b.  Only adjacent positions

@@ -1091,3 +1091,204 @@ static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
     free(Wr);
     return ORC_OK;
 }
+
+/* ---------------------------------------------------------------------- */
+/* The idle-device relaxation (R2): devices may hold zero blocks.          */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * DP over a chain where a device may hold no block and then leaves the
+ * pipeline; links join consecutive participating devices (tau_full gives
+ * every ordered pair of chain positions); the master always participates,
+ * with its head, and may hold no block (its stage is then the head alone).
+ * For a master mu, with x = blocks placed so far (0..N):
+ *   A_k(x)   = min over allowed predecessors k' (ascending, "none" first)
+ *              of max(E_k'(x), tau(k', k)); "none" (k is the first
+ *              participant) stands for E(0) = 0, E(x > 0) = INF, tau 0;
+ *              allowed: k < mu and k = mu: none or 1..k-1; k > mu: mu..k-1
+ *   E_k(x)   = min over j ascending in device k's window of
+ *              max(A_k(j), cost_k(j, x-1)) (blocks j..x-1 on device k, the
+ *              head on the master), then for k = mu the empty stage
+ *              max(A_mu(x), head) when the head bytes fit (strict <, so a
+ *              stage with blocks wins ties)
+ *   T_mu     = min over k >= mu of E_k(N), the smallest k on ties
+ * and mu* is the smallest master with the least T_mu.  Outputs as
+ * oracle_dp_pipe: sizes[k] = 0 for devices that sit out, *Lambda = stage
+ * times of the participants (+ head) + links between consecutive ones.
+ */
+int oracle_dp_idle(int m, int N, const uint64_t *tk, const uint64_t *hk, const uint64_t *tau_full,
+                   const uint64_t *memk, const uint64_t *W, uint64_t HB, uint64_t *T,
+                   uint64_t *Lambda, int *mu_star, int *sizes)
+{
+    *T = INF;
+    *Lambda = INF;
+    *mu_star = 0;
+    for (int k = 0; k < m; k++) sizes[k] = 0;
+    if (m < 1 || N < 1) return ORC_EINVAL;
+    const int X = N + 1;
+    uint64_t *pt = malloc(sizeof(uint64_t) * (size_t)m * X);
+    uint64_t *pw = malloc(sizeof(uint64_t) * (size_t)X);
+    uint64_t *E = malloc(sizeof(uint64_t) * (size_t)m * X);
+    uint64_t *A = malloc(sizeof(uint64_t) * (size_t)m * X);
+    int *Ek = malloc(sizeof(int) * (size_t)m * X);  /* predecessor of A_k(x): -1 none */
+    int *Ej = malloc(sizeof(int) * (size_t)m * X);  /* stage start j, or x for an empty stage */
+    if (!pt || !pw || !E || !A || !Ek || !Ej) {
+        free(pt); free(pw); free(E); free(A); free(Ek); free(Ej);
+        return ORC_ENOMEM;
+    }
+    for (int k = 0; k < m; k++) {
+        pt[(size_t)k * X] = 0;
+        for (int n = 0; n < N; n++) pt[(size_t)k * X + n + 1] = pt[(size_t)k * X + n] + tk[(size_t)k * N + n];
+    }
+    pw[0] = 0;
+    for (int n = 0; n < N; n++) pw[n + 1] = pw[n] + W[n];
+
+    uint64_t best = INF;
+    int best_mu = 0, best_last = -1;
+    for (int pass = 0; pass < 2; pass++) {
+        /* pass 0 finds mu*; pass 1 rebuilds its tables for the back tracing */
+        int mu_lo = pass ? best_mu : 1, mu_hi = pass ? best_mu : m;
+        if (pass && best == INF) break;
+        for (int mu = mu_lo; mu <= mu_hi; mu++) {
+            for (int k = 1; k <= m; k++) {
+                uint64_t *Ak = A + (size_t)(k - 1) * X;
+                uint64_t *Erow = E + (size_t)(k - 1) * X;
+                int *pk = Ek + (size_t)(k - 1) * X, *pj = Ej + (size_t)(k - 1) * X;
+                const int none_ok = k <= mu;
+                const int kp_lo = k > mu ? mu : 1;
+                for (int x = 0; x <= N; x++) {
+                    uint64_t a = INF;
+                    int arg = -2;
+                    if (none_ok && x == 0) {
+                        a = 0;
+                        arg = -1;
+                    }
+                    for (int kp = kp_lo; kp <= k - 1; kp++) {
+                        uint64_t e = E[(size_t)(kp - 1) * X + x];
+                        uint64_t tl = tau_full[(size_t)(kp - 1) * m + (k - 1)];
+                        if (e == INF || tl == INF) continue;
+                        uint64_t v = max2(e, tl);
+                        if (v < a) {
+                            a = v;
+                            arg = kp;
+                        }
+                    }
+                    Ak[x] = a;
+                    pk[x] = arg;
+                }
+                const uint64_t *ptk = pt + (size_t)(k - 1) * X;
+                const uint64_t head_t = (k == mu) ? hk[k - 1] : 0;
+                const uint64_t head_b = (k == mu) ? HB : 0;
+                for (int x = 0; x <= N; x++) {
+                    uint64_t e = INF;
+                    int jj = -1;
+                    for (int j = 0; j < x; j++) {
+                        if (Ak[j] == INF) continue;
+                        if (pw[x] - pw[j] + head_b > memk[k - 1]) continue;
+                        uint64_t v = max2(Ak[j], ptk[x] - ptk[j] + head_t);
+                        if (v < e) {
+                            e = v;
+                            jj = j;
+                        }
+                    }
+                    if (k == mu && Ak[x] != INF && HB <= memk[k - 1]) {
+                        uint64_t v = max2(Ak[x], hk[k - 1]);
+                        if (v < e) {
+                            e = v;
+                            jj = x;
+                        }
+                    }
+                    Erow[x] = e;
+                    pj[x] = jj;
+                }
+            }
+            uint64_t tmu = INF;
+            int last = -1;
+            for (int k = mu; k <= m; k++) {
+                uint64_t v = E[(size_t)(k - 1) * X + N];
+                if (v < tmu) {
+                    tmu = v;
+                    last = k;
+                }
+            }
+            if (!pass && tmu < best) {
+                best = tmu;
+                best_mu = mu;
+            }
+            if (pass) best_last = last;
+        }
+    }
+    if (best != INF) {
+        /* back tracing from (best_last, N) */
+        int k = best_last, x = N;
+        int prev_k = -1;
+        uint64_t lam = 0;
+        while (k >= 1) {
+            int j = Ej[(size_t)(k - 1) * X + x];
+            sizes[k - 1] = x - j;
+            lam += pt[(size_t)(k - 1) * X + x] - pt[(size_t)(k - 1) * X + j];
+            if (k == best_mu) lam += hk[k - 1];
+            if (prev_k > 0) lam += tau_full[(size_t)(k - 1) * m + (prev_k - 1)];
+            int kp = Ek[(size_t)(k - 1) * X + j];
+            prev_k = k;
+            k = kp;     /* -1: k was the first participant */
+            x = j;
+        }
+        *T = best;
+        *Lambda = lam;
+        *mu_star = best_mu;
+    }
+    free(pt); free(pw); free(E); free(A); free(Ek); free(Ej);
+    return ORC_OK;
+}
+
+/*
+ * Population solve under the idle-device relaxation: as oracle_solve, with
+ * links between any two chain devices from tau; m > N is allowed.
+ */
+int oracle_solve_idle(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
+                      const uint64_t *mem, const uint64_t *W, uint64_t HB, int P, int k_max,
+                      const uint8_t *labels, const uint8_t *roles, uint64_t *T, uint64_t *Lambda,
+                      int16_t *master, uint8_t *layers)
+{
+    if (M < 1 || M > 256 || N < 1 || N > 255 || P < 0 || k_max < 1 || k_max > 255)
+        return ORC_EINVAL;
+    int chain[256], sizes[256];
+    uint64_t hk[256], mk[256];
+    uint64_t *tk = malloc(sizeof(uint64_t) * (size_t)M * N);
+    uint64_t *tf = malloc(sizeof(uint64_t) * (size_t)M * M);
+    if (!tk || !tf) { free(tk); free(tf); return ORC_ENOMEM; }
+    for (int p = 0; p < P; p++) {
+        for (int d = 0; d < M; d++) layers[(size_t)p * M + d] = 0;
+        for (int q = 0; q < k_max; q++) {
+            size_t o = (size_t)p * k_max + q;
+            T[o] = INF;
+            Lambda[o] = INF;
+            master[o] = -1;
+            int m = 0;
+            for (int d = 0; d < M; d++)
+                if (labels[(size_t)p * M + d] == q) chain[m++] = d;
+            if (m == 0) continue;
+            int r = roles[o] != 0;
+            for (int a = 0; a < m; a++) {
+                memcpy(tk + (size_t)a * N, t + ((size_t)r * M + chain[a]) * N, sizeof(uint64_t) * N);
+                hk[a] = h[r * M + chain[a]];
+                mk[a] = mem[chain[a]];
+                for (int b = 0; b < m; b++)
+                    tf[(size_t)a * m + b] = a == b ? 0 : tau[((size_t)r * M + chain[a]) * M + chain[b]];
+            }
+            uint64_t Tv, Lv;
+            int mu;
+            int rc = oracle_dp_idle(m, N, tk, hk, tf, mk, W, HB, &Tv, &Lv, &mu, sizes);
+            if (rc) { free(tk); free(tf); return rc; }
+            if (Tv == INF) continue;
+            T[o] = Tv;
+            Lambda[o] = Lv;
+            master[o] = (int16_t)chain[mu - 1];
+            for (int a = 0; a < m; a++) layers[(size_t)p * M + chain[a]] = (uint8_t)sizes[a];
+        }
+    }
+    free(tk);
+    free(tf);
+    return ORC_OK;
+}
