@@ -395,6 +395,29 @@ int e2_eval_population_ft(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
                           uint64_t *s_p, uint64_t *s_d);
 
 /*
+ * The idle-device relaxation: as e2_solve_partitions / e2_eval_population,
+ * but a device of a cluster may hold no block and then sits out of the
+ * pipeline; links join consecutive participating devices (tau between any
+ * two devices of the cluster); the master always participates, with its
+ * head, possibly holding no block (its stage is then the head alone, which
+ * must fit its memory).  Clusters with more devices than blocks are solved.
+ * Per master mu and x blocks placed, A_k(x) = min over the allowed
+ * predecessors k' of max(E_k'(x), tau(k', k)) and E_k(x) = min over stage
+ * starts j of max(A_k(j), stage time) (ties: the smallest k', the smallest
+ * j, a stage with blocks before the empty one, the smallest last device,
+ * the smallest master).  layers[] is 0 for devices that sit out; Lambda
+ * sums the participants' stage times (+ head) and links.  Under this
+ * relaxation adding a device never raises T.
+ */
+int e2_solve_partitions_idle(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                             const uint8_t *labels, const uint8_t *roles, uint64_t *T,
+                             uint64_t *Lambda, int16_t *master, uint8_t *layers);
+int e2_eval_population_idle(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                            const uint8_t *labels, const uint8_t *roles,
+                            const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
+                            uint64_t *s_p, uint64_t *s_d);
+
+/*
  * Profiling of the DP kernel (the dominant cost of e2_solve_partitions and
  * e2_eval_population), for benchmarks and profilers.
  *

@@ -17,6 +17,7 @@ tensors on ROCm) and streams.  The wrappers keep the C names:
     e2_search_roles(..., splitwise_np_tokens=NP)     the ablations of Sec. 4.2:
     e2_solve_partitions(..., objective="finish_time")  adapted-SplitWise roles,
     e2_eval_population(..., objective="finish_time")   finishing-time objective
+    e2_solve_partitions / e2_eval_population(..., objective="idle")  idle devices
 
 `problem` is a dict with the fields of e2_problem (numpy arrays), as
 returned by workload.Workload.problem_arrays().  64-bit unsigned outputs
@@ -44,7 +45,8 @@ EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitio
             "e2_eval_population", "e2_ga_step", "e2_solve_partitions_ordered",
             "e2_eval_population_ordered", "e2_ga_step_ordered", "e2_ctx_create_slots",
             "e2_search_roles", "e2_assign_roles_splitwise", "e2_solve_partitions_ft",
-            "e2_eval_population_ft", "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror")
+            "e2_eval_population_ft", "e2_solve_partitions_idle", "e2_eval_population_idle",
+            "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror")
 
 
 class E2Error(RuntimeError):
@@ -136,6 +138,11 @@ def lib() -> ctypes.CDLL:
     L.e2_eval_population_ft.argtypes = [vp, vp, i32, i32, vp, vp,
                                         ctypes.POINTER(e2_fitness_params), vp, vp, vp, vp]
     L.e2_eval_population_ft.restype = ctypes.c_int
+    L.e2_solve_partitions_idle.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, vp, vp]
+    L.e2_solve_partitions_idle.restype = ctypes.c_int
+    L.e2_eval_population_idle.argtypes = [vp, vp, i32, i32, vp, vp,
+                                          ctypes.POINTER(e2_fitness_params), vp, vp, vp, vp]
+    L.e2_eval_population_idle.restype = ctypes.c_int
     L.e2_ctx_dp_timing.argtypes = [vp, i32]
     L.e2_ctx_dp_timing.restype = ctypes.c_int
     L.e2_ctx_dp_elapsed.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
@@ -272,7 +279,8 @@ def _ptr(t):
 def e2_solve_partitions(ctx: Context, labels, roles, stream=None, out: Optional[dict] = None,
                         objective: str = "bottleneck"):
     """Returns dict T, Lambda (int64 bits of u64) [P][k_max], master int16 [P][k_max],
-    layers uint8 [P][M].  objective "finish_time" calls e2_solve_partitions_ft."""
+    layers uint8 [P][M].  objective "finish_time" calls e2_solve_partitions_ft, "idle"
+    e2_solve_partitions_idle."""
     torch = _torch()
     P, M = labels.shape
     k_max = roles.shape[1]
@@ -284,7 +292,8 @@ def e2_solve_partitions(ctx: Context, labels, roles, stream=None, out: Optional[
                    Lambda=torch.empty((P, k_max), dtype=torch.int64, device=dev),
                    master=torch.empty((P, k_max), dtype=torch.int16, device=dev),
                    layers=torch.empty((P, M), dtype=torch.uint8, device=dev))
-    name = {"bottleneck": "e2_solve_partitions", "finish_time": "e2_solve_partitions_ft"}[objective]
+    name = {"bottleneck": "e2_solve_partitions", "finish_time": "e2_solve_partitions_ft",
+            "idle": "e2_solve_partitions_idle"}[objective]
     _check(getattr(lib(), name)(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
                                 _ptr(roles), _ptr(out["T"]), _ptr(out["Lambda"]),
                                 _ptr(out["master"]), _ptr(out["layers"])), name)
@@ -295,7 +304,7 @@ def e2_eval_population(ctx: Context, labels, roles, fitness: dict, stream=None,
                        with_rates: bool = True, out: Optional[dict] = None,
                        objective: str = "bottleneck"):
     """Returns dict w, phase (and s_p, s_d) as int64 bits of u64, shape [P].
-    objective "finish_time" calls e2_eval_population_ft."""
+    objective "finish_time" calls e2_eval_population_ft, "idle" e2_eval_population_idle."""
     torch = _torch()
     P = labels.shape[0]
     k_max = roles.shape[1]
@@ -307,7 +316,8 @@ def e2_eval_population(ctx: Context, labels, roles, fitness: dict, stream=None,
         out = {k: torch.empty(P, dtype=torch.int64, device=dev) for k in names}
     fp = e2_fitness_params(int(fitness["t_arrival_ns"]), int(fitness["nd_tokens"]),
                            int(fitness["min_tps_milli"]))
-    name = {"bottleneck": "e2_eval_population", "finish_time": "e2_eval_population_ft"}[objective]
+    name = {"bottleneck": "e2_eval_population", "finish_time": "e2_eval_population_ft",
+            "idle": "e2_eval_population_idle"}[objective]
     _check(getattr(lib(), name)(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
                                 _ptr(roles), ctypes.byref(fp), _ptr(out["w"]),
                                 _ptr(out["phase"]), _ptr(out.get("s_p")),

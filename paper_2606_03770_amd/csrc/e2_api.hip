@@ -113,21 +113,24 @@ int alloc_scratch(Scratch &sc, hipStream_t s, size_t bytes)
 
 // Lay out counters, the problem list and the split-point fallback.
 size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_bytes,
-                  int n_r = 1)
+                  int n_r = 1, int objective = 0)
 {
     const size_t problems = (size_t)P * k_max * n_r;
-    *slots = e2_dp_slots(ctx->N, (int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX));
+    const int np = (int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX);
+    *slots = objective == 2 ? e2_dp_idle_slots(np) : e2_dp_slots(ctx->N, np);
     const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
     // the global split-point table is needed only when some chain's split
     // points (m - 1 rows of at most N cells) can exceed their LDS copy
     const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_lds_tb_cells(ctx->N);
     *tb_bytes = need_tb ? (size_t)(*slots) * ctx->N * ctx->N : 0;
+    const size_t idle = objective == 2 ? (size_t)(*slots) * e2_dp_idle_bytes(ctx->M, ctx->N) : 0;
     return align256(32) + align256(problems * 4 * 4) +
-           align256((size_t)(*slots) * e2_dp_row_words(ctx->N) * 8) + align256(*tb_bytes);
+           align256((size_t)(*slots) * e2_dp_row_words(ctx->N) * 8) + align256(*tb_bytes) +
+           align256(idle);
 }
 
 void carve_work(void *base, e2_ctx *ctx, int P, int k_max, int slots, size_t tb_bytes,
-                E2Work *wk, int n_r = 1)
+                E2Work *wk, int n_r = 1, int objective = 0)
 {
     char *p = static_cast<char *>(base);
     wk->counters = reinterpret_cast<uint32_t *>(p);
@@ -137,6 +140,9 @@ void carve_work(void *base, e2_ctx *ctx, int P, int k_max, int slots, size_t tb_
     wk->rows = reinterpret_cast<uint64_t *>(p);
     p += align256((size_t)slots * e2_dp_row_words(ctx->N) * 8);
     wk->tb_global = tb_bytes ? reinterpret_cast<uint8_t *>(p) : nullptr;
+    p += align256(tb_bytes);
+    wk->idle_stride = objective == 2 ? e2_dp_idle_bytes(ctx->M, ctx->N) : 0;
+    wk->idle = objective == 2 ? reinterpret_cast<uint8_t *>(p) : nullptr;
     wk->n_slots = slots;
     wk->ev_begin = wk->ev_end = nullptr;
     if (ctx->dp_events && ctx->dp_events_used < ctx->dp_event_pairs) {
@@ -321,6 +327,8 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
     // largest prefix sum (+ head time) per role and device: every shifted
     // prefix sum of a chain stays below 2^53 when these and its link times
     // are below 2^45
+    std::vector<uint8_t> hfit((size_t)M);
+    for (int d = 0; d < M; ++d) hfit[d] = prob->head_bytes <= prob->mem_bytes[d];
     std::vector<uint64_t> vtot((size_t)R * M, 0);
     for (int r = 0; r < R; ++r)
         for (int d = 0; d < M; ++d)
@@ -337,7 +345,8 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
                     {winR.data(), winR.size(), nullptr},       {prefR.data(), prefR.size() * 8, nullptr},
                     {minwin.data(), minwin.size(), nullptr},   {minwinR.data(), minwinR.size(), nullptr},
                     {cap0.data(), cap0.size(), nullptr},       {capH.data(), capH.size(), nullptr},
-                    {vmax.data(), vmax.size() * 8, nullptr},   {vtot.data(), vtot.size() * 8, nullptr}};
+                    {vmax.data(), vmax.size() * 8, nullptr},   {vtot.data(), vtot.size() * 8, nullptr},
+                    {hfit.data(), hfit.size(), nullptr}};
     size_t total = 0;
     for (const Part &pt : parts) total += align256(pt.bytes);
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
@@ -380,6 +389,7 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
     tb.capH = reinterpret_cast<const uint8_t *>(parts[9].dst);
     tb.vmax = reinterpret_cast<const uint64_t *>(parts[10].dst);
     tb.vtot = reinterpret_cast<const uint64_t *>(parts[11].dst);
+    tb.hfit = reinterpret_cast<const uint8_t *>(parts[12].dst);
     tb.M = M;
     tb.N = N;
     tb.R = R;
@@ -495,11 +505,11 @@ int solve_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Geno
     hipStream_t s = as_stream(stream);
     int slots;
     size_t tbb;
-    const size_t bytes = work_bytes(ctx, P, k_max, &slots, &tbb);
+    const size_t bytes = work_bytes(ctx, P, k_max, &slots, &tbb, 1, objective);
     Scratch sc;
     if ((rc = alloc_scratch(sc, s, bytes))) return rc;
     E2Work wk;
-    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk);
+    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk, 1, objective);
     const hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, roles, wk, T,
                                               Lambda, master, layers, objective);
     return e == hipSuccess ? E2_OK : E2_EHIP;
@@ -519,12 +529,12 @@ int eval_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genom
     hipStream_t s = as_stream(stream);
     int slots;
     size_t tbb;
-    const size_t wb = work_bytes(ctx, P, k_max, &slots, &tbb);
+    const size_t wb = work_bytes(ctx, P, k_max, &slots, &tbb, 1, objective);
     const size_t tl = align256((size_t)P * k_max * 8);
     Scratch sc;
     if ((rc = alloc_scratch(sc, s, wb + 2 * tl))) return rc;
     E2Work wk;
-    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk);
+    carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk, 1, objective);
     uint64_t *Ts = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
     uint64_t *Ls = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb + tl);
     hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, roles, wk, Ts, Ls,
@@ -685,6 +695,25 @@ int e2_solve_partitions_ft(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
     if (P > 0 && !labels) return E2_EINVAL;
     const E2Genomes gen = {labels, nullptr, nullptr};
     return solve_impl(ctx, stream, P, k_max, gen, roles, T, Lambda, master, layers, 1);
+}
+
+int e2_solve_partitions_idle(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                             const uint8_t *labels, const uint8_t *roles, uint64_t *T,
+                             uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    if (P > 0 && !labels) return E2_EINVAL;
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    return solve_impl(ctx, stream, P, k_max, gen, roles, T, Lambda, master, layers, 2);
+}
+
+int e2_eval_population_idle(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                            const uint8_t *labels, const uint8_t *roles,
+                            const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
+                            uint64_t *s_p, uint64_t *s_d)
+{
+    if (P > 0 && !labels) return E2_EINVAL;
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    return eval_impl(ctx, stream, P, k_max, gen, roles, fp, w, phase, s_p, s_d, 2);
 }
 
 int e2_eval_population_ft(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,

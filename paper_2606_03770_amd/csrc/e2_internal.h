@@ -31,6 +31,7 @@ struct E2Tables {
     const uint64_t *vmax;  // [R][M] largest cost of a fitting stage (+ head time when it
                            //   holds the head bytes) per role and device
     const uint64_t *vtot;  // [R][M] total time of all blocks + head time per role and device
+    const uint8_t *hfit;   // [M] 1 when the head bytes alone fit the device
     int M;
     int N;
     int R;      // role indices
@@ -58,6 +59,8 @@ struct E2Work {
     uint64_t *rows;      // [n_slots][pool + 2 (N+1)] per-wave DP rows
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
     int n_slots;         // waves of the DP kernel
+    uint8_t *idle;       // idle-device relaxation: per wave, rows E [M][N+1] u64, their
+    size_t idle_stride;  //   predecessors [M][N+1] u16 and stage starts [M][N+1] u8
     hipEvent_t ev_begin; // recorded just before / after the DP kernel, or null
     hipEvent_t ev_end;
 };
@@ -70,6 +73,9 @@ int e2_dp_pool_cells(int N);
 int e2_dp_lds_tb_cells(int N);
 size_t e2_dp_row_words(int N);
 size_t e2_dp_lds_bytes(int N);
+// Waves and per-wave bytes of the idle-device relaxation's DP kernel.
+int e2_dp_idle_slots(int problems);
+size_t e2_dp_idle_bytes(int M, int N);
 
 // The genomes of a population: labels [P][M] (cluster id per device), or,
 // when labels is null, two-chromosome genomes: an ordering order [P][M] and
@@ -85,8 +91,8 @@ struct E2Genomes {
 // solved for every role index (R <= 16, P < 2^20) and T, Lambda are
 // [P][k_max][R]; master and layers must then be null.
 // objective 1: the finishing-time variant (least end-to-end time per
-// cluster; T reports that partition's bottleneck), label or ordered genomes
-// with roles only.
+// cluster; T reports that partition's bottleneck); objective 2: the
+// idle-device relaxation (wk.idle must be set).  Both with roles only.
 hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_max,
                                 const E2Genomes &gen, const uint8_t *roles, const E2Work &wk,
                                 uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers,

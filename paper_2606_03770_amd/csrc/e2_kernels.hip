@@ -138,7 +138,7 @@ __device__ __forceinline__ E2Tables mem_view(const E2Tables &tb, int r)
 // [P][k_max][R] and list codes (p << 12) | (q << 4) | r.
 __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_max,
                                                       E2Genomes gen, const uint8_t *roles,
-                                                      int n_r, uint32_t *counters,
+                                                      int n_r, int relaxed, uint32_t *counters,
                                                       uint32_t *list, size_t seg_cap,
                                                       uint64_t *T, uint64_t *Lambda,
                                                       int16_t *master, uint8_t *layers)
@@ -237,9 +237,11 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             if (p < P && q < k_max) {
                 const uint32_t pk = packed[g][q];
                 const uint32_t m = pk >> 16, csum = pk & 0xFFFF;
-                feas = m >= 1 && m <= (uint32_t)N && csum >= (uint32_t)N && mincap[g][q] >= 1 &&
-                       ((hmask[g][q >> 5] >> (q & 31)) & 1u) &&
-                       !((bad[g][q >> 5] >> (q & 31)) & 1u);
+                // the checks hold for chains whose every device takes a
+                // block; with idle devices allowed, every non-empty cluster
+                feas = m >= 1 && !((bad[g][q >> 5] >> (q & 31)) & 1u) &&
+                       (relaxed || (m <= (uint32_t)N && csum >= (uint32_t)N &&
+                                    mincap[g][q] >= 1 && ((hmask[g][q >> 5] >> (q & 31)) & 1u)));
                 cls = size_class((int)m);
                 if (!feas) {
                     const size_t o = n_r > 0 ? ((size_t)p * k_max + q) * n_r + ri
@@ -1350,6 +1352,179 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
 }
 
 // ---------------------------------------------------------------------------
+// The idle-device relaxation: a device may hold no block and then sits out;
+// links join consecutive participants (any pair of chain devices); the
+// master always takes part, with its head, possibly with no block.  For a
+// master mu and x = blocks placed so far:
+//   A_k(x) = min over allowed predecessors k' (ascending; "none", meaning k
+//            is the first participant, stands for 0 at x = 0) of
+//            max(E_k'(x), tau(k', k)); k <= mu: none or 1..k-1, k > mu:
+//            mu..k-1, so that every path past the master holds it
+//   E_k(x) = min over j ascending in the window of max(A_k(j), cost(j..x-1))
+//            then, for the master, the empty stage max(A_mu(x), head)
+//   T_mu   = min over k >= mu of E_k(N), the smallest k on ties
+// One wave per problem, lanes over x; A_k in LDS, the E rows (and, on the
+// second pass for the best master, the predecessors and stage starts) in
+// the wave's global region.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genomes gen,
+                                                const uint8_t *__restrict__ roles,
+                                                uint32_t *counters,
+                                                const uint32_t *__restrict__ list, size_t seg_cap,
+                                                uint8_t *idle, size_t idle_stride, uint64_t *T,
+                                                uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    extern __shared__ uint64_t A[];  // [N+1]
+    __shared__ uint8_t chain[256];
+    __shared__ uint8_t sizes[256];
+    __shared__ uint32_t job;
+    const int lane = threadIdx.x;
+    const int M = tb.M, N = tb.N, X = N + 1;
+    uint64_t *E = reinterpret_cast<uint64_t *>(idle + (size_t)blockIdx.x * idle_stride);
+    uint16_t *Ek = reinterpret_cast<uint16_t *>(E + (size_t)M * X);
+    uint8_t *Ej = reinterpret_cast<uint8_t *>(Ek + (size_t)M * X);
+    const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
+    const uint32_t n_jobs = n0 + n1 + n2 + n3;
+    for (;;) {
+        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
+        __syncthreads();
+        uint32_t idx = job;
+        __syncthreads();
+        if (idx >= n_jobs) break;
+        int cls = 0;
+        if (idx >= n0) { idx -= n0; cls = 1;
+            if (idx >= n1) { idx -= n1; cls = 2;
+                if (idx >= n2) { idx -= n2; cls = 3; } } }
+        const uint32_t code = list[(size_t)cls * seg_cap + idx];
+        const int p = (int)(code >> 8);
+        const int q = (int)(code & 0xFF);
+        const int m = build_chain(gen, p, q, k_max, M, lane, chain);
+        __syncthreads();
+        const int r = roles[(size_t)p * k_max + q] != 0;
+        const size_t o = (size_t)p * k_max + q;
+        const E2Tables tv = mem_view(tb, r);
+        uint64_t best = E2_INF64;
+        int best_mu = 0, last = 0;
+        for (int pass = 0; pass < 2; ++pass) {
+            if (pass == 1 && best == E2_INF64) break;
+            const int mu_lo = pass ? best_mu : 1, mu_hi = pass ? best_mu : m;
+            for (int mu = mu_lo; mu <= mu_hi; ++mu) {
+                for (int k = 1; k <= m; ++k) {
+                    const int c = uni(chain[k - 1]);
+                    const bool none_ok = k <= mu;
+                    const int kp_lo = k > mu ? mu : 1;
+                    for (int x = lane; x <= N; x += kWave) {
+                        uint64_t a = (none_ok && x == 0) ? 0 : E2_INF64;
+                        int arg = 0;
+                        for (int kp = kp_lo; kp <= k - 1; ++kp) {
+                            const uint64_t e = E[(size_t)(kp - 1) * X + x];
+                            const uint64_t tl = link_tau_u(tv, r, uni(chain[kp - 1]), c);
+                            if (e == E2_INF64 || tl == E2_INF64) continue;
+                            const uint64_t v = umax64(e, tl);
+                            if (v < a) {
+                                a = v;
+                                arg = kp;
+                            }
+                        }
+                        A[x] = a;
+                        if (pass) Ek[(size_t)(k - 1) * X + x] = (uint16_t)arg;
+                    }
+                    __syncthreads();
+                    const int f = (k == mu);
+                    const uint64_t *pr = pref_row(tv, r, c);
+                    const uint8_t *wr = win_row(tv, f, c);
+                    const uint64_t hadd = f ? uni64(tv.head[r * M + c]) : 0;
+                    const bool empty_ok = f && tv.hfit[c];
+                    for (int x = lane; x <= N; x += kWave) {
+                        uint64_t e = E2_INF64;
+                        int jj = 0;
+                        if (x >= 1) {
+                            const int w = wr[x - 1];
+                            if (w != E2_NO_START) {
+                                const uint64_t end = pr[x] + hadd;
+                                for (int j = w; j < x; ++j) {
+                                    const uint64_t aj = A[j];
+                                    if (aj == E2_INF64) continue;
+                                    const uint64_t v = umax64(aj, end - pr[j]);
+                                    if (v < e) {
+                                        e = v;
+                                        jj = j;
+                                    }
+                                }
+                            }
+                        }
+                        if (empty_ok && A[x] != E2_INF64) {
+                            const uint64_t v = umax64(A[x], hadd);
+                            if (v < e) {
+                                e = v;
+                                jj = x;
+                            }
+                        }
+                        E[(size_t)(k - 1) * X + x] = e;
+                        if (pass) Ej[(size_t)(k - 1) * X + x] = (uint8_t)jj;
+                    }
+                    __builtin_amdgcn_s_waitcnt(0);
+                    __threadfence_block();
+                    __syncthreads();
+                }
+                uint64_t tmu = E2_INF64;
+                int lk = 0;
+                for (int k = mu; k <= m; ++k) {
+                    const uint64_t v = E[(size_t)(k - 1) * X + N];
+                    if (v < tmu) {
+                        tmu = v;
+                        lk = k;
+                    }
+                }
+                if (pass == 0 && tmu < best) {
+                    best = tmu;
+                    best_mu = mu;
+                }
+                if (pass == 1) last = lk;
+                __syncthreads();
+            }
+        }
+        if (best == E2_INF64) {
+            if (lane == 0) {
+                T[o] = E2_INF64;
+                Lambda[o] = E2_INF64;
+                if (master) master[o] = -1;
+            }
+            if (layers)
+                for (int k = lane; k < m; k += kWave) layers[(size_t)p * M + chain[k]] = 0;
+            __syncthreads();
+            continue;
+        }
+        for (int k = lane; k < m; k += kWave) sizes[k] = 0;
+        __syncthreads();
+        if (lane == 0) {
+            // back tracing from (last, N): participants in reverse order
+            int k = last, x = N, next = 0;
+            uint64_t lam = 0;
+            while (k >= 1) {
+                const int c = chain[k - 1];
+                const int j = Ej[(size_t)(k - 1) * X + x];
+                sizes[k - 1] = (uint8_t)(x - j);
+                const uint64_t *pr = pref_row(tv, r, c);
+                lam += pr[x] - pr[j];
+                if (k == best_mu) lam += tv.head[r * M + c];
+                if (next) lam += link_tau(tv, r, c, chain[next - 1]);
+                next = k;
+                k = Ek[(size_t)(k - 1) * X + j];
+                x = j;
+            }
+            T[o] = best;
+            Lambda[o] = lam;
+            if (master) master[o] = (int16_t)chain[best_mu - 1];
+        }
+        __syncthreads();
+        if (layers)
+            for (int k = lane; k < m; k += kWave) layers[(size_t)p * M + chain[k]] = sizes[k];
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Fitness (Eq. 3-5): one thread per individual.
 // ---------------------------------------------------------------------------
 constexpr uint64_t kScale = 1ull << 50;
@@ -1853,6 +2028,18 @@ int e2_dp_pool_cells(int N)
     return max(best, kLdsTbCells);
 }
 
+int e2_dp_idle_slots(int problems)
+{
+    // every wave holds M x (N+1) rows in its global region: a bounded grid
+    const int cap = 1024;
+    return problems < cap ? (problems > 0 ? problems : 1) : cap;
+}
+
+size_t e2_dp_idle_bytes(int M, int N)
+{
+    return ((size_t)M * (N + 1) * 11 + 255) & ~(size_t)255;
+}
+
 int e2_dp_lds_tb_cells(int N)
 {
     (void)N;
@@ -1907,11 +2094,17 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
     const int n_r = roles ? 0 : t.R;
     const size_t seg = (size_t)P * k_max * (n_r ? n_r : 1);
     k_init<<<1, 64, 0, s>>>(wk.counters);
-    k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, roles, n_r, wk.counters,
-                                                       wk.list, seg, T, Lambda, master, layers);
+    k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, roles, n_r,
+                                                       objective == 2, wk.counters, wk.list, seg,
+                                                       T, Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
-    if (objective == 1)
+    if (objective == 2)
+        k_dp_idle<<<wk.n_slots, 64, (size_t)(t.N + 1) * 8, s>>>(t, k_max, gen, roles, wk.counters,
+                                                                wk.list, seg, wk.idle,
+                                                                wk.idle_stride, T, Lambda,
+                                                                master, layers);
+    else if (objective == 1)
         k_dp_ft<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles,
                                                              wk.counters, wk.list, seg, wk.rows,
                                                              wk.tb_global, T, Lambda, master,
