@@ -31,7 +31,8 @@ Printed on one JSON line:
   ablations    the two ablations of Sec. 4.2 on the same 1024-genome
                workload: finishing-time objective vs Algorithm 1, adapted
                SplitWise roles vs the brute-force search (time per call and
-               how many genomes each side wins)
+               how many genomes each side wins); and the idle-device
+               relaxation (time per call, clusters it solves faster)
   two_chromosome  the same measurements for the paper's two-chromosome
                genomes (an ordering of the devices cut into replicas, App. A):
                e2_eval_population_ordered + e2_ga_step_ordered per generation
@@ -536,6 +537,10 @@ def ablations(torch, dev, steps, warmup):
                    steps, warmup)
     ms_ft = _timed(torch, lambda: e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=ft,
                                                        objective="finish_time"), steps, warmup)
+    idle = e2.e2_solve_partitions(ctx, L, R, objective="idle")
+    bnp = e2.e2_solve_partitions(ctx, L, R)
+    ms_idle = _timed(torch, lambda: e2.e2_eval_population(ctx, L, R, fp, with_rates=False,
+                                                         objective="idle"), steps, warmup)
     sm = workload.slot_model(wl)
     sctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
     se = e2.e2_search_roles(sctx, L, fp, wl.k_max)
@@ -545,13 +550,19 @@ def ablations(torch, dev, steps, warmup):
                    steps, warmup)
     torch.cuda.synchronize()
     log(f"ablations on {wl.name}: eval {ms_bn:.3f} ms, finishing-time eval {ms_ft:.3f} ms, "
-        f"SplitWise roles {ms_sw:.3f} ms")
+        f"SplitWise roles {ms_sw:.3f} ms, idle-device eval {ms_idle:.3f} ms")
+    Ti, Tb = e2.u64(idle["T"]), e2.u64(bnp["T"])
+    fin = Tb != INF
     return {"workload": wl.name, "population": wl.population, "steps": steps,
             "finish_time": {"call": "e2_eval_population_ft", "ms_per_call": ms_ft,
                             "bottleneck_ms_per_call": ms_bn,
                             "bottleneck_vs_finish_time": _key_stats(
                                 e2.u64(bn["w"]), e2.u64(bn["phase"]), e2.u64(ft["w"]),
                                 e2.u64(ft["phase"]))},
+            "idle_devices": {"call": "e2_eval_population_idle", "ms_per_call": ms_idle,
+                             "clusters_feasible": int((Ti != INF).sum()),
+                             "clusters_feasible_algorithm_1": int(fin.sum()),
+                             "clusters_lower_T": int((Ti[fin] < Tb[fin]).sum())},
             "splitwise": {"call": "e2_assign_roles_splitwise", "ms_per_call": ms_sw,
                           "search_vs_splitwise": _key_stats(
                               e2.u64(se["w"]), e2.u64(se["phase"]), e2.u64(sw["w"]),
