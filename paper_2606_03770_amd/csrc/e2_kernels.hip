@@ -34,6 +34,7 @@ namespace {
 
 constexpr int kWave = 64;
 
+__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 
 // Wave-wide reductions: DPP permutations within each 16-lane row (quad
@@ -58,6 +59,15 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane)
     return ((uint64_t)hi << 32) | lo;
 }
 
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
+{
+    v = umin64(v, dpp_u64<0xb1>(v));
+    v = umin64(v, dpp_u64<0x4e>(v));
+    v = umin64(v, dpp_u64<0x141>(v));
+    v = umin64(v, dpp_u64<0x140>(v));
+    return umin64(umin64(readlane_u64(v, 0), readlane_u64(v, 16)),
+                  umin64(readlane_u64(v, 32), readlane_u64(v, 48)));
+}
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
 {
     v = umax64(v, dpp_u64<0xb1>(v));
@@ -1238,6 +1248,166 @@ __device__ uint64_t ft_table(const E2Tables &tb, const DpSmem &sm, int r, const 
     return prv[N - 1];
 }
 
+// One banded row of the finishing-time DP: cells i in [lo, hi],
+//   out(i) = min over j in [max(win(i), kmin), i], ascending (the smallest j
+//            on ties), of prev(j-1) + tau + P[i+1] - P[j] + hadd
+// with prev band-packed over [plo, phi] (INF outside) or, for the first
+// device, the stage 0..i alone.  Values to out[i - lo] (LDS or global),
+// split points to tbs[i - lo] when tbs is not null.
+__device__ __forceinline__ void ft_row(const uint64_t *pr, const uint8_t *wr, uint64_t hadd,
+                                       uint64_t tau, int lo, int hi, int kmin,
+                                       const uint64_t *prev, int plo, int phi, uint64_t *out,
+                                       uint8_t *tbs, int lane)
+{
+    for (int i = lo + lane; i <= hi; i += kWave) {
+        uint64_t best = E2_INF64;
+        int bj = 0;
+        const int w = wr[i];
+        if (w != E2_NO_START) {
+            const uint64_t end = pr[i + 1] + hadd;
+            if (!prev) {
+                if (w == 0) best = end - pr[0];
+            } else if (tau != E2_INF64) {
+                for (int j = max(w, kmin); j <= i; ++j) {
+                    const int x = j - 1;
+                    if (x < plo || x > phi) continue;
+                    const uint64_t pv = prev[x - plo];
+                    if (pv == E2_INF64) continue;
+                    const uint64_t v = pv + tau + (end - pr[j]);
+                    if (v < best) {
+                        best = v;
+                        bj = j;
+                    }
+                }
+            }
+        }
+        out[i - lo] = best;
+        if (tbs) tbs[i - lo] = (uint8_t)bj;
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __threadfence_block();
+    __syncthreads();
+}
+
+// The finishing-time DP by the same banded decomposition as dp_banded:
+// forward rows F_1..F_{m-1} (no master) in the wave's global pool, reversed
+// rows G_t over the last t devices in the LDS ping-pong, per master mu
+//   T_mu = min_i H_mu(i) + tau(mu, mu+1) + G_{m-mu}(N-2-i)
+// with H_mu the master's forward row (head time and bytes) over F_{mu-1};
+// the smallest mu with the least T_mu wins.  Rows mu*..m-1 of its table are
+// recomputed with split points and the back tracing fills start[].  Every
+// in-band cell's value equals the full table's (bands depend on memory
+// only), so the result is that of one full table per master.
+__device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs &cr, int r,
+                             int m, int lane, uint64_t *T_out, int *mu_out, uint8_t *start)
+{
+    const int N = tb.N, M = tb.M;
+    uint64_t *pool = sm.pool;
+    uint64_t *H = reinterpret_cast<uint64_t *>(sm.ps);  // N cells
+    uint64_t *Rw[2] = {sm.Rw0, sm.Rw1};
+    // ---- F_1..F_{m-1}, their split points kept for the rows below mu*
+    for (int k = 1; k < m; ++k) {
+        const uint32_t wa = lane_w(cr.wa, k - 1);
+        const int c = f8(wa, 0);
+        const uint64_t tau = k >= 2 ? lane_u64(cr.tau, k - 1) : 0;
+        ft_row(pref_row(tb, r, c), win_row(tb, 0, c), 0, tau, band_lo(cr, k), band_hi(cr, k),
+               k - 1, k >= 2 ? pool + pool_off(cr, k - 1) : nullptr,
+               k >= 2 ? band_lo(cr, k - 1) : 1, k >= 2 ? band_hi(cr, k - 1) : 0,
+               pool + pool_off(cr, k), k >= 2 ? sm.tbp + pool_off(cr, k) : nullptr, lane);
+    }
+    // ---- masters m, then after each reversed row t the master m - t
+    uint64_t best = E2_INF64;
+    int best_mu = 0;
+    int g_lo = 1, g_hi = 0;  // band of the last reversed row (reversed cells)
+    for (int t = 0; t < m; ++t) {
+        const int mu = m - t;
+        if (t >= 1) {
+            // reversed row t: device m+1-t holds reversed blocks y..x after
+            // the t-1 devices behind it
+            const uint32_t wd = lane_w(cr.wd, t - 1), wc = lane_w(cr.wc, t - 1);
+            const int c = f8(wd, 0);
+            const int lo = f8(wd, 8), hi = f8(wd, 16);
+            const uint64_t tau = t >= 2 ? lane_u64(cr.tauR, t - 1) : 0;
+            (void)wc;
+            ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, tau, lo, hi, t - 1,
+                   t >= 2 ? Rw[(t - 1) & 1] : nullptr, g_lo, g_hi, Rw[t & 1], nullptr, lane);
+            g_lo = lo;
+            g_hi = hi;
+        }
+        const uint32_t wa = lane_w(cr.wa, mu - 1);
+        const int c = f8(wa, 0);
+        if (f8(wa, 16) == 0) continue;  // the master's stage cannot hold the head
+        const uint64_t tau = mu >= 2 ? lane_u64(cr.tau, mu - 1) : 0;
+        const int lo = band_lo(cr, mu), hi = mu == m ? N - 1 : band_hi(cr, mu);
+        const int hlo = mu == m ? N - 1 : lo;
+        ft_row(pref_row(tb, r, c), win_row(tb, 1, c), uni64(tb.head[r * M + c]), tau, hlo, hi,
+               mu - 1, mu >= 2 ? pool + pool_off(cr, mu - 1) : nullptr,
+               mu >= 2 ? band_lo(cr, mu - 1) : 1, mu >= 2 ? band_hi(cr, mu - 1) : 0, H, nullptr,
+               lane);
+        uint64_t tm = E2_INF64;
+        if (mu == m) {
+            tm = H[0];
+        } else {
+            const uint64_t tn = lane_u64(cr.tau, mu);  // link mu -> mu+1
+            const uint64_t *G = Rw[t & 1];
+            for (int i = hlo + lane; i <= hi; i += kWave) {
+                const uint64_t h = H[i - hlo];
+                const int x = N - 2 - i;
+                if (h == E2_INF64 || tn == E2_INF64 || x < g_lo || x > g_hi) continue;
+                const uint64_t g = G[x - g_lo];
+                if (g == E2_INF64) continue;
+                const uint64_t v = h + tn + g;
+                tm = v < tm ? v : tm;
+            }
+            tm = wave_min_u64(tm);
+        }
+        if (tm <= best && tm != E2_INF64) {  // the smaller master wins ties
+            best = tm;
+            best_mu = mu;
+        }
+        __syncthreads();
+    }
+    *T_out = best;
+    *mu_out = best_mu;
+    if (best == E2_INF64) return;
+    // ---- rows mu*..m of the chosen master's table with split points (the
+    // previous row ping-pongs in LDS, F_{mu*-1} comes from the pool)
+    uint8_t *tbp = sm.tbp;
+    for (int k = best_mu; k <= m; ++k) {
+        const uint32_t wa = lane_w(cr.wa, k - 1);
+        const int c = f8(wa, 0);
+        const int f = (k == best_mu);
+        const uint64_t tau = k >= 2 ? lane_u64(cr.tau, k - 1) : 0;
+        const int lo = k == m ? N - 1 : band_lo(cr, k), hi = k == m ? N - 1 : band_hi(cr, k);
+        const uint64_t *prev = nullptr;
+        int plo = 1, phi = 0;
+        if (k >= 2) {
+            prev = (k == best_mu) ? pool + pool_off(cr, k - 1) : Rw[(k - 1) & 1];
+            plo = band_lo(cr, k - 1);
+            phi = band_hi(cr, k - 1);
+        }
+        uint8_t *tbs = k == m ? start + m : tbp + pool_off(cr, k);  // row m: one cell
+        ft_row(pref_row(tb, r, c), win_row(tb, f, c), f ? uni64(tb.head[r * M + c]) : 0, tau, lo,
+               hi, k - 1, prev, plo, phi, Rw[k & 1], k >= 2 ? tbs : nullptr, lane);
+    }
+    if (lane == 0) {
+        int i = N - 1;
+        int j = m >= 2 ? start[m] : 0;
+        for (int k = m; k >= 2; --k) {
+            if (k < m) {
+                const int blo = band_lo(cr, k), bhi = band_hi(cr, k);
+                const int ii = i < blo ? blo : (i > bhi ? bhi : i);
+                j = tbp[pool_off(cr, k) + (ii - blo)];
+            }
+            if (j > i) j = i;
+            start[k - 1] = (uint8_t)j;
+            i = j - 1;
+        }
+        start[0] = 0;
+    }
+    __syncthreads();
+}
+
 __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_cells, E2Genomes gen,
                                               const uint8_t *__restrict__ roles,
                                               uint32_t *counters,
@@ -1284,11 +1454,24 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
         // least end-to-end time over masters, the smallest master on ties
         uint64_t best = E2_INF64;
         int best_mu = 0;
-        for (int mu = 1; mu <= m; ++mu) {
-            const uint64_t v = ft_table(tv, sm, r, chain, m, mu, nullptr, lane);
-            if (v < best) {
-                best = v;
-                best_mu = mu;
+        ChainRegs cr;
+        uint64_t bound, bound_tot;
+        int pool_need = 0;
+        bool banded = chain_regs(tv, sm, r, chain, m, lane, cr, &bound, &bound_tot, &pool_need);
+        DpSmem smb = sm;
+        if (pool_need > kLdsTbCells) {
+            smb.tbp = tb_global ? tb_global + (size_t)blockIdx.x * N * N : nullptr;
+            banded = banded && tb_global != nullptr;
+        }
+        if (banded) {
+            dp_ft_banded(tv, smb, cr, r, m, lane, &best, &best_mu, start);
+        } else {
+            for (int mu = 1; mu <= m; ++mu) {
+                const uint64_t v = ft_table(tv, sm, r, chain, m, mu, nullptr, lane);
+                if (v < best) {
+                    best = v;
+                    best_mu = mu;
+                }
             }
         }
         if (best == E2_INF64) {
@@ -1302,24 +1485,26 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
             __syncthreads();
             continue;
         }
-        uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)kLdsTbCells)
-                           ? sm.tbp
-                           : tb_global + (size_t)blockIdx.x * N * N;
-        ft_table(tv, sm, r, chain, m, best_mu, tbp, lane);
-        __builtin_amdgcn_s_waitcnt(0);
-        __threadfence_block();
-        __syncthreads();
-        if (lane == 0) {
-            int i = N - 1;
-            for (int k = m; k >= 2; --k) {
-                int j = tbp[(size_t)(k - 2) * N + (i < 0 ? 0 : i)];
-                if (j > i) j = i < 0 ? 0 : i;
-                start[k - 1] = (uint8_t)j;
-                i = j - 1;
+        if (!banded) {
+            uint8_t *tbp = ((size_t)(m - 1) * N <= (size_t)kLdsTbCells)
+                               ? sm.tbp
+                               : tb_global + (size_t)blockIdx.x * N * N;
+            ft_table(tv, sm, r, chain, m, best_mu, tbp, lane);
+            __builtin_amdgcn_s_waitcnt(0);
+            __threadfence_block();
+            __syncthreads();
+            if (lane == 0) {
+                int i = N - 1;
+                for (int k = m; k >= 2; --k) {
+                    int j = tbp[(size_t)(k - 2) * N + (i < 0 ? 0 : i)];
+                    if (j > i) j = i < 0 ? 0 : i;
+                    start[k - 1] = (uint8_t)j;
+                    i = j - 1;
+                }
+                start[0] = 0;
             }
-            start[0] = 0;
+            __syncthreads();
         }
-        __syncthreads();
         // the partition's end-to-end time and its bottleneck
         uint64_t part = 0, bott = 0;
         for (int k = lane; k < m; k += kWave) {
