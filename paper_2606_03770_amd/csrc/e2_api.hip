@@ -117,7 +117,7 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
 {
     const size_t problems = (size_t)P * k_max * n_r;
     const int np = (int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX);
-    *slots = objective == 2 ? e2_dp_idle_slots(np) : e2_dp_slots(ctx->N, np);
+    *slots = objective == 2 ? e2_dp_idle_slots(np, ctx->M, ctx->N) : e2_dp_slots(ctx->N, np);
     const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
     // the global split-point table is needed only when some chain's split
     // points (m - 1 rows of at most N cells) can exceed their LDS copy

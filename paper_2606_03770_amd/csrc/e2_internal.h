@@ -74,7 +74,7 @@ int e2_dp_lds_tb_cells(int N);
 size_t e2_dp_row_words(int N);
 size_t e2_dp_lds_bytes(int N);
 // Waves and per-wave bytes of the idle-device relaxation's DP kernel.
-int e2_dp_idle_slots(int problems);
+int e2_dp_idle_slots(int problems, int M, int N);
 size_t e2_dp_idle_bytes(int M, int N);
 
 // The genomes of a population: labels [P][M] (cluster id per device), or,

@@ -1552,6 +1552,126 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
 // second pass for the best master, the predecessors and stage starts) in
 // the wave's global region.
 // ---------------------------------------------------------------------------
+// The least T_mu of every master of the idle-device relaxation at once.
+// F_k(x): the best bottleneck of x blocks on participants among devices
+// 1..k ending with k (every participant holding blocks, no master); R_t(x):
+// the same over reversed blocks for the last t devices (B_k'(y) =
+// R_{m+1-k'}(N-y): blocks y..N-1 on participants from k' on, starting at
+// k').  Then with
+//   A_mu(x) = min(0 if x = 0, min_{k' < mu} max(F_k'(x), tau(k', mu)))
+//   S_mu(y) = 0 if y = N, else min_{k'' > mu} max(tau(mu, k''), B_k''(y))
+//   T_mu    = min over x <= y of max(A_mu(x), stage_mu(x..y-1) with the
+//             head (the head alone when x = y), S_mu(y))
+// which is the per-master table's optimum, exactly (the bottleneck splits
+// at the master's stage); the smallest master with the least T_mu wins.
+// O(m^2 N + m N W / 64) per problem instead of O(m^3 N + m^2 N W / 64).
+__device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, int m, uint64_t *E,
+                             uint64_t *B, uint64_t *A, uint64_t *S, int lane, uint64_t *best_out,
+                             int *mu_out)
+{
+    const int N = tv.N, M = tv.M, X = N + 1;
+    // forward rows F_k into E, reversed rows R_t into B
+    for (int dir = 0; dir < 2; ++dir) {
+        uint64_t *rows = dir ? B : E;
+        for (int k = 1; k <= m; ++k) {
+            // forward: device k; reversed: device m+1-k, links to the ones behind it
+            const int pos = dir ? m - k : k - 1;
+            const int c = uni(chain[pos]);
+            for (int x = lane; x <= N; x += kWave) {
+                uint64_t a = x == 0 ? 0 : E2_INF64;
+                for (int kp = 1; kp <= k - 1; ++kp) {
+                    const uint64_t e = rows[(size_t)(kp - 1) * X + x];
+                    const int cp = uni(chain[dir ? m - kp : kp - 1]);
+                    // links run from the earlier chain position to the later one
+                    const uint64_t tl = dir ? link_tau_u(tv, r, c, cp) : link_tau_u(tv, r, cp, c);
+                    if (e == E2_INF64 || tl == E2_INF64) continue;
+                    const uint64_t v = umax64(e, tl);
+                    a = v < a ? v : a;
+                }
+                A[x] = a;
+            }
+            __syncthreads();
+            const uint64_t *pr = dir ? prefR_row(tv, r, c) : pref_row(tv, r, c);
+            const uint8_t *wr = dir ? tv.winR + (uint32_t)(c * N) : win_row(tv, 0, c);
+            for (int x = lane; x <= N; x += kWave) {
+                uint64_t e = E2_INF64;
+                if (x >= 1) {
+                    const int w = wr[x - 1];
+                    if (w != E2_NO_START)
+                        for (int j = w; j < x; ++j) {
+                            const uint64_t aj = A[j];
+                            if (aj == E2_INF64) continue;
+                            const uint64_t v = umax64(aj, pr[x] - pr[j]);
+                            e = v < e ? v : e;
+                        }
+                }
+                rows[(size_t)(k - 1) * X + x] = e;
+            }
+            __builtin_amdgcn_s_waitcnt(0);
+            __threadfence_block();
+            __syncthreads();
+        }
+    }
+    uint64_t best = E2_INF64;
+    int best_mu = 0;
+    for (int mu = 1; mu <= m; ++mu) {
+        const int c = uni(chain[mu - 1]);
+        for (int x = lane; x <= N; x += kWave) {
+            uint64_t a = x == 0 ? 0 : E2_INF64;
+            for (int kp = 1; kp < mu; ++kp) {
+                const uint64_t e = E[(size_t)(kp - 1) * X + x];
+                const uint64_t tl = link_tau_u(tv, r, uni(chain[kp - 1]), c);
+                if (e == E2_INF64 || tl == E2_INF64) continue;
+                const uint64_t v = umax64(e, tl);
+                a = v < a ? v : a;
+            }
+            A[x] = a;
+            uint64_t sv = x == N ? 0 : E2_INF64;
+            for (int kpp = mu + 1; kpp <= m; ++kpp) {
+                // participants from kpp on: reversed row t = m + 1 - kpp at N - x
+                const uint64_t e = B[(size_t)(m - kpp) * X + (N - x)];
+                const uint64_t tl = link_tau_u(tv, r, c, uni(chain[kpp - 1]));
+                if (e == E2_INF64 || tl == E2_INF64) continue;
+                const uint64_t v = umax64(e, tl);
+                sv = v < sv ? v : sv;
+            }
+            S[x] = sv;
+        }
+        __syncthreads();
+        const uint64_t *pr = pref_row(tv, r, c);
+        const uint8_t *wr = win_row(tv, 1, c);
+        const uint64_t head = uni64(tv.head[r * M + c]);
+        const bool empty_ok = tv.hfit[c];
+        uint64_t tm = E2_INF64;
+        for (int y = lane; y <= N; y += kWave) {
+            const uint64_t sv = S[y];
+            if (sv == E2_INF64) continue;
+            if (y >= 1) {
+                const int w = wr[y - 1];
+                if (w != E2_NO_START)
+                    for (int x = w; x < y; ++x) {
+                        const uint64_t ax = A[x];
+                        if (ax == E2_INF64) continue;
+                        const uint64_t v = umax64(umax64(ax, pr[y] - pr[x] + head), sv);
+                        tm = v < tm ? v : tm;
+                    }
+            }
+            if (empty_ok && A[y] != E2_INF64) {
+                const uint64_t v = umax64(umax64(A[y], head), sv);
+                tm = v < tm ? v : tm;
+            }
+        }
+        tm = wave_min_u64(tm);
+        if (tm < best) {
+            best = tm;
+            best_mu = mu;
+        }
+        __syncthreads();
+    }
+    *best_out = best;
+    *mu_out = best_mu;
+}
+
 __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genomes gen,
                                                 const uint8_t *__restrict__ roles,
                                                 uint32_t *counters,
@@ -1559,14 +1679,16 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
                                                 uint8_t *idle, size_t idle_stride, uint64_t *T,
                                                 uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
-    extern __shared__ uint64_t A[];  // [N+1]
+    extern __shared__ uint64_t A[];  // [N+1], then S [N+1]
     __shared__ uint8_t chain[256];
     __shared__ uint8_t sizes[256];
     __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N, X = N + 1;
+    uint64_t *S = A + X;
     uint64_t *E = reinterpret_cast<uint64_t *>(idle + (size_t)blockIdx.x * idle_stride);
-    uint16_t *Ek = reinterpret_cast<uint16_t *>(E + (size_t)M * X);
+    uint64_t *B = E + (size_t)M * X;
+    uint16_t *Ek = reinterpret_cast<uint16_t *>(B + (size_t)M * X);
     uint8_t *Ej = reinterpret_cast<uint8_t *>(Ek + (size_t)M * X);
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
@@ -1590,9 +1712,10 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
         const E2Tables tv = mem_view(tb, r);
         uint64_t best = E2_INF64;
         int best_mu = 0, last = 0;
-        for (int pass = 0; pass < 2; ++pass) {
-            if (pass == 1 && best == E2_INF64) break;
-            const int mu_lo = pass ? best_mu : 1, mu_hi = pass ? best_mu : m;
+        idle_masters(tv, r, chain, m, E, B, A, S, lane, &best, &best_mu);
+        for (int pass = 1; pass < 2; ++pass) {
+            if (best == E2_INF64) break;
+            const int mu_lo = best_mu, mu_hi = best_mu;
             for (int mu = mu_lo; mu <= mu_hi; ++mu) {
                 for (int k = 1; k <= m; ++k) {
                     const int c = uni(chain[k - 1]);
@@ -2213,16 +2336,20 @@ int e2_dp_pool_cells(int N)
     return max(best, kLdsTbCells);
 }
 
-int e2_dp_idle_slots(int problems)
+int e2_dp_idle_slots(int problems, int M, int N)
 {
-    // every wave holds M x (N+1) rows in its global region: a bounded grid
-    const int cap = 1024;
-    return problems < cap ? (problems > 0 ? problems : 1) : cap;
+    // every wave holds 2 M x (N+1) rows in its own global region: as many
+    // waves as 1 GiB of regions allows, at least 256 and at most 4096
+    const size_t budget = (size_t)1 << 30;
+    size_t cap = budget / e2_dp_idle_bytes(M, N);
+    cap = cap < 256 ? 256 : (cap > 4096 ? 4096 : cap);
+    return problems < (int)cap ? (problems > 0 ? problems : 1) : (int)cap;
 }
 
 size_t e2_dp_idle_bytes(int M, int N)
 {
-    return ((size_t)M * (N + 1) * 11 + 255) & ~(size_t)255;
+    // forward and reversed rows (u64), predecessors (u16), stage starts (u8)
+    return ((size_t)M * (N + 1) * 19 + 255) & ~(size_t)255;
 }
 
 int e2_dp_lds_tb_cells(int N)
@@ -2285,7 +2412,7 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
     if (objective == 2)
-        k_dp_idle<<<wk.n_slots, 64, (size_t)(t.N + 1) * 8, s>>>(t, k_max, gen, roles, wk.counters,
+        k_dp_idle<<<wk.n_slots, 64, (size_t)(t.N + 1) * 16, s>>>(t, k_max, gen, roles, wk.counters,
                                                                 wk.list, seg, wk.idle,
                                                                 wk.idle_stride, T, Lambda,
                                                                 master, layers);
