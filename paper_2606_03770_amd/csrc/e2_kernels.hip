@@ -2178,6 +2178,8 @@ __global__ __launch_bounds__(64) void k_breed_ordered(
     __shared__ uint32_t used[8];
     __shared__ uint16_t szs[256];
     __shared__ uint8_t rls[256];
+    __shared__ uint64_t draw[256];  // size / role draws of a regrowth
+    __shared__ uint8_t pj[256];     // swap partners of a new ordering
     const int s = blockIdx.x;
     const int lane = threadIdx.x;
     if ((uint32_t)s < n_elite) {
@@ -2263,8 +2265,24 @@ __global__ __launch_bounds__(64) void k_breed_ordered(
     }
     __syncthreads();
     const uint64_t um = rng_at(hs, kStOMut, 0);
-    if ((uint32_t)(um >> 32) < mut && lane == 0) {
-        const uint32_t kind = (uint32_t)um;
+    const bool mutate = (uint32_t)(um >> 32) < mut;
+    const uint32_t kind = (uint32_t)um;
+    if (mutate && kind >= kMutSwapBelow) {
+        // the draws of the regrowth (and of a new ordering) are independent
+        // counter-based values: all lanes compute them, lane 0 then runs the
+        // sequential steps on them
+        const uint64_t h_size = sm64(hs ^ (uint64_t)kStOSize);
+        for (int r = lane; r < k_max; r += kWave) draw[r] = sm64(h_size ^ (uint64_t)r);
+        if (kind >= kMutAllGroupBelow) {
+            const uint64_t h_perm = sm64(hs ^ (uint64_t)kStOPerm);
+            for (int t = lane; t < M; t += kWave) {
+                const uint64_t v = sm64(h_perm ^ (uint64_t)t);
+                pj[t] = (uint8_t)(((v >> 32) * (uint64_t)(t + 1)) >> 32);
+            }
+        }
+        __syncthreads();
+    }
+    if (mutate && lane == 0) {
         if (kind < kMutSwapBelow) {
             const uint64_t v = rng_at(hs, kStOSwap, 0);
             const int i = (int)(((v >> 32) * (uint64_t)M) >> 32);
@@ -2289,8 +2307,7 @@ __global__ __launch_bounds__(64) void k_breed_ordered(
                 // a new ordering: Fisher-Yates from the identity
                 for (int t = 0; t < M; ++t) child[t] = (uint8_t)t;
                 for (int t = M - 1; t >= 1; --t) {
-                    const uint64_t v = rng_at(hs, kStOPerm, (uint64_t)t);
-                    const int j = (int)(((v >> 32) * (uint64_t)(t + 1)) >> 32);
+                    const int j = pj[t];
                     const uint8_t x = child[t];
                     child[t] = child[j];
                     child[j] = x;
@@ -2302,7 +2319,7 @@ __global__ __launch_bounds__(64) void k_breed_ordered(
             if (remaining < 0) remaining = 0;
             int r = pos;
             while (remaining > 0 && r < k_max) {
-                const uint64_t u = rng_at(hs, kStOSize, (uint64_t)r);
+                const uint64_t u = draw[r];
                 long sz = 1 + (long)(((u >> 32) * (uint64_t)max_replica) >> 32);
                 if (r == k_max - 1 || sz > remaining) sz = remaining;
                 szs[r] = (uint16_t)sz;
