@@ -226,6 +226,9 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
     const int M = prob->n_dev, N = prob->n_layer;
     const int R = b_max + 1;
     const int C = kv ? R : 1;
+    // kv * slots below must not wrap: with kv < 2^48 and slots <= 15 it
+    // stays below 2^52, and the per-block test then catches 2^48 and above
+    if (kv >= kLimit48) return E2_EOVERFLOW;
     std::vector<uint64_t> t((size_t)R * M * N), h((size_t)R * M), tau((size_t)R * M * M);
     rc = quantise(prob, t.data(), h.data(), tau.data());
     if (rc) return rc;
@@ -650,11 +653,12 @@ int e2_ga_step_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
         gp->n_elite > (uint32_t)P || gp->max_replica < 1 || gp->max_replica > 256)
         return E2_EINVAL;
     const size_t no = (size_t)P * ctx->M, ns = (size_t)P * k_max * 2, nr = (size_t)P * k_max;
-    const void *ins[3] = {order_in, sizes_in, roles_in};
-    const size_t nin[3] = {no, ns, nr};
+    const size_t nk = (size_t)P * 8;
+    const void *ins[5] = {order_in, sizes_in, roles_in, w_in, phase_in};
+    const size_t nin[5] = {no, ns, nr, nk, nk};
     void *outs[3] = {order_out, sizes_out, roles_out};
     for (int i = 0; i < 3; ++i) {
-        for (int j = 0; j < 3; ++j)
+        for (int j = 0; j < 5; ++j)
             if (overlap(outs[i], nin[i], ins[j], nin[j])) return E2_EINVAL;
         for (int j = i + 1; j < 3; ++j)
             if (overlap(outs[i], nin[i], outs[j], nin[j])) return E2_EINVAL;
@@ -741,11 +745,13 @@ int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_
         return E2_EINVAL;
     const size_t M = (size_t)ctx->M;
     // outputs must not overlap the inputs
-    const size_t nl = (size_t)P * M, nr = (size_t)P * k_max;
-    if (overlap(labels_out, nl, labels_in, nl) || overlap(labels_out, nl, roles_in, nr) ||
-        overlap(roles_out, nr, labels_in, nl) || overlap(roles_out, nr, roles_in, nr) ||
-        overlap(labels_out, nl, roles_out, nr))
-        return E2_EINVAL;
+    const size_t nl = (size_t)P * M, nr = (size_t)P * k_max, nk = (size_t)P * 8;
+    const void *ins[4] = {labels_in, roles_in, w_in, phase_in};
+    const size_t nin[4] = {nl, nr, nk, nk};
+    for (int j = 0; j < 4; ++j)
+        if (overlap(labels_out, nl, ins[j], nin[j]) || overlap(roles_out, nr, ins[j], nin[j]))
+            return E2_EINVAL;
+    if (overlap(labels_out, nl, roles_out, nr)) return E2_EINVAL;
     if ((rc = check_device(ctx))) return rc;
     hipStream_t s = as_stream(stream);
     Scratch sc;

@@ -115,3 +115,22 @@ def test_entry_points_reject_bad_arguments_without_a_device():
     assert L.e2_ga_step(nul, nul, 1, 1, nul, nul, nul, nul, ctypes.byref(gp), nul,
                         nul) == e2.E2_EINVAL
     assert L.e2_ctx_create(None, ctypes.byref(ctypes.c_void_p())) == e2.E2_EINVAL
+
+
+@pytest.mark.parametrize("sm,code", [
+    (dict(b_max=0, beta_ppm=0, kv_bytes_per_block_slot=0), e2.E2_EINVAL),
+    (dict(b_max=16, beta_ppm=0, kv_bytes_per_block_slot=0), e2.E2_EINVAL),
+    (dict(b_max=2, beta_ppm=1000001, kv_bytes_per_block_slot=0), e2.E2_EINVAL),
+    # one slot's bytes at the limit, and a value whose product with the slot
+    # count would wrap 64 bits
+    (dict(b_max=2, beta_ppm=0, kv_bytes_per_block_slot=1 << 48), e2.E2_EOVERFLOW),
+    (dict(b_max=2, beta_ppm=0, kv_bytes_per_block_slot=(1 << 63) + 1), e2.E2_EOVERFLOW),
+    # b_max slots push a block to 2^48
+    (dict(b_max=15, beta_ppm=0, kv_bytes_per_block_slot=(1 << 48) // 15 + 1), e2.E2_EOVERFLOW),
+])
+def test_slot_context_rejects_before_any_hip_call(sm, code):
+    s, keep = e2._make_problem(_base_problem())
+    m = e2.e2_slot_model(sm["b_max"], sm["beta_ppm"], sm["kv_bytes_per_block_slot"])
+    h = ctypes.c_void_p()
+    assert e2.lib().e2_ctx_create_slots(ctypes.byref(s), ctypes.byref(m), ctypes.byref(h)) == code
+    assert h.value is None

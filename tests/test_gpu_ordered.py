@@ -253,6 +253,10 @@ def test_ordered_empty_population_and_bad_arguments(torch_dev):
     params["max_replica"] = 2
     with pytest.raises(e2.E2Error):        # outputs overlapping the inputs
         e2.e2_ga_step_ordered(ctx, O, S, R, W, W, params, out=(O, S.clone(), R.clone()))
+    with pytest.raises(e2.E2Error) as ei:  # roles_out inside the fitness keys
+        e2.e2_ga_step_ordered(ctx, O, S, R, W, W, params,
+                              out=(O.clone(), S.clone(), W.view(torch.uint8)[:2].view(1, 2)))
+    assert ei.value.code == e2.E2_EINVAL
     rc = e2.lib().e2_solve_partitions_ordered(ctx.handle, None, 1, 2, None, ctypes.c_void_p(
         S.data_ptr()), ctypes.c_void_p(R.data_ptr()), None, None, None, None)
     assert rc == e2.E2_EINVAL

@@ -247,6 +247,29 @@ def test_ga_step_parity_random(torch_dev, n_elite, tk):
     assert (got[0] == want[0]).all() and (got[1] == want[1]).all()
 
 
+def test_ga_step_rejects_outputs_overlapping_any_input(torch_dev):
+    """Argument checks on the host, before any launch: an output may not
+    share bytes with the labels, roles or the fitness keys it reads."""
+    torch, dev = torch_dev
+    wl = workload.random_small(2, M=4, N=5, P=2, k_max=2)
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    W = torch.zeros(2, dtype=torch.int64, device=dev)
+    PH = torch.zeros(2, dtype=torch.int64, device=dev)
+    ga = wl.ga_params(0)
+    for key in (W, PH):
+        alias = key.view(torch.uint8)[:4].view(2, 2)       # roles_out inside w or phase
+        with pytest.raises(e2.E2Error) as ei:
+            e2.e2_ga_step(ctx, L, R, W, PH, ga, out=(torch.empty_like(L), alias))
+        assert ei.value.code == e2.E2_EINVAL
+    with pytest.raises(e2.E2Error):
+        e2.e2_ga_step(ctx, L, R, W, PH, ga, out=(L, torch.empty_like(R)))
+    lo, ro = e2.e2_ga_step(ctx, L, R, W, PH, ga)
+    torch.cuda.synchronize()
+    assert lo.shape == L.shape and ro.shape == R.shape
+
+
 def test_ga_loop_on_the_16384_genome_workload(torch_dev):
     """Three generations of eval + GA on the GPU; each generation's GA output
     equals the oracle's GA fed the GPU's population and fitness, and sampled
