@@ -584,12 +584,17 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
         const int px = j - 1 - rw.plo;
         const int pxc = max(0, min(px, pspan));
         const uint64_t prj = rw.pr[j];
-        const K pvr = rw.prev[pxc];
         K pv;
-        if constexpr (__is_same(K, double))
-            pv = (px < 0 || px > pspan) ? KeyT<K>::inf : pvr;
-        else  // all ones (INF) outside the previous band, without a branch
+        if constexpr (__is_same(K, double)) {
+            // select on the bit pattern so that the load is not put under a
+            // branch (INF = 0x7FF0000000000000)
+            const uint64_t bits = reinterpret_cast<const uint64_t *>(rw.prev)[pxc];
+            const bool out = px < 0 || px > pspan;
+            pv = __builtin_bit_cast(double, out ? 0x7FF0000000000000ull : bits);
+        } else {  // all ones (INF) outside the previous band, without a branch
+            const K pvr = rw.prev[pxc];
             pv = pvr | ((K)0 - (K)(px < 0 || px > pspan));
+        }
         ps[j].a = pack_prev(pv, rw.tau, j);
         if constexpr (__is_same(K, double))  // may be negative when blocks take 0 ns
             ps[j].s = __builtin_fma((double)prj, 256.0, -(double)j);
