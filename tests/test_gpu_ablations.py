@@ -78,6 +78,18 @@ def test_ft_long_chain_uses_the_global_split_table(torch_dev):
     assert (got["T"] != INF).any()
 
 
+@pytest.mark.parametrize("k_max", [1, 3, 4])
+def test_ft_maximum_sizes(torch_dev, k_max):
+    """256 devices, 255 blocks: one chain longer than the model (no
+    partition), chains of about 85 devices (beyond the banded path: one
+    table per master) and of about 64 devices."""
+    wl = workload.random_small(40 + k_max, M=256, N=255, P=1, k_max=k_max, mem_lo_layers=2,
+                               mem_hi_layers=25)
+    got = _gpu_ft(torch_dev, wl)
+    _assert_equal(got, oracle.eval_population_ft(wl), FT_KEYS, tag=f"ft max {k_max}")
+    assert (got["T"] != INF).any() == (k_max > 1)
+
+
 @pytest.mark.parametrize("name,rows", [("c1_tiny_12dev_32L", None), ("c2_32dev_48L", None),
                                        ("c3_64dev_80L", None)])
 def test_ft_named_workloads(torch_dev, name, rows):

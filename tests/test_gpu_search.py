@@ -85,6 +85,18 @@ def test_search_sixteen_clusters(torch_dev):
     _assert_equal(_gpu_search(torch_dev, wl, sm), want, tag="k16")
 
 
+def test_search_maximum_sizes(torch_dev):
+    """256 devices, 255 blocks, 16 clusters, 15 decode slot counts with KV
+    bytes: 16 role indices per cluster and one memory class per index."""
+    wl = workload.random_small(12, M=256, N=255, P=2, k_max=16, mem_lo_layers=10,
+                               mem_hi_layers=40)
+    wl.min_tps_milli = 0
+    sm = dict(b_max=15, beta_ppm=125_000, kv_bytes_per_block_slot=int(wl.layer_bytes.mean()) // 16)
+    want = oracle.search_roles(wl, sm)
+    assert (want["T_all"] != INF).sum() > 100 and (want["slots"] > 1).any()
+    _assert_equal(_gpu_search(torch_dev, wl, sm), want, tag="max")
+
+
 @pytest.mark.parametrize("name,rows", [("c1_tiny_12dev_32L", None), ("c2_32dev_48L", None),
                                        ("c3_64dev_80L", 192)])
 def test_search_named_workloads(torch_dev, name, rows):
