@@ -183,13 +183,23 @@ def ordered_problems(order, sizes):
     return out
 
 
-def generation_work(wl, problems, roles, T, master, tabs):
+def head_free(problem):
+    """The same problem with no head time and no head bytes: every master
+    then ties, and the DP's optimum is the optimum without a master."""
+    return dict(problem, head_flops=np.zeros(2, dtype=np.uint64), head_bytes=0)
+
+
+def generation_work(wl, problems, roles, T, master, tabs, T0):
     """(Algorithm 1 cells over feasible problems, useful j-candidates the DP
     kernel evaluates with u64 keys, those it evaluates with u32 or fp64 keys)
-    for one population, given as its (genome, cluster, chain) problems.  The candidate count follows k_dp row by row:
-    forward rows, reversed rows, one combine per master, the chosen master's
-    rows and last cell (banded path), or one full table per master plus the
-    chosen master's again (reference path, u64 keys).  A problem takes the
+    for one population, given as its (genome, cluster, chain) problems, their
+    optima T, masters and optima T0 without a master (head_free).  The
+    candidate count follows k_dp row by row: reversed rows, the last cell of
+    the full reversed table (T0), then masters in ascending position with
+    the forward row after each, up to the first master whose optimum is T0
+    (every master when T0 < T, none when T0 is infinite), then the chosen
+    master's rows and last cell (banded path); or one full table per master
+    plus the chosen master's again (reference path, u64 keys).  A problem takes the
     banded path when its chain has at most 64 devices, its forward bands fit
     the pool and either every finite value it can produce (largest fitting
     stage cost of its devices, largest finite link time) is at most
@@ -240,6 +250,8 @@ def generation_work(wl, problems, roles, T, master, tabs):
         narrow = np.array([b <= U32_MAX_VALUE or bt < F64_LIMIT for b, bt in zip(b32, b64)],
                           dtype=bool)
         mu = np.zeros(n, dtype=np.int64)
+        t_opt = T[pq[:, 0], pq[:, 1]]
+        t_free = T0[pq[:, 0], pq[:, 1]]
         mdev = master[pq[:, 0], pq[:, 1]].astype(np.int64)
         for a in range(n):
             if feas[a]:
@@ -262,10 +274,19 @@ def generation_work(wl, problems, roles, T, master, tabs):
             kk = np.broadcast_to(k, lof.shape)
             jm0 = np.maximum(kk - 1, lof - c0f + 1)
             jmH = np.maximum(kk - 1, lof - cHf + 1)
-            # forward rows 2..m-1 and combines 2..m
+            # masters 1..ex, forward rows 1..ex-1: ex is the first master
+            # reaching T0 (the chosen one when T = T0), m when T0 < T, and 0
+            # when T0 is infinite; rows and combines of position 1 scan nothing
+            tf, t0f = t_opt[fast], t_free[fast]
+            ex = np.where(t0f == INF, 0, np.where(tf == t0f, muf, m))[:, None]
             fwd = rows(0, chf, jm0, lof, hif)
             comb = np.where(cHf > 0, rows(1, chf, jmH, lof, hif), 0)
-            tot_f = fwd[:, 1:m - 1].sum(1) + comb[:, 1:].sum(1)
+            tot_f = (fwd * ((kk >= 2) & (kk <= ex - 1) & (kk <= m - 1))).sum(1) + \
+                (comb * ((kk >= 2) & (kk <= ex))).sum(1)
+            # the last cell of the full reversed table (device 1, all blocks)
+            if m >= 2:
+                full = np.full(len(chf), N - 1)
+                tot_f += rrows(chf[:, 0], np.maximum(m - 1, N - c0f[:, 0]), full, full)
             # reversed rows t = 2..m-1: device k = m+1-t
             for t in range(2, m):
                 kd = m + 1 - t
@@ -346,6 +367,7 @@ def main():
     wl = workload.make(args.workload)
     P, M, K = wl.population, wl.n_dev, wl.k_max
     ctx = e2.e2_ctx_create(wl.problem_arrays())
+    ctx_free = e2.e2_ctx_create(head_free(wl.problem_arrays()))  # work accounting only
     stream = torch.cuda.current_stream()
     fp = wl.fitness_params()
     win, winR, cap = window_tables(wl)
@@ -368,11 +390,13 @@ def main():
         def count(g, pop):
             L, R = pop
             sol = e2.e2_solve_partitions(ctx, L, R)
+            sol0 = e2.e2_solve_partitions(ctx_free, L, R)
             f2 = e2.e2_eval_population(ctx, L, R, fp, with_rates=False)
             nxt = e2.e2_ga_step(ctx, L, R, f2["w"], f2["phase"], wl.ga_params(g))
             torch.cuda.synchronize()
             work = generation_work(wl, label_problems(L.cpu().numpy(), K), R.cpu().numpy(),
-                                   e2.u64(sol["T"]), sol["master"].cpu().numpy(), wcr)
+                                   e2.u64(sol["T"]), sol["master"].cpu().numpy(), wcr,
+                                   e2.u64(sol0["T"]))
             return work, nxt
 
         return measure(torch, ctx, stream, bufs, (L0, R0), step, count, args.warmup, n)
@@ -393,12 +417,13 @@ def main():
         def count(g, pop):
             O, S, Q = pop
             sol = e2.e2_solve_partitions_ordered(ctx, O, S, Q)
+            sol0 = e2.e2_solve_partitions_ordered(ctx_free, O, S, Q)
             f2 = e2.e2_eval_population_ordered(ctx, O, S, Q, fp, with_rates=False)
             nxt = e2.e2_ga_step_ordered(ctx, O, S, Q, f2["w"], f2["phase"], op.ga_params(wl, g))
             torch.cuda.synchronize()
             probs = ordered_problems(O.cpu().numpy(), S.cpu().numpy())
             work = generation_work(wl, probs, Q.cpu().numpy(), e2.u64(sol["T"]),
-                                   sol["master"].cpu().numpy(), wcr)
+                                   sol["master"].cpu().numpy(), wcr, e2.u64(sol0["T"]))
             return work, nxt
 
         return measure(torch, ctx, stream, bufs, (O0, S0, Q0), step, count, args.warmup, n)

@@ -471,6 +471,15 @@ __device__ __forceinline__ uint64_t uni64(uint64_t x)
     return ((uint64_t)hi << 32) | lo;
 }
 
+// a value every lane holds alike, moved to scalar registers
+template <typename K> __device__ __forceinline__ K uni_k(K v)
+{
+    if constexpr (__is_same(K, uint32_t)) return (uint32_t)uni((int)v);
+    else if constexpr (__is_same(K, double))
+        return __builtin_bit_cast(double, uni64(__builtin_bit_cast(uint64_t, v)));
+    else return uni64(v);
+}
+
 // Row starts of the per-device tables (element offsets fit in 32 bits:
 // at most 2 x 256 x 256 entries).
 __device__ __forceinline__ const uint64_t *pref_row(const E2Tables &tb, int r, int c)
@@ -695,7 +704,7 @@ __device__ __forceinline__ RowOut<K> store_to(K *vals, K *vals_g, uint8_t *tbs)
 // (others INF) leaves every in-band value and split point exact.
 //
 //   F_k  forward rows without master, k = 1..m-1 (values kept for the
-//        combines, split points in LDS)
+//        chosen master's first row, split points in LDS)
 //   G_k  backward rows without master: blocks j..N-1 on devices k..m with
 //        links k..m, computed as forward rows over reversed blocks
 //   T_mu = min_i max( min_j max(F_{mu-1}(j-1), tau(mu-1, mu), cost_mu(j, i)
@@ -706,11 +715,19 @@ __device__ __forceinline__ RowOut<K> store_to(K *vals, K *vals_g, uint8_t *tbs)
 //   attaining it; rows mu*..m of its table (rows below mu* are F) give the
 //   split points for the back tracing.
 //
+// Schedule: all G rows first (kept in a per-wave global pool), then the
+// optimum T0 without any master (the full reversed table's last cell), then
+// masters in ascending position, each combine followed by the forward row
+// the next one reads.  Head time and head bytes only ever add, so
+// T_mu >= T0 for every mu; the sweep stops at the first mu with
+// min(T_1..T_mu) = T0, which is then the best T and the smallest master
+// attaining it, and skips the forward rows and combines beyond it.
+//
 // The per-position data of a chain (device, capacities, links, head time,
 // bands, pool offsets, window-length bounds) is loaded once, one position
 // per lane (m <= 64), and each row reads its scalars with readlane.  The
 // previous row of every sweep sits in an LDS ping-pong pair; forward rows
-// are also written to a per-wave global pool for the combines.
+// are also written to a per-wave global pool for the chosen master's rows.
 // ---------------------------------------------------------------------------
 constexpr int kMaxBandedChain = kWave;
 // split-point bytes kept in LDS per wave; larger tables (the bands of long
@@ -727,6 +744,7 @@ struct ChainRegs {
     uint32_t wb;    // flo | fhi << 8 | lmin1 << 16                    (forward row k)
     uint32_t wc;    // pool offset of row k | lminR << 16 | capR << 24 (reversed row t = k)
     uint32_t wd;    // devR | glo << 8 | ghi << 16                     (reversed row t = k)
+    uint32_t we;    // offset of reversed row t = k in the backward-row pool
     uint64_t tau;   // link from position k-1 (k >= 2)
     uint64_t head;  // head time of the device
     uint64_t tauR;  // link of reversed row t = k: position m+1-k -> m+2-k
@@ -750,6 +768,10 @@ __device__ __forceinline__ int pool_off(const ChainRegs &cr, int k)
     return (int)(lane_w(cr.wc, k - 1) & 0xFFFFu);
 }
 __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int k) { return readlane_u64(v, k); }
+// band of reversed row t and its offset in the backward-row pool
+__device__ __forceinline__ int rband_lo(const ChainRegs &cr, int t) { return f8(lane_w(cr.wd, t - 1), 8); }
+__device__ __forceinline__ int rband_hi(const ChainRegs &cr, int t) { return f8(lane_w(cr.wd, t - 1), 16); }
+__device__ __forceinline__ int gpool_off(const ChainRegs &cr, int t) { return (int)lane_w(cr.we, t - 1); }
 
 __device__ __forceinline__ int scan_incl_i32(int x, int lane)
 {
@@ -766,6 +788,7 @@ struct DpSmem {
     uint64_t *Rw1;
     uint8_t *tbp;    // split points of the forward rows, band-packed (LDS)
     uint64_t *pool;  // band-packed forward row values (global, per wave)
+    uint64_t *gpool; // band-packed backward row values (global, per wave)
     uint64_t *Ga;    // full rows of the reference path (global, per wave)
     uint64_t *Gb;
     int pool_cells;
@@ -802,6 +825,31 @@ __device__ __forceinline__ void set_prev(Row<K> &rw, const K *prev, int plo, int
     rw.prev = prev;
     rw.plo = plo;
     rw.phi = phi;
+}
+
+// Reversed row t (1-based): the device at chain position m+1-t over the
+// blocks in reverse order (block N-1 first), without a master; prev / plo /
+// phi are filled in by the caller.  For t = m the caller also sets the cell
+// range (the band fields of position 1 are not packed).
+template <typename K>
+__device__ __forceinline__ Row<K> rev_row_of(const E2Tables &tb, const ChainRegs &cr, int r, int t)
+{
+    const uint32_t wc = lane_w(cr.wc, t - 1), wd = lane_w(cr.wd, t - 1);
+    const int c = f8(wd, 0);
+    Row<K> g;
+    g.pr = prefR_row(tb, r, c);
+    g.wr = tb.winR + (uint32_t)(c * tb.N);
+    g.hadd = 0;
+    g.tau = (t >= 2) ? to_k<K>(lane_u64(cr.tauR, t - 1)) : (K)0;
+    g.lo = f8(wd, 8);
+    g.hi = f8(wd, 16);
+    g.kmin = t - 1;
+    g.cap = f8(wc, 24);
+    g.lmin = f8(wc, 16);
+    g.prev = nullptr;
+    g.plo = 1;
+    g.phi = 0;
+    return g;
 }
 
 // Per-position table of a chain and the largest finite value its DP can
@@ -857,8 +905,15 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
     cr.wb = (uint32_t)lo | (uint32_t)hi << 8 | (uint32_t)lmin1 << 16;
     cr.wc = ((uint32_t)off & 0xFFFFu) | (uint32_t)lminR << 16 | (uint32_t)capR << 24;
     cr.wd = (uint32_t)devR | (uint32_t)glo << 8 | (uint32_t)ghi << 16;
+    // backward-row pool: reversed rows t = 1..m-1 band-packed in order (their
+    // bands are the forward bands of positions m-1..1 moved by one block, so
+    // they hold as many cells as the forward pool)
+    const int gsize = ghi >= glo ? ghi - glo + 1 : 0;
+    const int g_incl = scan_incl_i32(gsize, lane);
+    cr.we = (uint32_t)(g_incl - gsize);
+    const int gpool_need = lane_i(g_incl, kWave - 1);
     *pool_cells = pool_need;
-    return pool_need <= sm.pool_cells;
+    return pool_need <= sm.pool_cells && gpool_need <= sm.pool_cells;
 }
 
 // The banded DP of one chain with keys of width K.  Returns the optimum as
@@ -871,72 +926,75 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
     const int N = tb.N, M = tb.M;
     PS<K> *ps = static_cast<PS<K> *>(sm.ps);
     K *pool = reinterpret_cast<K *>(sm.pool);
+    K *gpool = reinterpret_cast<K *>(sm.gpool);
     K *Rw[2] = {reinterpret_cast<K *>(sm.Rw0), reinterpret_cast<K *>(sm.Rw1)};
-    // ---- forward rows F_1..F_{m-1}: LDS ping-pong + global pool + split points
-    for (int k = 1; k < m; ++k) {
-        Row<K> rw = fwd_row_of<K>(tb, cr, r, k, 0);
-        if (k >= 2) set_prev(rw, (const K *)Rw[(k - 1) & 1], band_lo(cr, k - 1), band_hi(cr, k - 1));
-        const int off = pool_off(cr, k);
-        row_pass(rw, store_to<K>(Rw[k & 1], pool + off, sm.tbp + off), ps, lane, N);
+    // ---- backward rows G_1..G_{m-1}: LDS ping-pong + the backward-row pool
+    for (int t = 1; t < m; ++t) {
+        Row<K> g = rev_row_of<K>(tb, cr, r, t);
+        if (t >= 2)
+            set_prev(g, (const K *)Rw[(t - 1) & 1], rband_lo(cr, t - 1), rband_hi(cr, t - 1));
+        row_pass(g, store_to<K>(Rw[t & 1], gpool + gpool_off(cr, t), nullptr), ps, lane, N);
     }
-    // the combines read the forward rows back from the pool
+    // ---- the optimum without a master (no head time or bytes anywhere):
+    // reversed row m at its last cell.  Every master's optimum is at least
+    // this, and none exists when it is infinite.
+    K tn = KeyT<K>::inf;
+    if (m >= 2) {
+        Row<K> g = rev_row_of<K>(tb, cr, r, m);
+        set_prev(g, (const K *)Rw[(m - 1) & 1], rband_lo(cr, m - 1), rband_hi(cr, m - 1));
+        g.lo = g.hi = N - 1;
+        g.lmin = uni(tb.minwinR[(size_t)f8(lane_w(cr.wd, m - 1), 0) * N + (N - 1)]);
+        row_pass(g, store_to<K>(Rw[m & 1], nullptr, nullptr), ps, lane, N);
+        tn = uni_k(Rw[m & 1][0]);
+        if (tn == KeyT<K>::inf) {
+            *T_out = E2_INF64;
+            *mu_out = 0;
+            return;
+        }
+    }
+    // the combines read the backward rows back from their pool
     __builtin_amdgcn_s_waitcnt(0);
     __threadfence_block();
 
-    // ---- combines: master m (its stage ends at N-1), then, after each
-    // reversed row t = 1..m-1 (backward row m+1-t), master m - t
+    // ---- masters in ascending position, each followed by the forward row
+    // it leaves for the next (F_mu: LDS ping-pong + pool + split points).
+    // The sweep stops at the first master whose optimum equals the optimum
+    // without a master: no later master can do better (a head only adds time
+    // and bytes), and ties go to the smaller master.
     K acc = KeyT<K>::inf;
-    {
-        Row<K> rw = fwd_row_of<K>(tb, cr, r, m, m);
-        if (rw.cap > 0) {
-            if (m >= 2)
-                set_prev(rw, (const K *)(pool + pool_off(cr, m - 1)), band_lo(cr, m - 1),
-                         band_hi(cr, m - 1));
-            RowOut<K> ro = store_to<K>(nullptr, nullptr, nullptr);
-            ro.combine = true;
-            ro.last_only = true;
-            ro.mu = m;
-            acc = kmin(acc, row_pass(rw, ro, ps, lane, N));
-        }
-    }
-    for (int t = 1; t < m; ++t) {
-        const uint32_t wc = lane_w(cr.wc, t - 1), wd = lane_w(cr.wd, t - 1);
-        const int c = f8(wd, 0);
-        Row<K> g;
-        g.pr = prefR_row(tb, r, c);
-        g.wr = tb.winR + (uint32_t)(c * N);
-        g.hadd = 0;
-        g.tau = (t >= 2) ? to_k<K>(lane_u64(cr.tauR, t - 1)) : (K)0;
-        g.lo = f8(wd, 8);
-        g.hi = f8(wd, 16);
-        g.kmin = t - 1;
-        g.cap = f8(wc, 24);
-        g.lmin = f8(wc, 16);
-        g.prev = nullptr;
-        g.plo = 1;
-        g.phi = 0;
-        if (t >= 2)
-            set_prev(g, (const K *)Rw[(t - 1) & 1], f8(lane_w(cr.wd, t - 2), 8),
-                     f8(lane_w(cr.wd, t - 2), 16));
-        K *Gt = Rw[t & 1];
-        row_pass(g, store_to<K>(Gt, nullptr, nullptr), ps, lane, N);
-        const int mu = m - t;
+    K key = KeyT<K>::inf;
+    for (int mu = 1; mu <= m; ++mu) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, mu, mu);
         if (rw.cap > 0) {
             if (mu >= 2)
-                set_prev(rw, (const K *)(pool + pool_off(cr, mu - 1)), band_lo(cr, mu - 1),
-                         band_hi(cr, mu - 1));
+                set_prev(rw, (const K *)Rw[(mu - 1) & 1], band_lo(cr, mu - 1), band_hi(cr, mu - 1));
             RowOut<K> ro = store_to<K>(nullptr, nullptr, nullptr);
             ro.combine = true;
-            ro.G = Gt;
-            ro.glo = g.lo;
-            ro.ghi = g.hi;
-            ro.tau_next = to_k<K>(lane_u64(cr.tau, mu));  // link mu -> mu+1
             ro.mu = mu;
+            if (mu == m) {
+                ro.last_only = true;  // the master's stage ends at block N-1
+            } else {
+                const int t = m - mu;  // backward row of devices mu+1..m
+                ro.G = gpool + gpool_off(cr, t);
+                ro.glo = rband_lo(cr, t);
+                ro.ghi = rband_hi(cr, t);
+                ro.tau_next = to_k<K>(lane_u64(cr.tau, mu));  // link mu -> mu+1
+            }
             acc = kmin(acc, row_pass(rw, ro, ps, lane, N));
+            key = wave_min_k(acc);
+            if (m >= 2 && unpack_val(key) == tn) break;
+        }
+        if (mu < m) {
+            Row<K> f = fwd_row_of<K>(tb, cr, r, mu, 0);
+            if (mu >= 2)
+                set_prev(f, (const K *)Rw[(mu - 1) & 1], band_lo(cr, mu - 1), band_hi(cr, mu - 1));
+            const int off = pool_off(cr, mu);
+            row_pass(f, store_to<K>(Rw[mu & 1], pool + off, sm.tbp + off), ps, lane, N);
         }
     }
-    const K key = wave_min_k(acc);
+    // the chosen master's first row reads its forward row back from the pool
+    __builtin_amdgcn_s_waitcnt(0);
+    __threadfence_block();
     const K bestk = unpack_val(key);
     const int best_mu = bestk == KeyT<K>::inf ? 0 : key_low8(key);
     *T_out = to_u64(bestk);
@@ -1086,9 +1144,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     sm.Rw0 = dyn + 2 * N;
     sm.Rw1 = sm.Rw0 + (N + 1);
     sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
-    uint64_t *my_rows = rows + (size_t)blockIdx.x * ((size_t)pool_cells + 2 * (N + 1));
+    uint64_t *my_rows = rows + (size_t)blockIdx.x * (2 * (size_t)pool_cells + 2 * (N + 1));
     sm.pool = my_rows;
-    sm.Ga = my_rows + pool_cells;
+    sm.gpool = my_rows + pool_cells;
+    sm.Ga = sm.gpool + pool_cells;
     sm.Gb = sm.Ga + (N + 1);
     sm.pool_cells = pool_cells;
     static_assert(kClasses == 4, "job mapping below assumes four classes");
@@ -1433,6 +1492,7 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
     uint64_t *my_rows = rows + (size_t)blockIdx.x * ((size_t)pool_cells + 2 * (N + 1));
     sm.pool = my_rows;
+    sm.gpool = nullptr;
     sm.Ga = my_rows + pool_cells;
     sm.Gb = sm.Ga + (N + 1);
     sm.pool_cells = pool_cells;
@@ -2380,7 +2440,7 @@ int e2_dp_lds_tb_cells(int N)
     return kLdsTbCells;
 }
 
-size_t e2_dp_row_words(int N) { return (size_t)e2_dp_pool_cells(N) + 2 * (size_t)(N + 1); }
+size_t e2_dp_row_words(int N) { return 2 * (size_t)e2_dp_pool_cells(N) + 2 * (size_t)(N + 1); }
 
 size_t e2_dp_lds_bytes(int N)
 {

@@ -6,6 +6,8 @@ j-candidates the DP kernel evaluates, split by key width; the roofline's
 over every row, cell and window of the banded decomposition, and the key
 width from a direct scan of every stage that fits memory.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -40,7 +42,16 @@ def _windows(wl):
     return win, winR
 
 
-def _direct(wl, problems, roles, T, master):
+def _free_optima(orc, wl, labels=None, order=None, sizes=None, roles=None):
+    """Optima without a master: the oracle on the same genomes with no head
+    time and no head bytes."""
+    wf = dataclasses.replace(wl, head_flops=np.zeros(2, dtype=np.uint64), head_bytes=0)
+    if order is not None:
+        return orc.eval_population_ordered(wf, order, sizes, roles)["T"]
+    return orc.eval_population(wf)["T"]
+
+
+def _direct(wl, problems, roles, T, master, T0):
     N = wl.n_layer
     win, winR = _windows(wl)
     t, h, tau = e2.e2_quantise(wl.problem_arrays())
@@ -80,12 +91,6 @@ def _direct(wl, problems, roles, T, master):
         assert pool <= (m - 1) * (N - m + 1)
         banded = m <= 64 and pool <= bench.pool_cells(N)
         if banded:
-            for k in range(2, m):                            # forward rows
-                c += cnt(win[0][ch[k - 1]], max(k - 1, flo[k] - c0[k - 1] + 1), flo[k], fhi[k])
-            for mm in range(2, m + 1):                       # combines
-                if cH[mm - 1] > 0:
-                    c += cnt(win[1][ch[mm - 1]], max(mm - 1, flo[mm] - cH[mm - 1] + 1),
-                             flo[mm], fhi[mm])
             for tt in range(2, m):                           # reversed rows
                 kd = m + 1 - tt
                 gl = max(kd - 1, N - (tot - pre[kd - 1]))
@@ -93,6 +98,19 @@ def _direct(wl, problems, roles, T, master):
                 if gh >= gl:
                     c += cnt(winR[ch[kd - 1]], max(tt - 1, N - 1 - gh - c0[kd - 1] + 1),
                              N - 1 - gh, N - 1 - gl)
+            if m >= 2:                                       # the full reversed table's last cell
+                c += cnt(winR[ch[0]], max(m - 1, N - 1 - c0[0] + 1), N - 1, N - 1)
+            # masters in ascending position with the forward row after each,
+            # up to the first master whose optimum is the optimum without one
+            t0 = int(T0[p, q])
+            last = 0 if t0 == INF else (mu if int(T[p, q]) == t0 else m)
+            for mm in range(1, last + 1):
+                if mm >= 2 and cH[mm - 1] > 0:               # combine of master mm
+                    c += cnt(win[1][ch[mm - 1]], max(mm - 1, flo[mm] - cH[mm - 1] + 1),
+                             flo[mm], fhi[mm])
+                if 2 <= mm < last and mm < m:                # forward row mm
+                    c += cnt(win[0][ch[mm - 1]], max(mm - 1, flo[mm] - c0[mm - 1] + 1),
+                             flo[mm], fhi[mm])
             if mu:                                           # chosen master's rows
                 for k in range(max(mu, 2), m):
                     f = int(k == mu)
@@ -129,24 +147,29 @@ def _direct(wl, problems, roles, T, master):
 def test_candidate_counts_match_a_direct_walk(orc, name, P):
     wl = workload.make(name, population=P)
     sol = oracle.eval_population(wl)
+    T0 = _free_optima(orc, wl)
     win, winR, cap = bench.window_tables(wl)
     tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
     probs = bench.label_problems(wl.labels, wl.k_max)
-    cells, c64, c32 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs)
-    assert (c64, c32) == _direct(wl, probs, wl.roles, sol["T"], sol["master"])
+    cells, c64, c32 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs, T0)
+    assert (c64, c32) == _direct(wl, probs, wl.roles, sol["T"], sol["master"], T0)
     assert c64 + c32 > 0
     assert c32 > 0                   # u32 / fp64 keys
+    # both ends of the master sweep occur: optima equal to T0 and above it
+    fin = sol["T"] != INF
+    assert (sol["T"][fin] == T0[fin]).any()
 
 
-def test_reference_path_counts():
+def test_reference_path_counts(orc):
     """Chains with more than 64 devices take one full table per master (u64 keys)."""
     wl = workload.random_small(3, M=70, N=80, P=1, k_max=1, mem_lo_layers=3, mem_hi_layers=30)
     sol = oracle.eval_population(wl)
+    T0 = _free_optima(orc, wl)
     win, winR, cap = bench.window_tables(wl)
     tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
     probs = bench.label_problems(wl.labels, wl.k_max)
-    _, c64, c32 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs)
-    assert (c64, c32) == _direct(wl, probs, wl.roles, sol["T"], sol["master"])
+    _, c64, c32 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs, T0)
+    assert (c64, c32) == _direct(wl, probs, wl.roles, sol["T"], sol["master"], T0)
     assert c64 > 0 and c32 == 0   # the reference path has u64 keys only
 
 
@@ -166,10 +189,11 @@ def test_candidate_counts_of_ordered_genomes(orc, name, P):
                 want.append((p, q, list(op.order[p, lo:hi])))
     assert [(p, q, list(c)) for p, q, c in probs] == want
     sol = oracle.eval_population_ordered(wl, op.order, op.sizes, op.roles)
+    T0 = _free_optima(orc, wl, order=op.order, sizes=op.sizes, roles=op.roles)
     win, winR, cap = bench.window_tables(wl)
     tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
-    cells, c64, c32 = bench.generation_work(wl, probs, op.roles, sol["T"], sol["master"], tabs)
-    assert (c64, c32) == _direct(wl, probs, op.roles, sol["T"], sol["master"])
+    cells, c64, c32 = bench.generation_work(wl, probs, op.roles, sol["T"], sol["master"], tabs, T0)
+    assert (c64, c32) == _direct(wl, probs, op.roles, sol["T"], sol["master"], T0)
     assert c64 + c32 > 0 and cells > 0
 
 
