@@ -6,6 +6,8 @@ genomes (GA step).  Inputs are seeded synthetic workloads; the named ones are
 run at their full population in the same launch configuration the bench
 uses, and checked on sampled individuals where the oracle would take long.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -131,6 +133,37 @@ def test_key_width_boundaries(torch_dev, block_ns, head_ns, zeros):
                      zero_blocks=zeros, mem_lo_layers=2, mem_hi_layers=14, cong_full=True)
         print(f"block_ns={block_ns} head_ns={head_ns} seed={seed}", flush=True)
         _assert_equal(_gpu_all(torch_dev, wl), _oracle_all(wl), tag=f"{block_ns}/{seed}")
+
+
+@pytest.mark.parametrize("seed", [600, 601, 602])
+def test_master_sweep_stops_and_runs_through(torch_dev, seed):
+    """The DP's master sweep stops at the first master whose optimum equals
+    the optimum with no head.  A heavy head gives clusters where it stops at
+    the first device, where it stops later, and where no master reaches that
+    bound (every master is then solved, and the chosen master's first row is
+    read back from the forward pool); all of them equal the oracle."""
+    wl = workload.random_small(seed, M=40, N=60, P=30, k_max=5, mem_lo_layers=2,
+                               mem_hi_layers=20)
+    wl = dataclasses.replace(wl, head_flops=np.array([4 * 10**11] * 2, np.uint64),
+                             head_bytes=2 * 10**8)
+    want = _oracle_all(wl)
+    got = _gpu_all(torch_dev, wl)
+    _assert_equal(got, want, tag=f"sweep {seed}")
+    free = dataclasses.replace(wl, head_flops=np.zeros(2, np.uint64), head_bytes=0)
+    T0 = _gpu_all(torch_dev, free)["T"]
+    assert (T0 == _oracle_all(free)["T"]).all()
+    kinds = set()
+    for p in range(wl.population):
+        for q in range(wl.k_max):
+            ch = np.nonzero(wl.labels[p] == q)[0]
+            if len(ch) == 0 or want["T"][p, q] == INF:
+                continue
+            pos = int(np.nonzero(ch == want["master"][p, q])[0][0]) + 1
+            if want["T"][p, q] == T0[p, q]:
+                kinds.add("stop at 1" if pos == 1 else "stop later")
+            elif 2 <= pos < len(ch):
+                kinds.add("through, master inside")
+    assert kinds == {"stop at 1", "stop later", "through, master inside"}
 
 
 def test_uniform_layers_many_ties(torch_dev):

@@ -1,5 +1,7 @@
 """Pins for the oracle's population solve (cluster extraction + Algorithm 1
 per replica + Eq. 3-5 per individual)."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -76,3 +78,41 @@ def test_named_workload_structure(orc, name):
         if sol["w"][p] != INF:
             assert sol["s_p"][p] != INF and sol["s_d"][p] != INF
     assert n_feasible > 0
+
+
+def test_a_head_never_lowers_the_optimum(orc):
+    """A head only adds time to the master's stage and bytes to its memory
+    test, so every cluster's optimum is at least its optimum with no head
+    (zero head time and bytes, where every master ties), and the two are
+    equal in a cluster exactly when some master reaches that bound.  Both
+    cases occur here; brute force confirms the head-free optimum on small
+    clusters."""
+    big = 0
+    for seed in range(3):
+        wl = workload.random_small(600 + seed, M=40, N=60, P=30, k_max=5, mem_lo_layers=2,
+                                   mem_hi_layers=20)
+        wl = dataclasses.replace(wl, head_flops=np.array([4 * 10**11] * 2, np.uint64),
+                                 head_bytes=2 * 10**8)
+        free = dataclasses.replace(wl, head_flops=np.zeros(2, np.uint64), head_bytes=0)
+        T = orc.eval_population(wl)["T"]
+        T0 = orc.eval_population(free)["T"]
+        assert (T >= T0).all()
+        assert (T[T0 == INF] == INF).all()           # no partition at all
+        fin = T != INF
+        big += int((T[fin] > T0[fin]).sum())
+        assert (T[fin] == T0[fin]).any()
+    assert big > 0
+    # the head-free optimum is the optimum over partitions without a master
+    wl = workload.random_small(9, M=7, N=9, P=4, k_max=2, mem_lo_layers=1, mem_hi_layers=5)
+    free = dataclasses.replace(wl, head_flops=np.zeros(2, np.uint64), head_bytes=0)
+    T0 = orc.eval_population(free)["T"]
+    t, h, tau = orc.quantise(**free.problem_arrays())
+    for p in range(wl.population):
+        for q in range(wl.k_max):
+            ch = np.nonzero(wl.labels[p] == q)[0]
+            if len(ch) == 0:
+                continue
+            r = int(wl.roles[p, q] != 0)
+            tl = np.array([0] + [tau[r, ch[k - 1], ch[k]] for k in range(1, len(ch))], np.uint64)
+            c = brute.Chain(t[r][ch], h[r][ch], tl, free.mem_bytes[ch], free.layer_bytes, 0)
+            assert int(T0[p, q]) == c.solve()[0]
