@@ -56,7 +56,7 @@ struct E2Work {
     uint32_t *counters;  // [0..3] problems listed per chain-length class, [4] next job
     uint32_t *list;      // [4][P * k_max * n_r] problems needing the DP: (p << 8) | q, or
                          //   with every role index searched (p << 12) | (q << 4) | r
-    uint64_t *rows;      // [n_slots][pool + 2 (N+1)] per-wave DP rows
+    uint64_t *rows;      // [n_slots][2 pool + 2 (N+1)] per-wave DP rows
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
     int n_slots;         // waves of the DP kernel
     uint8_t *idle;       // idle-device relaxation: per wave, rows E [M][N+1] u64, their
@@ -67,8 +67,9 @@ struct E2Work {
 
 // Number of DP waves launched for at most `problems` problems of N blocks.
 int e2_dp_slots(int N, int problems);
-// Forward-row pool of one DP wave (u64 cells), its global row storage
-// (u64 per wave) and its dynamic LDS bytes.
+// Cells of one DP wave's forward-row pool (its backward-row pool is as
+// large), its global row storage (u64 per wave: both pools and two full
+// rows) and its dynamic LDS bytes.
 int e2_dp_pool_cells(int N);
 int e2_dp_lds_tb_cells(int N);
 size_t e2_dp_row_words(int N);

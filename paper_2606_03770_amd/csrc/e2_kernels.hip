@@ -1123,7 +1123,7 @@ __device__ __forceinline__ int build_chain(const E2Genomes &gen, int p, int q, i
 // in list order through an atomic counter and exit when the list is
 // exhausted.  LDS: split-point pairs (N x 16 B) and the split-point bytes
 // of the forward-row pool; the row values live in a per-wave global region
-// (pool_cells + 2 (N+1) u64).
+// (forward pool, backward pool, two full rows: 2 pool_cells + 2 (N+1) u64).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_dp(E2Tables tb, int k_max, int pool_cells,
                                            E2Genomes gen, const uint8_t *__restrict__ roles,
@@ -1490,6 +1490,8 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     sm.Rw0 = dyn + 2 * N;
     sm.Rw1 = sm.Rw0 + (N + 1);
     sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
+    // this kernel keeps no backward-row pool: its regions are packed tighter
+    // than k_dp's within the same allocation
     uint64_t *my_rows = rows + (size_t)blockIdx.x * ((size_t)pool_cells + 2 * (N + 1));
     sm.pool = my_rows;
     sm.gpool = nullptr;
