@@ -659,13 +659,23 @@ def roofline(t, steps, traffic):
 LIB_SOURCES = ("e2_api.hip", "e2_internal.h", "e2_kernels.hip")
 
 
+def code_text(text: str) -> str:
+    """C++ source without its comments and blank space: what the compiler
+    sees, so that a comment edit keeps a profile current."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_hash() -> str:
-    """Hash of the library sources that decide what the DP kernel does."""
+    """Hash of the library sources that decide what the DP kernel does
+    (their code, comments and layout aside)."""
     import hashlib
     h = hashlib.sha256()
     for f in LIB_SOURCES:
-        with open(os.path.join(ROOT, "paper_2606_03770_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2606_03770_amd", "csrc", f)) as fh:
+            h.update(code_text(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

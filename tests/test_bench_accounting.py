@@ -202,3 +202,12 @@ def test_window_tables_match_brute_force():
     win, winR, _ = bench.window_tables(wl)
     w2, wR2 = _windows(wl)
     assert (win == w2).all() and (winR == wR2).all()
+
+
+def test_source_hash_ignores_comments_and_layout():
+    """The profile records are keyed by the code the compiler sees."""
+    a = "int f(int x) { return x + 1; } // one\n/* two\n lines */ int g;"
+    b = "int f(int x)  {\n  return x + 1;\n}\n\nint g;"
+    assert bench.code_text(a) == bench.code_text(b)
+    assert bench.code_text(a) != bench.code_text(a.replace("x + 1", "x + 2"))
+    assert len(bench.source_hash()) == 16
