@@ -4,10 +4,10 @@
 //   k_extract     one wave per individual: cluster sizes, a necessary
 //                 memory/size pre-check, the list of clusters that need the
 //                 DP (bucketed by chain length); INF results for the others
-//   k_dp          persistent waves: each takes the next listed cluster,
-//                 rebuilds its device chain from the genome, runs the
-//                 bottleneck DP of Algorithm 1 / Eq. 1-2 for every master
-//                 position, picks the best master, backtracks and writes
+//   k_dp          persistent waves: each takes its share of the listed
+//                 clusters, rebuilds a device chain from the genome, runs the
+//                 bottleneck DP of Algorithm 1 / Eq. 1-2 over the master
+//                 positions, picks the best master, backtracks and writes
 //                 T, Lambda, master and per-device block counts
 //   k_fitness     Eq. 3-5 per individual with the QoS floor (one wave per
 //                 individual, lanes over clusters)
@@ -1119,9 +1119,9 @@ __device__ __forceinline__ int build_chain(const E2Genomes &gen, int p, int q, i
 }
 
 // ---------------------------------------------------------------------------
-// Persistent DP kernel: one wave per workgroup; waves take listed problems
-// in list order through an atomic counter and exit when the list is
-// exhausted.  LDS: split-point pairs (N x 16 B) and the split-point bytes
+// Persistent DP kernel: one wave per workgroup; wave w of W solves listed
+// problems w, w + W, w + 2W, ... (the list runs longest chains first, so
+// every wave gets a like mix) and exits past the end of the list.  LDS: split-point pairs (N x 16 B) and the split-point bytes
 // of the forward-row pool; the row values live in a per-wave global region
 // (forward pool, backward pool, two full rows: 2 pool_cells + 2 (N+1) u64).
 // ---------------------------------------------------------------------------
@@ -1136,7 +1136,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     __shared__ uint8_t chain[256];
     __shared__ uint8_t start[256];
     __shared__ uint8_t last_tb;
-    __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
     DpSmem sm;
@@ -1154,12 +1153,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
 
-    for (;;) {
-        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
-        __syncthreads();
+    // wave w takes problems w, w + W, w + 2W, ... of the list (W waves, all
+    // resident at once): each wave gets a like mix of the longest-first
+    // classes, with no shared counter to contend for
+    for (uint32_t job = blockIdx.x; job < n_jobs; job += gridDim.x) {
         uint32_t idx = job;
-        __syncthreads();
-        if (idx >= n_jobs) break;
         // classes in order, longest chains first
         int cls = 0;
         if (idx >= n0) { idx -= n0; cls = 1;
@@ -1482,7 +1480,6 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     extern __shared__ uint64_t dyn[];
     __shared__ uint8_t chain[256];
     __shared__ uint8_t start[256];
-    __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
     DpSmem sm;
@@ -1500,12 +1497,9 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     sm.pool_cells = pool_cells;
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
-    for (;;) {
-        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
-        __syncthreads();
+    // wave w takes problems w, w + W, w + 2W, ... (as in k_dp)
+    for (uint32_t job = blockIdx.x; job < n_jobs; job += gridDim.x) {
         uint32_t idx = job;
-        __syncthreads();
-        if (idx >= n_jobs) break;
         int cls = 0;
         if (idx >= n0) { idx -= n0; cls = 1;
             if (idx >= n1) { idx -= n1; cls = 2;
@@ -1749,7 +1743,6 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
     extern __shared__ uint64_t A[];  // [N+1], then S [N+1]
     __shared__ uint8_t chain[256];
     __shared__ uint8_t sizes[256];
-    __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N, X = N + 1;
     uint64_t *S = A + X;
@@ -1759,12 +1752,9 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
     uint8_t *Ej = reinterpret_cast<uint8_t *>(Ek + (size_t)M * X);
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
-    for (;;) {
-        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
-        __syncthreads();
+    // wave w takes problems w, w + W, w + 2W, ... (as in k_dp)
+    for (uint32_t job = blockIdx.x; job < n_jobs; job += gridDim.x) {
         uint32_t idx = job;
-        __syncthreads();
-        if (idx >= n_jobs) break;
         int cls = 0;
         if (idx >= n0) { idx -= n0; cls = 1;
             if (idx >= n1) { idx -= n1; cls = 2;
