@@ -1480,6 +1480,7 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     extern __shared__ uint64_t dyn[];
     __shared__ uint8_t chain[256];
     __shared__ uint8_t start[256];
+    __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
     DpSmem sm;
@@ -1497,9 +1498,14 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     sm.pool_cells = pool_cells;
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
-    // wave w takes problems w, w + W, w + 2W, ... (as in k_dp)
-    for (uint32_t job = blockIdx.x; job < n_jobs; job += gridDim.x) {
+    // waves take the next listed problem from a shared counter: these grids
+    // need not be resident at once, and their problems vary more in cost
+    for (;;) {
+        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
+        __syncthreads();
         uint32_t idx = job;
+        __syncthreads();
+        if (idx >= n_jobs) break;
         int cls = 0;
         if (idx >= n0) { idx -= n0; cls = 1;
             if (idx >= n1) { idx -= n1; cls = 2;
@@ -1743,6 +1749,7 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
     extern __shared__ uint64_t A[];  // [N+1], then S [N+1]
     __shared__ uint8_t chain[256];
     __shared__ uint8_t sizes[256];
+    __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N, X = N + 1;
     uint64_t *S = A + X;
@@ -1752,9 +1759,14 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
     uint8_t *Ej = reinterpret_cast<uint8_t *>(Ek + (size_t)M * X);
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
-    // wave w takes problems w, w + W, w + 2W, ... (as in k_dp)
-    for (uint32_t job = blockIdx.x; job < n_jobs; job += gridDim.x) {
+    // waves take the next listed problem from a shared counter: these grids
+    // need not be resident at once, and their problems vary more in cost
+    for (;;) {
+        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
+        __syncthreads();
         uint32_t idx = job;
+        __syncthreads();
+        if (idx >= n_jobs) break;
         int cls = 0;
         if (idx >= n0) { idx -= n0; cls = 1;
             if (idx >= n1) { idx -= n1; cls = 2;
