@@ -773,13 +773,24 @@ __device__ __forceinline__ int rband_lo(const ChainRegs &cr, int t) { return f8(
 __device__ __forceinline__ int rband_hi(const ChainRegs &cr, int t) { return f8(lane_w(cr.wd, t - 1), 16); }
 __device__ __forceinline__ int gpool_off(const ChainRegs &cr, int t) { return (int)lane_w(cr.we, t - 1); }
 
+// Inclusive prefix sum over the wave with DPP moves only (no LDS round
+// trips): prefixes of 4 lanes within each 16-lane row from the inputs, then
+// of 8 and 16 lanes (row shifts by 4 and 8 on the upper banks), then the
+// totals of rows 0 and 2 into rows 1 and 3 (broadcast of lane 15) and of
+// rows 0-1 into rows 2 and 3 (broadcast of lane 31).  Disabled lanes and
+// shifts across a row start contribute 0.
 __device__ __forceinline__ int scan_incl_i32(int x, int lane)
 {
-    for (int d = 1; d < kWave; d <<= 1) {
-        const int y = __shfl_up(x, d, kWave);
-        if (lane >= d) x += y;
-    }
-    return x;
+    (void)lane;
+    int s = x;
+    s += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);  // row_shr:1
+    s += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);  // row_shr:2
+    s += __builtin_amdgcn_update_dpp(0, x, 0x113, 0xf, 0xf, true);  // row_shr:3
+    s += __builtin_amdgcn_update_dpp(0, s, 0x114, 0xf, 0xe, true);  // row_shr:4, lanes 4-15
+    s += __builtin_amdgcn_update_dpp(0, s, 0x118, 0xf, 0xc, true);  // row_shr:8, lanes 8-15
+    s += __builtin_amdgcn_update_dpp(0, s, 0x142, 0xa, 0xf, false); // row_bcast:15, rows 1, 3
+    s += __builtin_amdgcn_update_dpp(0, s, 0x143, 0xc, 0xf, false); // row_bcast:31, rows 2, 3
+    return s;
 }
 
 struct DpSmem {
