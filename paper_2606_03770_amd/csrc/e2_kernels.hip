@@ -574,22 +574,24 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
     const int cl = lane / S;
     const int jmin = max(rw.kmin, rw.lo - rw.cap + 1);
     // first pass's cell loads go out before the split points are built
-    int w_nx = E2_NO_START;
-    uint64_t p_nx = 0;
+    // (lanes past the row load its last cell, and their results are unused)
+    int w_nx;
+    uint64_t p_nx;
     K b_nx = 0;
     {
-        const int i = rw.lo + cl;
-        if (i <= rw.hi) {
-            w_nx = rw.wr[i];
-            p_nx = rw.pr[i + 1];
-            if (ro.combine) b_nx = combine_b(i, N, ro);
-        }
+        const int i = min(rw.lo + cl, rw.hi);
+        w_nx = rw.wr[i];
+        p_nx = rw.pr[i + 1];
+        if (ro.combine) b_nx = combine_b(i, N, ro);
     }
     // both loads of an entry go out before either is waited for: the
     // previous-row value comes from a clamped index and is replaced by INF
     // outside the previous band
     const int pspan = rw.phi - rw.plo;  // < 0: empty previous band (slot 0 is read, unused)
-    for (int j = jmin + lane; j <= rw.hi; j += kWave) {
+    // a uniform loop: lanes past the row repeat its last entry, writing the
+    // same values to the same slot
+    for (int j0 = jmin; j0 <= rw.hi; j0 += kWave) {
+        const int j = min(j0 + lane, rw.hi);
         const int px = j - 1 - rw.plo;
         const int pxc = max(0, min(px, pspan));
         const uint64_t prj = rw.pr[j];
@@ -622,10 +624,11 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
         const int w = w_nx;
         const uint64_t p1 = p_nx;
         const K b = b_nx;
-        if (i + CPP <= rw.hi) {
-            w_nx = rw.wr[i + CPP];
-            p_nx = rw.pr[i + CPP + 1];
-            if (ro.combine) b_nx = combine_b(i + CPP, N, ro);
+        if (base + CPP <= rw.hi) {  // a next pass exists (uniform)
+            const int in = min(i + CPP, rw.hi);
+            w_nx = rw.wr[in];
+            p_nx = rw.pr[in + 1];
+            if (ro.combine) b_nx = combine_b(in, N, ro);
         }
         const bool act = i <= rw.hi && w != (int)E2_NO_START;
         const int ie = act ? i : i_idle;
