@@ -534,8 +534,10 @@ template <typename K> __device__ __forceinline__ K cand(const PS<K> &e, K si1)
 template <typename K> __device__ __forceinline__ K combine_b(int i, int N, const RowOut<K> &ro)
 {
     if (ro.last_only) return (i == N - 1) ? (K)0 : KeyT<K>::inf;
+    // the load comes from a clamped index, so that it is not put under a branch
     const int x = N - 2 - i;
-    return (x >= ro.glo && x <= ro.ghi) ? kmax(ro.G[x - ro.glo], ro.tau_next) : KeyT<K>::inf;
+    const K g = ro.G[max(0, min(x - ro.glo, ro.ghi - ro.glo))];
+    return (x >= ro.glo && x <= ro.ghi) ? kmax(g, ro.tau_next) : KeyT<K>::inf;
 }
 template <typename K> __device__ __forceinline__ K combine_key(K v, K b, int mu)
 {
@@ -619,23 +621,26 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
     const int t_safe = Lm / S;
     const int i_idle = jmin + (Lm > 0 ? Lm - 1 : 0);  // idle lanes: in-range reads
     K acc = KeyT<K>::inf;
+    // Lanes past the row's last cell take that cell again: the S lanes of a
+    // cell hold the same reduced key, so every lane stores its cell's result
+    // (copies write the same value to the same slot) and no store is put
+    // under a branch.
     for (int base = rw.lo; base <= rw.hi; base += CPP) {
-        const int i = base + cl;
+        const int i = min(base + cl, rw.hi);
         const int w = w_nx;
         const uint64_t p1 = p_nx;
         const K b = b_nx;
         if (base + CPP <= rw.hi) {  // a next pass exists (uniform)
-            const int in = min(i + CPP, rw.hi);
+            const int in = min(base + CPP + cl, rw.hi);
             w_nx = rw.wr[in];
             p_nx = rw.pr[in + 1];
             if (ro.combine) b_nx = combine_b(in, N, ro);
         }
-        const bool act = i <= rw.hi && w != (int)E2_NO_START;
+        const bool act = w != (int)E2_NO_START;
         const int ie = act ? i : i_idle;
         const int jlo = act ? max(w, jmin) : jmin;
         const K si1 = (K)((p1 + rw.hadd) << 8);
         const K best = scan_cell<S>(ps, ie, jlo, o, si1, t_safe, t_all);
-        if (o != 0 || i > rw.hi) continue;
         const K v = act ? unpack_val(best) : KeyT<K>::inf;
         if (!ro.combine) {
             ro.vals[i - rw.lo] = v;
@@ -656,7 +661,8 @@ __device__ __forceinline__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<
 {
     if (rw.prev == nullptr) {  // first device: Eq. 2, no split point
         K acc = KeyT<K>::inf;
-        for (int i = rw.lo + lane; i <= rw.hi; i += kWave) {
+        for (int i0 = rw.lo; i0 <= rw.hi; i0 += kWave) {
+            const int i = min(i0 + lane, rw.hi);  // copies of the last cell past the row
             const K v = (rw.wr[i] == 0) ? (K)(rw.pr[i + 1] + rw.hadd) : KeyT<K>::inf;
             if (!ro.combine) {
                 ro.vals[i - rw.lo] = v;
