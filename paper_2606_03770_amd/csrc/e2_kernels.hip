@@ -531,13 +531,23 @@ template <typename K> __device__ __forceinline__ K cand(const PS<K> &e, K si1)
 {
     return kmax(e.a, (K)(si1 - e.s));
 }
+// v where keep holds, else INF, without a branch (all ones for integer keys,
+// the bit pattern of +infinity for doubles)
+template <typename K> __device__ __forceinline__ K inf_unless(K v, bool keep)
+{
+    if constexpr (__is_same(K, double))
+        return __builtin_bit_cast(double, keep ? __builtin_bit_cast(uint64_t, v)
+                                               : 0x7FF0000000000000ull);
+    else return v | ((K)0 - (K)!keep);
+}
 template <typename K> __device__ __forceinline__ K combine_b(int i, int N, const RowOut<K> &ro)
 {
     if (ro.last_only) return (i == N - 1) ? (K)0 : KeyT<K>::inf;
-    // the load comes from a clamped index, so that it is not put under a branch
+    // the load comes from a clamped index and the INF outside the band is
+    // selected on the bit pattern, so that the load is not put under a branch
     const int x = N - 2 - i;
     const K g = ro.G[max(0, min(x - ro.glo, ro.ghi - ro.glo))];
-    return (x >= ro.glo && x <= ro.ghi) ? kmax(g, ro.tau_next) : KeyT<K>::inf;
+    return kmax(inf_unless(g, x >= ro.glo && x <= ro.ghi), ro.tau_next);
 }
 template <typename K> __device__ __forceinline__ K combine_key(K v, K b, int mu)
 {
@@ -663,7 +673,7 @@ __device__ __forceinline__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<
         K acc = KeyT<K>::inf;
         for (int i0 = rw.lo; i0 <= rw.hi; i0 += kWave) {
             const int i = min(i0 + lane, rw.hi);  // copies of the last cell past the row
-            const K v = (rw.wr[i] == 0) ? (K)(rw.pr[i + 1] + rw.hadd) : KeyT<K>::inf;
+            const K v = inf_unless((K)(rw.pr[i + 1] + rw.hadd), rw.wr[i] == 0);
             if (!ro.combine) {
                 ro.vals[i - rw.lo] = v;
                 if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
