@@ -337,8 +337,9 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
 // prefix sums; the 32-bit path keeps the low 32 bits of (P << 8), whose
 // differences are exact because every visited stage cost is below 2^24.
 //
-// Lane mapping: S lanes per cell (S = 4 for at most 16 cells, 2 for at most
-// 32, else 1); lane o of a cell visits j = i - o - S t for t = 0, 1, ...
+// Lane mapping: S lanes per cell (S = 8 for at most 8 cells, 4 for at most
+// 16, 2 for at most 32, else 1); lane o of a cell visits j = i - o - S t for
+// t = 0, 1, ...
 // With L = min(cap, hi - jmin + 1) an upper bound and Lm a lower bound of
 // the cells' window lengths, the first floor(Lm / S) steps stay inside
 // every window and run unclamped (four at a time); the remaining steps
@@ -575,6 +576,7 @@ __device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K
     }
     if (S >= 2) best = kmin(best, dppk<0xb1>(best));
     if (S >= 4) best = kmin(best, dppk<0x4e>(best));
+    if (S >= 8) best = kmin(best, dppk<0x141>(best));  // row_half_mirror: the two quads
     return best;
 }
 
@@ -689,6 +691,7 @@ __device__ __forceinline__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<
         __syncthreads();
         return KeyT<K>::inf;
     }
+    if (n <= 8) return row_pass_s<8>(rw, ro, ps, lane, N);
     if (n <= 16) return row_pass_s<4>(rw, ro, ps, lane, N);
     if (n <= 32) return row_pass_s<2>(rw, ro, ps, lane, N);
     return row_pass_s<1>(rw, ro, ps, lane, N);
