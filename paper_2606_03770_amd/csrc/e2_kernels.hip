@@ -1384,83 +1384,111 @@ __device__ __forceinline__ void ft_row(const uint64_t *pr, const uint8_t *wr, ui
     __syncthreads();
 }
 
-// The finishing-time DP by the same banded decomposition as dp_banded:
-// forward rows F_1..F_{m-1} (no master) in the wave's global pool, reversed
-// rows G_t over the last t devices in the LDS ping-pong, per master mu
+// The finishing-time DP by the same banded decomposition and schedule as
+// dp_banded: reversed rows G_t over the last t devices in the wave's
+// backward-row pool, the head-free optimum T0 from the full reversed
+// table's last cell, then masters in ascending position with
 //   T_mu = min_i H_mu(i) + tau(mu, mu+1) + G_{m-mu}(N-2-i)
-// with H_mu the master's forward row (head time and bytes) over F_{mu-1};
-// the smallest mu with the least T_mu wins.  Rows mu*..m-1 of its table are
-// recomputed with split points and the back tracing fills start[].  Every
-// in-band cell's value equals the full table's (bands depend on memory
-// only), so the result is that of one full table per master.
+// (H_mu the master's forward row, head time and bytes, over F_{mu-1}), each
+// followed by the forward row F_mu (no master) in the forward pool.  Since
+// T_mu >= T0 + head(mu), the sweep stops once the best is at most T0 plus
+// the least head time of the masters still ahead; the smallest mu with the
+// least T_mu wins.  Rows mu*..m-1 of its table are recomputed with split
+// points and the back tracing fills start[].  Every in-band cell's value
+// equals the full table's (bands depend on memory only), so the result is
+// that of one full table per master.
 __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs &cr, int r,
                              int m, int lane, uint64_t *T_out, int *mu_out, uint8_t *start)
 {
     const int N = tb.N, M = tb.M;
     uint64_t *pool = sm.pool;
+    uint64_t *gpool = sm.gpool;
     uint64_t *H = reinterpret_cast<uint64_t *>(sm.ps);  // N cells
     uint64_t *Rw[2] = {sm.Rw0, sm.Rw1};
-    // ---- F_1..F_{m-1}, their split points kept for the rows below mu*
-    for (int k = 1; k < m; ++k) {
-        const uint32_t wa = lane_w(cr.wa, k - 1);
-        const int c = f8(wa, 0);
-        const uint64_t tau = k >= 2 ? lane_u64(cr.tau, k - 1) : 0;
-        ft_row(pref_row(tb, r, c), win_row(tb, 0, c), 0, tau, band_lo(cr, k), band_hi(cr, k),
-               k - 1, k >= 2 ? pool + pool_off(cr, k - 1) : nullptr,
-               k >= 2 ? band_lo(cr, k - 1) : 1, k >= 2 ? band_hi(cr, k - 1) : 0,
-               pool + pool_off(cr, k), k >= 2 ? sm.tbp + pool_off(cr, k) : nullptr, lane);
+    // ---- backward rows G_1..G_{m-1} in the backward-row pool: reversed row t
+    // is device m+1-t holding reversed blocks y..x after the t-1 devices
+    // behind it
+    for (int t = 1; t < m; ++t) {
+        const uint32_t wd = lane_w(cr.wd, t - 1);
+        const int c = f8(wd, 0);
+        const uint64_t tau = t >= 2 ? lane_u64(cr.tauR, t - 1) : 0;
+        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, tau, f8(wd, 8), f8(wd, 16),
+               t - 1, t >= 2 ? gpool + gpool_off(cr, t - 1) : nullptr,
+               t >= 2 ? rband_lo(cr, t - 1) : 1, t >= 2 ? rband_hi(cr, t - 1) : 0,
+               gpool + gpool_off(cr, t), nullptr, lane);
     }
-    // ---- masters m, then after each reversed row t the master m - t
+    // ---- T0, the least end-to-end time with no head anywhere: reversed row
+    // m at its last cell.  A master's optimum is at least T0 plus its head
+    // time (the head time is added once, its bytes only narrow windows).
+    uint64_t t0 = E2_INF64;
+    if (m >= 2) {
+        const int c = f8(lane_w(cr.wd, m - 1), 0);
+        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, lane_u64(cr.tauR, m - 1),
+               N - 1, N - 1, m - 1, gpool + gpool_off(cr, m - 1), rband_lo(cr, m - 1),
+               rband_hi(cr, m - 1), H, nullptr, lane);
+        t0 = uni64(H[0]);
+        if (t0 == E2_INF64) {
+            *T_out = E2_INF64;
+            *mu_out = 0;
+            return;
+        }
+    }
+    // head time of each position able to take the head (INF otherwise)
+    const uint64_t h_cap = (lane < m && f8(cr.wa, 16) != 0) ? cr.head : E2_INF64;
+
+    // ---- masters in ascending position, each followed by F_mu (pool, split
+    // points kept for the rows below mu*).  The sweep stops once the best is
+    // at most T0 plus the least head time of the masters still ahead: none
+    // of them can do better, and ties go to the smaller master.
     uint64_t best = E2_INF64;
     int best_mu = 0;
-    int g_lo = 1, g_hi = 0;  // band of the last reversed row (reversed cells)
-    for (int t = 0; t < m; ++t) {
-        const int mu = m - t;
-        if (t >= 1) {
-            // reversed row t: device m+1-t holds reversed blocks y..x after
-            // the t-1 devices behind it
-            const uint32_t wd = lane_w(cr.wd, t - 1), wc = lane_w(cr.wc, t - 1);
-            const int c = f8(wd, 0);
-            const int lo = f8(wd, 8), hi = f8(wd, 16);
-            const uint64_t tau = t >= 2 ? lane_u64(cr.tauR, t - 1) : 0;
-            (void)wc;
-            ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, tau, lo, hi, t - 1,
-                   t >= 2 ? Rw[(t - 1) & 1] : nullptr, g_lo, g_hi, Rw[t & 1], nullptr, lane);
-            g_lo = lo;
-            g_hi = hi;
-        }
+    for (int mu = 1; mu <= m; ++mu) {
         const uint32_t wa = lane_w(cr.wa, mu - 1);
         const int c = f8(wa, 0);
-        if (f8(wa, 16) == 0) continue;  // the master's stage cannot hold the head
-        const uint64_t tau = mu >= 2 ? lane_u64(cr.tau, mu - 1) : 0;
-        const int lo = band_lo(cr, mu), hi = mu == m ? N - 1 : band_hi(cr, mu);
-        const int hlo = mu == m ? N - 1 : lo;
-        ft_row(pref_row(tb, r, c), win_row(tb, 1, c), uni64(tb.head[r * M + c]), tau, hlo, hi,
-               mu - 1, mu >= 2 ? pool + pool_off(cr, mu - 1) : nullptr,
-               mu >= 2 ? band_lo(cr, mu - 1) : 1, mu >= 2 ? band_hi(cr, mu - 1) : 0, H, nullptr,
-               lane);
-        uint64_t tm = E2_INF64;
-        if (mu == m) {
-            tm = H[0];
-        } else {
-            const uint64_t tn = lane_u64(cr.tau, mu);  // link mu -> mu+1
-            const uint64_t *G = Rw[t & 1];
-            for (int i = hlo + lane; i <= hi; i += kWave) {
-                const uint64_t h = H[i - hlo];
-                const int x = N - 2 - i;
-                if (h == E2_INF64 || tn == E2_INF64 || x < g_lo || x > g_hi) continue;
-                const uint64_t g = G[x - g_lo];
-                if (g == E2_INF64) continue;
-                const uint64_t v = h + tn + g;
-                tm = v < tm ? v : tm;
+        if (f8(wa, 16) != 0) {
+            const uint64_t tau = mu >= 2 ? lane_u64(cr.tau, mu - 1) : 0;
+            const int lo = band_lo(cr, mu), hi = mu == m ? N - 1 : band_hi(cr, mu);
+            const int hlo = mu == m ? N - 1 : lo;
+            ft_row(pref_row(tb, r, c), win_row(tb, 1, c), uni64(tb.head[r * M + c]), tau, hlo,
+                   hi, mu - 1, mu >= 2 ? pool + pool_off(cr, mu - 1) : nullptr,
+                   mu >= 2 ? band_lo(cr, mu - 1) : 1, mu >= 2 ? band_hi(cr, mu - 1) : 0, H,
+                   nullptr, lane);
+            uint64_t tm = E2_INF64;
+            if (mu == m) {
+                tm = H[0];
+            } else {
+                const int t = m - mu;  // backward row of devices mu+1..m
+                const uint64_t tn = lane_u64(cr.tau, mu);  // link mu -> mu+1
+                const uint64_t *G = gpool + gpool_off(cr, t);
+                const int g_lo = rband_lo(cr, t), g_hi = rband_hi(cr, t);
+                for (int i = hlo + lane; i <= hi; i += kWave) {
+                    const uint64_t h = H[i - hlo];
+                    const int x = N - 2 - i;
+                    if (h == E2_INF64 || tn == E2_INF64 || x < g_lo || x > g_hi) continue;
+                    const uint64_t g = G[x - g_lo];
+                    if (g == E2_INF64) continue;
+                    const uint64_t v = h + tn + g;
+                    tm = v < tm ? v : tm;
+                }
+                tm = wave_min_u64(tm);
             }
-            tm = wave_min_u64(tm);
+            if (tm < best) {  // ascending positions: the smaller master keeps ties
+                best = tm;
+                best_mu = mu;
+            }
+            __syncthreads();
         }
-        if (tm <= best && tm != E2_INF64) {  // the smaller master wins ties
-            best = tm;
-            best_mu = mu;
+        if (m >= 2 && best != E2_INF64) {
+            const uint64_t ahead = wave_min_u64(lane >= mu ? h_cap : E2_INF64);
+            if (ahead == E2_INF64 || best <= t0 + ahead) break;
         }
-        __syncthreads();
+        if (mu < m) {
+            const uint64_t tau = mu >= 2 ? lane_u64(cr.tau, mu - 1) : 0;
+            ft_row(pref_row(tb, r, c), win_row(tb, 0, c), 0, tau, band_lo(cr, mu), band_hi(cr, mu),
+                   mu - 1, mu >= 2 ? pool + pool_off(cr, mu - 1) : nullptr,
+                   mu >= 2 ? band_lo(cr, mu - 1) : 1, mu >= 2 ? band_hi(cr, mu - 1) : 0,
+                   pool + pool_off(cr, mu), mu >= 2 ? sm.tbp + pool_off(cr, mu) : nullptr, lane);
+        }
     }
     *T_out = best;
     *mu_out = best_mu;
@@ -1521,12 +1549,10 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     sm.Rw0 = dyn + 2 * N;
     sm.Rw1 = sm.Rw0 + (N + 1);
     sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
-    // this kernel keeps no backward-row pool: its regions are packed tighter
-    // than k_dp's within the same allocation
-    uint64_t *my_rows = rows + (size_t)blockIdx.x * ((size_t)pool_cells + 2 * (N + 1));
+    uint64_t *my_rows = rows + (size_t)blockIdx.x * (2 * (size_t)pool_cells + 2 * (N + 1));
     sm.pool = my_rows;
-    sm.gpool = nullptr;
-    sm.Ga = my_rows + pool_cells;
+    sm.gpool = my_rows + pool_cells;
+    sm.Ga = sm.gpool + pool_cells;
     sm.Gb = sm.Ga + (N + 1);
     sm.pool_cells = pool_cells;
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
