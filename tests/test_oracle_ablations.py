@@ -64,6 +64,32 @@ def test_ft_orders_against_the_bottleneck_dp(orc):
             assert L_ft <= L_bn and T_ft >= T_bn
 
 
+def test_ft_head_adds_at_least_the_masters_head_time(orc):
+    """The head's time is added once, to the master's stage, and its bytes
+    only narrow that stage's window: the least end-to-end time with a head
+    is at least the head-free one plus the chosen master's head time, with
+    equality when the head-free optimum fits with the head on that device
+    (here: ample memory)."""
+    rng = np.random.default_rng(19)
+    equal = 0
+    for _ in range(300):
+        m, N = int(rng.integers(1, 6)), int(rng.integers(1, 12))
+        tk, hk, tl, mem, W, HB = rand_chain(rng, m, N)
+        T, L, mu, _ = orc.dp_pipe_ft(tk, hk, tl, mem, W, HB)
+        T0, L0, _, _ = orc.dp_pipe_ft(tk, np.zeros_like(hk), tl, mem, W, 0)
+        assert L0 != INF or L == INF                  # no partition at all
+        if L == INF:
+            continue
+        assert L >= L0 + int(hk[mu - 1]) >= L0 + int(hk.min())
+        # with memory to spare the head-free partitions stay feasible
+        roomy = np.full(m, 10**9, np.uint64)
+        _, Lr, mur, _ = orc.dp_pipe_ft(tk, hk, tl, roomy, W, HB)
+        _, L0r, _, _ = orc.dp_pipe_ft(tk, np.zeros_like(hk), tl, roomy, W, 0)
+        assert Lr == L0r + int(hk.min()) and int(hk[mur - 1]) == int(hk.min())
+        equal += L == L0 + int(hk[mu - 1])
+    assert equal > 50
+
+
 def test_ft_identical_devices_closed_form(orc):
     """Identical devices, free links, no head, ample memory: every partition
     takes N t end to end, so every master and split ties; the smallest-j rule
