@@ -588,7 +588,7 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
     const int cl = lane / S;
     const int jmin = max(rw.kmin, rw.lo - rw.cap + 1);
     // first pass's cell loads go out before the split points are built
-    // (lanes past the row load its last cell, and their results are unused)
+    // (lanes past the row load its last cell, which they compute again)
     int w_nx;
     uint64_t p_nx;
     K b_nx = 0;
