@@ -102,6 +102,7 @@ __global__ void k_init(uint32_t *counters)
 // early; each workgroup reserves its range of each segment with one atomic.
 // ---------------------------------------------------------------------------
 constexpr int kEG = 8;       // genomes per extraction workgroup
+constexpr int kDynTailShift = 2;  // the last 1/4 of the DP list is taken dynamically
 constexpr int kClasses = 4;  // chain-length classes: m >= 16, 12..15, 8..11, < 8
 
 __device__ __forceinline__ int size_class(int m)
@@ -1186,10 +1187,25 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
 
-    // wave w takes problems w, w + W, w + 2W, ... of the list (W waves, all
-    // resident at once): each wave gets a like mix of the longest-first
-    // classes, with no shared counter to contend for
-    for (uint32_t job = blockIdx.x; job < n_jobs; job += gridDim.x) {
+    // The list runs longest chains first.  Its first part is split statically
+    // (wave w of W takes problems w, w + W, w + 2W, ...: every wave gets a
+    // like mix, with no shared counter to contend for); the short problems
+    // of the last part go to whichever wave is free, from a shared counter,
+    // which evens out the waves' finishing times.
+    const uint32_t n_static = n_jobs - (n_jobs >> kDynTailShift);
+    auto take = [&](uint32_t done) -> uint32_t {
+        if (done + gridDim.x < n_static) return done + gridDim.x;
+        uint32_t v = 0;
+        if (lane == 0) v = atomicAdd(&counters[kClasses], 1u);
+        return n_static + (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+    };
+    uint32_t first = blockIdx.x;
+    if (first >= n_static) {
+        uint32_t v = 0;
+        if (lane == 0) v = atomicAdd(&counters[kClasses], 1u);
+        first = n_static + (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+    }
+    for (uint32_t job = first; job < n_jobs; job = take(job)) {
         uint32_t idx = job;
         // classes in order, longest chains first
         int cls = 0;
