@@ -102,7 +102,8 @@ __global__ void k_init(uint32_t *counters)
 // early; each workgroup reserves its range of each segment with one atomic.
 // ---------------------------------------------------------------------------
 constexpr int kEG = 8;       // genomes per extraction workgroup
-constexpr int kDynTailShift = 2;  // the last 1/4 of the DP list is taken dynamically
+constexpr int kDynTailShift = 2;  // the last 1/4 of the DP list is taken dynamically ...
+constexpr uint32_t kDynTailMinPerWave = 16;  // ... with at least this many problems per wave
 constexpr int kClasses = 4;  // chain-length classes: m >= 16, 12..15, 8..11, < 8
 
 __device__ __forceinline__ int size_class(int m)
@@ -1189,10 +1190,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
 
     // The list runs longest chains first.  Its first part is split statically
     // (wave w of W takes problems w, w + W, w + 2W, ...: every wave gets a
-    // like mix, with no shared counter to contend for); the short problems
-    // of the last part go to whichever wave is free, from a shared counter,
-    // which evens out the waves' finishing times.
-    const uint32_t n_static = n_jobs - (n_jobs >> kDynTailShift);
+    // like mix, with no shared counter to contend for); with many problems
+    // per wave, the short problems of the last part go to whichever wave is
+    // free, from a shared counter, which evens out the waves' finishing
+    // times.  (With few problems per wave the waves would all reach the
+    // counter at once; the whole list is then split statically.)
+    const bool dyn_tail = n_jobs >= kDynTailMinPerWave * gridDim.x;
+    const uint32_t n_static = dyn_tail ? n_jobs - (n_jobs >> kDynTailShift) : n_jobs;
     auto take = [&](uint32_t done) -> uint32_t {
         if (done + gridDim.x < n_static) return done + gridDim.x;
         uint32_t v = 0;
