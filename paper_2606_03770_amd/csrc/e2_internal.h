@@ -68,8 +68,8 @@ struct E2Work {
 // Number of DP waves launched for at most `problems` problems of N blocks.
 int e2_dp_slots(int N, int problems);
 // Cells of one DP wave's forward-row pool (its backward-row pool is as
-// large), its global row storage (u64 per wave: both pools and two full
-// rows) and its dynamic LDS bytes.
+// large), its global row storage (u64 per wave: both pools) and its dynamic
+// LDS bytes.
 int e2_dp_pool_cells(int N);
 int e2_dp_lds_tb_cells(int N);
 size_t e2_dp_row_words(int N);

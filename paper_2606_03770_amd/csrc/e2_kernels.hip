@@ -33,6 +33,9 @@
 namespace {
 
 constexpr int kWave = 64;
+// a pointer into LDS: reads and writes through it are ds_* instructions
+// with 32-bit addresses instead of flat ones
+template <typename T> using lds_t = __attribute__((address_space(3))) T;
 
 __device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
@@ -445,7 +448,7 @@ struct Row {
     int kmin;              // devices before this one
     int cap;               // longest stage that fits the device
     int lmin;              // lower bound of window lengths over cells >= lo (0: none)
-    const K *prev;         // previous row, band-packed over [plo, phi]; null: first device
+    const lds_t<K> *prev;  // previous row, band-packed over [plo, phi]; null: first device
     int plo, phi;
 };
 
@@ -455,7 +458,7 @@ struct Row {
 // [glo, ghi] (last_only: B = 0 at i = N-1, INF elsewhere).
 template <typename K>
 struct RowOut {
-    K *vals;            // band-packed values (LDS), may be null in combine mode
+    lds_t<K> *vals;     // band-packed values, may be null in combine mode
     K *vals_g;          // second copy of the values (global), or null
     uint8_t *tbs;       // split points, or null
     bool combine;
@@ -615,7 +618,7 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
         if constexpr (__is_same(K, double)) {
             // select on the bit pattern so that the load is not put under a
             // branch (INF = 0x7FF0000000000000)
-            const uint64_t bits = reinterpret_cast<const uint64_t *>(rw.prev)[pxc];
+            const uint64_t bits = reinterpret_cast<const lds_t<uint64_t> *>(rw.prev)[pxc];
             const bool out = px < 0 || px > pspan;
             pv = __builtin_bit_cast(double, out ? 0x7FF0000000000000ull : bits);
         } else {  // all ones (INF) outside the previous band, without a branch
@@ -700,7 +703,7 @@ __device__ __forceinline__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<
 }
 
 template <typename K>
-__device__ __forceinline__ RowOut<K> store_to(K *vals, K *vals_g, uint8_t *tbs)
+__device__ __forceinline__ RowOut<K> store_to(lds_t<K> *vals, K *vals_g, uint8_t *tbs)
 {
     RowOut<K> ro;
     ro.vals = vals;
@@ -819,13 +822,11 @@ __device__ __forceinline__ int scan_incl_i32(int x, int lane)
 
 struct DpSmem {
     void *ps;        // split-point pairs, N entries (LDS)
-    uint64_t *Rw0;   // LDS row ping-pong, N+1 entries each
-    uint64_t *Rw1;
+    lds_t<uint64_t> *Rw0;  // LDS row ping-pong, N+1 entries each
+    lds_t<uint64_t> *Rw1;
     uint8_t *tbp;    // split points of the forward rows, band-packed (LDS)
     uint64_t *pool;  // band-packed forward row values (global, per wave)
     uint64_t *gpool; // band-packed backward row values (global, per wave)
-    uint64_t *Ga;    // full rows of the reference path (global, per wave)
-    uint64_t *Gb;
     int pool_cells;
 };
 
@@ -855,7 +856,7 @@ __device__ __forceinline__ Row<K> fwd_row_of(const E2Tables &tb, const ChainRegs
 }
 
 template <typename K>
-__device__ __forceinline__ void set_prev(Row<K> &rw, const K *prev, int plo, int phi)
+__device__ __forceinline__ void set_prev(Row<K> &rw, const lds_t<K> *prev, int plo, int phi)
 {
     rw.prev = prev;
     rw.plo = plo;
@@ -962,12 +963,12 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
     PS<K> *ps = static_cast<PS<K> *>(sm.ps);
     K *pool = reinterpret_cast<K *>(sm.pool);
     K *gpool = reinterpret_cast<K *>(sm.gpool);
-    K *Rw[2] = {reinterpret_cast<K *>(sm.Rw0), reinterpret_cast<K *>(sm.Rw1)};
+    lds_t<K> *Rw[2] = {reinterpret_cast<lds_t<K> *>(sm.Rw0), reinterpret_cast<lds_t<K> *>(sm.Rw1)};
     // ---- backward rows G_1..G_{m-1}: LDS ping-pong + the backward-row pool
     for (int t = 1; t < m; ++t) {
         Row<K> g = rev_row_of<K>(tb, cr, r, t);
         if (t >= 2)
-            set_prev(g, (const K *)Rw[(t - 1) & 1], rband_lo(cr, t - 1), rband_hi(cr, t - 1));
+            set_prev(g, Rw[(t - 1) & 1], rband_lo(cr, t - 1), rband_hi(cr, t - 1));
         row_pass(g, store_to<K>(Rw[t & 1], gpool + gpool_off(cr, t), nullptr), ps, lane, N);
     }
     // ---- the optimum without a master (no head time or bytes anywhere):
@@ -976,7 +977,7 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
     K tn = KeyT<K>::inf;
     if (m >= 2) {
         Row<K> g = rev_row_of<K>(tb, cr, r, m);
-        set_prev(g, (const K *)Rw[(m - 1) & 1], rband_lo(cr, m - 1), rband_hi(cr, m - 1));
+        set_prev(g, Rw[(m - 1) & 1], rband_lo(cr, m - 1), rband_hi(cr, m - 1));
         g.lo = g.hi = N - 1;
         g.lmin = uni(tb.minwinR[(size_t)f8(lane_w(cr.wd, m - 1), 0) * N + (N - 1)]);
         row_pass(g, store_to<K>(Rw[m & 1], nullptr, nullptr), ps, lane, N);
@@ -998,11 +999,12 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
     // and bytes), and ties go to the smaller master.
     K acc = KeyT<K>::inf;
     K key = KeyT<K>::inf;
+    int f_last = 0;  // the last forward row computed
     for (int mu = 1; mu <= m; ++mu) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, mu, mu);
         if (rw.cap > 0) {
             if (mu >= 2)
-                set_prev(rw, (const K *)Rw[(mu - 1) & 1], band_lo(cr, mu - 1), band_hi(cr, mu - 1));
+                set_prev(rw, Rw[(mu - 1) & 1], band_lo(cr, mu - 1), band_hi(cr, mu - 1));
             RowOut<K> ro = store_to<K>(nullptr, nullptr, nullptr);
             ro.combine = true;
             ro.mu = mu;
@@ -1022,9 +1024,10 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         if (mu < m) {
             Row<K> f = fwd_row_of<K>(tb, cr, r, mu, 0);
             if (mu >= 2)
-                set_prev(f, (const K *)Rw[(mu - 1) & 1], band_lo(cr, mu - 1), band_hi(cr, mu - 1));
+                set_prev(f, Rw[(mu - 1) & 1], band_lo(cr, mu - 1), band_hi(cr, mu - 1));
             const int off = pool_off(cr, mu);
             row_pass(f, store_to<K>(Rw[mu & 1], pool + off, sm.tbp + off), ps, lane, N);
+            f_last = mu;
         }
     }
     // the chosen master's first row reads its forward row back from the pool
@@ -1037,22 +1040,27 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
     if (bestk == KeyT<K>::inf) return;
 
     // ---- rows mu*..m-1 of the chosen master's table (split points overwrite
-    // those of F), then cell N-1 of row m
+    // those of F), then cell N-1 of row m.  Their first row reads F_{mu*-1}
+    // from its ping-pong buffer, which still holds it unless the sweep ran on
+    // two or more rows past it: then it comes back from the pool.
+    if (best_mu >= 2 && best_mu - 1 < f_last - 1) {
+        const int k = best_mu - 1;
+        const int n = band_hi(cr, k) - band_lo(cr, k) + 1;
+        const K *src = pool + pool_off(cr, k);
+        lds_t<K> *dst = Rw[k & 1];
+        for (int x = lane; x < n; x += kWave) dst[x] = src[x];
+        __syncthreads();
+    }
     for (int k = best_mu; k < m; ++k) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, k, best_mu);
-        if (k >= 2) {
-            const K *prev = (k == best_mu) ? (const K *)(pool + pool_off(cr, k - 1))
-                                           : (const K *)Rw[(k - 1) & 1];
-            set_prev(rw, prev, band_lo(cr, k - 1), band_hi(cr, k - 1));
-        }
+        if (k >= 2) set_prev(rw, Rw[(k - 1) & 1], band_lo(cr, k - 1), band_hi(cr, k - 1));
         const int off = pool_off(cr, k);
         row_pass(rw, store_to<K>(Rw[k & 1], nullptr, sm.tbp + off), ps, lane, N);
     }
     if (m >= 2) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, m, best_mu);
-        const K *prev = (best_mu == m) ? (const K *)(pool + pool_off(cr, m - 1))
-                                       : (const K *)Rw[(m - 1) & 1];
-        set_prev(rw, prev, band_lo(cr, m - 1), band_hi(cr, m - 1));
+        // row m-1 of the chosen table (F_{m-1} when mu* = m: the sweep's last row)
+        set_prev(rw, Rw[(m - 1) & 1], band_lo(cr, m - 1), band_hi(cr, m - 1));
         rw.lo = rw.hi = N - 1;
         rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + f8(lane_w(cr.wa, m - 1), 0)) * N + (N - 1)];
         rw.lmin = uni(rw.lmin);
@@ -1091,7 +1099,7 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
 {
     const int N = tb.N;
     PS<uint64_t> *ps = static_cast<PS<uint64_t> *>(sm.ps);
-    uint64_t *cur = sm.Ga, *prv = sm.Gb;
+    lds_t<uint64_t> *cur = sm.Rw0, *prv = sm.Rw1;
     for (int k = 1; k <= m; ++k) {
         const int c = uni(chain[k - 1]);
         const int f = (mu == k);
@@ -1119,7 +1127,7 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
                  store_to<uint64_t>(cur, nullptr,
                                     (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1) : nullptr),
                  ps, lane, N);
-        uint64_t *tmp = prv;
+        lds_t<uint64_t> *tmp = prv;
         prv = cur;
         cur = tmp;
     }
@@ -1175,14 +1183,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     const int M = tb.M, N = tb.N;
     DpSmem sm;
     sm.ps = dyn;
-    sm.Rw0 = dyn + 2 * N;
+    sm.Rw0 = (lds_t<uint64_t> *)(dyn + 2 * N);
     sm.Rw1 = sm.Rw0 + (N + 1);
-    sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
-    uint64_t *my_rows = rows + (size_t)blockIdx.x * (2 * (size_t)pool_cells + 2 * (N + 1));
+    sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N + 2 * (N + 1));
+    uint64_t *my_rows = rows + (size_t)blockIdx.x * (2 * (size_t)pool_cells);
     sm.pool = my_rows;
     sm.gpool = my_rows + pool_cells;
-    sm.Ga = sm.gpool + pool_cells;
-    sm.Gb = sm.Ga + (N + 1);
     sm.pool_cells = pool_cells;
     static_assert(kClasses == 4, "job mapping below assumes four classes");
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
@@ -1323,7 +1329,7 @@ __device__ uint64_t ft_table(const E2Tables &tb, const DpSmem &sm, int r, const 
                              int m, int mu, uint8_t *tbp, int lane)
 {
     const int N = tb.N, M = tb.M;
-    uint64_t *cur = sm.Rw0, *prv = sm.Rw1;
+    uint64_t *cur = (uint64_t *)sm.Rw0, *prv = (uint64_t *)sm.Rw1;
     for (int k = 1; k <= m; ++k) {
         const int c = uni(chain[k - 1]);
         const int f = (mu == k);
@@ -1424,7 +1430,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
     uint64_t *pool = sm.pool;
     uint64_t *gpool = sm.gpool;
     uint64_t *H = reinterpret_cast<uint64_t *>(sm.ps);  // N cells
-    uint64_t *Rw[2] = {sm.Rw0, sm.Rw1};
+    uint64_t *Rw[2] = {(uint64_t *)sm.Rw0, (uint64_t *)sm.Rw1};
     // ---- backward rows G_1..G_{m-1} in the backward-row pool: reversed row t
     // is device m+1-t holding reversed blocks y..x after the t-1 devices
     // behind it
@@ -1566,14 +1572,12 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     const int M = tb.M, N = tb.N;
     DpSmem sm;
     sm.ps = dyn;
-    sm.Rw0 = dyn + 2 * N;
+    sm.Rw0 = (lds_t<uint64_t> *)(dyn + 2 * N);
     sm.Rw1 = sm.Rw0 + (N + 1);
-    sm.tbp = reinterpret_cast<uint8_t *>(sm.Rw1 + (N + 1));
-    uint64_t *my_rows = rows + (size_t)blockIdx.x * (2 * (size_t)pool_cells + 2 * (N + 1));
+    sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N + 2 * (N + 1));
+    uint64_t *my_rows = rows + (size_t)blockIdx.x * (2 * (size_t)pool_cells);
     sm.pool = my_rows;
     sm.gpool = my_rows + pool_cells;
-    sm.Ga = sm.gpool + pool_cells;
-    sm.Gb = sm.Ga + (N + 1);
     sm.pool_cells = pool_cells;
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
@@ -2523,7 +2527,7 @@ int e2_dp_lds_tb_cells(int N)
     return kLdsTbCells;
 }
 
-size_t e2_dp_row_words(int N) { return 2 * (size_t)e2_dp_pool_cells(N) + 2 * (size_t)(N + 1); }
+size_t e2_dp_row_words(int N) { return 2 * (size_t)e2_dp_pool_cells(N); }
 
 size_t e2_dp_lds_bytes(int N)
 {
