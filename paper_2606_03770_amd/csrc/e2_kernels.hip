@@ -568,11 +568,11 @@ __device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K
     int t = 0;
     const PS<K> *top = ps + (i - o);  // j at step t is top - S t
     for (; t + 4 <= t_safe; t += 4) {
+        // all four entries are loaded before any is used (one wait per step)
         const PS<K> *q = top - S * (t + 3);
-        best = kmin(best, cand(q[3 * S], si1));
-        best = kmin(best, cand(q[2 * S], si1));
-        best = kmin(best, cand(q[S], si1));
-        best = kmin(best, cand(q[0], si1));
+        const PS<K> e3 = q[3 * S], e2 = q[2 * S], e1 = q[S], e0 = q[0];
+        best = kmin(kmin(best, cand(e3, si1)), cand(e2, si1));
+        best = kmin(kmin(best, cand(e1, si1)), cand(e0, si1));
     }
     for (; t < t_all; ++t) {
         int j = i - o - S * t;
@@ -763,9 +763,10 @@ constexpr int kMaxBandedChain = kWave;
 constexpr int kLdsTbCells = 2048;
 
 // Per-position table of a chain: lane k-1 holds chain position k (1-based)
-// as four packed words (fields < 256 except the pool offset) and three u64
+// as five packed words (fields < 256 except the pool offsets) and two u64
 // times; a row reads its words with one readlane each and unpacks them in
-// scalar registers.
+// scalar registers.  Reversed row t's link (position m+1-t to m+2-t) is the
+// forward link held by lane m+1-t.
 struct ChainRegs {
     uint32_t wa;    // dev | cap0 << 8 | capH << 16 | lmin0 << 24      (forward row k)
     uint32_t wb;    // flo | fhi << 8 | lmin1 << 16                    (forward row k)
@@ -774,7 +775,7 @@ struct ChainRegs {
     uint32_t we;    // offset of reversed row t = k in the backward-row pool
     uint64_t tau;   // link from position k-1 (k >= 2)
     uint64_t head;  // head time of the device
-    uint64_t tauR;  // link of reversed row t = k: position m+1-k -> m+2-k
+    int m;          // chain length (uniform)
 };
 // cap0 / capH are the longest stages without / with the head, [flo, fhi]
 // the forward band, lmin0 / lmin1 its window-length bounds; reversed row
@@ -876,7 +877,7 @@ __device__ __forceinline__ Row<K> rev_row_of(const E2Tables &tb, const ChainRegs
     g.pr = prefR_row(tb, r, c);
     g.wr = tb.winR + (uint32_t)(c * tb.N);
     g.hadd = 0;
-    g.tau = (t >= 2) ? to_k<K>(lane_u64(cr.tauR, t - 1)) : (K)0;
+    g.tau = (t >= 2) ? to_k<K>(lane_u64(cr.tau, cr.m + 1 - t)) : (K)0;  // link m+1-t -> m+2-t
     g.lo = f8(wd, 8);
     g.hi = f8(wd, 16);
     g.kmin = t - 1;
@@ -925,7 +926,7 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
     const int devR = __shfl(dev, src, kWave);
     const int capR = __shfl(cap0, src, kWave);
     const int pre_km1 = (kk >= 2) ? __shfl(pre, max(0, kk - 2), kWave) : 0;
-    cr.tauR = __shfl(cr.tau, max(0, min(kWave - 1, kk)), kWave);  // link kk -> kk+1
+    cr.m = m;
     int glo = 1, ghi = 0, lminR = 0;
     {
         const bool vr = k1 < m;
@@ -1437,7 +1438,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
     for (int t = 1; t < m; ++t) {
         const uint32_t wd = lane_w(cr.wd, t - 1);
         const int c = f8(wd, 0);
-        const uint64_t tau = t >= 2 ? lane_u64(cr.tauR, t - 1) : 0;
+        const uint64_t tau = t >= 2 ? lane_u64(cr.tau, m + 1 - t) : 0;  // link m+1-t -> m+2-t
         ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, tau, f8(wd, 8), f8(wd, 16),
                t - 1, t >= 2 ? gpool + gpool_off(cr, t - 1) : nullptr,
                t >= 2 ? rband_lo(cr, t - 1) : 1, t >= 2 ? rband_hi(cr, t - 1) : 0,
@@ -1449,7 +1450,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
     uint64_t t0 = E2_INF64;
     if (m >= 2) {
         const int c = f8(lane_w(cr.wd, m - 1), 0);
-        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, lane_u64(cr.tauR, m - 1),
+        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, lane_u64(cr.tau, 1),
                N - 1, N - 1, m - 1, gpool + gpool_off(cr, m - 1), rband_lo(cr, m - 1),
                rband_hi(cr, m - 1), H, nullptr, lane);
         t0 = uni64(H[0]);
