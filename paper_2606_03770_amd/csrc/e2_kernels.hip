@@ -574,10 +574,13 @@ __device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K
         best = kmin(kmin(best, cand(e3, si1)), cand(e2, si1));
         best = kmin(kmin(best, cand(e1, si1)), cand(e0, si1));
     }
-    for (; t < t_all; ++t) {
-        int j = i - o - S * t;
-        if (j < jlo) j = jlo;
-        best = kmin(best, cand(ps[j], si1));
+    // the rest two steps at a time, both entries loaded before use; indices
+    // below the cell's window start read its first entry again (an odd last
+    // step repeats a candidate, which leaves the minimum unchanged)
+    for (; t < t_all; t += 2) {
+        const PS<K> e0 = ps[max(i - o - S * t, jlo)];
+        const PS<K> e1 = ps[max(i - o - S * (t + 1), jlo)];
+        best = kmin(kmin(best, cand(e0, si1)), cand(e1, si1));
     }
     if (S >= 2) best = kmin(best, dppk<0xb1>(best));
     if (S >= 4) best = kmin(best, dppk<0x4e>(best));
