@@ -338,6 +338,16 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
             vtot[(size_t)r * M + d] =
                 pref[((size_t)r * M + d) * (N + 1) + N] + h[(size_t)r * M + d];
 
+    // prefix sums pre-shifted for the DP's packed keys (value << 8 | index)
+    std::vector<uint32_t> pref8u(pref.size()), prefR8u(prefR.size());
+    std::vector<double> pref8d(pref.size()), prefR8d(prefR.size());
+    for (size_t x = 0; x < pref.size(); ++x) {
+        pref8u[x] = (uint32_t)(pref[x] << 8);
+        prefR8u[x] = (uint32_t)(prefR[x] << 8);
+        pref8d[x] = (double)pref[x] * 256.0;
+        prefR8d[x] = (double)prefR[x] * 256.0;
+    }
+
     struct Part {
         const void *src;
         size_t bytes;
@@ -349,7 +359,9 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
                     {minwin.data(), minwin.size(), nullptr},   {minwinR.data(), minwinR.size(), nullptr},
                     {cap0.data(), cap0.size(), nullptr},       {capH.data(), capH.size(), nullptr},
                     {vmax.data(), vmax.size() * 8, nullptr},   {vtot.data(), vtot.size() * 8, nullptr},
-                    {hfit.data(), hfit.size(), nullptr}};
+                    {hfit.data(), hfit.size(), nullptr},
+                    {pref8u.data(), pref8u.size() * 4, nullptr}, {prefR8u.data(), prefR8u.size() * 4, nullptr},
+                    {pref8d.data(), pref8d.size() * 8, nullptr}, {prefR8d.data(), prefR8d.size() * 8, nullptr}};
     size_t total = 0;
     for (const Part &pt : parts) total += align256(pt.bytes);
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
@@ -393,6 +405,10 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
     tb.vmax = reinterpret_cast<const uint64_t *>(parts[10].dst);
     tb.vtot = reinterpret_cast<const uint64_t *>(parts[11].dst);
     tb.hfit = reinterpret_cast<const uint8_t *>(parts[12].dst);
+    tb.pref8u = reinterpret_cast<const uint32_t *>(parts[13].dst);
+    tb.prefR8u = reinterpret_cast<const uint32_t *>(parts[14].dst);
+    tb.pref8d = reinterpret_cast<const double *>(parts[15].dst);
+    tb.prefR8d = reinterpret_cast<const double *>(parts[16].dst);
     tb.M = M;
     tb.N = N;
     tb.R = R;

@@ -32,6 +32,10 @@ struct E2Tables {
                            //   holds the head bytes) per role and device
     const uint64_t *vtot;  // [R][M] total time of all blocks + head time per role and device
     const uint8_t *hfit;   // [M] 1 when the head bytes alone fit the device
+    const uint32_t *pref8u;  // [R][M][N+1] pref << 8 modulo 2^32 (32-bit DP keys)
+    const uint32_t *prefR8u; // [R][M][N+1] prefR << 8 modulo 2^32
+    const double *pref8d;    // [R][M][N+1] pref x 256 as a double (exact below 2^45, the
+    const double *prefR8d;   //   only range the fp64 DP keys use); same for prefR
     int M;
     int N;
     int R;      // role indices

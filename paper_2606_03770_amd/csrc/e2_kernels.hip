@@ -441,8 +441,10 @@ struct PS {
 template <typename K>
 struct Row {
     const uint64_t *pr;    // prefix sums P[0..N] of the stage device
+    const K *p8;           // P << 8 as a key (null for u64 keys, which shift pr)
     const uint8_t *wr;     // smallest stage start per stage end, E2_NO_START if none
     uint64_t hadd;         // head time when this device is the master, else 0
+    K hadd8;               // hadd << 8 as a key
     K tau;                 // link from the previous device
     int lo, hi;            // cells of this row
     int kmin;              // devices before this one
@@ -486,6 +488,13 @@ template <typename K> __device__ __forceinline__ K uni_k(K v)
     else return uni64(v);
 }
 
+// *(p + off bytes) with a 32-bit unsigned byte offset from a wave-uniform
+// base (the load then adds the offset to the scalar base itself)
+template <typename T> __device__ __forceinline__ T at_byte(const T *p, uint32_t off)
+{
+    return *reinterpret_cast<const T *>(reinterpret_cast<const char *>(p) + off);
+}
+
 // Row starts of the per-device tables (element offsets fit in 32 bits:
 // at most 2 x 256 x 256 entries).
 __device__ __forceinline__ const uint64_t *pref_row(const E2Tables &tb, int r, int c)
@@ -495,6 +504,31 @@ __device__ __forceinline__ const uint64_t *pref_row(const E2Tables &tb, int r, i
 __device__ __forceinline__ const uint64_t *prefR_row(const E2Tables &tb, int r, int c)
 {
     return tb.prefR + (uint32_t)((r * tb.M + c) * (tb.N + 1));
+}
+// P << 8 of the same rows as a key of type K (u32: modulo 2^32; fp64: exact
+// for the problems that take fp64 keys)
+template <typename K> __device__ __forceinline__ const K *pref8_row(const E2Tables &tb, int r, int c)
+{
+    const uint32_t o = (uint32_t)((r * tb.M + c) * (tb.N + 1));
+    if constexpr (__is_same(K, double)) return tb.pref8d + o;
+    else return tb.pref8u + o;
+}
+template <typename K> __device__ __forceinline__ const K *prefR8_row(const E2Tables &tb, int r, int c)
+{
+    const uint32_t o = (uint32_t)((r * tb.M + c) * (tb.N + 1));
+    if constexpr (__is_same(K, double)) return tb.prefR8d + o;
+    else return tb.prefR8u + o;
+}
+template <typename K> __device__ __forceinline__ K shift8(uint64_t v)
+{
+    if constexpr (__is_same(K, double)) return (double)v * 256.0;
+    else return (K)(v << 8);
+}
+// P[x] << 8 of a row as a key
+template <typename K> __device__ __forceinline__ K prefix8(const Row<K> &rw, uint32_t x)
+{
+    if constexpr (__is_same(K, uint64_t)) return rw.pr[x] << 8;
+    else return at_byte(rw.p8, x * (uint32_t)sizeof(K));
 }
 __device__ __forceinline__ const uint8_t *win_row(const E2Tables &tb, int f, int c)
 {
@@ -598,41 +632,45 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
     // first pass's cell loads go out before the split points are built
     // (lanes past the row load its last cell, which they compute again)
     int w_nx;
-    uint64_t p_nx;
+    K p_nx;  // P[i+1] << 8
     K b_nx = 0;
     {
         const int i = min(rw.lo + cl, rw.hi);
         w_nx = rw.wr[i];
-        p_nx = rw.pr[i + 1];
+        p_nx = prefix8(rw, (uint32_t)(i + 1));
         if (ro.combine) b_nx = combine_b(i, N, ro);
     }
     // both loads of an entry go out before either is waited for: the
     // previous-row value comes from a clamped index and is replaced by INF
     // outside the previous band
-    const int pspan = rw.phi - rw.plo;  // < 0: empty previous band (slot 0 is read, unused)
+    // Entry x = j-1-plo of the previous row, as an unsigned offset: outside
+    // [0, span] (x < 0 wraps above it) the entry is INF and the read goes to a
+    // clamped, in-range slot.  An empty previous band moves plo to -2, which
+    // puts every x above span = 0.
+    const int pspan = rw.phi - rw.plo;
+    const int plo_e = pspan < 0 ? -2 : rw.plo;
+    const uint32_t span = pspan < 0 ? 0u : (uint32_t)pspan;
     // a uniform loop: lanes past the row repeat its last entry, writing the
     // same values to the same slot
     for (int j0 = jmin; j0 <= rw.hi; j0 += kWave) {
         const int j = min(j0 + lane, rw.hi);
-        const int px = j - 1 - rw.plo;
-        const int pxc = max(0, min(px, pspan));
-        const uint64_t prj = rw.pr[j];
+        const uint32_t ux = (uint32_t)(j - 1 - plo_e);
+        const uint32_t pxc = min(ux, span);
+        const bool in = ux <= span;
+        const K sj = prefix8(rw, (uint32_t)j);
         K pv;
         if constexpr (__is_same(K, double)) {
             // select on the bit pattern so that the load is not put under a
             // branch (INF = 0x7FF0000000000000)
             const uint64_t bits = reinterpret_cast<const lds_t<uint64_t> *>(rw.prev)[pxc];
-            const bool out = px < 0 || px > pspan;
-            pv = __builtin_bit_cast(double, out ? 0x7FF0000000000000ull : bits);
+            pv = __builtin_bit_cast(double, in ? bits : 0x7FF0000000000000ull);
         } else {  // all ones (INF) outside the previous band, without a branch
-            const K pvr = rw.prev[pxc];
-            pv = pvr | ((K)0 - (K)(px < 0 || px > pspan));
+            pv = inf_unless(rw.prev[pxc], in);
         }
         ps[j].a = pack_prev(pv, rw.tau, j);
-        if constexpr (__is_same(K, double))  // may be negative when blocks take 0 ns
-            ps[j].s = __builtin_fma((double)prj, 256.0, -(double)j);
-        else  // modular: only differences are used
-            ps[j].s = (K)((prj << 8) - (uint64_t)j);
+        // (P[j] << 8) - j; fp64: exact, may be negative when blocks take 0 ns;
+        // integers: modular, only differences are used
+        ps[j].s = sj - (K)j;
     }
     __syncthreads();
     const int L = min(rw.cap, rw.hi - jmin + 1);
@@ -648,18 +686,18 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
     for (int base = rw.lo; base <= rw.hi; base += CPP) {
         const int i = min(base + cl, rw.hi);
         const int w = w_nx;
-        const uint64_t p1 = p_nx;
+        const K p1 = p_nx;
         const K b = b_nx;
         if (base + CPP <= rw.hi) {  // a next pass exists (uniform)
             const int in = min(base + CPP + cl, rw.hi);
             w_nx = rw.wr[in];
-            p_nx = rw.pr[in + 1];
+            p_nx = prefix8(rw, (uint32_t)(in + 1));
             if (ro.combine) b_nx = combine_b(in, N, ro);
         }
         const bool act = w != (int)E2_NO_START;
         const int ie = act ? i : i_idle;
         const int jlo = act ? max(w, jmin) : jmin;
-        const K si1 = (K)((p1 + rw.hadd) << 8);
+        const K si1 = p1 + rw.hadd8;  // (P[i+1] + head) << 8
         const K best = scan_cell<S>(ps, ie, jlo, o, si1, t_safe, t_all);
         const K v = act ? unpack_val(best) : KeyT<K>::inf;
         if (!ro.combine) {
@@ -845,8 +883,10 @@ __device__ __forceinline__ Row<K> fwd_row_of(const E2Tables &tb, const ChainRegs
     const int c = f8(wa, 0);
     Row<K> rw;
     rw.pr = pref_row(tb, r, c);
+    rw.p8 = pref8_row<K>(tb, r, c);
     rw.wr = win_row(tb, f, c);
     rw.hadd = f ? lane_u64(cr.head, k - 1) : 0;
+    rw.hadd8 = shift8<K>(rw.hadd);
     rw.tau = (k >= 2) ? to_k<K>(lane_u64(cr.tau, k - 1)) : (K)0;
     rw.lo = f8(wb, 0);
     rw.hi = f8(wb, 8);
@@ -878,8 +918,10 @@ __device__ __forceinline__ Row<K> rev_row_of(const E2Tables &tb, const ChainRegs
     const int c = f8(wd, 0);
     Row<K> g;
     g.pr = prefR_row(tb, r, c);
+    g.p8 = prefR8_row<K>(tb, r, c);
     g.wr = tb.winR + (uint32_t)(c * tb.N);
     g.hadd = 0;
+    g.hadd8 = 0;
     g.tau = (t >= 2) ? to_k<K>(lane_u64(cr.tau, cr.m + 1 - t)) : (K)0;  // link m+1-t -> m+2-t
     g.lo = f8(wd, 8);
     g.hi = f8(wd, 16);
@@ -1111,6 +1153,8 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
         rw.pr = pref_row(tb, r, c);
         rw.wr = win_row(tb, f, c);
         rw.hadd = f ? uni64(tb.head[r * tb.M + c]) : 0;
+        rw.p8 = nullptr;
+        rw.hadd8 = rw.hadd << 8;
         rw.lo = k - 1;
         rw.hi = N - 1;
         rw.kmin = k - 1;
