@@ -43,10 +43,14 @@ __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > 
 // Wave-wide reductions: DPP permutations within each 16-lane row (quad
 // swaps, half mirror, mirror), then the four row results read into scalars.
 // The results are wave-uniform.
+// CTRL is always a full permutation of each row (every lane reads a lane of
+// its own row), so no lane keeps an old value and none is passed.
 template <int CTRL>
 __device__ __forceinline__ int dpp_i32(int v)
 {
-    return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xf, 0xf, false);
+    static_assert(CTRL == 0xb1 || CTRL == 0x4e || CTRL == 0x140 || CTRL == 0x141,
+                  "a full permutation within each row");
+    return __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, false);
 }
 template <int CTRL>
 __device__ __forceinline__ uint64_t dpp_u64(uint64_t v)
