@@ -140,8 +140,11 @@ def test_master_sweep_stops_and_runs_through(torch_dev, seed):
     """The DP's master sweep stops at the first master whose optimum equals
     the optimum with no head.  A heavy head gives clusters where it stops at
     the first device, where it stops later, and where no master reaches that
-    bound (every master is then solved, and the chosen master's first row is
-    read back from the forward pool); all of them equal the oracle."""
+    bound, so that every master is solved: the chosen one is then the first
+    device (no previous row), the last (its combine came last), one row
+    before the last (its previous forward row is still in LDS), or two or
+    more rows before it (its previous forward row is copied back from the
+    global pool).  All of them equal the oracle."""
     wl = workload.random_small(seed, M=40, N=60, P=30, k_max=5, mem_lo_layers=2,
                                mem_hi_layers=20)
     wl = dataclasses.replace(wl, head_flops=np.array([4 * 10**11] * 2, np.uint64),
@@ -159,11 +162,19 @@ def test_master_sweep_stops_and_runs_through(torch_dev, seed):
             if len(ch) == 0 or want["T"][p, q] == INF:
                 continue
             pos = int(np.nonzero(ch == want["master"][p, q])[0][0]) + 1
+            m = len(ch)
             if want["T"][p, q] == T0[p, q]:
                 kinds.add("stop at 1" if pos == 1 else "stop later")
-            elif 2 <= pos < len(ch):
-                kinds.add("through, master inside")
-    assert kinds == {"stop at 1", "stop later", "through, master inside"}
+            elif pos == 1:
+                kinds.add("through, master 1")
+            elif pos == m:
+                kinds.add("through, master m")
+            elif pos == m - 1:
+                kinds.add("through, one row past")
+            else:
+                kinds.add("through, two or more rows past")
+    assert kinds == {"stop at 1", "stop later", "through, master 1", "through, master m",
+                     "through, one row past", "through, two or more rows past"}
 
 
 def test_uniform_layers_many_ties(torch_dev):
