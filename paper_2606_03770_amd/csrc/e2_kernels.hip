@@ -1426,12 +1426,30 @@ __device__ uint64_t ft_table(const E2Tables &tb, const DpSmem &sm, int r, const 
 //            on ties), of prev(j-1) + tau + P[i+1] - P[j] + hadd
 // with prev band-packed over [plo, phi] (INF outside) or, for the first
 // device, the stage 0..i alone.  Values to out[i - lo] (LDS or global),
-// split points to tbs[i - lo] when tbs is not null.
+// split points to tbs[i - lo] when tbs is not null.  The terms that depend
+// on j alone, a(j) = prev(j-1) + (P[N] - P[j]) (INF when prev(j-1) is), are
+// staged in LDS first (st, N entries), so that a candidate is one LDS read:
+// a(j) + (P[i+1] + hadd + tau - P[N]) is the candidate exactly in modular
+// u64 arithmetic.
 __device__ __forceinline__ void ft_row(const uint64_t *pr, const uint8_t *wr, uint64_t hadd,
                                        uint64_t tau, int lo, int hi, int kmin,
                                        const uint64_t *prev, int plo, int phi, uint64_t *out,
-                                       uint8_t *tbs, int lane)
+                                       uint8_t *tbs, lds_t<uint64_t> *st, int N, int lane)
 {
+    const uint64_t pN = pr[N];
+    const bool linked = prev && tau != E2_INF64;
+    if (linked) {
+        for (int j = kmin + lane; j <= hi; j += kWave) {
+            const int x = j - 1;
+            uint64_t a = E2_INF64;
+            if (x >= plo && x <= phi) {
+                const uint64_t pv = prev[x - plo];
+                if (pv != E2_INF64) a = pv + (pN - pr[j]);
+            }
+            st[j] = a;
+        }
+        __syncthreads();
+    }
     for (int i = lo + lane; i <= hi; i += kWave) {
         uint64_t best = E2_INF64;
         int bj = 0;
@@ -1440,13 +1458,12 @@ __device__ __forceinline__ void ft_row(const uint64_t *pr, const uint8_t *wr, ui
             const uint64_t end = pr[i + 1] + hadd;
             if (!prev) {
                 if (w == 0) best = end - pr[0];
-            } else if (tau != E2_INF64) {
+            } else if (linked) {
+                const uint64_t c = end + tau - pN;
                 for (int j = max(w, kmin); j <= i; ++j) {
-                    const int x = j - 1;
-                    if (x < plo || x > phi) continue;
-                    const uint64_t pv = prev[x - plo];
-                    if (pv == E2_INF64) continue;
-                    const uint64_t v = pv + tau + (end - pr[j]);
+                    const uint64_t a = st[j];
+                    if (a == E2_INF64) continue;
+                    const uint64_t v = a + c;
                     if (v < best) {
                         best = v;
                         bj = j;
@@ -1481,7 +1498,10 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
     const int N = tb.N, M = tb.M;
     uint64_t *pool = sm.pool;
     uint64_t *gpool = sm.gpool;
-    uint64_t *H = reinterpret_cast<uint64_t *>(sm.ps);  // N cells
+    // the master's row (N cells) in the first LDS row buffer: the final rows,
+    // the only other users of the row buffers, come after the sweep
+    uint64_t *H = (uint64_t *)sm.Rw0;
+    lds_t<uint64_t> *st = (lds_t<uint64_t> *)sm.ps;  // ft_row's staged terms
     uint64_t *Rw[2] = {(uint64_t *)sm.Rw0, (uint64_t *)sm.Rw1};
     // ---- backward rows G_1..G_{m-1} in the backward-row pool: reversed row t
     // is device m+1-t holding reversed blocks y..x after the t-1 devices
@@ -1493,7 +1513,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
         ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, tau, f8(wd, 8), f8(wd, 16),
                t - 1, t >= 2 ? gpool + gpool_off(cr, t - 1) : nullptr,
                t >= 2 ? rband_lo(cr, t - 1) : 1, t >= 2 ? rband_hi(cr, t - 1) : 0,
-               gpool + gpool_off(cr, t), nullptr, lane);
+               gpool + gpool_off(cr, t), nullptr, st, N, lane);
     }
     // ---- T0, the least end-to-end time with no head anywhere: reversed row
     // m at its last cell.  A master's optimum is at least T0 plus its head
@@ -1503,7 +1523,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
         const int c = f8(lane_w(cr.wd, m - 1), 0);
         ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, lane_u64(cr.tau, 1),
                N - 1, N - 1, m - 1, gpool + gpool_off(cr, m - 1), rband_lo(cr, m - 1),
-               rband_hi(cr, m - 1), H, nullptr, lane);
+               rband_hi(cr, m - 1), H, nullptr, st, N, lane);
         t0 = uni64(H[0]);
         if (t0 == E2_INF64) {
             *T_out = E2_INF64;
@@ -1530,7 +1550,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
             ft_row(pref_row(tb, r, c), win_row(tb, 1, c), uni64(tb.head[r * M + c]), tau, hlo,
                    hi, mu - 1, mu >= 2 ? pool + pool_off(cr, mu - 1) : nullptr,
                    mu >= 2 ? band_lo(cr, mu - 1) : 1, mu >= 2 ? band_hi(cr, mu - 1) : 0, H,
-                   nullptr, lane);
+                   nullptr, st, N, lane);
             uint64_t tm = E2_INF64;
             if (mu == m) {
                 tm = H[0];
@@ -1565,7 +1585,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
             ft_row(pref_row(tb, r, c), win_row(tb, 0, c), 0, tau, band_lo(cr, mu), band_hi(cr, mu),
                    mu - 1, mu >= 2 ? pool + pool_off(cr, mu - 1) : nullptr,
                    mu >= 2 ? band_lo(cr, mu - 1) : 1, mu >= 2 ? band_hi(cr, mu - 1) : 0,
-                   pool + pool_off(cr, mu), mu >= 2 ? sm.tbp + pool_off(cr, mu) : nullptr, lane);
+                   pool + pool_off(cr, mu), mu >= 2 ? sm.tbp + pool_off(cr, mu) : nullptr, st, N, lane);
         }
     }
     *T_out = best;
@@ -1589,7 +1609,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
         }
         uint8_t *tbs = k == m ? start + m : tbp + pool_off(cr, k);  // row m: one cell
         ft_row(pref_row(tb, r, c), win_row(tb, f, c), f ? uni64(tb.head[r * M + c]) : 0, tau, lo,
-               hi, k - 1, prev, plo, phi, Rw[k & 1], k >= 2 ? tbs : nullptr, lane);
+               hi, k - 1, prev, plo, phi, Rw[k & 1], k >= 2 ? tbs : nullptr, st, N, lane);
     }
     if (lane == 0) {
         int i = N - 1;
