@@ -1788,9 +1788,11 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
 // at the master's stage); the smallest master with the least T_mu wins.
 // O(m^2 N + m N W / 64) per problem instead of O(m^3 N + m^2 N W / 64).
 __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, int m, uint64_t *E,
-                             uint64_t *B, uint64_t *A, uint64_t *S, int lane, uint64_t *best_out,
-                             int *mu_out)
+                             uint64_t *B, uint64_t *A, uint64_t *S, uint64_t *P, int lane,
+                             uint64_t *best_out, int *mu_out)
 {
+    // P (LDS, N+1 entries) holds the stage device's prefix sums, staged with
+    // A, so that the candidate loops read no global memory
     const int N = tv.N, M = tv.M, X = N + 1;
     // forward rows F_k into E, reversed rows R_t into B
     for (int dir = 0; dir < 2; ++dir) {
@@ -1799,7 +1801,9 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
             // forward: device k; reversed: device m+1-k, links to the ones behind it
             const int pos = dir ? m - k : k - 1;
             const int c = uni(chain[pos]);
+            const uint64_t *pr = dir ? prefR_row(tv, r, c) : pref_row(tv, r, c);
             for (int x = lane; x <= N; x += kWave) {
+                P[x] = pr[x];
                 uint64_t a = x == 0 ? 0 : E2_INF64;
                 for (int kp = 1; kp <= k - 1; ++kp) {
                     const uint64_t e = rows[(size_t)(kp - 1) * X + x];
@@ -1813,17 +1817,17 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
                 A[x] = a;
             }
             __syncthreads();
-            const uint64_t *pr = dir ? prefR_row(tv, r, c) : pref_row(tv, r, c);
             const uint8_t *wr = dir ? tv.winR + (uint32_t)(c * N) : win_row(tv, 0, c);
             for (int x = lane; x <= N; x += kWave) {
                 uint64_t e = E2_INF64;
                 if (x >= 1) {
                     const int w = wr[x - 1];
+                    const uint64_t px = P[x];
                     if (w != E2_NO_START)
                         for (int j = w; j < x; ++j) {
                             const uint64_t aj = A[j];
                             if (aj == E2_INF64) continue;
-                            const uint64_t v = umax64(aj, pr[x] - pr[j]);
+                            const uint64_t v = umax64(aj, px - P[j]);
                             e = v < e ? v : e;
                         }
                 }
@@ -1838,7 +1842,9 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
     int best_mu = 0;
     for (int mu = 1; mu <= m; ++mu) {
         const int c = uni(chain[mu - 1]);
+        const uint64_t *pr = pref_row(tv, r, c);
         for (int x = lane; x <= N; x += kWave) {
+            P[x] = pr[x];
             uint64_t a = x == 0 ? 0 : E2_INF64;
             for (int kp = 1; kp < mu; ++kp) {
                 const uint64_t e = E[(size_t)(kp - 1) * X + x];
@@ -1860,7 +1866,6 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
             S[x] = sv;
         }
         __syncthreads();
-        const uint64_t *pr = pref_row(tv, r, c);
         const uint8_t *wr = win_row(tv, 1, c);
         const uint64_t head = uni64(tv.head[r * M + c]);
         const bool empty_ok = tv.hfit[c];
@@ -1870,11 +1875,12 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
             if (sv == E2_INF64) continue;
             if (y >= 1) {
                 const int w = wr[y - 1];
+                const uint64_t py = P[y] + head;
                 if (w != E2_NO_START)
                     for (int x = w; x < y; ++x) {
                         const uint64_t ax = A[x];
                         if (ax == E2_INF64) continue;
-                        const uint64_t v = umax64(umax64(ax, pr[y] - pr[x] + head), sv);
+                        const uint64_t v = umax64(umax64(ax, py - P[x]), sv);
                         tm = v < tm ? v : tm;
                     }
             }
@@ -1901,13 +1907,14 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
                                                 uint8_t *idle, size_t idle_stride, uint64_t *T,
                                                 uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
-    extern __shared__ uint64_t A[];  // [N+1], then S [N+1]
+    extern __shared__ uint64_t A[];  // [N+1], then S [N+1] and P [N+1]
     __shared__ uint8_t chain[256];
     __shared__ uint8_t sizes[256];
     __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N, X = N + 1;
     uint64_t *S = A + X;
+    uint64_t *P = S + X;
     uint64_t *E = reinterpret_cast<uint64_t *>(idle + (size_t)blockIdx.x * idle_stride);
     uint64_t *B = E + (size_t)M * X;
     uint16_t *Ek = reinterpret_cast<uint16_t *>(B + (size_t)M * X);
@@ -1936,7 +1943,7 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
         const E2Tables tv = mem_view(tb, r);
         uint64_t best = E2_INF64;
         int best_mu = 0, last = 0;
-        idle_masters(tv, r, chain, m, E, B, A, S, lane, &best, &best_mu);
+        idle_masters(tv, r, chain, m, E, B, A, S, P, lane, &best, &best_mu);
         for (int pass = 1; pass < 2; ++pass) {
             if (best == E2_INF64) break;
             const int mu_lo = best_mu, mu_hi = best_mu;
@@ -2653,7 +2660,7 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
     if (objective == 2)
-        k_dp_idle<<<wk.n_slots, 64, (size_t)(t.N + 1) * 16, s>>>(t, k_max, gen, roles, wk.counters,
+        k_dp_idle<<<wk.n_slots, 64, (size_t)(t.N + 1) * 24, s>>>(t, k_max, gen, roles, wk.counters,
                                                                 wk.list, seg, wk.idle,
                                                                 wk.idle_stride, T, Lambda,
                                                                 master, layers);
