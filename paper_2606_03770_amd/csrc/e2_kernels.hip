@@ -1802,14 +1802,27 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
             const int pos = dir ? m - k : k - 1;
             const int c = uni(chain[pos]);
             const uint64_t *pr = dir ? prefR_row(tv, r, c) : pref_row(tv, r, c);
+            // the links from the earlier rows' devices: row kp <= 64 from lane
+            // kp-1, later rows (chains beyond 65 devices) load theirs
+            uint64_t tlk = E2_INF64;
+            if (lane < k - 1) {
+                const int cp = chain[dir ? m - (lane + 1) : lane];
+                // links run from the earlier chain position to the later one
+                tlk = dir ? link_tau(tv, r, c, cp) : link_tau(tv, r, cp, c);
+            }
             for (int x = lane; x <= N; x += kWave) {
                 P[x] = pr[x];
                 uint64_t a = x == 0 ? 0 : E2_INF64;
+#pragma unroll 4
                 for (int kp = 1; kp <= k - 1; ++kp) {
                     const uint64_t e = rows[(size_t)(kp - 1) * X + x];
-                    const int cp = uni(chain[dir ? m - kp : kp - 1]);
-                    // links run from the earlier chain position to the later one
-                    const uint64_t tl = dir ? link_tau_u(tv, r, c, cp) : link_tau_u(tv, r, cp, c);
+                    uint64_t tl;
+                    if (kp <= kWave) {
+                        tl = readlane_u64(tlk, kp - 1);
+                    } else {
+                        const int cp = uni(chain[dir ? m - kp : kp - 1]);
+                        tl = dir ? link_tau_u(tv, r, c, cp) : link_tau_u(tv, r, cp, c);
+                    }
                     if (e == E2_INF64 || tl == E2_INF64) continue;
                     const uint64_t v = umax64(e, tl);
                     a = v < a ? v : a;
@@ -1843,22 +1856,32 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
     for (int mu = 1; mu <= m; ++mu) {
         const int c = uni(chain[mu - 1]);
         const uint64_t *pr = pref_row(tv, r, c);
+        // links into the master from position kp (lane kp-1, kp < mu) and out
+        // of it to position kpp (lane kpp-1, kpp > mu); positions beyond 64
+        // load theirs
+        uint64_t tin = E2_INF64, tout = E2_INF64;
+        if (lane < mu - 1) tin = link_tau(tv, r, chain[lane], c);
+        if (lane >= mu && lane < m) tout = link_tau(tv, r, c, chain[lane]);
         for (int x = lane; x <= N; x += kWave) {
             P[x] = pr[x];
             uint64_t a = x == 0 ? 0 : E2_INF64;
+#pragma unroll 4
             for (int kp = 1; kp < mu; ++kp) {
                 const uint64_t e = E[(size_t)(kp - 1) * X + x];
-                const uint64_t tl = link_tau_u(tv, r, uni(chain[kp - 1]), c);
+                const uint64_t tl = kp <= kWave ? readlane_u64(tin, kp - 1)
+                                                : link_tau_u(tv, r, uni(chain[kp - 1]), c);
                 if (e == E2_INF64 || tl == E2_INF64) continue;
                 const uint64_t v = umax64(e, tl);
                 a = v < a ? v : a;
             }
             A[x] = a;
             uint64_t sv = x == N ? 0 : E2_INF64;
+#pragma unroll 4
             for (int kpp = mu + 1; kpp <= m; ++kpp) {
                 // participants from kpp on: reversed row t = m + 1 - kpp at N - x
                 const uint64_t e = B[(size_t)(m - kpp) * X + (N - x)];
-                const uint64_t tl = link_tau_u(tv, r, c, uni(chain[kpp - 1]));
+                const uint64_t tl = kpp <= kWave ? readlane_u64(tout, kpp - 1)
+                                                 : link_tau_u(tv, r, c, uni(chain[kpp - 1]));
                 if (e == E2_INF64 || tl == E2_INF64) continue;
                 const uint64_t v = umax64(e, tl);
                 sv = v < sv ? v : sv;

@@ -68,7 +68,8 @@ def test_idle_random_parity(torch_dev):
 
 
 def test_idle_maximum_sizes(torch_dev):
-    """256 devices, 255 blocks, four chains of about 64 devices."""
+    """256 devices, 255 blocks, four chains of 53-73 devices (links of chain
+    positions beyond 64 take the kernel's fallback path)."""
     wl = workload.random_small(9, M=256, N=255, P=1, k_max=4, mem_lo_layers=2, mem_hi_layers=25)
     got = _gpu_idle(torch_dev, wl)
     _assert_equal(got, oracle.eval_population_idle(wl), tag="idle max")
