@@ -1142,8 +1142,9 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
 }
 
 // Reference path (chains whose bands exceed the pool): Algorithm 1's table
-// for one master position, full rows k-1..N-1, ping-ponging Ga/Gb; split
-// points of rows 2..m go to tbp (row k at (k-2)*N) when tbp is not null.
+// for one master position, full rows k-1..N-1, ping-ponging the LDS row
+// buffers; split points of rows 2..m go to tbp (row k at (k-2)*N) when tbp
+// is not null.
 __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &sm, int r, const uint8_t *chain,
                              int m, int mu, uint8_t *tbp, int lane)
 {
@@ -1215,10 +1216,12 @@ __device__ __forceinline__ int build_chain(const E2Genomes &gen, int p, int q, i
 
 // ---------------------------------------------------------------------------
 // Persistent DP kernel: one wave per workgroup; wave w of W solves listed
-// problems w, w + W, w + 2W, ... (the list runs longest chains first, so
-// every wave gets a like mix) and exits past the end of the list.  LDS: split-point pairs (N x 16 B) and the split-point bytes
-// of the forward-row pool; the row values live in a per-wave global region
-// (forward pool, backward pool, two full rows: 2 pool_cells + 2 (N+1) u64).
+// problems w, w + W, w + 2W, ... of the first part of the list (it runs
+// longest chains first, so every wave gets a like mix), the rest from a
+// shared counter when there are many problems per wave, and exits past the
+// end of the list.  LDS: split-point pairs (N x 16 B), two row buffers of
+// N+1 keys and the split-point bytes of the forward rows; the forward and
+// backward row pools live in a per-wave global region (2 pool_cells u64).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_dp(E2Tables tb, int k_max, int pool_cells,
                                            E2Genomes gen, const uint8_t *__restrict__ roles,
