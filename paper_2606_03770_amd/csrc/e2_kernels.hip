@@ -1463,14 +1463,31 @@ __device__ __forceinline__ void ft_row(const uint64_t *pr, const uint8_t *wr, ui
                 if (w == 0) best = end - pr[0];
             } else if (linked) {
                 const uint64_t c = end + tau - pN;
-                for (int j = max(w, kmin); j <= i; ++j) {
+                // four entries loaded before use, taken in ascending j with a
+                // strict < (the smallest j keeps ties), without branches
+                int j = max(w, kmin);
+                for (; j + 3 <= i; j += 4) {
+                    const uint64_t a0 = st[j], a1 = st[j + 1], a2 = st[j + 2], a3 = st[j + 3];
+                    const uint64_t v0 = a0 + c, v1 = a1 + c, v2 = a2 + c, v3 = a3 + c;
+                    const bool t0 = a0 != E2_INF64 && v0 < best;
+                    best = t0 ? v0 : best;
+                    bj = t0 ? j : bj;
+                    const bool t1 = a1 != E2_INF64 && v1 < best;
+                    best = t1 ? v1 : best;
+                    bj = t1 ? j + 1 : bj;
+                    const bool t2 = a2 != E2_INF64 && v2 < best;
+                    best = t2 ? v2 : best;
+                    bj = t2 ? j + 2 : bj;
+                    const bool t3 = a3 != E2_INF64 && v3 < best;
+                    best = t3 ? v3 : best;
+                    bj = t3 ? j + 3 : bj;
+                }
+                for (; j <= i; ++j) {
                     const uint64_t a = st[j];
-                    if (a == E2_INF64) continue;
                     const uint64_t v = a + c;
-                    if (v < best) {
-                        best = v;
-                        bj = j;
-                    }
+                    const bool t = a != E2_INF64 && v < best;
+                    best = t ? v : best;
+                    bj = t ? j : bj;
                 }
             }
         }
