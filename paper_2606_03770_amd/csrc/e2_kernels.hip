@@ -1843,8 +1843,7 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
                         const int cp = uni(chain[dir ? m - kp : kp - 1]);
                         tl = dir ? link_tau_u(tv, r, c, cp) : link_tau_u(tv, r, cp, c);
                     }
-                    if (e == E2_INF64 || tl == E2_INF64) continue;
-                    const uint64_t v = umax64(e, tl);
+                    const uint64_t v = umax64(e, tl);  // INF when either is
                     a = v < a ? v : a;
                 }
                 A[x] = a;
@@ -1856,11 +1855,12 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
                 if (x >= 1) {
                     const int w = wr[x - 1];
                     const uint64_t px = P[x];
+                    // INF is the largest value, so an infeasible prefix needs
+                    // no branch: the max is INF
                     if (w != E2_NO_START)
+#pragma unroll 4
                         for (int j = w; j < x; ++j) {
-                            const uint64_t aj = A[j];
-                            if (aj == E2_INF64) continue;
-                            const uint64_t v = umax64(aj, px - P[j]);
+                            const uint64_t v = umax64(A[j], px - P[j]);
                             e = v < e ? v : e;
                         }
                 }
@@ -1890,7 +1890,6 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
                 const uint64_t e = E[(size_t)(kp - 1) * X + x];
                 const uint64_t tl = kp <= kWave ? readlane_u64(tin, kp - 1)
                                                 : link_tau_u(tv, r, uni(chain[kp - 1]), c);
-                if (e == E2_INF64 || tl == E2_INF64) continue;
                 const uint64_t v = umax64(e, tl);
                 a = v < a ? v : a;
             }
@@ -1902,7 +1901,6 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
                 const uint64_t e = B[(size_t)(m - kpp) * X + (N - x)];
                 const uint64_t tl = kpp <= kWave ? readlane_u64(tout, kpp - 1)
                                                  : link_tau_u(tv, r, c, uni(chain[kpp - 1]));
-                if (e == E2_INF64 || tl == E2_INF64) continue;
                 const uint64_t v = umax64(e, tl);
                 sv = v < sv ? v : sv;
             }
@@ -1920,10 +1918,9 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
                 const int w = wr[y - 1];
                 const uint64_t py = P[y] + head;
                 if (w != E2_NO_START)
+#pragma unroll 4
                     for (int x = w; x < y; ++x) {
-                        const uint64_t ax = A[x];
-                        if (ax == E2_INF64) continue;
-                        const uint64_t v = umax64(umax64(ax, py - P[x]), sv);
+                        const uint64_t v = umax64(umax64(A[x], py - P[x]), sv);
                         tm = v < tm ? v : tm;
                     }
             }
