@@ -1992,14 +1992,19 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
                     const int c = uni(chain[k - 1]);
                     const bool none_ok = k <= mu;
                     const int kp_lo = k > mu ? mu : 1;
+                    const uint64_t *pr = pref_row(tv, r, c);
+                    // links into position k from kp < k (lane kp-1; past 64 loaded)
+                    const uint64_t tin = lane < k - 1 ? link_tau(tv, r, chain[lane], c) : E2_INF64;
                     for (int x = lane; x <= N; x += kWave) {
+                        P[x] = pr[x];
                         uint64_t a = (none_ok && x == 0) ? 0 : E2_INF64;
                         int arg = 0;
+#pragma unroll 4
                         for (int kp = kp_lo; kp <= k - 1; ++kp) {
                             const uint64_t e = E[(size_t)(kp - 1) * X + x];
-                            const uint64_t tl = link_tau_u(tv, r, uni(chain[kp - 1]), c);
-                            if (e == E2_INF64 || tl == E2_INF64) continue;
-                            const uint64_t v = umax64(e, tl);
+                            const uint64_t tl = kp <= kWave ? readlane_u64(tin, kp - 1)
+                                                            : link_tau_u(tv, r, uni(chain[kp - 1]), c);
+                            const uint64_t v = umax64(e, tl);  // INF when either is
                             if (v < a) {
                                 a = v;
                                 arg = kp;
@@ -2010,7 +2015,6 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
                     }
                     __syncthreads();
                     const int f = (k == mu);
-                    const uint64_t *pr = pref_row(tv, r, c);
                     const uint8_t *wr = win_row(tv, f, c);
                     const uint64_t hadd = f ? uni64(tv.head[r * M + c]) : 0;
                     const bool empty_ok = f && tv.hfit[c];
@@ -2020,11 +2024,12 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
                         if (x >= 1) {
                             const int w = wr[x - 1];
                             if (w != E2_NO_START) {
-                                const uint64_t end = pr[x] + hadd;
+                                const uint64_t end = P[x] + hadd;
+                                // an INF prefix gives an INF max, which never
+                                // passes the strict test
+#pragma unroll 4
                                 for (int j = w; j < x; ++j) {
-                                    const uint64_t aj = A[j];
-                                    if (aj == E2_INF64) continue;
-                                    const uint64_t v = umax64(aj, end - pr[j]);
+                                    const uint64_t v = umax64(A[j], end - P[j]);
                                     if (v < e) {
                                         e = v;
                                         jj = j;
