@@ -2278,24 +2278,56 @@ __global__ __launch_bounds__(64) void k_roles(int P, int M, int k_max, int R, in
         else fixed_p += rho_p[q];
     }
     const int F = __popc(fmask);
-    Best best = {E2_INF64, E2_INF64, 0xFFFFFFFFu};
-    for (uint32_t x = (uint32_t)lane; x < (1u << F); x += kWave) {
-        // deposit the bits of x onto the free clusters (order preserving)
-        uint32_t mask = 0, rest = fmask;
-        uint64_t sp = fixed_p, sd = 0;
+    // A role set is x in [0, 2^F): bit i makes the i-th free cluster (in
+    // increasing q) decode.  Lane i holds that cluster's decode and prefill
+    // rates; each lane fixes the low six bits of x (its lane id) and the high
+    // bits run in Gray-code order, so each step adds or removes one cluster's
+    // rates.  The best set is kept as x: depositing x onto the free clusters
+    // preserves order, so (w, phase, x) orders sets exactly as (w, phase,
+    // mask) does, whatever order they are visited in.
+    uint64_t dq = 0, pq = 0;
+    {
+        uint32_t rest = fmask;
         for (int i = 0; i < F; ++i) {
             const int q = __ffs(rest) - 1;
             rest &= rest - 1;
-            if ((x >> i) & 1u) {
-                mask |= 1u << q;
-                sd += rho_d[q];
-            } else {
-                sp += rho_p[q];
+            if (lane == i) {
+                dq = rho_d[q];
+                pq = rho_p[q];
             }
         }
-        const Fit f = fitness_of_rates(sp, sd, t_arrival, nd);
-        const Best c = {f.w, f.phase, mask};
-        if (best_less(c, best)) best = c;
+    }
+    const uint64_t p_all = fixed_p + wave_sum_u64(pq);  // every cluster prefill
+    const int lowF = F < 6 ? F : 6;
+    uint64_t sd = 0, sxp = 0;  // decode rates and prefill rates of x's members
+    for (int i = 0; i < lowF; ++i) {
+        const uint64_t d = readlane_u64(dq, i), pp = readlane_u64(pq, i);
+        if ((lane >> i) & 1) {
+            sd += d;
+            sxp += pp;
+        }
+    }
+    const bool active = (uint32_t)lane < (1u << lowF);
+    Best best = {E2_INF64, E2_INF64, 0xFFFFFFFFu};
+    uint32_t g = 0;  // high bits of x
+    for (uint32_t t = 0; t < (1u << (F - lowF)); ++t) {
+        if (t) {
+            const int bt = __builtin_ctz(t);
+            const uint64_t d = readlane_u64(dq, bt + 6), pp = readlane_u64(pq, bt + 6);
+            g ^= 1u << bt;
+            if ((g >> bt) & 1u) {
+                sd += d;
+                sxp += pp;
+            } else {
+                sd -= d;
+                sxp -= pp;
+            }
+        }
+        if (active) {
+            const Fit f = fitness_of_rates(p_all - sxp, sd, t_arrival, nd);
+            const Best c = {f.w, f.phase, (uint32_t)lane | (g << 6)};
+            if (best_less(c, best)) best = c;
+        }
     }
     for (int off = kWave / 2; off >= 1; off >>= 1) {
         Best o;
@@ -2303,6 +2335,15 @@ __global__ __launch_bounds__(64) void k_roles(int P, int M, int k_max, int R, in
         o.phase = __shfl_xor(best.phase, off, kWave);
         o.mask = __shfl_xor(best.mask, off, kWave);
         if (best_less(o, best)) best = o;
+    }
+    {  // deposit the best x onto the free clusters
+        uint32_t mask = 0, rest = fmask;
+        for (int i = 0; i < F; ++i) {
+            const int q = __ffs(rest) - 1;
+            rest &= rest - 1;
+            if ((best.mask >> i) & 1u) mask |= 1u << q;
+        }
+        best.mask = mask;
     }
     if (lane < k_max) {
         const uint32_t dec = (best.mask >> lane) & 1u;
