@@ -2121,12 +2121,32 @@ struct Fit {
     uint64_t w, phase, sp, sd;
 };
 
+// ceil(kScale / s) for 1 <= s < 2^58 (a sum of at most 255 rates of at most
+// kScale each), without a 64-bit integer division: with n = kScale + s - 1
+// the quotient n / s is below 2^51, so its double-precision estimate (three
+// roundings of 2^-53 relative) is within 0.75 of it and the truncation is
+// the exact floor or one off; the integer checks fix that (every product
+// stays below n + 2s < 2^60).
+__device__ __forceinline__ uint64_t ceil_scale_div(uint64_t s)
+{
+    const uint64_t n = kScale + s - 1;
+    uint64_t q = (uint64_t)((double)n / (double)s);
+    if (q * s > n) {
+        q -= 1;
+        if (q * s > n) q -= 1;
+    } else if ((q + 1) * s <= n) {
+        q += 1;
+        if ((q + 1) * s <= n) q += 1;
+    }
+    return q;
+}
+
 __device__ __forceinline__ Fit fitness_of_rates(uint64_t sum_p, uint64_t sum_d, uint64_t t_arrival,
                                                 uint64_t nd)
 {
     Fit f;
-    f.sp = sum_p ? (kScale + sum_p - 1) / sum_p : E2_INF64;
-    f.sd = sum_d ? nd * ((kScale + sum_d - 1) / sum_d) : E2_INF64;
+    f.sp = sum_p ? ceil_scale_div(sum_p) : E2_INF64;
+    f.sd = sum_d ? nd * ceil_scale_div(sum_d) : E2_INF64;
     if (f.sp == E2_INF64 || f.sd == E2_INF64) {
         f.w = f.phase = E2_INF64;
         return f;

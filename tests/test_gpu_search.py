@@ -6,6 +6,7 @@ floor, and brute-forces the role assignment; every output (all DP results,
 roles, slot counts, w, phase) equals the CPU oracle bit for bit.
 """
 import ctypes
+import dataclasses
 
 import numpy as np
 import pytest
@@ -166,3 +167,44 @@ def test_search_empty_population_and_bad_arguments(torch_dev):
     bad = dict(b_max=16, beta_ppm=0, kv_bytes_per_block_slot=0)
     with pytest.raises(e2.E2Error):
         e2.e2_ctx_create_slots(wl.problem_arrays(), bad)
+
+
+def _one_ns_clusters(seed, M, k_max):
+    """Two-block models on devices fast enough that every block takes 1 ns:
+    clusters of one or two devices reach T = 1, the largest rate (2^50), so
+    a genome's rate sums pass 2^53, where doubles stop being exact."""
+    wl = workload.random_small(seed, M=M, N=2, P=6, k_max=k_max, mem_lo_layers=3,
+                               mem_hi_layers=6)
+    wl = dataclasses.replace(wl, speed_flops=np.full(wl.n_dev, 10**15, np.uint64),
+                             layer_flops=np.ones_like(wl.layer_flops),
+                             head_flops=np.zeros(2, np.uint64), act_bytes=np.zeros(2, np.uint64))
+    wl.min_tps_milli = 0
+    return wl
+
+
+def test_search_rate_sums_past_2_53(torch_dev):
+    """The role search's rate divisions at their largest sums (16 clusters of
+    rate up to 2^50)."""
+    wl = _one_ns_clusters(78, 32, 16)
+    sm = dict(b_max=1, beta_ppm=0, kv_bytes_per_block_slot=0)
+    want = oracle.search_roles(wl, sm)
+    t = want["T_all"][:, :, 0]
+    sums = [sum((1 << 50) // int(x) for x in row if x != INF) for row in t]
+    assert max(sums) > 1 << 53
+    _assert_equal(_gpu_search(torch_dev, wl, sm), want, tag="rates")
+
+
+def test_fitness_rate_sums_past_2_53(torch_dev):
+    """The fixed-role fitness at rate sums past 2^54 (40 clusters)."""
+    torch, dev = torch_dev
+    wl = _one_ns_clusters(79, 80, 40)
+    want = oracle.eval_population(wl)
+    fin = want["T"][want["T"] != INF]
+    assert (fin == 1).sum() > 60
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    fit = e2.e2_eval_population(ctx, L, R, wl.fitness_params())
+    torch.cuda.synchronize()
+    for k in ("w", "phase", "s_p", "s_d"):
+        assert (e2.u64(fit[k]) == want[k]).all(), k
