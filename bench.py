@@ -550,9 +550,9 @@ def ablations(torch, dev, steps, warmup):
     finishing-time objective against Algorithm 1's bottleneck (same genomes,
     roles and fitness), and the adapted-SplitWise role rule against the
     brute-force role search (same slot model and DP results)."""
-    import oracle
     wl = workload.make(SEARCH_WORKLOAD)
     fp = wl.fitness_params()
+    np_tok = wl.prompt_tokens()
     L = torch.from_numpy(wl.labels).to(dev)
     R = torch.from_numpy(wl.roles).to(dev)
     ctx = e2.e2_ctx_create(wl.problem_arrays())
@@ -569,9 +569,9 @@ def ablations(torch, dev, steps, warmup):
     sm = workload.slot_model(wl)
     sctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
     se = e2.e2_search_roles(sctx, L, fp, wl.k_max)
-    sw = e2.e2_search_roles(sctx, L, fp, wl.k_max, splitwise_np_tokens=oracle.np_tokens(wl))
+    sw = e2.e2_search_roles(sctx, L, fp, wl.k_max, splitwise_np_tokens=np_tok)
     ms_sw = _timed(torch, lambda: e2.e2_search_roles(sctx, L, fp, wl.k_max, out=sw,
-                                                    splitwise_np_tokens=oracle.np_tokens(wl)),
+                                                    splitwise_np_tokens=np_tok),
                    steps, warmup)
     torch.cuda.synchronize()
     log(f"ablations on {wl.name}: eval {ms_bn:.3f} ms, finishing-time eval {ms_ft:.3f} ms, "

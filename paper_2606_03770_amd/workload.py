@@ -81,6 +81,13 @@ class Workload:
         return dict(t_arrival_ns=self.t_arrival_ns, nd_tokens=self.nd_tokens,
                     min_tps_milli=self.min_tps_milli)
 
+    def prompt_tokens(self) -> int:
+        """Prompt length NP in tokens, as the activation sizes were built:
+        the prefill activation carries NP tokens, the decode one a single
+        token."""
+        act = [int(x) for x in self.act_bytes]
+        return act[0] // max(act[1], 1)
+
     def ga_params(self, generation: int = 0) -> dict:
         return dict(seed=self.ga_seed, generation=generation,
                     tournament_k=self.tournament_k,
@@ -311,7 +318,5 @@ def slot_model(wl: Workload, b_max: int = 8, beta_ppm: int = 125_000) -> dict:
     example of a device whose memory holds four or, with a second pipeline
     stage, eight concurrent requests.
     """
-    act = [int(x) for x in wl.act_bytes]
-    np_tokens = act[0] // max(act[1], 1)
-    kv = 2 * act[1] * (np_tokens + int(wl.nd_tokens))
+    kv = 2 * int(wl.act_bytes[1]) * (wl.prompt_tokens() + int(wl.nd_tokens))
     return dict(b_max=int(b_max), beta_ppm=int(beta_ppm), kv_bytes_per_block_slot=kv)

@@ -1,7 +1,7 @@
 """Write printed_plans.json from the deployment-plan tables of the E2LLM paper.
 
-Run once, where the paper's LaTeX source is available:
-    python tests/golden/extract_printed_plans.py /root/reference/PAPER.md
+Run once, with the path of the paper's LaTeX source as the one argument:
+    python tests/golden/extract_printed_plans.py <paper source>
 
 It parses every plan table (Sec. 4 Tables 3-6 and the App. B tables): each
 replica's mode (P/D), its devices, which device is the master (starred) and
@@ -80,7 +80,9 @@ def _add_dev(rep, text):
 
 
 def main():
-    src = sys.argv[1] if len(sys.argv) > 1 else "/root/reference/PAPER.md"
+    if len(sys.argv) != 2:
+        sys.exit("usage: extract_printed_plans.py <path of the paper's LaTeX source>")
+    src = sys.argv[1]
     tables = parse(src)
     out = []
     for t in tables:

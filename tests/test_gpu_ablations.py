@@ -111,7 +111,7 @@ def _gpu_splitwise(torch_dev, wl, sm, labels=None):
     ctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
     L = torch.from_numpy(np.ascontiguousarray(labels)).to(dev)
     out = e2.e2_search_roles(ctx, L, wl.fitness_params(), wl.k_max, with_tables=True,
-                             splitwise_np_tokens=oracle.np_tokens(wl))
+                             splitwise_np_tokens=wl.prompt_tokens())
     torch.cuda.synchronize()
     return dict(T_all=e2.u64(out["T_all"]), Lambda_all=e2.u64(out["Lambda_all"]),
                 roles=out["roles"].cpu().numpy(), slots=out["slots"].cpu().numpy(),
