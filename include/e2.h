@@ -223,6 +223,31 @@ int e2_eval_population(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
                        uint64_t *w, uint64_t *phase, uint64_t *s_p, uint64_t *s_d);
 
 /*
+ * e2_eval_population without any device allocation, for callers that cannot
+ * allocate: code under HIP graph capture, allocation-free serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, layouts and results as
+ * e2_eval_population.  Instead of a stream-ordered allocation, the call's
+ * working memory (counters, the problem list, per-cluster T and Lambda, the
+ * DP waves' row regions) is carved from one fixed 96 MiB device array that
+ * the library holds on each GPU it runs on until the process ends.
+ *   Limit: P * k_max * 32 bytes plus one DP wave's rows (2 * 8 * (the
+ *   largest band total, 3969 cells at N = 126) + N * N bytes) must fit in
+ *   96 MiB (P * k_max up to about 3.1 million at N = 126); larger inputs
+ *   return E2_EINVAL before anything is enqueued.  Large populations run
+ *   with fewer DP waves than e2_eval_population (same results, slower).
+ *   Every call on one GPU shares that GPU's array and leaves its contents
+ *   behind: calls that overlap on one GPU (several streams or threads) race
+ *   and must be serialised by the caller.  The counters are cleared by a
+ *   kernel at the start of each call (no memset node).
+ * Errors as e2_eval_population; E2_EHIP also when the array's device
+ * address could not be resolved.
+ */
+int e2_eval_population_noalloc(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                               const uint8_t *labels, const uint8_t *roles,
+                               const e2_fitness_params *fp,
+                               uint64_t *w, uint64_t *phase, uint64_t *s_p, uint64_t *s_d);
+
+/*
  * One GA generation (Algorithm 2: elites, crossover, mutation; Sec. 3.4).
  *   labels_in[P][M], roles_in[P][k_max], w_in[P], phase_in[P]  device in
  *   labels_out[P][M], roles_out[P][k_max]  device out; must not overlap

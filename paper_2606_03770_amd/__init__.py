@@ -46,7 +46,8 @@ EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitio
             "e2_eval_population_ordered", "e2_ga_step_ordered", "e2_ctx_create_slots",
             "e2_search_roles", "e2_assign_roles_splitwise", "e2_solve_partitions_ft",
             "e2_eval_population_ft", "e2_solve_partitions_idle", "e2_eval_population_idle",
-            "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror")
+            "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror",
+            "e2_eval_population_noalloc")
 
 
 class E2Error(RuntimeError):
@@ -112,6 +113,8 @@ def lib() -> ctypes.CDLL:
     L.e2_eval_population.argtypes = [vp, vp, i32, i32, vp, vp, ctypes.POINTER(e2_fitness_params),
                                      vp, vp, vp, vp]
     L.e2_eval_population.restype = ctypes.c_int
+    L.e2_eval_population_noalloc.argtypes = L.e2_eval_population.argtypes
+    L.e2_eval_population_noalloc.restype = ctypes.c_int
     L.e2_ga_step.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, ctypes.POINTER(e2_ga_params),
                              vp, vp]
     L.e2_ga_step.restype = ctypes.c_int
@@ -304,7 +307,9 @@ def e2_eval_population(ctx: Context, labels, roles, fitness: dict, stream=None,
                        with_rates: bool = True, out: Optional[dict] = None,
                        objective: str = "bottleneck"):
     """Returns dict w, phase (and s_p, s_d) as int64 bits of u64, shape [P].
-    objective "finish_time" calls e2_eval_population_ft, "idle" e2_eval_population_idle."""
+    objective "finish_time" calls e2_eval_population_ft, "idle" e2_eval_population_idle,
+    "noalloc" e2_eval_population_noalloc (the library's fixed scratch instead of an
+    allocation; outputs still come from `out` or torch)."""
     torch = _torch()
     P = labels.shape[0]
     k_max = roles.shape[1]
@@ -317,7 +322,7 @@ def e2_eval_population(ctx: Context, labels, roles, fitness: dict, stream=None,
     fp = e2_fitness_params(int(fitness["t_arrival_ns"]), int(fitness["nd_tokens"]),
                            int(fitness["min_tps_milli"]))
     name = {"bottleneck": "e2_eval_population", "finish_time": "e2_eval_population_ft",
-            "idle": "e2_eval_population_idle"}[objective]
+            "idle": "e2_eval_population_idle", "noalloc": "e2_eval_population_noalloc"}[objective]
     _check(getattr(lib(), name)(ctx.handle, _stream(stream), P, k_max, _ptr(labels),
                                 _ptr(roles), ctypes.byref(fp), _ptr(out["w"]),
                                 _ptr(out["phase"]), _ptr(out.get("s_p")),

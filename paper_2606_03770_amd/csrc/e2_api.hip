@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "../../include/e2.h"
@@ -80,6 +81,44 @@ int quantise(const e2_problem *pr, uint64_t *t, uint64_t *h, uint64_t *tau)
 }
 
 hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ---------------------------------------------------------------------------
+// Fixed device scratch of e2_eval_population_noalloc: the call's counters,
+// problem list, per-cluster T and Lambda and the DP waves' row regions are
+// carved from this array instead of a stream-ordered allocation.  Each GPU
+// the library runs on holds its own copy until the process ends.  In host
+// code `scratch` names a host-side stand-in: only the address returned by
+// hipGetSymbolAddress (one per device, kept in g_scratch) is a device
+// address.
+// ---------------------------------------------------------------------------
+constexpr size_t kNoAllocBytes = (size_t)96 << 20;
+__device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+struct ScratchSlot {
+    std::once_flag once;
+    void *ptr = nullptr;
+    hipError_t err = hipSuccess;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// Resolve (once per device, with that device current) and return the
+// device address of this device's scratch.
+int scratch_on(int dev, void **out)
+{
+    if (dev < 0 || dev >= kMaxDevices) return E2_EINVAL;
+    ScratchSlot &sl = g_scratch[dev];
+    std::call_once(sl.once, [&sl] {
+        sl.err = hipGetSymbolAddress(&sl.ptr, HIP_SYMBOL(scratch));
+        if (sl.err != hipSuccess) {
+            (void)hipGetLastError();
+            sl.ptr = nullptr;
+        }
+    });
+    if (sl.err != hipSuccess || !sl.ptr) return E2_EHIP;
+    *out = sl.ptr;
+    return E2_OK;
+}
 
 int check_device(const e2_ctx *ctx)
 {
@@ -369,6 +408,12 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
     if (hipGetDevice(&ctx->device) != hipSuccess) {
         free(ctx);
         return E2_EHIP;
+    }
+    // the allocation-free entry point's scratch address on this device; a
+    // failure is reported by that entry point, not here
+    {
+        void *unused = nullptr;
+        (void)scratch_on(ctx->device, &unused);
     }
     if (hipMalloc(&ctx->blob, total) != hipSuccess) {
         (void)hipGetLastError();
@@ -744,6 +789,51 @@ int e2_eval_population_ft(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
     if (P > 0 && !labels) return E2_EINVAL;
     const E2Genomes gen = {labels, nullptr, nullptr};
     return eval_impl(ctx, stream, P, k_max, gen, roles, fp, w, phase, s_p, s_d, 1);
+}
+
+int e2_eval_population_noalloc(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                               const uint8_t *labels, const uint8_t *roles,
+                               const e2_fitness_params *fp, uint64_t *w, uint64_t *phase,
+                               uint64_t *s_p, uint64_t *s_d)
+{
+    if (!ctx || !fp) return E2_EINVAL;
+    int rc = check_pop(P, k_max);
+    if (rc) return rc;
+    if (fp->nd_tokens > 8192) return E2_EINVAL;
+    if (P == 0) return E2_OK;
+    if (!labels || !roles || !w || !phase) return E2_EINVAL;
+    if ((rc = check_device(ctx))) return rc;
+    // layout of the fixed scratch: counters, list, T and Lambda, then as
+    // many DP waves' row regions (and split-point tables) as still fit
+    const size_t problems = (size_t)P * k_max;
+    const size_t tl = align256(problems * 8);
+    const size_t fixed = align256(32) + align256(problems * 4 * 4) + 2 * tl;
+    const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
+    const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_lds_tb_cells(ctx->N);
+    const size_t per_wave = e2_dp_row_words(ctx->N) * 8 + (need_tb ? (size_t)ctx->N * ctx->N : 0);
+    if (fixed + per_wave + 2 * 256 > kNoAllocBytes) return E2_EINVAL;  // beyond the maximum
+    const size_t fit = (kNoAllocBytes - fixed - 2 * 256) / per_wave;
+    const int np = (int)(problems < (size_t)INT32_MAX ? problems : INT32_MAX);
+    int slots = e2_dp_slots(ctx->N, np);
+    if ((size_t)slots > fit) slots = (int)fit;
+    const size_t tbb = need_tb ? (size_t)slots * ctx->N * ctx->N : 0;
+    void *base = nullptr;
+    if ((rc = scratch_on(ctx->device, &base))) return rc;
+    E2Work wk;
+    carve_work(base, ctx, P, k_max, slots, tbb, &wk);
+    char *after = static_cast<char *>(base) + align256(32) + align256(problems * 4 * 4) +
+                  align256((size_t)slots * e2_dp_row_words(ctx->N) * 8) + align256(tbb);
+    uint64_t *Ts = reinterpret_cast<uint64_t *>(after);
+    uint64_t *Ls = reinterpret_cast<uint64_t *>(after + tl);
+    hipStream_t s = as_stream(stream);
+    hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, {labels, nullptr, nullptr},
+                                        roles, wk, Ts, Ls, nullptr, nullptr);
+    if (e != hipSuccess) return E2_EHIP;
+    const uint64_t lam_max =
+        fp->min_tps_milli ? 1000000000000ull / fp->min_tps_milli : E2_INF64;
+    e = e2_launch_fitness(s, P, k_max, Ts, Ls, roles, fp->t_arrival_ns, fp->nd_tokens, lam_max,
+                          w, phase, s_p, s_d);
+    return e == hipSuccess ? E2_OK : E2_EHIP;
 }
 
 int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_t *labels_in,
