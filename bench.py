@@ -191,7 +191,10 @@ def head_free(problem):
 
 def generation_work(wl, problems, roles, T, master, tabs, T0):
     """(Algorithm 1 cells over feasible problems, useful j-candidates the DP
-    kernel evaluates with u64 keys, those it evaluates with u32 or fp64 keys)
+    kernel evaluates with u64 keys, those it evaluates with u32 or fp64 keys,
+    Algorithm 1's own memory-feasible j-candidates over the problems that
+    pass the pre-check: one full table per master, every cell scanning the
+    split points its window allows)
     for one population, given as its (genome, cluster, chain) problems, their
     optima T, masters and optima T0 without a master (head_free).  The
     candidate count follows k_dp row by row: reversed rows, the last cell of
@@ -211,6 +214,7 @@ def generation_work(wl, problems, roles, T, master, tabs, T0):
     cells = 0
     cand = 0
     cand32 = 0
+    alg1 = 0
 
     def rows(f, d, kmin, lo, hi):
         """useful candidates of rows with cells lo..hi (arrays, broadcast)"""
@@ -242,6 +246,14 @@ def generation_work(wl, problems, roles, T, master, tabs, T0):
             continue
         ch, c0, cH, feas, pq = ch[listed], c0[listed], cH[listed], feas[listed], pq[listed]
         n = len(ch)
+        # Algorithm 1 as the paper states it: for each master, rows 2..m over
+        # cells k-1..N-1, the master's row with its head window
+        k_all = np.arange(1, m + 1)
+        lo_a = np.broadcast_to(k_all - 1, ch.shape)
+        hi_a = np.full(ch.shape, N - 1)
+        a0 = rows(0, ch, lo_a, lo_a, hi_a)
+        a1 = rows(1, ch, lo_a, lo_a, hi_a)
+        alg1 += int(((m - 1) * a0 + a1)[:, 1:].sum())
         rr = (roles[pq[:, 0], pq[:, 1]] != 0).astype(np.int64)
         links = [[int(tau[rr[a], ch[a][k - 1], ch[a][k]]) for k in range(1, m)] for a in range(n)]
         links = [[x for x in lk if x != INF] for lk in links]
@@ -325,7 +337,7 @@ def generation_work(wl, problems, roles, T, master, tabs, T0):
             per = ((m - 1) * r0 + r1)[:, 1:].sum(1)
             extra = np.where(np.arange(1, m + 1)[None, :] == mus[:, None], r1, r0)[:, 1:].sum(1)
             cand += int((per + np.where(mus > 0, extra, 0)).sum())
-    return cells, cand, cand32
+    return cells, cand, cand32, alg1
 
 
 # ---------------------------------------------------------------------------
@@ -342,6 +354,9 @@ def main():
                          "(with --genomes both; 0 disables)")
     ap.add_argument("--search-steps", type=int, default=5,
                     help="timed role and slot searches on the 1024-genome workload "
+                         "(with --genomes both; 0 disables)")
+    ap.add_argument("--config-steps", type=int, default=10,
+                    help="timed evaluations of each of the 12- to 128-device workloads "
                          "(with --genomes both; 0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU-oracle sample (0 disables)")
@@ -432,10 +447,12 @@ def main():
         return {
             "ms_per_step": t["elapsed"] * 1e3 / n,
             "fitness_evals_per_s": P * n / t["elapsed"],
+            "kernel_candidates_per_s": (t["cand"] + t["cand32"]) / t["elapsed"],
             "dp_cells_per_step": t["cells"] / n,
             "j_candidates_per_step": (t["cand"] + t["cand32"]) / n,
             "j_candidates_u32_or_f64_keys_per_step": t["cand32"] / n,
-            "roofline": roofline(t, n, profiled_traffic(wl.name, genomes)),
+            "roofline": roofline(t, n, profiled(wl.name, genomes)),
+            "algorithm_1": algorithmic(t, n),
         }
 
     steps = {"labels": "one GA generation: e2_eval_population + e2_ga_step",
@@ -446,7 +463,7 @@ def main():
     result = {
         "metric": METRIC,
         "value": t["cells"] / t["elapsed"],
-        "unit": "DP cells/s",
+        "unit": "Algorithm-1-equivalent DP cells/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -471,12 +488,72 @@ def main():
     if args.genomes == "both" and args.search_steps > 0:
         result["role_search"] = role_search(torch, dev, args.search_steps, args.warmup)
         result["ablations"] = ablations(torch, dev, args.search_steps, args.warmup)
+    if args.genomes == "both" and args.config_steps > 0:
+        result["configs"] = {name: config_eval(torch, dev, name, args.config_steps, args.warmup)
+                             for name in workload.NAMES[:4]}
     if args.cpu_seconds > 0 and head == "labels":
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        L0 = torch.from_numpy(wl.labels).to(dev)
+        R0 = torch.from_numpy(wl.roles).to(dev)
+        sol = e2.e2_solve_partitions(ctx, L0, R0)
+        fit0 = e2.e2_eval_population(ctx, L0, R0, fp)
+        torch.cuda.synchronize()
+        gpu0 = dict(T=e2.u64(sol["T"]), Lambda=e2.u64(sol["Lambda"]),
+                    master=sol["master"].cpu().numpy(), layers=sol["layers"].cpu().numpy(),
+                    **{k: e2.u64(v) for k, v in fit0.items()})
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, gpu0)
     print(json.dumps(result), flush=True)
 
 
 SEARCH_WORKLOAD = "c3_64dev_80L"
+
+
+def config_eval(torch, dev, name, steps, warmup):
+    """One workload's whole population through e2_eval_population: time per
+    call (wall clock around `steps` calls after `warmup`), the DP kernel's
+    time from the library's events, fitness evaluations/s, and the
+    Algorithm 1 cells and candidates of the population against the kernel's
+    own candidates."""
+    wl = workload.make(name)
+    P, K = wl.population, wl.k_max
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    ctx_free = e2.e2_ctx_create(head_free(wl.problem_arrays()))
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    fp = wl.fitness_params()
+    out = e2.e2_eval_population(ctx, L, R, fp, with_rates=False)
+    for _ in range(warmup):
+        e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=out)
+    torch.cuda.synchronize()
+    e2.e2_ctx_dp_timing(ctx, steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=out)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    n_dp, dp_ms = e2.e2_ctx_dp_elapsed(ctx)
+    e2.e2_ctx_dp_timing(ctx, 0)
+    sol = e2.e2_solve_partitions(ctx, L, R)
+    sol0 = e2.e2_solve_partitions(ctx_free, L, R)
+    torch.cuda.synchronize()
+    win, winR, cap = window_tables(wl)
+    tabs = (win, winR, cap) + count_tables(win, winR, wl.n_layer) + value_bounds(wl, win)
+    cells, cand, cand32, alg1 = generation_work(
+        wl, label_problems(wl.labels, K), wl.roles, e2.u64(sol["T"]),
+        sol["master"].cpu().numpy(), tabs, e2.u64(sol0["T"]))
+    kern = cand + cand32
+    dp_s = dp_ms / 1e3 / n_dp
+    log(f"{name}: {elapsed * 1e3 / steps:.3f} ms per evaluation, DP kernel {dp_s * 1e3:.3f} ms")
+    return {"devices": wl.n_dev, "layers": wl.n_layer, "population": P,
+            "call": "e2_eval_population", "steps": steps,
+            "ms_per_eval": elapsed * 1e3 / steps,
+            "fitness_evals_per_s": P * steps / elapsed,
+            "dp_cells_per_s": cells * steps / elapsed,
+            "k_dp_avg_ms": dp_s * 1e3,
+            "kernel_candidates_per_eval": kern,
+            "alg1_candidates_per_eval": alg1,
+            "frac": (cand * OPS_PER_CANDIDATE + cand32 * OPS_PER_CANDIDATE_NARROW) / dp_s
+                    / INT_VALU_PEAK}
 
 
 def role_search(torch, dev, steps, warmup):
@@ -633,27 +710,69 @@ def measure(torch, ctx, stream, bufs, init, step, count, warmup, steps):
     step_ms = [a.elapsed_time(b) for a, b in events]
     log(f"timed {steps} steps: {elapsed * 1e3:.2f} ms; generation {np.mean(step_ms):.3f} ms "
         f"avg on the stream; DP kernel {dp_ms / n_dp:.3f} ms avg")
-    cells = cand = cand32 = 0
+    cells = cand = cand32 = alg1 = 0
     pop = tuple(x.clone() for x in init)
     for g in range(steps):
-        (c1, c2, c3), pop = count(g, pop)
+        (c1, c2, c3, c4), pop = count(g, pop)
         cells += c1
         cand += c2
         cand32 += c3
+        alg1 += c4
     return dict(elapsed=elapsed, dp_s=dp_ms / 1e3, step_ms=float(np.mean(step_ms)), cells=cells,
-                cand=cand, cand32=cand32)
+                cand=cand, cand32=cand32, alg1=alg1)
 
 
-def roofline(t, steps, traffic):
-    achieved = (t["cand"] * OPS_PER_CANDIDATE + t["cand32"] * OPS_PER_CANDIDATE_NARROW) / t["dp_s"]
-    return {"bound": "alu", "kernel": "k_dp",
-            "achieved": achieved / 1e12, "peak": INT_VALU_PEAK / 1e12,
-            "unit": "TOP/s (int32 VALU)", "frac": achieved / INT_VALU_PEAK,
-            "traffic": traffic,
-            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
-                            "copy-calibrated)",
-            "avg_launch_ms": t["dp_s"] * 1e3 / steps,
-            "generation_ms_on_stream": t["step_ms"]}
+def roofline(t, steps, prof):
+    """The DP kernel against the int32 VALU peak.  frac counts the j-candidates
+    the kernel itself evaluates (3 ops each on u32 or fp64 keys, 8 on u64
+    keys) per second of its launches.  From the committed rocprofv3 profile
+    of the same workload and sources (when there is one): HBM traffic, the
+    VALU issue fraction (every issued wave instruction as 64 lane-ops), the
+    share of those lane-ops that are candidate ops, VALUBusy, VALU lane
+    utilisation, SALUBusy, LDS activity and LDS bank conflicts."""
+    ops = t["cand"] * OPS_PER_CANDIDATE + t["cand32"] * OPS_PER_CANDIDATE_NARROW
+    achieved = ops / t["dp_s"]
+    out = {"bound": "alu", "kernel": "k_dp",
+           "achieved": achieved / 1e12, "peak": INT_VALU_PEAK / 1e12,
+           "unit": "TOP/s (int32 VALU)", "frac": achieved / INT_VALU_PEAK,
+           "frac_counts": "j-candidates the kernel evaluates (banded decomposition), "
+                          "3 VALU ops each",
+           "traffic": prof.get("k_dp_hbm_bytes_per_launch") if prof else None,
+           "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                           "copy-calibrated)",
+           "avg_launch_ms": t["dp_s"] * 1e3 / steps,
+           "generation_ms_on_stream": t["step_ms"]}
+    if prof and prof.get("sq_insts_valu_per_launch"):
+        us = prof["k_dp_avg_us"]
+        valu_lane_ops = prof["sq_insts_valu_per_launch"] * 64
+        out["profile"] = {
+            "valu_issue_frac": valu_lane_ops / (us * 1e-6 * INT_VALU_PEAK),
+            "candidate_share_of_valu_lane_ops": (ops / steps) / valu_lane_ops,
+            "valu_busy_pct": prof.get("valu_busy_pct"),
+            "valu_utilization_pct": prof.get("valu_utilization_pct"),
+            "salu_busy_pct": prof.get("salu_busy_pct"),
+            "lds_active_pct": prof.get("lds_active_pct"),
+            "lds_bank_conflict_pct": prof.get("lds_bank_conflict_pct"),
+            "wait_any_share_of_wave_cycles": prof.get("wait_any_share"),
+            "hbm_read_bytes_per_launch": prof.get("k_dp_hbm_read_bytes"),
+            "hbm_write_bytes_per_launch": prof.get("k_dp_hbm_write_bytes"),
+            "k_dp_avg_us_profiled": us,
+            "source": prof.get("summary")}
+    return out
+
+
+def algorithmic(t, steps):
+    """Algorithm 1's own work next to the kernel's: its memory-feasible
+    j-candidates (one full table per master) per step, their rate at 3 ops
+    each over the kernel's time as a fraction of the peak (above 1 means the
+    decomposition skips more work than the hardware could do), and the
+    reduction factor."""
+    kern = t["cand"] + t["cand32"]
+    return {"alg1_candidates_per_step": t["alg1"] / steps,
+            "kernel_candidates_per_step": kern / steps,
+            "algorithmic_reduction": t["alg1"] / kern if kern else None,
+            "alg1_equivalent_frac_of_peak":
+                t["alg1"] * OPS_PER_CANDIDATE_NARROW / t["dp_s"] / INT_VALU_PEAK}
 
 
 LIB_SOURCES = ("e2_api.hip", "e2_internal.h", "e2_kernels.hip")
@@ -679,17 +798,18 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def profiled_traffic(workload_name, genomes="labels"):
-    """HBM bytes per DP launch from the committed rocprofv3 counter summary
-    of this workload and genome kind, or None when none exists or the kernel
-    sources have changed since it was taken."""
+def profiled(workload_name, genomes="labels"):
+    """The committed rocprofv3 summary (profiles/k_dp_*.json) of this workload
+    and genome kind, or None when none exists or the kernel sources have
+    changed since it was taken."""
     import glob
     for f in sorted(glob.glob(os.path.join(ROOT, "profiles", "k_dp_*.json"))):
         with open(f) as fh:
             meta = json.load(fh)
         if (meta.get("workload") == workload_name and meta.get("genomes", "labels") == genomes
                 and meta.get("sources_sha256_16") == source_hash()):
-            return meta.get("k_dp_hbm_bytes_per_launch")
+            meta["summary"] = os.path.relpath(f[:-5] + ".md", ROOT)
+            return meta
     return None
 
 
@@ -705,9 +825,23 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_bytes": (nbytes // 8) * 8, "launches": 5}), flush=True)
 
 
-def cpu_baseline(wl, seconds):
-    """The oracle, as it is, on the first S genomes of the generation-0
-    population (S sized from a short probe to take about `seconds`)."""
+def host_cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, seconds, gpu0=None):
+    """The oracle, as it is (single-threaded C, one host core), on the first S
+    genomes of the generation-0 population, S sized from a short probe to
+    take about `seconds`.  Its rows are then compared with the GPU's
+    evaluation of the same genomes (gpu0: T, Lambda, master, layers, w,
+    phase, S_P, S_D of generation 0)."""
     import oracle
     oracle._load()
     probe = 16
@@ -726,11 +860,23 @@ def cpu_baseline(wl, seconds):
             if sol["T"][p, q] != INF:
                 m = int((sub.labels[p] == q).sum())
                 cells += m * sum(N - k + 1 for k in range(1, m + 1))
-    log(f"cpu oracle: {S} genomes in {dt:.2f} s")
-    return {"value": cells / dt, "unit": "DP cells/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {S} of {wl.population} genomes of generation 0, "
-                      f"full evaluation (quantise, DP per cluster, fitness)",
-            "fitness_evals_per_s": S / dt, "seconds": dt}
+    out = {"value": cells / dt, "unit": "Algorithm-1-equivalent DP cells/s", "cores": 1,
+           "kind": "oracle",
+           "sample": f"first {S} of {wl.population} genomes of generation 0 of the "
+                     f"256-device workload, full evaluation (quantise, Algorithm 1 per "
+                     f"cluster, Eq. 3-5), not the generation's GA step",
+           "fitness_evals_per_s": S / dt, "seconds": dt,
+           "host_cores": os.cpu_count(), "host_cpu_model": host_cpu_model()}
+    if gpu0 is not None:
+        keys = ("T", "Lambda", "master", "layers", "w", "phase", "s_p", "s_d")
+        same = np.ones(S, dtype=bool)
+        for k in keys:
+            same &= np.asarray(gpu0[k][:S] == sol[k]).reshape(S, -1).all(axis=1)
+        out["gpu_rows_equal"] = int(same.sum())
+        out["gpu_rows_compared"] = S
+    log(f"cpu oracle: {S} genomes in {dt:.2f} s"
+        + (f"; {out['gpu_rows_equal']} of {S} equal the GPU's rows" if gpu0 is not None else ""))
+    return out
 
 
 if __name__ == "__main__":

@@ -142,6 +142,40 @@ def _direct(wl, problems, roles, T, master, T0):
     return c64, c32
 
 
+def _alg1_direct(wl, problems):
+    """Memory-feasible split points of every cell of every master's table
+    (rows 2..m, cells k-1..N-1, starts j >= k-1) over the problems that pass
+    the pre-check (m <= N, every device holds a block, total capacity >= N,
+    some device holds a block with the head)."""
+    N = wl.n_layer
+    b = np.concatenate([[0], np.cumsum([int(x) for x in wl.layer_bytes])])
+    HB = int(wl.head_bytes)
+
+    def cap(d, extra):
+        best = 0
+        for i in range(N):
+            for j in range(i + 1):
+                if b[i + 1] - b[j] + extra <= int(wl.mem_bytes[d]):
+                    best = max(best, i - j + 1)
+                    break
+        return best
+    c0 = {d: cap(d, 0) for d in range(wl.n_dev)}
+    cH = {d: cap(d, HB) for d in range(wl.n_dev)}
+    total = 0
+    for _, _, chain in problems:
+        m = len(chain)
+        if not (m <= N and min(c0[d] for d in chain) >= 1 and
+                sum(c0[d] for d in chain) >= N and max(cH[d] for d in chain) >= 1):
+            continue
+        for mu in range(1, m + 1):
+            for k in range(2, m + 1):
+                mem = int(wl.mem_bytes[chain[k - 1]])
+                extra = HB if k == mu else 0
+                for i in range(k - 1, N):
+                    total += sum(1 for j in range(k - 1, i + 1) if b[i + 1] - b[j] + extra <= mem)
+    return total
+
+
 @pytest.mark.parametrize("name,P", [("c1_tiny_12dev_32L", 16), ("c2_32dev_48L", 24),
                                     ("c5_256dev_126L_ga", 6)])
 def test_candidate_counts_match_a_direct_walk(orc, name, P):
@@ -151,10 +185,14 @@ def test_candidate_counts_match_a_direct_walk(orc, name, P):
     win, winR, cap = bench.window_tables(wl)
     tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
     probs = bench.label_problems(wl.labels, wl.k_max)
-    cells, c64, c32 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs, T0)
+    cells, c64, c32, alg1 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"],
+                                                  tabs, T0)
     assert (c64, c32) == _direct(wl, probs, wl.roles, sol["T"], sol["master"], T0)
     assert c64 + c32 > 0
     assert c32 > 0                   # u32 / fp64 keys
+    # Algorithm 1's own candidates (the direct walk), more than the kernel's
+    assert alg1 == _alg1_direct(wl, probs)
+    assert alg1 > c64 + c32
     # both ends of the master sweep occur: optima equal to T0 and above it
     fin = sol["T"] != INF
     assert (sol["T"][fin] == T0[fin]).any()
@@ -168,7 +206,7 @@ def test_reference_path_counts(orc):
     win, winR, cap = bench.window_tables(wl)
     tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
     probs = bench.label_problems(wl.labels, wl.k_max)
-    _, c64, c32 = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs, T0)
+    _, c64, c32, _ = bench.generation_work(wl, probs, wl.roles, sol["T"], sol["master"], tabs, T0)
     assert (c64, c32) == _direct(wl, probs, wl.roles, sol["T"], sol["master"], T0)
     assert c64 > 0 and c32 == 0   # the reference path has u64 keys only
 
@@ -192,7 +230,9 @@ def test_candidate_counts_of_ordered_genomes(orc, name, P):
     T0 = _free_optima(orc, wl, order=op.order, sizes=op.sizes, roles=op.roles)
     win, winR, cap = bench.window_tables(wl)
     tabs = (win, winR, cap) + bench.count_tables(win, winR, wl.n_layer) + bench.value_bounds(wl, win)
-    cells, c64, c32 = bench.generation_work(wl, probs, op.roles, sol["T"], sol["master"], tabs, T0)
+    cells, c64, c32, alg1 = bench.generation_work(wl, probs, op.roles, sol["T"], sol["master"],
+                                                  tabs, T0)
+    assert alg1 == _alg1_direct(wl, probs)
     assert (c64, c32) == _direct(wl, probs, op.roles, sol["T"], sol["master"], T0)
     assert c64 + c32 > 0 and cells > 0
 
