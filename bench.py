@@ -591,6 +591,7 @@ def role_search(torch, dev, steps, warmup):
     slots = out["slots"].cpu().numpy()
     log(f"role search on {wl.name}: {elapsed * 1e3 / steps:.3f} ms per call, DP kernel "
         f"{dp_ms / n_dp:.3f} ms")
+    gen2 = ordered_search_generations(torch, dev, wl, sm, ctx, steps, warmup)
     return {"workload": wl.name, "population": wl.population, "devices": wl.n_dev,
             "layers": N, "clusters_per_genome": "8-12", "slot_model": sm,
             "call": "e2_search_roles", "steps": steps,
@@ -599,7 +600,46 @@ def role_search(torch, dev, steps, warmup):
             "feasible_dp_problems_per_call": problems,
             "dp_cells_per_s": cells * steps / elapsed,
             "k_dp_avg_ms": dp_ms / n_dp,
-            "decode_replicas_at_b_max": int((slots == sm["b_max"]).sum())}
+            "decode_replicas_at_b_max": int((slots == sm["b_max"]).sum()),
+            "two_chromosome_generation": gen2}
+
+
+def ordered_search_generations(torch, dev, wl, sm, ctx, steps, warmup):
+    """Algorithm 2's generation on the paper's two-chromosome genome (App. A):
+    e2_search_roles_ordered (every replica for prefill and each decode slot
+    count, the kept slot count, brute-force roles) scores the population,
+    then e2_ga_step_ordered breeds the next one from those keys with the
+    roles the search chose.  Timed over `steps` generations after `warmup`."""
+    op = workload.ordered_population(wl)
+    fp = wl.fitness_params()
+    O0, S0 = (torch.from_numpy(x).to(dev) for x in (op.order, op.sizes))
+    bufs = [(torch.empty_like(O0), torch.empty_like(S0), torch.empty((wl.population, wl.k_max),
+                                                                     dtype=torch.uint8,
+                                                                     device=dev))
+            for _ in range(2)]
+    res = e2.e2_search_roles_ordered(ctx, O0, S0, fp)
+
+    def run(n):
+        bufs[0][0].copy_(O0)
+        bufs[0][1].copy_(S0)
+        cur = 0
+        for g in range(n):
+            O, S, _ = bufs[cur]
+            e2.e2_search_roles_ordered(ctx, O, S, fp, out=res)
+            e2.e2_ga_step_ordered(ctx, O, S, res["roles"], res["w"], res["phase"],
+                                  op.ga_params(wl, g), out=bufs[1 - cur])
+            cur = 1 - cur
+    run(warmup)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(steps)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    log(f"two-chromosome search + GA on {wl.name}: {elapsed * 1e3 / steps:.3f} ms per generation")
+    return {"genomes": "two_chromosome", "population": wl.population,
+            "step": "e2_search_roles_ordered + e2_ga_step_ordered", "steps": steps,
+            "ms_per_generation": elapsed * 1e3 / steps,
+            "genomes_per_s": wl.population * steps / elapsed}
 
 
 def _timed(torch, fn, steps, warmup):

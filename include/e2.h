@@ -388,6 +388,25 @@ int e2_search_roles(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const u
                     uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all);
 
 /*
+ * The same role and slot search for two-chromosome genomes (App. A gene
+ * definition; Algorithm 2's inner loop on the paper's own genome): replica
+ * q's chain is its run of the ordering, in ordering order, exactly as in
+ * e2_solve_partitions_ordered (an id >= M makes the replica infeasible, an
+ * empty replica has no rates); then the same per-replica DPs for prefill and
+ * each b = 1..b_max, the same kept slot count b*, rates and brute-force role
+ * assignment, ties to the smallest decode bitmask over replica slots.
+ *   order[P][M], sizes[P][k_max]  device, as e2_solve_partitions_ordered
+ *   k_max            1..E2_MAX_SEARCH_CLUSTERS replica slots
+ *   outputs          as e2_search_roles, per replica slot
+ * E2_EINVAL for sizes out of range (P below 2^20), nd_tokens > 8192 or a
+ * NULL required pointer.
+ */
+int e2_search_roles_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                            const uint8_t *order, const uint16_t *sizes,
+                            const e2_fitness_params *fp, uint8_t *roles_out, uint8_t *slots_out,
+                            uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all);
+
+/*
  * The adapted-SplitWise role rule (the ablation of Sec. 4.2), on the same
  * per-cluster DP results as e2_search_roles: per genome the R' non-empty
  * clusters split by the token ratio, n_P = R' * np_tokens / (np_tokens +

@@ -79,6 +79,9 @@ def _load() -> ctypes.CDLL:
     lib.oracle_search_roles.argtypes = [i32, i32, P, P, P, P, P, u64, u64, i32, i32, i32, P,
                                         u64, u64, u64, P, P, P, P, P, P]
     lib.oracle_search_roles.restype = i32
+    lib.oracle_search_roles_ordered.argtypes = [i32, i32, P, P, P, P, P, u64, u64, i32, i32, i32,
+                                                P, P, u64, u64, u64, P, P, P, P, P, P]
+    lib.oracle_search_roles_ordered.restype = i32
     lib.oracle_assign_roles_splitwise.argtypes = [i32, i32, P, P, P, P, P, u64, u64, i32, i32,
                                                   i32, P, u64, u64, u64, u64, P, P, P, P, P, P]
     lib.oracle_assign_roles_splitwise.restype = i32
@@ -389,6 +392,38 @@ def search_roles(wl, slot_model, labels=None, policy="search"):
         raise OracleError(f"unknown policy {policy}")
     if rc != 0:
         raise OracleError(f"oracle role assignment ({policy}) failed: {rc}")
+    return dict(T_all=T, Lambda_all=L, roles=roles, slots=slots, w=w, phase=ph)
+
+
+def search_roles_ordered(wl, slot_model, order, sizes):
+    """The role and slot search for two-chromosome genomes (App. A): replica
+    q's chain is its run of the ordering.  Returns the same dict as
+    search_roles, per replica slot."""
+    lib = _load()
+    order = np.ascontiguousarray(order, dtype=np.uint8)
+    sizes = np.ascontiguousarray(sizes, dtype=np.uint16)
+    P, M = order.shape
+    K = sizes.shape[1]
+    if sizes.shape != (P, K) or M != wl.n_dev:
+        raise OracleError("order must be [P][M] and sizes [P][k_max]")
+    b_max = int(slot_model["b_max"])
+    R = b_max + 1
+    t, h, tau = quantise_slots(wl.problem_arrays(), b_max, slot_model["beta_ppm"])
+    t, h, tau = (np.ascontiguousarray(x) for x in (t, h, tau))
+    T = np.zeros((P, K, R), dtype=np.uint64)
+    L = np.zeros((P, K, R), dtype=np.uint64)
+    roles = np.zeros((P, K), dtype=np.uint8)
+    slots = np.zeros((P, K), dtype=np.uint8)
+    w = np.zeros(P, dtype=np.uint64)
+    ph = np.zeros(P, dtype=np.uint64)
+    fp = wl.fitness_params()
+    rc = lib.oracle_search_roles_ordered(
+        M, wl.n_layer, _p(t), _p(h), _p(tau), _p(_u64(wl.mem_bytes)), _p(_u64(wl.layer_bytes)),
+        int(wl.head_bytes), int(slot_model["kv_bytes_per_block_slot"]), b_max, P, K, _p(order),
+        _p(sizes), int(fp["t_arrival_ns"]), int(fp["nd_tokens"]), int(fp["min_tps_milli"]),
+        _p(T), _p(L), _p(roles), _p(slots), _p(w), _p(ph))
+    if rc != 0:
+        raise OracleError(f"oracle_search_roles_ordered failed: {rc}")
     return dict(T_all=T, Lambda_all=L, roles=roles, slots=slots, w=w, phase=ph)
 
 

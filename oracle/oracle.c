@@ -925,7 +925,8 @@ int oracle_quantise_slots(int M, int N, const uint64_t *speed, const uint64_t *b
  */
 static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
                         const uint64_t *mem, const uint64_t *W, uint64_t HB, uint64_t kv,
-                        int b_max, int P, int k_max, const uint8_t *labels, uint64_t t_arrival,
+                        int b_max, int P, int k_max, const uint8_t *labels,
+                        const uint8_t *order, const uint16_t *sizes_in, uint64_t t_arrival,
                         uint64_t nd, uint64_t min_tps_milli, int policy, uint64_t np_tokens,
                         uint64_t *T_all, uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
                         uint64_t *w, uint64_t *phase);
@@ -937,8 +938,28 @@ int oracle_search_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
                         uint8_t *roles_out, uint8_t *slots_out, uint64_t *w, uint64_t *phase)
 {
     if (k_max > 16) return ORC_EINVAL;
-    return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, labels, t_arrival, nd,
-                        min_tps_milli, 0, 0, T_all, L_all, roles_out, slots_out, w, phase);
+    return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, labels, NULL, NULL,
+                        t_arrival, nd, min_tps_milli, 0, 0, T_all, L_all, roles_out, slots_out,
+                        w, phase);
+}
+
+/*
+ * The same search for two-chromosome genomes (App. A): replica q's chain is
+ * its run of the ordering (replica_range); a replica holding an id >= M has
+ * no DP result and no rates.  k_max <= 16.
+ */
+int oracle_search_roles_ordered(int M, int N, const uint64_t *t, const uint64_t *h,
+                                const uint64_t *tau, const uint64_t *mem, const uint64_t *W,
+                                uint64_t HB, uint64_t kv, int b_max, int P, int k_max,
+                                const uint8_t *order, const uint16_t *sizes, uint64_t t_arrival,
+                                uint64_t nd, uint64_t min_tps_milli, uint64_t *T_all,
+                                uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
+                                uint64_t *w, uint64_t *phase)
+{
+    if (k_max > 16) return ORC_EINVAL;
+    return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, NULL, order, sizes,
+                        t_arrival, nd, min_tps_milli, 0, 0, T_all, L_all, roles_out, slots_out,
+                        w, phase);
 }
 
 /*
@@ -958,14 +979,15 @@ int oracle_assign_roles_splitwise(int M, int N, const uint64_t *t, const uint64_
                                   uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
                                   uint64_t *w, uint64_t *phase)
 {
-    return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, labels, t_arrival, nd,
-                        min_tps_milli, 1, np_tokens, T_all, L_all, roles_out, slots_out, w,
-                        phase);
+    return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, labels, NULL, NULL,
+                        t_arrival, nd, min_tps_milli, 1, np_tokens, T_all, L_all, roles_out,
+                        slots_out, w, phase);
 }
 
 static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
                         const uint64_t *mem, const uint64_t *W, uint64_t HB, uint64_t kv,
-                        int b_max, int P, int k_max, const uint8_t *labels, uint64_t t_arrival,
+                        int b_max, int P, int k_max, const uint8_t *labels,
+                        const uint8_t *order, const uint16_t *sizes_in, uint64_t t_arrival,
                         uint64_t nd, uint64_t min_tps_milli, int policy, uint64_t np_tokens,
                         uint64_t *T_all, uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
                         uint64_t *w, uint64_t *phase)
@@ -984,9 +1006,21 @@ static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
         uint64_t rho_p[256], rho_d[256];
         int bstar[256], used[256], n_used = 0;
         for (int q = 0; q < k_max; q++) {
-            int m = 0;
-            for (int d = 0; d < M; d++)
-                if (labels[(size_t)p * M + d] == q) chain[m++] = d;
+            /* the cluster's chain: the devices labelled q in ascending id,
+             * or replica q's run of the ordering (an id >= M: infeasible) */
+            int m = 0, valid = 1;
+            if (labels) {
+                for (int d = 0; d < M; d++)
+                    if (labels[(size_t)p * M + d] == q) chain[m++] = d;
+            } else {
+                int lo, hi;
+                replica_range(M, k_max, sizes_in + (size_t)p * k_max, q, &lo, &hi);
+                for (int k = lo; k < hi; k++) {
+                    chain[m] = order[(size_t)p * M + k];
+                    if (chain[m] >= M) valid = 0;
+                    m++;
+                }
+            }
             uint64_t *To = T_all + ((size_t)p * k_max + q) * R;
             uint64_t *Lo = L_all + ((size_t)p * k_max + q) * R;
             for (int r = 0; r < R; r++) To[r] = Lo[r] = INF;
@@ -994,6 +1028,7 @@ static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
             bstar[q] = 0;
             if (m == 0) continue;
             used[n_used++] = q;
+            if (!valid) continue;
             for (int r = 0; r < R; r++) {
                 uint64_t slots = r == 0 ? 1 : (uint64_t)r;
                 for (int n = 0; n < N; n++) Wr[n] = W[n] + kv * slots;

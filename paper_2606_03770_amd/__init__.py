@@ -14,6 +14,7 @@ tensors on ROCm) and streams.  The wrappers keep the C names:
     e2_ga_step_ordered(ctx, order, sizes, roles, w, phase, ga)     genomes (App. A)
     e2_ctx_create_slots(problem, slot_model) -> Context   with decode slot counts
     e2_search_roles(ctx, labels, fitness)   role + slot search (Algorithm 2 inner loop)
+    e2_search_roles_ordered(ctx, order, sizes, fitness)   the same on two-chromosome genomes
     e2_search_roles(..., splitwise_np_tokens=NP)     the ablations of Sec. 4.2:
     e2_solve_partitions(..., objective="finish_time")  adapted-SplitWise roles,
     e2_eval_population(..., objective="finish_time")   finishing-time objective
@@ -47,7 +48,7 @@ EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitio
             "e2_search_roles", "e2_assign_roles_splitwise", "e2_solve_partitions_ft",
             "e2_eval_population_ft", "e2_solve_partitions_idle", "e2_eval_population_idle",
             "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror",
-            "e2_eval_population_noalloc")
+            "e2_eval_population_noalloc", "e2_search_roles_ordered")
 
 
 class E2Error(RuntimeError):
@@ -132,6 +133,10 @@ def lib() -> ctypes.CDLL:
     L.e2_search_roles.argtypes = [vp, vp, i32, i32, vp, ctypes.POINTER(e2_fitness_params), vp, vp,
                                   vp, vp, vp, vp]
     L.e2_search_roles.restype = ctypes.c_int
+    L.e2_search_roles_ordered.argtypes = [vp, vp, i32, i32, vp, vp,
+                                          ctypes.POINTER(e2_fitness_params), vp, vp, vp, vp, vp,
+                                          vp]
+    L.e2_search_roles_ordered.restype = ctypes.c_int
     L.e2_assign_roles_splitwise.argtypes = [vp, vp, i32, i32, vp,
                                             ctypes.POINTER(e2_fitness_params), ctypes.c_uint32,
                                             vp, vp, vp, vp, vp, vp]
@@ -453,6 +458,35 @@ def e2_search_roles(ctx: Context, labels, fitness: dict, k_max: int, stream=None
                                                _ptr(labels), ctypes.byref(fp),
                                                int(splitwise_np_tokens), *outs),
                "e2_assign_roles_splitwise")
+    return out
+
+
+def e2_search_roles_ordered(ctx: Context, order, sizes, fitness: dict, stream=None,
+                            with_tables: bool = False, out: Optional[dict] = None):
+    """Role and slot search for two-chromosome genomes (order uint8 [P][M],
+    sizes uint16 [P][k_max]).  Returns the same dict as e2_search_roles, per
+    replica slot."""
+    torch = _torch()
+    P, k_max = sizes.shape
+    _dev(order, torch.uint8, (P, ctx.n_dev), "order")
+    _dev(sizes, torch.uint16, (P, k_max), "sizes")
+    dev = order.device
+    R = ctx.b_max + 1
+    if out is None:
+        out = dict(roles=torch.empty((P, k_max), dtype=torch.uint8, device=dev),
+                   slots=torch.empty((P, k_max), dtype=torch.uint8, device=dev),
+                   w=torch.empty(P, dtype=torch.int64, device=dev),
+                   phase=torch.empty(P, dtype=torch.int64, device=dev))
+        if with_tables:
+            out["T_all"] = torch.empty((P, k_max, R), dtype=torch.int64, device=dev)
+            out["Lambda_all"] = torch.empty((P, k_max, R), dtype=torch.int64, device=dev)
+    fp = e2_fitness_params(int(fitness["t_arrival_ns"]), int(fitness["nd_tokens"]),
+                           int(fitness["min_tps_milli"]))
+    _check(lib().e2_search_roles_ordered(ctx.handle, _stream(stream), P, int(k_max), _ptr(order),
+                                         _ptr(sizes), ctypes.byref(fp), _ptr(out["roles"]),
+                                         _ptr(out["slots"]), _ptr(out["w"]), _ptr(out["phase"]),
+                                         _ptr(out.get("T_all")), _ptr(out.get("Lambda_all"))),
+           "e2_search_roles_ordered")
     return out
 
 

@@ -613,7 +613,7 @@ int eval_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genom
 
 // Every cluster for every role index, then the role assignment of policy
 // 0 (brute force) or 1 (adapted SplitWise).
-int roles_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_t *labels,
+int roles_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genomes &gen,
                const e2_fitness_params *fp, int policy, uint32_t np_tokens, uint8_t *roles_out,
                uint8_t *slots_out, uint64_t *w, uint64_t *phase, uint64_t *T_all,
                uint64_t *Lambda_all)
@@ -623,7 +623,8 @@ int roles_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_
     if (fp->nd_tokens > 8192) return E2_EINVAL;
     if ((T_all == nullptr) != (Lambda_all == nullptr)) return E2_EINVAL;
     if (P == 0) return E2_OK;
-    if (!labels || !roles_out || !slots_out || !w || !phase) return E2_EINVAL;
+    if (!(gen.labels || (gen.order && gen.sizes)) || !roles_out || !slots_out || !w || !phase)
+        return E2_EINVAL;
     int rc = check_device(ctx);
     if (rc) return rc;
     const int R = ctx->b_max + 1;
@@ -639,13 +640,12 @@ int roles_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_
     uint64_t *Ts = T_all ? T_all : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
     uint64_t *Ls = Lambda_all ? Lambda_all
                               : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb + tl);
-    const E2Genomes gen = {labels, nullptr, nullptr};
     hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, nullptr, wk, Ts, Ls,
                                         nullptr, nullptr);
     if (e != hipSuccess) return E2_EHIP;
     const uint64_t lam_max =
         fp->min_tps_milli ? 1000000000000ull / fp->min_tps_milli : E2_INF64;
-    e = e2_launch_roles(s, P, ctx->M, k_max, R, policy, np_tokens, labels, Ts, Ls,
+    e = e2_launch_roles(s, P, ctx->M, k_max, R, policy, np_tokens, gen.labels, Ts, Ls,
                         fp->t_arrival_ns, fp->nd_tokens, lam_max, roles_out, slots_out, w, phase);
     return e == hipSuccess ? E2_OK : E2_EHIP;
 }
@@ -740,7 +740,21 @@ int e2_search_roles(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const u
                     uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all)
 {
     if (k_max > E2_MAX_SEARCH_CLUSTERS) return E2_EINVAL;
-    return roles_impl(ctx, stream, P, k_max, labels, fp, 0, 0, roles_out, slots_out, w, phase,
+    if (P > 0 && !labels) return E2_EINVAL;
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    return roles_impl(ctx, stream, P, k_max, gen, fp, 0, 0, roles_out, slots_out, w, phase,
+                      T_all, Lambda_all);
+}
+
+int e2_search_roles_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
+                            const uint8_t *order, const uint16_t *sizes,
+                            const e2_fitness_params *fp, uint8_t *roles_out, uint8_t *slots_out,
+                            uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all)
+{
+    if (k_max > E2_MAX_SEARCH_CLUSTERS) return E2_EINVAL;
+    if (P > 0 && (!order || !sizes)) return E2_EINVAL;
+    const E2Genomes gen = {nullptr, order, sizes};
+    return roles_impl(ctx, stream, P, k_max, gen, fp, 0, 0, roles_out, slots_out, w, phase,
                       T_all, Lambda_all);
 }
 
@@ -749,7 +763,9 @@ int e2_assign_roles_splitwise(e2_ctx *ctx, void *stream, int32_t P, int32_t k_ma
                               uint32_t np_tokens, uint8_t *roles_out, uint8_t *slots_out,
                               uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all)
 {
-    return roles_impl(ctx, stream, P, k_max, labels, fp, 1, np_tokens, roles_out, slots_out, w,
+    if (P > 0 && !labels) return E2_EINVAL;
+    const E2Genomes gen = {labels, nullptr, nullptr};
+    return roles_impl(ctx, stream, P, k_max, gen, fp, 1, np_tokens, roles_out, slots_out, w,
                       phase, T_all, Lambda_all);
 }
 
