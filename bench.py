@@ -815,7 +815,7 @@ def algorithmic(t, steps):
                 t["alg1"] * OPS_PER_CANDIDATE_NARROW / t["dp_s"] / INT_VALU_PEAK}
 
 
-LIB_SOURCES = ("e2_api.hip", "e2_internal.h", "e2_kernels.hip")
+LIB_SOURCES = ("e2_internal.h", "e2_kernels.hip")  # the kernels and their launch configuration
 
 
 def code_text(text: str) -> str:
@@ -828,8 +828,9 @@ def code_text(text: str) -> str:
 
 
 def source_hash() -> str:
-    """Hash of the library sources that decide what the DP kernel does
-    (their code, comments and layout aside)."""
+    """Hash of the library sources that decide what the DP kernel does and
+    how it is launched (their code, comments and layout aside); the host
+    API's argument checks and allocations are not part of it."""
     import hashlib
     h = hashlib.sha256()
     for f in LIB_SOURCES:
