@@ -478,6 +478,17 @@ int e2_eval_population_idle(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
 int e2_ctx_dp_timing(e2_ctx *ctx, int32_t max_launches);
 int e2_ctx_dp_elapsed(e2_ctx *ctx, int32_t *launches, double *total_ms);
 
+/*
+ * Failure injection for tests of callers' error handling: the next `calls`
+ * library calls that reach a HIP runtime call (context creation, every
+ * solve / eval / search / GA call, the timing hook) return E2_EHIP at that
+ * point, after their argument checks and before anything is allocated or
+ * enqueued; 0 turns it off.  Process-wide.  Returns how many injected
+ * failures were still pending before this call (>= 0), or E2_EINVAL for
+ * calls < 0.
+ */
+int e2_debug_inject_hip_error(int32_t calls);
+
 /* Static string for an E2_* code ("unknown error" otherwise). */
 const char *e2_strerror(int code);
 

@@ -48,7 +48,8 @@ EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitio
             "e2_search_roles", "e2_assign_roles_splitwise", "e2_solve_partitions_ft",
             "e2_eval_population_ft", "e2_solve_partitions_idle", "e2_eval_population_idle",
             "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror",
-            "e2_eval_population_noalloc", "e2_search_roles_ordered")
+            "e2_eval_population_noalloc", "e2_search_roles_ordered",
+            "e2_debug_inject_hip_error")
 
 
 class E2Error(RuntimeError):
@@ -151,6 +152,8 @@ def lib() -> ctypes.CDLL:
     L.e2_eval_population_idle.argtypes = [vp, vp, i32, i32, vp, vp,
                                           ctypes.POINTER(e2_fitness_params), vp, vp, vp, vp]
     L.e2_eval_population_idle.restype = ctypes.c_int
+    L.e2_debug_inject_hip_error.argtypes = [i32]
+    L.e2_debug_inject_hip_error.restype = ctypes.c_int
     L.e2_ctx_dp_timing.argtypes = [vp, i32]
     L.e2_ctx_dp_timing.restype = ctypes.c_int
     L.e2_ctx_dp_elapsed.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
@@ -241,6 +244,16 @@ def e2_ctx_create_slots(problem: dict, slot_model: dict) -> Context:
 
 def e2_ctx_destroy(ctx: Context):
     ctx.close()
+
+
+def e2_debug_inject_hip_error(calls: int) -> int:
+    """The next `calls` library calls that reach a HIP runtime call fail with
+    E2_EHIP there (0: off).  Returns the injected failures still pending
+    before this call."""
+    rc = lib().e2_debug_inject_hip_error(int(calls))
+    if rc < 0:
+        raise E2Error(rc, "e2_debug_inject_hip_error")
+    return rc
 
 
 def e2_ctx_dp_timing(ctx: Context, max_launches: int):

@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -120,8 +121,21 @@ int scratch_on(int dev, void **out)
     return E2_OK;
 }
 
+// Failure injection (e2_debug_inject_hip_error): calls left that fail with
+// E2_EHIP where they would make their first HIP runtime call.
+std::atomic<int> g_inject{0};
+
+bool injected_failure()
+{
+    int n = g_inject.load();
+    while (n > 0)
+        if (g_inject.compare_exchange_weak(n, n - 1)) return true;
+    return false;
+}
+
 int check_device(const e2_ctx *ctx)
 {
+    if (injected_failure()) return E2_EHIP;
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess) return E2_EHIP;
     return cur == ctx->device ? E2_OK : E2_EINVAL;
@@ -405,6 +419,10 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
     for (const Part &pt : parts) total += align256(pt.bytes);
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
     if (!ctx) return E2_ENOMEM;
+    if (injected_failure()) {
+        free(ctx);
+        return E2_EHIP;
+    }
     if (hipGetDevice(&ctx->device) != hipSuccess) {
         free(ctx);
         return E2_EHIP;
@@ -476,6 +494,12 @@ const char *e2_strerror(int code)
     case E2_EHIP: return "HIP runtime error";
     default: return "unknown error";
     }
+}
+
+int e2_debug_inject_hip_error(int32_t calls)
+{
+    if (calls < 0) return E2_EINVAL;
+    return g_inject.exchange(calls);
 }
 
 int e2_quantise(const e2_problem *prob, uint64_t *t, uint64_t *h, uint64_t *tau)

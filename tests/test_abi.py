@@ -134,3 +134,24 @@ def test_slot_context_rejects_before_any_hip_call(sm, code):
     h = ctypes.c_void_p()
     assert e2.lib().e2_ctx_create_slots(ctypes.byref(s), ctypes.byref(m), ctypes.byref(h)) == code
     assert h.value is None
+
+
+def test_injected_hip_failure_comes_after_the_argument_checks():
+    """e2_debug_inject_hip_error: a call consumes an injected failure only
+    once its arguments pass, and then returns E2_EHIP before any HIP call."""
+    assert e2.e2_debug_inject_hip_error(0) >= 0
+    wl = workload.random_small(1, M=5, N=6, P=1, k_max=2)
+    good = wl.problem_arrays()
+    bad = dict(good, speed_flops=np.zeros(5, dtype=np.uint64))     # a device of speed 0
+    assert e2.e2_debug_inject_hip_error(2) == 0
+    with pytest.raises(e2.E2Error) as ei:
+        e2.e2_ctx_create(bad)
+    assert ei.value.code == e2.E2_EINVAL
+    assert e2.e2_debug_inject_hip_error(2) == 2                    # nothing consumed
+    with pytest.raises(e2.E2Error) as ei:
+        e2.e2_ctx_create(good)
+    assert ei.value.code == e2.E2_EHIP
+    assert e2.e2_debug_inject_hip_error(0) == 1                    # one consumed
+    with pytest.raises(e2.E2Error) as ei:
+        e2.e2_debug_inject_hip_error(-1)
+    assert ei.value.code == e2.E2_EINVAL

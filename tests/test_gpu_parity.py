@@ -356,3 +356,27 @@ def test_dp_timing_records_each_launch(torch_dev):
     assert e2.e2_ctx_dp_elapsed(ctx) == (0, 0.0)
     for k in want:
         assert (got[k] == want[k]).all() and (extra[k] == want[k]).all(), k
+
+
+def test_injected_hip_failure_enqueues_nothing(torch_dev):
+    """With a HIP failure injected, e2_eval_population returns E2_EHIP and
+    leaves its outputs as they were; the next call runs normally."""
+    torch, dev = torch_dev
+    wl = workload.make("c2_32dev_48L")
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    out = {k: torch.full((wl.population,), 12345, dtype=torch.int64, device=dev)
+           for k in ("w", "phase", "s_p", "s_d")}
+    assert e2.e2_debug_inject_hip_error(1) == 0
+    with pytest.raises(e2.E2Error) as ei:
+        e2.e2_eval_population(ctx, L, R, wl.fitness_params(), out=out)
+    assert ei.value.code == e2.E2_EHIP
+    torch.cuda.synchronize()
+    assert all((v == 12345).all().item() for v in out.values())
+    assert e2.e2_debug_inject_hip_error(0) == 0
+    e2.e2_eval_population(ctx, L, R, wl.fitness_params(), out=out)
+    torch.cuda.synchronize()
+    want = oracle.eval_population(wl)
+    for k in out:
+        assert np.array_equal(e2.u64(out[k]), want[k]), k
