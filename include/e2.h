@@ -49,7 +49,7 @@ extern "C" {
 #define E2_MAX_LAYER 255  /* N: transformer blocks of the model              */
 #define E2_MAX_CLUSTERS 255 /* k_max: cluster ids per genome                 */
 #define E2_MAX_SLOTS 15     /* b_max: decode slot counts of a slot model      */
-#define E2_MAX_SEARCH_CLUSTERS 16 /* k_max of e2_search_roles (2^16 role sets) */
+#define E2_MAX_SEARCH_FREE 24 /* clusters with a decode rate per searched genome */
 
 /*
  * Problem instance: the inputs of Algorithm 1 and Algorithm 2 (Sec. 3.2,
@@ -369,14 +369,20 @@ int e2_ga_step_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
  * and every prefill/decode assignment of the clusters is scored as
  * e2_eval_population scores summed rates (Eq. 3-5); the smallest (w,
  * phase) wins, ties going to the assignment whose decode set, as a bitmask
- * over cluster ids, is smallest.
+ * over cluster ids, is smallest.  A cluster with rho_D = 0 is prefill in
+ * that winner (w and phase never grow with the prefill sum), so only the F
+ * clusters with a decode rate are enumerated (2^F sets); a genome with F >
+ * E2_MAX_SEARCH_FREE is not searched (all roles 0, all slots 0xFF, w =
+ * phase = INF).
  *   labels[P][M]     device: cluster id per device (ids >= k_max unassigned)
- *   k_max            1..E2_MAX_SEARCH_CLUSTERS
+ *   k_max            1..E2_MAX_CLUSTERS
  *   roles_out[P][k_max]  device: 1 decode, 0 prefill or empty cluster
  *   slots_out[P][k_max]  device: b* of a decode cluster (0 if none
- *                    qualified), 0 otherwise
+ *                    qualified), 0 otherwise; 0xFF throughout for a genome
+ *                    that was not searched
  *   w, phase [P]     device: the winning fitness (INF if no assignment has
- *                    both a usable prefill and a usable decode cluster)
+ *                    both a usable prefill and a usable decode cluster, or
+ *                    if the genome was not searched)
  *   T_all, Lambda_all [P][k_max][b_max+1]  device, optional (both or
  *                    neither): every DP result, index 0 prefill, b decode
  *                    with b requests; INF for empty or infeasible
@@ -394,9 +400,11 @@ int e2_search_roles(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const u
  * e2_solve_partitions_ordered (an id >= M makes the replica infeasible, an
  * empty replica has no rates); then the same per-replica DPs for prefill and
  * each b = 1..b_max, the same kept slot count b*, rates and brute-force role
- * assignment, ties to the smallest decode bitmask over replica slots.
+ * assignment over the replicas with a decode rate (at most
+ * E2_MAX_SEARCH_FREE, else not searched), ties to the smallest decode
+ * bitmask over replica slots.
  *   order[P][M], sizes[P][k_max]  device, as e2_solve_partitions_ordered
- *   k_max            1..E2_MAX_SEARCH_CLUSTERS replica slots
+ *   k_max            1..E2_MAX_CLUSTERS replica slots
  *   outputs          as e2_search_roles, per replica slot
  * E2_EINVAL for sizes out of range (P below 2^20), nd_tokens > 8192 or a
  * NULL required pointer.

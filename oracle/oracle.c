@@ -921,7 +921,17 @@ int oracle_quantise_slots(int M, int N, const uint64_t *speed, const uint64_t *b
  * wins; ties go to the assignment whose decode set, as a bitmask over q, is
  * smallest.  roles_out[p][q] = 1 for decode, 0 for prefill and for empty
  * clusters; slots_out[p][q] = b* of a decode cluster (0 if none qualified),
- * 0 otherwise.  At most 16 clusters per genome (2^16 assignments).
+ * 0 otherwise.
+ *
+ * Only the F "free" clusters, those with rho_D > 0, are enumerated (2^F
+ * assignments); every other cluster is prefill.  This finds the same
+ * winner as enumerating all non-empty clusters: w and phase never grow when
+ * the prefill sum grows and the decode sum stays (S_P falls, so phase and
+ * the excess fall, and w = S_P + excess or 0), so turning a cluster with
+ * rho_D = 0 from decode to prefill gives a (w, phase) no larger and a
+ * smaller decode bitmask.  A genome with more than ORC_MAX_FREE free
+ * clusters is not searched: roles 0, every slots_out entry 0xFF and w =
+ * phase = INF.
  */
 static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
                         const uint64_t *mem, const uint64_t *W, uint64_t HB, uint64_t kv,
@@ -931,13 +941,15 @@ static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
                         uint64_t *T_all, uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
                         uint64_t *w, uint64_t *phase);
 
+/* free clusters (a decode rate) a genome may have for the role search */
+#define ORC_MAX_FREE 24
+
 int oracle_search_roles(int M, int N, const uint64_t *t, const uint64_t *h, const uint64_t *tau,
                         const uint64_t *mem, const uint64_t *W, uint64_t HB, uint64_t kv,
                         int b_max, int P, int k_max, const uint8_t *labels, uint64_t t_arrival,
                         uint64_t nd, uint64_t min_tps_milli, uint64_t *T_all, uint64_t *L_all,
                         uint8_t *roles_out, uint8_t *slots_out, uint64_t *w, uint64_t *phase)
 {
-    if (k_max > 16) return ORC_EINVAL;
     return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, labels, NULL, NULL,
                         t_arrival, nd, min_tps_milli, 0, 0, T_all, L_all, roles_out, slots_out,
                         w, phase);
@@ -946,7 +958,7 @@ int oracle_search_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
 /*
  * The same search for two-chromosome genomes (App. A): replica q's chain is
  * its run of the ordering (replica_range); a replica holding an id >= M has
- * no DP result and no rates.  k_max <= 16.
+ * no DP result and no rates.
  */
 int oracle_search_roles_ordered(int M, int N, const uint64_t *t, const uint64_t *h,
                                 const uint64_t *tau, const uint64_t *mem, const uint64_t *W,
@@ -956,7 +968,6 @@ int oracle_search_roles_ordered(int M, int N, const uint64_t *t, const uint64_t 
                                 uint64_t *L_all, uint8_t *roles_out, uint8_t *slots_out,
                                 uint64_t *w, uint64_t *phase)
 {
-    if (k_max > 16) return ORC_EINVAL;
     return assign_roles(M, N, t, h, tau, mem, W, HB, kv, b_max, P, k_max, NULL, order, sizes,
                         t_arrival, nd, min_tps_milli, 0, 0, T_all, L_all, roles_out, slots_out,
                         w, phase);
@@ -1088,36 +1099,47 @@ static int assign_roles(int M, int N, const uint64_t *t, const uint64_t *h, cons
             }
             continue;
         }
-        /* every role assignment of the used clusters, in increasing order of
-         * the decode set's bitmask over q */
+        /* the free clusters in increasing q; the rest stay prefill */
+        int fr[256], F = 0;
+        for (int i = 0; i < n_used; i++)
+            if (rho_d[used[i]] > 0) fr[F++] = used[i];
+        if (F > ORC_MAX_FREE) {
+            for (int q = 0; q < k_max; q++) {
+                roles_out[(size_t)p * k_max + q] = 0;
+                slots_out[(size_t)p * k_max + q] = 0xFF;
+            }
+            w[p] = phase[p] = INF;
+            continue;
+        }
+        /* every role assignment of the free clusters: bit i of x makes fr[i]
+         * decode; x increases with the decode bitmask over q, so the first
+         * best x is the smallest bitmask among ties */
         uint64_t best_w = INF, best_ph = INF;
-        unsigned best_mask = 0;
+        uint32_t best_x = 0;
         int have = 0;
-        for (unsigned x = 0; x < (1u << n_used); x++) {
-            unsigned mask = 0;
-            uint64_t sum_p = 0, sum_d = 0;
-            for (int i = 0; i < n_used; i++) {
-                int q = used[i];
-                if ((x >> i) & 1u) {
-                    mask |= 1u << q;
-                    sum_d += rho_d[q];
-                } else {
-                    sum_p += rho_p[q];
-                }
+        uint64_t fixed_p = 0;
+        for (int i = 0; i < n_used; i++)
+            if (rho_d[used[i]] == 0) fixed_p += rho_p[used[i]];
+        for (uint32_t x = 0; x < (1u << F); x++) {
+            uint64_t sum_p = fixed_p, sum_d = 0;
+            for (int j = 0; j < F; j++) {
+                if ((x >> j) & 1u) sum_d += rho_d[fr[j]];
+                else sum_p += rho_p[fr[j]];
             }
             uint64_t wv, pv, sp, sd;
             rates_fitness(sum_p, sum_d, t_arrival, nd, &wv, &pv, &sp, &sd);
             if (!have || wv < best_w || (wv == best_w && pv < best_ph)) {
                 best_w = wv;
                 best_ph = pv;
-                best_mask = mask;
+                best_x = x;
                 have = 1;
             }
         }
+        uint8_t dec[256] = {0};
+        for (int j = 0; j < F; j++) dec[fr[j]] = (best_x >> j) & 1u;
         for (int q = 0; q < k_max; q++) {
-            int dec = (best_mask >> q) & 1u;
-            roles_out[(size_t)p * k_max + q] = (uint8_t)dec;
-            slots_out[(size_t)p * k_max + q] = (uint8_t)(dec ? bstar[q] : 0);
+            roles_out[(size_t)p * k_max + q] = dec[q];
+            slots_out[(size_t)p * k_max + q] = (uint8_t)(dec[q] ? bstar[q] : 0);
         }
         w[p] = best_w;
         phase[p] = best_ph;

@@ -12,6 +12,8 @@
 #include "../../include/e2.h"
 #include "e2_internal.h"
 
+static_assert(e2_search_max_free == E2_MAX_SEARCH_FREE, "role search bound");
+
 namespace {
 
 typedef unsigned __int128 u128;
@@ -763,7 +765,6 @@ int e2_search_roles(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const u
                     const e2_fitness_params *fp, uint8_t *roles_out, uint8_t *slots_out,
                     uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all)
 {
-    if (k_max > E2_MAX_SEARCH_CLUSTERS) return E2_EINVAL;
     if (P > 0 && !labels) return E2_EINVAL;
     const E2Genomes gen = {labels, nullptr, nullptr};
     return roles_impl(ctx, stream, P, k_max, gen, fp, 0, 0, roles_out, slots_out, w, phase,
@@ -775,7 +776,6 @@ int e2_search_roles_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
                             const e2_fitness_params *fp, uint8_t *roles_out, uint8_t *slots_out,
                             uint64_t *w, uint64_t *phase, uint64_t *T_all, uint64_t *Lambda_all)
 {
-    if (k_max > E2_MAX_SEARCH_CLUSTERS) return E2_EINVAL;
     if (P > 0 && (!order || !sizes)) return E2_EINVAL;
     const E2Genomes gen = {nullptr, order, sizes};
     return roles_impl(ctx, stream, P, k_max, gen, fp, 0, 0, roles_out, slots_out, w, phase,

@@ -103,9 +103,14 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
                                 uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers,
                                 int objective = 0);
 
+// Clusters with a decode rate that a genome may have for the brute-force
+// role search (2^24 role sets); a genome with more is not searched.
+constexpr int e2_search_max_free = 24;
+
 // Role assignment per genome from T, Lambda [P][k_max][R]: policy 0 the
-// brute force (k_max <= 16), policy 1 the adapted-SplitWise rule (labels
-// give the non-empty clusters, np_tokens the prompt length).
+// brute force over the clusters with a decode rate, policy 1 the
+// adapted-SplitWise rule (labels give the non-empty clusters, np_tokens the
+// prompt length).
 hipError_t e2_launch_roles(hipStream_t s, int P, int M, int k_max, int R, int policy,
                            uint32_t np_tokens, const uint8_t *labels, const uint64_t *T_all,
                            const uint64_t *L_all, uint64_t t_arrival, uint64_t nd,

@@ -2192,16 +2192,22 @@ __global__ __launch_bounds__(256) void k_fitness(int P, int k_max, const uint64_
 // ---------------------------------------------------------------------------
 // Role and slot search (Algorithm 2's inner loop and its brute-force role
 // assignment, policy 0; the adapted-SplitWise rule, policy 1, below): one
-// wave per genome.  Lane q < k_max turns cluster q's DP
-// results into a prefill rate and, at the largest slot count b that is
+// workgroup of four waves per genome.  Thread q < k_max turns cluster q's
+// DP results into a prefill rate and, at the largest slot count b that is
 // feasible and meets the QoS floor, a decode rate b * SCALE / T_b.  A
-// cluster without a decode rate is prefill in every optimum (as decode it
-// adds nothing to the decode sum and takes its prefill rate away; ties go
-// to the smaller decode set), so the wave enumerates the role sets of the F
-// other clusters: lanes stride over the 2^F subsets in increasing order of
-// the decode bitmask, each keeps its smallest (w, phase, mask), and a wave
-// reduction picks the overall smallest.
+// cluster without a decode rate is prefill in every optimum: as decode it
+// adds nothing to the decode sum and takes its prefill rate away, which
+// never lowers w or phase (Eq. 3-5 fall as the prefill sum grows), and ties
+// go to the smaller decode set.  So the workgroup enumerates the role sets
+// of the F other ("free") clusters only: each thread fixes the low eight
+// bits of the set and runs the high bits in Gray-code order, keeps its
+// smallest (w, phase, set), and a reduction picks the overall smallest.  A
+// genome with more than kMaxFree free clusters is not searched.
 // ---------------------------------------------------------------------------
+constexpr int kRolesThreads = 256;
+constexpr int kRolesLowBits = 8;  // log2(kRolesThreads)
+constexpr int kMaxFree = e2_search_max_free;
+
 struct Best {
     uint64_t w, phase;
     uint32_t mask;
@@ -2214,21 +2220,37 @@ __device__ __forceinline__ bool best_less(const Best &a, const Best &b)
     return a.mask < b.mask;
 }
 
-__global__ __launch_bounds__(64) void k_roles(int P, int M, int k_max, int R, int policy,
-                                              uint32_t np_tokens, const uint8_t *__restrict__ labels,
-                                              const uint64_t *__restrict__ T_all,
-                                              const uint64_t *__restrict__ L_all,
-                                              uint64_t t_arrival, uint64_t nd, uint64_t lambda_max,
-                                              uint8_t *roles_out, uint8_t *slots_out, uint64_t *w,
-                                              uint64_t *phase)
+__device__ __forceinline__ Best wave_min_best(Best best)
+{
+    for (int off = kWave / 2; off >= 1; off >>= 1) {
+        Best o;
+        o.w = __shfl_xor(best.w, off, kWave);
+        o.phase = __shfl_xor(best.phase, off, kWave);
+        o.mask = __shfl_xor(best.mask, off, kWave);
+        if (best_less(o, best)) best = o;
+    }
+    return best;
+}
+
+__global__ __launch_bounds__(kRolesThreads) void k_roles(
+    int P, int M, int k_max, int R, int policy, uint32_t np_tokens,
+    const uint8_t *__restrict__ labels, const uint64_t *__restrict__ T_all,
+    const uint64_t *__restrict__ L_all, uint64_t t_arrival, uint64_t nd, uint64_t lambda_max,
+    uint8_t *roles_out, uint8_t *slots_out, uint64_t *w, uint64_t *phase)
 {
     __shared__ uint64_t rho_p[256], rho_d[256];
     __shared__ uint32_t bstar[256];
     __shared__ uint32_t used[8];
+    __shared__ uint64_t free_d[kMaxFree], free_p[kMaxFree];  // the free clusters' rates
+    __shared__ uint8_t free_q[kMaxFree];                       // and ids, increasing
+    __shared__ uint8_t dec[256];
+    __shared__ int n_free;
+    __shared__ uint64_t fixed_p;  // prefill rates of the clusters that are not free
+    __shared__ Best wave_best[kRolesThreads / kWave];
     const int p = blockIdx.x;
-    const int lane = threadIdx.x;
-    if (lane < 8) used[lane] = 0;
-    for (int q = lane; q < k_max; q += kWave) {
+    const int tid = threadIdx.x, lane = tid % kWave, wv = tid / kWave;
+    if (tid < 8) used[tid] = 0;
+    for (int q = tid; q < k_max; q += kRolesThreads) {
         const uint64_t *Tq = T_all + ((size_t)p * k_max + q) * R;
         const uint64_t *Lq = L_all + ((size_t)p * k_max + q) * R;
         const uint64_t t0 = Tq[0];
@@ -2245,16 +2267,18 @@ __global__ __launch_bounds__(64) void k_roles(int P, int M, int k_max, int R, in
         }
         rho_d[q] = rd;
         bstar[q] = bs;
+        dec[q] = 0;
     }
     __syncthreads();
     if (policy == 1) {
         // adapted SplitWise: the token ratio sets the prefill count, the
         // highest prefill rates (ties to the smaller cluster id) take it
-        for (int d = lane; d < M; d += kWave) {
+        for (int d = tid; d < M; d += kRolesThreads) {
             const int lab = labels[(size_t)p * M + d];
             if (lab < k_max) atomicOr(&used[lab >> 5], 1u << (lab & 31));
         }
         __syncthreads();
+        if (wv != 0) return;
         int n_used = 0;
         for (int i = 0; i < 8; ++i) n_used += __popc(used[i]);
         int n_p = n_used;
@@ -2266,19 +2290,19 @@ __global__ __launch_bounds__(64) void k_roles(int P, int M, int k_max, int R, in
         }
         uint64_t sp = 0, sd = 0;
         for (int q = lane; q < k_max; q += kWave) {
-            uint32_t dec = 0;
+            uint32_t role = 0;
             if ((used[q >> 5] >> (q & 31)) & 1u) {
                 int rank = 0;
                 for (int k = 0; k < k_max; ++k) {
                     if (!((used[k >> 5] >> (k & 31)) & 1u)) continue;
                     rank += rho_p[k] > rho_p[q] || (rho_p[k] == rho_p[q] && k < q);
                 }
-                dec = rank >= n_p;
-                if (dec) sd += rho_d[q];
+                role = rank >= n_p;
+                if (role) sd += rho_d[q];
                 else sp += rho_p[q];
             }
-            roles_out[(size_t)p * k_max + q] = (uint8_t)dec;
-            slots_out[(size_t)p * k_max + q] = (uint8_t)(dec ? bstar[q] : 0);
+            roles_out[(size_t)p * k_max + q] = (uint8_t)role;
+            slots_out[(size_t)p * k_max + q] = (uint8_t)(role ? bstar[q] : 0);
         }
         sp = wave_sum_u64(sp);
         sd = wave_sum_u64(sd);
@@ -2289,90 +2313,97 @@ __global__ __launch_bounds__(64) void k_roles(int P, int M, int k_max, int R, in
         }
         return;
     }
-    // brute force (k_max <= 16): free clusters (a decode rate), in
-    // increasing q; the others are prefill
-    uint32_t fmask = 0;
-    uint64_t fixed_p = 0;
-    for (int q = 0; q < k_max; ++q) {
-        if (rho_d[q]) fmask |= 1u << q;
-        else fixed_p += rho_p[q];
-    }
-    const int F = __popc(fmask);
-    // A role set is x in [0, 2^F): bit i makes the i-th free cluster (in
-    // increasing q) decode.  Lane i holds that cluster's decode and prefill
-    // rates; each lane fixes the low six bits of x (its lane id) and the high
-    // bits run in Gray-code order, so each step adds or removes one cluster's
-    // rates.  The best set is kept as x: depositing x onto the free clusters
-    // preserves order, so (w, phase, x) orders sets exactly as (w, phase,
-    // mask) does, whatever order they are visited in.
-    uint64_t dq = 0, pq = 0;
-    {
-        uint32_t rest = fmask;
-        for (int i = 0; i < F; ++i) {
-            const int q = __ffs(rest) - 1;
-            rest &= rest - 1;
-            if (lane == i) {
-                dq = rho_d[q];
-                pq = rho_p[q];
+    // brute force over the free clusters (a decode rate), listed in
+    // increasing q by wave 0; the others are prefill
+    if (wv == 0) {
+        int F = 0;
+        uint64_t fixed = 0;
+        for (int base = 0; base < k_max; base += kWave) {
+            const int q = base + lane;
+            const bool in = q < k_max;
+            const bool is_free = in && rho_d[q] != 0;
+            const uint64_t bal = __ballot(is_free);
+            if (is_free) {
+                const int pos = F + (int)__popcll(bal & ((1ull << lane) - 1));
+                if (pos < kMaxFree) {
+                    free_q[pos] = (uint8_t)q;
+                    free_d[pos] = rho_d[q];
+                    free_p[pos] = rho_p[q];
+                }
+            } else if (in) {
+                fixed += rho_p[q];
             }
+            F += (int)__popcll(bal);
+        }
+        fixed = wave_sum_u64(fixed);
+        if (lane == 0) {
+            n_free = F;
+            fixed_p = fixed;
         }
     }
-    const uint64_t p_all = fixed_p + wave_sum_u64(pq);  // every cluster prefill
-    const int lowF = F < 6 ? F : 6;
-    uint64_t sd = 0, sxp = 0;  // decode rates and prefill rates of x's members
-    for (int i = 0; i < lowF; ++i) {
-        const uint64_t d = readlane_u64(dq, i), pp = readlane_u64(pq, i);
-        if ((lane >> i) & 1) {
-            sd += d;
-            sxp += pp;
+    __syncthreads();
+    const int F = n_free;
+    if (F > kMaxFree) {  // not searched
+        for (int q = tid; q < k_max; q += kRolesThreads) {
+            roles_out[(size_t)p * k_max + q] = 0;
+            slots_out[(size_t)p * k_max + q] = 0xFF;
         }
+        if (tid == 0) w[p] = phase[p] = E2_INF64;
+        return;
     }
-    const bool active = (uint32_t)lane < (1u << lowF);
+    // A role set is x in [0, 2^F): bit i makes free cluster i decode.  x
+    // orders sets as their decode bitmasks over q do (the free clusters are
+    // listed in increasing q), so (w, phase, x) picks the same set as (w,
+    // phase, mask), whatever order the sets are visited in.  Thread tid
+    // holds the low bits of x; each Gray-code step of the high bits adds or
+    // removes one cluster's rates.
+    uint64_t p_all = fixed_p;  // every cluster prefill
+    for (int i = 0; i < F; ++i) p_all += free_p[i];
+    const int low = F < kRolesLowBits ? F : kRolesLowBits;
     Best best = {E2_INF64, E2_INF64, 0xFFFFFFFFu};
-    uint32_t g = 0;  // high bits of x
-    for (uint32_t t = 0; t < (1u << (F - lowF)); ++t) {
-        if (t) {
-            const int bt = __builtin_ctz(t);
-            const uint64_t d = readlane_u64(dq, bt + 6), pp = readlane_u64(pq, bt + 6);
-            g ^= 1u << bt;
-            if ((g >> bt) & 1u) {
-                sd += d;
-                sxp += pp;
-            } else {
-                sd -= d;
-                sxp -= pp;
+    if ((uint32_t)tid < (1u << low)) {
+        uint64_t sd = 0, sxp = 0;  // decode and prefill rates of x's members
+        for (int i = 0; i < low; ++i) {
+            if ((tid >> i) & 1) {
+                sd += free_d[i];
+                sxp += free_p[i];
             }
         }
-        if (active) {
+        uint32_t g = 0;  // high bits of x
+        const uint32_t n_high = 1u << (F - low);
+        for (uint32_t t = 0; t < n_high; ++t) {
+            if (t) {
+                const int bt = __builtin_ctz(t);
+                const uint64_t d = free_d[bt + kRolesLowBits], pp = free_p[bt + kRolesLowBits];
+                g ^= 1u << bt;
+                if ((g >> bt) & 1u) {
+                    sd += d;
+                    sxp += pp;
+                } else {
+                    sd -= d;
+                    sxp -= pp;
+                }
+            }
             const Fit f = fitness_of_rates(p_all - sxp, sd, t_arrival, nd);
-            const Best c = {f.w, f.phase, (uint32_t)lane | (g << 6)};
+            const Best c = {f.w, f.phase, (uint32_t)tid | (g << kRolesLowBits)};
             if (best_less(c, best)) best = c;
         }
     }
-    for (int off = kWave / 2; off >= 1; off >>= 1) {
-        Best o;
-        o.w = __shfl_xor(best.w, off, kWave);
-        o.phase = __shfl_xor(best.phase, off, kWave);
-        o.mask = __shfl_xor(best.mask, off, kWave);
-        if (best_less(o, best)) best = o;
-    }
-    {  // deposit the best x onto the free clusters
-        uint32_t mask = 0, rest = fmask;
-        for (int i = 0; i < F; ++i) {
-            const int q = __ffs(rest) - 1;
-            rest &= rest - 1;
-            if ((best.mask >> i) & 1u) mask |= 1u << q;
-        }
-        best.mask = mask;
-    }
-    if (lane < k_max) {
-        const uint32_t dec = (best.mask >> lane) & 1u;
-        roles_out[(size_t)p * k_max + lane] = (uint8_t)dec;
-        slots_out[(size_t)p * k_max + lane] = (uint8_t)(dec ? bstar[lane] : 0);
-    }
-    if (lane == 0) {
+    best = wave_min_best(best);
+    if (lane == 0) wave_best[wv] = best;
+    __syncthreads();
+    if (tid == 0) {
+        for (int i = 1; i < kRolesThreads / kWave; ++i)
+            if (best_less(wave_best[i], best)) best = wave_best[i];
+        for (int i = 0; i < F; ++i)
+            if ((best.mask >> i) & 1u) dec[free_q[i]] = 1;
         w[p] = best.w;
         phase[p] = best.phase;
+    }
+    __syncthreads();
+    for (int q = tid; q < k_max; q += kRolesThreads) {
+        roles_out[(size_t)p * k_max + q] = dec[q];
+        slots_out[(size_t)p * k_max + q] = (uint8_t)(dec[q] ? bstar[q] : 0);
     }
 }
 
@@ -2799,7 +2830,7 @@ hipError_t e2_launch_roles(hipStream_t s, int P, int M, int k_max, int R, int po
                            uint64_t lambda_max, uint8_t *roles_out, uint8_t *slots_out,
                            uint64_t *w, uint64_t *phase)
 {
-    k_roles<<<P, 64, 0, s>>>(P, M, k_max, R, policy, np_tokens, labels, T_all, L_all, t_arrival,
+    k_roles<<<P, kRolesThreads, 0, s>>>(P, M, k_max, R, policy, np_tokens, labels, T_all, L_all, t_arrival,
                              nd, lambda_max, roles_out, slots_out, w, phase);
     return hipGetLastError();
 }

@@ -98,8 +98,51 @@ def test_search_maximum_sizes(torch_dev):
     _assert_equal(_gpu_search(torch_dev, wl, sm), want, tag="max")
 
 
+def test_search_past_sixteen_clusters(torch_dev):
+    """k_max from 17 to 255: only clusters with a decode rate are
+    enumerated, up to 24 of them per genome (2^24 role sets); genomes with
+    more are not searched (slots 0xFF, w = phase = INF), on both sides."""
+    rng = np.random.default_rng(1717)
+    free_seen = []
+    for it, K in enumerate((17, 20, 24, 31, 48, 64, 100, 255)):
+        M = int(min(256, max(K, int(rng.integers(K // 2, 2 * K)))))
+        N = int(rng.integers(4, 20))
+        wl = workload.random_small(8100 + it, M=M, N=N, P=4, k_max=K,
+                                   mem_lo_layers=float(N * rng.uniform(0.1, 0.5)),
+                                   mem_hi_layers=float(N * rng.uniform(0.7, 1.5)),
+                                   zero_bw_frac=0.05)
+        if it % 3:
+            wl.min_tps_milli = 0
+        sm = dict(b_max=int(rng.choice([1, 3, 8])), beta_ppm=125_000,
+                  kv_bytes_per_block_slot=int(rng.choice([0, 10**6])))
+        print(f"search k_max={K}: M={M} N={N} {sm}", flush=True)
+        want = oracle.search_roles(wl, sm)
+        lam = 10**12 // wl.min_tps_milli if wl.min_tps_milli else INF
+        F = ((want["T_all"][:, :, 1:] != INF) & (want["Lambda_all"][:, :, 1:] <= lam)).any(axis=2)
+        free_seen += F.sum(axis=1).tolist()
+        _assert_equal(_gpu_search(torch_dev, wl, sm), want, tag=f"k_max {K}")
+    assert max(free_seen) > 24 and any(17 <= f <= 24 for f in free_seen), free_seen
+
+
+def test_search_free_cluster_bound(torch_dev):
+    """25 single-device clusters that each hold the model: with one device
+    moved to another cluster (24 free clusters) the genome is searched over
+    2^24 role sets; with all 25 it is not."""
+    M = 25
+    wl = workload.random_small(501, M=M, N=M, P=2, k_max=M, mem_lo_layers=60,
+                               mem_hi_layers=80, head=False)
+    wl.min_tps_milli = 0
+    sm = dict(b_max=2, beta_ppm=125_000, kv_bytes_per_block_slot=0)
+    labels = np.tile(np.arange(M, dtype=np.uint8), (2, 1))
+    labels[0, 7] = 3
+    want = oracle.search_roles(wl, sm, labels=labels)
+    assert want["w"][0] != INF and want["w"][1] == INF and (want["slots"][1] == 0xFF).all()
+    _assert_equal(_gpu_search(torch_dev, wl, sm, labels=labels), want, tag="bound")
+
+
 @pytest.mark.parametrize("name,rows", [("c1_tiny_12dev_32L", None), ("c2_32dev_48L", None),
-                                       ("c3_64dev_80L", 192)])
+                                       ("c3_64dev_80L", 192), ("c4_128dev_80L", 128),
+                                       ("c5_256dev_126L_ga", 64)])
 def test_search_named_workloads(torch_dev, name, rows):
     print(f"search workload {name}", flush=True)
     wl = workload.make(name)
@@ -153,7 +196,7 @@ def test_search_empty_population_and_bad_arguments(torch_dev):
     assert out["w"].numel() == 0
     L = torch.zeros((1, 5), dtype=torch.uint8, device=dev)
     with pytest.raises(e2.E2Error):
-        e2.e2_search_roles(ctx, L, wl.fitness_params(), 17)        # more than 16 clusters
+        e2.e2_search_roles(ctx, L, wl.fitness_params(), 256)       # k_max past 255
     T = torch.empty((1, 2, 3), dtype=torch.int64, device=dev)
     fp = e2.e2_fitness_params(1, 1, 0)
     r = torch.empty((1, 2), dtype=torch.uint8, device=dev)

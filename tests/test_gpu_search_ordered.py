@@ -90,8 +90,27 @@ def test_search_ordered_random_parity(torch_dev):
                       oracle.search_roles_ordered(wl, sm, order, sizes), tag=f"it {it}")
 
 
+def test_search_ordered_many_replica_slots(torch_dev):
+    """17 to 96 replica slots: the search runs over the replicas with a
+    decode rate only (at most 24; genomes with more are not searched)."""
+    rng = np.random.default_rng(96)
+    for it, K in enumerate((17, 24, 40, 96)):
+        M = int(rng.integers(K, min(256, 2 * K) + 1))
+        N = int(rng.integers(4, 16))
+        wl = workload.random_small(9100 + it, M=M, N=N, P=4, k_max=K, mem_lo_layers=1,
+                                   mem_hi_layers=float(2 * N))
+        wl.min_tps_milli = 0
+        sm = dict(b_max=4, beta_ppm=125_000, kv_bytes_per_block_slot=10**6)
+        order, sizes = _random_genomes(rng, 4, M, K)
+        print(f"ordered search k_max={K}: M={M} N={N}", flush=True)
+        ctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
+        _assert_equal(_gpu(torch_dev, ctx, wl, order, sizes),
+                      oracle.search_roles_ordered(wl, sm, order, sizes), tag=f"K {K}")
+
+
 @pytest.mark.parametrize("name,rows", [("c1_tiny_12dev_32L", None), ("c2_32dev_48L", None),
-                                       ("c3_64dev_80L", 160)])
+                                       ("c3_64dev_80L", 160), ("c4_128dev_80L", 128),
+                                       ("c5_256dev_126L_ga", 64)])
 def test_search_ordered_named_workloads(torch_dev, name, rows):
     print(f"ordered search workload {name}", flush=True)
     wl = workload.make(name)
@@ -147,8 +166,8 @@ def test_search_ordered_arguments(torch_dev):
     wl = workload.random_small(3, M=6, N=8, P=2, k_max=17)
     ctx = e2.e2_ctx_create(wl.problem_arrays())
     order = torch.zeros((2, 6), dtype=torch.uint8, device=dev)
-    sizes = torch.zeros((2, 17), dtype=torch.uint16, device=dev)
-    with pytest.raises(e2.E2Error) as ei:                  # 2^17 role sets: refused
+    sizes = torch.zeros((2, 256), dtype=torch.uint16, device=dev)
+    with pytest.raises(e2.E2Error) as ei:                  # 256 replica slots: refused
         e2.e2_search_roles_ordered(ctx, order, sizes, wl.fitness_params())
     assert ei.value.code == e2.E2_EINVAL
     out = e2.e2_search_roles_ordered(ctx, order[:0], sizes[:0, :4], wl.fitness_params())

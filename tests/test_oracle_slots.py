@@ -183,3 +183,66 @@ def test_empty_clusters_are_left_out(orc):
                 assert got["roles"][p, q] == 0 and got["slots"][p, q] == 0
     # one cluster cannot cover both roles
     assert got["w"][1] == INF and got["phase"][1] == INF
+
+
+def _every_role_vector_optimum(wl, got, p):
+    """b_max = 1: the smallest (w, phase, decode bitmask) over every role
+    vector of genome p's non-empty clusters, each scored by the pinned
+    fixed-role fitness on the search's own prefill (index 0) and one-slot
+    decode (index 1) DP results."""
+    K = wl.k_max
+    used = sorted({int(x) for x in wl.labels[p] if x < K})
+    n = len(used)
+    bits = ((np.arange(1 << n)[:, None] >> np.arange(n)[None, :]) & 1).astype(np.uint8)
+    roles = np.zeros((1 << n, K), np.uint8)
+    roles[:, used] = bits
+    T = np.where(roles == 1, got["T_all"][p, :, 1], got["T_all"][p, :, 0])
+    L = np.where(roles == 1, got["Lambda_all"][p, :, 1], got["Lambda_all"][p, :, 0])
+    f = oracle.fitness(T, L, roles, **wl.fitness_params())
+    mask = (roles.astype(np.int64) << np.arange(K, dtype=np.int64)[None, :]).sum(axis=1)
+    i = np.lexsort((mask, f["phase"], f["w"]))[0]
+    return int(f["w"][i]), int(f["phase"][i]), int(mask[i])
+
+
+@pytest.mark.parametrize("K", [17, 18])
+def test_search_past_sixteen_clusters_equals_every_role_vector(orc, K):
+    """More than 16 non-empty clusters, some with a prefill rate but no
+    decode rate (a QoS floor set at the median decode Lambda): the search,
+    which enumerates only clusters with a decode rate, finds the optimum of
+    all 2^K role vectors."""
+    wl = workload.random_small(900 + K, M=3 * K, N=10, P=2, k_max=K, mem_lo_layers=3,
+                               mem_hi_layers=14, zero_bw_frac=0.05)
+    rng = np.random.default_rng(K)
+    wl.labels = np.stack([rng.permutation(np.concatenate([np.arange(K), rng.integers(0, K, 2 * K)]))
+                          for _ in range(2)]).astype(np.uint8)     # every cluster non-empty
+    sm = dict(b_max=1, beta_ppm=0, kv_bytes_per_block_slot=0)
+    wl.min_tps_milli = 0
+    L1 = orc.search_roles(wl, sm)["Lambda_all"][:, :, 1]
+    wl.min_tps_milli = max(1, 10**12 // int(np.median(L1[L1 != INF])))
+    got = orc.search_roles(wl, sm)
+    lam_max = 10**12 // wl.min_tps_milli
+    prefill_only = (got["T_all"][:, :, 0] != INF) & (got["Lambda_all"][:, :, 1] > lam_max)
+    assert prefill_only.sum() >= 2
+    for p in range(wl.population):
+        assert len({int(x) for x in wl.labels[p]}) == K
+        mask = sum(1 << q for q in range(K) if got["roles"][p, q])
+        assert (int(got["w"][p]), int(got["phase"][p]), mask) == \
+            _every_role_vector_optimum(wl, got, p), p
+
+
+def test_search_with_more_than_24_free_clusters_is_not_searched(orc):
+    """Single-device clusters on devices that each hold the model, no QoS
+    floor: every cluster has a decode rate.  24 of them are searched (2^24
+    role sets); 25 are not: roles 0, slots 0xFF, w = phase = INF."""
+    M = N_ = 25
+    wl = workload.random_small(501, M=M, N=N_, P=2, k_max=M, mem_lo_layers=60,
+                               mem_hi_layers=80, head=False)
+    wl.min_tps_milli = 0
+    sm = dict(b_max=2, beta_ppm=125_000, kv_bytes_per_block_slot=0)
+    labels = np.tile(np.arange(M, dtype=np.uint8), (2, 1))
+    labels[0, 7] = 3                                   # 24 clusters
+    got = orc.search_roles(wl, sm, labels=labels)
+    assert (got["T_all"][:, :, 1:] != INF).all(axis=2).sum(axis=1).tolist() == [24, 25]
+    assert got["w"][0] != INF and got["roles"][0].sum() >= 1 and (got["slots"][0] <= 2).all()
+    assert got["w"][1] == INF and got["phase"][1] == INF
+    assert (got["roles"][1] == 0).all() and (got["slots"][1] == 0xFF).all()
