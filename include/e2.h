@@ -228,13 +228,15 @@ int e2_eval_population(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
  * harnesses that forbid hipMalloc.  Same arguments, layouts and results as
  * e2_eval_population.  Instead of a stream-ordered allocation, the call's
  * working memory (counters, the problem list, per-cluster T and Lambda, the
- * DP waves' row regions) is carved from one fixed 96 MiB device array that
- * the library holds on each GPU it runs on until the process ends.
- *   Limit: P * k_max * 32 bytes plus one DP wave's rows (2 * 8 * (the
- *   largest band total, 3969 cells at N = 126) + N * N bytes) must fit in
+ * DP waves' split-point tables when chains can outgrow their LDS copy) is
+ * carved from one fixed 96 MiB device array that the library holds on each
+ * GPU it runs on until the process ends.
+ *   Limit: P * k_max * 32 bytes plus, when min(M, N) - 1 rows of N split
+ *   points exceed 2048 bytes, one DP wave's N * N-byte table must fit in
  *   96 MiB (P * k_max up to about 3.1 million at N = 126); larger inputs
- *   return E2_EINVAL before anything is enqueued.  Large populations run
- *   with fewer DP waves than e2_eval_population (same results, slower).
+ *   return E2_EINVAL before anything is enqueued.  When the tables of all
+ *   of e2_eval_population's DP waves do not fit, fewer waves run (same
+ *   results, slower).
  *   Every call on one GPU shares that GPU's array and leaves its contents
  *   behind: calls that overlap on one GPU (several streams or threads) race
  *   and must be serialised by the caller.  The counters are cleared by a

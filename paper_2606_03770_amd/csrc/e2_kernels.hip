@@ -465,11 +465,10 @@ struct Row {
 template <typename K>
 struct RowOut {
     lds_t<K> *vals;     // band-packed values, may be null in combine mode
-    K *vals_g;          // second copy of the values (global), or null
     uint8_t *tbs;       // split points, or null
     bool combine;
     bool last_only;
-    const K *G;
+    const lds_t<K> *G;
     int glo, ghi;
     K tau_next;
     int mu;
@@ -706,7 +705,6 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
         const K v = act ? unpack_val(best) : KeyT<K>::inf;
         if (!ro.combine) {
             ro.vals[i - rw.lo] = v;
-            if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
             if (ro.tbs) ro.tbs[i - rw.lo] = (uint8_t)key_low8(best);
         } else {
             acc = kmin(acc, combine_key(v, b, ro.mu));
@@ -728,7 +726,6 @@ __device__ __forceinline__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<
             const K v = inf_unless((K)(rw.pr[i + 1] + rw.hadd), rw.wr[i] == 0);
             if (!ro.combine) {
                 ro.vals[i - rw.lo] = v;
-                if (ro.vals_g) ro.vals_g[i - rw.lo] = v;
             } else {
                 acc = kmin(acc, combine_key(v, combine_b(i, N, ro), ro.mu));
             }
@@ -748,11 +745,10 @@ __device__ __forceinline__ K row_pass(const Row<K> &rw, const RowOut<K> &ro, PS<
 }
 
 template <typename K>
-__device__ __forceinline__ RowOut<K> store_to(lds_t<K> *vals, K *vals_g, uint8_t *tbs)
+__device__ __forceinline__ RowOut<K> store_to(lds_t<K> *vals, uint8_t *tbs)
 {
     RowOut<K> ro;
     ro.vals = vals;
-    ro.vals_g = vals_g;
     ro.tbs = tbs;
     ro.combine = false;
     ro.last_only = false;
@@ -806,6 +802,17 @@ constexpr int kMaxBandedChain = kWave;
 // chains with roomy devices, or the reference path's full rows) go to the
 // wave's region of the global split-point table
 constexpr int kLdsTbCells = 2048;
+// Dynamic LDS of k_dp: split-point pairs (16 N bytes), a row buffer, the
+// backward-row pool's fixed part (a row) and the extra bytes below, a second
+// row buffer and the split-point bytes.  The extra bytes lengthen the pool up
+// to 6656 bytes in all; at 7424 the kernel measured a quarter slower (fewer
+// resident waves).
+constexpr int kDpLdsTarget = 6656;
+__host__ __device__ constexpr int dp_lds_fixed(int N) { return 16 * N + 16 * (N + 1) + kLdsTbCells; }
+__host__ __device__ constexpr int dp_lds_extra(int N)
+{
+    return dp_lds_fixed(N) < kDpLdsTarget ? ((kDpLdsTarget - dp_lds_fixed(N)) & ~7) : 0;
+}
 
 // Per-position table of a chain: lane k-1 holds chain position k (1-based)
 // as five packed words (fields < 256 except the pool offsets) and two u64
@@ -871,8 +878,9 @@ struct DpSmem {
     lds_t<uint64_t> *Rw0;  // LDS row ping-pong, N+1 entries each
     lds_t<uint64_t> *Rw1;
     uint8_t *tbp;    // split points of the forward rows, band-packed (LDS)
-    uint64_t *pool;  // band-packed forward row values (global, per wave)
-    uint64_t *gpool; // band-packed backward row values (global, per wave)
+    lds_t<char> *pool_end; // end of the backward-row pool (k_dp)
+    uint64_t *pool;  // band-packed forward row values (global, per wave; k_dp_ft)
+    uint64_t *gpool; // band-packed backward row values (global, per wave; k_dp_ft)
     int pool_cells;
 };
 
@@ -1002,67 +1010,105 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
     return pool_need <= sm.pool_cells && gpool_need <= sm.pool_cells;
 }
 
+// First backward row of the longest run of rows ending at row t_end that
+// fits a backward-row pool of cap cells (rows band-packed in order).  Lane
+// t-1 holds the pool offset of row t, so the cells of rows t..t_end are
+// end(t_end) - offset(t), which falls as t grows.
+__device__ __forceinline__ int g_window_lo(const ChainRegs &cr, int lane, int t_end, int cap)
+{
+    const int end = gpool_off(cr, t_end) + (rband_hi(cr, t_end) - rband_lo(cr, t_end) + 1);
+    const bool fits = lane + 1 <= t_end && end - (int)cr.we <= cap;
+    const uint64_t b = __ballot(fits);
+    return b ? __builtin_ctzll(b) + 1 : t_end;
+}
+
+// Backward rows 1..t_end into the backward-row pool: rows from t_lo on at
+// their band-packed offsets less that of t_lo, the rows before t_lo in place
+// at the pool's start (a row reads its previous row completely before it
+// writes: every row pass has a barrier between the two).
+template <typename K>
+__device__ __forceinline__ void g_rows(const E2Tables &tb, const ChainRegs &cr, int r, int t_end,
+                                       int t_lo, lds_t<K> *gp, PS<K> *ps, int lane, int N)
+{
+    const int base = gpool_off(cr, t_lo);
+    for (int t = 1; t <= t_end; ++t) {
+        Row<K> g = rev_row_of<K>(tb, cr, r, t);
+        if (t >= 2)
+            set_prev(g, gp + (t - 1 >= t_lo ? gpool_off(cr, t - 1) - base : 0),
+                     rband_lo(cr, t - 1), rband_hi(cr, t - 1));
+        row_pass(g, store_to<K>(gp + (t >= t_lo ? gpool_off(cr, t) - base : 0), nullptr), ps,
+                 lane, N);
+    }
+}
+
 // The banded DP of one chain with keys of width K.  Returns the optimum as
 // a u64 (INF if none) and its master position in *mu_out (0 if none); the
 // stage starts go to start[].
+//
+// Every row lives in LDS.  Forward rows are computed in place in one row
+// buffer.  Backward rows go to a pool (the LDS after the split-point pairs
+// of this key width); the sweep reads them back in the reverse order, so
+// the pool keeps the last rows that fit, and a combine whose backward row
+// was not kept computes rows 1.. again, keeping the run that ends at the
+// row it needs.  When the sweep runs through every master and the chosen
+// one's previous forward row is no longer in the buffer, the forward rows
+// up to it are computed again.
 template <typename K>
 __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs &cr, int r, int m,
                           int lane, uint64_t *T_out, int *mu_out, uint8_t *start, uint8_t *last_tb)
 {
     const int N = tb.N, M = tb.M;
     PS<K> *ps = static_cast<PS<K> *>(sm.ps);
-    K *pool = reinterpret_cast<K *>(sm.pool);
-    K *gpool = reinterpret_cast<K *>(sm.gpool);
-    lds_t<K> *Rw[2] = {reinterpret_cast<lds_t<K> *>(sm.Rw0), reinterpret_cast<lds_t<K> *>(sm.Rw1)};
-    // ---- backward rows G_1..G_{m-1}: LDS ping-pong + the backward-row pool
-    for (int t = 1; t < m; ++t) {
-        Row<K> g = rev_row_of<K>(tb, cr, r, t);
-        if (t >= 2)
-            set_prev(g, Rw[(t - 1) & 1], rband_lo(cr, t - 1), rband_hi(cr, t - 1));
-        row_pass(g, store_to<K>(Rw[t & 1], gpool + gpool_off(cr, t), nullptr), ps, lane, N);
-    }
+    lds_t<K> *F = reinterpret_cast<lds_t<K> *>(sm.Rw0);  // forward rows, in place
+    lds_t<char> *pool_c = (lds_t<char> *)sm.ps + (uint32_t)N * sizeof(PS<K>);
+    lds_t<K> *gp = (lds_t<K> *)pool_c;
+    const int gcap = (int)((sm.pool_end - pool_c) / (int)sizeof(K));
+    // ---- backward rows G_1..G_{m-1}, the last ones that fit kept in the pool
+    int g_lo = m >= 2 ? g_window_lo(cr, lane, m - 1, gcap) : 1;  // first kept row
+    if (m >= 2) g_rows<K>(tb, cr, r, m - 1, g_lo, gp, ps, lane, N);
     // ---- the optimum without a master (no head time or bytes anywhere):
     // reversed row m at its last cell.  Every master's optimum is at least
     // this, and none exists when it is infinite.
     K tn = KeyT<K>::inf;
     if (m >= 2) {
         Row<K> g = rev_row_of<K>(tb, cr, r, m);
-        set_prev(g, Rw[(m - 1) & 1], rband_lo(cr, m - 1), rband_hi(cr, m - 1));
+        set_prev(g, gp + (gpool_off(cr, m - 1) - gpool_off(cr, g_lo)), rband_lo(cr, m - 1),
+                 rband_hi(cr, m - 1));
         g.lo = g.hi = N - 1;
         g.lmin = uni(tb.minwinR[(size_t)f8(lane_w(cr.wd, m - 1), 0) * N + (N - 1)]);
-        row_pass(g, store_to<K>(Rw[m & 1], nullptr, nullptr), ps, lane, N);
-        tn = uni_k(Rw[m & 1][0]);
+        row_pass(g, store_to<K>(F, nullptr), ps, lane, N);
+        tn = uni_k(F[0]);
         if (tn == KeyT<K>::inf) {
             *T_out = E2_INF64;
             *mu_out = 0;
             return;
         }
     }
-    // the combines read the backward rows back from their pool
-    __builtin_amdgcn_s_waitcnt(0);
-    __threadfence_block();
 
     // ---- masters in ascending position, each followed by the forward row
-    // it leaves for the next (F_mu: LDS ping-pong + pool + split points).
-    // The sweep stops at the first master whose optimum equals the optimum
+    // it leaves for the next (F_mu, in place, split points to tbp).  The
+    // sweep stops at the first master whose optimum equals the optimum
     // without a master: no later master can do better (a head only adds time
     // and bytes), and ties go to the smaller master.
     K acc = KeyT<K>::inf;
     K key = KeyT<K>::inf;
-    int f_last = 0;  // the last forward row computed
+    int f_last = 0;  // the forward row the buffer holds
     for (int mu = 1; mu <= m; ++mu) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, mu, mu);
         if (rw.cap > 0) {
-            if (mu >= 2)
-                set_prev(rw, Rw[(mu - 1) & 1], band_lo(cr, mu - 1), band_hi(cr, mu - 1));
-            RowOut<K> ro = store_to<K>(nullptr, nullptr, nullptr);
+            if (mu >= 2) set_prev(rw, F, band_lo(cr, mu - 1), band_hi(cr, mu - 1));
+            RowOut<K> ro = store_to<K>(nullptr, nullptr);
             ro.combine = true;
             ro.mu = mu;
             if (mu == m) {
                 ro.last_only = true;  // the master's stage ends at block N-1
             } else {
                 const int t = m - mu;  // backward row of devices mu+1..m
-                ro.G = gpool + gpool_off(cr, t);
+                if (t < g_lo) {        // not kept: rows 1..t again
+                    g_lo = g_window_lo(cr, lane, t, gcap);
+                    g_rows<K>(tb, cr, r, t, g_lo, gp, ps, lane, N);
+                }
+                ro.G = gp + (gpool_off(cr, t) - gpool_off(cr, g_lo));
                 ro.glo = rband_lo(cr, t);
                 ro.ghi = rband_hi(cr, t);
                 ro.tau_next = to_k<K>(lane_u64(cr.tau, mu));  // link mu -> mu+1
@@ -1073,16 +1119,11 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         }
         if (mu < m) {
             Row<K> f = fwd_row_of<K>(tb, cr, r, mu, 0);
-            if (mu >= 2)
-                set_prev(f, Rw[(mu - 1) & 1], band_lo(cr, mu - 1), band_hi(cr, mu - 1));
-            const int off = pool_off(cr, mu);
-            row_pass(f, store_to<K>(Rw[mu & 1], pool + off, sm.tbp + off), ps, lane, N);
+            if (mu >= 2) set_prev(f, F, band_lo(cr, mu - 1), band_hi(cr, mu - 1));
+            row_pass(f, store_to<K>(F, sm.tbp + pool_off(cr, mu)), ps, lane, N);
             f_last = mu;
         }
     }
-    // the chosen master's first row reads its forward row back from the pool
-    __builtin_amdgcn_s_waitcnt(0);
-    __threadfence_block();
     const K bestk = unpack_val(key);
     const int best_mu = bestk == KeyT<K>::inf ? 0 : key_low8(key);
     *T_out = to_u64(bestk);
@@ -1090,31 +1131,29 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
     if (bestk == KeyT<K>::inf) return;
 
     // ---- rows mu*..m-1 of the chosen master's table (split points overwrite
-    // those of F), then cell N-1 of row m.  Their first row reads F_{mu*-1}
-    // from its ping-pong buffer, which still holds it unless the sweep ran on
-    // two or more rows past it: then it comes back from the pool.
-    if (best_mu >= 2 && best_mu - 1 < f_last - 1) {
-        const int k = best_mu - 1;
-        const int n = band_hi(cr, k) - band_lo(cr, k) + 1;
-        const K *src = pool + pool_off(cr, k);
-        lds_t<K> *dst = Rw[k & 1];
-        for (int x = lane; x < n; x += kWave) dst[x] = src[x];
-        __syncthreads();
+    // those of F), then cell N-1 of row m.  Their first row reads F_{mu*-1},
+    // which the buffer holds unless the sweep went past it: then F_1..F_{mu*-1}
+    // are computed again (their split points are in tbp already).
+    if (best_mu >= 2 && f_last != best_mu - 1) {
+        for (int k = 1; k < best_mu; ++k) {
+            Row<K> f = fwd_row_of<K>(tb, cr, r, k, 0);
+            if (k >= 2) set_prev(f, F, band_lo(cr, k - 1), band_hi(cr, k - 1));
+            row_pass(f, store_to<K>(F, nullptr), ps, lane, N);
+        }
     }
     for (int k = best_mu; k < m; ++k) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, k, best_mu);
-        if (k >= 2) set_prev(rw, Rw[(k - 1) & 1], band_lo(cr, k - 1), band_hi(cr, k - 1));
-        const int off = pool_off(cr, k);
-        row_pass(rw, store_to<K>(Rw[k & 1], nullptr, sm.tbp + off), ps, lane, N);
+        if (k >= 2) set_prev(rw, F, band_lo(cr, k - 1), band_hi(cr, k - 1));
+        row_pass(rw, store_to<K>(F, sm.tbp + pool_off(cr, k)), ps, lane, N);
     }
     if (m >= 2) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, m, best_mu);
         // row m-1 of the chosen table (F_{m-1} when mu* = m: the sweep's last row)
-        set_prev(rw, Rw[(m - 1) & 1], band_lo(cr, m - 1), band_hi(cr, m - 1));
+        set_prev(rw, F, band_lo(cr, m - 1), band_hi(cr, m - 1));
         rw.lo = rw.hi = N - 1;
         rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + f8(lane_w(cr.wa, m - 1), 0)) * N + (N - 1)];
         rw.lmin = uni(rw.lmin);
-        row_pass(rw, store_to<K>(Rw[m & 1], nullptr, last_tb), ps, lane, N);
+        row_pass(rw, store_to<K>(F, last_tb), ps, lane, N);
         // the split points may sit in global memory (long bands): complete
         // every lane's stores before lane 0 walks them
         __builtin_amdgcn_s_waitcnt(0);
@@ -1177,8 +1216,8 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
             rw.phi = N - 1;
         }
         row_pass(rw,
-                 store_to<uint64_t>(cur, nullptr,
-                                    (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1) : nullptr),
+                 store_to<uint64_t>(cur, (tbp && k >= 2) ? tbp + (size_t)(k - 2) * N + (k - 1)
+                                                         : nullptr),
                  ps, lane, N);
         lds_t<uint64_t> *tmp = prv;
         prv = cur;
@@ -1226,8 +1265,7 @@ __device__ __forceinline__ int build_chain(const E2Genomes &gen, int p, int q, i
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_dp(E2Tables tb, int k_max, int pool_cells,
                                            E2Genomes gen, const uint8_t *__restrict__ roles,
                                            int n_r, uint32_t *counters, const uint32_t *__restrict__ list,
-                                           size_t seg_cap, uint64_t *rows, uint8_t *tb_global,
-                                           uint64_t *T,
+                                           size_t seg_cap, uint8_t *tb_global, uint64_t *T,
                                            uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
     extern __shared__ uint64_t dyn[];
@@ -1236,14 +1274,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     __shared__ uint8_t last_tb;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
+    // LDS: split-point pairs, then the banded path's backward-row pool (the
+    // pairs' unused half for 32-bit keys, a row buffer and the extra bytes),
+    // a row buffer and the split-point bytes
     DpSmem sm;
     sm.ps = dyn;
-    sm.Rw0 = (lds_t<uint64_t> *)(dyn + 2 * N);
-    sm.Rw1 = sm.Rw0 + (N + 1);
-    sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N + 2 * (N + 1));
-    uint64_t *my_rows = rows + (size_t)blockIdx.x * (2 * (size_t)pool_cells);
-    sm.pool = my_rows;
-    sm.gpool = my_rows + pool_cells;
+    sm.Rw1 = (lds_t<uint64_t> *)(dyn + 2 * N);
+    sm.pool_end = (lds_t<char> *)(dyn + 2 * N + (N + 1)) + dp_lds_extra(N);
+    sm.Rw0 = (lds_t<uint64_t> *)sm.pool_end;
+    sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N + 2 * (N + 1)) + dp_lds_extra(N);
+    sm.pool = nullptr;
+    sm.gpool = nullptr;
     sm.pool_cells = pool_cells;
     static_assert(kClasses == 4, "job mapping below assumes four classes");
     const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
@@ -2745,10 +2786,8 @@ int e2_dp_lds_tb_cells(int N)
 
 size_t e2_dp_row_words(int N) { return 2 * (size_t)e2_dp_pool_cells(N); }
 
-size_t e2_dp_lds_bytes(int N)
-{
-    return (size_t)16 * N + (size_t)16 * (N + 1) + (size_t)kLdsTbCells;
-}
+size_t e2_dp_lds_bytes(int N) { return (size_t)dp_lds_fixed(N) + (size_t)dp_lds_extra(N); }
+size_t e2_dp_ft_lds_bytes(int N) { return (size_t)dp_lds_fixed(N); }
 
 int e2_dp_slots(int N, int problems)
 {
@@ -2802,14 +2841,14 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
                                                                 wk.idle_stride, T, Lambda,
                                                                 master, layers);
     else if (objective == 1)
-        k_dp_ft<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles,
+        k_dp_ft<<<wk.n_slots, 64, e2_dp_ft_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles,
                                                              wk.counters, wk.list, seg, wk.rows,
                                                              wk.tb_global, T, Lambda, master,
                                                              layers);
     else
         k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles, n_r,
-                                                          wk.counters, wk.list, seg, wk.rows,
-                                                          wk.tb_global, T, Lambda, master, layers);
+                                                          wk.counters, wk.list, seg, wk.tb_global,
+                                                          T, Lambda, master, layers);
     if (wk.ev_end) (void)hipEventRecord(wk.ev_end, s);
     return hipGetLastError();
 }
