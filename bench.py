@@ -24,10 +24,13 @@ Printed on one JSON line:
                the current kernel sources
   cpu_baseline the CPU oracle on a bounded sample of the same generation-0
                population, single-threaded
-  role_search  e2_search_roles on the 1024-genome, 64-device workload (at
-               most 16 clusters per genome) with its decode-slot model: per
-               call, every cluster is solved for prefill and for 1..8 decode
-               requests in flight, then roles are brute-forced per genome
+  role_search  e2_search_roles on the 1024-genome, 64-device workload with
+               its decode-slot model: per call, every cluster is solved for
+               prefill and for 1..8 decode requests in flight, then roles are
+               brute-forced per genome over its clusters with a decode rate;
+               then a two-chromosome generation (search + App. A GA step)
+  role_search_256_devices  the same on the 16384-genome, 256-device workload
+               (32-48 clusters per genome)
   ablations    the two ablations of Sec. 4.2 on the same 1024-genome
                workload: finishing-time objective vs Algorithm 1, adapted
                SplitWise roles vs the brute-force search (time per call and
@@ -487,6 +490,8 @@ def main():
                                         **summary(t2, n, "two_chromosome"))
     if args.genomes == "both" and args.search_steps > 0:
         result["role_search"] = role_search(torch, dev, args.search_steps, args.warmup)
+        result["role_search_256_devices"] = role_search(torch, dev, args.search_steps,
+                                                        args.warmup, "c5_256dev_126L_ga")
         result["ablations"] = ablations(torch, dev, args.search_steps, args.warmup)
     if args.genomes == "both" and args.config_steps > 0:
         result["configs"] = {name: config_eval(torch, dev, name, args.config_steps, args.warmup)
@@ -556,12 +561,13 @@ def config_eval(torch, dev, name, steps, warmup):
                     / INT_VALU_PEAK}
 
 
-def role_search(torch, dev, steps, warmup):
+def role_search(torch, dev, steps, warmup, name=None):
     """Time e2_search_roles (every cluster for prefill and each decode slot
-    count, the QoS-feasible slot count, brute-force roles) on the 1024-genome
-    workload with its slot model; count the Algorithm 1 cells of the
-    feasible (cluster, role index) problems."""
-    wl = workload.make(SEARCH_WORKLOAD)
+    count, the QoS-feasible slot count, brute-force roles over the clusters
+    with a decode rate) on a workload with its slot model (by default the
+    1024-genome, 64-device one); count the Algorithm 1 cells of the feasible
+    (cluster, role index) problems."""
+    wl = workload.make(name or SEARCH_WORKLOAD)
     sm = workload.slot_model(wl)
     ctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
     L = torch.from_numpy(wl.labels).to(dev)
@@ -589,11 +595,17 @@ def role_search(torch, dev, steps, warmup):
         problems += ok
         cells += ok * m * (m * N - m * (m - 1) // 2)
     slots = out["slots"].cpu().numpy()
+    # clusters with a decode rate (the ones the brute force enumerates)
+    lam_max = 10**12 // wl.min_tps_milli if wl.min_tps_milli else INF
+    free = ((T_all[:, :, 1:] != INF) & (e2.u64(out["Lambda_all"])[:, :, 1:] <= lam_max)).any(axis=2)
+    free = free.sum(axis=1)
     log(f"role search on {wl.name}: {elapsed * 1e3 / steps:.3f} ms per call, DP kernel "
-        f"{dp_ms / n_dp:.3f} ms")
+        f"{dp_ms / n_dp:.3f} ms; clusters with a decode rate: mean {free.mean():.2f}, "
+        f"max {free.max()}")
     gen2 = ordered_search_generations(torch, dev, wl, sm, ctx, steps, warmup)
+    klo, khi = workload.SPECS[wl.name]["K"]
     return {"workload": wl.name, "population": wl.population, "devices": wl.n_dev,
-            "layers": N, "clusters_per_genome": "8-12", "slot_model": sm,
+            "layers": N, "clusters_per_genome": f"{klo}-{khi}", "slot_model": sm,
             "call": "e2_search_roles", "steps": steps,
             "ms_per_call": elapsed * 1e3 / steps,
             "genomes_per_s": wl.population * steps / elapsed,
@@ -601,6 +613,8 @@ def role_search(torch, dev, steps, warmup):
             "dp_cells_per_s": cells * steps / elapsed,
             "k_dp_avg_ms": dp_ms / n_dp,
             "decode_replicas_at_b_max": int((slots == sm["b_max"]).sum()),
+            "clusters_with_a_decode_rate": {"mean": float(free.mean()), "max": int(free.max())},
+            "genomes_not_searched": int((slots == 0xFF).all(axis=1).sum()),
             "two_chromosome_generation": gen2}
 
 
