@@ -493,9 +493,12 @@ def main():
         result["role_search_256_devices"] = role_search(torch, dev, args.search_steps,
                                                         args.warmup, "c5_256dev_126L_ga")
         result["ablations"] = ablations(torch, dev, args.search_steps, args.warmup)
+    cfg_rows = {}
     if args.genomes == "both" and args.config_steps > 0:
-        result["configs"] = {name: config_eval(torch, dev, name, args.config_steps, args.warmup)
-                             for name in workload.NAMES[:4]}
+        result["configs"] = {}
+        for name in workload.NAMES[:4]:
+            result["configs"][name], cfg_rows[name] = config_eval(torch, dev, name,
+                                                                  args.config_steps, args.warmup)
     if args.cpu_seconds > 0 and head == "labels":
         L0 = torch.from_numpy(wl.labels).to(dev)
         R0 = torch.from_numpy(wl.roles).to(dev)
@@ -505,7 +508,7 @@ def main():
         gpu0 = dict(T=e2.u64(sol["T"]), Lambda=e2.u64(sol["Lambda"]),
                     master=sol["master"].cpu().numpy(), layers=sol["layers"].cpu().numpy(),
                     **{k: e2.u64(v) for k, v in fit0.items()})
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, gpu0)
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, gpu0, cfg_rows)
     print(json.dumps(result), flush=True)
 
 
@@ -517,7 +520,8 @@ def config_eval(torch, dev, name, steps, warmup):
     call (wall clock around `steps` calls after `warmup`), the DP kernel's
     time from the library's events, fitness evaluations/s, and the
     Algorithm 1 cells and candidates of the population against the kernel's
-    own candidates."""
+    own candidates.  Returns that record and the GPU's rows of the
+    population (T, Lambda, master, layers, w, phase, S_P, S_D)."""
     wl = workload.make(name)
     P, K = wl.population, wl.k_max
     ctx = e2.e2_ctx_create(wl.problem_arrays())
@@ -540,7 +544,11 @@ def config_eval(torch, dev, name, steps, warmup):
     e2.e2_ctx_dp_timing(ctx, 0)
     sol = e2.e2_solve_partitions(ctx, L, R)
     sol0 = e2.e2_solve_partitions(ctx_free, L, R)
+    fit = e2.e2_eval_population(ctx, L, R, fp)
     torch.cuda.synchronize()
+    rows = dict(T=e2.u64(sol["T"]), Lambda=e2.u64(sol["Lambda"]),
+                master=sol["master"].cpu().numpy(), layers=sol["layers"].cpu().numpy(),
+                **{k: e2.u64(v) for k, v in fit.items()})
     win, winR, cap = window_tables(wl)
     tabs = (win, winR, cap) + count_tables(win, winR, wl.n_layer) + value_bounds(wl, win)
     cells, cand, cand32, alg1 = generation_work(
@@ -556,9 +564,10 @@ def config_eval(torch, dev, name, steps, warmup):
             "dp_cells_per_s": cells * steps / elapsed,
             "k_dp_avg_ms": dp_s * 1e3,
             "kernel_candidates_per_eval": kern,
+            "kernel_candidates_per_s": kern * steps / elapsed,
             "alg1_candidates_per_eval": alg1,
             "frac": (cand * OPS_PER_CANDIDATE + cand32 * OPS_PER_CANDIDATE_NARROW) / dp_s
-                    / INT_VALU_PEAK}
+                    / INT_VALU_PEAK}, rows
 
 
 def role_search(torch, dev, steps, warmup, name=None):
@@ -891,12 +900,17 @@ def host_cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(wl, seconds, gpu0=None):
+CPU_CONFIG_GENOMES = 1024  # oracle sample per smaller workload (its first genomes)
+
+
+def cpu_baseline(wl, seconds, gpu0=None, cfg_rows=None):
     """The oracle, as it is (single-threaded C, one host core), on the first S
     genomes of the generation-0 population, S sized from a short probe to
     take about `seconds`.  Its rows are then compared with the GPU's
     evaluation of the same genomes (gpu0: T, Lambda, master, layers, w,
-    phase, S_P, S_D of generation 0)."""
+    phase, S_P, S_D of generation 0).  With cfg_rows (the GPU's rows of the
+    smaller workloads' populations), the oracle also evaluates the first
+    CPU_CONFIG_GENOMES genomes of each, timed, and compares them row by row."""
     import oracle
     oracle._load()
     probe = 16
@@ -931,6 +945,22 @@ def cpu_baseline(wl, seconds, gpu0=None):
         out["gpu_rows_compared"] = S
     log(f"cpu oracle: {S} genomes in {dt:.2f} s"
         + (f"; {out['gpu_rows_equal']} of {S} equal the GPU's rows" if gpu0 is not None else ""))
+    if cfg_rows:
+        out["configs"] = {}
+        for name, rows in cfg_rows.items():
+            cw = workload.make(name)
+            n = min(cw.population, CPU_CONFIG_GENOMES)
+            t0 = time.perf_counter()
+            ref = oracle.eval_population(cw.subset(np.arange(n)))
+            cdt = time.perf_counter() - t0
+            same = np.ones(n, dtype=bool)
+            for k in ("T", "Lambda", "master", "layers", "w", "phase", "s_p", "s_d"):
+                same &= np.asarray(rows[k][:n] == ref[k]).reshape(n, -1).all(axis=1)
+            out["configs"][name] = {"genomes": n, "population": cw.population, "seconds": cdt,
+                                    "ms_per_genome": cdt * 1e3 / n, "cores": 1,
+                                    "gpu_rows_equal": int(same.sum()), "gpu_rows_compared": n}
+            log(f"cpu oracle on {name}: {n} genomes in {cdt:.2f} s; {int(same.sum())} of {n} "
+                f"equal the GPU's rows")
     return out
 
 
