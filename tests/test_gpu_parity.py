@@ -380,3 +380,38 @@ def test_injected_hip_failure_enqueues_nothing(torch_dev):
     want = oracle.eval_population(wl)
     for k in out:
         assert np.array_equal(e2.u64(out[k]), want[k]), k
+
+
+@pytest.mark.parametrize("kind", ["labels", "two_chromosome"])
+def test_genome_ranges_merge_to_the_whole_population(torch_dev, kind):
+    """The one-GPU part of sharding the evaluation by genome range: the
+    16384-genome population evaluated as four contiguous ranges (separate
+    calls on slices of the same device arrays, uneven sizes) concatenates
+    to the single call's every output, bit for bit."""
+    torch, dev = torch_dev
+    wl = workload.make("c5_256dev_126L_ga")
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    fp = wl.fitness_params()
+    if kind == "labels":
+        ins = [torch.from_numpy(x).to(dev) for x in (wl.labels, wl.roles)]
+        solve, evaluate = e2.e2_solve_partitions, e2.e2_eval_population
+    else:
+        op = workload.ordered_population(wl)
+        ins = [torch.from_numpy(x).to(dev) for x in (op.order, op.sizes, op.roles)]
+        solve, evaluate = e2.e2_solve_partitions_ordered, e2.e2_eval_population_ordered
+
+    def run(lo, hi):
+        part = [x[lo:hi] for x in ins]
+        sol = solve(ctx, *part)
+        fit = evaluate(ctx, *part, fp)
+        torch.cuda.synchronize()
+        out = dict(T=e2.u64(sol["T"]), Lambda=e2.u64(sol["Lambda"]),
+                   master=sol["master"].cpu().numpy(), layers=sol["layers"].cpu().numpy())
+        out.update({k: e2.u64(fit[k]) for k in ("w", "phase", "s_p", "s_d")})
+        return out
+
+    whole = run(0, wl.population)
+    cuts = [0, 1000, 5096, 12001, wl.population]
+    parts = [run(a, b) for a, b in zip(cuts[:-1], cuts[1:])]
+    for k in whole:
+        assert np.array_equal(np.concatenate([p[k] for p in parts]), whole[k]), k
