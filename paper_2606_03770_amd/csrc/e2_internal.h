@@ -55,9 +55,16 @@ struct e2_ctx {
     int dp_events_used;
 };
 
+// Per-call counters, each on a 256-byte line of its own so that the
+// extraction's atomics on different counters do not serialise on one line.
+constexpr int kCounters = 5;
+constexpr int kCounterStride = 64;  // u32
+constexpr size_t kCounterBytes = (size_t)kCounters * kCounterStride * 4;
+
 // Scratch layout of one solve/eval call (device memory, stream-ordered).
 struct E2Work {
-    uint32_t *counters;  // [0..3] problems listed per chain-length class, [4] next job
+    uint32_t *counters;  // [c * kCounterStride]: c = 0..3 problems listed per chain-length
+                         //   class, c = 4 next job; one 256-byte line each
     uint32_t *list;      // [4][P * k_max * n_r] problems needing the DP: (p << 8) | q, or
                          //   with every role index searched (p << 12) | (q << 4) | r
     uint64_t *rows;      // [n_slots][2 pool] per-wave rows of the finishing-time kernel, or null

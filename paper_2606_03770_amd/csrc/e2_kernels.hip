@@ -95,7 +95,7 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
 
 __global__ void k_init(uint32_t *counters)
 {
-    if (threadIdx.x < 8) counters[threadIdx.x] = 0;
+    if (threadIdx.x < kCounters) counters[threadIdx.x * kCounterStride] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -162,14 +162,14 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                                                       uint64_t *T, uint64_t *Lambda,
                                                       int16_t *master, uint8_t *layers)
 {
-    // per genome: (count << 16) + sum of cap0, min cap0, head-capable bitmask,
-    // listed bitmask
+    // per genome: (count << 16) + sum of cap0, min cap0, head-capable flag per
+    // cluster, listed bitmask
     __shared__ uint32_t packed[kEG][256];
     __shared__ uint32_t mincap[kEG][256];
-    __shared__ uint32_t hmask[kEG][8];
+    __shared__ uint32_t hflag[kEG][256];  // 1 when some device can hold a block and the head
     __shared__ uint32_t lmask[kEG][8];
-    __shared__ uint32_t ncls[kEG][kClasses];
-    __shared__ uint32_t base[kEG][kClasses];
+    __shared__ uint32_t ncls[kEG][16][kClasses];  // per genome, pass and class
+    __shared__ uint32_t base[kEG][16][kClasses];
     __shared__ uint32_t offs[kEG][256];  // replica starts of two-chromosome genomes
     __shared__ uint32_t bad[kEG][8];     // replicas holding a device id >= M
     const int g = threadIdx.x / 64;
@@ -219,17 +219,30 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             devs[u] = d;
         }
     }
+    // Every pass (one per role index) decides its clusters and counts them per
+    // class; slot u keeps each pass's class + 1 (0: not listed) in 3 bits of
+    // code[u].  The list ranges of all passes are then reserved with one
+    // atomic per class per workgroup.
     const int passes = n_r > 0 ? n_r : 1;
+    uint64_t code[4] = {0, 0, 0, 0};
+    if (n_r > 0 && p < P) {
+        // every role index of every cluster starts infeasible, in one
+        // contiguous sweep of the genome's [k_max][R] block (the DP kernel,
+        // which runs after this one, overwrites the listed problems)
+        const size_t o0 = (size_t)p * k_max * n_r;
+        for (int i = lane; i < k_max * n_r; i += kWave) {
+            T[o0 + i] = E2_INF64;
+            Lambda[o0 + i] = E2_INF64;
+        }
+    }
+    ncls[g][lane >> 2][lane & 3] = 0;
     for (int ri = 0; ri < passes; ++ri) {
-        for (int q = lane; q < 256; q += 64) {
+        for (int q = lane; q < k_max; q += 64) {
             packed[g][q] = 0;
             mincap[g][q] = 0xFFFFFFFFu;
+            hflag[g][q] = 0;
         }
-        if (lane < 8) {
-            hmask[g][lane] = 0;
-            lmask[g][lane] = 0;
-        }
-        if (lane < kClasses) ncls[g][lane] = 0;
+        if (lane < 8) lmask[g][lane] = 0;
         __syncthreads();
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -241,15 +254,17 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                 const uint32_t c0 = tb.cap0[(size_t)c * M + devs[u]];
                 atomicAdd(&packed[g][lab], (1u << 16) | c0);
                 atomicMin(&mincap[g][lab], c0);
-                if (tb.capH[(size_t)c * M + devs[u]])
-                    atomicOr(&hmask[g][lab >> 5], 1u << (lab & 31));
+                // a per-cluster flag: the atomics of one word meet only the
+                // devices of one cluster
+                if (tb.capH[(size_t)c * M + devs[u]]) atomicOr(&hflag[g][lab], 1u);
             }
         }
         __syncthreads();
-        // decide per cluster; count listed problems per class
-        uint32_t my_cls[4] = {0, 0, 0, 0};
+        // decide per cluster; count listed problems per class (slots u with
+        // no cluster id below k_max are skipped: the bound is uniform)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
+            if (64 * u >= k_max) break;
             const int q = lane + 64 * u;
             bool feas = false;
             int cls = 0;
@@ -260,17 +275,16 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                 // block; with idle devices allowed, every non-empty cluster
                 feas = m >= 1 && !((bad[g][q >> 5] >> (q & 31)) & 1u) &&
                        (relaxed || (m <= (uint32_t)N && csum >= (uint32_t)N &&
-                                    mincap[g][q] >= 1 && ((hmask[g][q >> 5] >> (q & 31)) & 1u)));
+                                    mincap[g][q] >= 1 && hflag[g][q] != 0));
                 cls = size_class((int)m);
-                if (!feas) {
-                    const size_t o = n_r > 0 ? ((size_t)p * k_max + q) * n_r + ri
-                                             : (size_t)p * k_max + q;
+                if (!feas && n_r == 0) {  // (every role index: filled above)
+                    const size_t o = (size_t)p * k_max + q;
                     T[o] = E2_INF64;
                     Lambda[o] = E2_INF64;
                     if (master) master[o] = -1;
                 }
             }
-            my_cls[u] = feas ? (uint32_t)(cls + 1) : 0;
+            code[u] |= (uint64_t)(feas ? cls + 1 : 0) << (3 * ri);
             const uint64_t fm = __ballot(feas);
             if (lane == 0 && fm) {
                 // q = 64u + bit: listed bitmask words 2u and 2u + 1
@@ -279,32 +293,37 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             }
             for (int c = 0; c < kClasses; ++c) {
                 const uint64_t bm = __ballot(feas && cls == c);
-                if (lane == 0) ncls[g][c] += (uint32_t)__popcll(bm);
+                if (lane == 0) ncls[g][ri][c] += (uint32_t)__popcll(bm);
             }
         }
-        __syncthreads();
-        // one atomic per class per workgroup; genome g's share follows genomes < g
-        if (threadIdx.x < kClasses) {
-            const int c = threadIdx.x;
-            uint32_t tot = 0;
-            for (int h = 0; h < kEG; ++h) tot += ncls[h][c];
-            uint32_t b0 = tot ? atomicAdd(&counters[c], tot) : 0;
-            for (int h = 0; h < kEG; ++h) {
-                base[h][c] = b0;
-                b0 += ncls[h][c];
+        __syncthreads();  // the next pass clears the per-cluster sums
+    }
+    // one atomic per class per workgroup; the ranges follow (genome, pass)
+    if (threadIdx.x < kClasses) {
+        const int c = threadIdx.x;
+        uint32_t tot = 0;
+        for (int h = 0; h < kEG; ++h)
+            for (int ri = 0; ri < passes; ++ri) tot += ncls[h][ri][c];
+        uint32_t b0 = tot ? atomicAdd(&counters[c * kCounterStride], tot) : 0;
+        for (int h = 0; h < kEG; ++h)
+            for (int ri = 0; ri < passes; ++ri) {
+                base[h][ri][c] = b0;
+                b0 += ncls[h][ri][c];
             }
-        }
-        __syncthreads();
+    }
+    __syncthreads();
+    for (int ri = 0; ri < passes; ++ri) {
         uint32_t run[kClasses] = {0, 0, 0, 0};
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
+            if (64 * u >= k_max) break;
             const int q = lane + 64 * u;
-            const uint32_t mc = my_cls[u];
+            const uint32_t mc = (uint32_t)(code[u] >> (3 * ri)) & 7u;
             for (int c = 0; c < kClasses; ++c) {
                 const uint64_t bm = __ballot(mc == (uint32_t)(c + 1));
                 if (mc == (uint32_t)(c + 1)) {
                     const uint32_t pos =
-                        base[g][c] + run[c] + (uint32_t)__popcll(bm & ((1ull << lane) - 1));
+                        base[g][ri][c] + run[c] + (uint32_t)__popcll(bm & ((1ull << lane) - 1));
                     list[(size_t)c * seg_cap + pos] =
                         n_r > 0 ? ((uint32_t)p << 12) | ((uint32_t)q << 4) | (uint32_t)ri
                                 : ((uint32_t)p << 8) | (uint32_t)q;
@@ -312,7 +331,6 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                 run[c] += (uint32_t)__popcll(bm);
             }
         }
-        __syncthreads();
     }
     // layers of devices the DP kernel will not write: those outside every
     // listed cluster; for ordered genomes every device (the DP kernel, which
@@ -1287,7 +1305,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     sm.gpool = nullptr;
     sm.pool_cells = pool_cells;
     static_assert(kClasses == 4, "job mapping below assumes four classes");
-    const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
+    const uint32_t n0 = counters[0], n1 = counters[kCounterStride],
+                   n2 = counters[2 * kCounterStride], n3 = counters[3 * kCounterStride];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
 
     // The list runs longest chains first.  Its first part is split statically
@@ -1302,13 +1321,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     auto take = [&](uint32_t done) -> uint32_t {
         if (done + gridDim.x < n_static) return done + gridDim.x;
         uint32_t v = 0;
-        if (lane == 0) v = atomicAdd(&counters[kClasses], 1u);
+        if (lane == 0) v = atomicAdd(&counters[kClasses * kCounterStride], 1u);
         return n_static + (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
     };
     uint32_t first = blockIdx.x;
     if (first >= n_static) {
         uint32_t v = 0;
-        if (lane == 0) v = atomicAdd(&counters[kClasses], 1u);
+        if (lane == 0) v = atomicAdd(&counters[kClasses * kCounterStride], 1u);
         first = n_static + (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
     }
     for (uint32_t job = first; job < n_jobs; job = take(job)) {
@@ -1712,12 +1731,13 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     sm.pool = my_rows;
     sm.gpool = my_rows + pool_cells;
     sm.pool_cells = pool_cells;
-    const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
+    const uint32_t n0 = counters[0], n1 = counters[kCounterStride],
+                   n2 = counters[2 * kCounterStride], n3 = counters[3 * kCounterStride];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
     // waves take the next listed problem from a shared counter: these grids
     // need not be resident at once, and their problems vary more in cost
     for (;;) {
-        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
+        if (lane == 0) job = atomicAdd(&counters[kClasses * kCounterStride], 1u);
         __syncthreads();
         uint32_t idx = job;
         __syncthreads();
@@ -2000,12 +2020,13 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
     uint64_t *B = E + (size_t)M * X;
     uint16_t *Ek = reinterpret_cast<uint16_t *>(B + (size_t)M * X);
     uint8_t *Ej = reinterpret_cast<uint8_t *>(Ek + (size_t)M * X);
-    const uint32_t n0 = counters[0], n1 = counters[1], n2 = counters[2], n3 = counters[3];
+    const uint32_t n0 = counters[0], n1 = counters[kCounterStride],
+                   n2 = counters[2 * kCounterStride], n3 = counters[3 * kCounterStride];
     const uint32_t n_jobs = n0 + n1 + n2 + n3;
     // waves take the next listed problem from a shared counter: these grids
     // need not be resident at once, and their problems vary more in cost
     for (;;) {
-        if (lane == 0) job = atomicAdd(&counters[kClasses], 1u);
+        if (lane == 0) job = atomicAdd(&counters[kClasses * kCounterStride], 1u);
         __syncthreads();
         uint32_t idx = job;
         __syncthreads();
