@@ -186,7 +186,7 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
     const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_lds_tb_cells(ctx->N);
     *tb_bytes = need_tb ? (size_t)(*slots) * ctx->N * ctx->N : 0;
     const size_t idle = objective == 2 ? (size_t)(*slots) * e2_dp_idle_bytes(ctx->M, ctx->N) : 0;
-    return kCounterBytes + align256(problems * 4 * 4) + row_bytes(ctx, *slots, objective) +
+    return kCounterBytes + align256(problems * 4 * kListSegs) + row_bytes(ctx, *slots, objective) +
            align256(*tb_bytes) + align256(idle);
 }
 
@@ -196,8 +196,8 @@ void carve_work(void *base, e2_ctx *ctx, int P, int k_max, int slots, size_t tb_
     char *p = static_cast<char *>(base);
     wk->counters = reinterpret_cast<uint32_t *>(p);
     p += kCounterBytes;
-    wk->list = reinterpret_cast<uint32_t *>(p);  // four chain-length segments of P * k_max * n_r
-    p += align256((size_t)P * k_max * n_r * 4 * 4);
+    wk->list = reinterpret_cast<uint32_t *>(p);  // kListSegs segments of P * k_max * n_r
+    p += align256((size_t)P * k_max * n_r * 4 * kListSegs);
     wk->rows = objective == 1 ? reinterpret_cast<uint64_t *>(p) : nullptr;
     p += row_bytes(ctx, slots, objective);
     wk->tb_global = tb_bytes ? reinterpret_cast<uint8_t *>(p) : nullptr;
@@ -853,7 +853,7 @@ int e2_eval_population_noalloc(e2_ctx *ctx, void *stream, int32_t P, int32_t k_m
     // many DP waves' row regions (and split-point tables) as still fit
     const size_t problems = (size_t)P * k_max;
     const size_t tl = align256(problems * 8);
-    const size_t fixed = kCounterBytes + align256(problems * 4 * 4) + 2 * tl;
+    const size_t fixed = kCounterBytes + align256(problems * 4 * kListSegs) + 2 * tl;
     const int mcap = ctx->M < ctx->N ? ctx->M : ctx->N;
     const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_lds_tb_cells(ctx->N);
     const size_t per_wave = need_tb ? (size_t)ctx->N * ctx->N : 0;
@@ -869,7 +869,7 @@ int e2_eval_population_noalloc(e2_ctx *ctx, void *stream, int32_t P, int32_t k_m
     if ((rc = scratch_on(ctx->device, &base))) return rc;
     E2Work wk;
     carve_work(base, ctx, P, k_max, slots, tbb, &wk);
-    char *after = static_cast<char *>(base) + kCounterBytes + align256(problems * 4 * 4) +
+    char *after = static_cast<char *>(base) + kCounterBytes + align256(problems * 4 * kListSegs) +
                   row_bytes(ctx, slots, 0) + align256(tbb);
     uint64_t *Ts = reinterpret_cast<uint64_t *>(after);
     uint64_t *Ls = reinterpret_cast<uint64_t *>(after + tl);

@@ -57,15 +57,18 @@ struct e2_ctx {
 
 // Per-call counters, each on a 256-byte line of its own so that the
 // extraction's atomics on different counters do not serialise on one line.
-constexpr int kCounters = 5;
-constexpr int kCounterStride = 64;  // u32
+constexpr int kCounters = 7;        // 0..4: problems listed per list segment, 5: next job,
+constexpr int kCounterStride = 64;  // 6: next job of the long-chain kernel (u32 stride)
+constexpr int kListSegs = 5;        // chain-length classes m >= 16, 12..15, 8..11, < 8, and
+                                    // (bottleneck objective only) m > 64
+constexpr int kJobCounter = 5;
+constexpr int kLongJobCounter = 6;
 constexpr size_t kCounterBytes = (size_t)kCounters * kCounterStride * 4;
 
 // Scratch layout of one solve/eval call (device memory, stream-ordered).
 struct E2Work {
-    uint32_t *counters;  // [c * kCounterStride]: c = 0..3 problems listed per chain-length
-                         //   class, c = 4 next job; one 256-byte line each
-    uint32_t *list;      // [4][P * k_max * n_r] problems needing the DP: (p << 8) | q, or
+    uint32_t *counters;  // [c * kCounterStride], one 256-byte line each (see kCounters)
+    uint32_t *list;      // [kListSegs][P * k_max * n_r] problems needing the DP: (p << 8) | q, or
                          //   with every role index searched (p << 12) | (q << 4) | r
     uint64_t *rows;      // [n_slots][2 pool] per-wave rows of the finishing-time kernel, or null
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null

@@ -112,6 +112,9 @@ constexpr int kEG = 8;       // genomes per extraction workgroup
 constexpr int kDynTailShift = 2;  // the last 1/4 of the DP list is taken dynamically ...
 constexpr uint32_t kDynTailMinPerWave = 16;  // ... with at least this many problems per wave
 constexpr int kClasses = 4;  // chain-length classes: m >= 16, 12..15, 8..11, < 8
+// longest chain whose per-position table fits one register per lane; longer
+// chains of the bottleneck objective go to the list's last segment
+constexpr int kMaxBandedChain = kWave;
 
 __device__ __forceinline__ int size_class(int m)
 {
@@ -157,7 +160,8 @@ __device__ __forceinline__ E2Tables mem_view(const E2Tables &tb, int r)
 // [P][k_max][R] and list codes (p << 12) | (q << 4) | r.
 __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_max,
                                                       E2Genomes gen, const uint8_t *roles,
-                                                      int n_r, int relaxed, uint32_t *counters,
+                                                      int n_r, int relaxed, int long_seg,
+                                                      uint32_t *counters,
                                                       uint32_t *list, size_t seg_cap,
                                                       uint64_t *T, uint64_t *Lambda,
                                                       int16_t *master, uint8_t *layers)
@@ -168,8 +172,8 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
     __shared__ uint32_t mincap[kEG][256];
     __shared__ uint32_t hflag[kEG][256];  // 1 when some device can hold a block and the head
     __shared__ uint32_t lmask[kEG][8];
-    __shared__ uint32_t ncls[kEG][16][kClasses];  // per genome, pass and class
-    __shared__ uint32_t base[kEG][16][kClasses];
+    __shared__ uint32_t ncls[kEG][16][kListSegs];  // per genome, pass and list segment
+    __shared__ uint32_t base[kEG][16][kListSegs];
     __shared__ uint32_t offs[kEG][256];  // replica starts of two-chromosome genomes
     __shared__ uint32_t bad[kEG][8];     // replicas holding a device id >= M
     const int g = threadIdx.x / 64;
@@ -235,7 +239,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             Lambda[o0 + i] = E2_INF64;
         }
     }
-    ncls[g][lane >> 2][lane & 3] = 0;
+    for (int i = lane; i < 16 * kListSegs; i += kWave) ncls[g][i / kListSegs][i % kListSegs] = 0;
     for (int ri = 0; ri < passes; ++ri) {
         for (int q = lane; q < k_max; q += 64) {
             packed[g][q] = 0;
@@ -276,7 +280,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                 feas = m >= 1 && !((bad[g][q >> 5] >> (q & 31)) & 1u) &&
                        (relaxed || (m <= (uint32_t)N && csum >= (uint32_t)N &&
                                     mincap[g][q] >= 1 && hflag[g][q] != 0));
-                cls = size_class((int)m);
+                cls = (long_seg && m > (uint32_t)kMaxBandedChain) ? kClasses : size_class((int)m);
                 if (!feas && n_r == 0) {  // (every role index: filled above)
                     const size_t o = (size_t)p * k_max + q;
                     T[o] = E2_INF64;
@@ -291,7 +295,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                 lmask[g][2 * u] = (uint32_t)fm;
                 lmask[g][2 * u + 1] = (uint32_t)(fm >> 32);
             }
-            for (int c = 0; c < kClasses; ++c) {
+            for (int c = 0; c < kListSegs; ++c) {
                 const uint64_t bm = __ballot(feas && cls == c);
                 if (lane == 0) ncls[g][ri][c] += (uint32_t)__popcll(bm);
             }
@@ -299,7 +303,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
         __syncthreads();  // the next pass clears the per-cluster sums
     }
     // one atomic per class per workgroup; the ranges follow (genome, pass)
-    if (threadIdx.x < kClasses) {
+    if (threadIdx.x < kListSegs) {
         const int c = threadIdx.x;
         uint32_t tot = 0;
         for (int h = 0; h < kEG; ++h)
@@ -313,13 +317,13 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
     }
     __syncthreads();
     for (int ri = 0; ri < passes; ++ri) {
-        uint32_t run[kClasses] = {0, 0, 0, 0};
+        uint32_t run[kListSegs] = {0, 0, 0, 0, 0};
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             if (64 * u >= k_max) break;
             const int q = lane + 64 * u;
             const uint32_t mc = (uint32_t)(code[u] >> (3 * ri)) & 7u;
-            for (int c = 0; c < kClasses; ++c) {
+            for (int c = 0; c < kListSegs; ++c) {
                 const uint64_t bm = __ballot(mc == (uint32_t)(c + 1));
                 if (mc == (uint32_t)(c + 1)) {
                     const uint32_t pos =
@@ -815,7 +819,6 @@ __device__ __forceinline__ RowOut<K> store_to(lds_t<K> *vals, uint8_t *tbs)
 // previous row of every sweep sits in an LDS ping-pong pair; forward rows
 // are also written to a per-wave global pool for the chosen master's rows.
 // ---------------------------------------------------------------------------
-constexpr int kMaxBandedChain = kWave;
 // split-point bytes kept in LDS per wave; larger tables (the bands of long
 // chains with roomy devices, or the reference path's full rows) go to the
 // wave's region of the global split-point table
@@ -832,11 +835,20 @@ __host__ __device__ constexpr int dp_lds_extra(int N)
     return dp_lds_fixed(N) < kDpLdsTarget ? ((kDpLdsTarget - dp_lds_fixed(N)) & ~7) : 0;
 }
 
+__device__ __forceinline__ int f8(uint32_t w, int sh) { return (int)((w >> sh) & 0xFFu); }
+
+__device__ __forceinline__ int lane_i(int v, int k) { return __builtin_amdgcn_readlane(v, k); }
+__device__ __forceinline__ uint32_t lane_w(uint32_t v, int k)
+{
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, k);
+}
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int k) { return readlane_u64(v, k); }
+
 // Per-position table of a chain: lane k-1 holds chain position k (1-based)
 // as five packed words (fields < 256 except the pool offsets) and two u64
 // times; a row reads its words with one readlane each and unpacks them in
 // scalar registers.  Reversed row t's link (position m+1-t to m+2-t) is the
-// forward link held by lane m+1-t.
+// forward link held by lane m+1-t.  The accessors take 0-based positions.
 struct ChainRegs {
     uint32_t wa;    // dev | cap0 << 8 | capH << 16 | lmin0 << 24      (forward row k)
     uint32_t wb;    // flo | fhi << 8 | lmin1 << 16                    (forward row k)
@@ -846,30 +858,66 @@ struct ChainRegs {
     uint64_t tau;   // link from position k-1 (k >= 2)
     uint64_t head;  // head time of the device
     int m;          // chain length (uniform)
+    __device__ __forceinline__ uint32_t A(int k0) const { return lane_w(wa, k0); }
+    __device__ __forceinline__ uint32_t B(int k0) const { return lane_w(wb, k0); }
+    __device__ __forceinline__ uint32_t C(int k0) const { return lane_w(wc, k0); }
+    __device__ __forceinline__ uint32_t D(int k0) const { return lane_w(wd, k0); }
+    __device__ __forceinline__ uint32_t E(int k0) const { return lane_w(we, k0); }
+    __device__ __forceinline__ uint64_t TAU(int k0) const { return lane_u64(tau, k0); }
+    __device__ __forceinline__ uint64_t HEAD(int k0) const { return lane_u64(head, k0); }
 };
 // cap0 / capH are the longest stages without / with the head, [flo, fhi]
 // the forward band, lmin0 / lmin1 its window-length bounds; reversed row
 // t = k runs on device devR (position m+1-k) with cap0 capR over the band
 // [glo, ghi] with window-length bound lminR.
-__device__ __forceinline__ int f8(uint32_t w, int sh) { return (int)((w >> sh) & 0xFFu); }
 
-__device__ __forceinline__ int lane_i(int v, int k) { return __builtin_amdgcn_readlane(v, k); }
-__device__ __forceinline__ uint32_t lane_w(uint32_t v, int k)
-{
-    return (uint32_t)__builtin_amdgcn_readlane((int)v, k);
-}
+// The same table for chains of up to kLongSets x 64 devices: position k0
+// (0-based) sits in set k0 / 64 at lane k0 % 64.  Positions are uniform, so
+// an accessor reads one lane of each set and keeps the one its set names.
+constexpr int kLongSets = 4;
+struct ChainRegsLong {
+    ChainRegs s[kLongSets];  // the m field of each set is unused
+    int m;
+    template <typename F>
+    __device__ __forceinline__ uint32_t pick(int k0, F f) const
+    {
+        const int set = k0 >> 6, l = k0 & 63;
+        uint32_t v = lane_w(f(s[0]), l);
+#pragma unroll
+        for (int i = 1; i < kLongSets; ++i)
+            if (set == i) v = lane_w(f(s[i]), l);
+        return v;
+    }
+    template <typename F>
+    __device__ __forceinline__ uint64_t pick64(int k0, F f) const
+    {
+        const int set = k0 >> 6, l = k0 & 63;
+        uint64_t v = lane_u64(f(s[0]), l);
+#pragma unroll
+        for (int i = 1; i < kLongSets; ++i)
+            if (set == i) v = lane_u64(f(s[i]), l);
+        return v;
+    }
+    __device__ __forceinline__ uint32_t A(int k0) const { return pick(k0, [](const ChainRegs &c) { return c.wa; }); }
+    __device__ __forceinline__ uint32_t B(int k0) const { return pick(k0, [](const ChainRegs &c) { return c.wb; }); }
+    __device__ __forceinline__ uint32_t C(int k0) const { return pick(k0, [](const ChainRegs &c) { return c.wc; }); }
+    __device__ __forceinline__ uint32_t D(int k0) const { return pick(k0, [](const ChainRegs &c) { return c.wd; }); }
+    __device__ __forceinline__ uint32_t E(int k0) const { return pick(k0, [](const ChainRegs &c) { return c.we; }); }
+    __device__ __forceinline__ uint64_t TAU(int k0) const { return pick64(k0, [](const ChainRegs &c) { return c.tau; }); }
+    __device__ __forceinline__ uint64_t HEAD(int k0) const { return pick64(k0, [](const ChainRegs &c) { return c.head; }); }
+};
+
 // band of forward row k and its pool offset
-__device__ __forceinline__ int band_lo(const ChainRegs &cr, int k) { return f8(lane_w(cr.wb, k - 1), 0); }
-__device__ __forceinline__ int band_hi(const ChainRegs &cr, int k) { return f8(lane_w(cr.wb, k - 1), 8); }
-__device__ __forceinline__ int pool_off(const ChainRegs &cr, int k)
+template <class CR> __device__ __forceinline__ int band_lo(const CR &cr, int k) { return f8(cr.B(k - 1), 0); }
+template <class CR> __device__ __forceinline__ int band_hi(const CR &cr, int k) { return f8(cr.B(k - 1), 8); }
+template <class CR> __device__ __forceinline__ int pool_off(const CR &cr, int k)
 {
-    return (int)(lane_w(cr.wc, k - 1) & 0xFFFFu);
+    return (int)(cr.C(k - 1) & 0xFFFFu);
 }
-__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int k) { return readlane_u64(v, k); }
 // band of reversed row t and its offset in the backward-row pool
-__device__ __forceinline__ int rband_lo(const ChainRegs &cr, int t) { return f8(lane_w(cr.wd, t - 1), 8); }
-__device__ __forceinline__ int rband_hi(const ChainRegs &cr, int t) { return f8(lane_w(cr.wd, t - 1), 16); }
-__device__ __forceinline__ int gpool_off(const ChainRegs &cr, int t) { return (int)lane_w(cr.we, t - 1); }
+template <class CR> __device__ __forceinline__ int rband_lo(const CR &cr, int t) { return f8(cr.D(t - 1), 8); }
+template <class CR> __device__ __forceinline__ int rband_hi(const CR &cr, int t) { return f8(cr.D(t - 1), 16); }
+template <class CR> __device__ __forceinline__ int gpool_off(const CR &cr, int t) { return (int)cr.E(t - 1); }
 
 // Inclusive prefix sum over the wave with DPP moves only (no LDS round
 // trips): prefixes of 4 lanes within each 16-lane row from the inputs, then
@@ -904,20 +952,20 @@ struct DpSmem {
 
 // Row k (1-based) of the table for master mu (mu = 0: no master) as a
 // forward row; prev / plo / phi are filled in by the caller.
-template <typename K>
-__device__ __forceinline__ Row<K> fwd_row_of(const E2Tables &tb, const ChainRegs &cr, int r, int k,
+template <typename K, class CR>
+__device__ __forceinline__ Row<K> fwd_row_of(const E2Tables &tb, const CR &cr, int r, int k,
                                              int mu)
 {
     const int f = (mu == k);
-    const uint32_t wa = lane_w(cr.wa, k - 1), wb = lane_w(cr.wb, k - 1);
+    const uint32_t wa = cr.A(k - 1), wb = cr.B(k - 1);
     const int c = f8(wa, 0);
     Row<K> rw;
     rw.pr = pref_row(tb, r, c);
     rw.p8 = pref8_row<K>(tb, r, c);
     rw.wr = win_row(tb, f, c);
-    rw.hadd = f ? lane_u64(cr.head, k - 1) : 0;
+    rw.hadd = f ? cr.HEAD(k - 1) : 0;
     rw.hadd8 = shift8<K>(rw.hadd);
-    rw.tau = (k >= 2) ? to_k<K>(lane_u64(cr.tau, k - 1)) : (K)0;
+    rw.tau = (k >= 2) ? to_k<K>(cr.TAU(k - 1)) : (K)0;
     rw.lo = f8(wb, 0);
     rw.hi = f8(wb, 8);
     rw.kmin = k - 1;
@@ -941,10 +989,10 @@ __device__ __forceinline__ void set_prev(Row<K> &rw, const lds_t<K> *prev, int p
 // blocks in reverse order (block N-1 first), without a master; prev / plo /
 // phi are filled in by the caller.  For t = m the caller also sets the cell
 // range (the band fields of position 1 are not packed).
-template <typename K>
-__device__ __forceinline__ Row<K> rev_row_of(const E2Tables &tb, const ChainRegs &cr, int r, int t)
+template <typename K, class CR>
+__device__ __forceinline__ Row<K> rev_row_of(const E2Tables &tb, const CR &cr, int r, int t)
 {
-    const uint32_t wc = lane_w(cr.wc, t - 1), wd = lane_w(cr.wd, t - 1);
+    const uint32_t wc = cr.C(t - 1), wd = cr.D(t - 1);
     const int c = f8(wd, 0);
     Row<K> g;
     g.pr = prefR_row(tb, r, c);
@@ -952,7 +1000,7 @@ __device__ __forceinline__ Row<K> rev_row_of(const E2Tables &tb, const ChainRegs
     g.wr = tb.winR + (uint32_t)(c * tb.N);
     g.hadd = 0;
     g.hadd8 = 0;
-    g.tau = (t >= 2) ? to_k<K>(lane_u64(cr.tau, cr.m + 1 - t)) : (K)0;  // link m+1-t -> m+2-t
+    g.tau = (t >= 2) ? to_k<K>(cr.TAU(cr.m + 1 - t)) : (K)0;  // link m+1-t -> m+2-t
     g.lo = f8(wd, 8);
     g.hi = f8(wd, 16);
     g.kmin = t - 1;
@@ -1028,6 +1076,101 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
     return pool_need <= sm.pool_cells && gpool_need <= sm.pool_cells;
 }
 
+// The per-position table of a chain of up to kLongSets x 64 devices (as
+// chain_regs, position k0 = 64 i + lane in set i), with the prefix sums
+// carried from set to set.  The banded path takes every such chain: its
+// rows live in LDS, and split points beyond the LDS copy go to the wave's
+// global table.
+__device__ __forceinline__ void chain_regs_long(const E2Tables &tb, int r, const uint8_t *chain,
+                                                int m, int lane, ChainRegsLong &cr,
+                                                uint64_t *bound, uint64_t *bound_tot,
+                                                int *pool_cells)
+{
+    const int N = tb.N, M = tb.M;
+    cr.m = m;
+    int dev[kLongSets], cap0[kLongSets], pre[kLongSets];
+    uint64_t vb = 0, vt = 0;
+    int carry = 0;
+#pragma unroll
+    for (int i = 0; i < kLongSets; ++i) {
+        const int k0 = 64 * i + lane;
+        const bool valid = k0 < m;
+        dev[i] = valid ? chain[k0] : 0;
+        cap0[i] = valid ? tb.cap0[dev[i]] : 0;
+        ChainRegs &c = cr.s[i];
+        c.m = m;
+        c.head = valid ? tb.head[r * M + dev[i]] : 0;
+        c.tau = (valid && k0 >= 1) ? link_tau(tb, r, chain[k0 - 1], dev[i]) : 0;
+        const uint64_t tf = c.tau != E2_INF64 ? c.tau : 0;
+        vb = umax64(vb, umax64(valid ? tb.vmax[r * M + dev[i]] : 0, tf));
+        vt = umax64(vt, umax64(valid ? tb.vtot[r * M + dev[i]] : 0, tf));
+        pre[i] = scan_incl_i32(cap0[i], lane) + carry;
+        carry = lane_i(pre[i], kWave - 1);
+    }
+    *bound = wave_max_u64(vb);
+    *bound_tot = wave_max_u64(vt);
+    auto at = [&](const int (&v)[kLongSets], int k0) {  // value of position k0, per lane
+        const int l = k0 & 63, set = k0 >> 6;
+        int x = 0;
+#pragma unroll
+        for (int i = 0; i < kLongSets; ++i) {
+            const int y = __shfl(v[i], l, kWave);
+            if (set == i) x = y;
+        }
+        return x;
+    };
+    int tot = 0;  // pre at the last position (a uniform set, selected without indexing)
+#pragma unroll
+    for (int i = 0; i < kLongSets; ++i) {
+        const int v = lane_i(pre[i], (m - 1) & 63);
+        if (((m - 1) >> 6) == i) tot = v;
+    }
+    int size_carry = 0, g_carry = 0;
+#pragma unroll
+    for (int i = 0; i < kLongSets; ++i) {
+        ChainRegs &c = cr.s[i];
+        const int k1 = 64 * i + lane + 1;
+        const bool valid = k1 <= m;
+        const int d = dev[i];
+        const int capH = valid ? tb.capH[d] : 0;
+        int lo = max(k1 - 1, N - 1 - (tot - pre[i]));
+        int hi = min(N - 1 - (m - k1), pre[i] - 1);
+        if (hi < lo) { lo = 1; hi = 0; }
+        const int size = (valid && k1 < m) ? hi - lo + 1 : 0;
+        const int size_incl = scan_incl_i32(size, lane) + size_carry;
+        size_carry = lane_i(size_incl, kWave - 1);
+        const int off = size_incl - size;
+        const int lmin0 = (valid && lo <= hi) ? tb.minwin[(size_t)d * N + lo] : 0;
+        const int lmin1 = (valid && lo <= hi) ? tb.minwin[((size_t)M + d) * N + lo] : 0;
+        // reversed row t = k1 covers original position kk = m+1-t
+        const int kk = m + 1 - k1;
+        const int src = max(0, min(kLongSets * 64 - 1, kk - 1));
+        const int devR = at(dev, src);
+        const int capR = at(cap0, src);
+        const int pre_km1 = (kk >= 2) ? at(pre, max(0, kk - 2)) : 0;
+        int glo = 1, ghi = 0, lminR = 0;
+        {
+            const bool vr = k1 < m;
+            const int gl = max(kk - 1, N - (tot - pre_km1));
+            const int gh = min(pre_km1, N - (m - kk + 1));
+            if (vr && gh >= gl) {
+                glo = N - 1 - gh;
+                ghi = N - 1 - gl;
+                lminR = tb.minwinR[(size_t)devR * N + glo];
+            }
+        }
+        c.wa = (uint32_t)d | (uint32_t)cap0[i] << 8 | (uint32_t)capH << 16 | (uint32_t)lmin0 << 24;
+        c.wb = (uint32_t)lo | (uint32_t)hi << 8 | (uint32_t)lmin1 << 16;
+        c.wc = ((uint32_t)off & 0xFFFFu) | (uint32_t)lminR << 16 | (uint32_t)capR << 24;
+        c.wd = (uint32_t)devR | (uint32_t)glo << 8 | (uint32_t)ghi << 16;
+        const int gsize = ghi >= glo ? ghi - glo + 1 : 0;
+        const int g_incl = scan_incl_i32(gsize, lane) + g_carry;
+        g_carry = lane_i(g_incl, kWave - 1);
+        c.we = (uint32_t)(g_incl - gsize);
+    }
+    *pool_cells = size_carry;
+}
+
 // First backward row of the longest run of rows ending at row t_end that
 // fits a backward-row pool of cap cells (rows band-packed in order).  Lane
 // t-1 holds the pool offset of row t, so the cells of rows t..t_end are
@@ -1039,13 +1182,25 @@ __device__ __forceinline__ int g_window_lo(const ChainRegs &cr, int lane, int t_
     const uint64_t b = __ballot(fits);
     return b ? __builtin_ctzll(b) + 1 : t_end;
 }
+__device__ __forceinline__ int g_window_lo(const ChainRegsLong &cr, int lane, int t_end, int cap)
+{
+    const int end = gpool_off(cr, t_end) + (rband_hi(cr, t_end) - rband_lo(cr, t_end) + 1);
+    int first = t_end;
+#pragma unroll
+    for (int i = kLongSets - 1; i >= 0; --i) {  // the lowest set with a fitting row wins
+        const int t = 64 * i + lane + 1;
+        const uint64_t b = __ballot(t <= t_end && end - (int)cr.s[i].we <= cap);
+        if (b) first = 64 * i + __builtin_ctzll(b) + 1;
+    }
+    return first;
+}
 
 // Backward rows 1..t_end into the backward-row pool: rows from t_lo on at
 // their band-packed offsets less that of t_lo, the rows before t_lo in place
 // at the pool's start (a row reads its previous row completely before it
 // writes: every row pass has a barrier between the two).
-template <typename K>
-__device__ __forceinline__ void g_rows(const E2Tables &tb, const ChainRegs &cr, int r, int t_end,
+template <typename K, class CR>
+__device__ __forceinline__ void g_rows(const E2Tables &tb, const CR &cr, int r, int t_end,
                                        int t_lo, lds_t<K> *gp, PS<K> *ps, int lane, int N)
 {
     const int base = gpool_off(cr, t_lo);
@@ -1071,8 +1226,8 @@ __device__ __forceinline__ void g_rows(const E2Tables &tb, const ChainRegs &cr, 
 // row it needs.  When the sweep runs through every master and the chosen
 // one's previous forward row is no longer in the buffer, the forward rows
 // up to it are computed again.
-template <typename K>
-__device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs &cr, int r, int m,
+template <typename K, class CR>
+__device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const CR &cr, int r, int m,
                           int lane, uint64_t *T_out, int *mu_out, uint8_t *start, uint8_t *last_tb)
 {
     const int N = tb.N, M = tb.M;
@@ -1093,7 +1248,7 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         set_prev(g, gp + (gpool_off(cr, m - 1) - gpool_off(cr, g_lo)), rband_lo(cr, m - 1),
                  rband_hi(cr, m - 1));
         g.lo = g.hi = N - 1;
-        g.lmin = uni(tb.minwinR[(size_t)f8(lane_w(cr.wd, m - 1), 0) * N + (N - 1)]);
+        g.lmin = uni(tb.minwinR[(size_t)f8(cr.D(m - 1), 0) * N + (N - 1)]);
         row_pass(g, store_to<K>(F, nullptr), ps, lane, N);
         tn = uni_k(F[0]);
         if (tn == KeyT<K>::inf) {
@@ -1129,7 +1284,7 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
                 ro.G = gp + (gpool_off(cr, t) - gpool_off(cr, g_lo));
                 ro.glo = rband_lo(cr, t);
                 ro.ghi = rband_hi(cr, t);
-                ro.tau_next = to_k<K>(lane_u64(cr.tau, mu));  // link mu -> mu+1
+                ro.tau_next = to_k<K>(cr.TAU(mu));  // link mu -> mu+1
             }
             acc = kmin(acc, row_pass(rw, ro, ps, lane, N));
             key = wave_min_k(acc);
@@ -1169,7 +1324,7 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         // row m-1 of the chosen table (F_{m-1} when mu* = m: the sweep's last row)
         set_prev(rw, F, band_lo(cr, m - 1), band_hi(cr, m - 1));
         rw.lo = rw.hi = N - 1;
-        rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + f8(lane_w(cr.wa, m - 1), 0)) * N + (N - 1)];
+        rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + f8(cr.A(m - 1), 0)) * N + (N - 1)];
         rw.lmin = uni(rw.lmin);
         row_pass(rw, store_to<K>(F, last_tb), ps, lane, N);
         // the split points may sit in global memory (long bands): complete
@@ -1280,16 +1435,19 @@ __device__ __forceinline__ int build_chain(const E2Genomes &gen, int p, int q, i
 // N+1 keys and the split-point bytes of the forward rows; the forward and
 // backward row pools live in a per-wave global region (2 pool_cells u64).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_dp(E2Tables tb, int k_max, int pool_cells,
-                                           E2Genomes gen, const uint8_t *__restrict__ roles,
-                                           int n_r, uint32_t *counters, const uint32_t *__restrict__ list,
-                                           size_t seg_cap, uint8_t *tb_global, uint64_t *T,
-                                           uint64_t *Lambda, int16_t *master, uint8_t *layers)
+template <bool L> struct CRSel { using T = ChainRegs; };
+template <> struct CRSel<true> { using T = ChainRegsLong; };
+
+template <bool LONG>
+__device__ __forceinline__ void dp_jobs(const E2Tables &tb, int k_max, int pool_cells,
+                                        const E2Genomes &gen, const uint8_t *__restrict__ roles,
+                                        int n_r, uint32_t *counters,
+                                        const uint32_t *__restrict__ list, size_t seg_cap,
+                                        uint8_t *tb_global, uint64_t *T, uint64_t *Lambda,
+                                        int16_t *master, uint8_t *layers, uint64_t *dyn,
+                                        uint8_t *chain, uint8_t *start, uint8_t *last_tb_p)
 {
-    extern __shared__ uint64_t dyn[];
-    __shared__ uint8_t chain[256];
-    __shared__ uint8_t start[256];
-    __shared__ uint8_t last_tb;
+    uint8_t &last_tb = *last_tb_p;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
     // LDS: split-point pairs, then the banded path's backward-row pool (the
@@ -1305,9 +1463,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     sm.gpool = nullptr;
     sm.pool_cells = pool_cells;
     static_assert(kClasses == 4, "job mapping below assumes four classes");
-    const uint32_t n0 = counters[0], n1 = counters[kCounterStride],
-                   n2 = counters[2 * kCounterStride], n3 = counters[3 * kCounterStride];
-    const uint32_t n_jobs = n0 + n1 + n2 + n3;
+    const uint32_t n0 = LONG ? 0 : counters[0], n1 = LONG ? 0 : counters[kCounterStride],
+                   n2 = LONG ? 0 : counters[2 * kCounterStride],
+                   n3 = LONG ? 0 : counters[3 * kCounterStride];
+    // the long-chain kernel takes segment kClasses alone, one job at a time
+    const uint32_t n_jobs = LONG ? counters[kClasses * kCounterStride] : n0 + n1 + n2 + n3;
+    const int job_ctr = (LONG ? kLongJobCounter : kJobCounter) * kCounterStride;
 
     // The list runs longest chains first.  Its first part is split statically
     // (wave w of W takes problems w, w + W, w + 2W, ...: every wave gets a
@@ -1317,26 +1478,29 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
     // times.  (With few problems per wave the waves would all reach the
     // counter at once; the whole list is then split statically.)
     const bool dyn_tail = n_jobs >= kDynTailMinPerWave * gridDim.x;
-    const uint32_t n_static = dyn_tail ? n_jobs - (n_jobs >> kDynTailShift) : n_jobs;
+    const uint32_t n_static =
+        LONG ? 0u : (dyn_tail ? n_jobs - (n_jobs >> kDynTailShift) : n_jobs);
     auto take = [&](uint32_t done) -> uint32_t {
         if (done + gridDim.x < n_static) return done + gridDim.x;
         uint32_t v = 0;
-        if (lane == 0) v = atomicAdd(&counters[kClasses * kCounterStride], 1u);
+        if (lane == 0) v = atomicAdd(&counters[job_ctr], 1u);
         return n_static + (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
     };
     uint32_t first = blockIdx.x;
     if (first >= n_static) {
         uint32_t v = 0;
-        if (lane == 0) v = atomicAdd(&counters[kClasses * kCounterStride], 1u);
+        if (lane == 0) v = atomicAdd(&counters[job_ctr], 1u);
         first = n_static + (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
     }
     for (uint32_t job = first; job < n_jobs; job = take(job)) {
         uint32_t idx = job;
         // classes in order, longest chains first
-        int cls = 0;
-        if (idx >= n0) { idx -= n0; cls = 1;
-            if (idx >= n1) { idx -= n1; cls = 2;
-                if (idx >= n2) { idx -= n2; cls = 3; } } }
+        int cls = LONG ? kClasses : 0;
+        if (!LONG) {
+            if (idx >= n0) { idx -= n0; cls = 1;
+                if (idx >= n1) { idx -= n1; cls = 2;
+                    if (idx >= n2) { idx -= n2; cls = 3; } } }
+        }
         const uint32_t code = list[(size_t)cls * seg_cap + idx];
         const int p = n_r > 0 ? (int)(code >> 12) : (int)(code >> 8);
         const int q = n_r > 0 ? (int)((code >> 4) & 0xFF) : (int)(code & 0xFF);
@@ -1350,10 +1514,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
 
         uint64_t best = E2_INF64;
         int best_mu = 0;
-        ChainRegs cr;
+        typename CRSel<LONG>::T cr;
         uint64_t bound = E2_INF64, bound_tot = E2_INF64;
         int pool_need = 0;
-        bool banded = chain_regs(tv, sm, r, chain, m, lane, cr, &bound, &bound_tot, &pool_need);
+        bool banded;
+        if constexpr (LONG) {
+            chain_regs_long(tv, r, chain, m, lane, cr, &bound, &bound_tot, &pool_need);
+            banded = true;
+        } else {
+            banded = chain_regs(tv, sm, r, chain, m, lane, cr, &bound, &bound_tot, &pool_need);
+        }
         // split points of bands beyond the LDS copy go to the global table
         DpSmem smb = sm;
         if (pool_need > kLdsTbCells) {
@@ -1427,6 +1597,35 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_
         }
         __syncthreads();
     }
+}
+
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(5))) void k_dp(
+    E2Tables tb, int k_max, int pool_cells, E2Genomes gen, const uint8_t *__restrict__ roles,
+    int n_r, uint32_t *counters, const uint32_t *__restrict__ list, size_t seg_cap,
+    uint8_t *tb_global, uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    extern __shared__ uint64_t dyn[];
+    __shared__ uint8_t chain[256];
+    __shared__ uint8_t start[256];
+    __shared__ uint8_t last_tb;
+    dp_jobs<false>(tb, k_max, pool_cells, gen, roles, n_r, counters, list, seg_cap, tb_global, T,
+                   Lambda, master, layers, dyn, chain, start, &last_tb);
+}
+
+// Chains of more than 64 devices (the list's last segment): the same banded
+// path with the per-position table four positions per lane.  A kernel of its
+// own, so that its larger register table leaves k_dp's occupancy alone.
+__global__ __launch_bounds__(64) void k_dp_long(
+    E2Tables tb, int k_max, int pool_cells, E2Genomes gen, const uint8_t *__restrict__ roles,
+    int n_r, uint32_t *counters, const uint32_t *__restrict__ list, size_t seg_cap,
+    uint8_t *tb_global, uint64_t *T, uint64_t *Lambda, int16_t *master, uint8_t *layers)
+{
+    extern __shared__ uint64_t dyn[];
+    __shared__ uint8_t chain[256];
+    __shared__ uint8_t start[256];
+    __shared__ uint8_t last_tb;
+    dp_jobs<true>(tb, k_max, pool_cells, gen, roles, n_r, counters, list, seg_cap, tb_global, T,
+                  Lambda, master, layers, dyn, chain, start, &last_tb);
 }
 
 // ---------------------------------------------------------------------------
@@ -1737,7 +1936,7 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     // waves take the next listed problem from a shared counter: these grids
     // need not be resident at once, and their problems vary more in cost
     for (;;) {
-        if (lane == 0) job = atomicAdd(&counters[kClasses * kCounterStride], 1u);
+        if (lane == 0) job = atomicAdd(&counters[kJobCounter * kCounterStride], 1u);
         __syncthreads();
         uint32_t idx = job;
         __syncthreads();
@@ -2026,7 +2225,7 @@ __global__ __launch_bounds__(64) void k_dp_idle(E2Tables tb, int k_max, E2Genome
     // waves take the next listed problem from a shared counter: these grids
     // need not be resident at once, and their problems vary more in cost
     for (;;) {
-        if (lane == 0) job = atomicAdd(&counters[kClasses * kCounterStride], 1u);
+        if (lane == 0) job = atomicAdd(&counters[kJobCounter * kCounterStride], 1u);
         __syncthreads();
         uint32_t idx = job;
         __syncthreads();
@@ -2851,9 +3050,14 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
     const int n_r = roles ? 0 : t.R;
     const size_t seg = (size_t)P * k_max * (n_r ? n_r : 1);
     k_init<<<1, 64, 0, s>>>(wk.counters);
+    // Chains longer than the one-register table go to the long-chain kernel
+    // when they are plausible: more devices than that, at least 16 per
+    // cluster id on average.  Otherwise (no launch to pay for) the rare long
+    // chain takes k_dp's reference path; the results are the same.
+    const bool long_seg = objective == 0 && t.M > kMaxBandedChain && t.M >= 16 * k_max;
     k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, roles, n_r,
-                                                       objective == 2, wk.counters, wk.list, seg,
-                                                       T, Lambda, master, layers);
+                                                       objective == 2, long_seg, wk.counters,
+                                                       wk.list, seg, T, Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
     if (objective == 2)
@@ -2866,10 +3070,16 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
                                                              wk.counters, wk.list, seg, wk.rows,
                                                              wk.tb_global, T, Lambda, master,
                                                              layers);
-    else
+    else {
         k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles, n_r,
                                                           wk.counters, wk.list, seg, wk.tb_global,
                                                           T, Lambda, master, layers);
+        // the long chains, if any (each wave exits at once when there are none)
+        if (long_seg)
+            k_dp_long<<<wk.n_slots < 256 ? wk.n_slots : 256, 64, e2_dp_lds_bytes(t.N), s>>>(
+                t, k_max, pool, gen, roles, n_r, wk.counters, wk.list, seg, wk.tb_global, T,
+                Lambda, master, layers);
+    }
     if (wk.ev_end) (void)hipEventRecord(wk.ev_end, s);
     return hipGetLastError();
 }

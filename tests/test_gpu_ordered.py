@@ -260,3 +260,18 @@ def test_ordered_empty_population_and_bad_arguments(torch_dev):
     rc = e2.lib().e2_solve_partitions_ordered(ctx.handle, None, 1, 2, None, ctypes.c_void_p(
         S.data_ptr()), ctypes.c_void_p(R.data_ptr()), None, None, None, None)
     assert rc == e2.E2_EINVAL
+
+
+def test_ordered_replicas_past_64_devices(torch_dev):
+    """Replicas of 70 to 150 devices along the ordering (the long-chain
+    kernel) equal the oracle."""
+    M, N = 256, 160
+    wl = workload.random_small(2901, M=M, N=N, P=2, k_max=3, mem_lo_layers=2, mem_hi_layers=6)
+    rng = np.random.default_rng(29)
+    order = np.stack([rng.permutation(M) for _ in range(2)]).astype(np.uint8)
+    sizes = np.array([[70, 150, 36], [100, 90, 66]], dtype=np.uint16)
+    roles = np.array([[0, 1, 0], [1, 0, 1]], dtype=np.uint8)
+    print("ordered long replicas", flush=True)
+    want = oracle.eval_population_ordered(wl, order, sizes, roles)
+    assert (want["T"] != INF).any()
+    _assert_equal(_gpu_eval(torch_dev, wl, order, sizes, roles), want, tag="long replicas")

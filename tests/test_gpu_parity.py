@@ -415,3 +415,35 @@ def test_genome_ranges_merge_to_the_whole_population(torch_dev, kind):
     parts = [run(a, b) for a, b in zip(cuts[:-1], cuts[1:])]
     for k in whole:
         assert np.array_equal(np.concatenate([p[k] for p in parts]), whole[k]), k
+
+
+@pytest.mark.parametrize("M,N,k_max,P", [(65, 80, 1, 2), (130, 200, 2, 2), (200, 255, 1, 1),
+                                         (255, 255, 1, 1), (256, 126, 3, 2)])
+def test_chains_past_64_devices(torch_dev, M, N, k_max, P):
+    """Chains of 65 to 255 devices take the long-chain kernel (the banded
+    path with four positions per lane) and equal the oracle on every
+    output; roomy devices so that they are feasible."""
+    print(f"long chains M={M} N={N} k_max={k_max}", flush=True)
+    wl = workload.random_small(1300 + M + N, M=M, N=N, P=P, k_max=k_max,
+                               mem_lo_layers=max(1.0, 3.0 * N / M), mem_hi_layers=max(4.0, 8.0 * N / M),
+                               zero_bw_frac=0.0)
+    want = _oracle_all(wl)
+    chains = [int((wl.labels[p] == q).sum()) for p in range(P) for q in range(k_max)]
+    assert max(chains) > 64 and (want["T"] != INF).any(), (chains, want["T"])
+    _assert_equal(_gpu_all(torch_dev, wl), want, tag=f"long M{M} N{N}")
+
+
+def test_long_chain_among_many_cluster_ids_takes_the_reference_path(torch_dev):
+    """With fewer than 16 devices per cluster id on average the long-chain
+    kernel is not launched; a 70-device chain then takes k_dp's reference
+    path, with the same results."""
+    M, N, k_max = 100, 90, 7
+    wl = workload.random_small(1777, M=M, N=N, P=2, k_max=k_max, mem_lo_layers=2,
+                               mem_hi_layers=10)
+    rng = np.random.default_rng(17)
+    labels = rng.integers(1, k_max, size=(2, M)).astype(np.uint8)
+    for p in range(2):
+        labels[p, rng.choice(M, 70, replace=False)] = 0          # one 70-device chain
+    want = _oracle_all(wl, labels=labels)
+    assert (want["T"][:, 0] != INF).any()
+    _assert_equal(_gpu_all(torch_dev, wl, labels=labels), want, tag="reference long")

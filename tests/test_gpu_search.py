@@ -251,3 +251,16 @@ def test_fitness_rate_sums_past_2_53(torch_dev):
     torch.cuda.synchronize()
     for k in ("w", "phase", "s_p", "s_d"):
         assert (e2.u64(fit[k]) == want[k]).all(), k
+
+
+def test_search_with_chains_past_64_devices(torch_dev):
+    """The role and slot search (every role index of every cluster) on
+    clusters of about 70-130 devices: the long-chain kernel in search mode."""
+    wl = workload.random_small(4401, M=256, N=140, P=2, k_max=3, mem_lo_layers=2,
+                               mem_hi_layers=8)
+    wl.min_tps_milli = 0
+    sm = dict(b_max=3, beta_ppm=125_000, kv_bytes_per_block_slot=10**6)
+    print("search long chains", flush=True)
+    want = oracle.search_roles(wl, sm)
+    assert (want["T_all"] != INF).any()
+    _assert_equal(_gpu_search(torch_dev, wl, sm), want, tag="long search")
