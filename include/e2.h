@@ -231,9 +231,9 @@ int e2_eval_population(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
  * DP waves' split-point tables when chains can outgrow their LDS copy) is
  * carved from one fixed 96 MiB device array that the library holds on each
  * GPU it runs on until the process ends.
- *   Limit: P * k_max * 32 bytes plus, when min(M, N) - 1 rows of N split
+ *   Limit: P * k_max * 36 bytes plus, when min(M, N) - 1 rows of N split
  *   points exceed 2048 bytes, one DP wave's N * N-byte table must fit in
- *   96 MiB (P * k_max up to about 3.1 million at N = 126); larger inputs
+ *   96 MiB (P * k_max up to about 2.8 million at N = 126); larger inputs
  *   return E2_EINVAL before anything is enqueued.  When the tables of all
  *   of e2_eval_population's DP waves do not fit, fewer waves run (same
  *   results, slower).
