@@ -78,3 +78,38 @@ def test_noalloc_rejects_inputs_beyond_its_scratch(torch_dev):
     out = e2.e2_eval_population(ctx, L, R, wl.fitness_params())
     torch.cuda.synchronize()
     assert out["w"].shape[0] == wl.population
+
+
+def test_noalloc_replays_from_a_captured_graph(torch_dev):
+    """The allocation-free evaluation captured in a HIP graph (torch's
+    capture of the current stream): each replay, after a different
+    population is copied into the captured input buffers and with eager
+    library calls and synchronisations between replays, equals the eager
+    e2_eval_population on that population."""
+    torch, dev = torch_dev
+    wl = workload.make("c3_64dev_80L")
+    P = wl.population
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    fp = wl.fitness_params()
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    out = {k: torch.empty(P, dtype=torch.int64, device=dev) for k in ("w", "phase", "s_p", "s_d")}
+    e2.e2_eval_population(ctx, L, R, fp, objective="noalloc", out=out)  # set-up outside capture
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        e2.e2_eval_population(ctx, L, R, fp, objective="noalloc", out=out)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(11)
+    for it in range(4):
+        perm = rng.permutation(P)
+        L.copy_(torch.from_numpy(np.ascontiguousarray(wl.labels[perm])).to(dev))
+        R.copy_(torch.from_numpy(np.ascontiguousarray(wl.roles[perm])).to(dev))
+        torch.cuda.synchronize()
+        print(f"graph replay {it}", flush=True)
+        graph.replay()
+        torch.cuda.synchronize()
+        got = {k: e2.u64(v).copy() for k, v in out.items()}
+        want = e2.e2_eval_population(ctx, L, R, fp)   # eager, allocating entry point
+        torch.cuda.synchronize()
+        _check(got, {k: e2.u64(v) for k, v in want.items()}, f"replay {it}")
