@@ -9,7 +9,10 @@ mutation 1/256 for label genomes, the App. A operators for two-chromosome
 genomes) runs on the GPU; every one of its 50 GA steps is compared in full
 with the oracle's GA fed the same population and fitness keys, every
 generation's evaluation is checked on 256 sampled genomes, and the last
-generation's on every genome.
+generation's on every genome.  Algorithm 2's own generation (the role and
+slot search, then the GA from the searched roles and keys) runs for 50
+generations of both genome kinds, every GA step compared in full and each
+generation's search on 96 sampled genomes.
 
 The oracle runs over genome ranges in worker processes (oracle.pool), which
 the GPU results never feed: the oracle sees the population only.
@@ -195,4 +198,80 @@ def test_fifty_generations_256_devices(torch_dev, kind):
     # generation 0's (one elite is kept every step)
     k0 = min(zip(fits[0]["w"].tolist(), fits[0]["phase"].tolist()))
     k1 = min(zip(fits[last]["w"].tolist(), fits[last]["phase"].tolist()))
+    assert k1 <= k0
+
+
+SEARCH_GENERATIONS = 50
+SEARCH_SAMPLE = 96
+
+
+@pytest.mark.parametrize("kind", ["labels", "two_chromosome"])
+def test_search_and_breed_fifty_generations_256_devices(torch_dev, kind):
+    """Algorithm 2's generation as the paper runs it on the 256-device
+    workload: the role and slot search scores every genome (a DP per cluster
+    for prefill and each of 1..8 decode requests in flight, the kept slot
+    count, brute-force roles), then the GA breeds from the searched roles and
+    keys.  Fifty generations on the GPU; every GA step equals the oracle's GA
+    fed the same population, searched roles and keys, and each generation's
+    search equals the oracle's on 96 sampled genomes (every DP result, role,
+    slot count and key)."""
+    torch, dev = torch_dev
+    t0 = time.perf_counter()
+    wl = workload.make("c5_256dev_126L_ga")
+    sm = workload.slot_model(wl)
+    ctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
+    fp = wl.fitness_params()
+    op = workload.ordered_population(wl)
+    if kind == "labels":
+        cur = [torch.from_numpy(x).to(dev) for x in (wl.labels, wl.roles)]
+    else:
+        cur = [torch.from_numpy(x).to(dev) for x in (op.order, op.sizes)]
+    rng = np.random.default_rng(2607)
+    pops, searched = [], []
+    for g in range(SEARCH_GENERATIONS):
+        if kind == "labels":
+            res = e2.e2_search_roles(ctx, cur[0], fp, wl.k_max, with_tables=True)
+            nxt = e2.e2_ga_step(ctx, cur[0], res["roles"], res["w"], res["phase"],
+                                wl.ga_params(g))
+        else:
+            res = e2.e2_search_roles_ordered(ctx, cur[0], cur[1], fp, with_tables=True)
+            nxt = e2.e2_ga_step_ordered(ctx, cur[0], cur[1], res["roles"], res["w"],
+                                        res["phase"], op.ga_params(wl, g))
+        torch.cuda.synchronize()
+        pick = np.sort(rng.choice(wl.population, SEARCH_SAMPLE, replace=False))
+        idx = torch.from_numpy(pick).to(dev)
+        searched.append(dict(pick=pick, roles=res["roles"].cpu().numpy(),
+                             w=e2.u64(res["w"]), phase=e2.u64(res["phase"]),
+                             slots=res["slots"].index_select(0, idx).cpu().numpy(),
+                             T_all=e2.u64(res["T_all"].index_select(0, idx)),
+                             Lambda_all=e2.u64(res["Lambda_all"].index_select(0, idx))))
+        pops.append([x.cpu().numpy() for x in cur])
+        cur = list(nxt)
+    pops.append([x.cpu().numpy() for x in cur])
+    _say(f"{kind}: {SEARCH_GENERATIONS} search + GA generations on the GPU in "
+         f"{time.perf_counter() - t0:.1f} s")
+    for g in range(SEARCH_GENERATIONS):
+        s = searched[g]
+        if kind == "labels":
+            want = oracle.ga_step(pops[g][0], s["roles"], s["w"], s["phase"], wl.k_max,
+                                  **wl.ga_params(g))
+        else:
+            want = oracle.ga_step_ordered(pops[g][0], pops[g][1], s["roles"], s["w"],
+                                          s["phase"], **op.ga_params(wl, g))
+        for a, b in zip(pops[g + 1], want):
+            assert np.array_equal(a, b), f"{kind} GA step {g}"
+        p = s["pick"]
+        if kind == "labels":
+            ref = pool.search_roles(wl, sm, pops[g][0][p])
+        else:
+            ref = pool.search_roles_ordered(wl, sm, pops[g][0][p], pops[g][1][p])
+        got = dict(T_all=s["T_all"], Lambda_all=s["Lambda_all"], roles=s["roles"][p],
+                   slots=s["slots"], w=s["w"][p], phase=s["phase"][p])
+        for k in pool.SEARCH_KEYS:
+            bad = np.argwhere(np.asarray(got[k] != ref[k]).reshape(len(p), -1).any(axis=1))
+            assert bad.size == 0, f"{kind} generation {g} {k}: {bad.size} genomes differ"
+        _say(f"{kind}: generation {g} GA step and {len(p)} searched genomes equal")
+    # the search improves on generation 0's best key (elites are kept)
+    k0 = min(zip(searched[0]["w"].tolist(), searched[0]["phase"].tolist()))
+    k1 = min(zip(searched[-1]["w"].tolist(), searched[-1]["phase"].tolist()))
     assert k1 <= k0

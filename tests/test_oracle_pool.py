@@ -32,3 +32,17 @@ def test_ranges_equal_one_call_ordered():
 def test_worker_count_is_bounded():
     assert 1 <= pool.workers() <= 16
     assert pool.workers(limit=1) == 1
+
+
+def test_search_ranges_equal_one_call():
+    wl = workload.make("c2_32dev_48L")
+    sm = workload.slot_model(wl)
+    want = oracle.search_roles(wl, sm)
+    got = pool.search_roles(wl, sm, wl.labels, n_workers=3)
+    for k in pool.SEARCH_KEYS:
+        assert np.array_equal(got[k], want[k]), k
+    op = workload.ordered_population(wl)
+    want = oracle.search_roles_ordered(wl, sm, op.order, op.sizes)
+    got = pool.search_roles_ordered(wl, sm, op.order, op.sizes, n_workers=2)
+    for k in pool.SEARCH_KEYS:
+        assert np.array_equal(got[k], want[k]), k
