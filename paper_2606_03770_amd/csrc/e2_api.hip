@@ -166,13 +166,6 @@ int alloc_scratch(Scratch &sc, hipStream_t s, size_t bytes)
     return E2_OK;
 }
 
-// Per-wave global row pools: only the finishing-time kernel keeps its rows
-// in global memory (the bottleneck kernel keeps them in LDS).
-size_t row_bytes(const e2_ctx *ctx, int slots, int objective)
-{
-    return objective == 1 ? align256((size_t)slots * e2_dp_row_words(ctx->N) * 8) : 0;
-}
-
 // Lay out counters, the problem list and the split-point fallback.
 size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_bytes,
                   int n_r = 1, int objective = 0)
@@ -186,8 +179,8 @@ size_t work_bytes(const e2_ctx *ctx, int P, int k_max, int *slots, size_t *tb_by
     const bool need_tb = (size_t)(mcap - 1) * ctx->N > (size_t)e2_dp_lds_tb_cells(ctx->N);
     *tb_bytes = need_tb ? (size_t)(*slots) * ctx->N * ctx->N : 0;
     const size_t idle = objective == 2 ? (size_t)(*slots) * e2_dp_idle_bytes(ctx->M, ctx->N) : 0;
-    return kCounterBytes + align256(problems * 4 * kListSegs) + row_bytes(ctx, *slots, objective) +
-           align256(*tb_bytes) + align256(idle);
+    return kCounterBytes + align256(problems * 4 * kListSegs) + align256(*tb_bytes) +
+           align256(idle);
 }
 
 void carve_work(void *base, e2_ctx *ctx, int P, int k_max, int slots, size_t tb_bytes,
@@ -198,8 +191,6 @@ void carve_work(void *base, e2_ctx *ctx, int P, int k_max, int slots, size_t tb_
     p += kCounterBytes;
     wk->list = reinterpret_cast<uint32_t *>(p);  // kListSegs segments of P * k_max * n_r
     p += align256((size_t)P * k_max * n_r * 4 * kListSegs);
-    wk->rows = objective == 1 ? reinterpret_cast<uint64_t *>(p) : nullptr;
-    p += row_bytes(ctx, slots, objective);
     wk->tb_global = tb_bytes ? reinterpret_cast<uint8_t *>(p) : nullptr;
     p += align256(tb_bytes);
     wk->idle_stride = objective == 2 ? e2_dp_idle_bytes(ctx->M, ctx->N) : 0;
@@ -870,7 +861,7 @@ int e2_eval_population_noalloc(e2_ctx *ctx, void *stream, int32_t P, int32_t k_m
     E2Work wk;
     carve_work(base, ctx, P, k_max, slots, tbb, &wk);
     char *after = static_cast<char *>(base) + kCounterBytes + align256(problems * 4 * kListSegs) +
-                  row_bytes(ctx, slots, 0) + align256(tbb);
+                  align256(tbb);
     uint64_t *Ts = reinterpret_cast<uint64_t *>(after);
     uint64_t *Ls = reinterpret_cast<uint64_t *>(after + tl);
     hipStream_t s = as_stream(stream);

@@ -70,7 +70,6 @@ struct E2Work {
     uint32_t *counters;  // [c * kCounterStride], one 256-byte line each (see kCounters)
     uint32_t *list;      // [kListSegs][P * k_max * n_r] problems needing the DP: (p << 8) | q, or
                          //   with every role index searched (p << 12) | (q << 4) | r
-    uint64_t *rows;      // [n_slots][2 pool] per-wave rows of the finishing-time kernel, or null
     uint8_t *tb_global;  // [n_slots][N][N] split-point table fallback, or null
     int n_slots;         // waves of the DP kernel
     uint8_t *idle;       // idle-device relaxation: per wave, rows E [M][N+1] u64, their
@@ -81,14 +80,11 @@ struct E2Work {
 
 // Number of DP waves launched for at most `problems` problems of N blocks.
 int e2_dp_slots(int N, int problems);
-// Cells of one DP wave's forward-row pool (its backward-row pool is as
-// large), its global row storage (u64 per wave: both pools) and its dynamic
-// LDS bytes.
+// Largest band total of a chain the one-register table takes, the LDS copy
+// of the split points (bytes) and the DP kernels' dynamic LDS bytes.
 int e2_dp_pool_cells(int N);
 int e2_dp_lds_tb_cells(int N);
-size_t e2_dp_row_words(int N);
 size_t e2_dp_lds_bytes(int N);
-size_t e2_dp_ft_lds_bytes(int N);  // the finishing-time kernel's dynamic LDS
 // Waves and per-wave bytes of the idle-device relaxation's DP kernel.
 int e2_dp_idle_slots(int problems, int M, int N);
 size_t e2_dp_idle_bytes(int M, int N);

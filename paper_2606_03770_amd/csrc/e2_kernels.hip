@@ -945,8 +945,6 @@ struct DpSmem {
     lds_t<uint64_t> *Rw1;
     uint8_t *tbp;    // split points of the forward rows, band-packed (LDS)
     lds_t<char> *pool_end; // end of the backward-row pool (k_dp)
-    uint64_t *pool;  // band-packed forward row values (global, per wave; k_dp_ft)
-    uint64_t *gpool; // band-packed backward row values (global, per wave; k_dp_ft)
     int pool_cells;
 };
 
@@ -1459,8 +1457,6 @@ __device__ __forceinline__ void dp_jobs(const E2Tables &tb, int k_max, int pool_
     sm.pool_end = (lds_t<char> *)(dyn + 2 * N + (N + 1)) + dp_lds_extra(N);
     sm.Rw0 = (lds_t<uint64_t> *)sm.pool_end;
     sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N + 2 * (N + 1)) + dp_lds_extra(N);
-    sm.pool = nullptr;
-    sm.gpool = nullptr;
     sm.pool_cells = pool_cells;
     static_assert(kClasses == 4, "job mapping below assumes four classes");
     const uint32_t n0 = LONG ? 0 : counters[0], n1 = LONG ? 0 : counters[kCounterStride],
@@ -1693,10 +1689,11 @@ __device__ uint64_t ft_table(const E2Tables &tb, const DpSmem &sm, int r, const 
 // staged in LDS first (st, N entries), so that a candidate is one LDS read:
 // a(j) + (P[i+1] + hadd + tau - P[N]) is the candidate exactly in modular
 // u64 arithmetic.
-__device__ __forceinline__ void ft_row(const uint64_t *pr, const uint8_t *wr, uint64_t hadd,
-                                       uint64_t tau, int lo, int hi, int kmin,
-                                       const uint64_t *prev, int plo, int phi, uint64_t *out,
-                                       uint8_t *tbs, lds_t<uint64_t> *st, int N, int lane)
+__device__ __forceinline__ void ft_row_plain(const uint64_t *pr, const uint8_t *wr,
+                                             uint64_t hadd, uint64_t tau, int lo, int hi,
+                                             int kmin, const lds_t<uint64_t> *prev, int plo,
+                                             int phi, lds_t<uint64_t> *out, uint8_t *tbs,
+                                             lds_t<uint64_t> *st, int N, int lane)
 {
     const uint64_t pN = pr[N];
     const bool linked = prev && tau != E2_INF64;
@@ -1753,56 +1750,153 @@ __device__ __forceinline__ void ft_row(const uint64_t *pr, const uint8_t *wr, ui
         out[i - lo] = best;
         if (tbs) tbs[i - lo] = (uint8_t)bj;
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __threadfence_block();
+    // rows live in LDS (the next row reads this one after the barrier); the
+    // split points may be global and are waited for once, before the back
+    // tracing
     __syncthreads();
 }
 
+// The same row with S lanes per cell.  A staged term is packed as a key
+// (a(j) << 8) | j, so one unsigned min keeps the least a(j) and, among equal
+// ones, the smallest j: the strict ascending scan above.  Lane o of a cell
+// scans j = i - o, i - o - S, ... down to the window start; the S partial
+// minima meet through DPP quad permutations (and a half-row mirror for
+// S = 8).  Used when every a(j) of the problem is below 2^56.
+template <int S>
+__device__ __forceinline__ void ft_row_keyed_s(const uint64_t *pr, const uint8_t *wr,
+                                               uint64_t hadd, uint64_t tau, int lo, int hi,
+                                               int kmin, const lds_t<uint64_t> *prev, int plo,
+                                               int phi, lds_t<uint64_t> *out, uint8_t *tbs,
+                                               lds_t<uint64_t> *st, int N, int lane)
+{
+    constexpr int CPP = kWave / S;  // cells per pass
+    const int o = lane % S;
+    const int cl = lane / S;
+    // the first pass's cell loads go out before the terms are staged
+    int w_nx;
+    uint64_t p_nx;  // P[i+1]
+    {
+        const int i = min(lo + cl, hi);
+        w_nx = wr[i];
+        p_nx = pr[i + 1];
+    }
+    const uint64_t pN = pr[N];
+    for (int j = kmin + lane; j <= hi; j += kWave) {
+        const int x = j - 1;
+        uint64_t key = E2_INF64;
+        if (x >= plo && x <= phi) {
+            const uint64_t pv = prev[x - plo];
+            if (pv != E2_INF64) key = ((pv + (pN - pr[j])) << 8) | (uint64_t)j;
+        }
+        st[j] = key;
+    }
+    __syncthreads();
+    for (int base = lo; base <= hi; base += CPP) {
+        const int i = min(base + cl, hi);  // lanes past the row repeat its last cell
+        const int w = w_nx;
+        const uint64_t p1 = p_nx;
+        if (base + CPP <= hi) {  // the next pass's loads (uniform)
+            const int in = min(base + CPP + cl, hi);
+            w_nx = wr[in];
+            p_nx = pr[in + 1];
+        }
+        uint64_t best = E2_INF64;
+        if (w != E2_NO_START) {
+            const int jlo = max(w, kmin);
+            int j = i - o;
+            for (; j - S >= jlo; j -= 2 * S) best = umin64(best, umin64(st[j], st[j - S]));
+            if (j >= jlo) best = umin64(best, st[j]);
+        }
+        if (S >= 2) best = umin64(best, dpp_u64<0xb1>(best));
+        if (S >= 4) best = umin64(best, dpp_u64<0x4e>(best));
+        if (S >= 8) best = umin64(best, dpp_u64<0x141>(best));
+        // the cell's value: a(j*) + P[i+1] + head + tau - P[N] (modular sums)
+        const uint64_t v = best == E2_INF64 ? E2_INF64 : (best >> 8) + (p1 + hadd + tau - pN);
+        out[i - lo] = v;
+        if (tbs) tbs[i - lo] = (uint8_t)(best == E2_INF64 ? 0 : (best & 0xFF));
+    }
+    __syncthreads();
+}
+
+// One FT row: the keyed lane-split scan where it applies (a previous row, a
+// finite link, keys that fit), else the one-lane-per-cell scan.
+__device__ __forceinline__ void ft_row(const uint64_t *pr, const uint8_t *wr, uint64_t hadd,
+                                       uint64_t tau, int lo, int hi, int kmin,
+                                       const lds_t<uint64_t> *prev, int plo, int phi,
+                                       lds_t<uint64_t> *out, uint8_t *tbs, lds_t<uint64_t> *st,
+                                       int N, int lane, bool keyed)
+{
+    const int n = hi - lo + 1;
+    if (!keyed || !prev || tau == E2_INF64 || n <= 0) {
+        ft_row_plain(pr, wr, hadd, tau, lo, hi, kmin, prev, plo, phi, out, tbs, st, N, lane);
+        return;
+    }
+    if (n <= 8)
+        ft_row_keyed_s<8>(pr, wr, hadd, tau, lo, hi, kmin, prev, plo, phi, out, tbs, st, N, lane);
+    else if (n <= 16)
+        ft_row_keyed_s<4>(pr, wr, hadd, tau, lo, hi, kmin, prev, plo, phi, out, tbs, st, N, lane);
+    else if (n <= 32)
+        ft_row_keyed_s<2>(pr, wr, hadd, tau, lo, hi, kmin, prev, plo, phi, out, tbs, st, N, lane);
+    else
+        ft_row_keyed_s<1>(pr, wr, hadd, tau, lo, hi, kmin, prev, plo, phi, out, tbs, st, N, lane);
+}
+
+// Backward FT rows 1..t_end into the LDS backward-row pool, as g_rows does
+// for Algorithm 1's rows: rows from t_lo on at their band-packed offsets less
+// that of t_lo, the rows before it in place at the pool's start.
+__device__ __forceinline__ void ft_g_rows(const E2Tables &tb, const ChainRegs &cr, int r, int m,
+                                          int t_end, int t_lo, lds_t<uint64_t> *gp,
+                                          lds_t<uint64_t> *st, int N, int lane, bool keyed)
+{
+    const int base = gpool_off(cr, t_lo);
+    for (int t = 1; t <= t_end; ++t) {
+        const uint32_t wd = cr.D(t - 1);
+        const int c = f8(wd, 0);
+        const uint64_t tau = t >= 2 ? cr.TAU(m + 1 - t) : 0;  // link m+1-t -> m+2-t
+        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, tau, f8(wd, 8), f8(wd, 16),
+               t - 1, t >= 2 ? gp + (t - 1 >= t_lo ? gpool_off(cr, t - 1) - base : 0) : nullptr,
+               t >= 2 ? rband_lo(cr, t - 1) : 1, t >= 2 ? rband_hi(cr, t - 1) : 0,
+               gp + (t >= t_lo ? gpool_off(cr, t) - base : 0), nullptr, st, N, lane, keyed);
+    }
+}
+
 // The finishing-time DP by the same banded decomposition and schedule as
-// dp_banded: reversed rows G_t over the last t devices in the wave's
-// backward-row pool, the head-free optimum T0 from the full reversed
-// table's last cell, then masters in ascending position with
+// dp_banded: reversed rows G_t over the last t devices in the LDS
+// backward-row pool (rows the sweep reaches that the pool did not keep are
+// computed again), the head-free optimum T0 from the full reversed table's
+// last cell, then masters in ascending position with
 //   T_mu = min_i H_mu(i) + tau(mu, mu+1) + G_{m-mu}(N-2-i)
 // (H_mu the master's forward row, head time and bytes, over F_{mu-1}), each
-// followed by the forward row F_mu (no master) in the forward pool.  Since
+// followed by the forward row F_mu (no master), computed in place.  Since
 // T_mu >= T0 + head(mu), the sweep stops once the best is at most T0 plus
 // the least head time of the masters still ahead; the smallest mu with the
-// least T_mu wins.  Rows mu*..m-1 of its table are recomputed with split
-// points and the back tracing fills start[].  Every in-band cell's value
-// equals the full table's (bands depend on memory only), so the result is
-// that of one full table per master.
+// least T_mu wins.  Rows mu*..m of its table are recomputed with split
+// points (F_1..F_{mu*-1} first when the sweep went past them) and the back
+// tracing fills start[].  Every in-band cell's value equals the full
+// table's (bands depend on memory only), so the result is that of one full
+// table per master.
 __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRegs &cr, int r,
-                             int m, int lane, uint64_t *T_out, int *mu_out, uint8_t *start)
+                             int m, int lane, uint64_t *T_out, int *mu_out, uint8_t *start,
+                             bool keyed)
 {
     const int N = tb.N, M = tb.M;
-    uint64_t *pool = sm.pool;
-    uint64_t *gpool = sm.gpool;
-    // the master's row (N cells) in the first LDS row buffer: the final rows,
-    // the only other users of the row buffers, come after the sweep
-    uint64_t *H = (uint64_t *)sm.Rw0;
-    lds_t<uint64_t> *st = (lds_t<uint64_t> *)sm.ps;  // ft_row's staged terms
-    uint64_t *Rw[2] = {(uint64_t *)sm.Rw0, (uint64_t *)sm.Rw1};
-    // ---- backward rows G_1..G_{m-1} in the backward-row pool: reversed row t
-    // is device m+1-t holding reversed blocks y..x after the t-1 devices
-    // behind it
-    for (int t = 1; t < m; ++t) {
-        const uint32_t wd = lane_w(cr.wd, t - 1);
-        const int c = f8(wd, 0);
-        const uint64_t tau = t >= 2 ? lane_u64(cr.tau, m + 1 - t) : 0;  // link m+1-t -> m+2-t
-        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, tau, f8(wd, 8), f8(wd, 16),
-               t - 1, t >= 2 ? gpool + gpool_off(cr, t - 1) : nullptr,
-               t >= 2 ? rband_lo(cr, t - 1) : 1, t >= 2 ? rband_hi(cr, t - 1) : 0,
-               gpool + gpool_off(cr, t), nullptr, st, N, lane);
-    }
+    lds_t<uint64_t> *st = (lds_t<uint64_t> *)sm.ps;  // ft_row's staged terms (N)
+    lds_t<uint64_t> *gp = st + N;                     // backward-row pool
+    const int gcap = (int)((sm.pool_end - (lds_t<char> *)gp) / 8);
+    lds_t<uint64_t> *H = sm.Rw0;  // the master's row
+    lds_t<uint64_t> *F = sm.Rw1;  // forward rows, in place
+    // ---- backward rows G_1..G_{m-1}, the last ones that fit kept in the pool
+    int g_lo = m >= 2 ? g_window_lo(cr, lane, m - 1, gcap) : 1;
+    if (m >= 2) ft_g_rows(tb, cr, r, m, m - 1, g_lo, gp, st, N, lane, keyed);
     // ---- T0, the least end-to-end time with no head anywhere: reversed row
     // m at its last cell.  A master's optimum is at least T0 plus its head
     // time (the head time is added once, its bytes only narrow windows).
     uint64_t t0 = E2_INF64;
     if (m >= 2) {
-        const int c = f8(lane_w(cr.wd, m - 1), 0);
-        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, lane_u64(cr.tau, 1),
-               N - 1, N - 1, m - 1, gpool + gpool_off(cr, m - 1), rband_lo(cr, m - 1),
-               rband_hi(cr, m - 1), H, nullptr, st, N, lane);
+        const int c = f8(cr.D(m - 1), 0);
+        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, cr.TAU(1), N - 1, N - 1,
+               m - 1, gp + (gpool_off(cr, m - 1) - gpool_off(cr, g_lo)), rband_lo(cr, m - 1),
+               rband_hi(cr, m - 1), H, nullptr, st, N, lane, keyed);
         t0 = uni64(H[0]);
         if (t0 == E2_INF64) {
             *T_out = E2_INF64;
@@ -1813,36 +1907,40 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
     // head time of each position able to take the head (INF otherwise)
     const uint64_t h_cap = (lane < m && f8(cr.wa, 16) != 0) ? cr.head : E2_INF64;
 
-    // ---- masters in ascending position, each followed by F_mu (pool, split
-    // points kept for the rows below mu*).  The sweep stops once the best is
-    // at most T0 plus the least head time of the masters still ahead: none
-    // of them can do better, and ties go to the smaller master.
+    // ---- masters in ascending position, each followed by F_mu (split points
+    // kept for the rows below mu*).  The sweep stops once the best is at most
+    // T0 plus the least head time of the masters still ahead: none of them
+    // can do better, and ties go to the smaller master.
     uint64_t best = E2_INF64;
     int best_mu = 0;
+    int f_last = 0;  // the forward row the buffer holds
     for (int mu = 1; mu <= m; ++mu) {
-        const uint32_t wa = lane_w(cr.wa, mu - 1);
+        const uint32_t wa = cr.A(mu - 1);
         const int c = f8(wa, 0);
         if (f8(wa, 16) != 0) {
-            const uint64_t tau = mu >= 2 ? lane_u64(cr.tau, mu - 1) : 0;
+            const int t = m - mu;  // backward row of devices mu+1..m
+            if (mu < m && t < g_lo) {  // not kept: rows 1..t again
+                g_lo = g_window_lo(cr, lane, t, gcap);
+                ft_g_rows(tb, cr, r, m, t, g_lo, gp, st, N, lane, keyed);
+            }
+            const uint64_t tau = mu >= 2 ? cr.TAU(mu - 1) : 0;
             const int lo = band_lo(cr, mu), hi = mu == m ? N - 1 : band_hi(cr, mu);
             const int hlo = mu == m ? N - 1 : lo;
             ft_row(pref_row(tb, r, c), win_row(tb, 1, c), uni64(tb.head[r * M + c]), tau, hlo,
-                   hi, mu - 1, mu >= 2 ? pool + pool_off(cr, mu - 1) : nullptr,
-                   mu >= 2 ? band_lo(cr, mu - 1) : 1, mu >= 2 ? band_hi(cr, mu - 1) : 0, H,
-                   nullptr, st, N, lane);
+                   hi, mu - 1, mu >= 2 ? F : nullptr, mu >= 2 ? band_lo(cr, mu - 1) : 1,
+                   mu >= 2 ? band_hi(cr, mu - 1) : 0, H, nullptr, st, N, lane, keyed);
             uint64_t tm = E2_INF64;
             if (mu == m) {
                 tm = H[0];
             } else {
-                const int t = m - mu;  // backward row of devices mu+1..m
-                const uint64_t tn = lane_u64(cr.tau, mu);  // link mu -> mu+1
-                const uint64_t *G = gpool + gpool_off(cr, t);
-                const int g_lo = rband_lo(cr, t), g_hi = rband_hi(cr, t);
+                const uint64_t tn = cr.TAU(mu);  // link mu -> mu+1
+                const lds_t<uint64_t> *G = gp + (gpool_off(cr, t) - gpool_off(cr, g_lo));
+                const int gl = rband_lo(cr, t), gh = rband_hi(cr, t);
                 for (int i = hlo + lane; i <= hi; i += kWave) {
                     const uint64_t h = H[i - hlo];
                     const int x = N - 2 - i;
-                    if (h == E2_INF64 || tn == E2_INF64 || x < g_lo || x > g_hi) continue;
-                    const uint64_t g = G[x - g_lo];
+                    if (h == E2_INF64 || tn == E2_INF64 || x < gl || x > gh) continue;
+                    const uint64_t g = G[x - gl];
                     if (g == E2_INF64) continue;
                     const uint64_t v = h + tn + g;
                     tm = v < tm ? v : tm;
@@ -1860,36 +1958,45 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
             if (ahead == E2_INF64 || best <= t0 + ahead) break;
         }
         if (mu < m) {
-            const uint64_t tau = mu >= 2 ? lane_u64(cr.tau, mu - 1) : 0;
+            const uint64_t tau = mu >= 2 ? cr.TAU(mu - 1) : 0;
             ft_row(pref_row(tb, r, c), win_row(tb, 0, c), 0, tau, band_lo(cr, mu), band_hi(cr, mu),
-                   mu - 1, mu >= 2 ? pool + pool_off(cr, mu - 1) : nullptr,
-                   mu >= 2 ? band_lo(cr, mu - 1) : 1, mu >= 2 ? band_hi(cr, mu - 1) : 0,
-                   pool + pool_off(cr, mu), mu >= 2 ? sm.tbp + pool_off(cr, mu) : nullptr, st, N, lane);
+                   mu - 1, mu >= 2 ? F : nullptr, mu >= 2 ? band_lo(cr, mu - 1) : 1,
+                   mu >= 2 ? band_hi(cr, mu - 1) : 0, F,
+                   mu >= 2 ? sm.tbp + pool_off(cr, mu) : nullptr, st, N, lane, keyed);
+            f_last = mu;
         }
     }
     *T_out = best;
     *mu_out = best_mu;
     if (best == E2_INF64) return;
-    // ---- rows mu*..m of the chosen master's table with split points (the
-    // previous row ping-pongs in LDS, F_{mu*-1} comes from the pool)
+    // ---- rows mu*..m of the chosen master's table with split points, in
+    // place; their first row reads F_{mu*-1}, computed again when the sweep
+    // went past it (its split points are in tbp already)
     uint8_t *tbp = sm.tbp;
+    if (best_mu >= 2 && f_last != best_mu - 1) {
+        for (int k = 1; k < best_mu; ++k) {
+            const int c = f8(cr.A(k - 1), 0);
+            ft_row(pref_row(tb, r, c), win_row(tb, 0, c), 0, k >= 2 ? cr.TAU(k - 1) : 0,
+                   band_lo(cr, k), band_hi(cr, k), k - 1, k >= 2 ? F : nullptr,
+                   k >= 2 ? band_lo(cr, k - 1) : 1, k >= 2 ? band_hi(cr, k - 1) : 0, F, nullptr,
+                   st, N, lane, keyed);
+        }
+    }
     for (int k = best_mu; k <= m; ++k) {
-        const uint32_t wa = lane_w(cr.wa, k - 1);
+        const uint32_t wa = cr.A(k - 1);
         const int c = f8(wa, 0);
         const int f = (k == best_mu);
-        const uint64_t tau = k >= 2 ? lane_u64(cr.tau, k - 1) : 0;
+        const uint64_t tau = k >= 2 ? cr.TAU(k - 1) : 0;
         const int lo = k == m ? N - 1 : band_lo(cr, k), hi = k == m ? N - 1 : band_hi(cr, k);
-        const uint64_t *prev = nullptr;
-        int plo = 1, phi = 0;
-        if (k >= 2) {
-            prev = (k == best_mu) ? pool + pool_off(cr, k - 1) : Rw[(k - 1) & 1];
-            plo = band_lo(cr, k - 1);
-            phi = band_hi(cr, k - 1);
-        }
         uint8_t *tbs = k == m ? start + m : tbp + pool_off(cr, k);  // row m: one cell
         ft_row(pref_row(tb, r, c), win_row(tb, f, c), f ? uni64(tb.head[r * M + c]) : 0, tau, lo,
-               hi, k - 1, prev, plo, phi, Rw[k & 1], k >= 2 ? tbs : nullptr, st, N, lane);
+               hi, k - 1, k >= 2 ? F : nullptr, k >= 2 ? band_lo(cr, k - 1) : 1,
+               k >= 2 ? band_hi(cr, k - 1) : 0, F, k >= 2 ? tbs : nullptr, st, N, lane, keyed);
     }
+    // the split points may sit in global memory (long bands): complete every
+    // lane's stores before lane 0 walks them
+    __builtin_amdgcn_s_waitcnt(0);
+    __threadfence_block();
     if (lane == 0) {
         int i = N - 1;
         int j = m >= 2 ? start[m] : 0;
@@ -1912,7 +2019,7 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
                                               const uint8_t *__restrict__ roles,
                                               uint32_t *counters,
                                               const uint32_t *__restrict__ list, size_t seg_cap,
-                                              uint64_t *rows, uint8_t *tb_global, uint64_t *T,
+                                              uint8_t *tb_global, uint64_t *T,
                                               uint64_t *Lambda, int16_t *master, uint8_t *layers)
 {
     extern __shared__ uint64_t dyn[];
@@ -1921,14 +2028,15 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
     __shared__ uint32_t job;
     const int lane = threadIdx.x;
     const int M = tb.M, N = tb.N;
+    // LDS: the staged terms (N u64), the backward-row pool (N u64 and the
+    // extra bytes), the master's row and the forward row, the split-point
+    // bytes; the reference path uses the two rows as a ping-pong
     DpSmem sm;
     sm.ps = dyn;
-    sm.Rw0 = (lds_t<uint64_t> *)(dyn + 2 * N);
+    sm.pool_end = (lds_t<char> *)(dyn + 2 * N) + dp_lds_extra(N);
+    sm.Rw0 = (lds_t<uint64_t> *)sm.pool_end;
     sm.Rw1 = sm.Rw0 + (N + 1);
-    sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N + 2 * (N + 1));
-    uint64_t *my_rows = rows + (size_t)blockIdx.x * (2 * (size_t)pool_cells);
-    sm.pool = my_rows;
-    sm.gpool = my_rows + pool_cells;
+    sm.tbp = reinterpret_cast<uint8_t *>(dyn + 2 * N + 2 * (N + 1)) + dp_lds_extra(N);
     sm.pool_cells = pool_cells;
     const uint32_t n0 = counters[0], n1 = counters[kCounterStride],
                    n2 = counters[2 * kCounterStride], n3 = counters[3 * kCounterStride];
@@ -1966,7 +2074,10 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
             banded = banded && tb_global != nullptr;
         }
         if (banded) {
-            dp_ft_banded(tv, smb, cr, r, m, lane, &best, &best_mu, start);
+            // keyed rows when every staged term a(j) < 2^56: a(j) is at most the
+            // chain's summed device totals and links plus one device's total
+            const bool keyed = bound_tot < (1ull << 56) / (uint64_t)(2 * m + 2);
+            dp_ft_banded(tv, smb, cr, r, m, lane, &best, &best_mu, start, keyed);
         } else {
             for (int mu = 1; mu <= m; ++mu) {
                 const uint64_t v = ft_table(tv, sm, r, chain, m, mu, nullptr, lane);
@@ -3004,10 +3115,8 @@ int e2_dp_lds_tb_cells(int N)
     return kLdsTbCells;
 }
 
-size_t e2_dp_row_words(int N) { return 2 * (size_t)e2_dp_pool_cells(N); }
 
 size_t e2_dp_lds_bytes(int N) { return (size_t)dp_lds_fixed(N) + (size_t)dp_lds_extra(N); }
-size_t e2_dp_ft_lds_bytes(int N) { return (size_t)dp_lds_fixed(N); }
 
 int e2_dp_slots(int N, int problems)
 {
@@ -3066,10 +3175,9 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
                                                                 wk.idle_stride, T, Lambda,
                                                                 master, layers);
     else if (objective == 1)
-        k_dp_ft<<<wk.n_slots, 64, e2_dp_ft_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles,
-                                                             wk.counters, wk.list, seg, wk.rows,
-                                                             wk.tb_global, T, Lambda, master,
-                                                             layers);
+        k_dp_ft<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles,
+                                                          wk.counters, wk.list, seg, wk.tb_global,
+                                                          T, Lambda, master, layers);
     else {
         k_dp<<<wk.n_slots, 64, e2_dp_lds_bytes(t.N), s>>>(t, k_max, pool, gen, roles, n_r,
                                                           wk.counters, wk.list, seg, wk.tb_global,

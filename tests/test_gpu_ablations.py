@@ -158,3 +158,21 @@ def test_splitwise_named_workloads(torch_dev, name, rows):
     sub = wl.subset(pick)
     _assert_equal(got, oracle.search_roles(sub, sm, policy="splitwise"), SW_KEYS, rows=pick,
                   tag=name)
+
+
+def test_ft_huge_times_take_the_plain_scan(torch_dev):
+    """Blocks of about 2^46-2^47 ns (devices of a few FLOP/s): the staged FT
+    terms no longer fit a 56-bit key for longer chains, which then take the
+    one-lane-per-cell scan, while short chains keep the keyed one; both
+    equal the oracle."""
+    import dataclasses
+    wl = workload.random_small(6100, M=24, N=60, P=6, k_max=5, mem_lo_layers=4,
+                               mem_hi_layers=30, head=False)
+    wl = dataclasses.replace(wl, speed_flops=np.full(wl.n_dev, 3, np.uint64),
+                             layer_flops=np.full_like(wl.layer_flops, 300_000),
+                             act_bytes=np.array([10**6, 10**4], np.uint64))
+    wl.min_tps_milli = 0
+    want = oracle.eval_population_ft(wl)
+    assert (want["T"] != (1 << 64) - 1).any()
+    keys = ("T", "Lambda", "master", "layers", "w", "phase", "s_p", "s_d")
+    _assert_equal(_gpu_ft(torch_dev, wl), want, keys, tag="huge FT")
