@@ -155,3 +155,15 @@ def test_injected_hip_failure_comes_after_the_argument_checks():
     with pytest.raises(e2.E2Error) as ei:
         e2.e2_debug_inject_hip_error(-1)
     assert ei.value.code == e2.E2_EINVAL
+
+
+def test_missing_library_raises_instead_of_falling_back(monkeypatch, tmp_path):
+    """Without libe2.so every entry point fails loudly: the binding has no
+    CPU path to fall back on."""
+    import paper_2606_03770_amd as pkg
+    monkeypatch.setattr(pkg, "_lib", None)
+    monkeypatch.setattr(pkg, "LIB_PATH", str(tmp_path / "libe2.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        pkg.lib()
+    with pytest.raises(RuntimeError, match="not built"):
+        pkg.e2_ctx_create(workload.make("c1_tiny_12dev_32L").problem_arrays())
