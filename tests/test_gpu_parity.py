@@ -447,3 +447,33 @@ def test_long_chain_among_many_cluster_ids_takes_the_reference_path(torch_dev):
     want = _oracle_all(wl, labels=labels)
     assert (want["T"][:, 0] != INF).any()
     _assert_equal(_gpu_all(torch_dev, wl, labels=labels), want, tag="reference long")
+
+
+def test_one_context_on_two_streams_at_once(torch_dev):
+    """A context is immutable after creation and every call's scratch is
+    stream-ordered, so two streams may evaluate different populations with
+    one context at the same time; each result equals the same call made
+    alone."""
+    torch, dev = torch_dev
+    wl = workload.make("c4_128dev_80L")
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    fp = wl.fitness_params()
+    halves = [np.arange(0, 2048), np.arange(2048, 4096)]
+    ins = [(torch.from_numpy(np.ascontiguousarray(wl.labels[h])).to(dev),
+            torch.from_numpy(np.ascontiguousarray(wl.roles[h])).to(dev)) for h in halves]
+    alone = []
+    for L, R in ins:
+        out = e2.e2_eval_population(ctx, L, R, fp)
+        torch.cuda.synchronize()
+        alone.append({k: e2.u64(v).copy() for k, v in out.items()})
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]   # default priority
+    torch.cuda.synchronize()
+    for rep in range(3):
+        outs = []
+        for (L, R), st in zip(ins, streams):
+            with torch.cuda.stream(st):
+                outs.append(e2.e2_eval_population(ctx, L, R, fp))
+        torch.cuda.synchronize()
+        for a, b in zip(outs, alone):
+            for k in b:
+                assert np.array_equal(e2.u64(a[k]), b[k]), (rep, k)
