@@ -805,7 +805,7 @@ __device__ __forceinline__ RowOut<K> store_to(lds_t<K> *vals, uint8_t *tbs)
 //   attaining it; rows mu*..m of its table (rows below mu* are F) give the
 //   split points for the back tracing.
 //
-// Schedule: all G rows first (kept in a per-wave global pool), then the
+// Schedule: all G rows first (kept in the wave's LDS backward-row pool), then the
 // optimum T0 without any master (the full reversed table's last cell), then
 // masters in ascending position, each combine followed by the forward row
 // the next one reads.  Head time and head bytes only ever add, so
@@ -815,9 +815,9 @@ __device__ __forceinline__ RowOut<K> store_to(lds_t<K> *vals, uint8_t *tbs)
 //
 // The per-position data of a chain (device, capacities, links, head time,
 // bands, pool offsets, window-length bounds) is loaded once, one position
-// per lane (m <= 64), and each row reads its scalars with readlane.  The
-// previous row of every sweep sits in an LDS ping-pong pair; forward rows
-// are also written to a per-wave global pool for the chosen master's rows.
+// per lane (m <= 64; four per lane in the long-chain kernel), and each row
+// reads its scalars with readlane.  Every row lives in LDS: forward rows in
+// place in one buffer, backward rows in a pool (dp_banded).
 // ---------------------------------------------------------------------------
 // split-point bytes kept in LDS per wave; larger tables (the bands of long
 // chains with roomy devices, or the reference path's full rows) go to the
@@ -1065,7 +1065,7 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
     cr.wd = (uint32_t)devR | (uint32_t)glo << 8 | (uint32_t)ghi << 16;
     // backward-row pool: reversed rows t = 1..m-1 band-packed in order (their
     // bands are the forward bands of positions m-1..1 moved by one block, so
-    // they hold as many cells as the forward pool)
+    // they hold as many cells as the forward bands)
     const int gsize = ghi >= glo ? ghi - glo + 1 : 0;
     const int g_incl = scan_incl_i32(gsize, lane);
     cr.we = (uint32_t)(g_incl - gsize);
@@ -1429,9 +1429,8 @@ __device__ __forceinline__ int build_chain(const E2Genomes &gen, int p, int q, i
 // problems w, w + W, w + 2W, ... of the first part of the list (it runs
 // longest chains first, so every wave gets a like mix), the rest from a
 // shared counter when there are many problems per wave, and exits past the
-// end of the list.  LDS: split-point pairs (N x 16 B), two row buffers of
-// N+1 keys and the split-point bytes of the forward rows; the forward and
-// backward row pools live in a per-wave global region (2 pool_cells u64).
+// end of the list.  LDS: split-point pairs (N x 16 B), the backward-row pool,
+// a row buffer and the split-point bytes of the forward rows (see k_dp).
 // ---------------------------------------------------------------------------
 template <bool L> struct CRSel { using T = ChainRegs; };
 template <> struct CRSel<true> { using T = ChainRegsLong; };
