@@ -28,6 +28,8 @@
 // The memory cap turns into a window j >= win[i] (block bytes are
 // non-negative, so the fitting starts of a stage ending at i are a suffix).
 
+#include <atomic>
+
 #include "e2_internal.h"
 
 namespace {
@@ -3120,12 +3122,14 @@ size_t e2_dp_lds_bytes(int N) { return (size_t)dp_lds_fixed(N) + (size_t)dp_lds_
 int e2_dp_slots(int N, int problems)
 {
     // resident one-wave workgroups per CU for this LDS size (the occupancy
-    // the compiled kernel reaches), times the CUs of the device
-    static int per_cu[256];
-    static int n_cu;
+    // the compiled kernel reaches), times the CUs of the device; cached,
+    // and threads that race here compute and store the same values
+    static std::atomic<int> per_cu[256];
+    static std::atomic<int> n_cu{0};
     if (N < 1 || N > 255) return 1;
-    if (n_cu == 0) {
-        int dev = 0, cus = 0;
+    int cus = n_cu.load(std::memory_order_relaxed);
+    if (cus == 0) {
+        int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
                 hipSuccess ||
@@ -3133,19 +3137,20 @@ int e2_dp_slots(int N, int problems)
             (void)hipGetLastError();
             cus = 256;
         }
-        n_cu = cus;
+        n_cu.store(cus, std::memory_order_relaxed);
     }
-    if (per_cu[N] == 0) {
-        int nb = 0;
+    int nb = per_cu[N].load(std::memory_order_relaxed);
+    if (nb == 0) {
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_dp, 64, e2_dp_lds_bytes(N)) !=
                 hipSuccess ||
             nb < 1) {
             (void)hipGetLastError();
             nb = 20;
         }
-        per_cu[N] = nb > 32 ? 32 : nb;
+        nb = nb > 32 ? 32 : nb;
+        per_cu[N].store(nb, std::memory_order_relaxed);
     }
-    const int cap = n_cu * per_cu[N];
+    const int cap = cus * nb;
     return problems < cap ? (problems > 0 ? problems : 1) : cap;
 }
 
