@@ -477,3 +477,44 @@ def test_one_context_on_two_streams_at_once(torch_dev):
         for a, b in zip(outs, alone):
             for k in b:
                 assert np.array_equal(e2.u64(a[k]), b[k]), (rep, k)
+
+
+def test_one_context_from_four_host_threads(torch_dev):
+    """A context may serve several host threads at once: four threads, each
+    on its own stream, evaluate their quarter of a population through one
+    context (the binding releases the interpreter lock inside the library
+    calls); every result equals the single-threaded evaluation."""
+    import threading
+    torch, dev = torch_dev
+    wl = workload.make("c3_64dev_80L")
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    fp = wl.fitness_params()
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    want = e2.e2_eval_population(ctx, L, R, fp)
+    torch.cuda.synchronize()
+    want = {k: e2.u64(v).copy() for k, v in want.items()}
+    quarters = np.array_split(np.arange(wl.population), 4)
+    results, errors = [None] * 4, []
+
+    def work(i):
+        try:
+            st = torch.cuda.Stream()
+            with torch.cuda.stream(st):
+                rows = quarters[i]
+                for _ in range(5):
+                    out = e2.e2_eval_population(ctx, L[rows[0]:rows[-1] + 1],
+                                                R[rows[0]:rows[-1] + 1], fp)
+                st.synchronize()
+            results[i] = {k: e2.u64(v).copy() for k, v in out.items()}
+        except Exception as exc:  # reported below, in the main thread
+            errors.append(repr(exc))
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for k in want:
+        assert np.array_equal(np.concatenate([r[k] for r in results]), want[k]), k
