@@ -178,6 +178,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
     __shared__ uint32_t base[kEG][16][kListSegs];
     __shared__ uint32_t offs[kEG][256];  // replica starts of two-chromosome genomes
     __shared__ uint32_t bad[kEG][8];     // replicas holding a device id >= M
+    __shared__ uint16_t posc[kEG][256];  // two-chromosome genomes: cap0 | head bit per position
     const int g = threadIdx.x / 64;
     const int lane = threadIdx.x % 64;
     const int p = blockIdx.x * kEG + g;
@@ -258,14 +259,39 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                 const int r = n_r > 0 ? ri : (tb.n_mem > 1 ? roles[(size_t)p * k_max + lab] != 0 : 0);
                 const int c = mem_class(tb, r);
                 const uint32_t c0 = tb.cap0[(size_t)c * M + devs[u]];
-                atomicAdd(&packed[g][lab], (1u << 16) | c0);
-                atomicMin(&mincap[g][lab], c0);
-                // a per-cluster flag: the atomics of one word meet only the
-                // devices of one cluster
-                if (tb.capH[(size_t)c * M + devs[u]]) atomicOr(&hflag[g][lab], 1u);
+                const uint32_t cH = tb.capH[(size_t)c * M + devs[u]];
+                if (ordered) {
+                    posc[g][lane + 64 * u] = (uint16_t)(c0 | (cH ? 0x100u : 0u));
+                } else {
+                    atomicAdd(&packed[g][lab], (1u << 16) | c0);
+                    atomicMin(&mincap[g][lab], c0);
+                    // a per-cluster flag: the atomics of one word meet only
+                    // the devices of one cluster
+                    if (cH) atomicOr(&hflag[g][lab], 1u);
+                }
             }
         }
         __syncthreads();
+        if (ordered) {  // uniform over the workgroup
+            // a replica is a run of ordering positions [offs[q], offs[q+1]):
+            // one lane per replica sums its run, with no atomics (the lanes
+            // of one run would all meet on its words).  Positions holding an
+            // id >= M lie in replicas marked bad, which are not listed.
+            for (int q = lane; p < P && q < k_max; q += kWave) {
+                const int lo = (int)offs[g][q], hi = (int)offs[g][q + 1];
+                uint32_t sum = 0, mn = 0xFFFFFFFFu, any = 0;
+                for (int x = lo; x < hi; ++x) {
+                    const uint32_t v = posc[g][x];
+                    sum += v & 0xFFu;
+                    mn = min(mn, v & 0xFFu);
+                    any |= v >> 8;
+                }
+                packed[g][q] = ((uint32_t)(hi - lo) << 16) | sum;
+                mincap[g][q] = mn;
+                hflag[g][q] = any;
+            }
+            __syncthreads();
+        }
         // decide per cluster; count listed problems per class (slots u with
         // no cluster id below k_max are skipped: the bound is uniform)
 #pragma unroll
