@@ -647,6 +647,16 @@ template <typename K> __device__ __forceinline__ K combine_key(K v, K b, int mu)
     return pack_low8(kmax(v, b), mu);
 }
 
+// the entry at LDS byte address addr
+template <typename K> __device__ __forceinline__ PS<K> ps_at(int addr)
+{
+    const lds_t<PS<K>> *p = (const lds_t<PS<K>> *)(uintptr_t)(uint32_t)addr;
+    PS<K> e;
+    e.a = p->a;
+    e.s = p->s;
+    return e;
+}
+
 template <int S, typename K>
 __device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K si1, int t_safe,
                                        int t_all)
@@ -661,13 +671,25 @@ __device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K
         best = kmin(kmin(best, cand(e3, si1)), cand(e2, si1));
         best = kmin(kmin(best, cand(e1, si1)), cand(e0, si1));
     }
+    if (t + 2 <= t_safe) {  // a pair that every cell's window still holds
+        const PS<K> *q = top - S * (t + 1);
+        const PS<K> e1 = q[S], e0 = q[0];
+        best = kmin(kmin(best, cand(e1, si1)), cand(e0, si1));
+        t += 2;
+    }
     // the rest two steps at a time, both entries loaded before use; indices
     // below the cell's window start read its first entry again (an odd last
-    // step repeats a candidate, which leaves the minimum unchanged)
+    // step repeats a candidate, which leaves the minimum unchanged).  The
+    // clamp works on LDS byte addresses (signed: the step's address may fall
+    // below the array's start before it is clamped).
+    const lds_t<PS<K>> *pl = (const lds_t<PS<K>> *)ps;
+    const int a_lo = (int)(uint32_t)(uintptr_t)(pl + jlo);
+    int a = (int)(uint32_t)(uintptr_t)pl + (i - o - S * t) * (int)sizeof(PS<K>);
     for (; t < t_all; t += 2) {
-        const PS<K> e0 = ps[max(i - o - S * t, jlo)];
-        const PS<K> e1 = ps[max(i - o - S * (t + 1), jlo)];
+        const PS<K> e0 = ps_at<K>(max(a, a_lo));
+        const PS<K> e1 = ps_at<K>(max(a - S * (int)sizeof(PS<K>), a_lo));
         best = kmin(kmin(best, cand(e0, si1)), cand(e1, si1));
+        a -= 2 * S * (int)sizeof(PS<K>);
     }
     if (S >= 2) best = kmin(best, dppk<0xb1>(best));
     if (S >= 4) best = kmin(best, dppk<0x4e>(best));
