@@ -745,34 +745,30 @@ def measure(torch, ctx, stream, bufs, init, step, count, warmup, steps):
             dst.copy_(src)
         torch.cuda.synchronize()
 
-    def run(n, events=None):
+    def run(n):
         cur = 0
         for g in range(n):
-            if events is not None:
-                events[g][0].record(stream)
             step(g, cur)
-            if events is not None:
-                events[g][1].record(stream)
             cur = 1 - cur
 
     reset()
     run(warmup)
     torch.cuda.synchronize()
     reset()
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(steps)]
+    # the timed region holds the generations and the library's event pair
+    # around each DP launch, nothing else (an event record costs the stream
+    # a few microseconds)
     e2.e2_ctx_dp_timing(ctx, steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run(steps, events)
+    run(steps)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     n_dp, dp_ms = e2.e2_ctx_dp_elapsed(ctx)
     e2.e2_ctx_dp_timing(ctx, 0)
     assert n_dp == steps, (n_dp, steps)
-    step_ms = [a.elapsed_time(b) for a, b in events]
-    log(f"timed {steps} steps: {elapsed * 1e3:.2f} ms; generation {np.mean(step_ms):.3f} ms "
-        f"avg on the stream; DP kernel {dp_ms / n_dp:.3f} ms avg")
+    log(f"timed {steps} steps: {elapsed * 1e3:.2f} ms, {elapsed * 1e3 / steps:.3f} ms per "
+        f"generation; DP kernel {dp_ms / n_dp:.3f} ms avg")
     cells = cand = cand32 = alg1 = 0
     pop = tuple(x.clone() for x in init)
     for g in range(steps):
@@ -781,7 +777,7 @@ def measure(torch, ctx, stream, bufs, init, step, count, warmup, steps):
         cand += c2
         cand32 += c3
         alg1 += c4
-    return dict(elapsed=elapsed, dp_s=dp_ms / 1e3, step_ms=float(np.mean(step_ms)), cells=cells,
+    return dict(elapsed=elapsed, dp_s=dp_ms / 1e3, step_ms=elapsed * 1e3 / steps, cells=cells,
                 cand=cand, cand32=cand32, alg1=alg1)
 
 
@@ -804,7 +800,7 @@ def roofline(t, steps, prof):
            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
                            "copy-calibrated)",
            "avg_launch_ms": t["dp_s"] * 1e3 / steps,
-           "generation_ms_on_stream": t["step_ms"]}
+           "generation_ms": t["step_ms"]}
     if prof and prof.get("sq_insts_valu_per_launch"):
         us = prof["k_dp_avg_us"]
         valu_lane_ops = prof["sq_insts_valu_per_launch"] * 64
