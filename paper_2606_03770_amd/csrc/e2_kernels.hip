@@ -1060,8 +1060,16 @@ __device__ __forceinline__ Row<K> rev_row_of(const E2Tables &tb, const CR &cr, i
     return g;
 }
 
+// every lane's v is at most lim (the answer is wave-uniform)
+__device__ __forceinline__ bool wave_all_le(uint64_t v, uint64_t lim)
+{
+    return __ballot(v > lim) == 0;
+}
+
 // Per-position table of a chain and the largest finite value its DP can
-// produce; false when the banded path cannot take the chain.
+// produce, as this lane's share (the bound is the maximum over the lanes:
+// callers compare it with wave_all_le); false when the banded path cannot
+// take the chain.
 __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm, int r,
                                            const uint8_t *chain, int m, int lane, ChainRegs &cr,
                                            uint64_t *bound, uint64_t *bound_tot, int *pool_cells)
@@ -1076,8 +1084,8 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
     cr.head = valid ? tb.head[r * M + dev] : 0;
     cr.tau = (valid && lane >= 1) ? link_tau(tb, r, chain[lane - 1], dev) : 0;
     const uint64_t tf = cr.tau != E2_INF64 ? cr.tau : 0;
-    *bound = wave_max_u64(umax64(valid ? tb.vmax[r * M + dev] : 0, tf));
-    *bound_tot = wave_max_u64(umax64(valid ? tb.vtot[r * M + dev] : 0, tf));
+    *bound = umax64(valid ? tb.vmax[r * M + dev] : 0, tf);
+    *bound_tot = umax64(valid ? tb.vtot[r * M + dev] : 0, tf);
     const int pre = scan_incl_i32(cap0, lane);
     const int tot = lane_i(pre, m - 1);
     int lo = max(k1 - 1, N - 1 - (tot - pre));
@@ -1155,8 +1163,8 @@ __device__ __forceinline__ void chain_regs_long(const E2Tables &tb, int r, const
         pre[i] = scan_incl_i32(cap0[i], lane) + carry;
         carry = lane_i(pre[i], kWave - 1);
     }
-    *bound = wave_max_u64(vb);
-    *bound_tot = wave_max_u64(vt);
+    *bound = vb;  // this lane's share, as in chain_regs
+    *bound_tot = vt;
     auto at = [&](const int (&v)[kLongSets], int k0) {  // value of position k0, per lane
         const int l = k0 & 63, set = k0 >> 6;
         int x = 0;
@@ -1575,9 +1583,9 @@ __device__ __forceinline__ void dp_jobs(const E2Tables &tb, int k_max, int pool_
             smb.tbp = tb_global ? tb_global + (size_t)blockIdx.x * N * N : nullptr;
             banded = banded && tb_global != nullptr;
         }
-        if (banded && bound <= kU32MaxValue)
+        if (banded && wave_all_le(bound, kU32MaxValue))
             dp_banded<uint32_t>(tv, smb, cr, r, m, lane, &best, &best_mu, start, &last_tb);
-        else if (banded && bound_tot < kF64Limit)
+        else if (banded && wave_all_le(bound_tot, kF64Limit - 1))
             dp_banded<double>(tv, smb, cr, r, m, lane, &best, &best_mu, start, &last_tb);
         else {
             // reference path: a full table per master, then the chosen
@@ -2125,7 +2133,8 @@ __global__ __launch_bounds__(64) void k_dp_ft(E2Tables tb, int k_max, int pool_c
         if (banded) {
             // keyed rows when every staged term a(j) < 2^56: a(j) is at most the
             // chain's summed device totals and links plus one device's total
-            const bool keyed = bound_tot < (1ull << 56) / (uint64_t)(2 * m + 2);
+            const bool keyed =
+                wave_all_le(bound_tot, (1ull << 56) / (uint64_t)(2 * m + 2) - 1);
             dp_ft_banded(tv, smb, cr, r, m, lane, &best, &best_mu, start, keyed);
         } else {
             for (int mu = 1; mu <= m; ++mu) {
