@@ -30,6 +30,7 @@
 
 #include <atomic>
 
+#include "../../include/e2.h"
 #include "e2_internal.h"
 
 namespace {
@@ -1463,9 +1464,23 @@ __device__ __forceinline__ int build_chain(const E2Genomes &gen, int p, int q, i
 {
     int m = 0;
     if (gen.labels) {
-        for (int base = 0; base < M; base += kWave) {
-            const int d = base + lane;
-            const bool in = d < M && gen.labels[(size_t)p * M + d] == q;
+        // the genome's labels, device lane + 64 t in slot t, all loads issued
+        // before the first is used (clamped indices: no branch around them)
+        // (the lane index goes through an empty asm so that the offsets are
+        // formed here, in 32 bits from the row's scalar base, instead of being
+        // kept live across the job loop)
+        constexpr int kSlots = (E2_MAX_DEV + kWave - 1) / kWave;
+        const uint8_t *row = gen.labels + (size_t)p * M;
+        int l = lane;
+        asm volatile("" : "+v"(l));
+        int lab[kSlots];
+#pragma unroll
+        for (int t = 0; t < kSlots; ++t) lab[t] = at_byte(row, (uint32_t)min(l + kWave * t, M - 1));
+#pragma unroll
+        for (int t = 0; t < kSlots; ++t) {
+            if (kWave * t >= M) break;
+            const int d = kWave * t + lane;
+            const bool in = d < M && lab[t] == q;
             const uint64_t mask = __ballot(in);
             if (in) chain[m + __popcll(mask & ((1ull << lane) - 1))] = (uint8_t)d;
             m += __popcll(mask);
