@@ -390,14 +390,34 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
             vtot[(size_t)r * M + d] =
                 pref[((size_t)r * M + d) * (N + 1) + N] + h[(size_t)r * M + d];
 
-    // prefix sums pre-shifted for the DP's packed keys (value << 8 | index)
-    std::vector<uint32_t> pref8u(pref.size()), prefR8u(prefR.size());
-    std::vector<double> pref8d(pref.size()), prefR8d(prefR.size());
-    for (size_t x = 0; x < pref.size(); ++x) {
-        pref8u[x] = (uint32_t)(pref[x] << 8);
-        prefR8u[x] = (uint32_t)(prefR[x] << 8);
-        pref8d[x] = (double)pref[x] * 256.0;
-        prefR8d[x] = (double)prefR[x] * 256.0;
+    // one prefix row block per role index and device: P, PR, P x 256 and
+    // PR x 256 as doubles, P << 8 and PR << 8 modulo 2^32 (the DP's packed
+    // keys, value << 8 | index)
+    const size_t X = (size_t)N + 1;
+    std::vector<uint8_t> prow((size_t)R * M * kRowBlock * X);
+    for (size_t b = 0; b < (size_t)R * M; ++b) {
+        uint8_t *blk = &prow[b * kRowBlock * X];
+        const uint64_t *P = &pref[b * X], *PR = &prefR[b * X];
+        for (size_t x = 0; x < X; ++x) {
+            const uint32_t p8 = (uint32_t)(P[x] << 8), pr8 = (uint32_t)(PR[x] << 8);
+            const double p8d = (double)P[x] * 256.0, pr8d = (double)PR[x] * 256.0;
+            memcpy(blk + kRowPref * X + 8 * x, &P[x], 8);
+            memcpy(blk + kRowPrefR * X + 8 * x, &PR[x], 8);
+            memcpy(blk + kRowPref8d * X + 8 * x, &p8d, 8);
+            memcpy(blk + kRowPrefR8d * X + 8 * x, &pr8d, 8);
+            memcpy(blk + kRowPref8u * X + 4 * x, &p8, 4);
+            memcpy(blk + kRowPrefR8u * X + 4 * x, &pr8, 4);
+        }
+    }
+    // one memory-window block per class: win, minwin, winR, minwinR
+    const size_t MN = (size_t)M * N;
+    std::vector<uint8_t> wtab((size_t)C * 6 * MN);
+    for (int c = 0; c < C; ++c) {
+        uint8_t *blk = &wtab[(size_t)c * 6 * MN];
+        memcpy(blk, &win[(size_t)c * 2 * MN], 2 * MN);
+        memcpy(blk + 2 * MN, &minwin[(size_t)c * 2 * MN], 2 * MN);
+        memcpy(blk + 4 * MN, &winR[(size_t)c * MN], MN);
+        memcpy(blk + 5 * MN, &minwinR[(size_t)c * MN], MN);
     }
 
     struct Part {
@@ -405,15 +425,11 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
         size_t bytes;
         char *dst;
     };
-    Part parts[] = {{pref.data(), pref.size() * 8, nullptr},   {h.data(), h.size() * 8, nullptr},
-                    {tau.data(), tau.size() * 8, nullptr},     {win.data(), win.size(), nullptr},
-                    {winR.data(), winR.size(), nullptr},       {prefR.data(), prefR.size() * 8, nullptr},
-                    {minwin.data(), minwin.size(), nullptr},   {minwinR.data(), minwinR.size(), nullptr},
+    Part parts[] = {{prow.data(), prow.size(), nullptr},       {h.data(), h.size() * 8, nullptr},
+                    {tau.data(), tau.size() * 8, nullptr},     {wtab.data(), wtab.size(), nullptr},
                     {cap0.data(), cap0.size(), nullptr},       {capH.data(), capH.size(), nullptr},
                     {vmax.data(), vmax.size() * 8, nullptr},   {vtot.data(), vtot.size() * 8, nullptr},
-                    {hfit.data(), hfit.size(), nullptr},
-                    {pref8u.data(), pref8u.size() * 4, nullptr}, {prefR8u.data(), prefR8u.size() * 4, nullptr},
-                    {pref8d.data(), pref8d.size() * 8, nullptr}, {prefR8d.data(), prefR8d.size() * 8, nullptr}};
+                    {hfit.data(), hfit.size(), nullptr}};
     size_t total = 0;
     for (const Part &pt : parts) total += align256(pt.bytes);
     e2_ctx *ctx = static_cast<e2_ctx *>(calloc(1, sizeof(e2_ctx)));
@@ -454,23 +470,15 @@ int build_ctx(const e2_problem *prob, int b_max, uint32_t beta_ppm, uint64_t kv,
     ctx->b_max = b_max;
     ctx->head_bytes = prob->head_bytes;
     E2Tables &tb = ctx->tables;
-    tb.pref = reinterpret_cast<const uint64_t *>(parts[0].dst);
+    tb.prow = reinterpret_cast<const uint8_t *>(parts[0].dst);
     tb.head = reinterpret_cast<const uint64_t *>(parts[1].dst);
     tb.tau = reinterpret_cast<const uint64_t *>(parts[2].dst);
-    tb.win = reinterpret_cast<const uint8_t *>(parts[3].dst);
-    tb.winR = reinterpret_cast<const uint8_t *>(parts[4].dst);
-    tb.prefR = reinterpret_cast<const uint64_t *>(parts[5].dst);
-    tb.minwin = reinterpret_cast<const uint8_t *>(parts[6].dst);
-    tb.minwinR = reinterpret_cast<const uint8_t *>(parts[7].dst);
-    tb.cap0 = reinterpret_cast<const uint8_t *>(parts[8].dst);
-    tb.capH = reinterpret_cast<const uint8_t *>(parts[9].dst);
-    tb.vmax = reinterpret_cast<const uint64_t *>(parts[10].dst);
-    tb.vtot = reinterpret_cast<const uint64_t *>(parts[11].dst);
-    tb.hfit = reinterpret_cast<const uint8_t *>(parts[12].dst);
-    tb.pref8u = reinterpret_cast<const uint32_t *>(parts[13].dst);
-    tb.prefR8u = reinterpret_cast<const uint32_t *>(parts[14].dst);
-    tb.pref8d = reinterpret_cast<const double *>(parts[15].dst);
-    tb.prefR8d = reinterpret_cast<const double *>(parts[16].dst);
+    tb.wtab = reinterpret_cast<const uint8_t *>(parts[3].dst);
+    tb.cap0 = reinterpret_cast<const uint8_t *>(parts[4].dst);
+    tb.capH = reinterpret_cast<const uint8_t *>(parts[5].dst);
+    tb.vmax = reinterpret_cast<const uint64_t *>(parts[6].dst);
+    tb.vtot = reinterpret_cast<const uint64_t *>(parts[7].dst);
+    tb.hfit = reinterpret_cast<const uint8_t *>(parts[8].dst);
     tb.M = M;
     tb.N = N;
     tb.R = R;

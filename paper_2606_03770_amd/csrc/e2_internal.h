@@ -13,29 +13,34 @@
 // slot model).  Memory tables exist per memory class: one shared class
 // (n_mem = 1, no KV bytes) or one per role index (n_mem = R, block bytes
 // W[n] + kv * slots(r)); the [C] below is that class.
+// Byte layout of a prefix row block (per role index r and device c, N+1
+// entries in each part): the prefix sums of block times P (u64), the same
+// over reversed blocks PR[x] = P[N] - P[N-x] (u64), P x 256 and PR x 256 as
+// doubles (exact below 2^45, the only range the fp64 DP keys use), and
+// P << 8 and PR << 8 modulo 2^32 (32-bit DP keys).  One block per (r, c), so
+// that a row of the DP finds every part from one base and the row index.
+constexpr int kRowPref = 0, kRowPrefR = 8, kRowPref8d = 16, kRowPrefR8d = 24, kRowPref8u = 32,
+              kRowPrefR8u = 36, kRowBlock = 40;  // bytes per entry of N+1
+
 struct E2Tables {
-    const uint64_t *pref;  // [R][M][N+1] prefix sums of block times per role and device
+    const uint8_t *prow;   // [R][M] prefix row blocks of kRowBlock x (N+1) bytes (above)
     const uint64_t *head;  // [R][M] head + output-layer time per role and device
     const uint64_t *tau;   // [R][M][M] link time per role, INF for a dead link
-    const uint8_t *win;    // [C][2][M][N] smallest stage start j so that blocks j..i fit
-                           //   ([0]: no head bytes, [1]: with head bytes), E2_NO_START if none
-    const uint64_t *prefR; // [R][M][N+1] prefix sums over reversed blocks: prefR[x] =
-                           //   pref[N] - pref[N-x] (block N-1 first)
-    const uint8_t *winR;   // [C][M][N] reversed-block window starts without the head:
-                           //   smallest y so that reversed blocks y..x fit, E2_NO_START if none
-    const uint8_t *minwin; // [C][2][M][N] lower bound of window lengths i - win(i) + 1 over
-                           //   cells i >= x (0 if unknown); same for reversed blocks in
-    const uint8_t *minwinR;//   [C][M][N]
+    const uint8_t *wtab;   // [C] memory-window blocks of 6 M N bytes, each
+                           //   [2][M][N] win: smallest stage start j so that blocks
+                           //     j..i fit ([0]: no head bytes, [1]: with head bytes),
+                           //     E2_NO_START if none;
+                           //   [2][M][N] minwin: lower bound of window lengths
+                           //     i - win(i) + 1 over cells i >= x (0 if unknown);
+                           //   [M][N] winR: reversed-block window starts without the
+                           //     head (smallest y so that reversed blocks y..x fit);
+                           //   [M][N] minwinR: minwin of winR
     const uint8_t *cap0;   // [C][M] most blocks one stage can hold without the head
     const uint8_t *capH;   // [C][M] most blocks one stage can hold with the head
     const uint64_t *vmax;  // [R][M] largest cost of a fitting stage (+ head time when it
                            //   holds the head bytes) per role and device
     const uint64_t *vtot;  // [R][M] total time of all blocks + head time per role and device
     const uint8_t *hfit;   // [M] 1 when the head bytes alone fit the device
-    const uint32_t *pref8u;  // [R][M][N+1] pref << 8 modulo 2^32 (32-bit DP keys)
-    const uint32_t *prefR8u; // [R][M][N+1] prefR << 8 modulo 2^32
-    const double *pref8d;    // [R][M][N+1] pref x 256 as a double (exact below 2^45, the
-    const double *prefR8d;   //   only range the fp64 DP keys use); same for prefR
     int M;
     int N;
     int R;      // role indices

@@ -149,10 +149,7 @@ __device__ __forceinline__ E2Tables mem_view(const E2Tables &tb, int r)
     E2Tables v = tb;
     const size_t c = (size_t)mem_class(tb, r);
     const size_t MN = (size_t)tb.M * tb.N;
-    v.win += c * 2 * MN;
-    v.minwin += c * 2 * MN;
-    v.winR += c * MN;
-    v.minwinR += c * MN;
+    v.wtab += c * 6 * MN;
     v.cap0 += c * tb.M;
     v.capH += c * tb.M;
     return v;
@@ -549,29 +546,34 @@ template <typename T> __device__ __forceinline__ T at_byte(const T *p, uint32_t 
     return *reinterpret_cast<const T *>(reinterpret_cast<const char *>(p) + off);
 }
 
-// Row starts of the per-device tables (element offsets fit in 32 bits:
-// at most 2 x 256 x 256 entries).
+// Row starts of the per-device tables.  A prefix row block's byte offset
+// fits in 32 bits (at most 16 x 256 blocks of 40 x 257 bytes); every part of
+// a row comes from the one table base, so that the DP keeps one base live
+// instead of a pointer per part.
+__device__ __forceinline__ const uint8_t *prow_block(const E2Tables &tb, int r, int c)
+{
+    return tb.prow + (uint32_t)((r * tb.M + c) * kRowBlock * (tb.N + 1));
+}
 __device__ __forceinline__ const uint64_t *pref_row(const E2Tables &tb, int r, int c)
 {
-    return tb.pref + (uint32_t)((r * tb.M + c) * (tb.N + 1));
+    return reinterpret_cast<const uint64_t *>(prow_block(tb, r, c));
 }
 __device__ __forceinline__ const uint64_t *prefR_row(const E2Tables &tb, int r, int c)
 {
-    return tb.prefR + (uint32_t)((r * tb.M + c) * (tb.N + 1));
+    return reinterpret_cast<const uint64_t *>(prow_block(tb, r, c) +
+                                              (uint32_t)(kRowPrefR * (tb.N + 1)));
 }
 // P << 8 of the same rows as a key of type K (u32: modulo 2^32; fp64: exact
 // for the problems that take fp64 keys)
 template <typename K> __device__ __forceinline__ const K *pref8_row(const E2Tables &tb, int r, int c)
 {
-    const uint32_t o = (uint32_t)((r * tb.M + c) * (tb.N + 1));
-    if constexpr (__is_same(K, double)) return tb.pref8d + o;
-    else return tb.pref8u + o;
+    constexpr int part = __is_same(K, double) ? kRowPref8d : kRowPref8u;
+    return reinterpret_cast<const K *>(prow_block(tb, r, c) + (uint32_t)(part * (tb.N + 1)));
 }
 template <typename K> __device__ __forceinline__ const K *prefR8_row(const E2Tables &tb, int r, int c)
 {
-    const uint32_t o = (uint32_t)((r * tb.M + c) * (tb.N + 1));
-    if constexpr (__is_same(K, double)) return tb.prefR8d + o;
-    else return tb.prefR8u + o;
+    constexpr int part = __is_same(K, double) ? kRowPrefR8d : kRowPrefR8u;
+    return reinterpret_cast<const K *>(prow_block(tb, r, c) + (uint32_t)(part * (tb.N + 1)));
 }
 template <typename K> __device__ __forceinline__ K shift8(uint64_t v)
 {
@@ -584,9 +586,23 @@ template <typename K> __device__ __forceinline__ K prefix8(const Row<K> &rw, uin
     if constexpr (__is_same(K, uint64_t)) return rw.pr[x] << 8;
     else return at_byte(rw.p8, x * (uint32_t)sizeof(K));
 }
+// the memory-window tables of a view's class (wtab block: win, minwin,
+// winR, minwinR)
 __device__ __forceinline__ const uint8_t *win_row(const E2Tables &tb, int f, int c)
 {
-    return tb.win + (uint32_t)((f * tb.M + c) * tb.N);
+    return tb.wtab + (uint32_t)((f * tb.M + c) * tb.N);
+}
+__device__ __forceinline__ const uint8_t *winR_row(const E2Tables &tb, int c)
+{
+    return tb.wtab + (uint32_t)((4 * tb.M + c) * tb.N);
+}
+__device__ __forceinline__ int minwin_at(const E2Tables &tb, int f, int c, int x)
+{
+    return tb.wtab[(uint32_t)(((2 + f) * tb.M + c) * tb.N + x)];
+}
+__device__ __forceinline__ int minwinR_at(const E2Tables &tb, int c, int x)
+{
+    return tb.wtab[(uint32_t)((5 * tb.M + c) * tb.N + x)];
 }
 __device__ __forceinline__ uint64_t link_tau(const E2Tables &tb, int r, int a, int b)
 {
@@ -1046,7 +1062,7 @@ __device__ __forceinline__ Row<K> rev_row_of(const E2Tables &tb, const CR &cr, i
     Row<K> g;
     g.pr = prefR_row(tb, r, c);
     g.p8 = prefR8_row<K>(tb, r, c);
-    g.wr = tb.winR + (uint32_t)(c * tb.N);
+    g.wr = winR_row(tb, c);
     g.hadd = 0;
     g.hadd8 = 0;
     g.tau = (t >= 2) ? to_k<K>(cr.TAU(cr.m + 1 - t)) : (K)0;  // link m+1-t -> m+2-t
@@ -1096,8 +1112,8 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
     const int size_incl = scan_incl_i32(size, lane);
     const int off = size_incl - size;
     const int pool_need = lane_i(size_incl, kWave - 1);
-    const int lmin0 = (valid && lo <= hi) ? tb.minwin[(size_t)dev * N + lo] : 0;
-    const int lmin1 = (valid && lo <= hi) ? tb.minwin[((size_t)M + dev) * N + lo] : 0;
+    const int lmin0 = (valid && lo <= hi) ? minwin_at(tb, 0, dev, lo) : 0;
+    const int lmin1 = (valid && lo <= hi) ? minwin_at(tb, 1, dev, lo) : 0;
     // reversed row t = k1 covers original position kk = m+1-t: blocks j..N-1
     // with max(kk-1, N-(tot-pre[kk-1])) <= j <= min(N-(m-kk+1), pre[kk-1]),
     // i.e. reversed cells x = N-1-j
@@ -1115,7 +1131,7 @@ __device__ __forceinline__ bool chain_regs(const E2Tables &tb, const DpSmem &sm,
         if (vr && gh >= gl) {
             glo = N - 1 - gh;
             ghi = N - 1 - gl;
-            lminR = tb.minwinR[(size_t)devR * N + glo];
+            lminR = minwinR_at(tb, devR, glo);
         }
     }
     cr.wa = (uint32_t)dev | (uint32_t)cap0 << 8 | (uint32_t)capH << 16 | (uint32_t)lmin0 << 24;
@@ -1197,8 +1213,8 @@ __device__ __forceinline__ void chain_regs_long(const E2Tables &tb, int r, const
         const int size_incl = scan_incl_i32(size, lane) + size_carry;
         size_carry = lane_i(size_incl, kWave - 1);
         const int off = size_incl - size;
-        const int lmin0 = (valid && lo <= hi) ? tb.minwin[(size_t)d * N + lo] : 0;
-        const int lmin1 = (valid && lo <= hi) ? tb.minwin[((size_t)M + d) * N + lo] : 0;
+        const int lmin0 = (valid && lo <= hi) ? minwin_at(tb, 0, d, lo) : 0;
+        const int lmin1 = (valid && lo <= hi) ? minwin_at(tb, 1, d, lo) : 0;
         // reversed row t = k1 covers original position kk = m+1-t
         const int kk = m + 1 - k1;
         const int src = max(0, min(kLongSets * 64 - 1, kk - 1));
@@ -1213,7 +1229,7 @@ __device__ __forceinline__ void chain_regs_long(const E2Tables &tb, int r, const
             if (vr && gh >= gl) {
                 glo = N - 1 - gh;
                 ghi = N - 1 - gl;
-                lminR = tb.minwinR[(size_t)devR * N + glo];
+                lminR = minwinR_at(tb, devR, glo);
             }
         }
         c.wa = (uint32_t)d | (uint32_t)cap0[i] << 8 | (uint32_t)capH << 16 | (uint32_t)lmin0 << 24;
@@ -1287,7 +1303,7 @@ template <typename K, class CR>
 __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, const CR &cr, int r, int m,
                           int lane, uint64_t *T_out, int *mu_out, uint8_t *start, uint8_t *last_tb)
 {
-    const int N = tb.N, M = tb.M;
+    const int N = tb.N;
     PS<K> *ps = static_cast<PS<K> *>(sm.ps);
     lds_t<K> *F = reinterpret_cast<lds_t<K> *>(sm.Rw0);  // forward rows, in place
     lds_t<char> *pool_c = (lds_t<char> *)sm.ps + (uint32_t)N * sizeof(PS<K>);
@@ -1305,7 +1321,7 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         set_prev(g, gp + (gpool_off(cr, m - 1) - gpool_off(cr, g_lo)), rband_lo(cr, m - 1),
                  rband_hi(cr, m - 1));
         g.lo = g.hi = N - 1;
-        g.lmin = uni(tb.minwinR[(size_t)f8(cr.D(m - 1), 0) * N + (N - 1)]);
+        g.lmin = uni(minwinR_at(tb, f8(cr.D(m - 1), 0), N - 1));
         row_pass(g, store_to<K>(F, nullptr), ps, lane, N);
         tn = uni_k(F[0]);
         if (tn == KeyT<K>::inf) {
@@ -1381,7 +1397,7 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         // row m-1 of the chosen table (F_{m-1} when mu* = m: the sweep's last row)
         set_prev(rw, F, band_lo(cr, m - 1), band_hi(cr, m - 1));
         rw.lo = rw.hi = N - 1;
-        rw.lmin = tb.minwin[((size_t)(best_mu == m) * M + f8(cr.A(m - 1), 0)) * N + (N - 1)];
+        rw.lmin = minwin_at(tb, best_mu == m, f8(cr.A(m - 1), 0), N - 1);
         rw.lmin = uni(rw.lmin);
         row_pass(rw, store_to<K>(F, last_tb), ps, lane, N);
         // the split points may sit in global memory (long bands): complete
@@ -1433,7 +1449,7 @@ __device__ __forceinline__ uint64_t dp_table(const E2Tables &tb, const DpSmem &s
         rw.hi = N - 1;
         rw.kmin = k - 1;
         rw.cap = N;
-        rw.lmin = uni(tb.minwin[((size_t)f * tb.M + c) * N + rw.lo]);
+        rw.lmin = uni(minwin_at(tb, f, c, rw.lo));
         if (k == 1) {
             rw.tau = 0;
             rw.prev = nullptr;
@@ -1925,7 +1941,7 @@ __device__ __forceinline__ void ft_g_rows(const E2Tables &tb, const ChainRegs &c
         const uint32_t wd = cr.D(t - 1);
         const int c = f8(wd, 0);
         const uint64_t tau = t >= 2 ? cr.TAU(m + 1 - t) : 0;  // link m+1-t -> m+2-t
-        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, tau, f8(wd, 8), f8(wd, 16),
+        ft_row(prefR_row(tb, r, c), winR_row(tb, c), 0, tau, f8(wd, 8), f8(wd, 16),
                t - 1, t >= 2 ? gp + (t - 1 >= t_lo ? gpool_off(cr, t - 1) - base : 0) : nullptr,
                t >= 2 ? rband_lo(cr, t - 1) : 1, t >= 2 ? rband_hi(cr, t - 1) : 0,
                gp + (t >= t_lo ? gpool_off(cr, t) - base : 0), nullptr, st, N, lane, keyed);
@@ -1966,7 +1982,7 @@ __device__ void dp_ft_banded(const E2Tables &tb, const DpSmem &sm, const ChainRe
     uint64_t t0 = E2_INF64;
     if (m >= 2) {
         const int c = f8(cr.D(m - 1), 0);
-        ft_row(prefR_row(tb, r, c), tb.winR + (uint32_t)(c * N), 0, cr.TAU(1), N - 1, N - 1,
+        ft_row(prefR_row(tb, r, c), winR_row(tb, c), 0, cr.TAU(1), N - 1, N - 1,
                m - 1, gp + (gpool_off(cr, m - 1) - gpool_off(cr, g_lo)), rband_lo(cr, m - 1),
                rband_hi(cr, m - 1), H, nullptr, st, N, lane, keyed);
         t0 = uni64(H[0]);
@@ -2293,7 +2309,7 @@ __device__ void idle_masters(const E2Tables &tv, int r, const uint8_t *chain, in
                 A[x] = a;
             }
             __syncthreads();
-            const uint8_t *wr = dir ? tv.winR + (uint32_t)(c * N) : win_row(tv, 0, c);
+            const uint8_t *wr = dir ? winR_row(tv, c) : win_row(tv, 0, c);
             for (int x = lane; x <= N; x += kWave) {
                 uint64_t e = E2_INF64;
                 if (x >= 1) {
