@@ -450,12 +450,20 @@ template <typename K> __device__ __forceinline__ K kmin(K a, K b)
     if constexpr (__is_same(K, double)) return vmin_f64(a, b);
     else return a < b ? a : b;
 }
+// v permuted within each 16-lane row, as an operand of a min.  For 32-bit
+// keys the move carries the min's identity (all ones) as its old value, which
+// lets the compiler fold it into the min (one DPP min instead of a DPP move
+// and a min); the permutation is full, so no lane keeps the old value.
 template <int CTRL, typename K> __device__ __forceinline__ K dppk(K v)
 {
     if constexpr (__is_same(K, double))
         return __builtin_bit_cast(double, dpp_u64<CTRL>(__builtin_bit_cast(uint64_t, v)));
     else if constexpr (sizeof(K) == 8) return dpp_u64<CTRL>(v);
-    else return (K)(uint32_t)dpp_i32<CTRL>((int)v);
+    else {
+        static_assert(CTRL == 0xb1 || CTRL == 0x4e || CTRL == 0x140 || CTRL == 0x141,
+                      "a full permutation within each row");
+        return (K)(uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, CTRL, 0xf, 0xf, false);
+    }
 }
 template <typename K> __device__ __forceinline__ K readlane_k(K v, int lane)
 {
