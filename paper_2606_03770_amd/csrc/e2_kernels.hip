@@ -2892,41 +2892,143 @@ __device__ __forceinline__ uint64_t sm64(uint64_t x)
 constexpr uint32_t kStSelA = 0, kStSelB = 64, kStXoLabel = 128, kStXoRole = 129,
                    kStMutLabel = 130, kStMutRole = 131;
 
-__device__ __forceinline__ bool key_less(const uint64_t *w, const uint64_t *ph, uint32_t a,
-                                         uint32_t b)
+// (w, phase, index) order of two keys held in registers
+__device__ __forceinline__ bool kless(uint64_t wa, uint64_t pa, uint32_t ia, uint64_t wb,
+                                      uint64_t pb, uint32_t ib)
 {
-    if (w[a] != w[b]) return w[a] < w[b];
-    if (ph[a] != ph[b]) return ph[a] < ph[b];
-    return a < b;
+    if (wa != wb) return wa < wb;
+    if (pa != pb) return pa < pb;
+    return ia < ib;
 }
 
-// n_elite rounds of "smallest key strictly after the previous pick".
-__global__ __launch_bounds__(1024) void k_elites(int P, uint32_t n_elite,
-                                                 const uint64_t *__restrict__ w,
-                                                 const uint64_t *__restrict__ ph,
-                                                 uint32_t *elite)
+// The least key of the 32 lanes of each half-wave, in every lane of the half
+// (xor shuffles that stay within the half).  The sentinel (all ones, index
+// 0xFFFFFFFF) loses to every key of a genome.
+__device__ __forceinline__ void half_wave_min_key(uint64_t &bw, uint64_t &bp, uint32_t &bi)
 {
-    __shared__ uint32_t cand[1024];
-    const int t = threadIdx.x;
-    uint32_t last = 0xFFFFFFFFu;
+#pragma unroll
+    for (int o = 16; o >= 1; o >>= 1) {
+        const uint64_t ow = __shfl_xor(bw, o, kWave), op = __shfl_xor(bp, o, kWave);
+        const uint32_t oi = __shfl_xor(bi, o, kWave);
+        if (kless(ow, op, oi, bw, bp, bi)) {
+            bw = ow;
+            bp = op;
+            bi = oi;
+        }
+    }
+}
+
+// Tournament selection of both parents: parent a takes the least key among
+// its tk draws (draw t from stream kStSelA + t), parent b among its own
+// (stream kStSelB + t).  Lanes 0-31 hold a's draws, lanes 32-63 b's (two per
+// lane when tk > 32), so that every draw's key is loaded at once; the least
+// key of a set does not depend on the order of its draws.
+__device__ __forceinline__ void tournament_pair(const uint64_t *__restrict__ w,
+                                                const uint64_t *__restrict__ ph, uint64_t hs,
+                                                uint32_t P, uint32_t tk, int lane, uint32_t &a,
+                                                uint32_t &b)
+{
+    const uint32_t st0 = lane < 32 ? kStSelA : kStSelB;
+    uint64_t bw = ~0ull, bp = ~0ull;
+    uint32_t bi = 0xFFFFFFFFu;
+    for (uint32_t t = (uint32_t)(lane & 31); t < tk; t += 32) {
+        const uint64_t u = sm64(sm64(hs ^ (uint64_t)(st0 + t)) ^ 0ull);
+        const uint32_t idx = (uint32_t)(((u >> 32) * (uint64_t)P) >> 32);
+        const uint64_t kw = w[idx], kp = ph[idx];
+        if (kless(kw, kp, idx, bw, bp, bi)) {
+            bw = kw;
+            bp = kp;
+            bi = idx;
+        }
+    }
+    half_wave_min_key(bw, bp, bi);
+    a = (uint32_t)__builtin_amdgcn_readlane((int)bi, 0);
+    b = (uint32_t)__builtin_amdgcn_readlane((int)bi, 32);
+}
+
+// n_elite rounds of "smallest key strictly after the previous pick".  Each
+// thread holds up to kEliteKeys keys in registers (populations of up to
+// 16384 genomes; larger ones read theirs every round); a round reduces over
+// each wave with shuffles and over the 16 waves through LDS.
+constexpr int kEliteThreads = 1024, kEliteKeys = 16;
+__global__ __launch_bounds__(kEliteThreads) void k_elites(int P, uint32_t n_elite,
+                                                          const uint64_t *__restrict__ w,
+                                                          const uint64_t *__restrict__ ph,
+                                                          uint32_t *elite)
+{
+    constexpr int kWaves = kEliteThreads / kWave;
+    __shared__ uint64_t rw[kWaves], rp[kWaves];
+    __shared__ uint32_t ri[kWaves];
+    const int t = threadIdx.x, lane = t % kWave, wv = t / kWave;
+    const bool held = P <= kEliteThreads * kEliteKeys;
+    uint64_t kw[kEliteKeys], kp[kEliteKeys];
+    if (held) {
+#pragma unroll
+        for (int i = 0; i < kEliteKeys; ++i) {
+            const int p = min(t + kEliteThreads * i, P - 1);  // in-range loads, no branch
+            kw[i] = w[p];
+            kp[i] = ph[p];
+        }
+    }
+    bool have_last = false;  // no previous pick: every key qualifies
+    uint64_t lw = 0, lp = 0;
+    uint32_t li = 0;
     for (uint32_t e = 0; e < n_elite; ++e) {
-        uint32_t pick = 0xFFFFFFFFu;
-        for (int p = t; p < P; p += blockDim.x) {
-            if (last != 0xFFFFFFFFu && !key_less(w, ph, last, (uint32_t)p)) continue;
-            if (pick == 0xFFFFFFFFu || key_less(w, ph, (uint32_t)p, pick)) pick = (uint32_t)p;
-        }
-        cand[t] = pick;
-        __syncthreads();
-        for (int s = blockDim.x / 2; s >= 1; s >>= 1) {
-            if (t < s) {
-                const uint32_t a = cand[t], b = cand[t + s];
-                if (b != 0xFFFFFFFFu && (a == 0xFFFFFFFFu || key_less(w, ph, b, a))) cand[t] = b;
+        uint64_t bw = ~0ull, bp = ~0ull;
+        uint32_t bi = 0xFFFFFFFFu;
+        if (held) {
+#pragma unroll
+            for (int i = 0; i < kEliteKeys; ++i) {
+                const uint32_t p = (uint32_t)(t + kEliteThreads * i);
+                if (p < (uint32_t)P && (!have_last || kless(lw, lp, li, kw[i], kp[i], p)) &&
+                    kless(kw[i], kp[i], p, bw, bp, bi)) {
+                    bw = kw[i];
+                    bp = kp[i];
+                    bi = p;
+                }
             }
-            __syncthreads();
+        } else {
+            for (int p = t; p < P; p += kEliteThreads) {
+                const uint64_t xw = w[p], xp = ph[p];
+                if ((!have_last || kless(lw, lp, li, xw, xp, (uint32_t)p)) &&
+                    kless(xw, xp, (uint32_t)p, bw, bp, bi)) {
+                    bw = xw;
+                    bp = xp;
+                    bi = (uint32_t)p;
+                }
+            }
         }
-        last = cand[0];
-        if (t == 0) elite[e] = last;
+        half_wave_min_key(bw, bp, bi);
+        {  // the two halves of the wave
+            const uint64_t ow = __shfl_xor(bw, 32, kWave), op = __shfl_xor(bp, 32, kWave);
+            const uint32_t oi = __shfl_xor(bi, 32, kWave);
+            if (kless(ow, op, oi, bw, bp, bi)) {
+                bw = ow;
+                bp = op;
+                bi = oi;
+            }
+        }
+        if (lane == 0) {
+            rw[wv] = bw;
+            rp[wv] = bp;
+            ri[wv] = bi;
+        }
         __syncthreads();
+        bw = rw[0];
+        bp = rp[0];
+        bi = ri[0];
+        for (int j = 1; j < kWaves; ++j)
+            if (kless(rw[j], rp[j], ri[j], bw, bp, bi)) {
+                bw = rw[j];
+                bp = rp[j];
+                bi = ri[j];
+            }
+        __syncthreads();  // every thread has read the wave results
+        if (t == 0) elite[e] = bi;
+        have_last = bi != 0xFFFFFFFFu;
+        lw = bw;
+        lp = bp;
+        li = bi;
     }
 }
 
@@ -2950,36 +3052,37 @@ __global__ __launch_bounds__(64) void k_breed(int M, int P, int k_max,
         return;
     }
     const uint64_t hs = sm64(sm64(seed ^ (uint64_t)g) ^ (uint64_t)s);  // (seed, g, s) prefix
-    // lane 0 runs the tournament of parent a, lane 1 that of parent b
-    uint32_t win = 0;
-    if (lane < 2) {
-        const uint32_t st0 = lane == 0 ? kStSelA : kStSelB;
-        uint32_t best = 0xFFFFFFFFu;
-        for (uint32_t t = 0; t < tk; ++t) {
-            const uint64_t u = sm64(sm64(hs ^ (uint64_t)(st0 + t)) ^ 0ull);
-            const uint32_t idx = (uint32_t)(((u >> 32) * (uint64_t)P) >> 32);
-            if (best == 0xFFFFFFFFu || key_less(w, ph, idx, best)) best = idx;
-        }
-        win = best;
-    }
-    const uint32_t a = __shfl(win, 0, kWave);
-    const uint32_t b = __shfl(win, 1, kWave);
+    uint32_t a, b;
+    tournament_pair(w, ph, hs, (uint32_t)P, tk, lane, a, b);
     const uint64_t h_xl = sm64(hs ^ kStXoLabel), h_ml = sm64(hs ^ kStMutLabel);
     const uint64_t h_xr = sm64(hs ^ kStXoRole), h_mr = sm64(hs ^ kStMutRole);
-    for (int d = lane; d < M; d += kWave) {
-        const uint64_t u = sm64(h_xl ^ (uint64_t)d);
-        uint8_t v = ((uint32_t)u < xo) ? labels_in[(size_t)b * M + d] : labels_in[(size_t)a * M + d];
-        const uint64_t z = sm64(h_ml ^ (uint64_t)d);
-        if ((uint32_t)(z >> 32) < mut) v = (uint8_t)(((uint64_t)(uint32_t)z * (uint64_t)k_max) >> 32);
-        lo[d] = v;
+    // every gene's parent byte is loaded before any is used (gene lane + 64 t
+    // in slot t; clamped indices past the row, whose results are not stored)
+    constexpr int kSlots = (E2_MAX_DEV + kWave - 1) / kWave;
+    uint8_t pl[kSlots], pr[kSlots];
+#pragma unroll
+    for (int t = 0; t < kSlots; ++t) {
+        const int d = lane + kWave * t;
+        const uint32_t src = (uint32_t)sm64(h_xl ^ (uint64_t)d) < xo ? b : a;
+        pl[t] = labels_in[(size_t)src * M + min(d, M - 1)];
+        const uint32_t srq = (uint32_t)sm64(h_xr ^ (uint64_t)d) < xo ? b : a;
+        pr[t] = roles_in[(size_t)srq * k_max + min(d, k_max - 1)];
     }
-    for (int q = lane; q < k_max; q += kWave) {
-        const uint64_t u = sm64(h_xr ^ (uint64_t)q);
-        uint8_t v = ((uint32_t)u < xo) ? roles_in[(size_t)b * k_max + q] : roles_in[(size_t)a * k_max + q];
-        v = v != 0;
-        const uint64_t z = sm64(h_mr ^ (uint64_t)q);
-        if ((uint32_t)(z >> 32) < mut) v ^= 1u;
-        ro[q] = v;
+#pragma unroll
+    for (int t = 0; t < kSlots; ++t) {
+        const int d = lane + kWave * t;
+        if (d < M) {
+            uint8_t v = pl[t];
+            const uint64_t z = sm64(h_ml ^ (uint64_t)d);
+            if ((uint32_t)(z >> 32) < mut) v = (uint8_t)(((uint64_t)(uint32_t)z * (uint64_t)k_max) >> 32);
+            lo[d] = v;
+        }
+        if (d < k_max) {
+            uint8_t v = pr[t] != 0;
+            const uint64_t z = sm64(h_mr ^ (uint64_t)d);
+            if ((uint32_t)(z >> 32) < mut) v ^= 1u;
+            ro[d] = v;
+        }
     }
 }
 
@@ -3030,19 +3133,8 @@ __global__ __launch_bounds__(64) void k_breed_ordered(
         return;
     }
     const uint64_t hs = sm64(sm64(seed ^ (uint64_t)g) ^ (uint64_t)s);  // (seed, g, s) prefix
-    uint32_t win = 0;
-    if (lane < 2) {
-        const uint32_t st0 = lane == 0 ? kStSelA : kStSelB;
-        uint32_t best = 0xFFFFFFFFu;
-        for (uint32_t t = 0; t < tk; ++t) {
-            const uint64_t u = sm64(sm64(hs ^ (uint64_t)(st0 + t)) ^ 0ull);
-            const uint32_t idx = (uint32_t)(((u >> 32) * (uint64_t)P) >> 32);
-            if (best == 0xFFFFFFFFu || key_less(w, ph, idx, best)) best = idx;
-        }
-        win = best;
-    }
-    const uint32_t a = __shfl(win, 0, kWave);
-    const uint32_t b = __shfl(win, 1, kWave);
+    uint32_t a, b;
+    tournament_pair(w, ph, hs, (uint32_t)P, tk, lane, a, b);
     const uint8_t *A = order_in + (size_t)a * M;
     const uint8_t *B = order_in + (size_t)b * M;
     const uint64_t lt = (1ull << lane) - 1;
