@@ -722,24 +722,11 @@ __device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K
     return best;
 }
 
-template <int S, typename K>
-__device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int lane, int N)
+// The staged pairs of a row for split points j = jmin..hi: a = max(prev(j-1),
+// tau) << 8 | j and s = (P[j] << 8) - j, then the barrier before the scans.
+template <typename K>
+__device__ __forceinline__ void stage_pairs(const Row<K> &rw, PS<K> *ps, int lane, int jmin)
 {
-    constexpr int CPP = kWave / S;  // cells per pass
-    const int o = lane % S;
-    const int cl = lane / S;
-    const int jmin = max(rw.kmin, rw.lo - rw.cap + 1);
-    // first pass's cell loads go out before the split points are built
-    // (lanes past the row load its last cell, which they compute again)
-    int w_nx;
-    K p_nx;  // P[i+1] << 8
-    K b_nx = 0;
-    {
-        const int i = min(rw.lo + cl, rw.hi);
-        w_nx = rw.wr[i];
-        p_nx = prefix8(rw, (uint32_t)(i + 1));
-        if (ro.combine) b_nx = combine_b(i, N, ro);
-    }
     // both loads of an entry go out before either is waited for: the
     // previous-row value comes from a clamped index and is replaced by INF
     // outside the previous band
@@ -773,6 +760,27 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
         ps[j].s = sj - (K)j;
     }
     __syncthreads();
+}
+
+template <int S, typename K>
+__device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, PS<K> *ps, int lane, int N)
+{
+    constexpr int CPP = kWave / S;  // cells per pass
+    const int o = lane % S;
+    const int cl = lane / S;
+    const int jmin = max(rw.kmin, rw.lo - rw.cap + 1);
+    // first pass's cell loads go out before the split points are built
+    // (lanes past the row load its last cell, which they compute again)
+    int w_nx;
+    K p_nx;  // P[i+1] << 8
+    K b_nx = 0;
+    {
+        const int i = min(rw.lo + cl, rw.hi);
+        w_nx = rw.wr[i];
+        p_nx = prefix8(rw, (uint32_t)(i + 1));
+        if (ro.combine) b_nx = combine_b(i, N, ro);
+    }
+    stage_pairs(rw, ps, lane, jmin);
     const int L = min(rw.cap, rw.hi - jmin + 1);
     const int Lm = max(0, min(rw.lmin, rw.lo - jmin + 1));
     const int t_all = (L + S - 1) / S;
@@ -809,6 +817,60 @@ __device__ __forceinline__ K row_pass_s(const Row<K> &rw, const RowOut<K> &ro, P
     }
     __syncthreads();
     return acc;
+}
+
+// A master's combine (row mu of its table, rc) and the forward row F_mu
+// without a master (rf) in one pass, one half-wave each: both rows run on
+// device mu over the same band and read the same staged pairs of F_{mu-1}
+// (the combine adds the head time and keeps the head-bytes window, whose
+// stages are the shorter, so the forward row's staging range covers it).
+// Rows of at most 32 cells (one pass per half, S2 lanes per cell).  Lanes
+// 0-31 return the combine's keys as row_pass does (INF in lanes 32-63);
+// lanes 32-63 leave their cell's value, split point and index in fv, fb and
+// fi, which the caller stores once it knows that the sweep goes on (F_mu
+// replaces F_{mu-1} in place).
+template <int S2, typename K>
+__device__ __forceinline__ K row_pass_pair_s(const Row<K> &rc, const Row<K> &rf,
+                                             const RowOut<K> &ro, PS<K> *ps, int lane, int N,
+                                             K &fv, int &fb, int &fi)
+{
+    const bool fwd = lane >= kWave / 2;
+    const int l = lane % (kWave / 2);
+    const int o = l % S2;
+    const int cl = l / S2;
+    const int jmin = max(rf.kmin, rf.lo - rf.cap + 1);
+    // the cell loads go out before the pairs are staged
+    const int i = min(rf.lo + cl, rf.hi);
+    const int w = (fwd ? rf.wr : rc.wr)[i];
+    const K p1 = prefix8(rf, (uint32_t)(i + 1));
+    const K b = combine_b(i, N, ro);
+    stage_pairs(rf, ps, lane, jmin);
+    // uniform scan bounds: the longer stages' range, the shorter windows' bound
+    const int L = min(rf.cap, rf.hi - jmin + 1);
+    const int Lm = max(0, min(min(rf.lmin, rc.lmin), rf.lo - jmin + 1));
+    const int t_all = (L + S2 - 1) / S2;
+    const int t_safe = Lm / S2;
+    const int i_idle = jmin + (Lm > 0 ? Lm - 1 : 0);
+    const bool act = w != (int)E2_NO_START;
+    const int ie = act ? i : i_idle;
+    const int jlo = act ? max(w, jmin) : jmin;
+    const K si1 = p1 + (fwd ? rf.hadd8 : rc.hadd8);
+    const K best = scan_cell<S2>(ps, ie, jlo, o, si1, t_safe, t_all);
+    const K v = act ? unpack_val(best) : KeyT<K>::inf;
+    fv = v;
+    fb = key_low8(best);
+    fi = i - rf.lo;
+    return fwd ? KeyT<K>::inf : combine_key(v, b, ro.mu);
+}
+
+template <typename K>
+__device__ __forceinline__ K row_pass_pair(const Row<K> &rc, const Row<K> &rf, const RowOut<K> &ro,
+                                           PS<K> *ps, int lane, int N, K &fv, int &fb, int &fi)
+{
+    const int n = rf.hi - rf.lo + 1;
+    if (n <= 8) return row_pass_pair_s<4>(rc, rf, ro, ps, lane, N, fv, fb, fi);
+    if (n <= 16) return row_pass_pair_s<2>(rc, rf, ro, ps, lane, N, fv, fb, fi);
+    return row_pass_pair_s<1>(rc, rf, ro, ps, lane, N, fv, fb, fi);
 }
 
 // Store mode returns INF; combine mode returns the lane's running minimum of
@@ -1366,6 +1428,26 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
                 ro.glo = rband_lo(cr, t);
                 ro.ghi = rband_hi(cr, t);
                 ro.tau_next = to_k<K>(cr.TAU(mu));  // link mu -> mu+1
+            }
+            // with a previous row and a band of at most 32 cells, F_mu rides
+            // along in the other half-wave and is stored only if the sweep
+            // goes on
+            const int n = rw.hi - rw.lo + 1;
+            if (mu >= 2 && mu < m && n >= 1 && n <= kWave / 2) {
+                Row<K> f = fwd_row_of<K>(tb, cr, r, mu, 0);
+                set_prev(f, F, band_lo(cr, mu - 1), band_hi(cr, mu - 1));
+                K fv;
+                int fb, fi;
+                acc = kmin(acc, row_pass_pair(rw, f, ro, ps, lane, N, fv, fb, fi));
+                key = wave_min_k(acc);
+                if (unpack_val(key) == tn) break;
+                if (lane >= kWave / 2) {  // the S2 lanes of a cell store the same
+                    F[fi] = fv;
+                    sm.tbp[pool_off(cr, mu) + fi] = (uint8_t)fb;
+                }
+                __syncthreads();
+                f_last = mu;
+                continue;
             }
             acc = kmin(acc, row_pass(rw, ro, ps, lane, N));
             key = wave_min_k(acc);
