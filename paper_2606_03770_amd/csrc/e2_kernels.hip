@@ -1409,6 +1409,7 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
     K acc = KeyT<K>::inf;
     K key = KeyT<K>::inf;
     int f_last = 0;  // the forward row the buffer holds
+    bool kept = false;  // the buffer holds row mu* of the chosen master's table
     for (int mu = 1; mu <= m; ++mu) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, mu, mu);
         if (rw.cap > 0) {
@@ -1440,7 +1441,18 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
                 int fb, fi;
                 acc = kmin(acc, row_pass_pair(rw, f, ro, ps, lane, N, fv, fb, fi));
                 key = wave_min_k(acc);
-                if (unpack_val(key) == tn) break;
+                if (unpack_val(key) == tn) {
+                    // mu is the chosen master (the first to reach T0), and the
+                    // combine half holds row mu of its table: keep that row,
+                    // values over F_{mu-1}, split points in tbp
+                    if (lane < kWave / 2) {
+                        F[fi] = fv;
+                        sm.tbp[pool_off(cr, mu) + fi] = (uint8_t)fb;
+                    }
+                    __syncthreads();
+                    kept = true;
+                    break;
+                }
                 if (lane >= kWave / 2) {  // the S2 lanes of a cell store the same
                     F[fi] = fv;
                     sm.tbp[pool_off(cr, mu) + fi] = (uint8_t)fb;
@@ -1469,15 +1481,16 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
     // ---- rows mu*..m-1 of the chosen master's table (split points overwrite
     // those of F), then cell N-1 of row m.  Their first row reads F_{mu*-1},
     // which the buffer holds unless the sweep went past it: then F_1..F_{mu*-1}
-    // are computed again (their split points are in tbp already).
-    if (best_mu >= 2 && f_last != best_mu - 1) {
+    // are computed again (their split points are in tbp already).  A sweep
+    // that stopped in a paired pass has left row mu* itself in the buffer.
+    if (!kept && best_mu >= 2 && f_last != best_mu - 1) {
         for (int k = 1; k < best_mu; ++k) {
             Row<K> f = fwd_row_of<K>(tb, cr, r, k, 0);
             if (k >= 2) set_prev(f, F, band_lo(cr, k - 1), band_hi(cr, k - 1));
             row_pass(f, store_to<K>(F, nullptr), ps, lane, N);
         }
     }
-    for (int k = best_mu; k < m; ++k) {
+    for (int k = kept ? best_mu + 1 : best_mu; k < m; ++k) {
         Row<K> rw = fwd_row_of<K>(tb, cr, r, k, best_mu);
         if (k >= 2) set_prev(rw, F, band_lo(cr, k - 1), band_hi(cr, k - 1));
         row_pass(rw, store_to<K>(F, sm.tbp + pool_off(cr, k)), ps, lane, N);
