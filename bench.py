@@ -74,6 +74,7 @@ def log(msg):
 # ---------------------------------------------------------------------------
 MAX_BANDED_CHAIN = 64  # longest chain the banded DP path takes (one device per lane)
 LDS_TB_CELLS = 2048    # split-point bytes a DP wave keeps in LDS
+PAIR_MAX_CELLS = 32    # widest band whose combine and forward row share one pass
 
 
 def pool_cells(N):
@@ -329,6 +330,16 @@ def generation_work(wl, problems, roles, T, master, tabs, T0):
                 v0 = rows(0, chf[:, m - 1], jm, np.full(len(chf), N - 1), np.full(len(chf), N - 1))
                 v1 = rows(1, chf[:, m - 1], jm, np.full(len(chf), N - 1), np.full(len(chf), N - 1))
                 tot_f += np.where(ff, np.where(isn, v1, v0), 0)
+            # a sweep that stops at mu* in a paired pass (2 <= mu* <= m-1,
+            # a band of at most 32 cells) also evaluates F_mu* in the other
+            # half-wave and keeps the combine's row as the chosen master's
+            # row mu*, which is then not computed again
+            idx = np.clip(muf - 1, 0, m - 1)[:, None]
+            n_mu = np.take_along_axis(np.where(hif >= lof, hif - lof + 1, 0), idx, 1)[:, 0]
+            paired = (tf == t0f) & (t0f != INF) & (muf >= 2) & (muf <= m - 1) & \
+                (n_mu >= 1) & (n_mu <= PAIR_MAX_CELLS)
+            tot_f += np.where(paired, np.take_along_axis(fwd, idx, 1)[:, 0] -
+                              np.take_along_axis(comb, idx, 1)[:, 0], 0)
             cand32 += int(tot_f.sum())
         # --- reference path
         if (~fast).any():

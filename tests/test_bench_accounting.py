@@ -104,15 +104,21 @@ def _direct(wl, problems, roles, T, master, T0):
             # up to the first master whose optimum is the optimum without one
             t0 = int(T0[p, q])
             last = 0 if t0 == INF else (mu if int(T[p, q]) == t0 else m)
+            # a stop in a paired pass (combine and forward row of one master
+            # in one pass, bands of at most 32 cells): the forward row of the
+            # stopping master is evaluated too, and the combine's row stands
+            # for the chosen master's first row
+            paired_stop = (last == mu and 2 <= mu <= m - 1 and
+                           1 <= fhi[mu] - flo[mu] + 1 <= bench.PAIR_MAX_CELLS)
             for mm in range(1, last + 1):
                 if mm >= 2 and cH[mm - 1] > 0:               # combine of master mm
                     c += cnt(win[1][ch[mm - 1]], max(mm - 1, flo[mm] - cH[mm - 1] + 1),
                              flo[mm], fhi[mm])
-                if 2 <= mm < last and mm < m:                # forward row mm
+                if (2 <= mm < last or (paired_stop and mm == last)) and mm < m:  # forward row mm
                     c += cnt(win[0][ch[mm - 1]], max(mm - 1, flo[mm] - c0[mm - 1] + 1),
                              flo[mm], fhi[mm])
             if mu:                                           # chosen master's rows
-                for k in range(max(mu, 2), m):
+                for k in range(max(mu + int(paired_stop), 2), m):
                     f = int(k == mu)
                     cp = cH[k - 1] if f else c0[k - 1]
                     c += cnt(win[f][ch[k - 1]], max(k - 1, flo[k] - cp + 1), flo[k], fhi[k])
