@@ -204,8 +204,10 @@ def generation_work(wl, problems, roles, T, master, tabs, T0):
     candidate count follows k_dp row by row: reversed rows, the last cell of
     the full reversed table (T0), then masters in ascending position with
     the forward row after each, up to the first master whose optimum is T0
-    (every master when T0 < T, none when T0 is infinite), then the chosen
-    master's rows and last cell (banded path); or one full table per master
+    (every master when T0 < T, none when T0 is infinite; a stop in a pass
+    that pairs the combine with the forward row evaluates that forward row
+    too and keeps the combine's row as the chosen master's first), then the
+    chosen master's rows and last cell (banded path); or one full table per master
     plus the chosen master's again (reference path, u64 keys).  A problem takes the
     banded path when its chain has at most 64 devices, its forward bands fit
     the pool and either every finite value it can produce (largest fitting
