@@ -873,6 +873,45 @@ __device__ __forceinline__ K row_pass_pair(const Row<K> &rc, const Row<K> &rf, c
     return row_pass_pair_s<1>(rc, rf, ro, ps, lane, N, fv, fb, fi);
 }
 
+// Cell N-1 of a row (lo = hi = N-1) without staging: one lane per split point
+// j of its window, each candidate formed from the previous row and the prefix
+// sums directly, then one wave minimum.  The same candidates and tie rule as
+// row_pass on a one-cell row; returns the packed key (value << 8 | j), INF
+// when no stage ending at block N-1 fits the device.
+template <typename K>
+__device__ __forceinline__ K single_cell_key(const Row<K> &rw, int lane, int N)
+{
+    const int i = N - 1;
+    const int w = rw.wr[i];
+    K best = KeyT<K>::inf;
+    if (w != (int)E2_NO_START) {
+        const int jlo = max(w, max(rw.kmin, rw.lo - rw.cap + 1));
+        const K si1 = prefix8(rw, (uint32_t)(i + 1)) + rw.hadd8;
+        // previous-row entry x = j-1-plo, INF outside [0, span] (as stage_pairs)
+        const int pspan = rw.phi - rw.plo;
+        const int plo_e = pspan < 0 ? -2 : rw.plo;
+        const uint32_t span = pspan < 0 ? 0u : (uint32_t)pspan;
+        for (int j0 = jlo; j0 <= i; j0 += kWave) {
+            const int j = min(j0 + lane, i);  // lanes past the window repeat j = i
+            const uint32_t ux = (uint32_t)(j - 1 - plo_e);
+            const uint32_t pxc = min(ux, span);
+            const bool in = ux <= span;
+            K pv;
+            if constexpr (__is_same(K, double)) {
+                const uint64_t bits = reinterpret_cast<const lds_t<uint64_t> *>(rw.prev)[pxc];
+                pv = __builtin_bit_cast(double, in ? bits : 0x7FF0000000000000ull);
+            } else {
+                pv = inf_unless(rw.prev[pxc], in);
+            }
+            PS<K> e;
+            e.a = pack_prev(pv, rw.tau, j);
+            e.s = prefix8(rw, (uint32_t)j) - (K)j;
+            best = kmin(best, cand(e, si1));
+        }
+    }
+    return wave_min_k(best);
+}
+
 // Store mode returns INF; combine mode returns the lane's running minimum of
 // (max(value, B) << 8 | mu) (the caller reduces over the wave once).
 template <typename K>
@@ -1391,9 +1430,7 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         set_prev(g, gp + (gpool_off(cr, m - 1) - gpool_off(cr, g_lo)), rband_lo(cr, m - 1),
                  rband_hi(cr, m - 1));
         g.lo = g.hi = N - 1;
-        g.lmin = uni(minwinR_at(tb, f8(cr.D(m - 1), 0), N - 1));
-        row_pass(g, store_to<K>(F, nullptr), ps, lane, N);
-        tn = uni_k(F[0]);
+        tn = unpack_val(single_cell_key(g, lane, N));
         if (tn == KeyT<K>::inf) {
             *T_out = E2_INF64;
             *mu_out = 0;
@@ -1500,9 +1537,8 @@ __device__ __forceinline__ void dp_banded(const E2Tables &tb, const DpSmem &sm, 
         // row m-1 of the chosen table (F_{m-1} when mu* = m: the sweep's last row)
         set_prev(rw, F, band_lo(cr, m - 1), band_hi(cr, m - 1));
         rw.lo = rw.hi = N - 1;
-        rw.lmin = minwin_at(tb, best_mu == m, f8(cr.A(m - 1), 0), N - 1);
-        rw.lmin = uni(rw.lmin);
-        row_pass(rw, store_to<K>(F, last_tb), ps, lane, N);
+        const K lk = single_cell_key(rw, lane, N);
+        if (lane == 0) *last_tb = (uint8_t)key_low8(lk);
         // the split points may sit in global memory (long bands): complete
         // every lane's stores before lane 0 walks them
         __builtin_amdgcn_s_waitcnt(0);
