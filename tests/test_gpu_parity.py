@@ -177,6 +177,55 @@ def test_master_sweep_stops_and_runs_through(torch_dev, seed):
                      "through, one row past", "through, two or more rows past"}
 
 
+def test_paired_pass_band_widths_and_single_cells(torch_dev):
+    """The master sweep pairs a master's combine with the forward row after
+    it when the band holds at most 32 cells, and a sweep that stops there
+    keeps the combine's row as the chosen master's first row; wider bands
+    take separate passes; the optimum without a master and the chosen
+    table's last cell are single-cell reductions whose windows can exceed
+    one wave.  Tight memory (22-40 layers per device over 140 blocks) gives
+    stops at masters with bands on both sides of 32 cells, roomy memory
+    (30-90 layers over 120 blocks) wider bands and first-device windows past
+    64 blocks; every kind occurs and every output equals the oracle."""
+    import bench
+    kinds = set()
+    for seed, N, lo, hi in [(700, 140, 22, 40), (701, 140, 22, 40), (702, 140, 22, 40),
+                            (700, 120, 30, 90)]:
+        wl = workload.random_small(seed, M=24, N=N, P=12, k_max=5, mem_lo_layers=lo,
+                                   mem_hi_layers=hi)
+        wl = dataclasses.replace(wl, head_flops=np.array([2 * 10**11] * 2, np.uint64),
+                                 head_bytes=10**8)
+        print(f"paired-pass case seed={seed} N={N} memory {lo}-{hi} layers", flush=True)
+        want = _oracle_all(wl)
+        _assert_equal(_gpu_all(torch_dev, wl), want, tag=f"paired {seed}")
+        free = dataclasses.replace(wl, head_flops=np.zeros(2, np.uint64), head_bytes=0)
+        T0 = _oracle_all(free)["T"]
+        _, _, cap = bench.window_tables(wl)
+        for p in range(wl.population):
+            for q in range(wl.k_max):
+                ch = np.nonzero(wl.labels[p] == q)[0]
+                m = len(ch)
+                if m == 0 or want["T"][p, q] == INF:
+                    continue
+                c0 = cap[0][ch]
+                pre = np.concatenate([[0], np.cumsum(c0)])
+                mu = int(np.nonzero(ch == want["master"][p, q])[0][0]) + 1
+                lo_b = max(mu - 1, N - 1 - (pre[m] - pre[mu]))
+                hi_b = min(N - 1 - (m - mu), pre[mu] - 1)
+                n = hi_b - lo_b + 1
+                if want["T"][p, q] == T0[p, q] and 2 <= mu <= m - 1:
+                    kinds.add("paired stop" if n <= 32 else
+                              "stop, band 33-64" if n <= 64 else "stop, band past 64")
+                elif want["T"][p, q] == T0[p, q]:
+                    kinds.add("stop at the first or last device")
+                else:
+                    kinds.add("through")
+                if c0[0] > 64:
+                    kinds.add("T0 window past 64")
+    assert kinds == {"paired stop", "stop, band 33-64", "stop, band past 64",
+                     "stop at the first or last device", "through", "T0 window past 64"}
+
+
 def test_uniform_layers_many_ties(torch_dev):
     """Identical blocks and devices: every master and many split points tie."""
     wl = workload.random_small(5, M=30, N=40, P=12, k_max=3, layer_var=False,
