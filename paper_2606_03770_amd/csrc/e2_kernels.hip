@@ -722,18 +722,32 @@ __device__ __forceinline__ K scan_cell(const PS<K> *ps, int i, int jlo, int o, K
     return best;
 }
 
+// The previous row's value at block j-1, INF outside its band [plo, phi].
+// Entry x = j-1-plo as an unsigned offset: outside [0, span] (x < 0 wraps
+// above it) the entry is INF and the read goes to a clamped, in-range slot,
+// so that the load is not put under a branch.  An empty previous band moves
+// plo to -2 (plo_e), which puts every x above span = 0.
+template <typename K>
+__device__ __forceinline__ K prev_value(const Row<K> &rw, int j, int plo_e, uint32_t span)
+{
+    const uint32_t ux = (uint32_t)(j - 1 - plo_e);
+    const uint32_t pxc = min(ux, span);
+    const bool in = ux <= span;
+    if constexpr (__is_same(K, double)) {
+        // select on the bit pattern (INF = 0x7FF0000000000000)
+        const uint64_t bits = reinterpret_cast<const lds_t<uint64_t> *>(rw.prev)[pxc];
+        return __builtin_bit_cast(double, in ? bits : 0x7FF0000000000000ull);
+    } else {  // all ones (INF) outside the previous band
+        return inf_unless(rw.prev[pxc], in);
+    }
+}
+
 // The staged pairs of a row for split points j = jmin..hi: a = max(prev(j-1),
 // tau) << 8 | j and s = (P[j] << 8) - j, then the barrier before the scans.
 template <typename K>
 __device__ __forceinline__ void stage_pairs(const Row<K> &rw, PS<K> *ps, int lane, int jmin)
 {
-    // both loads of an entry go out before either is waited for: the
-    // previous-row value comes from a clamped index and is replaced by INF
-    // outside the previous band
-    // Entry x = j-1-plo of the previous row, as an unsigned offset: outside
-    // [0, span] (x < 0 wraps above it) the entry is INF and the read goes to a
-    // clamped, in-range slot.  An empty previous band moves plo to -2, which
-    // puts every x above span = 0.
+    // both loads of an entry go out before either is waited for
     const int pspan = rw.phi - rw.plo;
     const int plo_e = pspan < 0 ? -2 : rw.plo;
     const uint32_t span = pspan < 0 ? 0u : (uint32_t)pspan;
@@ -741,19 +755,8 @@ __device__ __forceinline__ void stage_pairs(const Row<K> &rw, PS<K> *ps, int lan
     // same values to the same slot
     for (int j0 = jmin; j0 <= rw.hi; j0 += kWave) {
         const int j = min(j0 + lane, rw.hi);
-        const uint32_t ux = (uint32_t)(j - 1 - plo_e);
-        const uint32_t pxc = min(ux, span);
-        const bool in = ux <= span;
         const K sj = prefix8(rw, (uint32_t)j);
-        K pv;
-        if constexpr (__is_same(K, double)) {
-            // select on the bit pattern so that the load is not put under a
-            // branch (INF = 0x7FF0000000000000)
-            const uint64_t bits = reinterpret_cast<const lds_t<uint64_t> *>(rw.prev)[pxc];
-            pv = __builtin_bit_cast(double, in ? bits : 0x7FF0000000000000ull);
-        } else {  // all ones (INF) outside the previous band, without a branch
-            pv = inf_unless(rw.prev[pxc], in);
-        }
+        const K pv = prev_value(rw, j, plo_e, span);
         ps[j].a = pack_prev(pv, rw.tau, j);
         // (P[j] << 8) - j; fp64: exact, may be negative when blocks take 0 ns;
         // integers: modular, only differences are used
@@ -887,24 +890,13 @@ __device__ __forceinline__ K single_cell_key(const Row<K> &rw, int lane, int N)
     if (w != (int)E2_NO_START) {
         const int jlo = max(w, max(rw.kmin, rw.lo - rw.cap + 1));
         const K si1 = prefix8(rw, (uint32_t)(i + 1)) + rw.hadd8;
-        // previous-row entry x = j-1-plo, INF outside [0, span] (as stage_pairs)
         const int pspan = rw.phi - rw.plo;
         const int plo_e = pspan < 0 ? -2 : rw.plo;
         const uint32_t span = pspan < 0 ? 0u : (uint32_t)pspan;
         for (int j0 = jlo; j0 <= i; j0 += kWave) {
             const int j = min(j0 + lane, i);  // lanes past the window repeat j = i
-            const uint32_t ux = (uint32_t)(j - 1 - plo_e);
-            const uint32_t pxc = min(ux, span);
-            const bool in = ux <= span;
-            K pv;
-            if constexpr (__is_same(K, double)) {
-                const uint64_t bits = reinterpret_cast<const lds_t<uint64_t> *>(rw.prev)[pxc];
-                pv = __builtin_bit_cast(double, in ? bits : 0x7FF0000000000000ull);
-            } else {
-                pv = inf_unless(rw.prev[pxc], in);
-            }
             PS<K> e;
-            e.a = pack_prev(pv, rw.tau, j);
+            e.a = pack_prev(prev_value(rw, j, plo_e, span), rw.tau, j);
             e.s = prefix8(rw, (uint32_t)j) - (K)j;
             best = kmin(best, cand(e, si1));
         }
