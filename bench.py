@@ -398,6 +398,7 @@ def main():
     wl = workload.make(args.workload)
     P, M, K = wl.population, wl.n_dev, wl.k_max
     ctx = e2.e2_ctx_create(wl.problem_arrays())
+    e2.e2_ctx_keep_scratch(ctx)  # a serving loop: scratch kept per stream
     ctx_free = e2.e2_ctx_create(head_free(wl.problem_arrays()))  # work accounting only
     stream = torch.cuda.current_stream()
     fp = wl.fitness_params()
@@ -538,6 +539,7 @@ def config_eval(torch, dev, name, steps, warmup):
     wl = workload.make(name)
     P, K = wl.population, wl.k_max
     ctx = e2.e2_ctx_create(wl.problem_arrays())
+    e2.e2_ctx_keep_scratch(ctx)
     ctx_free = e2.e2_ctx_create(head_free(wl.problem_arrays()))
     L = torch.from_numpy(wl.labels).to(dev)
     R = torch.from_numpy(wl.roles).to(dev)
@@ -592,6 +594,7 @@ def role_search(torch, dev, steps, warmup, name=None):
     wl = workload.make(name or SEARCH_WORKLOAD)
     sm = workload.slot_model(wl)
     ctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
+    e2.e2_ctx_keep_scratch(ctx)
     L = torch.from_numpy(wl.labels).to(dev)
     fp = wl.fitness_params()
     out = e2.e2_search_roles(ctx, L, fp, wl.k_max, with_tables=True)
@@ -709,6 +712,7 @@ def ablations(torch, dev, steps, warmup):
     L = torch.from_numpy(wl.labels).to(dev)
     R = torch.from_numpy(wl.roles).to(dev)
     ctx = e2.e2_ctx_create(wl.problem_arrays())
+    e2.e2_ctx_keep_scratch(ctx)
     bn = e2.e2_eval_population(ctx, L, R, fp, with_rates=False)
     ft = e2.e2_eval_population(ctx, L, R, fp, with_rates=False, objective="finish_time")
     ms_bn = _timed(torch, lambda: e2.e2_eval_population(ctx, L, R, fp, with_rates=False, out=bn),
@@ -721,6 +725,7 @@ def ablations(torch, dev, steps, warmup):
                                                          objective="idle"), steps, warmup)
     sm = workload.slot_model(wl)
     sctx = e2.e2_ctx_create_slots(wl.problem_arrays(), sm)
+    e2.e2_ctx_keep_scratch(sctx)
     se = e2.e2_search_roles(sctx, L, fp, wl.k_max)
     sw = e2.e2_search_roles(sctx, L, fp, wl.k_max, splitwise_np_tokens=np_tok)
     ms_sw = _timed(torch, lambda: e2.e2_search_roles(sctx, L, fp, wl.k_max, out=sw,

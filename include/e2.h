@@ -21,7 +21,8 @@
  *     Every compute call is asynchronous on that stream and never
  *     synchronises the device.  Calls that need temporary device memory
  *     take it stream-ordered from HIP's default memory pool
- *     (hipMallocAsync / hipFreeAsync on the same stream).
+ *     (hipMallocAsync / hipFreeAsync on the same stream), per call, or
+ *     from a buffer the context keeps per stream (e2_ctx_keep_scratch).
  *   - INF = UINT64_MAX marks "no feasible value" in every u64 output.
  *   - A context is immutable after creation (apart from the profiling
  *     records of e2_ctx_dp_timing): one context may serve several streams
@@ -164,8 +165,30 @@ typedef struct e2_slot_model {
  */
 int e2_ctx_create_slots(const e2_problem *prob, const e2_slot_model *sm, e2_ctx **out);
 
-/* Free a context (E2_EINVAL for NULL).  Work using it must have completed. */
+/* Free a context (E2_EINVAL for NULL).  Work using it must have completed.
+ * When the context holds per-stream scratch it waits for the device
+ * (hipDeviceSynchronize) before releasing it. */
 int e2_ctx_destroy(e2_ctx *ctx);
+
+/*
+ * Per-stream scratch for serving loops: with enable = 1 the context keeps
+ * the temporary device memory of its calls (counters, problem lists, the
+ * per-cluster T and Lambda of an evaluation, the GA's elite list) in one
+ * buffer per stream, for up to 16 streams told apart by handle, instead of
+ * allocating and freeing it on the stream in every call.  A stream's buffer
+ * is allocated on it (hipMallocAsync) by its first call and grown on it
+ * (hipFreeAsync, then hipMallocAsync) when a call needs more; calls on one
+ * stream share it in stream order, calls on different streams never share
+ * one, and calls on further streams allocate per call as before.  This
+ * removes the allocation and release packets that otherwise separate
+ * consecutive calls on a stream.  Condition while it is on: a stream with
+ * calls on this context in flight is not destroyed (a new stream could
+ * take its handle and with it a buffer still in use).  enable = 0 waits
+ * for the device (hipDeviceSynchronize) and releases the buffers.  Not to
+ * be called while other host threads use ctx.  E2_EINVAL for a NULL ctx or
+ * enable outside {0, 1}; E2_ENOMEM, E2_EHIP on failure.
+ */
+int e2_ctx_keep_scratch(e2_ctx *ctx, int32_t enable);
 
 /*
  * Host-only quantisation, same formulas and errors as e2_ctx_create, for

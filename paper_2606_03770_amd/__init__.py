@@ -49,7 +49,7 @@ EXPORTED = ("e2_ctx_create", "e2_ctx_destroy", "e2_quantise", "e2_solve_partitio
             "e2_eval_population_ft", "e2_solve_partitions_idle", "e2_eval_population_idle",
             "e2_ctx_dp_timing", "e2_ctx_dp_elapsed", "e2_strerror",
             "e2_eval_population_noalloc", "e2_search_roles_ordered",
-            "e2_debug_inject_hip_error")
+            "e2_debug_inject_hip_error", "e2_ctx_keep_scratch")
 
 
 class E2Error(RuntimeError):
@@ -154,6 +154,8 @@ def lib() -> ctypes.CDLL:
     L.e2_eval_population_idle.restype = ctypes.c_int
     L.e2_debug_inject_hip_error.argtypes = [i32]
     L.e2_debug_inject_hip_error.restype = ctypes.c_int
+    L.e2_ctx_keep_scratch.argtypes = [vp, i32]
+    L.e2_ctx_keep_scratch.restype = ctypes.c_int
     L.e2_ctx_dp_timing.argtypes = [vp, i32]
     L.e2_ctx_dp_timing.restype = ctypes.c_int
     L.e2_ctx_dp_elapsed.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
@@ -254,6 +256,12 @@ def e2_debug_inject_hip_error(calls: int) -> int:
     if rc < 0:
         raise E2Error(rc, "e2_debug_inject_hip_error")
     return rc
+
+
+def e2_ctx_keep_scratch(ctx: Context, enable: bool = True):
+    """Keep each stream's call scratch in ctx between calls (True), or
+    release it and allocate per call again (False)."""
+    _check(lib().e2_ctx_keep_scratch(ctx.handle, int(bool(enable))), "e2_ctx_keep_scratch")
 
 
 def e2_ctx_dp_timing(ctx: Context, max_launches: int):

@@ -6,7 +6,9 @@
 #include <string.h>
 
 #include <atomic>
+#include <list>
 #include <mutex>
+#include <new>
 #include <vector>
 
 #include "../../include/e2.h"
@@ -145,25 +147,106 @@ int check_device(const e2_ctx *ctx)
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Stream-ordered scratch for one call.
+}  // namespace
+
+// Scratch kept per stream between calls (e2_ctx_keep_scratch).  A call's
+// temporary memory is one buffer; calls on one stream run in stream order,
+// so they can all use the same buffer, which grows (stream-ordered free,
+// then allocation) when a call needs more.  Keeping it removes the per-call
+// allocation and release packets from the stream.  Streams are told apart
+// by handle: the caller keeps every stream with calls in flight alive, so
+// that no new stream takes a handle whose buffer is still in use.  Streams
+// past the first kCachedStreams allocate and free per call.
+constexpr int kCachedStreams = 16;
+struct StreamScratch {
+    hipStream_t stream = nullptr;
+    void *base = nullptr;
+    size_t bytes = 0;
+    std::mutex mu;  // held by a call from its lookup to the end of its launches
+};
+struct ScratchCache {
+    std::mutex mu;
+    std::list<StreamScratch> entries;  // stable addresses
+};
+
+namespace {
+
+// Scratch for one call: the stream's kept buffer (locked for the call), or
+// a stream-ordered allocation of the call's own.
 struct Scratch {
     void *base = nullptr;
     hipStream_t stream = nullptr;
+    bool owned = false;
+    std::unique_lock<std::mutex> held;
     ~Scratch()
     {
-        if (base) (void)hipFreeAsync(base, stream);
+        if (owned && base) (void)hipFreeAsync(base, stream);
     }
 };
 
-int alloc_scratch(Scratch &sc, hipStream_t s, size_t bytes)
+StreamScratch *stream_entry(e2_ctx *ctx, hipStream_t s)
+{
+    ScratchCache *c = ctx->scratch_cache;
+    if (!c) return nullptr;
+    std::lock_guard<std::mutex> g(c->mu);
+    for (StreamScratch &e : c->entries)
+        if (e.stream == s) return &e;
+    if ((int)c->entries.size() >= kCachedStreams) return nullptr;
+    c->entries.emplace_back();
+    StreamScratch &e = c->entries.back();
+    e.stream = s;
+    return &e;
+}
+
+int alloc_scratch(e2_ctx *ctx, Scratch &sc, hipStream_t s, size_t bytes)
 {
     sc.stream = s;
+    if (StreamScratch *e = stream_entry(ctx, s)) {
+        sc.held = std::unique_lock<std::mutex>(e->mu);
+        if (e->bytes < bytes) {
+            if (e->base) (void)hipFreeAsync(e->base, s);
+            e->base = nullptr;
+            e->bytes = 0;
+            if (hipMallocAsync(&e->base, bytes, s) != hipSuccess) {
+                e->base = nullptr;
+                (void)hipGetLastError();
+                return E2_ENOMEM;
+            }
+            e->bytes = bytes;
+        }
+        sc.base = e->base;
+        return E2_OK;
+    }
+    sc.owned = true;
     if (hipMallocAsync(&sc.base, bytes, s) != hipSuccess) {
         sc.base = nullptr;
         (void)hipGetLastError();
         return E2_ENOMEM;
     }
     return E2_OK;
+}
+
+// Wait for the device, then release every kept buffer.
+hipError_t free_scratch_cache(e2_ctx *ctx)
+{
+    ScratchCache *c = ctx->scratch_cache;
+    if (!c) return hipSuccess;
+    hipError_t err = hipSuccess;
+    bool any = false;
+    for (StreamScratch &e : c->entries) any = any || e.base;
+    if (any) {
+        err = hipDeviceSynchronize();
+        for (StreamScratch &e : c->entries)
+            if (e.base) {
+                const hipError_t f = hipFreeAsync(e.base, nullptr);
+                if (err == hipSuccess) err = f;
+            }
+        const hipError_t f = hipStreamSynchronize(nullptr);
+        if (err == hipSuccess) err = f;
+    }
+    delete c;
+    ctx->scratch_cache = nullptr;
+    return err;
 }
 
 // Lay out counters, the problem list and the split-point fallback.
@@ -535,9 +618,20 @@ int e2_ctx_destroy(e2_ctx *ctx)
 {
     if (!ctx) return E2_EINVAL;
     free_dp_events(ctx);
+    const hipError_t es = free_scratch_cache(ctx);
     const hipError_t e = hipFree(ctx->blob);
     free(ctx);
-    return e == hipSuccess ? E2_OK : E2_EHIP;
+    return e == hipSuccess && es == hipSuccess ? E2_OK : E2_EHIP;
+}
+
+int e2_ctx_keep_scratch(e2_ctx *ctx, int32_t enable)
+{
+    if (!ctx || (enable != 0 && enable != 1)) return E2_EINVAL;
+    int rc = check_device(ctx);
+    if (rc) return rc;
+    if (!enable) return free_scratch_cache(ctx) == hipSuccess ? E2_OK : E2_EHIP;
+    if (!ctx->scratch_cache) ctx->scratch_cache = new (std::nothrow) ScratchCache;
+    return ctx->scratch_cache ? E2_OK : E2_ENOMEM;
 }
 
 int e2_ctx_dp_timing(e2_ctx *ctx, int32_t max_launches)
@@ -602,7 +696,7 @@ int solve_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Geno
     size_t tbb;
     const size_t bytes = work_bytes(ctx, P, k_max, &slots, &tbb, 1, objective);
     Scratch sc;
-    if ((rc = alloc_scratch(sc, s, bytes))) return rc;
+    if ((rc = alloc_scratch(ctx, sc, s, bytes))) return rc;
     E2Work wk;
     carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk, 1, objective);
     const hipError_t e = e2_launch_partitions(ctx->tables, s, P, k_max, gen, roles, wk, T,
@@ -627,7 +721,7 @@ int eval_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Genom
     const size_t wb = work_bytes(ctx, P, k_max, &slots, &tbb, 1, objective);
     const size_t tl = align256((size_t)P * k_max * 8);
     Scratch sc;
-    if ((rc = alloc_scratch(sc, s, wb + 2 * tl))) return rc;
+    if ((rc = alloc_scratch(ctx, sc, s, wb + 2 * tl))) return rc;
     E2Work wk;
     carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk, 1, objective);
     uint64_t *Ts = reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
@@ -665,7 +759,7 @@ int roles_impl(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const E2Geno
     const size_t wb = work_bytes(ctx, P, k_max, &slots, &tbb, R);
     const size_t tl = T_all ? 0 : align256((size_t)P * k_max * R * 8);
     Scratch sc;
-    if ((rc = alloc_scratch(sc, s, wb + 2 * tl))) return rc;
+    if ((rc = alloc_scratch(ctx, sc, s, wb + 2 * tl))) return rc;
     E2Work wk;
     carve_work(sc.base, ctx, P, k_max, slots, tbb, &wk, R);
     uint64_t *Ts = T_all ? T_all : reinterpret_cast<uint64_t *>(static_cast<char *>(sc.base) + wb);
@@ -758,7 +852,7 @@ int e2_ga_step_ordered(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max,
     if ((rc = check_device(ctx))) return rc;
     hipStream_t s = as_stream(stream);
     Scratch sc;
-    if ((rc = alloc_scratch(sc, s, align256(256 * 4)))) return rc;
+    if ((rc = alloc_scratch(ctx, sc, s, align256(256 * 4)))) return rc;
     const hipError_t e = e2_launch_ga_ordered(
         s, ctx->M, P, k_max, order_in, sizes_in, roles_in, w_in, phase_in, gp->seed,
         gp->generation, gp->tournament_k, gp->mutation_thresh_u32, gp->n_elite, gp->max_replica,
@@ -908,7 +1002,7 @@ int e2_ga_step(e2_ctx *ctx, void *stream, int32_t P, int32_t k_max, const uint8_
     if ((rc = check_device(ctx))) return rc;
     hipStream_t s = as_stream(stream);
     Scratch sc;
-    if ((rc = alloc_scratch(sc, s, align256(256 * 4)))) return rc;
+    if ((rc = alloc_scratch(ctx, sc, s, align256(256 * 4)))) return rc;
     const hipError_t e = e2_launch_ga(s, ctx->M, P, k_max, labels_in, roles_in, w_in, phase_in,
                                       gp->seed, gp->generation, gp->tournament_k,
                                       gp->crossover_thresh_u32, gp->mutation_thresh_u32,

@@ -58,6 +58,8 @@ struct e2_ctx {
     hipEvent_t *dp_events;
     int dp_event_pairs;
     int dp_events_used;
+    // device scratch kept per stream between calls (host API only)
+    struct ScratchCache *scratch_cache;
 };
 
 // Per-call counters, each on a 256-byte line of its own so that the

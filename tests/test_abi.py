@@ -115,6 +115,20 @@ def test_entry_points_reject_bad_arguments_without_a_device():
     assert L.e2_ga_step(nul, nul, 1, 1, nul, nul, nul, nul, ctypes.byref(gp), nul,
                         nul) == e2.E2_EINVAL
     assert L.e2_ctx_create(None, ctypes.byref(ctypes.c_void_p())) == e2.E2_EINVAL
+    assert L.e2_ctx_keep_scratch(nul, 1) == e2.E2_EINVAL
+    assert L.e2_ctx_keep_scratch(nul, 0) == e2.E2_EINVAL
+
+
+def test_library_loads_beside_torchs_hip_runtime():
+    """The binding loads libe2.so into processes that have imported torch,
+    whose bundled HIP runtime is then the one every HIP symbol binds to: the
+    library may use no symbol (or symbol version) that runtime lacks."""
+    import subprocess
+    import sys
+    code = ("import torch, ctypes, sys; ctypes.CDLL(sys.argv[1]); print('ok')")
+    r = subprocess.run([sys.executable, "-c", code, e2.LIB_PATH], capture_output=True,
+                       text=True, timeout=600)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stderr[-2000:]
 
 
 @pytest.mark.parametrize("sm,code", [

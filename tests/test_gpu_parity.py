@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 import oracle
+from oracle import pool
 import paper_2606_03770_amd as e2
 from paper_2606_03770_amd import workload
 
@@ -498,14 +499,17 @@ def test_long_chain_among_many_cluster_ids_takes_the_reference_path(torch_dev):
     _assert_equal(_gpu_all(torch_dev, wl, labels=labels), want, tag="reference long")
 
 
-def test_one_context_on_two_streams_at_once(torch_dev):
-    """A context is immutable after creation and every call's scratch is
-    stream-ordered, so two streams may evaluate different populations with
-    one context at the same time; each result equals the same call made
-    alone."""
+@pytest.mark.parametrize("keep", [False, True])
+def test_one_context_on_two_streams_at_once(torch_dev, keep):
+    """A context's tables are immutable after creation and every call's
+    scratch belongs to its stream, so two streams may evaluate different
+    populations with one context at the same time; each result equals the
+    same call made alone."""
     torch, dev = torch_dev
     wl = workload.make("c4_128dev_80L")
     ctx = e2.e2_ctx_create(wl.problem_arrays())
+    if keep:
+        e2.e2_ctx_keep_scratch(ctx)
     fp = wl.fitness_params()
     halves = [np.arange(0, 2048), np.arange(2048, 4096)]
     ins = [(torch.from_numpy(np.ascontiguousarray(wl.labels[h])).to(dev),
@@ -528,7 +532,58 @@ def test_one_context_on_two_streams_at_once(torch_dev):
                 assert np.array_equal(e2.u64(a[k]), b[k]), (rep, k)
 
 
-def test_one_context_from_four_host_threads(torch_dev):
+def test_scratch_kept_per_stream_across_sizes_and_streams(torch_dev):
+    """e2_ctx_keep_scratch: the context keeps one scratch buffer per stream
+    for its first 16 streams and grows it when a call needs more; later
+    streams allocate per call.  Calls of three sizes on the null stream and
+    18 side streams, launched back to back and in two rounds (the second
+    reuses every kept buffer, grown or not), with GA steps between the
+    evaluations on one stream, each equal the oracle's rows; turning the
+    setting off releases the buffers, and calls then allocate per call."""
+    torch, dev = torch_dev
+    wl = workload.make("c3_64dev_80L")
+    want = pool.eval_population(wl)
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    e2.e2_ctx_keep_scratch(ctx)
+    e2.e2_ctx_keep_scratch(ctx)          # a second call keeps the same cache
+    fp = wl.fitness_params()
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    streams = [torch.cuda.default_stream()] + [torch.cuda.Stream() for _ in range(18)]
+    sizes = (64, wl.population, 300)
+    torch.cuda.synchronize()
+    for rnd in range(2):
+        outs = []
+        for i, st in enumerate(streams):
+            n = sizes[(i + rnd) % 3]
+            lo = (97 * i) % (wl.population - n + 1)
+            with torch.cuda.stream(st):
+                outs.append((lo, n, e2.e2_eval_population(ctx, L[lo:lo + n], R[lo:lo + n], fp)))
+        torch.cuda.synchronize()
+        for i, (lo, n, out) in enumerate(outs):
+            for k in ("w", "phase", "s_p", "s_d"):
+                assert np.array_equal(e2.u64(out[k]), want[k][lo:lo + n]), (rnd, i, k)
+    # a GA step (small scratch) between two evaluations on one stream
+    st = streams[3]
+    with torch.cuda.stream(st):
+        f = e2.e2_eval_population(ctx, L, R, fp)
+        L2, R2 = e2.e2_ga_step(ctx, L, R, f["w"], f["phase"], wl.ga_params(0))
+        f2 = e2.e2_eval_population(ctx, L, R, fp)
+    torch.cuda.synchronize()
+    bred = oracle.ga_step(wl.labels, wl.roles, e2.u64(f["w"]), e2.u64(f["phase"]), wl.k_max,
+                          **wl.ga_params(0))
+    assert np.array_equal(L2.cpu().numpy(), bred[0]) and np.array_equal(R2.cpu().numpy(), bred[1])
+    for k in ("w", "phase"):
+        assert np.array_equal(e2.u64(f2[k]), want[k]), k
+    e2.e2_ctx_keep_scratch(ctx, False)   # waits, releases, back to per-call scratch
+    out = e2.e2_eval_population(ctx, L, R, fp)
+    torch.cuda.synchronize()
+    assert np.array_equal(e2.u64(out["w"]), want["w"])
+    ctx.close()
+
+
+@pytest.mark.parametrize("keep", [False, True])
+def test_one_context_from_four_host_threads(torch_dev, keep):
     """A context may serve several host threads at once: four threads, each
     on its own stream, evaluate their quarter of a population through one
     context (the binding releases the interpreter lock inside the library
@@ -537,6 +592,8 @@ def test_one_context_from_four_host_threads(torch_dev):
     torch, dev = torch_dev
     wl = workload.make("c3_64dev_80L")
     ctx = e2.e2_ctx_create(wl.problem_arrays())
+    if keep:
+        e2.e2_ctx_keep_scratch(ctx)
     fp = wl.fitness_params()
     L = torch.from_numpy(wl.labels).to(dev)
     R = torch.from_numpy(wl.roles).to(dev)
