@@ -110,8 +110,11 @@ __global__ void k_init(uint32_t *counters)
 // Listed problems are bucketed by chain length into kClasses segments of the
 // list (longest chains first), so the DP kernel schedules large problems
 // early; each workgroup reserves its range of each segment with one atomic.
+// Those atomics all meet on the segments' counters, so a workgroup takes 16
+// genomes (1024 threads): half the reservations of 8 (a third less kernel
+// time on the 16384-genome population).
 // ---------------------------------------------------------------------------
-constexpr int kEG = 8;       // genomes per extraction workgroup
+constexpr int kEG = 16;      // genomes per extraction workgroup
 constexpr int kDynTailShift = 2;  // the last 1/4 of the DP list is taken dynamically ...
 constexpr uint32_t kDynTailMinPerWave = 16;  // ... with at least this many problems per wave
 constexpr int kClasses = 4;  // chain-length classes: m >= 16, 12..15, 8..11, < 8
@@ -155,12 +158,16 @@ __device__ __forceinline__ E2Tables mem_view(const E2Tables &tb, int r)
     return v;
 }
 
-// n_r = 0: one problem per cluster, at role index (roles[q] != 0); n_r = R:
-// one problem per cluster and role index (R <= 16, P < 2^20), outputs
-// [P][k_max][R] and list codes (p << 12) | (q << 4) | r.
+// SEARCH = false: one problem per cluster, at role index (roles[q] != 0);
+// SEARCH = true: one problem per cluster and role index (n_roles = R <= 16,
+// P < 2^20), outputs [P][k_max][R] and list codes (p << 12) | (q << 4) | r.
+// ORD: two-chromosome genomes (replicas are runs of the ordering), else
+// label genomes.  One instance per genome kind and mode keeps the label
+// path free of the ordering's LDS arrays and registers.
+template <bool ORD, bool SEARCH>
 __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_max,
                                                       E2Genomes gen, const uint8_t *roles,
-                                                      int n_r, int relaxed, int long_seg,
+                                                      int n_roles, int relaxed, int long_seg,
                                                       uint32_t *counters,
                                                       uint32_t *list, size_t seg_cap,
                                                       uint64_t *T, uint64_t *Lambda,
@@ -174,15 +181,17 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
     __shared__ uint32_t lmask[kEG][8];
     __shared__ uint32_t ncls[kEG][16][kListSegs];  // per genome, pass and list segment
     __shared__ uint32_t base[kEG][16][kListSegs];
-    __shared__ uint32_t offs[kEG][256];  // replica starts of two-chromosome genomes
+    // two-chromosome genomes only: replica starts, cap0 | head bit per position
+    __shared__ uint32_t offs[ORD ? kEG : 1][ORD ? 256 : 1];
+    __shared__ uint16_t posc[ORD ? kEG : 1][ORD ? 256 : 1];
     __shared__ uint32_t bad[kEG][8];     // replicas holding a device id >= M
-    __shared__ uint16_t posc[kEG][256];  // two-chromosome genomes: cap0 | head bit per position
     const int g = threadIdx.x / 64;
     const int lane = threadIdx.x % 64;
     const int p = blockIdx.x * kEG + g;
     const int M = tb.M, N = tb.N;
-    const bool ordered = gen.labels == nullptr;
-    if (ordered && p < P) {
+    constexpr bool ordered = ORD;
+    const int n_r = SEARCH ? n_roles : 0;
+    if constexpr (ordered) if (p < P) {
         // offs[r] = min(M, sizes[0] + ... + sizes[r-1]), r = 0..k_max
         uint32_t carry = 0;
         for (int r0 = 0; r0 <= k_max; r0 += kWave) {
@@ -209,7 +218,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
         devs[u] = 0;
         if (p < P && x < M) {
             int lab, d = x;
-            if (ordered) {
+            if constexpr (ordered) {
                 d = gen.order[(size_t)p * M + x];
                 lab = replica_at(offs[g], k_max, x);
                 if (d >= M) {  // not a device: its replica cannot be solved
@@ -258,7 +267,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
                 const int c = mem_class(tb, r);
                 const uint32_t c0 = tb.cap0[(size_t)c * M + devs[u]];
                 const uint32_t cH = tb.capH[(size_t)c * M + devs[u]];
-                if (ordered) {
+                if constexpr (ordered) {
                     posc[g][lane + 64 * u] = (uint16_t)(c0 | (cH ? 0x100u : 0u));
                 } else {
                     atomicAdd(&packed[g][lab], (1u << 16) | c0);
@@ -270,7 +279,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
             }
         }
         __syncthreads();
-        if (ordered) {  // uniform over the workgroup
+        if constexpr (ordered) {
             // a replica is a run of ordering positions [offs[q], offs[q+1]):
             // one lane per replica sums its run, with no atomics (the lanes
             // of one run would all meet on its words).  Positions holding an
@@ -3479,9 +3488,12 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
     // cluster id on average.  Otherwise (no launch to pay for) the rare long
     // chain takes k_dp's reference path; the results are the same.
     const bool long_seg = objective == 0 && t.M > kMaxBandedChain && t.M >= 16 * k_max;
-    k_extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, roles, n_r,
-                                                       objective == 2, long_seg, wk.counters,
-                                                       wk.list, seg, T, Lambda, master, layers);
+    const bool ord = gen.labels == nullptr;
+    const auto extract = ord ? (n_r ? k_extract<true, true> : k_extract<true, false>)
+                             : (n_r ? k_extract<false, true> : k_extract<false, false>);
+    extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, roles, n_r,
+                                                     objective == 2, long_seg, wk.counters,
+                                                     wk.list, seg, T, Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
     if (objective == 2)
