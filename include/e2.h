@@ -24,9 +24,11 @@
  *     (hipMallocAsync / hipFreeAsync on the same stream), per call, or
  *     from a buffer the context keeps per stream (e2_ctx_keep_scratch).
  *   - INF = UINT64_MAX marks "no feasible value" in every u64 output.
- *   - A context is immutable after creation (apart from the profiling
- *     records of e2_ctx_dp_timing): one context may serve several streams
- *     and host threads at once.  It lives on the device that was
+ *   - A context's tables are immutable after creation; besides them it
+ *     holds only the profiling records of e2_ctx_dp_timing and, when
+ *     e2_ctx_keep_scratch is on, per-stream scratch that its calls share
+ *     under a lock.  One context may serve several streams and host threads
+ *     at once.  It lives on the device that was
  *     current when it was created; calls must be made with that device
  *     current.
  */
