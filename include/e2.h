@@ -181,7 +181,8 @@ int e2_ctx_destroy(e2_ctx *ctx);
  * is allocated on it (hipMallocAsync) by its first call and grown on it
  * (hipFreeAsync, then hipMallocAsync) when a call needs more; calls on one
  * stream share it in stream order, calls on different streams never share
- * one, and calls on further streams allocate per call as before.  This
+ * one, and calls on further streams, or on hipStreamPerThread (a different
+ * stream in every host thread), allocate per call as before.  This
  * removes the allocation and release packets that otherwise separate
  * consecutive calls on a stream.  Condition while it is on: a stream with
  * calls on this context in flight is not destroyed (a new stream could

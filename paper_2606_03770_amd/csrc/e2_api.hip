@@ -156,7 +156,8 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // allocation and release packets from the stream.  Streams are told apart
 // by handle: the caller keeps every stream with calls in flight alive, so
 // that no new stream takes a handle whose buffer is still in use.  Streams
-// past the first kCachedStreams allocate and free per call.
+// past the first kCachedStreams, and the per-thread default stream, allocate
+// and free per call.
 constexpr int kCachedStreams = 16;
 struct StreamScratch {
     hipStream_t stream = nullptr;
@@ -187,7 +188,9 @@ struct Scratch {
 StreamScratch *stream_entry(e2_ctx *ctx, hipStream_t s)
 {
     ScratchCache *c = ctx->scratch_cache;
-    if (!c) return nullptr;
+    // hipStreamPerThread names a different stream in every host thread, so
+    // one buffer behind that handle could serve two streams at once
+    if (!c || s == hipStreamPerThread) return nullptr;
     std::lock_guard<std::mutex> g(c->mu);
     for (StreamScratch &e : c->entries)
         if (e.stream == s) return &e;

@@ -582,6 +582,49 @@ def test_scratch_kept_per_stream_across_sizes_and_streams(torch_dev):
     ctx.close()
 
 
+def test_per_thread_default_stream_from_two_host_threads_with_kept_scratch(torch_dev):
+    """hipStreamPerThread is one handle that names each host thread's own
+    stream, so a context never keeps scratch behind it: two threads that
+    evaluate through it at once, with the setting on, each get the
+    single-threaded result on every call."""
+    import threading
+    import types
+    torch, dev = torch_dev
+    wl = workload.make("c3_64dev_80L")
+    ctx = e2.e2_ctx_create(wl.problem_arrays())
+    e2.e2_ctx_keep_scratch(ctx)
+    fp = wl.fitness_params()
+    L = torch.from_numpy(wl.labels).to(dev)
+    R = torch.from_numpy(wl.roles).to(dev)
+    want = e2.e2_eval_population(ctx, L, R, fp)
+    torch.cuda.synchronize()
+    want = {k: e2.u64(v).copy() for k, v in want.items()}
+    per_thread = types.SimpleNamespace(cuda_stream=2)   # hipStreamPerThread
+    halves = np.array_split(np.arange(wl.population), 2)
+    results, errors = [[] for _ in halves], []
+
+    def work(i):
+        try:
+            lo, hi = int(halves[i][0]), int(halves[i][-1]) + 1
+            outs = [e2.e2_eval_population(ctx, L[lo:hi], R[lo:hi], fp, stream=per_thread)
+                    for _ in range(6)]
+            torch.cuda.synchronize()
+            results[i] = [{k: e2.u64(v).copy() for k, v in o.items()} for o in outs]
+        except Exception as exc:  # reported below, in the main thread
+            errors.append(repr(exc))
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for i, rows in enumerate(halves):
+        for rep, out in enumerate(results[i]):
+            for k in want:
+                assert np.array_equal(out[k], want[k][rows]), (i, rep, k)
+
+
 @pytest.mark.parametrize("keep", [False, True])
 def test_one_context_from_four_host_threads(torch_dev, keep):
     """A context may serve several host threads at once: four threads, each
