@@ -102,7 +102,8 @@ __global__ void k_init(uint32_t *counters)
 }
 
 // ---------------------------------------------------------------------------
-// Extraction and pre-check: one wave per genome, kEG genomes per workgroup.
+// Extraction and pre-check: one wave per genome, eg_of<SEARCH>() genomes per
+// workgroup.
 // A cluster goes to the DP list unless it is empty or provably infeasible:
 //   more devices than blocks (every device must hold a block), a device that
 //   cannot hold a single block, total single-stage capacity below N, or no
@@ -110,11 +111,13 @@ __global__ void k_init(uint32_t *counters)
 // Listed problems are bucketed by chain length into kClasses segments of the
 // list (longest chains first), so the DP kernel schedules large problems
 // early; each workgroup reserves its range of each segment with one atomic.
-// Those atomics all meet on the segments' counters, so a workgroup takes 16
-// genomes (1024 threads): half the reservations of 8 (a third less kernel
-// time on the 16384-genome population).
+// Those atomics all meet on the segments' counters, so an evaluation's
+// workgroup takes 16 genomes (1024 threads): half the reservations of 8 (a
+// third less kernel time on the 16384-genome population).  The role
+// search's instances hold about 80 VGPRs, so that one 1024-thread
+// workgroup per CU would fit: they keep 8 genomes per workgroup.
 // ---------------------------------------------------------------------------
-constexpr int kEG = 16;      // genomes per extraction workgroup
+template <bool SEARCH> constexpr int eg_of() { return SEARCH ? 8 : 16; }
 constexpr int kDynTailShift = 2;  // the last 1/4 of the DP list is taken dynamically ...
 constexpr uint32_t kDynTailMinPerWave = 16;  // ... with at least this many problems per wave
 constexpr int kClasses = 4;  // chain-length classes: m >= 16, 12..15, 8..11, < 8
@@ -165,7 +168,7 @@ __device__ __forceinline__ E2Tables mem_view(const E2Tables &tb, int r)
 // label genomes.  One instance per genome kind and mode keeps the label
 // path free of the ordering's LDS arrays and registers.
 template <bool ORD, bool SEARCH>
-__global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_max,
+__global__ __launch_bounds__(64 * eg_of<SEARCH>()) void k_extract(E2Tables tb, int P, int k_max,
                                                       E2Genomes gen, const uint8_t *roles,
                                                       int n_roles, int relaxed, int long_seg,
                                                       uint32_t *counters,
@@ -175,6 +178,7 @@ __global__ __launch_bounds__(64 * kEG) void k_extract(E2Tables tb, int P, int k_
 {
     // per genome: (count << 16) + sum of cap0, min cap0, head-capable flag per
     // cluster, listed bitmask
+    constexpr int kEG = eg_of<SEARCH>();
     __shared__ uint32_t packed[kEG][256];
     __shared__ uint32_t mincap[kEG][256];
     __shared__ uint32_t hflag[kEG][256];  // 1 when some device can hold a block and the head
@@ -3491,9 +3495,10 @@ hipError_t e2_launch_partitions(const E2Tables &t, hipStream_t s, int P, int k_m
     const bool ord = gen.labels == nullptr;
     const auto extract = ord ? (n_r ? k_extract<true, true> : k_extract<true, false>)
                              : (n_r ? k_extract<false, true> : k_extract<false, false>);
-    extract<<<(P + kEG - 1) / kEG, 64 * kEG, 0, s>>>(t, P, k_max, gen, roles, n_r,
-                                                     objective == 2, long_seg, wk.counters,
-                                                     wk.list, seg, T, Lambda, master, layers);
+    const int eg = n_r ? eg_of<true>() : eg_of<false>();
+    extract<<<(P + eg - 1) / eg, 64 * eg, 0, s>>>(t, P, k_max, gen, roles, n_r, objective == 2,
+                                                   long_seg, wk.counters, wk.list, seg, T,
+                                                   Lambda, master, layers);
     const int pool = e2_dp_pool_cells(t.N);
     if (wk.ev_begin) (void)hipEventRecord(wk.ev_begin, s);
     if (objective == 2)
